@@ -1,0 +1,225 @@
+/*
+ * abcd.h -- C ABI of the ABCD active-block step on MI355X (gfx950).
+ *
+ * ABCD (Alpha-Composited Block Coordinate Descent) trains a radiance field one
+ * spatial partition at a time: only the active partition is rendered; its
+ * image is composited between a foreground F and a background B that hold the
+ * pre-accumulated renders of the frozen partitions in front of and behind it,
+ * and gradients flow into the active parameters only (paper, Method section).
+ * Because "over" is associative, the cached per-partition renders collapse
+ * into F and B (Abstract; Method section). The renderer is 3D Gaussian
+ * Splatting (Introduction), whose constants the paper does not state; they
+ * are runtime parameters here (abcd_raster_params).
+ *
+ * One step on one camera is
+ *   abcd_composite_cache  cached partition renders -> F, B (once per camera)
+ *   abcd_project          parameters -> screen-space Gaussians
+ *   abcd_bin_sort         -> per 16x16 tile, Gaussians sorted by (depth, index)
+ *   abcd_render_fwd       -> out = F over A over B
+ *   (loss gradient, e.g. abcd_loss_l1_grad)
+ *   abcd_render_bwd       -> gradients of the active parameters only
+ *
+ * Conventions for every entry point:
+ *  - Returns an abcd_status (int32). Arguments are validated on the host before
+ *    any HIP call; an invalid call returns ABCD_E_INVALID and touches nothing.
+ *  - Array arguments are DEVICE pointers owned by the caller unless marked
+ *    "host". The library never allocates device memory: scratch space is a
+ *    caller-provided workspace whose size the *_workspace_size helpers give.
+ *  - All work is enqueued on `stream` and is asynchronous, except where a call
+ *    is documented to synchronise.
+ *  - Floating-point data is fp32 unless stated; fp16 is IEEE binary16 passed as
+ *    uint16_t. Images are row-major [height][width][4] premultiplied RGBA.
+ *  - Parameter arrays are contiguous structure-of-arrays:
+ *      means [n][3], log_scales [n][3], quats [n][4] (w, x, y, z; any norm),
+ *      opacity_logits [n], sh [n][(sh_degree+1)^2][3].
+ *  - Functions are stateless and reentrant; concurrent calls on one stream
+ *    must not share a workspace.
+ */
+#ifndef ABCD_H
+#define ABCD_H
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ABCD_API __attribute__((visibility("default")))
+
+#define ABCD_TILE 16           /* tile side in pixels */
+#define ABCD_MAX_TILES 32768   /* ceil(W/16) * ceil(H/16) limit */
+#define ABCD_MAX_GAUSSIANS (1LL << 30)
+
+typedef enum {
+  ABCD_OK = 0,
+  ABCD_E_INVALID = 1,   /* bad argument; nothing was enqueued */
+  ABCD_E_CAPACITY = 2,  /* intersection count exceeds the capacity given */
+  ABCD_E_OVERFLOW = 3,  /* intersection count does not fit 32 bits */
+  ABCD_E_HIP = 4        /* a HIP call failed; see abcd_last_error() */
+} abcd_status;
+
+/* Pinhole camera. x_cam = R x_world + t with OpenCV axes (x right, y down,
+ * z forward); pixel (i, j) covers [i, i+1) x [j, j+1) and is sampled at its
+ * centre (i + 0.5, j + 0.5). campos is the camera centre in world space (for
+ * the view direction of the SH colour). Gaussians with view depth <= near_plane
+ * are culled. */
+typedef struct {
+  int32_t width, height;
+  float fx, fy, cx, cy;
+  float R[9]; /* row major */
+  float t[3];
+  float campos[3];
+  float near_plane;
+} abcd_camera;
+
+/* Rasteriser constants of the 3D Gaussian Splatting renderer. */
+typedef struct {
+  float alpha_min;     /* blends with alpha below this are skipped (1/255) */
+  float alpha_max;     /* alpha is clamped to this (0.99) */
+  float t_min;         /* a blend that would take transmittance below this ends the pixel (1e-4) */
+  float eps2d;         /* dilation added to every 2D covariance, px^2 (0.3) */
+  float radius_sigmas; /* support radius in sigmas of the major axis (3) */
+  float guard;         /* guard-band factor on the field of view inside the Jacobian (1.3) */
+  int32_t sh_degree;   /* 0..3 */
+  uint32_t flags;      /* reserved, must be 0 */
+} abcd_raster_params;
+
+/* ------------------------------------------------------------------------ */
+/* Projection (3DGS EWA splatting: Introduction; Method section -- "only the
+ * active partition is rendered").
+ *
+ * Per Gaussian i writes
+ *   means2d[i][2]        pixel-space mean (u, v)
+ *   conic_opacity[i][4]  (a, b, c, o): inverse 2D covariance [[a, b], [b, c]]
+ *                        and opacity o = sigmoid(logit)
+ *   depth[i]             view-space z
+ *   radius[i]            support radius in pixels
+ *   tiles_touched[i]     number of 16x16 tiles of its support rectangle
+ *   rgb[i][3]            colour max(0, SH(view direction) + 0.5)
+ * A culled Gaussian (behind near_plane, degenerate, non-finite, or with no tile
+ * on screen) gets zeros in every output. The values deciding culling, the tile
+ * rectangle and the depth key follow one fixed fp32 operation order (the
+ * numerical contract of this library). n may be 0. */
+ABCD_API int32_t abcd_project(const abcd_camera* cam /* host */, const abcd_raster_params* prm /* host */,
+                     int64_t n, const float* means, const float* log_scales, const float* quats,
+                     const float* opacity_logits, const float* sh, float* means2d,
+                     float* conic_opacity, float* depth, float* radius, uint32_t* tiles_touched,
+                     float* rgb, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Binning: every (tile, Gaussian) pair of the support rectangles, sorted by
+ * key = tile << 32 | fp32 bits of depth, ties by Gaussian index (the unique
+ * front-to-back order of each tile's list).
+ *
+ * Outputs: values_sorted[M] Gaussian indices; keys_sorted[M] the keys (may be
+ * NULL, then not written); tile_ranges[tiles][2] = [start, end) per tile
+ * (start = number of pairs of lower tiles).
+ *
+ * capacity: number of elements values_sorted (and keys_sorted) can hold. If
+ * the intersection count M exceeds it, nothing is written to values_sorted,
+ * keys_sorted or tile_ranges.
+ * n_isect (host, may be NULL): if given, the call synchronises `stream` once,
+ * stores M there and returns ABCD_E_CAPACITY when M > capacity. If NULL, the
+ * call does not synchronise; M (uint64) is left at the start of the workspace
+ * and a capacity overflow leaves the outputs unwritten.
+ * workspace: at least abcd_bin_sort_workspace_size() bytes, 256-byte aligned. */
+ABCD_API int32_t abcd_bin_sort_workspace_size(int64_t n, int32_t width, int32_t height, size_t* bytes);
+ABCD_API int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const float* means2d,
+                      const float* radius, const float* depth, const uint32_t* tiles_touched,
+                      int64_t capacity, void* workspace, size_t ws_bytes, uint64_t* keys_sorted,
+                      uint32_t* values_sorted, uint32_t* tile_ranges, int64_t* n_isect /* host */,
+                      hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Forward render and composite (Method section: F over active over B).
+ *
+ * Per pixel, front to back over its tile's list, starting from T = 1, C = 0:
+ *   power = -(a dx^2 + c dy^2)/2 - b dx dy, (dx, dy) = pixel centre - mean;
+ *   skip if power > 0; alpha = min(alpha_max, o exp(power)); skip if
+ *   alpha < alpha_min; stop (without blending) if T (1 - alpha) < t_min;
+ *   else C += rgb alpha T, T *= 1 - alpha.
+ * The active render A = (C, 1 - T) is composited as out = F over A over B:
+ *   out_rgb = F_rgb + (1 - F_a)(C + T B_rgb),
+ *   out_a   = F_a + (1 - F_a)(1 - T (1 - B_a)).
+ * F or B may be NULL (transparent). Also writes final_T[H][W] and last[H][W]
+ * (entries of the tile's list walked up to and including the last blended
+ * one), both needed by abcd_render_bwd. n_blends (may be NULL): the number of
+ * blended (pixel, Gaussian) pairs of this call is ADDED to *n_blends. */
+ABCD_API int32_t abcd_render_fwd(const abcd_camera* cam /* host */, const abcd_raster_params* prm /* host */,
+                        const uint32_t* tile_ranges, const uint32_t* values_sorted,
+                        const float* means2d, const float* conic_opacity, const float* rgb,
+                        const float* F, const float* B, float* out_rgba, float* final_T,
+                        uint32_t* last, unsigned long long* n_blends, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Backward (Method section: gradients are back-propagated only through the
+ * active parameters; F and B are constants).
+ *
+ * Given dL_dout[H][W][4], writes the gradient of L with respect to every
+ * active parameter: d_means [n][3], d_log_scales [n][3], d_quats [n][4],
+ * d_opacity_logits [n], d_sh [n][(sh_degree+1)^2][3]; d_means2d [n][2] (may be
+ * NULL) receives dL/d(u, v). With accumulate != 0 the gradients are added to
+ * the arrays, otherwise they overwrite them. The derivative is exact for the
+ * forward above, including zero derivative of a clamped alpha and of a
+ * clamped colour. Inputs are those of the forward call on the same camera.
+ * workspace: at least abcd_render_bwd_workspace_size(n) bytes, 256-byte aligned. */
+ABCD_API int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes);
+ABCD_API int32_t abcd_render_bwd(const abcd_camera* cam /* host */, const abcd_raster_params* prm /* host */,
+                        int64_t n, const float* means, const float* log_scales, const float* quats,
+                        const float* opacity_logits, const float* sh, const float* means2d,
+                        const float* conic_opacity, const float* rgb, const float* radius,
+                        const uint32_t* tile_ranges, const uint32_t* values_sorted,
+                        const float* F, const float* B, const float* final_T, const uint32_t* last,
+                        const float* dL_dout, void* workspace, size_t ws_bytes, float* d_means,
+                        float* d_log_scales, float* d_quats, float* d_opacity_logits, float* d_sh,
+                        float* d_means2d, int32_t accumulate, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Collapse of cached partition renders into F and B (Abstract; Method section:
+ * cached renders of frozen partitions are composited into F and B according
+ * to depth ordering).
+ *
+ * images: k premultiplied RGBA fp16 renders [k][H][W][4]. order (host): a
+ * permutation of 0..k-1, front to back. F = images[order[0]] over ... over
+ * images[order[n_front-1]], B = images[order[n_front]] over ... over
+ * images[order[k-1]], both fp32 [H][W][4]. With accumulate != 0 the incoming
+ * F and B stay in front (F <- F over fold, B <- B over fold), so chunks of
+ * cached images can stream in front to back; otherwise they are overwritten.
+ * k = 0 writes transparent F and B (or leaves them unchanged when
+ * accumulating). */
+ABCD_API int32_t abcd_composite_cache(int32_t width, int32_t height, int32_t k, const uint16_t* images,
+                             const int32_t* order /* host */, int32_t n_front, float* F, float* B,
+                             int32_t accumulate, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* L1 reconstruction loss gradient (the paper evaluates a reconstruction loss
+ * without naming it, Method section). img = out_rgb + (1 - out_a) bg;
+ * dL/dimg = sign(img - target) / (3 H W) (sign(0) = 0); writes dL_dout[H][W][4]
+ * (alpha channel -sum_c bg_c dL/dimg_c). bg (host) may be NULL (black). loss
+ * (may be NULL): sum |img - target| / (3 H W) is ADDED to *loss. */
+ABCD_API int32_t abcd_loss_l1_grad(int32_t width, int32_t height, const float* out_rgba,
+                          const float* target_rgb, const float* bg /* host, 3 floats */,
+                          float* dL_dout, float* loss, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Helpers. abcd_last_error: message of the last failure on this thread.
+ * abcd_timing_*: optional per-kernel HIP-event timing of every launch made by
+ * this thread (off by default; enabling it adds two event records per launch
+ * on the caller's stream). abcd_timing_read synchronises, and returns the
+ * accumulated milliseconds and launch count of the kernel named `kernel`
+ * (names: project, project_bwd, depth_keys, radix_hist, radix_scan,
+ * radix_scatter, bin_count, bin_scan_columns, bin_scan_tiles, bin_scatter,
+ * render_fwd, render_bwd, zero_fill, composite, loss_l1). */
+ABCD_API const char* abcd_last_error(void);
+ABCD_API const char* abcd_version(void);
+ABCD_API const char* abcd_status_string(int32_t status);
+ABCD_API int32_t abcd_timing_enable(int32_t enable);
+ABCD_API int32_t abcd_timing_reset(void);
+ABCD_API int32_t abcd_timing_read(const char* kernel, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ABCD_H */

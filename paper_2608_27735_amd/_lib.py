@@ -1,0 +1,107 @@
+"""ctypes loader of libabcd.so and the C structures of include/abcd.h.
+
+The library is built in-tree (paper_2608_27735_amd/libabcd.so). There is no
+fallback: if it is missing, importing the binding raises.
+"""
+import ctypes as C
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libabcd.so")
+
+ABCD_OK, ABCD_E_INVALID, ABCD_E_CAPACITY, ABCD_E_OVERFLOW, ABCD_E_HIP = 0, 1, 2, 3, 4
+TILE = 16
+MAX_TILES = 32768
+
+
+class abcd_camera(C.Structure):
+    _fields_ = [("width", C.c_int32), ("height", C.c_int32), ("fx", C.c_float), ("fy", C.c_float),
+                ("cx", C.c_float), ("cy", C.c_float), ("R", C.c_float * 9), ("t", C.c_float * 3),
+                ("campos", C.c_float * 3), ("near_plane", C.c_float)]
+
+
+class abcd_raster_params(C.Structure):
+    _fields_ = [("alpha_min", C.c_float), ("alpha_max", C.c_float), ("t_min", C.c_float),
+                ("eps2d", C.c_float), ("radius_sigmas", C.c_float), ("guard", C.c_float),
+                ("sh_degree", C.c_int32), ("flags", C.c_uint32)]
+
+
+_P = C.c_void_p  # device pointers travel as integers
+_I32, _I64, _SZ = C.c_int32, C.c_int64, C.c_size_t
+_CAM, _PRM = C.POINTER(abcd_camera), C.POINTER(abcd_raster_params)
+
+# name -> (restype, argtypes); mirrors include/abcd.h
+SIGNATURES = {
+    "abcd_project": (_I32, [_CAM, _PRM, _I64] + [_P] * 5 + [_P] * 6 + [_P]),
+    "abcd_bin_sort_workspace_size": (_I32, [_I64, _I32, _I32, C.POINTER(_SZ)]),
+    "abcd_bin_sort": (_I32, [_I32, _I32, _I64, _P, _P, _P, _P, _I64, _P, _SZ, _P, _P, _P,
+                             C.POINTER(_I64), _P]),
+    "abcd_render_fwd": (_I32, [_CAM, _PRM] + [_P] * 11 + [_P]),
+    "abcd_render_bwd_workspace_size": (_I32, [_I64, C.POINTER(_SZ)]),
+    "abcd_render_bwd": (_I32, [_CAM, _PRM, _I64] + [_P] * 5 + [_P] * 4 + [_P] * 2 + [_P] * 5 +
+                        [_P, _SZ] + [_P] * 6 + [_I32, _P]),
+    "abcd_composite_cache": (_I32, [_I32, _I32, _I32, _P, C.POINTER(C.c_int32), _I32, _P, _P,
+                                    _I32, _P]),
+    "abcd_loss_l1_grad": (_I32, [_I32, _I32, _P, _P, C.POINTER(C.c_float), _P, _P, _P]),
+    "abcd_last_error": (C.c_char_p, []),
+    "abcd_version": (C.c_char_p, []),
+    "abcd_status_string": (C.c_char_p, [_I32]),
+    "abcd_timing_enable": (_I32, [_I32]),
+    "abcd_timing_reset": (_I32, []),
+    "abcd_timing_read": (_I32, [C.c_char_p, C.POINTER(C.c_double), C.POINTER(_I64)]),
+}
+
+_lib = None
+
+
+def load():
+    """Load libabcd.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = C.CDLL(LIB_PATH)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+class AbcdError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(message)
+        self.status = status
+
+
+def check(status):
+    if status != ABCD_OK:
+        lib = load()
+        raise AbcdError(status, "%s: %s" % (lib.abcd_status_string(status).decode(),
+                                            lib.abcd_last_error().decode()))
+    return status
+
+
+def camera_struct(cam):
+    c = abcd_camera()
+    c.width, c.height = int(cam.width), int(cam.height)
+    c.fx, c.fy, c.cx, c.cy = float(cam.fx), float(cam.fy), float(cam.cx), float(cam.cy)
+    R = [float(x) for row in cam.R for x in row] if hasattr(cam.R[0], "__len__") else list(cam.R)
+    for i in range(9):
+        c.R[i] = float(R[i])
+    for i in range(3):
+        c.t[i] = float(cam.t[i])
+        c.campos[i] = float(cam.campos[i])
+    c.near_plane = float(cam.near)
+    return c
+
+
+def params_struct(p):
+    q = abcd_raster_params()
+    q.alpha_min, q.alpha_max, q.t_min = float(p.alpha_min), float(p.alpha_max), float(p.t_min)
+    q.eps2d, q.radius_sigmas, q.guard = float(p.eps2d), float(p.radius_sigmas), float(p.guard)
+    q.sh_degree, q.flags = int(p.sh_degree), 0
+    return q

@@ -1,0 +1,253 @@
+"""Python binding of the ABCD C ABI (include/abcd.h) for torch tensors on the GPU.
+
+Argument marshalling only: tensors are checked for device, dtype and layout,
+their device pointers and the current HIP stream are passed to libabcd.so,
+and every step runs in the library's kernels. There is no CPU fallback.
+"""
+import ctypes as C
+
+import torch
+
+from . import _lib
+from ._lib import AbcdError, check
+
+_lib.load()  # no fallback: the binding is unusable without the built library
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _need(t, name, dtype, shape=None):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+def _opt(t, name, dtype, shape=None):
+    return None if t is None else _need(t, name, dtype, shape)
+
+
+def n_tiles(width, height):
+    return ((width + 15) // 16) * ((height + 15) // 16)
+
+
+def _empty(shape, dtype, device):
+    return torch.empty(shape, dtype=dtype, device=device)
+
+
+def version():
+    return _lib.load().abcd_version().decode()
+
+
+# ------------------------------------------------------------------ project
+
+def project(cam, prm, means, log_scales, quats, opacity_logits, sh, out=None):
+    """EWA projection; returns dict(means2d, conic_opacity, depth, radius,
+    tiles_touched (int32 view of uint32), rgb)."""
+    n = means.shape[0]
+    nc = (prm.sh_degree + 1) ** 2
+    f32 = torch.float32
+    _need(means, "means", f32, (n, 3))
+    _need(log_scales, "log_scales", f32, (n, 3))
+    _need(quats, "quats", f32, (n, 4))
+    _need(opacity_logits, "opacity_logits", f32, (n,))
+    _need(sh, "sh", f32, (n, nc, 3))
+    dev = means.device
+    if out is None:
+        out = dict(means2d=_empty((n, 2), f32, dev), conic_opacity=_empty((n, 4), f32, dev),
+                   depth=_empty((n,), f32, dev), radius=_empty((n,), f32, dev),
+                   tiles_touched=_empty((n,), torch.int32, dev), rgb=_empty((n, 3), f32, dev))
+    lib = _lib.load()
+    check(lib.abcd_project(C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)), n,
+                           _ptr(means), _ptr(log_scales), _ptr(quats), _ptr(opacity_logits),
+                           _ptr(sh), _ptr(out["means2d"]), _ptr(out["conic_opacity"]),
+                           _ptr(out["depth"]), _ptr(out["radius"]), _ptr(out["tiles_touched"]),
+                           _ptr(out["rgb"]), _stream()))
+    return out
+
+
+# ------------------------------------------------------------------ binning
+
+def bin_sort_workspace_size(n, width, height):
+    sz = C.c_size_t(0)
+    check(_lib.load().abcd_bin_sort_workspace_size(n, width, height, C.byref(sz)))
+    return sz.value
+
+
+def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, keys=None,
+             tile_ranges=None, want_keys=False, sync=True):
+    """Per-tile depth-sorted lists. Returns dict(values, tile_ranges, keys, n_isect).
+
+    With sync=True (default) M is read back (one stream synchronisation) and
+    the buffers are grown to fit it; with sync=False the call never
+    synchronises and `capacity`/`values` must already be large enough (an
+    overflow leaves the outputs unwritten)."""
+    means2d, radius = proj["means2d"], proj["radius"]
+    depth, tiles = proj["depth"], proj["tiles_touched"]
+    n = means2d.shape[0]
+    dev = means2d.device
+    _need(means2d, "means2d", torch.float32, (n, 2))
+    _need(radius, "radius", torch.float32, (n,))
+    _need(depth, "depth", torch.float32, (n,))
+    _need(tiles, "tiles_touched", torch.int32, (n,))
+    ws_bytes = bin_sort_workspace_size(n, width, height)
+    if workspace is None or workspace.numel() < ws_bytes:
+        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    if tile_ranges is None:
+        tile_ranges = _empty((n_tiles(width, height), 2), torch.int32, dev)
+    if capacity is None:
+        capacity = 0 if values is None else values.numel()
+    if values is None and capacity > 0:
+        values = _empty((capacity,), torch.int32, dev)
+    if want_keys and (keys is None or keys.numel() < capacity):
+        keys = _empty((max(capacity, 1),), torch.int64, dev)
+    lib = _lib.load()
+    m = C.c_int64(0)
+    st = lib.abcd_bin_sort(width, height, n, _ptr(means2d), _ptr(radius), _ptr(depth), _ptr(tiles),
+                           capacity, _ptr(workspace), workspace.numel(),
+                           _ptr(keys) if want_keys else None, _ptr(values), _ptr(tile_ranges),
+                           C.byref(m) if sync else None, _stream())
+    if st == _lib.ABCD_E_CAPACITY and sync:
+        capacity = int(m.value)
+        values = _empty((max(capacity, 1),), torch.int32, dev)
+        if want_keys:
+            keys = _empty((max(capacity, 1),), torch.int64, dev)
+        st = lib.abcd_bin_sort(width, height, n, _ptr(means2d), _ptr(radius), _ptr(depth),
+                               _ptr(tiles), capacity, _ptr(workspace), workspace.numel(),
+                               _ptr(keys) if want_keys else None, _ptr(values), _ptr(tile_ranges),
+                               C.byref(m), _stream())
+    check(st)
+    return dict(values=values, tile_ranges=tile_ranges, keys=keys if want_keys else None,
+                n_isect=int(m.value) if sync else None, workspace=workspace, capacity=capacity)
+
+
+# -------------------------------------------------------------- rasterise
+
+def render_fwd(cam, prm, bins, proj, F=None, B=None, n_blends=None, out=None):
+    """out = F over A over B; returns dict(out, final_T, last)."""
+    H, W = cam.height, cam.width
+    dev = proj["means2d"].device
+    _opt(F, "F", torch.float32, (H, W, 4))
+    _opt(B, "B", torch.float32, (H, W, 4))
+    _opt(n_blends, "n_blends", torch.int64, (1,))
+    if out is None:
+        out = dict(out=_empty((H, W, 4), torch.float32, dev),
+                   final_T=_empty((H, W), torch.float32, dev),
+                   last=_empty((H, W), torch.int32, dev))
+    lib = _lib.load()
+    check(lib.abcd_render_fwd(C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)),
+                              _ptr(bins["tile_ranges"]), _ptr(bins["values"]),
+                              _ptr(proj["means2d"]), _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]),
+                              _ptr(F), _ptr(B), _ptr(out["out"]), _ptr(out["final_T"]),
+                              _ptr(out["last"]), _ptr(n_blends), _stream()))
+    return out
+
+
+def render_bwd_workspace_size(n):
+    sz = C.c_size_t(0)
+    check(_lib.load().abcd_render_bwd_workspace_size(n, C.byref(sz)))
+    return sz.value
+
+
+def render_bwd(cam, prm, params, proj, bins, fwd, dL_dout, F=None, B=None, workspace=None,
+               grads=None, accumulate=False, want_means2d=False):
+    """Gradients of the active parameters; returns dict(means, log_scales, quats,
+    opacity_logits, sh[, means2d])."""
+    n = params["means"].shape[0]
+    H, W = cam.height, cam.width
+    dev = params["means"].device
+    _need(dL_dout, "dL_dout", torch.float32, (H, W, 4))
+    _opt(F, "F", torch.float32, (H, W, 4))
+    _opt(B, "B", torch.float32, (H, W, 4))
+    ws_bytes = render_bwd_workspace_size(n)
+    if workspace is None or workspace.numel() < ws_bytes:
+        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    if grads is None:
+        grads = {k: torch.zeros_like(params[k]) for k in
+                 ("means", "log_scales", "quats", "opacity_logits", "sh")}
+        if want_means2d:
+            grads["means2d"] = torch.zeros((n, 2), dtype=torch.float32, device=dev)
+    lib = _lib.load()
+    check(lib.abcd_render_bwd(
+        C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)), n,
+        _ptr(params["means"]), _ptr(params["log_scales"]), _ptr(params["quats"]),
+        _ptr(params["opacity_logits"]), _ptr(params["sh"]), _ptr(proj["means2d"]),
+        _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]), _ptr(proj["radius"]),
+        _ptr(bins["tile_ranges"]), _ptr(bins["values"]), _ptr(F), _ptr(B), _ptr(fwd["final_T"]),
+        _ptr(fwd["last"]), _ptr(dL_dout), _ptr(workspace), workspace.numel(), _ptr(grads["means"]),
+        _ptr(grads["log_scales"]), _ptr(grads["quats"]), _ptr(grads["opacity_logits"]),
+        _ptr(grads["sh"]), _ptr(grads.get("means2d")), 1 if accumulate else 0, _stream()))
+    return grads
+
+
+# ---------------------------------------------------------------- collapse
+
+def composite_cache(images, order, n_front, F=None, B=None, accumulate=False):
+    """Collapse cached fp16 renders [K, H, W, 4] (torch.float16, or int16
+    holding binary16 bits) into F and B (fp32 [H, W, 4])."""
+    if images.dtype not in (torch.float16, torch.int16):
+        raise ValueError("images must be float16 (or int16 bit patterns)")
+    if not images.is_cuda or not images.is_contiguous() or images.dim() != 4:
+        raise ValueError("images must be a contiguous GPU tensor [K, H, W, 4]")
+    k, H, W, c = images.shape
+    if c != 4:
+        raise ValueError("images must be RGBA")
+    dev = images.device
+    if F is None:
+        F = _empty((H, W, 4), torch.float32, dev)
+    if B is None:
+        B = _empty((H, W, 4), torch.float32, dev)
+    _need(F, "F", torch.float32, (H, W, 4))
+    _need(B, "B", torch.float32, (H, W, 4))
+    order_arr = (C.c_int32 * max(k, 1))(*[int(x) for x in order])
+    check(_lib.load().abcd_composite_cache(W, H, k, _ptr(images), order_arr, int(n_front), _ptr(F),
+                                           _ptr(B), 1 if accumulate else 0, _stream()))
+    return F, B
+
+
+def loss_l1_grad(out, target, bg=None, dL_dout=None, loss=None):
+    H, W = out.shape[:2]
+    _need(out, "out", torch.float32, (H, W, 4))
+    _need(target, "target", torch.float32, (H, W, 3))
+    _opt(loss, "loss", torch.float32, (1,))
+    if dL_dout is None:
+        dL_dout = torch.empty_like(out)
+    bg_arr = None if bg is None else (C.c_float * 3)(*[float(x) for x in bg])
+    check(_lib.load().abcd_loss_l1_grad(W, H, _ptr(out), _ptr(target), bg_arr, _ptr(dL_dout),
+                                        _ptr(loss), _stream()))
+    return dL_dout
+
+
+# ------------------------------------------------------------------ timing
+
+def timing_enable(flag=True):
+    check(_lib.load().abcd_timing_enable(1 if flag else 0))
+
+
+def timing_reset():
+    check(_lib.load().abcd_timing_reset())
+
+
+def timing_read(kernel):
+    ms = C.c_double(0)
+    cnt = C.c_int64(0)
+    check(_lib.load().abcd_timing_read(kernel.encode(), C.byref(ms), C.byref(cnt)))
+    return ms.value, cnt.value
+
+
+__all__ = ["AbcdError", "project", "bin_sort", "bin_sort_workspace_size", "render_fwd",
+           "render_bwd", "render_bwd_workspace_size", "composite_cache", "loss_l1_grad",
+           "timing_enable", "timing_reset", "timing_read", "version", "n_tiles"]

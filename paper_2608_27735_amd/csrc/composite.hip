@@ -1,0 +1,146 @@
+// composite.hip -- collapse of cached per-partition renders into F and B.
+//
+// The paper pre-renders every frozen partition per camera and, by the
+// associativity of alpha compositing, collapses the renders in front of the
+// active partition into F and those behind it into B (Abstract; Method
+// section). Per pixel this is a left fold of premultiplied "over":
+//   acc <- acc + (1 - acc_alpha) x,
+// over the fp16 cached images in front-to-back order. The kernel is a pure
+// HBM stream (8 bytes per layer-pixel read, 32 per pixel written): each thread
+// owns two adjacent pixels, so every layer is one 16-byte load per thread,
+// and the layer order travels in the kernel arguments.
+#include "abcd_internal.h"
+
+namespace abcd {
+namespace {
+
+constexpr int kMaxLayers = 448;  // layers per launch (order table in kernel arguments)
+constexpr int kBatch = 8;        // loads in flight per thread
+
+struct LayerTable {
+  int32_t idx[kMaxLayers];
+};
+
+// modes: 0 overwrite with the fold, 1 fold behind the incoming value, 2 leave untouched
+struct FoldPlan {
+  int nf, nb, mode_f, mode_b;
+};
+
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float4 to_f4(uint2 bits) {
+  const h4 h = __builtin_bit_cast(h4, bits);
+  return make_float4((float)h[0], (float)h[1], (float)h[2], (float)h[3]);
+}
+
+__device__ __forceinline__ void over(float4& acc, const float4 x) {
+  const float s = 1.0f - acc.w;
+  acc.x += s * x.x;
+  acc.y += s * x.y;
+  acc.z += s * x.z;
+  acc.w += s * x.w;
+}
+
+// Fold layers tab[first .. first+count) at pixel pair `pp` (or single pixel).
+template <bool kPair>
+__device__ __forceinline__ void fold(const uint2* __restrict__ img, int64_t npix, int64_t pp,
+                                     const LayerTable& tab, int first, int count, float4& a0,
+                                     float4& a1) {
+  for (int j0 = 0; j0 < count; j0 += kBatch) {
+    const int m = min(kBatch, count - j0);
+    uint4 v[kBatch];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      if (b < m) {
+        const uint2* src = img + (int64_t)tab.idx[first + j0 + b] * npix + pp;
+        if (kPair) {
+          v[b] = *reinterpret_cast<const uint4*>(src);
+        } else {
+          const uint2 s = *src;
+          v[b] = make_uint4(s.x, s.y, 0u, 0u);
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      if (b < m) {
+        over(a0, to_f4(make_uint2(v[b].x, v[b].y)));
+        if (kPair) over(a1, to_f4(make_uint2(v[b].z, v[b].w)));
+      }
+    }
+  }
+}
+
+template <bool kPair>
+__global__ __launch_bounds__(256) void composite_kernel(int64_t npix, const uint2* __restrict__ img,
+                                                        LayerTable tab, FoldPlan plan,
+                                                        float4* __restrict__ F,
+                                                        float4* __restrict__ B) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t pp = kPair ? 2 * t : t;
+  if (pp >= npix) return;
+  const float4 zero = make_float4(0, 0, 0, 0);
+  // F
+  if (plan.mode_f != 2) {
+    float4 a0 = plan.mode_f == 1 ? F[pp] : zero;
+    float4 a1 = (kPair && plan.mode_f == 1) ? F[pp + 1] : zero;
+    fold<kPair>(img, npix, pp, tab, 0, plan.nf, a0, a1);
+    F[pp] = a0;
+    if (kPair) F[pp + 1] = a1;
+  }
+  // B
+  if (plan.mode_b != 2) {
+    float4 a0 = plan.mode_b == 1 ? B[pp] : zero;
+    float4 a1 = (kPair && plan.mode_b == 1) ? B[pp + 1] : zero;
+    fold<kPair>(img, npix, pp, tab, plan.nf, plan.nb, a0, a1);
+    B[pp] = a0;
+    if (kPair) B[pp + 1] = a1;
+  }
+}
+
+}  // namespace
+
+int32_t launch_composite(int width, int height, int k, const uint16_t* images,
+                         const int32_t* order, int n_front, float* F, float* B, int accumulate,
+                         hipStream_t stream) {
+  const int64_t npix = (int64_t)width * height;
+  const uint2* img = reinterpret_cast<const uint2*>(images);
+  // pairs need 16-byte alignment of every layer: even pixel count, aligned base
+  const bool pair = (npix % 2 == 0) && ((reinterpret_cast<uintptr_t>(images) & 15) == 0) &&
+                    ((reinterpret_cast<uintptr_t>(F) & 31) == 0) &&
+                    ((reinterpret_cast<uintptr_t>(B) & 31) == 0);
+  const int64_t threads = pair ? npix / 2 : npix;
+  const int64_t blocks = (threads + kBlock - 1) / kBlock;
+  int fi = 0, bi = 0;
+  const int nfront = n_front, nback = k - n_front;
+  bool first = true;
+  if (k == 0 && accumulate) return ABCD_OK;
+  while (first || fi < nfront || bi < nback) {
+    LayerTable tab;
+    FoldPlan plan;
+    plan.nf = std::min(nfront - fi, kMaxLayers);
+    plan.nb = std::min(nback - bi, kMaxLayers - plan.nf);
+    for (int j = 0; j < plan.nf; ++j) tab.idx[j] = order[fi + j];
+    for (int j = 0; j < plan.nb; ++j) tab.idx[plan.nf + j] = order[n_front + bi + j];
+    // a layer group that gets no layers in this launch is left alone, except
+    // on the first launch without accumulation, which must write transparent
+    plan.mode_f = (fi > 0 || accumulate) ? (plan.nf ? 1 : 2) : 0;
+    plan.mode_b = (bi > 0 || accumulate) ? (plan.nb ? 1 : 2) : 0;
+    if (!first && plan.nf == 0) plan.mode_f = 2;
+    if (!first && plan.nb == 0) plan.mode_b = 2;
+    if (pair) {
+      ABCD_LAUNCH("composite", composite_kernel<true>, blocks, kBlock, 0, stream, npix, img, tab,
+                  plan, reinterpret_cast<float4*>(F), reinterpret_cast<float4*>(B));
+    } else {
+      ABCD_LAUNCH("composite", composite_kernel<false>, blocks, kBlock, 0, stream, npix, img, tab,
+                  plan, reinterpret_cast<float4*>(F), reinterpret_cast<float4*>(B));
+    }
+    ABCD_HIP(hipGetLastError());
+    fi += plan.nf;
+    bi += plan.nb;
+    first = false;
+  }
+  return ABCD_OK;
+}
+
+}  // namespace abcd

@@ -1,0 +1,438 @@
+// project.hip -- EWA projection of 3D Gaussians (forward) and its chain rule
+// (backward), one thread per Gaussian.
+//
+// The paper renders the active partition with 3D Gaussian Splatting
+// (Introduction; Method section). Each Gaussian is projected to a 2D Gaussian:
+// mean by the pinhole map, covariance by the first-order (EWA) approximation
+// J W Sigma W^T J^T of the perspective map, dilated by eps2d, colour from real
+// spherical harmonics of the view direction, opacity by a sigmoid.
+//
+// The values that decide culling, the tile rectangle and the depth key are
+// computed with a fixed fp32 operation order (no contraction, correctly
+// rounded division and square root, exp of the log-scale taken in double and
+// rounded once), so binning is reproducible bit for bit on any IEEE machine
+// that follows the same order.
+#include "abcd_internal.h"
+
+namespace abcd {
+namespace {
+
+// Real orthonormal spherical harmonics to degree 3 of a unit direction, index
+// l^2 + l + m, written as homogeneous harmonic polynomials:
+//   l=1: y, z, x;  l=2: xy, yz, 2z^2-x^2-y^2, xz, x^2-y^2;
+//   l=3: y(3x^2-y^2), xyz, y(4z^2-x^2-y^2), z(2z^2-3x^2-3y^2),
+//        x(4z^2-x^2-y^2), z(x^2-y^2), x(x^2-3y^2),
+// each with its normalisation constant.
+constexpr float kY0 = 0.28209479177387814f;   // 1/(2 sqrt(pi))
+constexpr float kY1 = 0.48860251190291992f;   // sqrt(3/(4 pi))
+constexpr float kY2a = 1.0925484305920792f;   // sqrt(15/pi)/2
+constexpr float kY2b = 0.31539156525252005f;  // sqrt(5/pi)/4
+constexpr float kY2c = 0.54627421529603959f;  // sqrt(15/pi)/4
+constexpr float kY3a = 0.59004358992664352f;  // sqrt(35/(2 pi))/4
+constexpr float kY3b = 2.8906114426405538f;   // sqrt(105/pi)/2
+constexpr float kY3c = 0.45704579946446572f;  // sqrt(21/(2 pi))/4
+constexpr float kY3d = 0.37317633259011540f;  // sqrt(7/pi)/4
+constexpr float kY3e = 1.4453057213202769f;   // sqrt(105/pi)/4
+
+__device__ __forceinline__ int sh_count(int degree) { return (degree + 1) * (degree + 1); }
+
+// Y[16] and, when G != nullptr, dY/d(x, y, z) as G[16][3].
+__device__ __forceinline__ void sh_eval(int degree, float x, float y, float z, float* Y, float* G) {
+  Y[0] = kY0;
+  if (G) G[0] = G[1] = G[2] = 0.0f;
+  if (degree < 1) return;
+  Y[1] = kY1 * y;
+  Y[2] = kY1 * z;
+  Y[3] = kY1 * x;
+  if (G) {
+    G[3] = 0; G[4] = kY1; G[5] = 0;
+    G[6] = 0; G[7] = 0; G[8] = kY1;
+    G[9] = kY1; G[10] = 0; G[11] = 0;
+  }
+  if (degree < 2) return;
+  const float xx = x * x, yy = y * y, zz = z * z;
+  Y[4] = kY2a * x * y;
+  Y[5] = kY2a * y * z;
+  Y[6] = kY2b * (2.0f * zz - xx - yy);
+  Y[7] = kY2a * x * z;
+  Y[8] = kY2c * (xx - yy);
+  if (G) {
+    G[12] = kY2a * y; G[13] = kY2a * x; G[14] = 0;
+    G[15] = 0; G[16] = kY2a * z; G[17] = kY2a * y;
+    G[18] = -2.0f * kY2b * x; G[19] = -2.0f * kY2b * y; G[20] = 4.0f * kY2b * z;
+    G[21] = kY2a * z; G[22] = 0; G[23] = kY2a * x;
+    G[24] = 2.0f * kY2c * x; G[25] = -2.0f * kY2c * y; G[26] = 0;
+  }
+  if (degree < 3) return;
+  Y[9] = kY3a * y * (3.0f * xx - yy);
+  Y[10] = kY3b * x * y * z;
+  Y[11] = kY3c * y * (4.0f * zz - xx - yy);
+  Y[12] = kY3d * z * (2.0f * zz - 3.0f * xx - 3.0f * yy);
+  Y[13] = kY3c * x * (4.0f * zz - xx - yy);
+  Y[14] = kY3e * z * (xx - yy);
+  Y[15] = kY3a * x * (xx - 3.0f * yy);
+  if (G) {
+    G[27] = kY3a * 6.0f * x * y; G[28] = kY3a * 3.0f * (xx - yy); G[29] = 0;
+    G[30] = kY3b * y * z; G[31] = kY3b * x * z; G[32] = kY3b * x * y;
+    G[33] = -2.0f * kY3c * x * y; G[34] = kY3c * (4.0f * zz - xx - 3.0f * yy);
+    G[35] = 8.0f * kY3c * y * z;
+    G[36] = -6.0f * kY3d * x * z; G[37] = -6.0f * kY3d * y * z;
+    G[38] = kY3d * (6.0f * zz - 3.0f * xx - 3.0f * yy);
+    G[39] = kY3c * (4.0f * zz - 3.0f * xx - yy); G[40] = -2.0f * kY3c * x * y;
+    G[41] = 8.0f * kY3c * x * z;
+    G[42] = 2.0f * kY3e * x * z; G[43] = -2.0f * kY3e * y * z; G[44] = kY3e * (xx - yy);
+    G[45] = kY3a * 3.0f * (xx - yy); G[46] = -6.0f * kY3a * x * y; G[47] = 0;
+  }
+}
+
+// Intermediates of the fp32 projection chain of one Gaussian.
+struct Proj {
+  float tx, ty, tz, xc, yc;
+  bool clx, cly;
+  float j00, j02, j11, j12;
+  float s0, s1, s2;
+  float qn, qw, qx, qy, qz;
+  float r[9];        // Rq, row major
+  float m[9];        // Rq diag(s)
+  float S[6];        // Sigma: 00 01 02 11 12 22
+  float T[6];        // J Rcam: row 0 then row 1
+  float A, B, C, det;
+  float u, v, rad;
+  int x0, y0, x1, y1;
+};
+
+// The fixed-order fp32 chain. Every statement below is evaluated as written:
+// left-to-right sums of separately rounded products; nothing is fused except
+// the two fmaf of Kahan's determinant.
+__device__ bool project_chain(const abcd_camera& c, const abcd_raster_params& p, int ntx, int nty,
+                              const float* mu, const float* ls, const float* q, Proj& o) {
+#pragma clang fp contract(off)
+  const float* R = c.R;
+  o.tx = ((R[0] * mu[0] + R[1] * mu[1]) + R[2] * mu[2]) + c.t[0];
+  o.ty = ((R[3] * mu[0] + R[4] * mu[1]) + R[5] * mu[2]) + c.t[1];
+  o.tz = ((R[6] * mu[0] + R[7] * mu[1]) + R[8] * mu[2]) + c.t[2];
+  if (!(o.tz > c.near_plane)) return false;
+  const float xr = o.tx / o.tz;
+  const float yr = o.ty / o.tz;
+  o.u = c.fx * xr + c.cx;
+  o.v = c.fy * yr + c.cy;
+  const float limx = (p.guard * (0.5f * (float)c.width)) / c.fx;
+  const float limy = (p.guard * (0.5f * (float)c.height)) / c.fy;
+  o.clx = xr < -limx || xr > limx;
+  o.cly = yr < -limy || yr > limy;
+  o.xc = xr < -limx ? -limx : (xr > limx ? limx : xr);
+  o.yc = yr < -limy ? -limy : (yr > limy ? limy : yr);
+  o.j00 = c.fx / o.tz;
+  o.j02 = -(c.fx * o.xc) / o.tz;
+  o.j11 = c.fy / o.tz;
+  o.j12 = -(c.fy * o.yc) / o.tz;
+
+  o.s0 = (float)exp((double)ls[0]);
+  o.s1 = (float)exp((double)ls[1]);
+  o.s2 = (float)exp((double)ls[2]);
+
+  o.qn = sqrtf(((q[0] * q[0] + q[1] * q[1]) + q[2] * q[2]) + q[3] * q[3]);
+  if (!(o.qn > 0.0f) || !isfinite(o.qn)) return false;
+  const float w = q[0] / o.qn, x = q[1] / o.qn, y = q[2] / o.qn, z = q[3] / o.qn;
+  o.qw = w; o.qx = x; o.qy = y; o.qz = z;
+  float* r = o.r;
+  r[0] = 1.0f - 2.0f * (y * y + z * z);
+  r[1] = 2.0f * (x * y - w * z);
+  r[2] = 2.0f * (x * z + w * y);
+  r[3] = 2.0f * (x * y + w * z);
+  r[4] = 1.0f - 2.0f * (x * x + z * z);
+  r[5] = 2.0f * (y * z - w * x);
+  r[6] = 2.0f * (x * z - w * y);
+  r[7] = 2.0f * (y * z + w * x);
+  r[8] = 1.0f - 2.0f * (x * x + y * y);
+  float* m = o.m;
+  m[0] = r[0] * o.s0; m[1] = r[1] * o.s1; m[2] = r[2] * o.s2;
+  m[3] = r[3] * o.s0; m[4] = r[4] * o.s1; m[5] = r[5] * o.s2;
+  m[6] = r[6] * o.s0; m[7] = r[7] * o.s1; m[8] = r[8] * o.s2;
+  float* S = o.S;
+  S[0] = (m[0] * m[0] + m[1] * m[1]) + m[2] * m[2];
+  S[1] = (m[0] * m[3] + m[1] * m[4]) + m[2] * m[5];
+  S[2] = (m[0] * m[6] + m[1] * m[7]) + m[2] * m[8];
+  S[3] = (m[3] * m[3] + m[4] * m[4]) + m[5] * m[5];
+  S[4] = (m[3] * m[6] + m[4] * m[7]) + m[5] * m[8];
+  S[5] = (m[6] * m[6] + m[7] * m[7]) + m[8] * m[8];
+  float* T = o.T;
+  T[0] = o.j00 * R[0] + o.j02 * R[6];
+  T[1] = o.j00 * R[1] + o.j02 * R[7];
+  T[2] = o.j00 * R[2] + o.j02 * R[8];
+  T[3] = o.j11 * R[3] + o.j12 * R[6];
+  T[4] = o.j11 * R[4] + o.j12 * R[7];
+  T[5] = o.j11 * R[5] + o.j12 * R[8];
+  // U = T Sigma (Sigma symmetric: S01 = S10, ...)
+  const float U00 = (T[0] * S[0] + T[1] * S[1]) + T[2] * S[2];
+  const float U01 = (T[0] * S[1] + T[1] * S[3]) + T[2] * S[4];
+  const float U02 = (T[0] * S[2] + T[1] * S[4]) + T[2] * S[5];
+  const float U10 = (T[3] * S[0] + T[4] * S[1]) + T[5] * S[2];
+  const float U11 = (T[3] * S[1] + T[4] * S[3]) + T[5] * S[4];
+  const float U12 = (T[3] * S[2] + T[4] * S[4]) + T[5] * S[5];
+  o.A = ((U00 * T[0] + U01 * T[1]) + U02 * T[2]) + p.eps2d;
+  o.B = (U00 * T[3] + U01 * T[4]) + U02 * T[5];
+  o.C = ((U10 * T[3] + U11 * T[4]) + U12 * T[5]) + p.eps2d;
+  // Kahan: A*C - B*B with one rounding error
+  const float kw = o.B * o.B;
+  const float ke = fmaf(-o.B, o.B, kw);
+  const float kf = fmaf(o.A, o.C, -kw);
+  o.det = kf + ke;
+  if (!(o.det > 0.0f)) return false;
+  const float mid = 0.5f * (o.A + o.C);
+  float disc = mid * mid - o.det;
+  disc = disc > 0.0f ? disc : 0.0f;
+  const float lmax = mid + sqrtf(disc);
+  o.rad = p.radius_sigmas * sqrtf(lmax);
+  if (!isfinite(o.u) || !isfinite(o.v) || !isfinite(o.rad)) return false;
+  return tile_rect(o.u, o.v, o.rad, ntx, nty, o.x0, o.y0, o.x1, o.y1);
+}
+
+__global__ __launch_bounds__(256) void project_kernel(
+    abcd_camera cam, abcd_raster_params prm, int64_t n, int ntx, int nty, const float* __restrict__ means,
+    const float* __restrict__ log_scales, const float* __restrict__ quats,
+    const float* __restrict__ opacity_logits, const float* __restrict__ sh, float* __restrict__ means2d,
+    float* __restrict__ conic_opacity, float* __restrict__ depth, float* __restrict__ radius,
+    uint32_t* __restrict__ tiles_touched, float* __restrict__ rgb) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const float mu[3] = {means[3 * i], means[3 * i + 1], means[3 * i + 2]};
+  const float ls[3] = {log_scales[3 * i], log_scales[3 * i + 1], log_scales[3 * i + 2]};
+  const float q[4] = {quats[4 * i], quats[4 * i + 1], quats[4 * i + 2], quats[4 * i + 3]};
+  Proj pr;
+  const bool vis = project_chain(cam, prm, ntx, nty, mu, ls, q, pr);
+  if (!vis) {
+    means2d[2 * i] = 0.0f;
+    means2d[2 * i + 1] = 0.0f;
+    reinterpret_cast<float4*>(conic_opacity)[i] = make_float4(0, 0, 0, 0);
+    depth[i] = 0.0f;
+    radius[i] = 0.0f;
+    tiles_touched[i] = 0u;
+    rgb[3 * i] = rgb[3 * i + 1] = rgb[3 * i + 2] = 0.0f;
+    return;
+  }
+  const float inv = 1.0f / pr.det;
+  const float ca = pr.C * inv, cb = -pr.B * inv, cc = pr.A * inv;
+  const float o = 1.0f / (1.0f + __expf(-opacity_logits[i]));
+  // colour from the view direction
+  float dx = mu[0] - cam.campos[0], dy = mu[1] - cam.campos[1], dz = mu[2] - cam.campos[2];
+  const float dn = rsqrtf(dx * dx + dy * dy + dz * dz);
+  dx *= dn; dy *= dn; dz *= dn;
+  float Y[16];
+  sh_eval(prm.sh_degree, dx, dy, dz, Y, nullptr);
+  const int nc = sh_count(prm.sh_degree);
+  const float* k = sh + (int64_t)3 * nc * i;
+  float col[3] = {0.5f, 0.5f, 0.5f};
+  for (int b = 0; b < nc; ++b) {
+    col[0] += Y[b] * k[3 * b];
+    col[1] += Y[b] * k[3 * b + 1];
+    col[2] += Y[b] * k[3 * b + 2];
+  }
+  means2d[2 * i] = pr.u;
+  means2d[2 * i + 1] = pr.v;
+  reinterpret_cast<float4*>(conic_opacity)[i] = make_float4(ca, cb, cc, o);
+  depth[i] = pr.tz;
+  radius[i] = pr.rad;
+  tiles_touched[i] = (uint32_t)((pr.x1 - pr.x0 + 1) * (pr.y1 - pr.y0 + 1));
+  rgb[3 * i] = fmaxf(col[0], 0.0f);
+  rgb[3 * i + 1] = fmaxf(col[1], 0.0f);
+  rgb[3 * i + 2] = fmaxf(col[2], 0.0f);
+}
+
+// Chain rule from the screen-space gradients g2d[i][9] = dL/d(u, v, a, b, c,
+// o, r, g, b) to the parameters; exact derivative of the forward chain
+// (guard-band clamp and colour clamp have zero derivative where active).
+__global__ __launch_bounds__(256) void project_bwd_kernel(
+    abcd_camera cam, abcd_raster_params prm, int64_t n, int ntx, int nty,
+    const float* __restrict__ means, const float* __restrict__ log_scales,
+    const float* __restrict__ quats, const float* __restrict__ opacity_logits,
+    const float* __restrict__ sh, const float* __restrict__ radius, const float* __restrict__ g2d,
+    float* __restrict__ d_means, float* __restrict__ d_log_scales, float* __restrict__ d_quats,
+    float* __restrict__ d_opacity_logits, float* __restrict__ d_sh, float* __restrict__ d_means2d,
+    int accumulate) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int nc = sh_count(prm.sh_degree);
+  float gm[3] = {0, 0, 0}, gl[3] = {0, 0, 0}, gq[4] = {0, 0, 0, 0}, gop = 0.0f;
+  float gsh[48];
+  for (int k = 0; k < 3 * nc; ++k) gsh[k] = 0.0f;
+  float gu = 0.0f, gv = 0.0f;
+  const float mu[3] = {means[3 * i], means[3 * i + 1], means[3 * i + 2]};
+  Proj pr;
+  bool vis = radius[i] > 0.0f;
+  if (vis) {
+    const float ls[3] = {log_scales[3 * i], log_scales[3 * i + 1], log_scales[3 * i + 2]};
+    const float q[4] = {quats[4 * i], quats[4 * i + 1], quats[4 * i + 2], quats[4 * i + 3]};
+    vis = project_chain(cam, prm, ntx, nty, mu, ls, q, pr);
+  }
+  if (vis) {
+    const float* G = g2d + 9 * i;
+    gu = G[0];
+    gv = G[1];
+    const float ga = G[2], gb = G[3], gc = G[4], go = G[5];
+    // conic Q = Sigma'^-1:  dL/dSigma' = -Q GQ Q, GQ = [[ga, gb/2], [gb/2, gc]]
+    const float inv = 1.0f / pr.det;
+    const float qa = pr.C * inv, qb = -pr.B * inv, qc = pr.A * inv;
+    const float hb = 0.5f * gb;
+    const float P00 = qa * ga + qb * hb, P01 = qa * hb + qb * gc;
+    const float P10 = qb * ga + qc * hb, P11 = qb * hb + qc * gc;
+    const float G00 = -(P00 * qa + P01 * qb);
+    const float G01 = -0.5f * ((P00 * qb + P01 * qc) + (P10 * qa + P11 * qb));
+    const float G11 = -(P10 * qb + P11 * qc);
+    // Sigma' = T Sigma T^T + eps I
+    const float* T = pr.T;
+    const float* S = pr.S;
+    const float Sm[9] = {S[0], S[1], S[2], S[1], S[3], S[4], S[2], S[4], S[5]};
+    float GS[9];  // T^T G T
+    for (int a = 0; a < 3; ++a)
+      for (int b = 0; b < 3; ++b) {
+        const float t0a = T[a], t1a = T[3 + a], t0b = T[b], t1b = T[3 + b];
+        GS[3 * a + b] = t0a * (G00 * t0b + G01 * t1b) + t1a * (G01 * t0b + G11 * t1b);
+      }
+    float GT[6];  // 2 G T Sigma
+    for (int r = 0; r < 2; ++r) {
+      const float g0 = r == 0 ? G00 : G01, g1 = r == 0 ? G01 : G11;
+      for (int b = 0; b < 3; ++b) {
+        float acc = 0.0f;
+        for (int k = 0; k < 3; ++k) acc += (g0 * T[k] + g1 * T[3 + k]) * Sm[3 * k + b];
+        GT[3 * r + b] = 2.0f * acc;
+      }
+    }
+    // T = J Rcam
+    const float* Rc = cam.R;
+    const float gj00 = GT[0] * Rc[0] + GT[1] * Rc[1] + GT[2] * Rc[2];
+    const float gj02 = GT[0] * Rc[6] + GT[1] * Rc[7] + GT[2] * Rc[8];
+    const float gj11 = GT[3] * Rc[3] + GT[4] * Rc[4] + GT[5] * Rc[5];
+    const float gj12 = GT[3] * Rc[6] + GT[4] * Rc[7] + GT[5] * Rc[8];
+    // J(t), (u, v)(t)
+    const float fx = cam.fx, fy = cam.fy, tz = pr.tz, iz = 1.0f / tz, iz2 = iz * iz;
+    float gtx = 0.0f, gty = 0.0f, gtz = 0.0f;
+    gtz += -fx * iz2 * gj00 - fy * iz2 * gj11 + fx * pr.xc * iz2 * gj02 + fy * pr.yc * iz2 * gj12;
+    const float gxc = -fx * iz * gj02, gyc = -fy * iz * gj12;
+    if (!pr.clx) {
+      gtx += gxc * iz;
+      gtz -= gxc * pr.tx * iz2;
+    }
+    if (!pr.cly) {
+      gty += gyc * iz;
+      gtz -= gyc * pr.ty * iz2;
+    }
+    gtx += fx * iz * gu;
+    gtz -= fx * pr.tx * iz2 * gu;
+    gty += fy * iz * gv;
+    gtz -= fy * pr.ty * iz2 * gv;
+    for (int k = 0; k < 3; ++k) gm[k] = Rc[k] * gtx + Rc[3 + k] * gty + Rc[6 + k] * gtz;
+    // Sigma = M M^T, M = Rq diag(s)
+    float GM[9];
+    for (int a = 0; a < 3; ++a)
+      for (int b = 0; b < 3; ++b)
+        GM[3 * a + b] = 2.0f * (GS[3 * a] * pr.m[b] + GS[3 * a + 1] * pr.m[3 + b] +
+                                GS[3 * a + 2] * pr.m[6 + b]);
+    const float s[3] = {pr.s0, pr.s1, pr.s2};
+    float gR[9];
+    for (int b = 0; b < 3; ++b) {
+      float gs = 0.0f;
+      for (int a = 0; a < 3; ++a) {
+        gs += GM[3 * a + b] * pr.r[3 * a + b];
+        gR[3 * a + b] = GM[3 * a + b] * s[b];
+      }
+      gl[b] = gs * s[b];
+    }
+    // rotation entries as functions of the unit quaternion
+    const float w = pr.qw, x = pr.qx, y = pr.qy, z = pr.qz;
+    float gw = 0.0f, gx = 0.0f, gy = 0.0f, gz = 0.0f;
+    gy += -4.0f * y * gR[0]; gz += -4.0f * z * gR[0];
+    gw += -2.0f * z * gR[1]; gx += 2.0f * y * gR[1]; gy += 2.0f * x * gR[1]; gz += -2.0f * w * gR[1];
+    gw += 2.0f * y * gR[2]; gx += 2.0f * z * gR[2]; gy += 2.0f * w * gR[2]; gz += 2.0f * x * gR[2];
+    gw += 2.0f * z * gR[3]; gx += 2.0f * y * gR[3]; gy += 2.0f * x * gR[3]; gz += 2.0f * w * gR[3];
+    gx += -4.0f * x * gR[4]; gz += -4.0f * z * gR[4];
+    gw += -2.0f * x * gR[5]; gx += -2.0f * w * gR[5]; gy += 2.0f * z * gR[5]; gz += 2.0f * y * gR[5];
+    gw += -2.0f * y * gR[6]; gx += 2.0f * z * gR[6]; gy += -2.0f * w * gR[6]; gz += 2.0f * x * gR[6];
+    gw += 2.0f * x * gR[7]; gx += 2.0f * w * gR[7]; gy += 2.0f * z * gR[7]; gz += 2.0f * y * gR[7];
+    gx += -4.0f * x * gR[8]; gy += -4.0f * y * gR[8];
+    const float dotq = gw * w + gx * x + gy * y + gz * z;
+    const float iq = 1.0f / pr.qn;
+    gq[0] = (gw - w * dotq) * iq;
+    gq[1] = (gx - x * dotq) * iq;
+    gq[2] = (gy - y * dotq) * iq;
+    gq[3] = (gz - z * dotq) * iq;
+    // opacity
+    const float o = 1.0f / (1.0f + __expf(-opacity_logits[i]));
+    gop = go * o * (1.0f - o);
+    // colour
+    float d[3] = {mu[0] - cam.campos[0], mu[1] - cam.campos[1], mu[2] - cam.campos[2]};
+    const float dn = sqrtf(d[0] * d[0] + d[1] * d[1] + d[2] * d[2]);
+    const float idn = 1.0f / dn;
+    const float dir[3] = {d[0] * idn, d[1] * idn, d[2] * idn};
+    float Y[16], YG[48];
+    sh_eval(prm.sh_degree, dir[0], dir[1], dir[2], Y, YG);
+    const float* k = sh + (int64_t)3 * nc * i;
+    float gdir[3] = {0, 0, 0};
+    for (int ch = 0; ch < 3; ++ch) {
+      float raw = 0.5f;
+      for (int b = 0; b < nc; ++b) raw += Y[b] * k[3 * b + ch];
+      if (!(raw > 0.0f)) continue;
+      const float gcol = G[6 + ch];
+      for (int b = 0; b < nc; ++b) {
+        gsh[3 * b + ch] = Y[b] * gcol;
+        const float kc = gcol * k[3 * b + ch];
+        gdir[0] += kc * YG[3 * b];
+        gdir[1] += kc * YG[3 * b + 1];
+        gdir[2] += kc * YG[3 * b + 2];
+      }
+    }
+    const float dd = gdir[0] * dir[0] + gdir[1] * dir[1] + gdir[2] * dir[2];
+    for (int a = 0; a < 3; ++a) gm[a] += (gdir[a] - dir[a] * dd) * idn;
+  }
+  float* om = d_means + 3 * i;
+  float* ol = d_log_scales + 3 * i;
+  float* oq = d_quats + 4 * i;
+  float* os = d_sh + (int64_t)3 * nc * i;
+  if (accumulate) {
+    for (int a = 0; a < 3; ++a) { om[a] += gm[a]; ol[a] += gl[a]; }
+    for (int a = 0; a < 4; ++a) oq[a] += gq[a];
+    d_opacity_logits[i] += gop;
+    for (int a = 0; a < 3 * nc; ++a) os[a] += gsh[a];
+    if (d_means2d) { d_means2d[2 * i] += gu; d_means2d[2 * i + 1] += gv; }
+  } else {
+    for (int a = 0; a < 3; ++a) { om[a] = gm[a]; ol[a] = gl[a]; }
+    for (int a = 0; a < 4; ++a) oq[a] = gq[a];
+    d_opacity_logits[i] = gop;
+    for (int a = 0; a < 3 * nc; ++a) os[a] = gsh[a];
+    if (d_means2d) { d_means2d[2 * i] = gu; d_means2d[2 * i + 1] = gv; }
+  }
+}
+
+}  // namespace
+
+int32_t launch_project(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
+                       const float* means, const float* log_scales, const float* quats,
+                       const float* opacity_logits, const float* sh, float* means2d,
+                       float* conic_opacity, float* depth, float* radius, uint32_t* tiles_touched,
+                       float* rgb, hipStream_t stream) {
+  if (n == 0) return ABCD_OK;
+  const int64_t blocks = (n + kBlock - 1) / kBlock;
+  ABCD_LAUNCH("project", project_kernel, blocks, kBlock, 0, stream, cam, prm, n,
+              tiles_x(cam.width), tiles_y(cam.height), means, log_scales, quats, opacity_logits,
+              sh, means2d, conic_opacity, depth, radius, tiles_touched, rgb);
+  ABCD_HIP(hipGetLastError());
+  return ABCD_OK;
+}
+
+int32_t launch_project_bwd(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
+                           const float* means, const float* log_scales, const float* quats,
+                           const float* opacity_logits, const float* sh, const float* radius,
+                           const float* g2d, float* d_means, float* d_log_scales, float* d_quats,
+                           float* d_opacity_logits, float* d_sh, float* d_means2d,
+                           int accumulate, hipStream_t stream) {
+  if (n == 0) return ABCD_OK;
+  const int64_t blocks = (n + kBlock - 1) / kBlock;
+  ABCD_LAUNCH("project_bwd", project_bwd_kernel, blocks, kBlock, 0, stream, cam, prm, n,
+              tiles_x(cam.width), tiles_y(cam.height), means, log_scales, quats, opacity_logits,
+              sh, radius, g2d, d_means, d_log_scales, d_quats, d_opacity_logits, d_sh, d_means2d,
+              accumulate);
+  ABCD_HIP(hipGetLastError());
+  return ABCD_OK;
+}
+
+}  // namespace abcd

@@ -1,0 +1,78 @@
+"""One ABCD active-block step on one camera, with every buffer allocated once.
+
+The paper's inner loop (Method section): for a sampled camera observing the
+active partition, render only the active partition, composite it with that
+camera's F and B, evaluate the reconstruction loss and back-propagate into the
+active parameters only. F and B come from collapsing the camera's cached
+frozen-partition renders (composite_cache), done once per (block, camera).
+
+This class only owns buffers and issues the C-ABI calls in order on the
+current stream; it never synchronises unless asked for the intersection count.
+"""
+import torch
+
+from . import api
+
+
+class ActiveBlockStep:
+    def __init__(self, cam, prm, params, capacity=None, headroom=1.25, bg=None):
+        self.cam, self.prm, self.params = cam, prm, params
+        self.bg = bg
+        n = params["means"].shape[0]
+        dev = params["means"].device
+        H, W = cam.height, cam.width
+        f32 = torch.float32
+        self.proj = dict(means2d=torch.empty((n, 2), dtype=f32, device=dev),
+                         conic_opacity=torch.empty((n, 4), dtype=f32, device=dev),
+                         depth=torch.empty((n,), dtype=f32, device=dev),
+                         radius=torch.empty((n,), dtype=f32, device=dev),
+                         tiles_touched=torch.empty((n,), dtype=torch.int32, device=dev),
+                         rgb=torch.empty((n, 3), dtype=f32, device=dev))
+        self.fwd = dict(out=torch.empty((H, W, 4), dtype=f32, device=dev),
+                        final_T=torch.empty((H, W), dtype=f32, device=dev),
+                        last=torch.empty((H, W), dtype=torch.int32, device=dev))
+        self.dL_dout = torch.empty((H, W, 4), dtype=f32, device=dev)
+        self.loss = torch.zeros((1,), dtype=f32, device=dev)
+        self.n_blends = torch.zeros((1,), dtype=torch.int64, device=dev)
+        self.bin_ws = torch.empty(max(api.bin_sort_workspace_size(n, W, H), 256), dtype=torch.uint8,
+                                  device=dev)
+        self.bwd_ws = torch.empty(max(api.render_bwd_workspace_size(n), 256), dtype=torch.uint8,
+                                  device=dev)
+        self.tile_ranges = torch.empty((api.n_tiles(W, H), 2), dtype=torch.int32, device=dev)
+        self.grads = {k: torch.zeros_like(params[k]) for k in
+                      ("means", "log_scales", "quats", "opacity_logits", "sh")}
+        if capacity is None:
+            # size the intersection buffer from one synchronising pass
+            api.project(cam, prm, **params, out=self.proj)
+            b = api.bin_sort(W, H, self.proj, capacity=0, workspace=self.bin_ws,
+                             tile_ranges=self.tile_ranges)
+            capacity = int(b["n_isect"] * headroom) + 1024
+        self.capacity = capacity
+        self.values = torch.empty((capacity,), dtype=torch.int32, device=dev)
+        self.bins = dict(values=self.values, tile_ranges=self.tile_ranges)
+
+    def project_and_bin(self, sync=False):
+        api.project(self.cam, self.prm, **self.params, out=self.proj)
+        b = api.bin_sort(self.cam.width, self.cam.height, self.proj, capacity=self.capacity,
+                         workspace=self.bin_ws, values=self.values, tile_ranges=self.tile_ranges,
+                         sync=sync)
+        return b["n_isect"]
+
+    def forward(self, F=None, B=None):
+        return api.render_fwd(self.cam, self.prm, self.bins, self.proj, F=F, B=B,
+                              n_blends=self.n_blends, out=self.fwd)
+
+    def loss_grad(self, target):
+        return api.loss_l1_grad(self.fwd["out"], target, bg=self.bg, dL_dout=self.dL_dout,
+                                loss=self.loss)
+
+    def backward(self, dL_dout, F=None, B=None):
+        return api.render_bwd(self.cam, self.prm, self.params, self.proj, self.bins, self.fwd,
+                              dL_dout, F=F, B=B, workspace=self.bwd_ws, grads=self.grads)
+
+    def step(self, target, F=None, B=None):
+        """project -> bin -> forward -> L1 gradient -> backward (no synchronisation)."""
+        self.project_and_bin(sync=False)
+        self.forward(F, B)
+        self.loss_grad(target)
+        return self.backward(self.dL_dout, F, B)
