@@ -1,0 +1,210 @@
+"""Benchmark of one ABCD active-block step on one MI355X.
+
+A step is one pass of the whole hot path on one camera:
+  composite_cache (99 cached fp16 partition renders -> F, B)
+  -> project -> bin_sort -> render_fwd (F over A over B) -> L1 gradient
+  -> render_bwd (gradients of the active parameters).
+Workload: the 1M-Gaussian active partition (SH degree 3, log-scales
+N(log 0.25, 0.5), means uniform in one 5-unit cell of a 5x5x4 grid) seen by
+camera 0 of a 200-camera elliptical orbit at 1297x840; F and B from the 99
+frozen cells, ordered front to back for that camera; seeded synthetic data.
+
+The metric is Gaussian-pixel blends per second: blended (pixel, Gaussian)
+pairs of the step divided by the step time (all inputs resident in HBM).
+Prints one JSON line.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Gaussian-pixel blends/sec (fwd+bwd) and ms per active-block step, 1 GPU"
+HBM_PEAK_GBS = 8000.0
+# fp32 vector peak without packed-fp32 instructions: 256 CUs x 4 SIMDs x 16
+# lanes x 2.4 GHz = 39.3 T lane-instructions/s (78.6 TFLOP/s counting FMA as 2)
+VALU_PEAK_TOPS = 39.3
+
+KERNELS = ["composite", "project", "depth_keys", "radix_hist", "radix_scan", "radix_scatter",
+           "bin_count", "bin_scan_columns", "bin_scan_tiles", "bin_scatter", "render_fwd",
+           "loss_l1", "zero_fill", "render_bwd", "project_bwd"]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--n", type=int, default=1_000_000)
+    ap.add_argument("--width", type=int, default=1297)
+    ap.add_argument("--height", type=int, default=840)
+    ap.add_argument("--cpu-baseline", type=int, default=1, help="time the CPU oracle on a sample")
+    ap.add_argument("--profile-kernels", type=int, default=1)
+    return ap.parse_args()
+
+
+def algorithmic_bytes(name, n, n_vis, m, npix, k, sh_coeffs):
+    """Bytes a kernel must move at minimum (inputs read once, outputs written once)."""
+    param = 4 * (3 + 3 + 4 + 1 + 3 * sh_coeffs)       # means, log-scales, quats, logit, SH
+    proj = 4 * (2 + 4 + 1 + 1 + 1 + 3)                 # means2d, conic_opacity, depth, radius, tiles, rgb
+    if name == "composite":
+        return npix * (8 * k + 32)
+    if name == "project":
+        return n * (param + proj)
+    if name == "project_bwd":
+        return n * (2 * param + 9 * 4 + 4)             # params in, grads out, g2d and radius in
+    if name == "bin_scatter":
+        return m * 4 + n_vis * 16
+    return None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              "(the path runs on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2608_27735_amd import api, synthetic as S
+    from paper_2608_27735_amd.step import ActiveBlockStep
+
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    w = S.active_block_1m(n=args.n, width=args.width, height=args.height)
+    cam, prm = w.cam, w.params
+    params = {k: torch.from_numpy(v).to(dev) for k, v in w.scene.items()}
+    order = [c for c in w.order if c != w.active]          # 99 frozen cells, front to back
+    n_front = w.order.index(w.active)
+    k = len(order)
+    images = S.cached_images_device(k, cam.height, cam.width, seed=4101, device=dev)
+    order_idx = list(range(k))                              # images are stored in front-to-back order
+    target = torch.from_numpy(S.rng(4102).uniform(0, 1, (cam.height, cam.width, 3))
+                              .astype(np.float32)).to(dev)
+    F = torch.empty((cam.height, cam.width, 4), dtype=torch.float32, device=dev)
+    B = torch.empty_like(F)
+    st = ActiveBlockStep(cam, prm, params)
+    m = st.project_and_bin(sync=True)
+    n_vis = int((st.proj["tiles_touched"] > 0).sum().item())
+    setup_s = time.time() - t0
+
+    def one_step():
+        api.composite_cache(images, order_idx, n_front, F=F, B=B)
+        st.step(target, F=F, B=B)
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    st.n_blends.zero_()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        one_step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    ms_step = ms_total / args.steps
+    blends_step = st.n_blends.item() / args.steps
+    value = blends_step / (ms_step / 1e3)
+
+    # per-kernel durations: HIP events around every launch, on the launch stream
+    kern = {}
+    if args.profile_kernels:
+        api.timing_reset()
+        api.timing_enable(True)
+        for _ in range(args.steps):
+            one_step()
+        torch.cuda.synchronize()
+        api.timing_enable(False)
+        for name in KERNELS:
+            ms, cnt = api.timing_read(name)
+            if cnt:
+                kern[name] = dict(ms_per_step=ms / args.steps, launches_per_step=cnt / args.steps,
+                                  ms_per_launch=ms / cnt)
+        api.timing_reset()
+    sh_coeffs = (prm.sh_degree + 1) ** 2
+    npix = cam.width * cam.height
+    dominant = max(kern, key=lambda x: kern[x]["ms_per_step"]) if kern else None
+    roofline = None
+    if dominant:
+        d = kern[dominant]
+        bytes_ = algorithmic_bytes(dominant, args.n, n_vis, m, npix, k, sh_coeffs)
+        if bytes_ is not None:
+            launch_bytes = bytes_ / d["launches_per_step"]
+            achieved = launch_bytes / (d["ms_per_launch"] / 1e3) / 1e9
+            roofline = dict(bound="hbm", kernel=dominant, achieved=achieved, peak=HBM_PEAK_GBS,
+                            unit="GB/s", frac=achieved / HBM_PEAK_GBS, traffic=None,
+                            algorithmic_bytes_per_launch=launch_bytes)
+        else:
+            roofline = dict(bound="alu", kernel=dominant, achieved=None, peak=VALU_PEAK_TOPS,
+                            unit="Tops/s", frac=None, traffic=None)
+    for name, d in kern.items():
+        b = algorithmic_bytes(name, args.n, n_vis, m, npix, k, sh_coeffs)
+        if b is not None:
+            d["algorithmic_GBs"] = b / d["launches_per_step"] / (d["ms_per_launch"] / 1e3) / 1e9
+
+    cpu = None
+    if args.cpu_baseline:
+        cpu = cpu_baseline(w, cam, prm, k)
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "blends/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"ABCD active-block step: {args.n} Gaussians (SH 3) at "
+                               f"{cam.width}x{cam.height}, F/B collapsed from {k} cached fp16 "
+                               "partition renders",
+                   "n_gaussians": args.n, "width": cam.width, "height": cam.height,
+                   "sh_degree": prm.sh_degree, "k_cached": k, "n_front": n_front,
+                   "n_isect": m, "n_visible": n_vis, "blends_per_step": blends_step,
+                   "sync_in_step": False},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kern,
+        "setup_s": setup_s,
+    }
+    print(json.dumps(out))
+
+
+def cpu_baseline(w, cam, prm, k):
+    """The oracle, as it stands, on a bounded sample of the same workload: the
+    full step (projection of all Gaussians of a 1/4 random subset, binning,
+    forward and backward over every pixel, and the F/B collapse of k cached
+    renders over a 1/16 band of image rows), on this host's cores."""
+    import numpy as np
+
+    from oracle import oracle as O
+    from paper_2608_27735_amd import synthetic as S
+
+    cores = len(os.sched_getaffinity(0))
+    os.environ.setdefault("OMP_NUM_THREADS", str(cores))
+    r = S.rng(4103)
+    n = w.scene["means"].shape[0]
+    sub = S.subset(w.scene, r.random(n) < 1.0 / 4)
+    F, B = S.background_pair(r, cam.height, cam.width)
+    G = S.upstream_grad(r, cam.height, cam.width)
+    t0 = time.perf_counter()
+    res = O.step(cam, prm, sub, F=F, B=B, dL_dout=G.astype(np.float64))
+    t_step = time.perf_counter() - t0
+    rows = max(1, cam.height // 16)
+    imgs = S.half_bits(S.premultiplied_images(r, k, rows, cam.width, coverage=0.35))
+    t1 = time.perf_counter()
+    O.composite(cam.width, rows, imgs, list(range(k)), k // 2)
+    t_comp = (time.perf_counter() - t1) * (cam.height / rows)  # scaled to the full frame
+    blends = res["fwd"]["n_blends"]
+    secs = t_step + t_comp
+    return dict(value=blends / secs, unit="blends/s", cores=cores, kind="oracle",
+                sample=f"1/4 random subset of the Gaussians ({len(sub['means'])}), full "
+                       f"{cam.width}x{cam.height} frame: project+bin+fwd+bwd; F/B collapse of "
+                       f"{k} layers timed on {rows} rows and scaled to the frame",
+                step_s=t_step, composite_s_scaled=t_comp, blends=blends)
+
+
+if __name__ == "__main__":
+    main()

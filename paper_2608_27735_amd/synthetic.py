@@ -254,3 +254,27 @@ def splats_2d(r, n, width, height, sigma_px=(1.0, 12.0), depth_range=(0.5, 20.0)
     co = np.stack([cov_c / det, -cov_b / det, cov_a / det, op], axis=1)
     return dict(means2d=np.stack([u, v], 1).astype(f), conic_opacity=co.astype(f),
                 depth=depth.astype(f), radius=rad.astype(f), rgb=rgb.astype(f))
+
+
+def cached_images_device(k, height, width, seed, device, coverage=0.35, alpha_max=0.9):
+    """k premultiplied fp16 RGBA cached renders [k, H, W, 4] drawn on the GPU
+    with a seeded torch generator (for workloads too large to draw on the
+    host): per layer a random axis-aligned rectangle covering about
+    `coverage` of the frame, alpha uniform on [0, alpha_max] inside, colour
+    uniform on [0, 1], zero outside."""
+    import torch
+
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    out = torch.zeros((k, height, width, 4), dtype=torch.float16, device=device)
+    side = math.sqrt(coverage)
+    hh, ww = max(1, int(height * side)), max(1, int(width * side))
+    corners = torch.rand((k, 2), generator=g, device=device)
+    for j in range(k):
+        h0 = int(corners[j, 0].item() * (height - hh + 1))
+        w0 = int(corners[j, 1].item() * (width - ww + 1))
+        a = torch.rand((hh, ww, 1), generator=g, device=device) * alpha_max
+        c = torch.rand((hh, ww, 3), generator=g, device=device)
+        out[j, h0:h0 + hh, w0:w0 + ww, :3] = (c * a).half()
+        out[j, h0:h0 + hh, w0:w0 + ww, 3:] = a.half()
+    return out
