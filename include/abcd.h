@@ -32,6 +32,8 @@
  *  - Parameter arrays are contiguous structure-of-arrays:
  *      means [n][3], log_scales [n][3], quats [n][4] (w, x, y, z; any norm),
  *      opacity_logits [n], sh [n][(sh_degree+1)^2][3].
+ *  - Alignment: quats, d_quats, conic_opacity and RGBA images 16 bytes,
+ *    means2d 8 bytes, workspaces 256 bytes (an unaligned call is rejected).
  *  - Functions are stateless and reentrant; concurrent calls on one stream
  *    must not share a workspace.
  */

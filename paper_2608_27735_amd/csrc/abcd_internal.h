@@ -73,8 +73,30 @@ __device__ __forceinline__ bool tile_rect(float u, float v, float r, int ntx, in
   return true;
 }
 
-// Alpha of a screen-space Gaussian at pixel offset (dx, dy) = centre - mean.
-// The forward and backward kernels both call this, so their skip / clamp
+// A screen-space Gaussian as the blend kernels stage it in LDS: the conic is
+// pre-scaled so that p2 = qa dx^2 + qb dx dy + qc dy^2 = power * log2(e), and
+// alpha = min(alpha_max, o 2^p2) is one v_exp_f32 away.
+constexpr float kLog2e = 1.4426950408889634f;
+
+struct Splat {
+  float u, v;       // mean
+  float qa, qb, qc; // -a log2(e) / 2, -b log2(e), -c log2(e) / 2
+  float o;          // opacity
+};
+
+__device__ __forceinline__ Splat make_splat(float2 m, float4 co) {
+  Splat s;
+  s.u = m.x;
+  s.v = m.y;
+  s.qa = -0.5f * kLog2e * co.x;
+  s.qb = -kLog2e * co.y;
+  s.qc = -0.5f * kLog2e * co.z;
+  s.o = co.w;
+  return s;
+}
+
+// Alpha of a splat at pixel offset (dx, dy) = centre - mean. The forward and
+// backward kernels both call this one function, so their skip and clamp
 // decisions are bit-identical.
 struct AlphaEval {
   float alpha;   // clamped alpha (valid when !skip)
@@ -83,25 +105,62 @@ struct AlphaEval {
   bool clamped;  // o * exp(power) > alpha_max
 };
 
-__device__ __forceinline__ AlphaEval eval_alpha(float dx, float dy, float a, float b, float c,
+__device__ __forceinline__ AlphaEval eval_alpha(float dx, float dy, float qa, float qb, float qc,
                                                 float o, float alpha_min, float alpha_max) {
   AlphaEval r;
-  const float power = -0.5f * (a * dx * dx + c * dy * dy) - b * dx * dy;
-  r.e = __expf(power);
+  const float p2 = dx * (qa * dx + qb * dy) + qc * (dy * dy);
+  r.e = __builtin_amdgcn_exp2f(p2);
   const float raw = o * r.e;
   r.clamped = raw > alpha_max;
   r.alpha = r.clamped ? alpha_max : raw;
-  r.skip = (power > 0.0f) || (r.alpha < alpha_min);
+  r.skip = (p2 > 0.0f) || (r.alpha < alpha_min);
   return r;
 }
 
-// Wave-wide helpers (wave64).
-__device__ __forceinline__ int lane_id() { return __lane_id(); }
-
-__device__ __forceinline__ float wave_sum(float v) {
+// Conservative tile test: can any pixel centre of the box [bx0, bx1] x [by0,
+// by1] see this Gaussian with alpha >= alpha_min? That needs
+// d^T Q d <= tau = 2 ln(o / alpha_min) for some centre; the minimum of the
+// convex quadratic over the box is 0 if the mean is inside, else it lies on
+// an edge, where the one-dimensional minimiser is clamped. The margin keeps
+// every entry whose per-pixel decision could go either way in fp32.
+__device__ __forceinline__ bool splat_touches_box(float u, float v, float a, float b, float c,
+                                                  float o, float alpha_min, float bx0, float bx1,
+                                                  float by0, float by1) {
+  if (!(o >= alpha_min)) return false;
+  const float dx0 = bx0 - u, dx1 = bx1 - u, dy0 = by0 - v, dy1 = by1 - v;
+  if (dx0 <= 0.0f && dx1 >= 0.0f && dy0 <= 0.0f && dy1 >= 0.0f) return true;
+  const float tau = 2.0f * (__logf(o) - __logf(alpha_min));
+  const float lim = tau * 1.001f + 1e-3f;
+  float best = 3.4e38f;
+  const float ia = a > 0.0f ? 1.0f / a : 0.0f, ic = c > 0.0f ? 1.0f / c : 0.0f;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
+  for (int k = 0; k < 2; ++k) {
+    const float dx = k ? dx1 : dx0;
+    const float dy = fminf(fmaxf(-b * dx * ic, dy0), dy1);
+    best = fminf(best, a * dx * dx + 2.0f * b * dx * dy + c * dy * dy);
+    const float ey = k ? dy1 : dy0;
+    const float ex = fminf(fmaxf(-b * ey * ia, dx0), dx1);
+    best = fminf(best, a * ex * ex + 2.0f * b * ex * ey + c * ey * ey);
+  }
+  return best <= lim;
+}
+
+// Wave64 sum with DPP row operations; the total is returned to every lane.
+__device__ __forceinline__ float wave_sum(float x) {
+  const int xi0 = __float_as_int(x);
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, xi0, 0xB1, 0xF, 0xF, false));  // quad [1,0,3,2]
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));  // [2,3,0,1]
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false));  // half mirror
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false));  // mirror
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x142, 0xA, 0xF, false));  // bcast15
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x143, 0xC, 0xF, false));  // bcast31
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
+__device__ __forceinline__ unsigned int wave_sum_u32(unsigned int x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  return x;
 }
 
 // ------------------------------------------------------ kernel launchers

@@ -138,8 +138,9 @@ int32_t abcd_project(const abcd_camera* cam, const abcd_raster_params* prm, int6
     REQUIRE(means2d && conic_opacity && depth && radius && tiles_touched && rgb,
             "output array is NULL");
     REQUIRE((reinterpret_cast<uintptr_t>(conic_opacity) & 15) == 0 &&
+                (reinterpret_cast<uintptr_t>(quats) & 15) == 0 &&
                 (reinterpret_cast<uintptr_t>(means2d) & 7) == 0,
-            "conic_opacity must be 16-byte and means2d 8-byte aligned");
+            "quats and conic_opacity must be 16-byte and means2d 8-byte aligned");
   }
   return launch_project(*cam, *prm, n, means, log_scales, quats, opacity_logits, sh, means2d,
                         conic_opacity, depth, radius, tiles_touched, rgb, stream);
@@ -246,8 +247,10 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
             "workspace must be non-NULL and 256-byte aligned");
     REQUIRE(ws_bytes >= need, "workspace of %zu bytes, %zu needed", ws_bytes, need);
     REQUIRE((reinterpret_cast<uintptr_t>(conic_opacity) & 15) == 0 &&
+                (reinterpret_cast<uintptr_t>(quats) & 15) == 0 &&
+                (reinterpret_cast<uintptr_t>(d_quats) & 15) == 0 &&
                 (reinterpret_cast<uintptr_t>(means2d) & 7) == 0,
-            "conic_opacity must be 16-byte and means2d 8-byte aligned");
+            "quats, d_quats and conic_opacity must be 16-byte and means2d 8-byte aligned");
   } else {
     return ABCD_OK;
   }

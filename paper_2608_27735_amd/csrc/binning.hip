@@ -48,7 +48,7 @@ inline int chunk_waves_for(int ntiles) {
 }
 
 struct WsLayout {
-  size_t hdr, keys_a, keys_b, vals_a, vals_b, hist, counts, tile_total, tile_off, total;
+  size_t hdr, keys_a, keys_b, vals_a, vals_b, hist, totals, counts, tile_total, tile_off, total;
   int64_t rs_blocks, chunks;
   int chunk_ranks, chunk_waves;
 };
@@ -71,6 +71,7 @@ WsLayout ws_layout(int64_t n, int ntiles) {
   L.vals_a = take(sizeof(uint32_t) * n);
   L.vals_b = take(sizeof(uint32_t) * n);
   L.hist = take(sizeof(uint32_t) * 256 * L.rs_blocks);
+  L.totals = take(sizeof(uint32_t) * 256);
   L.counts = take(sizeof(uint32_t) * (size_t)L.chunks * ntiles);
   L.tile_total = take(sizeof(uint32_t) * ntiles);
   L.tile_off = take(sizeof(uint32_t) * ntiles);
@@ -127,38 +128,50 @@ __global__ __launch_bounds__(256) void radix_hist_kernel(const uint32_t* __restr
   hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
 }
 
-// Exclusive scan of `count` u32 values in place, one workgroup.
-__global__ __launch_bounds__(kScanThreads) void scan_u32_kernel(uint32_t* __restrict__ data, int64_t count) {
-  __shared__ uint32_t part[kScanThreads];
-  const int64_t per = (count + kScanThreads - 1) / kScanThreads;
-  const int64_t lo = std::min<int64_t>(count, per * threadIdx.x);
-  const int64_t hi = std::min<int64_t>(count, lo + per);
-  uint32_t s = 0;
-  for (int64_t i = lo; i < hi; ++i) s += data[i];
-  part[threadIdx.x] = s;
-  __syncthreads();
-  for (int off = 1; off < kScanThreads; off <<= 1) {
-    const uint32_t v = threadIdx.x >= off ? part[threadIdx.x - off] : 0u;
+// Exclusive scan of each digit's row of block counts in place (one
+// workgroup per digit) and the digit totals.
+__global__ __launch_bounds__(256) void radix_scan_rows_kernel(uint32_t* __restrict__ hist,
+                                                              int64_t nblocks,
+                                                              uint32_t* __restrict__ totals) {
+  __shared__ uint32_t part[256];
+  uint32_t* row = hist + (int64_t)blockIdx.x * nblocks;
+  uint32_t carry = 0;
+  for (int64_t b0 = 0; b0 < nblocks; b0 += 256) {
+    const int64_t b = b0 + threadIdx.x;
+    const uint32_t v = b < nblocks ? row[b] : 0u;
+    part[threadIdx.x] = v;
     __syncthreads();
-    part[threadIdx.x] += v;
+    for (int off = 1; off < 256; off <<= 1) {
+      const uint32_t x = threadIdx.x >= off ? part[threadIdx.x - off] : 0u;
+      __syncthreads();
+      part[threadIdx.x] += x;
+      __syncthreads();
+    }
+    if (b < nblocks) row[b] = carry + part[threadIdx.x] - v;
+    carry += part[255];
     __syncthreads();
   }
-  uint32_t run = part[threadIdx.x] - s;
-  for (int64_t i = lo; i < hi; ++i) {
-    const uint32_t v = data[i];
-    data[i] = run;
-    run += v;
-  }
+  if (threadIdx.x == 0) totals[blockIdx.x] = carry;
 }
 
 __global__ __launch_bounds__(256) void radix_scatter_kernel(
     const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, int64_t n, int shift,
-    const uint32_t* __restrict__ hist, int64_t nblocks, uint32_t* __restrict__ keys_out,
-    uint32_t* __restrict__ vals_out) {
+    const uint32_t* __restrict__ hist, int64_t nblocks, const uint32_t* __restrict__ totals,
+    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out) {
   __shared__ uint32_t sbase[256];
   __shared__ uint32_t wcnt[4][256];
   const int tid = threadIdx.x, w = tid >> 6;
-  sbase[tid] = hist[(int64_t)tid * nblocks + blockIdx.x];
+  // digit base = exclusive scan of the digit totals
+  const uint32_t tot = totals[tid];
+  sbase[tid] = tot;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const uint32_t x = tid >= off ? sbase[tid - off] : 0u;
+    __syncthreads();
+    sbase[tid] += x;
+    __syncthreads();
+  }
+  sbase[tid] += hist[(int64_t)tid * nblocks + blockIdx.x] - tot;
 #pragma unroll
   for (int k = 0; k < 4; ++k) wcnt[k][tid] = 0;
   const int64_t base = (int64_t)blockIdx.x * kRsTile;
@@ -349,7 +362,7 @@ __global__ __launch_bounds__(256) void bin_scatter_kernel(
   }
   __syncthreads();
   // in rank order: lanes spread over the cells of one rectangle (distinct tiles)
-#pragma unroll 1
+#pragma unroll
   for (int j = 0; j < 4; ++j) {
 #pragma unroll 1
     for (int l = 0; l < 64; ++l) {
@@ -412,6 +425,7 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   uint32_t* keys[2] = {reinterpret_cast<uint32_t*>(ws + L.keys_a), reinterpret_cast<uint32_t*>(ws + L.keys_b)};
   uint32_t* vals[2] = {reinterpret_cast<uint32_t*>(ws + L.vals_a), reinterpret_cast<uint32_t*>(ws + L.vals_b)};
   uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
+  uint32_t* totals = reinterpret_cast<uint32_t*>(ws + L.totals);
   uint32_t* counts = reinterpret_cast<uint32_t*>(ws + L.counts);
   uint32_t* tile_total = reinterpret_cast<uint32_t*>(ws + L.tile_total);
   uint32_t* tile_off = reinterpret_cast<uint32_t*>(ws + L.tile_off);
@@ -423,9 +437,10 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
     const int src = pass & 1, dst = src ^ 1;
     ABCD_LAUNCH("radix_hist", radix_hist_kernel, L.rs_blocks, kBlock, 0, stream, keys[src], n,
                 8 * pass, hist, L.rs_blocks);
-    ABCD_LAUNCH("radix_scan", scan_u32_kernel, 1, kScanThreads, 0, stream, hist, 256 * L.rs_blocks);
+    ABCD_LAUNCH("radix_scan", radix_scan_rows_kernel, 256, kBlock, 0, stream, hist, L.rs_blocks,
+                totals);
     ABCD_LAUNCH("radix_scatter", radix_scatter_kernel, L.rs_blocks, kBlock, 0, stream, keys[src],
-                vals[src], n, 8 * pass, hist, L.rs_blocks, keys[dst], vals[dst]);
+                vals[src], n, 8 * pass, hist, L.rs_blocks, totals, keys[dst], vals[dst]);
   }
   const uint32_t* order = vals[0];  // four passes: back in buffer 0
 

@@ -34,8 +34,6 @@ constexpr float kY3c = 0.45704579946446572f;  // sqrt(21/(2 pi))/4
 constexpr float kY3d = 0.37317633259011540f;  // sqrt(7/pi)/4
 constexpr float kY3e = 1.4453057213202769f;   // sqrt(105/pi)/4
 
-__device__ __forceinline__ int sh_count(int degree) { return (degree + 1) * (degree + 1); }
-
 // Y[16] and, when G != nullptr, dY/d(x, y, z) as G[16][3].
 __device__ __forceinline__ void sh_eval(int degree, float x, float y, float z, float* Y, float* G) {
   Y[0] = kY0;
@@ -83,6 +81,32 @@ __device__ __forceinline__ void sh_eval(int degree, float x, float y, float z, f
     G[42] = 2.0f * kY3e * x * z; G[43] = -2.0f * kY3e * y * z; G[44] = kY3e * (xx - yy);
     G[45] = kY3a * 3.0f * (xx - yy); G[46] = -6.0f * kY3a * x * y; G[47] = 0;
   }
+}
+
+// sum_b w[b] dY_b/d(x, y, z): the SH gradient contracted with per-basis
+// weights, without materialising the 16 x 3 table.
+template <int D>
+__device__ __forceinline__ void sh_grad_dot(float x, float y, float z, const float* w, float* g) {
+  g[0] = g[1] = g[2] = 0.0f;
+  if (D < 1) return;
+  g[0] += kY1 * w[3];
+  g[1] += kY1 * w[1];
+  g[2] += kY1 * w[2];
+  if (D < 2) return;
+  const float xx = x * x, yy = y * y, zz = z * z;
+  g[0] += kY2a * (y * w[4] + z * w[7]) - 2.0f * kY2b * x * w[6] + 2.0f * kY2c * x * w[8];
+  g[1] += kY2a * (x * w[4] + z * w[5]) - 2.0f * kY2b * y * w[6] - 2.0f * kY2c * y * w[8];
+  g[2] += kY2a * (y * w[5] + x * w[7]) + 4.0f * kY2b * z * w[6];
+  if (D < 3) return;
+  g[0] += kY3a * 6.0f * x * y * w[9] + kY3b * y * z * w[10] - 2.0f * kY3c * x * y * w[11] -
+          6.0f * kY3d * x * z * w[12] + kY3c * (4.0f * zz - 3.0f * xx - yy) * w[13] +
+          2.0f * kY3e * x * z * w[14] + kY3a * 3.0f * (xx - yy) * w[15];
+  g[1] += kY3a * 3.0f * (xx - yy) * w[9] + kY3b * x * z * w[10] +
+          kY3c * (4.0f * zz - xx - 3.0f * yy) * w[11] - 6.0f * kY3d * y * z * w[12] -
+          2.0f * kY3c * x * y * w[13] - 2.0f * kY3e * y * z * w[14] - 6.0f * kY3a * x * y * w[15];
+  g[2] += kY3b * x * y * w[10] + 8.0f * kY3c * y * z * w[11] +
+          kY3d * (6.0f * zz - 3.0f * xx - 3.0f * yy) * w[12] + 8.0f * kY3c * x * z * w[13] +
+          kY3e * (xx - yy) * w[14];
 }
 
 // Intermediates of the fp32 projection chain of one Gaussian.
@@ -188,22 +212,52 @@ __device__ bool project_chain(const abcd_camera& c, const abcd_raster_params& p,
   return tile_rect(o.u, o.v, o.rad, ntx, nty, o.x0, o.y0, o.x1, o.y1);
 }
 
-__global__ __launch_bounds__(256) void project_kernel(
+// SH coefficients of a 64-Gaussian group are staged through LDS so that the
+// global loads and stores are coalesced (each Gaussian owns 3 (D+1)^2
+// consecutive floats; one thread per Gaussian would stride by 48 floats).
+constexpr int kProjThreads = 64;
+
+template <int D>
+struct ShTile {
+  static constexpr int kCoeffs = (D + 1) * (D + 1);
+  static constexpr int kFloats = 3 * kCoeffs;
+  static constexpr int kStride = kFloats + 1;  // odd stride: conflict-free LDS rows
+};
+
+template <int D>
+__device__ __forceinline__ void sh_stage_in(const float* __restrict__ sh, int64_t base, int cnt,
+                                            float* s) {
+  using Tl = ShTile<D>;
+  const float* src = sh + base * Tl::kFloats;
+  for (int e = threadIdx.x; e < cnt * Tl::kFloats; e += kProjThreads) {
+    const int g = e / Tl::kFloats;
+    s[g * Tl::kStride + (e - g * Tl::kFloats)] = src[e];
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kProjThreads) void project_kernel(
     abcd_camera cam, abcd_raster_params prm, int64_t n, int ntx, int nty, const float* __restrict__ means,
     const float* __restrict__ log_scales, const float* __restrict__ quats,
     const float* __restrict__ opacity_logits, const float* __restrict__ sh, float* __restrict__ means2d,
     float* __restrict__ conic_opacity, float* __restrict__ depth, float* __restrict__ radius,
     uint32_t* __restrict__ tiles_touched, float* __restrict__ rgb) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
+  using Tl = ShTile<D>;
+  __shared__ float s_sh[kProjThreads * Tl::kStride];
+  const int64_t base = (int64_t)blockIdx.x * kProjThreads;
+  const int cnt = (int)min<int64_t>(kProjThreads, n - base);
+  sh_stage_in<D>(sh, base, cnt, s_sh);
+  __syncthreads();
+  const int64_t i = base + threadIdx.x;
+  if (threadIdx.x >= cnt) return;
   const float mu[3] = {means[3 * i], means[3 * i + 1], means[3 * i + 2]};
   const float ls[3] = {log_scales[3 * i], log_scales[3 * i + 1], log_scales[3 * i + 2]};
-  const float q[4] = {quats[4 * i], quats[4 * i + 1], quats[4 * i + 2], quats[4 * i + 3]};
+  const float4 q4 = *reinterpret_cast<const float4*>(quats + 4 * i);
+  const float q[4] = {q4.x, q4.y, q4.z, q4.w};
   Proj pr;
   const bool vis = project_chain(cam, prm, ntx, nty, mu, ls, q, pr);
   if (!vis) {
-    means2d[2 * i] = 0.0f;
-    means2d[2 * i + 1] = 0.0f;
+    reinterpret_cast<float2*>(means2d)[i] = make_float2(0.0f, 0.0f);
     reinterpret_cast<float4*>(conic_opacity)[i] = make_float4(0, 0, 0, 0);
     depth[i] = 0.0f;
     radius[i] = 0.0f;
@@ -214,22 +268,20 @@ __global__ __launch_bounds__(256) void project_kernel(
   const float inv = 1.0f / pr.det;
   const float ca = pr.C * inv, cb = -pr.B * inv, cc = pr.A * inv;
   const float o = 1.0f / (1.0f + __expf(-opacity_logits[i]));
-  // colour from the view direction
   float dx = mu[0] - cam.campos[0], dy = mu[1] - cam.campos[1], dz = mu[2] - cam.campos[2];
   const float dn = rsqrtf(dx * dx + dy * dy + dz * dz);
   dx *= dn; dy *= dn; dz *= dn;
   float Y[16];
-  sh_eval(prm.sh_degree, dx, dy, dz, Y, nullptr);
-  const int nc = sh_count(prm.sh_degree);
-  const float* k = sh + (int64_t)3 * nc * i;
+  sh_eval(D, dx, dy, dz, Y, nullptr);
+  const float* k = s_sh + threadIdx.x * Tl::kStride;
   float col[3] = {0.5f, 0.5f, 0.5f};
-  for (int b = 0; b < nc; ++b) {
+#pragma unroll
+  for (int b = 0; b < Tl::kCoeffs; ++b) {
     col[0] += Y[b] * k[3 * b];
     col[1] += Y[b] * k[3 * b + 1];
     col[2] += Y[b] * k[3 * b + 2];
   }
-  means2d[2 * i] = pr.u;
-  means2d[2 * i + 1] = pr.v;
+  reinterpret_cast<float2*>(means2d)[i] = make_float2(pr.u, pr.v);
   reinterpret_cast<float4*>(conic_opacity)[i] = make_float4(ca, cb, cc, o);
   depth[i] = pr.tz;
   radius[i] = pr.rad;
@@ -242,7 +294,8 @@ __global__ __launch_bounds__(256) void project_kernel(
 // Chain rule from the screen-space gradients g2d[i][9] = dL/d(u, v, a, b, c,
 // o, r, g, b) to the parameters; exact derivative of the forward chain
 // (guard-band clamp and colour clamp have zero derivative where active).
-__global__ __launch_bounds__(256) void project_bwd_kernel(
+template <int D>
+__global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
     abcd_camera cam, abcd_raster_params prm, int64_t n, int ntx, int nty,
     const float* __restrict__ means, const float* __restrict__ log_scales,
     const float* __restrict__ quats, const float* __restrict__ opacity_logits,
@@ -250,19 +303,25 @@ __global__ __launch_bounds__(256) void project_bwd_kernel(
     float* __restrict__ d_means, float* __restrict__ d_log_scales, float* __restrict__ d_quats,
     float* __restrict__ d_opacity_logits, float* __restrict__ d_sh, float* __restrict__ d_means2d,
     int accumulate) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const int nc = sh_count(prm.sh_degree);
+  using Tl = ShTile<D>;
+  __shared__ float s_sh[kProjThreads * Tl::kStride];
+  const int64_t base = (int64_t)blockIdx.x * kProjThreads;
+  const int cnt = (int)min<int64_t>(kProjThreads, n - base);
+  sh_stage_in<D>(sh, base, cnt, s_sh);
+  __syncthreads();
+  const int64_t i = base + threadIdx.x;
+  const bool live = threadIdx.x < cnt;
+  float* kk = s_sh + threadIdx.x * Tl::kStride;  // SH in, then dL/dSH out
   float gm[3] = {0, 0, 0}, gl[3] = {0, 0, 0}, gq[4] = {0, 0, 0, 0}, gop = 0.0f;
-  float gsh[48];
-  for (int k = 0; k < 3 * nc; ++k) gsh[k] = 0.0f;
   float gu = 0.0f, gv = 0.0f;
-  const float mu[3] = {means[3 * i], means[3 * i + 1], means[3 * i + 2]};
   Proj pr;
-  bool vis = radius[i] > 0.0f;
+  bool vis = live && radius[i] > 0.0f;
+  float mu[3] = {0, 0, 0};
   if (vis) {
+    mu[0] = means[3 * i]; mu[1] = means[3 * i + 1]; mu[2] = means[3 * i + 2];
     const float ls[3] = {log_scales[3 * i], log_scales[3 * i + 1], log_scales[3 * i + 2]};
-    const float q[4] = {quats[4 * i], quats[4 * i + 1], quats[4 * i + 2], quats[4 * i + 3]};
+    const float4 q4 = *reinterpret_cast<const float4*>(quats + 4 * i);
+    const float q[4] = {q4.x, q4.y, q4.z, q4.w};
     vis = project_chain(cam, prm, ntx, nty, mu, ls, q, pr);
   }
   if (vis) {
@@ -270,6 +329,7 @@ __global__ __launch_bounds__(256) void project_bwd_kernel(
     gu = G[0];
     gv = G[1];
     const float ga = G[2], gb = G[3], gc = G[4], go = G[5];
+    const float gcol[3] = {G[6], G[7], G[8]};
     // conic Q = Sigma'^-1:  dL/dSigma' = -Q GQ Q, GQ = [[ga, gb/2], [gb/2, gc]]
     const float inv = 1.0f / pr.det;
     const float qa = pr.C * inv, qb = -pr.B * inv, qc = pr.A * inv;
@@ -284,16 +344,19 @@ __global__ __launch_bounds__(256) void project_bwd_kernel(
     const float* S = pr.S;
     const float Sm[9] = {S[0], S[1], S[2], S[1], S[3], S[4], S[2], S[4], S[5]};
     float GS[9];  // T^T G T
+#pragma unroll
     for (int a = 0; a < 3; ++a)
-      for (int b = 0; b < 3; ++b) {
-        const float t0a = T[a], t1a = T[3 + a], t0b = T[b], t1b = T[3 + b];
-        GS[3 * a + b] = t0a * (G00 * t0b + G01 * t1b) + t1a * (G01 * t0b + G11 * t1b);
-      }
+#pragma unroll
+      for (int b = 0; b < 3; ++b)
+        GS[3 * a + b] = T[a] * (G00 * T[b] + G01 * T[3 + b]) + T[3 + a] * (G01 * T[b] + G11 * T[3 + b]);
     float GT[6];  // 2 G T Sigma
+#pragma unroll
     for (int r = 0; r < 2; ++r) {
       const float g0 = r == 0 ? G00 : G01, g1 = r == 0 ? G01 : G11;
+#pragma unroll
       for (int b = 0; b < 3; ++b) {
         float acc = 0.0f;
+#pragma unroll
         for (int k = 0; k < 3; ++k) acc += (g0 * T[k] + g1 * T[3 + k]) * Sm[3 * k + b];
         GT[3 * r + b] = 2.0f * acc;
       }
@@ -305,7 +368,7 @@ __global__ __launch_bounds__(256) void project_bwd_kernel(
     const float gj11 = GT[3] * Rc[3] + GT[4] * Rc[4] + GT[5] * Rc[5];
     const float gj12 = GT[3] * Rc[6] + GT[4] * Rc[7] + GT[5] * Rc[8];
     // J(t), (u, v)(t)
-    const float fx = cam.fx, fy = cam.fy, tz = pr.tz, iz = 1.0f / tz, iz2 = iz * iz;
+    const float fx = cam.fx, fy = cam.fy, iz = 1.0f / pr.tz, iz2 = iz * iz;
     float gtx = 0.0f, gty = 0.0f, gtz = 0.0f;
     gtz += -fx * iz2 * gj00 - fy * iz2 * gj11 + fx * pr.xc * iz2 * gj02 + fy * pr.yc * iz2 * gj12;
     const float gxc = -fx * iz * gj02, gyc = -fy * iz * gj12;
@@ -321,17 +384,22 @@ __global__ __launch_bounds__(256) void project_bwd_kernel(
     gtz -= fx * pr.tx * iz2 * gu;
     gty += fy * iz * gv;
     gtz -= fy * pr.ty * iz2 * gv;
+#pragma unroll
     for (int k = 0; k < 3; ++k) gm[k] = Rc[k] * gtx + Rc[3 + k] * gty + Rc[6 + k] * gtz;
     // Sigma = M M^T, M = Rq diag(s)
     float GM[9];
+#pragma unroll
     for (int a = 0; a < 3; ++a)
+#pragma unroll
       for (int b = 0; b < 3; ++b)
         GM[3 * a + b] = 2.0f * (GS[3 * a] * pr.m[b] + GS[3 * a + 1] * pr.m[3 + b] +
                                 GS[3 * a + 2] * pr.m[6 + b]);
     const float s[3] = {pr.s0, pr.s1, pr.s2};
     float gR[9];
+#pragma unroll
     for (int b = 0; b < 3; ++b) {
       float gs = 0.0f;
+#pragma unroll
       for (int a = 0; a < 3; ++a) {
         gs += GM[3 * a + b] * pr.r[3 * a + b];
         gR[3 * a + b] = GM[3 * a + b] * s[b];
@@ -359,47 +427,63 @@ __global__ __launch_bounds__(256) void project_bwd_kernel(
     // opacity
     const float o = 1.0f / (1.0f + __expf(-opacity_logits[i]));
     gop = go * o * (1.0f - o);
-    // colour
-    float d[3] = {mu[0] - cam.campos[0], mu[1] - cam.campos[1], mu[2] - cam.campos[2]};
-    const float dn = sqrtf(d[0] * d[0] + d[1] * d[1] + d[2] * d[2]);
-    const float idn = 1.0f / dn;
+    // colour: dL/dSH overwrites the thread's SH row in LDS after use
+    const float d[3] = {mu[0] - cam.campos[0], mu[1] - cam.campos[1], mu[2] - cam.campos[2]};
+    const float idn = 1.0f / sqrtf(d[0] * d[0] + d[1] * d[1] + d[2] * d[2]);
     const float dir[3] = {d[0] * idn, d[1] * idn, d[2] * idn};
-    float Y[16], YG[48];
-    sh_eval(prm.sh_degree, dir[0], dir[1], dir[2], Y, YG);
-    const float* k = sh + (int64_t)3 * nc * i;
-    float gdir[3] = {0, 0, 0};
+    float Y[16];
+    sh_eval(D, dir[0], dir[1], dir[2], Y, nullptr);
+    float gc_[3];
+#pragma unroll
     for (int ch = 0; ch < 3; ++ch) {
       float raw = 0.5f;
-      for (int b = 0; b < nc; ++b) raw += Y[b] * k[3 * b + ch];
-      if (!(raw > 0.0f)) continue;
-      const float gcol = G[6 + ch];
-      for (int b = 0; b < nc; ++b) {
-        gsh[3 * b + ch] = Y[b] * gcol;
-        const float kc = gcol * k[3 * b + ch];
-        gdir[0] += kc * YG[3 * b];
-        gdir[1] += kc * YG[3 * b + 1];
-        gdir[2] += kc * YG[3 * b + 2];
-      }
+#pragma unroll
+      for (int b = 0; b < Tl::kCoeffs; ++b) raw += Y[b] * kk[3 * b + ch];
+      gc_[ch] = raw > 0.0f ? gcol[ch] : 0.0f;
     }
+    float wb[16];
+#pragma unroll
+    for (int b = 0; b < Tl::kCoeffs; ++b) {
+      wb[b] = gc_[0] * kk[3 * b] + gc_[1] * kk[3 * b + 1] + gc_[2] * kk[3 * b + 2];
+      kk[3 * b] = Y[b] * gc_[0];
+      kk[3 * b + 1] = Y[b] * gc_[1];
+      kk[3 * b + 2] = Y[b] * gc_[2];
+    }
+    float gdir[3];
+    sh_grad_dot<D>(dir[0], dir[1], dir[2], wb, gdir);
     const float dd = gdir[0] * dir[0] + gdir[1] * dir[1] + gdir[2] * dir[2];
+#pragma unroll
     for (int a = 0; a < 3; ++a) gm[a] += (gdir[a] - dir[a] * dd) * idn;
+  } else if (live) {
+#pragma unroll
+    for (int k = 0; k < Tl::kFloats; ++k) kk[k] = 0.0f;
   }
-  float* om = d_means + 3 * i;
-  float* ol = d_log_scales + 3 * i;
-  float* oq = d_quats + 4 * i;
-  float* os = d_sh + (int64_t)3 * nc * i;
-  if (accumulate) {
-    for (int a = 0; a < 3; ++a) { om[a] += gm[a]; ol[a] += gl[a]; }
-    for (int a = 0; a < 4; ++a) oq[a] += gq[a];
-    d_opacity_logits[i] += gop;
-    for (int a = 0; a < 3 * nc; ++a) os[a] += gsh[a];
-    if (d_means2d) { d_means2d[2 * i] += gu; d_means2d[2 * i + 1] += gv; }
-  } else {
-    for (int a = 0; a < 3; ++a) { om[a] = gm[a]; ol[a] = gl[a]; }
-    for (int a = 0; a < 4; ++a) oq[a] = gq[a];
-    d_opacity_logits[i] = gop;
-    for (int a = 0; a < 3 * nc; ++a) os[a] = gsh[a];
-    if (d_means2d) { d_means2d[2 * i] = gu; d_means2d[2 * i + 1] = gv; }
+  if (live) {
+    float* om = d_means + 3 * i;
+    float* ol = d_log_scales + 3 * i;
+    float4* oq = reinterpret_cast<float4*>(d_quats) + i;
+    if (accumulate) {
+#pragma unroll
+      for (int a = 0; a < 3; ++a) { om[a] += gm[a]; ol[a] += gl[a]; }
+      const float4 q0 = *oq;
+      *oq = make_float4(q0.x + gq[0], q0.y + gq[1], q0.z + gq[2], q0.w + gq[3]);
+      d_opacity_logits[i] += gop;
+      if (d_means2d) { d_means2d[2 * i] += gu; d_means2d[2 * i + 1] += gv; }
+    } else {
+#pragma unroll
+      for (int a = 0; a < 3; ++a) { om[a] = gm[a]; ol[a] = gl[a]; }
+      *oq = make_float4(gq[0], gq[1], gq[2], gq[3]);
+      d_opacity_logits[i] = gop;
+      if (d_means2d) { d_means2d[2 * i] = gu; d_means2d[2 * i + 1] = gv; }
+    }
+  }
+  __syncthreads();
+  // coalesced write-out of dL/dSH
+  float* dst = d_sh + base * Tl::kFloats;
+  for (int e = threadIdx.x; e < cnt * Tl::kFloats; e += kProjThreads) {
+    const int g = e / Tl::kFloats;
+    const float v = s_sh[g * Tl::kStride + (e - g * Tl::kFloats)];
+    dst[e] = accumulate ? dst[e] + v : v;
   }
 }
 
@@ -411,10 +495,19 @@ int32_t launch_project(const abcd_camera& cam, const abcd_raster_params& prm, in
                        float* conic_opacity, float* depth, float* radius, uint32_t* tiles_touched,
                        float* rgb, hipStream_t stream) {
   if (n == 0) return ABCD_OK;
-  const int64_t blocks = (n + kBlock - 1) / kBlock;
-  ABCD_LAUNCH("project", project_kernel, blocks, kBlock, 0, stream, cam, prm, n,
-              tiles_x(cam.width), tiles_y(cam.height), means, log_scales, quats, opacity_logits,
-              sh, means2d, conic_opacity, depth, radius, tiles_touched, rgb);
+  const int64_t blocks = (n + kProjThreads - 1) / kProjThreads;
+  const int ntx = tiles_x(cam.width), nty = tiles_y(cam.height);
+#define ABCD_PROJ(Dg)                                                                          \
+  ABCD_LAUNCH("project", project_kernel<Dg>, blocks, kProjThreads, 0, stream, cam, prm, n, ntx, \
+              nty, means, log_scales, quats, opacity_logits, sh, means2d, conic_opacity, depth,  \
+              radius, tiles_touched, rgb)
+  switch (prm.sh_degree) {
+    case 0: ABCD_PROJ(0); break;
+    case 1: ABCD_PROJ(1); break;
+    case 2: ABCD_PROJ(2); break;
+    default: ABCD_PROJ(3); break;
+  }
+#undef ABCD_PROJ
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }
@@ -426,11 +519,19 @@ int32_t launch_project_bwd(const abcd_camera& cam, const abcd_raster_params& prm
                            float* d_opacity_logits, float* d_sh, float* d_means2d,
                            int accumulate, hipStream_t stream) {
   if (n == 0) return ABCD_OK;
-  const int64_t blocks = (n + kBlock - 1) / kBlock;
-  ABCD_LAUNCH("project_bwd", project_bwd_kernel, blocks, kBlock, 0, stream, cam, prm, n,
-              tiles_x(cam.width), tiles_y(cam.height), means, log_scales, quats, opacity_logits,
-              sh, radius, g2d, d_means, d_log_scales, d_quats, d_opacity_logits, d_sh, d_means2d,
-              accumulate);
+  const int64_t blocks = (n + kProjThreads - 1) / kProjThreads;
+  const int ntx = tiles_x(cam.width), nty = tiles_y(cam.height);
+#define ABCD_PROJ_BWD(Dg)                                                                    \
+  ABCD_LAUNCH("project_bwd", project_bwd_kernel<Dg>, blocks, kProjThreads, 0, stream, cam, prm, \
+              n, ntx, nty, means, log_scales, quats, opacity_logits, sh, radius, g2d, d_means,  \
+              d_log_scales, d_quats, d_opacity_logits, d_sh, d_means2d, accumulate)
+  switch (prm.sh_degree) {
+    case 0: ABCD_PROJ_BWD(0); break;
+    case 1: ABCD_PROJ_BWD(1); break;
+    case 2: ABCD_PROJ_BWD(2); break;
+    default: ABCD_PROJ_BWD(3); break;
+  }
+#undef ABCD_PROJ_BWD
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }

@@ -26,15 +26,77 @@ __device__ __forceinline__ int tile_of_block(const BlendConsts& k) {
   return (b & 7) * k.per_xcd + (b >> 3);
 }
 
+// One list entry as loaded from global memory by one thread.
+struct Rec {
+  float2 m;
+  float4 co;
+  float r, g, b;
+  uint32_t gid;
+  bool valid;
+};
+
+__device__ __forceinline__ Rec load_rec(const uint32_t* __restrict__ values, uint32_t idx,
+                                        bool valid, const float2* __restrict__ means2d,
+                                        const float4* __restrict__ conic_opacity,
+                                        const float* __restrict__ rgb) {
+  Rec r;
+  r.valid = valid;
+  r.gid = 0;
+  if (valid) {
+    r.gid = values[idx];
+    r.m = means2d[r.gid];
+    r.co = conic_opacity[r.gid];
+    r.r = rgb[3 * r.gid];
+    r.g = rgb[3 * r.gid + 1];
+    r.b = rgb[3 * r.gid + 2];
+  }
+  return r;
+}
+
+// Pixel-centre box of a tile, clipped to the image.
+struct TileBox {
+  float x0, x1, y0, y1;
+};
+
+__device__ __forceinline__ TileBox tile_box(const BlendConsts& k, int tile) {
+  const int tx = tile % k.ntx, ty = tile / k.ntx;
+  TileBox b;
+  b.x0 = (float)(tx * kTile) + 0.5f;
+  b.y0 = (float)(ty * kTile) + 0.5f;
+  b.x1 = (float)(min(tx * kTile + kTile, k.width) - 1) + 0.5f;
+  b.y1 = (float)(min(ty * kTile + kTile, k.height) - 1) + 0.5f;
+  return b;
+}
+
+// Block-wide stream compaction of this thread's entry into slot `*pos`;
+// returns the number kept. s_wcnt holds 4 wave counts.
+__device__ __forceinline__ int compact(bool keep, int* s_wcnt, int& pos) {
+  const int w = threadIdx.x >> 6;
+  const uint64_t bal = __ballot(keep);
+  if ((threadIdx.x & 63) == 0) s_wcnt[w] = __popcll(bal);
+  __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int c = s_wcnt[k];
+    off += k < w ? c : 0;
+    tot += c;
+  }
+  pos = off + __popcll(bal & ((1ull << (threadIdx.x & 63)) - 1ull));
+  return tot;
+}
+
 __global__ __launch_bounds__(256) void render_fwd_kernel(
     BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
     const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
     float4* __restrict__ out, float* __restrict__ final_T, uint32_t* __restrict__ last,
     unsigned long long* __restrict__ n_blends) {
-  __shared__ float2 s_xy[256];
-  __shared__ float4 s_co[256];
-  __shared__ float4 s_rgb[256];
+  __shared__ float4 s_ga[256];  // u, v, qa, qb
+  __shared__ float4 s_gb[256];  // qc, o, r, g
+  __shared__ float s_bl[256];   // b
+  __shared__ int s_pos[256];    // position in the tile's list
+  __shared__ int s_wcnt[4];
   __shared__ unsigned long long s_nb;
   const int tile = tile_of_block(k);
   if (tile >= k.ntiles) return;
@@ -42,28 +104,37 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
   const int px = (tile % k.ntx) * kTile + (tid & 15);
   const int py = (tile / k.ntx) * kTile + (tid >> 4);
   const bool inside = px < k.width && py < k.height;
+  const TileBox box = tile_box(k, tile);
   const uint32_t start = tile_ranges[2 * tile], end = tile_ranges[2 * tile + 1];
   const float fx = (float)px + 0.5f, fy = (float)py + 0.5f;
   float T = 1.0f, cr = 0.0f, cg = 0.0f, cb = 0.0f;
   uint32_t lastk = 0, nb = 0;
   bool done = !inside;
   if (tid == 0) s_nb = 0;
+  Rec rec = load_rec(values, start + tid, start + tid < end, means2d, conic_opacity, rgb);
   for (uint32_t b0 = start; b0 < end; b0 += 256) {
     if (__syncthreads_count(done) == 256) break;
-    const uint32_t idx = b0 + tid;
-    if (idx < end) {
-      const uint32_t g = values[idx];
-      s_xy[tid] = means2d[g];
-      s_co[tid] = conic_opacity[g];
-      s_rgb[tid] = make_float4(rgb[3 * g], rgb[3 * g + 1], rgb[3 * g + 2], 0.0f);
+    const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, rec.co.x, rec.co.y, rec.co.z,
+                                                     rec.co.w, k.alpha_min, box.x0, box.x1,
+                                                     box.y0, box.y1);
+    int pos;
+    const int cnt = compact(keep, s_wcnt, pos);
+    if (keep) {
+      const Splat sp = make_splat(rec.m, rec.co);
+      s_ga[pos] = make_float4(sp.u, sp.v, sp.qa, sp.qb);
+      s_gb[pos] = make_float4(sp.qc, sp.o, rec.r, rec.g);
+      s_bl[pos] = rec.b;
+      s_pos[pos] = (int)(b0 - start) + tid;
     }
     __syncthreads();
-    const int cnt = (int)min(256u, end - b0);
+    // gathers of the next batch overlap the blend of this one
+    const uint32_t nxt = b0 + 256 + tid;
+    rec = load_rec(values, nxt, nxt < end, means2d, conic_opacity, rgb);
     if (!done) {
       for (int j = 0; j < cnt; ++j) {
-        const float2 m = s_xy[j];
-        const float4 co = s_co[j];
-        const AlphaEval ae = eval_alpha(fx - m.x, fy - m.y, co.x, co.y, co.z, co.w, k.alpha_min,
+        const float4 ga = s_ga[j];
+        const float4 gb = s_gb[j];
+        const AlphaEval ae = eval_alpha(fx - ga.x, fy - ga.y, ga.z, ga.w, gb.x, gb.y, k.alpha_min,
                                         k.alpha_max);
         if (ae.skip) continue;
         const float Tn = T * (1.0f - ae.alpha);
@@ -71,16 +142,16 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
           done = true;
           break;
         }
-        const float4 c = s_rgb[j];
         const float wgt = ae.alpha * T;
-        cr += c.x * wgt;
-        cg += c.y * wgt;
-        cb += c.z * wgt;
+        cr += gb.z * wgt;
+        cg += gb.w * wgt;
+        cb += s_bl[j] * wgt;
         T = Tn;
-        lastk = b0 - start + j + 1;
+        lastk = (uint32_t)s_pos[j] + 1;
         ++nb;
       }
     }
+    // s_wcnt is rewritten only after the next barrier
   }
   if (inside) {
     const int64_t p = (int64_t)py * k.width + px;
@@ -93,10 +164,7 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     last[p] = lastk;
   }
   if (n_blends) {
-    unsigned int x = nb;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
-    const unsigned long long wsum = x;
+    const unsigned long long wsum = wave_sum_u32(nb);
     __syncthreads();
     if ((tid & 63) == 0) atomicAdd(&s_nb, wsum);
     __syncthreads();
@@ -110,18 +178,21 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
     const float* __restrict__ final_T, const uint32_t* __restrict__ last,
     const float4* __restrict__ dL_dout, float* __restrict__ g2d) {
-  __shared__ float2 s_xy[256];
-  __shared__ float4 s_co[256];
-  __shared__ float4 s_rgb[256];
+  __shared__ float4 s_ga[256];  // u, v, qa, qb
+  __shared__ float4 s_gb[256];  // qc, o, r, g
+  __shared__ float4 s_gc[256];  // a, b, c (conic), colour b
+  __shared__ int s_pos[256];
   __shared__ uint32_t s_g[256];
   __shared__ float s_acc[9][256];
+  __shared__ int s_wcnt[4];
   __shared__ uint32_t s_max;
   const int tile = tile_of_block(k);
   if (tile >= k.ntiles) return;
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = threadIdx.x;
   const int px = (tile % k.ntx) * kTile + (tid & 15);
   const int py = (tile / k.ntx) * kTile + (tid >> 4);
   const bool inside = px < k.width && py < k.height;
+  const TileBox box = tile_box(k, tile);
   const uint32_t start = tile_ranges[2 * tile];
   const float fx = (float)px + 0.5f, fy = (float)py + 0.5f;
   float T = 1.0f, gcr = 0, gcg = 0, gcb = 0, gT = 0;
@@ -140,57 +211,71 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
     gcg = s * G.y;
     gcb = s * G.z;
     gT = s * (G.x * bb.x + G.y * bb.y + G.z * bb.z - G.w * (1.0f - bb.w));
-    atomicMax(&s_max, lastp);
+    if (lastp) atomicMax(&s_max, lastp);
   }
   const float Tfin = T;
   float Rr = 0.0f, Rg = 0.0f, Rb = 0.0f;
   __syncthreads();
   const uint32_t nent = s_max;
-  for (uint32_t bend = start + nent; bend > start;) {
+  // entry j of a batch is list position bend - 1 - j (back to front)
+  uint32_t bend = start + nent;
+  Rec rec = load_rec(values, bend - 1 - tid, tid < (int)nent, means2d, conic_opacity, rgb);
+  while (bend > start) {
     const uint32_t bbeg = bend - min(256u, bend - start);
-    const int cnt = (int)(bend - bbeg);
     __syncthreads();
-    if (tid < cnt) {
-      const uint32_t g = values[bend - 1 - tid];
-      s_g[tid] = g;
-      s_xy[tid] = means2d[g];
-      s_co[tid] = conic_opacity[g];
-      s_rgb[tid] = make_float4(rgb[3 * g], rgb[3 * g + 1], rgb[3 * g + 2], 0.0f);
+    const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, rec.co.x, rec.co.y, rec.co.z,
+                                                     rec.co.w, k.alpha_min, box.x0, box.x1,
+                                                     box.y0, box.y1);
+    int pos;
+    const int cnt = compact(keep, s_wcnt, pos);
+    if (keep) {
+      const Splat sp = make_splat(rec.m, rec.co);
+      s_ga[pos] = make_float4(sp.u, sp.v, sp.qa, sp.qb);
+      s_gb[pos] = make_float4(sp.qc, sp.o, rec.r, rec.g);
+      s_gc[pos] = make_float4(rec.co.x, rec.co.y, rec.co.z, rec.b);
+      s_pos[pos] = (int)(bend - 1 - tid - start);
+      s_g[pos] = rec.gid;
 #pragma unroll
-      for (int q = 0; q < 9; ++q) s_acc[q][tid] = 0.0f;
+      for (int q = 0; q < 9; ++q) s_acc[q][pos] = 0.0f;
     }
     __syncthreads();
+    {
+      const uint32_t nxt_end = bbeg;
+      const bool v = (uint32_t)tid < nxt_end - start;
+      rec = load_rec(values, nxt_end - 1 - tid, v, means2d, conic_opacity, rgb);
+    }
     for (int j = 0; j < cnt; ++j) {
-      const uint32_t kk = bend - 1 - j - start;  // position in the tile's list
+      const uint32_t kk = (uint32_t)s_pos[j];
       float gr[9];
       bool contrib = false;
       if (kk < lastp) {
-        const float2 m = s_xy[j];
-        const float4 co = s_co[j];
-        const float dx = fx - m.x, dy = fy - m.y;
-        const AlphaEval ae = eval_alpha(dx, dy, co.x, co.y, co.z, co.w, k.alpha_min, k.alpha_max);
+        const float4 ga = s_ga[j];
+        const float4 gb = s_gb[j];
+        const float dx = fx - ga.x, dy = fy - ga.y;
+        const AlphaEval ae = eval_alpha(dx, dy, ga.z, ga.w, gb.x, gb.y, k.alpha_min, k.alpha_max);
         if (!ae.skip) {
           contrib = true;
-          const float4 c = s_rgb[j];
+          const float4 gc = s_gc[j];
           const float om = 1.0f - ae.alpha;
-          const float Tk = T / om;
+          const float iom = 1.0f / om;
+          const float Tk = T * iom;
           const float wgt = ae.alpha * Tk;
           gr[6] = wgt * gcr;
           gr[7] = wgt * gcg;
           gr[8] = wgt * gcb;
-          const float dLda = Tk * ((c.x - Rr) * gcr + (c.y - Rg) * gcg + (c.z - Rb) * gcb) -
-                             (Tfin / om) * gT;
-          Rr = ae.alpha * c.x + om * Rr;
-          Rg = ae.alpha * c.y + om * Rg;
-          Rb = ae.alpha * c.z + om * Rb;
+          const float dLda = Tk * ((gb.z - Rr) * gcr + (gb.w - Rg) * gcg + (gc.w - Rb) * gcb) -
+                             (Tfin * iom) * gT;
+          Rr = ae.alpha * gb.z + om * Rr;
+          Rg = ae.alpha * gb.w + om * Rg;
+          Rb = ae.alpha * gc.w + om * Rb;
           T = Tk;
           if (ae.clamped) {
             gr[0] = gr[1] = gr[2] = gr[3] = gr[4] = gr[5] = 0.0f;
           } else {
             const float gp = ae.alpha * dLda;
             gr[5] = ae.e * dLda;
-            gr[0] = gp * (co.x * dx + co.y * dy);
-            gr[1] = gp * (co.y * dx + co.z * dy);
+            gr[0] = gp * (gc.x * dx + gc.y * dy);
+            gr[1] = gp * (gc.y * dx + gc.z * dy);
             gr[2] = -0.5f * gp * dx * dx;
             gr[3] = -gp * dx * dy;
             gr[4] = -0.5f * gp * dy * dy;
@@ -205,7 +290,7 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
 #pragma unroll
         for (int q = 0; q < 9; ++q) {
           const float v = wave_sum(gr[q]);
-          if (lane == 0) atomicAdd(&s_acc[q][j], v);
+          if ((tid & 63) == 0) atomicAdd(&s_acc[q][j], v);
         }
       }
     }
