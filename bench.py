@@ -30,8 +30,9 @@ HBM_PEAK_GBS = 8000.0
 VALU_PEAK_TOPS = 39.3
 
 KERNELS = ["composite", "project", "depth_keys", "radix_hist", "radix_scan", "radix_scatter",
-           "bin_count", "bin_scan_columns", "bin_scan_tiles", "bin_scatter", "render_fwd",
-           "loss_l1", "zero_fill", "render_bwd", "project_bwd"]
+           "l1_count", "l1_scan_columns", "l1_finish", "l1_scatter", "l2_count", "l2_scan",
+           "bin_scan_tiles", "l2_scatter", "render_fwd", "loss_l1", "zero_fill", "render_bwd",
+           "project_bwd"]
 
 
 def parse():
@@ -44,6 +45,9 @@ def parse():
     ap.add_argument("--height", type=int, default=840)
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the CPU oracle on a sample")
     ap.add_argument("--profile-kernels", type=int, default=1)
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="after the steps, copy this many MiB device to device (a plain copy of "
+                         "known size that scales the HBM byte counters)")
     return ap.parse_args()
 
 
@@ -57,8 +61,8 @@ def algorithmic_bytes(name, n, n_vis, m, npix, k, sh_coeffs):
         return n * (param + proj)
     if name == "project_bwd":
         return n * (2 * param + 9 * 4 + 4)             # params in, grads out, g2d and radius in
-    if name == "bin_scatter":
-        return m * 4 + n_vis * 16
+    if name == "l2_scatter":
+        return m * 4                                   # the sorted Gaussian indices
     return None
 
 
@@ -148,6 +152,16 @@ def main():
         b = algorithmic_bytes(name, args.n, n_vis, m, npix, k, sh_coeffs)
         if b is not None:
             d["algorithmic_GBs"] = b / d["launches_per_step"] / (d["ms_per_launch"] / 1e3) / 1e9
+
+    if args.copy_calibration_mb:
+        nbytes = args.copy_calibration_mb << 20
+        src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cpu = None
     if args.cpu_baseline:

@@ -126,8 +126,13 @@ ABCD_API int32_t abcd_project(const abcd_camera* cam /* host */, const abcd_rast
  * stores M there and returns ABCD_E_CAPACITY when M > capacity. If NULL, the
  * call does not synchronise; M (uint64) is left at the start of the workspace
  * and a capacity overflow leaves the outputs unwritten.
- * workspace: at least abcd_bin_sort_workspace_size() bytes, 256-byte aligned. */
-ABCD_API int32_t abcd_bin_sort_workspace_size(int64_t n, int32_t width, int32_t height, size_t* bytes);
+ * capacity must be below 2^32.
+ * workspace: at least abcd_bin_sort_workspace_size(n, capacity, width, height)
+ * bytes, 256-byte aligned; it grows with the capacity (8 bytes per element for
+ * an intermediate list of (Gaussian, 8x8-tile block) pairs, which never holds
+ * more than M elements). */
+ABCD_API int32_t abcd_bin_sort_workspace_size(int64_t n, int64_t capacity, int32_t width,
+                                              int32_t height, size_t* bytes);
 ABCD_API int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const float* means2d,
                       const float* radius, const float* depth, const uint32_t* tiles_touched,
                       int64_t capacity, void* workspace, size_t ws_bytes, uint64_t* keys_sorted,

@@ -33,7 +33,7 @@ _CAM, _PRM = C.POINTER(abcd_camera), C.POINTER(abcd_raster_params)
 # name -> (restype, argtypes); mirrors include/abcd.h
 SIGNATURES = {
     "abcd_project": (_I32, [_CAM, _PRM, _I64] + [_P] * 5 + [_P] * 6 + [_P]),
-    "abcd_bin_sort_workspace_size": (_I32, [_I64, _I32, _I32, C.POINTER(_SZ)]),
+    "abcd_bin_sort_workspace_size": (_I32, [_I64, _I64, _I32, _I32, C.POINTER(_SZ)]),
     "abcd_bin_sort": (_I32, [_I32, _I32, _I64, _P, _P, _P, _P, _I64, _P, _SZ, _P, _P, _P,
                              C.POINTER(_I64), _P]),
     "abcd_render_fwd": (_I32, [_CAM, _PRM] + [_P] * 11 + [_P]),

@@ -81,9 +81,9 @@ def project(cam, prm, means, log_scales, quats, opacity_logits, sh, out=None):
 
 # ------------------------------------------------------------------ binning
 
-def bin_sort_workspace_size(n, width, height):
+def bin_sort_workspace_size(n, width, height, capacity=0):
     sz = C.c_size_t(0)
-    check(_lib.load().abcd_bin_sort_workspace_size(n, width, height, C.byref(sz)))
+    check(_lib.load().abcd_bin_sort_workspace_size(n, capacity, width, height, C.byref(sz)))
     return sz.value
 
 
@@ -103,13 +103,13 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
     _need(radius, "radius", torch.float32, (n,))
     _need(depth, "depth", torch.float32, (n,))
     _need(tiles, "tiles_touched", torch.int32, (n,))
-    ws_bytes = bin_sort_workspace_size(n, width, height)
-    if workspace is None or workspace.numel() < ws_bytes:
-        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
     if tile_ranges is None:
         tile_ranges = _empty((n_tiles(width, height), 2), torch.int32, dev)
     if capacity is None:
         capacity = 0 if values is None else values.numel()
+    ws_bytes = bin_sort_workspace_size(n, width, height, capacity)
+    if workspace is None or workspace.numel() < ws_bytes:
+        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
     if values is None and capacity > 0:
         values = _empty((capacity,), torch.int32, dev)
     if want_keys and (keys is None or keys.numel() < capacity):
@@ -125,6 +125,9 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
         values = _empty((max(capacity, 1),), torch.int32, dev)
         if want_keys:
             keys = _empty((max(capacity, 1),), torch.int64, dev)
+        ws_bytes = bin_sort_workspace_size(n, width, height, capacity)
+        if workspace.numel() < ws_bytes:
+            workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
         st = lib.abcd_bin_sort(width, height, n, _ptr(means2d), _ptr(radius), _ptr(depth),
                                _ptr(tiles), capacity, _ptr(workspace), workspace.numel(),
                                _ptr(keys) if want_keys else None, _ptr(values), _ptr(tile_ranges),

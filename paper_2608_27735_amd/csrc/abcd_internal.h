@@ -179,7 +179,7 @@ int32_t launch_project_bwd(const abcd_camera& cam, const abcd_raster_params& prm
                            int accumulate, hipStream_t stream);
 
 // binning.hip
-size_t bin_sort_workspace_bytes(int64_t n, int ntiles);
+size_t bin_sort_workspace_bytes(int64_t n, int64_t capacity, int width, int height);
 int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, const float* radius,
                         const float* depth, const uint32_t* tiles_touched, int64_t capacity,
                         void* workspace, uint64_t* keys_sorted, uint32_t* values_sorted,

@@ -146,13 +146,15 @@ int32_t abcd_project(const abcd_camera* cam, const abcd_raster_params* prm, int6
                         conic_opacity, depth, radius, tiles_touched, rgb, stream);
 }
 
-int32_t abcd_bin_sort_workspace_size(int64_t n, int32_t width, int32_t height, size_t* bytes) {
+int32_t abcd_bin_sort_workspace_size(int64_t n, int64_t capacity, int32_t width, int32_t height,
+                                     size_t* bytes) {
   TRY(check_n(n));
   REQUIRE(bytes != nullptr, "bytes is NULL");
+  REQUIRE(capacity >= 0 && capacity < (1ll << 32), "capacity must be in [0, 2^32)");
   REQUIRE(width > 0 && height > 0, "image size must be positive");
   const int64_t tiles = (int64_t)tiles_x(width) * tiles_y(height);
   REQUIRE(tiles <= ABCD_MAX_TILES, "too many tiles");
-  *bytes = bin_sort_workspace_bytes(n, (int)tiles);
+  *bytes = bin_sort_workspace_bytes(n, capacity, width, height);
   return ABCD_OK;
 }
 
@@ -165,11 +167,11 @@ int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const float* mea
   REQUIRE(width > 0 && height > 0, "image size must be positive");
   const int64_t tiles = (int64_t)tiles_x(width) * tiles_y(height);
   REQUIRE(tiles <= ABCD_MAX_TILES, "too many tiles");
-  REQUIRE(capacity >= 0, "capacity must be >= 0");
+  REQUIRE(capacity >= 0 && capacity < (1ll << 32), "capacity must be in [0, 2^32)");
   REQUIRE(tile_ranges != nullptr, "tile_ranges is NULL");
   REQUIRE(workspace != nullptr, "workspace is NULL");
   REQUIRE((reinterpret_cast<uintptr_t>(workspace) & 255) == 0, "workspace must be 256-byte aligned");
-  const size_t need = bin_sort_workspace_bytes(n, (int)tiles);
+  const size_t need = bin_sort_workspace_bytes(n, capacity, width, height);
   REQUIRE(ws_bytes >= need, "workspace of %zu bytes, %zu needed", ws_bytes, need);
   if (n > 0) {
     REQUIRE(means2d && radius && depth && tiles_touched, "input array is NULL");

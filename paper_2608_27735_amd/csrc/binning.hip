@@ -3,25 +3,32 @@
 // The 3DGS renderer the paper builds on (Introduction) blends, per 16x16 tile,
 // the Gaussians whose support rectangle covers the tile, front to back. The
 // required order is key = tile << 32 | fp32 depth bits, ties by Gaussian
-// index. Instead of sorting M (tile, depth) keys (M ~ 10^8 at the 1M-Gaussian
-// block), this file sorts the n Gaussians once by depth (stable LSD radix
-// sort, 8-bit digits) and then performs ONE stable counting sort by tile,
-// generated directly from the support rectangles in depth order:
+// index. Instead of sorting the M (tile, depth) keys (M ~ 10^8 at a 1M-Gaussian
+// block), the n Gaussians are sorted once by depth (stable LSD radix sort,
+// 8-bit digits) and the lists are then GENERATED in depth order by two stable
+// counting sorts driven by the support rectangles:
 //
-//   1. depth_keys       key = depth bits (culled -> 0xffffffff), value = index
-//   2. radix passes     hist / scan / scatter, 4 x 8 bits, stable
-//   3. bin_count        per chunk of consecutive depth ranks, per tile count
-//                       (LDS histogram of every rectangle cell)
-//   4. bin_scan_columns exclusive prefix of the chunk counts down each tile
-//   5. bin_scan_tiles   exclusive prefix over tiles -> tile_ranges, M
-//   6. bin_scatter      each wave walks its ranks IN ORDER, its lanes covering
-//                       the cells of one rectangle (distinct tiles), so the
-//                       position of every pair is its stable rank: the result
-//                       is the unique sorted list, with no key array.
+//   level 1  Gaussians -> buckets of 8x8-tile blocks (a few per Gaussian)
+//   level 2  each block's bucket -> its 64 tile lists
 //
-// HBM traffic is O(n) for the sort and ~4 bytes per intersection for the
-// scatter (8 more if the keys are requested), against ~150 bytes per
-// intersection for a six-pass LSD sort of 64-bit keys.
+// Both levels use the same ordered scatter: a wave walks its entries in depth
+// order and its lanes cover the distinct cells (blocks, tiles) of one
+// rectangle, so every write position is the pair's stable rank. Level 2 is
+// split into sub-chunks of a bucket, each of which writes only 64 output
+// streams, so consecutive writes of a stream meet in L2 and leave it as whole
+// lines (a one-level scatter over all tiles of the frame writes every 4-byte
+// entry into a different line and pays several times the payload in HBM
+// writes).
+//
+//   depth_keys, radix x4   depth order of the n Gaussians
+//   l1_count               per chunk of 1024 ranks: block counts; total M
+//   l1_scan_columns        exclusive prefix of the chunk counts per block
+//   l1_finish              bucket offsets, sub-chunk table, overflow flag
+//   l1_scatter             (block, Gaussian) pairs, bucket-major, depth order
+//   l2_count               per sub-chunk: counts of its block's 64 tiles
+//   l2_scan                exclusive prefix of the sub-chunk counts per tile
+//   bin_scan_tiles         tile_ranges
+//   l2_scatter             values (and keys), tile-major, depth order
 #include <algorithm>
 
 #include "abcd_internal.h"
@@ -33,32 +40,49 @@ constexpr int kRsItems = 16;
 constexpr int kRsTile = kBlock * kRsItems;  // keys per radix block
 constexpr int kScanThreads = 1024;
 constexpr int kRanksPerWave = 256;
+constexpr int kChunk = 4 * kRanksPerWave;   // level 1: depth ranks per workgroup
+constexpr int kSub = 256;                   // level 2: bucket entries per sub-chunk
+constexpr int kBlk = 8;                     // block side in tiles
+constexpr int kBlkTiles = kBlk * kBlk;
+constexpr int kStrideGrid = 2048;           // workgroups of the grid-stride level-2 kernels
 
 struct WsHeader {
-  unsigned long long m;  // number of intersections
-  uint32_t overflow;     // m exceeded the capacity
-  uint32_t pad[61];
+  unsigned long long m;   // intersections (sum of tiles_touched)
+  unsigned long long m1;  // (Gaussian, block) pairs
+  uint32_t overflow;      // m > capacity or m >= 2^32: nothing is written
+  uint32_t total_sub;     // level-2 sub-chunks
+  uint32_t pad[58];
 };
 static_assert(sizeof(WsHeader) == 256, "header is one 256-byte slot");
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-inline int chunk_waves_for(int ntiles) {
-  return std::min(4, std::max(1, 32768 / std::max(ntiles, 1)));
+struct Geo {
+  int ntx, nty, nbx, nby, nblk;
+};
+
+inline Geo geo_of(int width, int height) {
+  Geo g;
+  g.ntx = tiles_x(width);
+  g.nty = tiles_y(height);
+  g.nbx = (g.ntx + kBlk - 1) / kBlk;
+  g.nby = (g.nty + kBlk - 1) / kBlk;
+  g.nblk = g.nbx * g.nby;
+  return g;
 }
 
 struct WsLayout {
-  size_t hdr, keys_a, keys_b, vals_a, vals_b, hist, totals, counts, tile_total, tile_off, total;
-  int64_t rs_blocks, chunks;
-  int chunk_ranks, chunk_waves;
+  size_t hdr, keys_a, keys_b, vals_a, vals_b, rects, hist, totals, c1, blk_total, blk_off, sub_off,
+      pairs, c2, tile_total, tile_off, total;
+  int64_t rs_blocks, chunks, max_sub;
 };
 
-WsLayout ws_layout(int64_t n, int ntiles) {
+WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
   WsLayout L;
+  const int64_t ntiles = (int64_t)g.ntx * g.nty;
   L.rs_blocks = (n + kRsTile - 1) / kRsTile;
-  L.chunk_waves = chunk_waves_for(ntiles);
-  L.chunk_ranks = kRanksPerWave * L.chunk_waves;
-  L.chunks = (n + L.chunk_ranks - 1) / L.chunk_ranks;
+  L.chunks = (n + kChunk - 1) / kChunk;
+  L.max_sub = (capacity + kSub - 1) / kSub + g.nblk;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t at = off;
@@ -70,9 +94,15 @@ WsLayout ws_layout(int64_t n, int ntiles) {
   L.keys_b = take(sizeof(uint32_t) * n);
   L.vals_a = take(sizeof(uint32_t) * n);
   L.vals_b = take(sizeof(uint32_t) * n);
+  L.rects = take(sizeof(unsigned long long) * n);
   L.hist = take(sizeof(uint32_t) * 256 * L.rs_blocks);
   L.totals = take(sizeof(uint32_t) * 256);
-  L.counts = take(sizeof(uint32_t) * (size_t)L.chunks * ntiles);
+  L.c1 = take(sizeof(uint32_t) * (size_t)L.chunks * g.nblk);
+  L.blk_total = take(sizeof(uint32_t) * g.nblk);
+  L.blk_off = take(sizeof(uint32_t) * (g.nblk + 1));
+  L.sub_off = take(sizeof(uint32_t) * (g.nblk + 1));
+  L.pairs = take(sizeof(unsigned long long) * (size_t)capacity);  // m1 <= m <= capacity
+  L.c2 = take(sizeof(uint32_t) * (size_t)L.max_sub * kBlkTiles);
   L.tile_total = take(sizeof(uint32_t) * ntiles);
   L.tile_off = take(sizeof(uint32_t) * ntiles);
   L.total = off;
@@ -98,14 +128,34 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 
 // ---------------------------------------------------------- depth sort
 
-__global__ __launch_bounds__(256) void depth_keys_kernel(int64_t n, const float* __restrict__ depth,
-                                                         const uint32_t* __restrict__ tiles,
-                                                         uint32_t* __restrict__ keys,
-                                                         uint32_t* __restrict__ vals) {
+// Tile rectangle packed as x0 | x1 << 16 | y0 << 32 | y1 << 48 (empty: x0 = 1 > x1 = 0).
+__device__ __forceinline__ unsigned long long pack_rect(int x0, int y0, int x1, int y1) {
+  return (unsigned long long)x0 | ((unsigned long long)x1 << 16) | ((unsigned long long)y0 << 32) |
+         ((unsigned long long)y1 << 48);
+}
+
+__global__ __launch_bounds__(256) void depth_keys_kernel(
+    int64_t n, const float* __restrict__ depth, const uint32_t* __restrict__ tiles,
+    const float* __restrict__ means2d, const float* __restrict__ radius, int ntx, int nty,
+    uint32_t* __restrict__ keys, uint32_t* __restrict__ vals, unsigned long long* __restrict__ rects,
+    WsHeader* __restrict__ hdr) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) {
+    hdr->m = 0;
+    hdr->m1 = 0;
+    hdr->overflow = 0;
+    hdr->total_sub = 0;
+  }
   if (i >= n) return;
-  keys[i] = tiles[i] ? __float_as_uint(depth[i]) : 0xffffffffu;
+  const bool vis = tiles[i] != 0;
+  keys[i] = vis ? __float_as_uint(depth[i]) : 0xffffffffu;
   vals[i] = (uint32_t)i;
+  int x0 = 1, y0 = 0, x1 = 0, y1 = 0;
+  if (vis) {
+    const float2 m = reinterpret_cast<const float2*>(means2d)[i];
+    if (!tile_rect(m.x, m.y, radius[i], ntx, nty, x0, y0, x1, y1)) x0 = 1, y0 = 0, x1 = 0, y1 = 0;
+  }
+  rects[i] = pack_rect(x0, y0, x1, y1);
 }
 
 __global__ __launch_bounds__(256) void radix_hist_kernel(const uint32_t* __restrict__ keys, int64_t n,
@@ -209,24 +259,38 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(
   }
 }
 
-// ------------------------------------------------- tile counting sort
+// ------------------------------------------------------------ rectangles
 
 struct Rect {
-  int x0, y0, x1, y1;
-  bool ok;
+  int x0, y0, x1, y1;  // inclusive tile rectangle; empty if x1 < x0
 };
 
-__device__ __forceinline__ Rect rect_of(uint32_t g, const float* __restrict__ means2d,
-                                        const float* __restrict__ radius,
-                                        const uint32_t* __restrict__ tiles, int ntx, int nty) {
+__device__ __forceinline__ Rect rect_of(uint32_t g, const unsigned long long* __restrict__ rects) {
+  const unsigned long long p = rects[g];
+  return Rect{(int)(p & 0xffff), (int)((p >> 32) & 0xffff), (int)((p >> 16) & 0xffff),
+              (int)(p >> 48)};
+}
+
+__device__ __forceinline__ Rect block_rect(const Rect& t) {
+  if (t.x1 < t.x0) return t;
+  return Rect{t.x0 / kBlk, t.y0 / kBlk, t.x1 / kBlk, t.y1 / kBlk};
+}
+
+// the part of a tile rectangle inside block b, in local tile coordinates
+__device__ __forceinline__ Rect clip_to_block(const Rect& t, int bx, int by) {
   Rect r;
-  r.ok = tiles[g] != 0;
-  if (r.ok) {
-    const float2 m = reinterpret_cast<const float2*>(means2d)[g];
-    r.ok = tile_rect(m.x, m.y, radius[g], ntx, nty, r.x0, r.y0, r.x1, r.y1);
-  }
-  if (!r.ok) r.x0 = r.y0 = 0, r.x1 = r.y1 = -1;
+  r.x0 = max(t.x0, bx * kBlk) - bx * kBlk;
+  r.x1 = min(t.x1, bx * kBlk + kBlk - 1) - bx * kBlk;
+  r.y0 = max(t.y0, by * kBlk) - by * kBlk;
+  r.y1 = min(t.y1, by * kBlk + kBlk - 1) - by * kBlk;
+  if (r.x0 > r.x1 || r.y0 > r.y1) r = Rect{0, 0, -1, -1};
   return r;
+}
+
+// local rectangle packed as x0 | y0 << 3 | x1 << 6 | y1 << 9 | 1 << 12 (0 = none)
+__device__ __forceinline__ int pack_local(const Rect& r) {
+  if (r.x1 < r.x0) return 0;
+  return r.x0 | (r.y0 << 3) | (r.x1 << 6) | (r.y1 << 9) | (1 << 12);
 }
 
 // cell -> (cx, cy) of a rectangle of width wr, row major; exact for cell < 2^22
@@ -238,60 +302,276 @@ __device__ __forceinline__ void cell_xy(int cell, int wr, float inv_wr, int& cx,
   cx = cell - q * wr;
 }
 
-__global__ __launch_bounds__(256) void bin_count_kernel(
-    int64_t n, const uint32_t* __restrict__ order, const float* __restrict__ means2d,
-    const float* __restrict__ radius, const uint32_t* __restrict__ tiles, int ntx, int nty,
-    int chunk_ranks, uint32_t* __restrict__ counts) {
-  extern __shared__ uint32_t cnt[];
-  const int ntiles = ntx * nty;
-  for (int t = threadIdx.x; t < ntiles; t += blockDim.x) cnt[t] = 0;
+// ------------------------------------------------------------- level 1
+
+__global__ __launch_bounds__(256) void l1_count_kernel(
+    int64_t n, const uint32_t* __restrict__ order, const unsigned long long* __restrict__ rects,
+    const uint32_t* __restrict__ tiles, Geo geo, uint32_t* __restrict__ c1,
+    WsHeader* __restrict__ hdr) {
+  extern __shared__ uint32_t cnt[];  // [nblk]
+  for (int b = threadIdx.x; b < geo.nblk; b += blockDim.x) cnt[b] = 0;
   __syncthreads();
-  const int64_t r0 = (int64_t)blockIdx.x * chunk_ranks;
-  const int64_t r1 = std::min<int64_t>(n, r0 + chunk_ranks);
+  const int64_t r0 = (int64_t)blockIdx.x * kChunk;
+  const int64_t r1 = min<int64_t>(n, r0 + kChunk);
+  unsigned int m = 0;
   for (int64_t r = r0 + threadIdx.x; r < r1; r += blockDim.x) {
-    const Rect rc = rect_of(order[r], means2d, radius, tiles, ntx, nty);
-    for (int y = rc.y0; y <= rc.y1; ++y)
-      for (int x = rc.x0; x <= rc.x1; ++x) atomicAdd(&cnt[y * ntx + x], 1u);
+    const uint32_t g = order[r];
+    const Rect t = rect_of(g, rects);
+    if (t.x1 >= t.x0) m += (unsigned int)((t.x1 - t.x0 + 1) * (t.y1 - t.y0 + 1));
+    const Rect b = block_rect(t);
+    for (int y = b.y0; y <= b.y1; ++y)
+      for (int x = b.x0; x <= b.x1; ++x) atomicAdd(&cnt[y * geo.nbx + x], 1u);
   }
+  const unsigned int wm = wave_sum_u32(m);
+  if ((threadIdx.x & 63) == 0 && wm) atomicAdd(&hdr->m, (unsigned long long)wm);
   __syncthreads();
-  uint32_t* out = counts + (int64_t)blockIdx.x * ntiles;
-  for (int t = threadIdx.x; t < ntiles; t += blockDim.x) out[t] = cnt[t];
+  uint32_t* out = c1 + (int64_t)blockIdx.x * geo.nblk;
+  for (int b = threadIdx.x; b < geo.nblk; b += blockDim.x) out[b] = cnt[b];
 }
 
-// counts[chunk][tile] -> exclusive prefix down each tile column; column
-// totals -> tile_total. Lane = tile, the 16 waves split the chunks.
-__global__ __launch_bounds__(1024) void bin_scan_columns_kernel(uint32_t* __restrict__ counts,
-                                                                int64_t chunks, int ntiles,
-                                                                uint32_t* __restrict__ tile_total) {
+// counts[row][col] -> exclusive prefix down each column; column totals.
+// Lane = column, the 16 waves split the rows.
+__global__ __launch_bounds__(1024) void scan_columns_kernel(uint32_t* __restrict__ counts,
+                                                            int64_t rows, int cols,
+                                                            uint32_t* __restrict__ col_total) {
   __shared__ uint32_t part[16][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int t = blockIdx.x * 64 + lane;
-  const int64_t per = (chunks + 15) / 16;
-  const int64_t c0 = std::min<int64_t>(chunks, per * w), c1 = std::min<int64_t>(chunks, c0 + per);
+  const int c = blockIdx.x * 64 + lane;
+  const int64_t per = (rows + 15) / 16;
+  const int64_t q0 = min<int64_t>(rows, per * w), q1 = min<int64_t>(rows, q0 + per);
   uint32_t s = 0;
-  if (t < ntiles)
-    for (int64_t c = c0; c < c1; ++c) s += counts[c * ntiles + t];
+  if (c < cols)
+    for (int64_t q = q0; q < q1; ++q) s += counts[q * cols + c];
   part[w][lane] = s;
   __syncthreads();
   uint32_t run = 0;
   for (int k = 0; k < w; ++k) run += part[k][lane];
-  if (t < ntiles) {
-    for (int64_t c = c0; c < c1; ++c) {
-      const uint32_t v = counts[c * ntiles + t];
-      counts[c * ntiles + t] = run;
+  if (c < cols) {
+    for (int64_t q = q0; q < q1; ++q) {
+      const uint32_t v = counts[q * cols + c];
+      counts[q * cols + c] = run;
       run += v;
     }
-    if (w == 15) tile_total[t] = run;
+    if (w == 15) col_total[c] = run;
   }
 }
 
-// Exclusive scan over tiles -> tile_off, tile_ranges, M; one workgroup.
+// Bucket offsets, sub-chunk offsets and the overflow decision; one workgroup.
+__global__ __launch_bounds__(kScanThreads) void l1_finish_kernel(
+    const uint32_t* __restrict__ blk_total, int nblk, unsigned long long capacity,
+    uint32_t* __restrict__ blk_off, uint32_t* __restrict__ sub_off, WsHeader* __restrict__ hdr) {
+  __shared__ unsigned long long part[kScanThreads];
+  __shared__ unsigned long long spart[kScanThreads];
+  const unsigned long long m = hdr->m;
+  const bool over = m > capacity || m >= (1ull << 32);
+  const int per = (nblk + kScanThreads - 1) / kScanThreads;
+  const int lo = min(nblk, per * (int)threadIdx.x), hi = min(nblk, lo + per);
+  unsigned long long s = 0, ss = 0;
+  for (int b = lo; b < hi; ++b) {
+    s += blk_total[b];
+    ss += (blk_total[b] + kSub - 1) / kSub;
+  }
+  part[threadIdx.x] = s;
+  spart[threadIdx.x] = ss;
+  __syncthreads();
+  for (int off = 1; off < kScanThreads; off <<= 1) {
+    const unsigned long long v = threadIdx.x >= off ? part[threadIdx.x - off] : 0ull;
+    const unsigned long long vs = threadIdx.x >= off ? spart[threadIdx.x - off] : 0ull;
+    __syncthreads();
+    part[threadIdx.x] += v;
+    spart[threadIdx.x] += vs;
+    __syncthreads();
+  }
+  unsigned long long run = part[threadIdx.x] - s, srun = spart[threadIdx.x] - ss;
+  for (int b = lo; b < hi; ++b) {
+    blk_off[b] = (uint32_t)run;
+    sub_off[b] = (uint32_t)srun;
+    run += blk_total[b];
+    srun += (blk_total[b] + kSub - 1) / kSub;
+  }
+  if (threadIdx.x == kScanThreads - 1) {
+    blk_off[nblk] = (uint32_t)run;
+    sub_off[nblk] = (uint32_t)srun;
+    hdr->m1 = run;
+    hdr->overflow = over ? 1u : 0u;
+    hdr->total_sub = over ? 0u : (uint32_t)srun;
+  }
+}
+
+// Ordered scatter of (block, Gaussian) pairs of one chunk of depth ranks into
+// the bucket-major pair array. Wave w owns ranks [w * 256, w * 256 + 256) of
+// the chunk; LDS holds, per wave and block, the next free slot.
+__global__ __launch_bounds__(256) void l1_scatter_kernel(
+    int64_t n, const uint32_t* __restrict__ order, const unsigned long long* __restrict__ rects,
+    Geo geo,
+    const uint32_t* __restrict__ c1, const uint32_t* __restrict__ blk_off,
+    const WsHeader* __restrict__ hdr, unsigned long long* __restrict__ pairs) {
+  extern __shared__ uint32_t slot[];  // [4][nblk]
+  if (hdr->overflow) return;
+  const int nblk = geo.nblk;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t rbase = (int64_t)blockIdx.x * kChunk + (int64_t)w * kRanksPerWave;
+  uint32_t* my = slot + w * nblk;
+  for (int t = threadIdx.x; t < 4 * nblk; t += blockDim.x) slot[t] = 0;
+  __syncthreads();
+  uint32_t gj[4];
+  Rect bj[4], tj[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t r = rbase + lane + 64 * j;
+    gj[j] = r < n ? order[r] : 0u;
+    tj[j] = r < n ? rect_of(gj[j], rects) : Rect{0, 0, -1, -1};
+    bj[j] = block_rect(tj[j]);
+    for (int y = bj[j].y0; y <= bj[j].y1; ++y)
+      for (int x = bj[j].x0; x <= bj[j].x1; ++x) atomicAdd(&my[y * geo.nbx + x], 1u);
+  }
+  __syncthreads();
+  const uint32_t* crow = c1 + (int64_t)blockIdx.x * nblk;
+  for (int b = threadIdx.x; b < nblk; b += blockDim.x) {
+    uint32_t run = blk_off[b] + crow[b];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t c = slot[k * nblk + b];
+      slot[k * nblk + b] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+#pragma unroll 1
+    for (int l = 0; l < 64; ++l) {
+      const int x0 = __builtin_amdgcn_readlane(bj[j].x0, l);
+      const int x1 = __builtin_amdgcn_readlane(bj[j].x1, l);
+      if (x1 < x0) continue;
+      const int y0 = __builtin_amdgcn_readlane(bj[j].y0, l);
+      const int y1 = __builtin_amdgcn_readlane(bj[j].y1, l);
+      const uint32_t g = (uint32_t)__builtin_amdgcn_readlane((int)gj[j], l);
+      const Rect t{__builtin_amdgcn_readlane(tj[j].x0, l), __builtin_amdgcn_readlane(tj[j].y0, l),
+                   __builtin_amdgcn_readlane(tj[j].x1, l), __builtin_amdgcn_readlane(tj[j].y1, l)};
+      const int wr = x1 - x0 + 1;
+      const int area = wr * (y1 - y0 + 1);
+      const float inv_wr = 1.0f / (float)wr;
+      for (int cell = lane; cell < area; cell += 64) {
+        int cx, cy;
+        cell_xy(cell, wr, inv_wr, cx, cy);
+        const int bx = x0 + cx, by = y0 + cy;
+        const uint32_t pos = atomicAdd(&my[by * geo.nbx + bx], 1u);
+        // the pair carries the rectangle clipped to its block, packed
+        pairs[pos] = (unsigned long long)g |
+                     ((unsigned long long)pack_local(clip_to_block(t, bx, by)) << 32);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------- level 2
+//
+// A block has 8 x 8 = 64 tiles: lane l of a wave owns local tile l
+// (x = l % 8, y = l / 8). For each bucket entry, in depth order, every lane
+// tests whether its tile lies in the entry's rectangle; counts and running
+// positions stay in registers. Sub-chunks of 256 entries are staged in LDS
+// (at most 256 x 64 entries) and leave as one coalesced run per tile.
+
+struct SubChunk {
+  int bx, by;        // block
+  uint32_t e0, e1;   // entries [e0, e1) of the pair array
+};
+
+// block of sub-chunk s: the last b with sub_off[b] <= s (uniform scalar search)
+__device__ __forceinline__ SubChunk sub_chunk(uint32_t s, const uint32_t* __restrict__ sub_off,
+                                              const uint32_t* __restrict__ blk_off, const Geo& geo) {
+  int lo = 0, hi = geo.nblk;  // sub_off[lo] <= s < sub_off[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (sub_off[mid] <= s) lo = mid; else hi = mid;
+  }
+  SubChunk c;
+  c.bx = lo % geo.nbx;
+  c.by = lo / geo.nbx;
+  c.e0 = blk_off[lo] + (s - sub_off[lo]) * kSub;
+  c.e1 = min(c.e0 + (uint32_t)kSub, blk_off[lo + 1]);
+  return c;
+}
+
+__device__ __forceinline__ bool lane_in(int packed, int lx, int ly) {
+  const int x0 = packed & 7, y0 = (packed >> 3) & 7, x1 = (packed >> 6) & 7, y1 = (packed >> 9) & 7;
+  return packed != 0 && lx >= x0 && lx <= x1 && ly >= y0 && ly <= y1;
+}
+
+__device__ __forceinline__ void load_entry(const unsigned long long* __restrict__ pairs,
+                                           uint32_t e, uint32_t e1, uint32_t& g, int& packed) {
+  g = 0;
+  packed = 0;
+  if (e < e1) {
+    const unsigned long long p = pairs[e];
+    g = (uint32_t)p;
+    packed = (int)(p >> 32);
+  }
+}
+
+// One wave per sub-chunk (grid stride): c2[s][tile] = entries covering the tile.
+__global__ __launch_bounds__(64) void l2_count_kernel(
+    const unsigned long long* __restrict__ pairs, Geo geo, const uint32_t* __restrict__ sub_off,
+    const uint32_t* __restrict__ blk_off, const WsHeader* __restrict__ hdr,
+    uint32_t* __restrict__ c2) {
+  const uint32_t total = hdr->total_sub;
+  const int lane = threadIdx.x, lx = lane & 7, ly = lane >> 3;
+  for (uint32_t s = blockIdx.x; s < total; s += gridDim.x) {
+    const SubChunk sc = sub_chunk(s, sub_off, blk_off, geo);
+    int pk[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t g;
+      load_entry(pairs, sc.e0 + lane + 64 * j, sc.e1, g, pk[j]);
+    }
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll 8
+      for (int l = 0; l < 64; ++l) cnt += lane_in(__builtin_amdgcn_readlane(pk[j], l), lx, ly);
+    c2[(int64_t)s * kBlkTiles + lane] = cnt;
+  }
+}
+
+// Per block: exclusive prefix of its sub-chunks' tile counts (lane = local
+// tile, the 16 waves split the sub-chunks) and the tile totals.
+__global__ __launch_bounds__(1024) void l2_scan_kernel(uint32_t* __restrict__ c2, Geo geo,
+                                                       const uint32_t* __restrict__ sub_off,
+                                                       const WsHeader* __restrict__ hdr,
+                                                       uint32_t* __restrict__ tile_total) {
+  __shared__ uint32_t part[16][64];
+  const int b = blockIdx.x, lt = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const bool live = !hdr->overflow;
+  const uint32_t s0 = live ? sub_off[b] : 0u, s1 = live ? sub_off[b + 1] : 0u;
+  const uint32_t per = (s1 - s0 + 15) / 16;
+  const uint32_t q0 = min(s1, s0 + per * w), q1 = min(s1, q0 + per);
+  uint32_t sum = 0;
+  for (uint32_t q = q0; q < q1; ++q) sum += c2[(int64_t)q * kBlkTiles + lt];
+  part[w][lt] = sum;
+  __syncthreads();
+  uint32_t run = 0;
+  for (int k = 0; k < w; ++k) run += part[k][lt];
+  for (uint32_t q = q0; q < q1; ++q) {
+    const uint32_t v = c2[(int64_t)q * kBlkTiles + lt];
+    c2[(int64_t)q * kBlkTiles + lt] = run;
+    run += v;
+  }
+  if (w == 15) {
+    const int bx = b % geo.nbx, by = b / geo.nbx;
+    const int tx = bx * kBlk + (lt & 7), ty = by * kBlk + (lt >> 3);
+    if (tx < geo.ntx && ty < geo.nty) tile_total[ty * geo.ntx + tx] = run;
+  }
+}
+
+// Exclusive scan over tiles -> tile_off and tile_ranges; one workgroup.
 __global__ __launch_bounds__(kScanThreads) void bin_scan_tiles_kernel(
     const uint32_t* __restrict__ tile_total, int ntiles, uint32_t* __restrict__ tile_off,
-    uint32_t* __restrict__ tile_ranges, WsHeader* __restrict__ hdr, unsigned long long capacity) {
+    uint32_t* __restrict__ tile_ranges, const WsHeader* __restrict__ hdr) {
   __shared__ unsigned long long part[kScanThreads];
+  if (hdr->overflow) return;
   const int per = (ntiles + kScanThreads - 1) / kScanThreads;
-  const int lo = std::min(ntiles, per * (int)threadIdx.x), hi = std::min(ntiles, lo + per);
+  const int lo = min(ntiles, per * (int)threadIdx.x), hi = min(ntiles, lo + per);
   unsigned long long s = 0;
   for (int i = lo; i < hi; ++i) s += tile_total[i];
   part[threadIdx.x] = s;
@@ -302,90 +582,92 @@ __global__ __launch_bounds__(kScanThreads) void bin_scan_tiles_kernel(
     part[threadIdx.x] += v;
     __syncthreads();
   }
-  const unsigned long long m = part[kScanThreads - 1];
-  const bool fits = m <= capacity && m < (1ull << 32);
   unsigned long long run = part[threadIdx.x] - s;
   for (int i = lo; i < hi; ++i) {
     const uint32_t v = tile_total[i];
     tile_off[i] = (uint32_t)run;
-    if (fits) {
-      tile_ranges[2 * i] = (uint32_t)run;
-      tile_ranges[2 * i + 1] = (uint32_t)(run + v);
-    }
+    tile_ranges[2 * i] = (uint32_t)run;
+    tile_ranges[2 * i + 1] = (uint32_t)(run + v);
     run += v;
-  }
-  if (threadIdx.x == 0) {
-    hdr->m = m;
-    hdr->overflow = fits ? 0u : 1u;
   }
 }
 
-// Stable scatter of every (tile, Gaussian) pair of one chunk of depth ranks.
-// Block = chunk_waves waves, wave w owns ranks [w * 256, w * 256 + 256) of the
-// chunk. LDS holds, per wave and tile, the next free slot.
-__global__ __launch_bounds__(256) void bin_scatter_kernel(
-    int64_t n, const uint32_t* __restrict__ order, const float* __restrict__ means2d,
-    const float* __restrict__ radius, const uint32_t* __restrict__ tiles,
-    const float* __restrict__ depth, int ntx, int nty, int chunk_ranks,
-    const uint32_t* __restrict__ counts, const uint32_t* __restrict__ tile_off,
+// Ordered scatter of one 256-entry sub-chunk into its block's 64 tile lists.
+// Wave w owns entries [64 w, 64 w + 64) of the sub-chunk; lane l counts and
+// places the entries of local tile l; the runs are staged in LDS (at most
+// 256 x 64 entries) and leave as one coalesced burst per tile.
+__global__ __launch_bounds__(256) void l2_scatter_kernel(
+    const unsigned long long* __restrict__ pairs, const float* __restrict__ depth, Geo geo,
+    const uint32_t* __restrict__ sub_off, const uint32_t* __restrict__ blk_off,
+    const uint32_t* __restrict__ c2, const uint32_t* __restrict__ tile_off,
     const WsHeader* __restrict__ hdr, uint32_t* __restrict__ values_sorted,
     unsigned long long* __restrict__ keys_sorted) {
-  extern __shared__ uint32_t slot[];  // [waves][ntiles]
-  if (hdr->overflow) return;
-  const int ntiles = ntx * nty;
-  const int nw = blockDim.x >> 6, w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t rbase = (int64_t)blockIdx.x * chunk_ranks + (int64_t)w * kRanksPerWave;
-  uint32_t* my = slot + (int64_t)w * ntiles;
-  for (int t = threadIdx.x; t < nw * ntiles; t += blockDim.x) slot[t] = 0;
-  __syncthreads();
-  // this lane's 4 ranks: rbase + lane + 64 j
-  uint32_t gj[4];
-  Rect rj[4];
+  __shared__ uint32_t stage[kSub * kBlkTiles];  // per tile, a run in depth order
+  __shared__ uint32_t wcnt[4][kBlkTiles];       // per wave counts, then first slots
+  __shared__ uint32_t soff[kBlkTiles + 1];      // run start of each tile in `stage`
+  __shared__ uint32_t dst[kBlkTiles];           // global start of each tile's run
+  const uint32_t total = hdr->total_sub;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, lx = lane & 7, ly = lane >> 3;
+  for (uint32_t s = blockIdx.x; s < total; s += gridDim.x) {
+    const SubChunk sc = sub_chunk(s, sub_off, blk_off, geo);
+    uint32_t g;
+    int pk;
+    load_entry(pairs, sc.e0 + threadIdx.x, sc.e1, g, pk);
+    uint32_t cnt = 0;
+#pragma unroll 8
+    for (int l = 0; l < 64; ++l) cnt += lane_in(__builtin_amdgcn_readlane(pk, l), lx, ly);
+    wcnt[w][lane] = cnt;
+    __syncthreads();
+    if (w == 0) {
+      uint32_t c[4], tot = 0;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int64_t r = rbase + lane + 64 * j;
-    gj[j] = r < n ? order[r] : 0u;
-    rj[j] = r < n ? rect_of(gj[j], means2d, radius, tiles, ntx, nty) : Rect{0, 0, -1, -1, false};
-    for (int y = rj[j].y0; y <= rj[j].y1; ++y)
-      for (int x = rj[j].x0; x <= rj[j].x1; ++x) atomicAdd(&my[y * ntx + x], 1u);
-  }
-  __syncthreads();
-  // per-wave counts -> first free slot of each wave
-  const uint32_t* crow = counts + (int64_t)blockIdx.x * ntiles;
-  for (int t = threadIdx.x; t < ntiles; t += blockDim.x) {
-    uint32_t run = tile_off[t] + crow[t];
-    for (int k = 0; k < nw; ++k) {
-      const uint32_t c = slot[k * ntiles + t];
-      slot[k * ntiles + t] = run;
-      run += c;
+      for (int k = 0; k < 4; ++k) {
+        c[k] = wcnt[k][lane];
+        tot += c[k];
+      }
+      // exclusive scan of the tile totals across the wave
+      uint32_t incl = tot;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t v = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += v;
+      }
+      const uint32_t start = incl - tot;
+      soff[lane] = start;
+      if (lane == 63) soff[64] = incl;
+      uint32_t run = start;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        wcnt[k][lane] = run;
+        run += c[k];
+      }
+      const int tx = sc.bx * kBlk + lx, ty = sc.by * kBlk + ly;
+      dst[lane] = (tx < geo.ntx && ty < geo.nty)
+                      ? tile_off[ty * geo.ntx + tx] + c2[(int64_t)s * kBlkTiles + lane]
+                      : 0u;
     }
-  }
-  __syncthreads();
-  // in rank order: lanes spread over the cells of one rectangle (distinct tiles)
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-#pragma unroll 1
+    __syncthreads();
+    // place, in depth order, into the LDS runs
+    uint32_t pos = wcnt[w][lane];
+#pragma unroll 8
     for (int l = 0; l < 64; ++l) {
-      const int x0 = __builtin_amdgcn_readlane(rj[j].x0, l);
-      const int y0 = __builtin_amdgcn_readlane(rj[j].y0, l);
-      const int x1 = __builtin_amdgcn_readlane(rj[j].x1, l);
-      const int y1 = __builtin_amdgcn_readlane(rj[j].y1, l);
-      if (x1 < x0) continue;
-      const uint32_t g = (uint32_t)__builtin_amdgcn_readlane((int)gj[j], l);
-      const int wr = x1 - x0 + 1;
-      const int area = wr * (y1 - y0 + 1);
-      const float inv_wr = 1.0f / (float)wr;
-      const unsigned long long dkey = keys_sorted ? (unsigned long long)__float_as_uint(depth[g]) : 0ull;
-      for (int cell = lane; cell < area; cell += 64) {
-        int cx, cy;
-        cell_xy(cell, wr, inv_wr, cx, cy);
-        const int t = (y0 + cy) * ntx + (x0 + cx);
-        const uint32_t pos = my[t];
-        my[t] = pos + 1;
-        values_sorted[pos] = g;
-        if (keys_sorted) keys_sorted[pos] = ((unsigned long long)t << 32) | dkey;
+      const int p = __builtin_amdgcn_readlane(pk, l);
+      const uint32_t gl = (uint32_t)__builtin_amdgcn_readlane((int)g, l);
+      if (lane_in(p, lx, ly)) stage[pos++] = gl;
+    }
+    __syncthreads();
+    // write out: wave w copies the runs of tiles w, w + 4, ...
+    for (int lt = w; lt < kBlkTiles; lt += 4) {
+      const uint32_t r0 = soff[lt], len = soff[lt + 1] - r0, d = dst[lt];
+      const int t = (sc.by * kBlk + (lt >> 3)) * geo.ntx + (sc.bx * kBlk + (lt & 7));
+      for (uint32_t i = lane; i < len; i += 64) {
+        const uint32_t gv = stage[r0 + i];
+        values_sorted[d + i] = gv;
+        if (keys_sorted)
+          keys_sorted[d + i] = ((unsigned long long)t << 32) | __float_as_uint(depth[gv]);
       }
     }
+    __syncthreads();
   }
 }
 
@@ -395,7 +677,9 @@ __global__ void bin_empty_kernel(int ntiles, uint32_t* __restrict__ tile_ranges,
     tile_ranges[i] = 0u;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     hdr->m = 0;
+    hdr->m1 = 0;
     hdr->overflow = 0;
+    hdr->total_sub = 0;
   }
 }
 
@@ -406,14 +690,17 @@ int32_t set_max_lds(const void* fn, size_t bytes) {
 
 }  // namespace
 
-size_t bin_sort_workspace_bytes(int64_t n, int ntiles) { return ws_layout(n, ntiles).total; }
+size_t bin_sort_workspace_bytes(int64_t n, int64_t capacity, int width, int height) {
+  return ws_layout(n, capacity, geo_of(width, height)).total;
+}
 
 int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, const float* radius,
                         const float* depth, const uint32_t* tiles_touched, int64_t capacity,
                         void* workspace, uint64_t* keys_sorted, uint32_t* values_sorted,
                         uint32_t* tile_ranges, hipStream_t stream) {
-  const int ntx = tiles_x(width), nty = tiles_y(height), ntiles = ntx * nty;
-  const WsLayout L = ws_layout(n, ntiles);
+  const Geo geo = geo_of(width, height);
+  const int ntiles = geo.ntx * geo.nty;
+  const WsLayout L = ws_layout(n, capacity, geo);
   char* ws = static_cast<char*>(workspace);
   WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
   if (n == 0) {
@@ -422,17 +709,16 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
     ABCD_HIP(hipGetLastError());
     return ABCD_OK;
   }
-  uint32_t* keys[2] = {reinterpret_cast<uint32_t*>(ws + L.keys_a), reinterpret_cast<uint32_t*>(ws + L.keys_b)};
-  uint32_t* vals[2] = {reinterpret_cast<uint32_t*>(ws + L.vals_a), reinterpret_cast<uint32_t*>(ws + L.vals_b)};
-  uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
-  uint32_t* totals = reinterpret_cast<uint32_t*>(ws + L.totals);
-  uint32_t* counts = reinterpret_cast<uint32_t*>(ws + L.counts);
-  uint32_t* tile_total = reinterpret_cast<uint32_t*>(ws + L.tile_total);
-  uint32_t* tile_off = reinterpret_cast<uint32_t*>(ws + L.tile_off);
+  auto u32 = [&](size_t off) { return reinterpret_cast<uint32_t*>(ws + off); };
+  uint32_t* keys[2] = {u32(L.keys_a), u32(L.keys_b)};
+  uint32_t* vals[2] = {u32(L.vals_a), u32(L.vals_b)};
+  uint32_t* hist = u32(L.hist);
+  uint32_t* totals = u32(L.totals);
 
   const int64_t gb = (n + kBlock - 1) / kBlock;
+  unsigned long long* rects = reinterpret_cast<unsigned long long*>(ws + L.rects);
   ABCD_LAUNCH("depth_keys", depth_keys_kernel, gb, kBlock, 0, stream, n, depth, tiles_touched,
-              keys[0], vals[0]);
+              means2d, radius, geo.ntx, geo.nty, keys[0], vals[0], rects, hdr);
   for (int pass = 0; pass < 4; ++pass) {
     const int src = pass & 1, dst = src ^ 1;
     ABCD_LAUNCH("radix_hist", radix_hist_kernel, L.rs_blocks, kBlock, 0, stream, keys[src], n,
@@ -444,26 +730,40 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   }
   const uint32_t* order = vals[0];  // four passes: back in buffer 0
 
-  const size_t count_lds = sizeof(uint32_t) * ntiles;
-  const size_t scatter_lds = sizeof(uint32_t) * ntiles * L.chunk_waves;
   static bool attrs_set = false;
   if (!attrs_set) {
-    int32_t st = set_max_lds((const void*)bin_count_kernel, sizeof(uint32_t) * 32768);
+    int32_t st = set_max_lds((const void*)l1_count_kernel, 65536);
     if (st != ABCD_OK) return st;
-    st = set_max_lds((const void*)bin_scatter_kernel, sizeof(uint32_t) * 32768);
+    st = set_max_lds((const void*)l1_scatter_kernel, 65536);
     if (st != ABCD_OK) return st;
     attrs_set = true;
   }
-  ABCD_LAUNCH("bin_count", bin_count_kernel, L.chunks, kBlock, count_lds, stream, n, order, means2d,
-              radius, tiles_touched, ntx, nty, L.chunk_ranks, counts);
-  ABCD_LAUNCH("bin_scan_columns", bin_scan_columns_kernel, (ntiles + 63) / 64, 1024, 0, stream,
-              counts, L.chunks, ntiles, tile_total);
+  const unsigned long long cap = (unsigned long long)std::max<int64_t>(capacity, 0);
+  uint32_t* c1 = u32(L.c1);
+  uint32_t* blk_total = u32(L.blk_total);
+  uint32_t* blk_off = u32(L.blk_off);
+  uint32_t* sub_off = u32(L.sub_off);
+  unsigned long long* pairs = reinterpret_cast<unsigned long long*>(ws + L.pairs);
+  uint32_t* c2 = u32(L.c2);
+  uint32_t* tile_total = u32(L.tile_total);
+  uint32_t* tile_off = u32(L.tile_off);
+  ABCD_LAUNCH("l1_count", l1_count_kernel, L.chunks, kBlock, sizeof(uint32_t) * geo.nblk, stream, n,
+              order, rects, tiles_touched, geo, c1, hdr);
+  ABCD_LAUNCH("l1_scan_columns", scan_columns_kernel, (geo.nblk + 63) / 64, 1024, 0, stream, c1,
+              L.chunks, geo.nblk, blk_total);
+  ABCD_LAUNCH("l1_finish", l1_finish_kernel, 1, kScanThreads, 0, stream, blk_total, geo.nblk, cap,
+              blk_off, sub_off, hdr);
+  ABCD_LAUNCH("l1_scatter", l1_scatter_kernel, L.chunks, kBlock, 4 * sizeof(uint32_t) * geo.nblk,
+              stream, n, order, rects, geo, c1, blk_off, hdr, pairs);
+  ABCD_LAUNCH("l2_count", l2_count_kernel, 4 * kStrideGrid, 64, 0, stream, pairs, geo, sub_off,
+              blk_off, hdr, c2);
+  ABCD_LAUNCH("l2_scan", l2_scan_kernel, geo.nblk, 1024, 0, stream, c2, geo, sub_off, hdr,
+              tile_total);
   ABCD_LAUNCH("bin_scan_tiles", bin_scan_tiles_kernel, 1, kScanThreads, 0, stream, tile_total,
-              ntiles, tile_off, tile_ranges, hdr,
-              (unsigned long long)std::max<int64_t>(capacity, 0));
-  ABCD_LAUNCH("bin_scatter", bin_scatter_kernel, L.chunks, 64 * L.chunk_waves, scatter_lds, stream,
-              n, order, means2d, radius, tiles_touched, depth, ntx, nty, L.chunk_ranks, counts,
-              tile_off, hdr, values_sorted, reinterpret_cast<unsigned long long*>(keys_sorted));
+              ntiles, tile_off, tile_ranges, hdr);
+  ABCD_LAUNCH("l2_scatter", l2_scatter_kernel, kStrideGrid, kBlock, 0, stream, pairs, depth, geo,
+              sub_off, blk_off, c2, tile_off, hdr, values_sorted,
+              reinterpret_cast<unsigned long long*>(keys_sorted));
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }

@@ -34,8 +34,6 @@ class ActiveBlockStep:
         self.dL_dout = torch.empty((H, W, 4), dtype=f32, device=dev)
         self.loss = torch.zeros((1,), dtype=f32, device=dev)
         self.n_blends = torch.zeros((1,), dtype=torch.int64, device=dev)
-        self.bin_ws = torch.empty(max(api.bin_sort_workspace_size(n, W, H), 256), dtype=torch.uint8,
-                                  device=dev)
         self.bwd_ws = torch.empty(max(api.render_bwd_workspace_size(n), 256), dtype=torch.uint8,
                                   device=dev)
         self.tile_ranges = torch.empty((api.n_tiles(W, H), 2), dtype=torch.int32, device=dev)
@@ -44,10 +42,11 @@ class ActiveBlockStep:
         if capacity is None:
             # size the intersection buffer from one synchronising pass
             api.project(cam, prm, **params, out=self.proj)
-            b = api.bin_sort(W, H, self.proj, capacity=0, workspace=self.bin_ws,
-                             tile_ranges=self.tile_ranges)
+            b = api.bin_sort(W, H, self.proj, capacity=0, tile_ranges=self.tile_ranges)
             capacity = int(b["n_isect"] * headroom) + 1024
         self.capacity = capacity
+        self.bin_ws = torch.empty(max(api.bin_sort_workspace_size(n, W, H, capacity), 256),
+                                  dtype=torch.uint8, device=dev)
         self.values = torch.empty((capacity,), dtype=torch.int32, device=dev)
         self.bins = dict(values=self.values, tile_ranges=self.tile_ranges)
 

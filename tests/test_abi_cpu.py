@@ -108,19 +108,23 @@ def test_project_rejects_null_and_misaligned(lib):
 
 def test_workspace_size_helpers_are_host_only(lib):
     sz = C.c_size_t(0)
-    assert lib.abcd_bin_sort_workspace_size(1_000_000, 1297, 840, C.byref(sz)) == 0
-    assert sz.value > 8 * 1_000_000
+    assert lib.abcd_bin_sort_workspace_size(1_000_000, 0, 1297, 840, C.byref(sz)) == 0
+    assert sz.value > 16 * 1_000_000
+    big = C.c_size_t(0)
+    assert lib.abcd_bin_sort_workspace_size(1_000_000, 10_000_000, 1297, 840, C.byref(big)) == 0
+    assert big.value >= sz.value + 4 * 10_000_000
     small = C.c_size_t(0)
-    assert lib.abcd_bin_sort_workspace_size(0, 16, 16, C.byref(small)) == 0
+    assert lib.abcd_bin_sort_workspace_size(0, 0, 16, 16, C.byref(small)) == 0
     assert small.value >= 256
-    assert lib.abcd_bin_sort_workspace_size(10, 0, 16, C.byref(sz)) == 1
+    assert lib.abcd_bin_sort_workspace_size(10, 0, 0, 16, C.byref(sz)) == 1
+    assert lib.abcd_bin_sort_workspace_size(10, 1 << 33, 16, 16, C.byref(sz)) == 1
     assert lib.abcd_render_bwd_workspace_size(1000, C.byref(sz)) == 0
     assert sz.value >= 9 * 4 * 1000 and sz.value % 256 == 0
 
 
 def test_bin_sort_rejects_small_or_misaligned_workspace(lib):
     need = C.c_size_t(0)
-    lib.abcd_bin_sort_workspace_size(100, 64, 48, C.byref(need))
+    lib.abcd_bin_sort_workspace_size(100, 1000, 64, 48, C.byref(need))
     m = C.c_int64(0)
     base = [64, 48, 100, FAKE, FAKE, FAKE, FAKE, 1000]
     assert lib.abcd_bin_sort(*base, FAKE + 8, need.value, None, FAKE, FAKE, C.byref(m), None) == 1

@@ -351,8 +351,8 @@ def _raw_bin(api, cam, p, capacity, values, ranges):
     import ctypes as C
     from paper_2608_27735_amd import _lib
     n = p["means2d"].shape[0]
-    ws = torch.empty(api.bin_sort_workspace_size(n, cam.width, cam.height), dtype=torch.uint8,
-                     device=dev())
+    ws = torch.empty(api.bin_sort_workspace_size(n, cam.width, cam.height, capacity),
+                     dtype=torch.uint8, device=dev())
     m = C.c_int64(0)
     st = _lib.load().abcd_bin_sort(cam.width, cam.height, n, p["means2d"].data_ptr(),
                                    p["radius"].data_ptr(), p["depth"].data_ptr(),
