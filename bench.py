@@ -25,9 +25,13 @@ sys.path.insert(0, ROOT)
 
 METRIC = "Gaussian-pixel blends/sec (fwd+bwd) and ms per active-block step, 1 GPU"
 HBM_PEAK_GBS = 8000.0
-# fp32 vector peak without packed-fp32 instructions: 256 CUs x 4 SIMDs x 16
-# lanes x 2.4 GHz = 39.3 T lane-instructions/s (78.6 TFLOP/s counting FMA as 2)
-VALU_PEAK_TOPS = 39.3
+# MI355X fp32 vector peak: 256 CUs x 2.4 GHz x 128 lanes-per-clock with packed FMA x 2 flops
+VALU_PEAK_TFLOPS = 157.3
+# algorithmic flops per evaluated (pixel, Gaussian) pair: alpha of the pair (offset, quadratic
+# form, exp, opacity, tests ~16) and, in the backward, its derivative terms and the sums over
+# the tile's pixels (~45)
+FLOPS_PER_PAIR = {"render_fwd": 16, "render_bwd": 45}
+PROFILES = os.path.join(ROOT, "profiles")
 
 KERNELS = ["composite", "project", "depth_keys", "radix_hist", "radix_scan", "radix_scatter",
            "l1_count", "l1_scan_columns", "l1_finish", "l1_scatter", "l2_count", "l2_scan",
@@ -64,6 +68,36 @@ def algorithmic_bytes(name, n, n_vis, m, npix, k, sh_coeffs):
     if name == "l2_scatter":
         return m * 4                                   # the sorted Gaussian indices
     return None
+
+
+def source_digest(names):
+    import hashlib
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2608_27735_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE runs, scaled by the plain-copy calibration), if
+    it was taken on the kernel source built now; else None."""
+    path = os.path.join(PROFILES, f"{kernel}_hbm_bytes.md")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if line.startswith("- ") and " = " in line:
+            k, v = line[2:].strip().split(" = ", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    try:
+        if vals["source_digest"] != source_digest(vals["sources"].split(",")):
+            return None
+        return (float(vals["fetch_kib"]) * float(vals["fetch_factor"]) +
+                float(vals["write_kib"]) * float(vals["write_factor"])) * 1024.0
+    except (KeyError, ValueError, OSError):
+        return None
 
 
 def main():
@@ -134,6 +168,8 @@ def main():
         api.timing_reset()
     sh_coeffs = (prm.sh_degree + 1) ** 2
     npix = cam.width * cam.height
+    # evaluated pairs: every pixel walks its tile list up to its last blended entry
+    pairs = int(st.fwd["last"].to(torch.int64).sum().item())
     dominant = max(kern, key=lambda x: kern[x]["ms_per_step"]) if kern else None
     roofline = None
     if dominant:
@@ -143,11 +179,19 @@ def main():
             launch_bytes = bytes_ / d["launches_per_step"]
             achieved = launch_bytes / (d["ms_per_launch"] / 1e3) / 1e9
             roofline = dict(bound="hbm", kernel=dominant, achieved=achieved, peak=HBM_PEAK_GBS,
-                            unit="GB/s", frac=achieved / HBM_PEAK_GBS, traffic=None,
+                            unit="GB/s", frac=achieved / HBM_PEAK_GBS,
+                            traffic=measured_traffic(dominant),
                             algorithmic_bytes_per_launch=launch_bytes)
-        else:
-            roofline = dict(bound="alu", kernel=dominant, achieved=None, peak=VALU_PEAK_TOPS,
-                            unit="Tops/s", frac=None, traffic=None)
+        elif dominant in FLOPS_PER_PAIR:
+            flops = pairs * FLOPS_PER_PAIR[dominant]
+            achieved = flops / (d["ms_per_launch"] / 1e3) / 1e12
+            roofline = dict(bound="alu", kernel=dominant, achieved=achieved,
+                            peak=VALU_PEAK_TFLOPS, unit="TFLOP/s",
+                            frac=achieved / VALU_PEAK_TFLOPS, traffic=measured_traffic(dominant),
+                            evaluated_pairs=pairs, flops_per_pair=FLOPS_PER_PAIR[dominant])
+    for name in FLOPS_PER_PAIR:
+        if name in kern:
+            kern[name]["TFLOPs"] = pairs * FLOPS_PER_PAIR[name] / (kern[name]["ms_per_launch"] / 1e3) / 1e12
     for name, d in kern.items():
         b = algorithmic_bytes(name, args.n, n_vis, m, npix, k, sh_coeffs)
         if b is not None:
@@ -177,6 +221,7 @@ def main():
                    "n_gaussians": args.n, "width": cam.width, "height": cam.height,
                    "sh_degree": prm.sh_degree, "k_cached": k, "n_front": n_front,
                    "n_isect": m, "n_visible": n_vis, "blends_per_step": blends_step,
+                   "evaluated_pairs_per_pass": pairs,
                    "sync_in_step": False},
         "roofline": roofline,
         "cpu_baseline": cpu,
