@@ -35,8 +35,8 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 KERNELS = ["composite", "project", "depth_keys", "radix_hist", "radix_scan", "radix_scatter",
            "l1_count", "l1_scan_columns", "l1_finish", "l1_scatter", "l2_count", "l2_scan",
-           "bin_scan_tiles", "l2_scatter", "render_fwd", "loss_l1", "zero_fill", "render_bwd",
-           "project_bwd"]
+           "bin_scan_tiles", "l2_scatter", "bin_tile_order", "render_fwd", "loss_l1", "zero_fill",
+           "bwd_order", "render_bwd", "project_bwd"]
 
 
 def parse():

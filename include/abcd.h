@@ -117,11 +117,13 @@ ABCD_API int32_t abcd_project(const abcd_camera* cam /* host */, const abcd_rast
  *
  * Outputs: values_sorted[M] Gaussian indices; keys_sorted[M] the keys (may be
  * NULL, then not written); tile_ranges[tiles][2] = [start, end) per tile
- * (start = number of pairs of lower tiles).
+ * (start = number of pairs of lower tiles); tile_order[tiles] (may be NULL,
+ * then not written): a schedule for abcd_render_fwd, the tile indices
+ * ordered by decreasing floor(log2(list length)), ties in tile order.
  *
  * capacity: number of elements values_sorted (and keys_sorted) can hold. If
  * the intersection count M exceeds it, nothing is written to values_sorted,
- * keys_sorted or tile_ranges.
+ * keys_sorted, tile_ranges or tile_order.
  * n_isect (host, may be NULL): if given, the call synchronises `stream` once,
  * stores M there and returns ABCD_E_CAPACITY when M > capacity. If NULL, the
  * call does not synchronise; M (uint64) is left at the start of the workspace
@@ -136,8 +138,8 @@ ABCD_API int32_t abcd_bin_sort_workspace_size(int64_t n, int64_t capacity, int32
 ABCD_API int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const float* means2d,
                       const float* radius, const float* depth, const uint32_t* tiles_touched,
                       int64_t capacity, void* workspace, size_t ws_bytes, uint64_t* keys_sorted,
-                      uint32_t* values_sorted, uint32_t* tile_ranges, int64_t* n_isect /* host */,
-                      hipStream_t stream);
+                      uint32_t* values_sorted, uint32_t* tile_ranges, uint32_t* tile_order,
+                      int64_t* n_isect /* host */, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Forward render and composite (Method section: F over active over B).
@@ -153,9 +155,14 @@ ABCD_API int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const f
  * F or B may be NULL (transparent). Also writes final_T[H][W] and last[H][W]
  * (entries of the tile's list walked up to and including the last blended
  * one), both needed by abcd_render_bwd. n_blends (may be NULL): the number of
- * blended (pixel, Gaussian) pairs of this call is ADDED to *n_blends. */
+ * blended (pixel, Gaussian) pairs of this call is ADDED to *n_blends.
+ * tile_order (may be NULL): the order in which workgroups take tiles, a
+ * permutation of the tiles such as abcd_bin_sort's tile_order (heaviest
+ * first balances the GPU); it changes no output. NULL takes tiles in raster
+ * order. */
 ABCD_API int32_t abcd_render_fwd(const abcd_camera* cam /* host */, const abcd_raster_params* prm /* host */,
-                        const uint32_t* tile_ranges, const uint32_t* values_sorted,
+                        const uint32_t* tile_ranges, const uint32_t* tile_order,
+                        const uint32_t* values_sorted,
                         const float* means2d, const float* conic_opacity, const float* rgb,
                         const float* F, const float* B, float* out_rgba, float* final_T,
                         uint32_t* last, unsigned long long* n_blends, hipStream_t stream);
@@ -171,7 +178,10 @@ ABCD_API int32_t abcd_render_fwd(const abcd_camera* cam /* host */, const abcd_r
  * the arrays, otherwise they overwrite them. The derivative is exact for the
  * forward above, including zero derivative of a clamped alpha and of a
  * clamped colour. Inputs are those of the forward call on the same camera.
- * workspace: at least abcd_render_bwd_workspace_size(n) bytes, 256-byte aligned. */
+ * workspace: at least abcd_render_bwd_workspace_size(n) bytes, 256-byte
+ * aligned (screen-space gradients, 36 bytes per Gaussian, and the tile
+ * schedule of the backward, heaviest walk first, 8 bytes per tile at the
+ * maximum tile count). */
 ABCD_API int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes);
 ABCD_API int32_t abcd_render_bwd(const abcd_camera* cam /* host */, const abcd_raster_params* prm /* host */,
                         int64_t n, const float* means, const float* log_scales, const float* quats,

@@ -88,8 +88,9 @@ def bin_sort_workspace_size(n, width, height, capacity=0):
 
 
 def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, keys=None,
-             tile_ranges=None, want_keys=False, sync=True):
-    """Per-tile depth-sorted lists. Returns dict(values, tile_ranges, keys, n_isect).
+             tile_ranges=None, tile_order=None, want_keys=False, sync=True):
+    """Per-tile depth-sorted lists. Returns dict(values, tile_ranges, tile_order,
+    keys, n_isect); tile_order is the forward's schedule (heaviest lists first).
 
     With sync=True (default) M is read back (one stream synchronisation) and
     the buffers are grown to fit it; with sync=False the call never
@@ -105,6 +106,8 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
     _need(tiles, "tiles_touched", torch.int32, (n,))
     if tile_ranges is None:
         tile_ranges = _empty((n_tiles(width, height), 2), torch.int32, dev)
+    if tile_order is None:
+        tile_order = _empty((n_tiles(width, height),), torch.int32, dev)
     if capacity is None:
         capacity = 0 if values is None else values.numel()
     ws_bytes = bin_sort_workspace_size(n, width, height, capacity)
@@ -119,7 +122,7 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
     st = lib.abcd_bin_sort(width, height, n, _ptr(means2d), _ptr(radius), _ptr(depth), _ptr(tiles),
                            capacity, _ptr(workspace), workspace.numel(),
                            _ptr(keys) if want_keys else None, _ptr(values), _ptr(tile_ranges),
-                           C.byref(m) if sync else None, _stream())
+                           _ptr(tile_order), C.byref(m) if sync else None, _stream())
     if st == _lib.ABCD_E_CAPACITY and sync:
         capacity = int(m.value)
         values = _empty((max(capacity, 1),), torch.int32, dev)
@@ -131,9 +134,10 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
         st = lib.abcd_bin_sort(width, height, n, _ptr(means2d), _ptr(radius), _ptr(depth),
                                _ptr(tiles), capacity, _ptr(workspace), workspace.numel(),
                                _ptr(keys) if want_keys else None, _ptr(values), _ptr(tile_ranges),
-                               C.byref(m), _stream())
+                               _ptr(tile_order), C.byref(m), _stream())
     check(st)
-    return dict(values=values, tile_ranges=tile_ranges, keys=keys if want_keys else None,
+    return dict(values=values, tile_ranges=tile_ranges, tile_order=tile_order,
+                keys=keys if want_keys else None,
                 n_isect=int(m.value) if sync else None, workspace=workspace, capacity=capacity)
 
 
@@ -152,8 +156,8 @@ def render_fwd(cam, prm, bins, proj, F=None, B=None, n_blends=None, out=None):
                    last=_empty((H, W), torch.int32, dev))
     lib = _lib.load()
     check(lib.abcd_render_fwd(C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)),
-                              _ptr(bins["tile_ranges"]), _ptr(bins["values"]),
-                              _ptr(proj["means2d"]), _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]),
+                              _ptr(bins["tile_ranges"]), _ptr(bins.get("tile_order")),
+                              _ptr(bins["values"]), _ptr(proj["means2d"]), _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]),
                               _ptr(F), _ptr(B), _ptr(out["out"]), _ptr(out["final_T"]),
                               _ptr(out["last"]), _ptr(n_blends), _stream()))
     return out

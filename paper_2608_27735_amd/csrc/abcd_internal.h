@@ -24,6 +24,12 @@ inline int tiles_y(int h) { return (h + kTile - 1) / kTile; }
 void set_error(const char* fmt, ...);
 int32_t hip_fail(hipError_t e, const char* what);
 
+#define TRY_STATUS(call)            \
+  do {                              \
+    const int32_t st_ = (call);     \
+    if (st_ != ABCD_OK) return st_; \
+  } while (0)
+
 #define ABCD_HIP(call)                                   \
   do {                                                   \
     hipError_t e_ = (call);                              \
@@ -183,7 +189,7 @@ size_t bin_sort_workspace_bytes(int64_t n, int64_t capacity, int width, int heig
 int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, const float* radius,
                         const float* depth, const uint32_t* tiles_touched, int64_t capacity,
                         void* workspace, uint64_t* keys_sorted, uint32_t* values_sorted,
-                        uint32_t* tile_ranges, hipStream_t stream);
+                        uint32_t* tile_ranges, uint32_t* tile_order, hipStream_t stream);
 
 // render.hip
 size_t render_bwd_workspace_bytes(int64_t n);
@@ -191,7 +197,8 @@ int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
                           const uint32_t* tile_ranges, const uint32_t* values_sorted,
                           const float* means2d, const float* conic_opacity, const float* rgb,
                           const float* F, const float* B, float* out_rgba, float* final_T,
-                          uint32_t* last, unsigned long long* n_blends, hipStream_t stream);
+                          uint32_t* last, unsigned long long* n_blends, const uint32_t* tile_order,
+                          hipStream_t stream);
 int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
                                  const uint32_t* tile_ranges, const uint32_t* values_sorted,
                                  const float* means2d, const float* conic_opacity,
@@ -202,6 +209,14 @@ int32_t launch_zero(float* p, int64_t count, hipStream_t stream);
 int32_t launch_loss_l1(int width, int height, const float* out_rgba, const float* target_rgb,
                        float bg0, float bg1, float bg2, float* dL_dout, float* loss,
                        hipStream_t stream);
+
+// schedule.hip: tiles ordered by decreasing octave of `work` (stable; the
+// kernel does nothing if `skip` is non-NULL and *skip != 0 on the device),
+// and the per-tile maximum of the forward's walk lengths as a work estimate.
+int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, const uint32_t* skip,
+                          const char* name, hipStream_t stream);
+int32_t launch_tile_walk(int width, int height, const uint32_t* last, uint32_t* work,
+                         hipStream_t stream);
 
 // composite.hip
 int32_t launch_composite(int width, int height, int k, const uint16_t* images,

@@ -161,8 +161,8 @@ int32_t abcd_bin_sort_workspace_size(int64_t n, int64_t capacity, int32_t width,
 int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const float* means2d,
                       const float* radius, const float* depth, const uint32_t* tiles_touched,
                       int64_t capacity, void* workspace, size_t ws_bytes, uint64_t* keys_sorted,
-                      uint32_t* values_sorted, uint32_t* tile_ranges, int64_t* n_isect,
-                      hipStream_t stream) {
+                      uint32_t* values_sorted, uint32_t* tile_ranges, uint32_t* tile_order,
+                      int64_t* n_isect, hipStream_t stream) {
   TRY(check_n(n));
   REQUIRE(width > 0 && height > 0, "image size must be positive");
   const int64_t tiles = (int64_t)tiles_x(width) * tiles_y(height);
@@ -179,7 +179,7 @@ int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const float* mea
   }
   REQUIRE(capacity == 0 || values_sorted != nullptr, "values_sorted is NULL with capacity > 0");
   TRY(launch_bin_sort(width, height, n, means2d, radius, depth, tiles_touched, capacity, workspace,
-                      keys_sorted, values_sorted, tile_ranges, stream));
+                      keys_sorted, values_sorted, tile_ranges, tile_order, stream));
   if (n_isect) {
     unsigned long long m = 0;
     ABCD_HIP(hipMemcpyAsync(&m, workspace, sizeof m, hipMemcpyDeviceToHost, stream));
@@ -198,7 +198,8 @@ int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const float* mea
 }
 
 int32_t abcd_render_fwd(const abcd_camera* cam, const abcd_raster_params* prm,
-                        const uint32_t* tile_ranges, const uint32_t* values_sorted,
+                        const uint32_t* tile_ranges, const uint32_t* tile_order,
+                        const uint32_t* values_sorted,
                         const float* means2d, const float* conic_opacity, const float* rgb,
                         const float* F, const float* B, float* out_rgba, float* final_T,
                         uint32_t* last, unsigned long long* n_blends, hipStream_t stream) {
@@ -212,7 +213,7 @@ int32_t abcd_render_fwd(const abcd_camera* cam, const abcd_raster_params* prm,
               (reinterpret_cast<uintptr_t>(means2d) & 7) == 0,
           "RGBA images and conic_opacity must be 16-byte aligned, means2d 8-byte aligned");
   return launch_render_fwd(*cam, *prm, tile_ranges, values_sorted, means2d, conic_opacity, rgb, F,
-                           B, out_rgba, final_T, last, n_blends, stream);
+                           B, out_rgba, final_T, last, n_blends, tile_order, stream);
 }
 
 int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes) {

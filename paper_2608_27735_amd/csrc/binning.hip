@@ -672,9 +672,11 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
 }
 
 __global__ void bin_empty_kernel(int ntiles, uint32_t* __restrict__ tile_ranges,
-                                 WsHeader* __restrict__ hdr) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < 2 * ntiles; i += gridDim.x * blockDim.x)
+                                 uint32_t* __restrict__ tile_order, WsHeader* __restrict__ hdr) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < 2 * ntiles; i += gridDim.x * blockDim.x) {
     tile_ranges[i] = 0u;
+    if (tile_order && i < ntiles) tile_order[i] = (uint32_t)i;
+  }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     hdr->m = 0;
     hdr->m1 = 0;
@@ -697,7 +699,7 @@ size_t bin_sort_workspace_bytes(int64_t n, int64_t capacity, int width, int heig
 int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, const float* radius,
                         const float* depth, const uint32_t* tiles_touched, int64_t capacity,
                         void* workspace, uint64_t* keys_sorted, uint32_t* values_sorted,
-                        uint32_t* tile_ranges, hipStream_t stream) {
+                        uint32_t* tile_ranges, uint32_t* tile_order, hipStream_t stream) {
   const Geo geo = geo_of(width, height);
   const int ntiles = geo.ntx * geo.nty;
   const WsLayout L = ws_layout(n, capacity, geo);
@@ -705,7 +707,7 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
   if (n == 0) {
     ABCD_LAUNCH("bin_scan_tiles", bin_empty_kernel, std::max(1, (2 * ntiles + 255) / 256), 256, 0,
-                stream, ntiles, tile_ranges, hdr);
+                stream, ntiles, tile_ranges, tile_order, hdr);
     ABCD_HIP(hipGetLastError());
     return ABCD_OK;
   }
@@ -765,6 +767,10 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
               sub_off, blk_off, c2, tile_off, hdr, values_sorted,
               reinterpret_cast<unsigned long long*>(keys_sorted));
   ABCD_HIP(hipGetLastError());
+  // forward schedule: heaviest lists first (nothing is written on overflow)
+  if (tile_order)
+    TRY_STATUS(launch_tile_order(ntiles, tile_total, tile_order, &hdr->overflow, "bin_tile_order",
+                                 stream));
   return ABCD_OK;
 }
 

@@ -19,10 +19,13 @@ struct BlendConsts {
   float alpha_min, alpha_max, t_min;
 };
 
-// Workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous
-// band of tiles so neighbouring tiles (which share Gaussians) share an L2.
-__device__ __forceinline__ int tile_of_block(const BlendConsts& k) {
+// Tile of this workgroup: the given schedule (heaviest tiles first), or, with
+// none, raster order with each of the 8 XCDs (which take workgroups round
+// robin) given a contiguous band of tiles, so that neighbouring tiles (which
+// share Gaussians) share an L2.
+__device__ __forceinline__ int tile_of_block(const BlendConsts& k, const uint32_t* order) {
   const int b = blockIdx.x;
+  if (order) return (int)order[b];
   return (b & 7) * k.per_xcd + (b >> 3);
 }
 
@@ -91,14 +94,14 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
     float4* __restrict__ out, float* __restrict__ final_T, uint32_t* __restrict__ last,
-    unsigned long long* __restrict__ n_blends) {
+    unsigned long long* __restrict__ n_blends, const uint32_t* __restrict__ order) {
   __shared__ float4 s_ga[256];  // u, v, qa, qb
   __shared__ float4 s_gb[256];  // qc, o, r, g
   __shared__ float s_bl[256];   // b
   __shared__ int s_pos[256];    // position in the tile's list
   __shared__ int s_wcnt[4];
   __shared__ unsigned long long s_nb;
-  const int tile = tile_of_block(k);
+  const int tile = tile_of_block(k, order);
   if (tile >= k.ntiles) return;
   const int tid = threadIdx.x;
   const int px = (tile % k.ntx) * kTile + (tid & 15);
@@ -225,7 +228,7 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
     const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
     const float* __restrict__ final_T, const uint32_t* __restrict__ last,
-    const float4* __restrict__ dL_dout, float* __restrict__ g2d) {
+    const float4* __restrict__ dL_dout, float* __restrict__ g2d, const uint32_t* __restrict__ order) {
   __shared__ float4 s_ga[256];  // u, v, qa, qb
   __shared__ float4 s_gb[256];  // qc, o, r, g
   __shared__ float4 s_gc[256];  // a, b, c (conic), colour b
@@ -234,7 +237,7 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
   __shared__ float s_acc[9 * 256];  // entry-major: [entry][9]
   __shared__ int s_wcnt[4];
   __shared__ uint32_t s_max;
-  const int tile = tile_of_block(k);
+  const int tile = tile_of_block(k, order);
   if (tile >= k.ntiles) return;
   const int tid = threadIdx.x;
   const int px = (tile % k.ntx) * kTile + (tid & 15);
@@ -310,7 +313,7 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
           contrib = true;
           const float4 gc = s_gc[j];
           const float om = 1.0f - ae.alpha;
-          const float iom = 1.0f / om;
+          const float iom = __builtin_amdgcn_rcpf(om);  // om >= 1 - alpha_max > 0
           const float Tk = T * iom;
           const float wgt = ae.alpha * Tk;
           gr[6] = wgt * gcr;
@@ -408,21 +411,28 @@ BlendConsts consts(const abcd_camera& cam, const abcd_raster_params& prm) {
 
 }  // namespace
 
-size_t render_bwd_workspace_bytes(int64_t n) {
+static size_t g2d_bytes(int64_t n) {
   return ((size_t)9 * sizeof(float) * (size_t)n + 255) & ~size_t(255);
+}
+
+// g2d[n][9], then the backward's tile work and tile order.
+size_t render_bwd_workspace_bytes(int64_t n) {
+  return g2d_bytes(n) + 2 * sizeof(uint32_t) * ABCD_MAX_TILES;
 }
 
 int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
                           const uint32_t* tile_ranges, const uint32_t* values_sorted,
                           const float* means2d, const float* conic_opacity, const float* rgb,
                           const float* F, const float* B, float* out_rgba, float* final_T,
-                          uint32_t* last, unsigned long long* n_blends, hipStream_t stream) {
+                          uint32_t* last, unsigned long long* n_blends, const uint32_t* tile_order,
+                          hipStream_t stream) {
   const BlendConsts k = consts(cam, prm);
-  ABCD_LAUNCH("render_fwd", render_fwd_kernel, 8 * k.per_xcd, kBlock, 0, stream, k, tile_ranges,
+  const int grid = tile_order ? k.ntiles : 8 * k.per_xcd;
+  ABCD_LAUNCH("render_fwd", render_fwd_kernel, grid, kBlock, 0, stream, k, tile_ranges,
               values_sorted, reinterpret_cast<const float2*>(means2d),
               reinterpret_cast<const float4*>(conic_opacity), rgb,
               reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B),
-              reinterpret_cast<float4*>(out_rgba), final_T, last, n_blends);
+              reinterpret_cast<float4*>(out_rgba), final_T, last, n_blends, tile_order);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }
@@ -433,13 +443,16 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
                                  const float* rgb, const float* F, const float* B,
                                  const float* final_T, const uint32_t* last,
                                  const float* dL_dout, float* g2d, hipStream_t stream) {
-  (void)n;
   const BlendConsts k = consts(cam, prm);
-  ABCD_LAUNCH("render_bwd", render_bwd_kernel, 8 * k.per_xcd, kBlock, 0, stream, k, tile_ranges,
+  uint32_t* work = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(g2d) + g2d_bytes(n));
+  uint32_t* order = work + ABCD_MAX_TILES;
+  TRY_STATUS(launch_tile_walk(k.width, k.height, last, work, stream));
+  TRY_STATUS(launch_tile_order(k.ntiles, work, order, nullptr, "bwd_order", stream));
+  ABCD_LAUNCH("render_bwd", render_bwd_kernel, k.ntiles, kBlock, 0, stream, k, tile_ranges,
               values_sorted, reinterpret_cast<const float2*>(means2d),
               reinterpret_cast<const float4*>(conic_opacity), rgb,
               reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B), final_T,
-              last, reinterpret_cast<const float4*>(dL_dout), g2d);
+              last, reinterpret_cast<const float4*>(dL_dout), g2d, order);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }

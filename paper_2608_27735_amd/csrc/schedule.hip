@@ -1,0 +1,135 @@
+// schedule.hip -- the order in which the blend kernels take their tiles.
+//
+// Per-tile work in the blend kernels is very uneven (a tile's walk length
+// ranges over two orders of magnitude), and a workgroup holds its CU slot
+// until its slowest wave finishes. Launched in raster order, a few heavy tiles
+// start late and run on an otherwise idle GPU. Taking tiles heaviest first
+// (longest-processing-time order) lets the light tiles fill in around them.
+//
+// The work estimate is the tile's list length for the forward (known after
+// binning) and the tile's largest per-pixel walk length for the backward
+// (known after the forward). The order is a stable bucket sort by the octave
+// of the estimate, so tiles of one octave keep their raster order and
+// neighbouring tiles stay close in launch order.
+#include "abcd_internal.h"
+
+namespace abcd {
+namespace {
+
+constexpr int kOrderThreads = 1024;
+constexpr int kOrderWaves = kOrderThreads / 64;
+constexpr int kBuckets = 33;  // leading-zero count of the work, 32 for no work
+constexpr int kNone = 64;     // no tile
+
+__device__ __forceinline__ int bucket_of(uint32_t work) { return work ? __clz(work) : 32; }
+
+// For each distinct bucket among the wave's lanes: the lanes holding it, and
+// this lane's rank among them. Returns per-lane rank; calls emit(bucket,
+// count) once per distinct bucket from lane 0.
+template <typename Emit>
+__device__ __forceinline__ uint32_t rank_in_wave(int key, Emit emit) {
+  const int l = threadIdx.x & 63;
+  const uint64_t below = (1ull << l) - 1ull;
+  uint32_t rank = 0;
+  bool pending = key != kNone;
+  while (true) {
+    const uint64_t act = __ballot(pending);
+    if (!act) break;
+    const int kb = __shfl(key, __ffsll((unsigned long long)act) - 1, 64);
+    const uint64_t same = __ballot(key == kb);
+    if (key == kb) {
+      rank = __popcll(same & below);
+      pending = false;
+    }
+    if (l == 0) emit(kb, (uint32_t)__popcll(same));
+  }
+  return rank;
+}
+
+__global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
+                                                                   const uint32_t* __restrict__ work,
+                                                                   uint32_t* __restrict__ order,
+                                                                   const uint32_t* __restrict__ skip) {
+  __shared__ uint32_t s_base[kBuckets];
+  __shared__ uint32_t s_wc[kOrderWaves][kBuckets];
+  if (skip && *skip) return;
+  const int tid = threadIdx.x, w = tid >> 6;
+  if (tid < kBuckets) s_base[tid] = 0;
+  __syncthreads();
+  // bucket totals
+  for (int t0 = 0; t0 < ntiles; t0 += kOrderThreads) {
+    const int t = t0 + tid;
+    const int key = t < ntiles ? bucket_of(work[t]) : kNone;
+    rank_in_wave(key, [&](int b, uint32_t c) { atomicAdd(&s_base[b], c); });
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t acc = 0;
+    for (int b = 0; b < kBuckets; ++b) {
+      const uint32_t c = s_base[b];
+      s_base[b] = acc;
+      acc += c;
+    }
+  }
+  // stable placement, one chunk of tiles at a time
+  for (int t0 = 0; t0 < ntiles; t0 += kOrderThreads) {
+    for (int i = tid; i < kOrderWaves * kBuckets; i += kOrderThreads) (&s_wc[0][0])[i] = 0;
+    __syncthreads();
+    const int t = t0 + tid;
+    const int key = t < ntiles ? bucket_of(work[t]) : kNone;
+    const uint32_t rank = rank_in_wave(key, [&](int b, uint32_t c) { s_wc[w][b] = c; });
+    __syncthreads();
+    if (key != kNone) {
+      uint32_t off = s_base[key] + rank;
+      for (int v = 0; v < w; ++v) off += s_wc[v][key];
+      order[off] = (uint32_t)t;
+    }
+    __syncthreads();
+    if (tid < kBuckets) {
+      uint32_t c = 0;
+      for (int v = 0; v < kOrderWaves; ++v) c += s_wc[v][tid];
+      s_base[tid] += c;
+    }
+    __syncthreads();
+  }
+}
+
+// Largest per-pixel walk length (the forward's `last`) of each tile.
+__global__ __launch_bounds__(kBlock) void tile_walk_kernel(int width, int height, int ntx,
+                                                           const uint32_t* __restrict__ last,
+                                                           uint32_t* __restrict__ work) {
+  __shared__ uint32_t s_m;
+  const int tile = blockIdx.x;
+  const int px = (tile % ntx) * kTile + (threadIdx.x & 15);
+  const int py = (tile / ntx) * kTile + (threadIdx.x >> 4);
+  if (threadIdx.x == 0) s_m = 0;
+  __syncthreads();
+  uint32_t v = (px < width && py < height) ? last[(int64_t)py * width + px] : 0u;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off, 64));
+  if ((threadIdx.x & 63) == 0 && v) atomicMax(&s_m, v);
+  __syncthreads();
+  if (threadIdx.x == 0) work[tile] = s_m;
+}
+
+}  // namespace
+
+int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, const uint32_t* skip,
+                          const char* name, hipStream_t stream) {
+  if (ntiles <= 0) return ABCD_OK;
+  ABCD_LAUNCH(name, tile_order_kernel, 1, kOrderThreads, 0, stream, ntiles, work, order, skip);
+  ABCD_HIP(hipGetLastError());
+  return ABCD_OK;
+}
+
+int32_t launch_tile_walk(int width, int height, const uint32_t* last, uint32_t* work,
+                         hipStream_t stream) {
+  const int ntiles = tiles_x(width) * tiles_y(height);
+  if (ntiles <= 0) return ABCD_OK;
+  ABCD_LAUNCH("bwd_order", tile_walk_kernel, ntiles, kBlock, 0, stream, width, height,
+              tiles_x(width), last, work);
+  ABCD_HIP(hipGetLastError());
+  return ABCD_OK;
+}
+
+}  // namespace abcd

@@ -37,23 +37,27 @@ class ActiveBlockStep:
         self.bwd_ws = torch.empty(max(api.render_bwd_workspace_size(n), 256), dtype=torch.uint8,
                                   device=dev)
         self.tile_ranges = torch.empty((api.n_tiles(W, H), 2), dtype=torch.int32, device=dev)
+        self.tile_order = torch.empty((api.n_tiles(W, H),), dtype=torch.int32, device=dev)
         self.grads = {k: torch.zeros_like(params[k]) for k in
                       ("means", "log_scales", "quats", "opacity_logits", "sh")}
         if capacity is None:
             # size the intersection buffer from one synchronising pass
             api.project(cam, prm, **params, out=self.proj)
-            b = api.bin_sort(W, H, self.proj, capacity=0, tile_ranges=self.tile_ranges)
+            b = api.bin_sort(W, H, self.proj, capacity=0, tile_ranges=self.tile_ranges,
+                             tile_order=self.tile_order)
             capacity = int(b["n_isect"] * headroom) + 1024
         self.capacity = capacity
         self.bin_ws = torch.empty(max(api.bin_sort_workspace_size(n, W, H, capacity), 256),
                                   dtype=torch.uint8, device=dev)
         self.values = torch.empty((capacity,), dtype=torch.int32, device=dev)
-        self.bins = dict(values=self.values, tile_ranges=self.tile_ranges)
+        self.bins = dict(values=self.values, tile_ranges=self.tile_ranges,
+                         tile_order=self.tile_order)
 
     def project_and_bin(self, sync=False):
         api.project(self.cam, self.prm, **self.params, out=self.proj)
         b = api.bin_sort(self.cam.width, self.cam.height, self.proj, capacity=self.capacity,
                          workspace=self.bin_ws, values=self.values, tile_ranges=self.tile_ranges,
+                         tile_order=self.tile_order,
                          sync=sync)
         return b["n_isect"]
 

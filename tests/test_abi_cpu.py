@@ -119,7 +119,7 @@ def test_workspace_size_helpers_are_host_only(lib):
     assert lib.abcd_bin_sort_workspace_size(10, 0, 0, 16, C.byref(sz)) == 1
     assert lib.abcd_bin_sort_workspace_size(10, 1 << 33, 16, 16, C.byref(sz)) == 1
     assert lib.abcd_render_bwd_workspace_size(1000, C.byref(sz)) == 0
-    assert sz.value >= 9 * 4 * 1000 and sz.value % 256 == 0
+    assert sz.value >= 9 * 4 * 1000 + 8 * 32768 and sz.value % 256 == 0
 
 
 def test_bin_sort_rejects_small_or_misaligned_workspace(lib):
@@ -127,10 +127,11 @@ def test_bin_sort_rejects_small_or_misaligned_workspace(lib):
     lib.abcd_bin_sort_workspace_size(100, 1000, 64, 48, C.byref(need))
     m = C.c_int64(0)
     base = [64, 48, 100, FAKE, FAKE, FAKE, FAKE, 1000]
-    assert lib.abcd_bin_sort(*base, FAKE + 8, need.value, None, FAKE, FAKE, C.byref(m), None) == 1
-    assert lib.abcd_bin_sort(*base, FAKE, need.value - 1, None, FAKE, FAKE, C.byref(m), None) == 1
+    tail = [None, FAKE, FAKE, FAKE, C.byref(m), None]
+    assert lib.abcd_bin_sort(*base, FAKE + 8, need.value, *tail) == 1
+    assert lib.abcd_bin_sort(*base, FAKE, need.value - 1, *tail) == 1
     base[7] = -1  # negative capacity
-    assert lib.abcd_bin_sort(*base, FAKE, need.value, None, FAKE, FAKE, C.byref(m), None) == 1
+    assert lib.abcd_bin_sort(*base, FAKE, need.value, *tail) == 1
 
 
 def test_composite_rejects_bad_order(lib):
@@ -146,11 +147,11 @@ def test_composite_rejects_bad_order(lib):
 
 def test_render_calls_reject_bad_arguments(lib):
     c, p = _cam(), _prm()
-    args = [FAKE] * 11
+    args = [FAKE] * 12
     args[0] = None  # tile_ranges
     assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, None) == 1
-    args = [FAKE] * 11
-    args[5] = FAKE + 4  # F misaligned
+    args = [FAKE] * 12
+    args[6] = FAKE + 4  # F misaligned
     assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, None) == 1
     bwd = [FAKE] * 16 + [FAKE, 1 << 20] + [FAKE] * 6 + [0, None]
     bwd[13] = None  # final_T

@@ -124,6 +124,10 @@ def test_bin_sort_bitexact(api, case):
     assert np.array_equal(np32(b["values"][:m]).view(np.uint32), values)
     assert np.array_equal(np32(b["keys"][:m]).view(np.uint64), keys)
     assert np.array_equal(np32(b["tile_ranges"]).view(np.uint32), ranges)
+    # the forward's schedule: tiles by decreasing octave of list length, stable
+    length = (ranges[:, 1] - ranges[:, 0]).astype(np.int64)
+    octave = np.array([32 - int(x).bit_length() for x in length])
+    assert np.array_equal(np32(b["tile_order"]), np.argsort(octave, kind="stable"))
     # determinism: a second call gives identical bytes
     b2 = api.bin_sort(cam.width, cam.height, pd, want_keys=True)
     torch.cuda.synchronize()
@@ -173,6 +177,15 @@ def test_render_fwd_stage(api, case, with_fb):
     assert np.array_equal(np32(fw["last"]).view(np.uint32)[ok], ref["last"][ok])
     assert np.max(np.abs(np32(fw["final_T"]) - ref["final_T"])[ok]) <= FWD_TOL
     assert abs(int(nb.item()) - ref["n_blends"]) <= nk * 4
+    # the tile schedule changes no output: raster order gives identical bytes
+    nb2 = torch.zeros(1, dtype=torch.int64, device=dev())
+    fw2 = api.render_fwd(cam, prm, dict(bins, tile_order=None), pd,
+                         F=None if F is None else torch.from_numpy(F).to(dev()),
+                         B=None if B is None else torch.from_numpy(B).to(dev()), n_blends=nb2)
+    torch.cuda.synchronize()
+    for key in ("out", "final_T", "last"):
+        assert torch.equal(fw2[key], fw[key])
+    assert nb2.item() == nb.item()
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
@@ -311,6 +324,7 @@ def test_edge_cases_empty_block_and_culled(api):
     fw = api.render_fwd(cam, prm, bins, p, F=Fd, B=Bd)
     torch.cuda.synchronize()
     assert bins["n_isect"] == 0
+    assert np.array_equal(np32(bins["tile_order"]), np.arange(api.n_tiles(cam.width, cam.height)))
     exp = F.astype(np.float64) + (1 - F[..., 3:]) * B
     assert np.abs(np32(fw["out"]) - exp).max() <= FWD_TOL
     say("all culled (behind the camera)")
@@ -325,6 +339,7 @@ def test_edge_cases_empty_block_and_culled(api):
     grads = api.render_bwd(cam, prm, params, p, bins, fw, G, F=Fd, B=Bd)
     torch.cuda.synchronize()
     assert bins["n_isect"] == 0 and int(p["tiles_touched"].sum()) == 0
+    assert np.array_equal(np32(bins["tile_order"]), np.arange(api.n_tiles(cam.width, cam.height)))
     for v in grads.values():
         assert not torch.any(v != 0)
 
@@ -339,14 +354,15 @@ def test_capacity_overflow_leaves_outputs_untouched(api):
     m = full["n_isect"]
     values = torch.full((m - 1,), -7, dtype=torch.int32, device=dev())
     ranges = torch.full_like(full["tile_ranges"], -7)
+    order = torch.full_like(full["tile_order"], -7)
     with pytest.raises(AbcdError) as e:
-        _raw_bin(api, cam, p, m - 1, values, ranges)
+        _raw_bin(api, cam, p, m - 1, values, ranges, order)
     assert e.value.status == 2
     torch.cuda.synchronize()
-    assert torch.all(values == -7) and torch.all(ranges == -7)
+    assert torch.all(values == -7) and torch.all(ranges == -7) and torch.all(order == -7)
 
 
-def _raw_bin(api, cam, p, capacity, values, ranges):
+def _raw_bin(api, cam, p, capacity, values, ranges, order):
     """bin_sort without the binding's automatic regrow."""
     import ctypes as C
     from paper_2608_27735_amd import _lib
@@ -358,7 +374,8 @@ def _raw_bin(api, cam, p, capacity, values, ranges):
                                    p["radius"].data_ptr(), p["depth"].data_ptr(),
                                    p["tiles_touched"].data_ptr(), capacity, ws.data_ptr(),
                                    ws.numel(), None, values.data_ptr(), ranges.data_ptr(),
-                                   C.byref(m), torch.cuda.current_stream().cuda_stream)
+                                   order.data_ptr(), C.byref(m),
+                                   torch.cuda.current_stream().cuda_stream)
     _lib.check(st)
 
 
