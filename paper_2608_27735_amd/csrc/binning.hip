@@ -471,7 +471,8 @@ __global__ __launch_bounds__(256) void l1_scatter_kernel(
 // (x = l % 8, y = l / 8). For each bucket entry, in depth order, every lane
 // tests whether its tile lies in the entry's rectangle; counts and running
 // positions stay in registers. Sub-chunks of 256 entries are staged in LDS
-// (at most 256 x 64 entries) and leave as one coalesced run per tile.
+// as one-byte entry indices (at most 256 x 64 of them, 16 KB, so that eight
+// workgroups fit a CU) and leave as one coalesced run per tile.
 
 struct SubChunk {
   int bx, by;        // block
@@ -602,7 +603,8 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
     const uint32_t* __restrict__ c2, const uint32_t* __restrict__ tile_off,
     const WsHeader* __restrict__ hdr, uint32_t* __restrict__ values_sorted,
     unsigned long long* __restrict__ keys_sorted) {
-  __shared__ uint32_t stage[kSub * kBlkTiles];  // per tile, a run in depth order
+  __shared__ uint8_t stage[kSub * kBlkTiles];   // per tile, a run of sub-chunk entry indices
+  __shared__ uint32_t s_gid[kSub];               // Gaussian of each sub-chunk entry
   __shared__ uint32_t wcnt[4][kBlkTiles];       // per wave counts, then first slots
   __shared__ uint32_t soff[kBlkTiles + 1];      // run start of each tile in `stage`
   __shared__ uint32_t dst[kBlkTiles];           // global start of each tile's run
@@ -613,6 +615,7 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
     uint32_t g;
     int pk;
     load_entry(pairs, sc.e0 + threadIdx.x, sc.e1, g, pk);
+    s_gid[threadIdx.x] = g;
     uint32_t cnt = 0;
 #pragma unroll 8
     for (int l = 0; l < 64; ++l) cnt += lane_in(__builtin_amdgcn_readlane(pk, l), lx, ly);
@@ -652,8 +655,7 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
 #pragma unroll 8
     for (int l = 0; l < 64; ++l) {
       const int p = __builtin_amdgcn_readlane(pk, l);
-      const uint32_t gl = (uint32_t)__builtin_amdgcn_readlane((int)g, l);
-      if (lane_in(p, lx, ly)) stage[pos++] = gl;
+      if (lane_in(p, lx, ly)) stage[pos++] = (uint8_t)(64 * w + l);
     }
     __syncthreads();
     // write out: wave w copies the runs of tiles w, w + 4, ...
@@ -661,7 +663,7 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
       const uint32_t r0 = soff[lt], len = soff[lt + 1] - r0, d = dst[lt];
       const int t = (sc.by * kBlk + (lt >> 3)) * geo.ntx + (sc.bx * kBlk + (lt & 7));
       for (uint32_t i = lane; i < len; i += 64) {
-        const uint32_t gv = stage[r0 + i];
+        const uint32_t gv = s_gid[stage[r0 + i]];
         values_sorted[d + i] = gv;
         if (keys_sorted)
           keys_sorted[d + i] = ((unsigned long long)t << 32) | __float_as_uint(depth[gv]);

@@ -224,14 +224,59 @@ struct ShTile {
   static constexpr int kStride = kFloats + 1;  // odd stride: conflict-free LDS rows
 };
 
+// A full group issues all its loads before the first LDS write (one round
+// trip to memory instead of one per element); the last, partial group loops.
 template <int D>
 __device__ __forceinline__ void sh_stage_in(const float* __restrict__ sh, int64_t base, int cnt,
                                             float* s) {
   using Tl = ShTile<D>;
   const float* src = sh + base * Tl::kFloats;
+  if (cnt == kProjThreads) {
+    float v[Tl::kFloats];
+#pragma unroll
+    for (int r = 0; r < Tl::kFloats; ++r) v[r] = src[threadIdx.x + kProjThreads * r];
+#pragma unroll
+    for (int r = 0; r < Tl::kFloats; ++r) {
+      const int e = threadIdx.x + kProjThreads * r;
+      const int g = e / Tl::kFloats;
+      s[g * Tl::kStride + (e - g * Tl::kFloats)] = v[r];
+    }
+    return;
+  }
   for (int e = threadIdx.x; e < cnt * Tl::kFloats; e += kProjThreads) {
     const int g = e / Tl::kFloats;
     s[g * Tl::kStride + (e - g * Tl::kFloats)] = src[e];
+  }
+}
+
+// Coalesced write-out (or accumulation) of a group's LDS rows to dst.
+template <int D>
+__device__ __forceinline__ void sh_stage_out(const float* s, int cnt, int accumulate,
+                                             float* __restrict__ dst) {
+  using Tl = ShTile<D>;
+  if (cnt == kProjThreads) {
+    float v[Tl::kFloats];
+#pragma unroll
+    for (int r = 0; r < Tl::kFloats; ++r) {
+      const int e = threadIdx.x + kProjThreads * r;
+      const int g = e / Tl::kFloats;
+      v[r] = s[g * Tl::kStride + (e - g * Tl::kFloats)];
+    }
+    if (accumulate) {
+      float a[Tl::kFloats];
+#pragma unroll
+      for (int r = 0; r < Tl::kFloats; ++r) a[r] = dst[threadIdx.x + kProjThreads * r];
+#pragma unroll
+      for (int r = 0; r < Tl::kFloats; ++r) v[r] += a[r];
+    }
+#pragma unroll
+    for (int r = 0; r < Tl::kFloats; ++r) dst[threadIdx.x + kProjThreads * r] = v[r];
+    return;
+  }
+  for (int e = threadIdx.x; e < cnt * Tl::kFloats; e += kProjThreads) {
+    const int g = e / Tl::kFloats;
+    const float v = s[g * Tl::kStride + (e - g * Tl::kFloats)];
+    dst[e] = accumulate ? dst[e] + v : v;
   }
 }
 
@@ -246,13 +291,19 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(
   __shared__ float s_sh[kProjThreads * Tl::kStride];
   const int64_t base = (int64_t)blockIdx.x * kProjThreads;
   const int cnt = (int)min<int64_t>(kProjThreads, n - base);
+  const int64_t i = base + threadIdx.x;
+  // every global load of the thread is issued before the first wait
+  float mu[3] = {0.0f, 0.0f, 0.0f}, ls[3] = {0.0f, 0.0f, 0.0f}, ologit = 0.0f;
+  float4 q4 = make_float4(1.0f, 0.0f, 0.0f, 0.0f);
+  if (threadIdx.x < cnt) {
+    mu[0] = means[3 * i]; mu[1] = means[3 * i + 1]; mu[2] = means[3 * i + 2];
+    ls[0] = log_scales[3 * i]; ls[1] = log_scales[3 * i + 1]; ls[2] = log_scales[3 * i + 2];
+    q4 = *reinterpret_cast<const float4*>(quats + 4 * i);
+    ologit = opacity_logits[i];
+  }
   sh_stage_in<D>(sh, base, cnt, s_sh);
   __syncthreads();
-  const int64_t i = base + threadIdx.x;
   if (threadIdx.x >= cnt) return;
-  const float mu[3] = {means[3 * i], means[3 * i + 1], means[3 * i + 2]};
-  const float ls[3] = {log_scales[3 * i], log_scales[3 * i + 1], log_scales[3 * i + 2]};
-  const float4 q4 = *reinterpret_cast<const float4*>(quats + 4 * i);
   const float q[4] = {q4.x, q4.y, q4.z, q4.w};
   Proj pr;
   const bool vis = project_chain(cam, prm, ntx, nty, mu, ls, q, pr);
@@ -267,7 +318,7 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(
   }
   const float inv = 1.0f / pr.det;
   const float ca = pr.C * inv, cb = -pr.B * inv, cc = pr.A * inv;
-  const float o = 1.0f / (1.0f + __expf(-opacity_logits[i]));
+  const float o = 1.0f / (1.0f + __expf(-ologit));
   float dx = mu[0] - cam.campos[0], dy = mu[1] - cam.campos[1], dz = mu[2] - cam.campos[2];
   const float dn = rsqrtf(dx * dx + dy * dy + dz * dz);
   dx *= dn; dy *= dn; dz *= dn;
@@ -307,25 +358,34 @@ __global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
   __shared__ float s_sh[kProjThreads * Tl::kStride];
   const int64_t base = (int64_t)blockIdx.x * kProjThreads;
   const int cnt = (int)min<int64_t>(kProjThreads, n - base);
-  sh_stage_in<D>(sh, base, cnt, s_sh);
-  __syncthreads();
   const int64_t i = base + threadIdx.x;
   const bool live = threadIdx.x < cnt;
+  // every global load of the thread is issued before the first wait
+  float mu[3] = {0, 0, 0}, ls[3] = {0, 0, 0}, ologit = 0.0f, rad = 0.0f, G[9];
+  float4 q4 = make_float4(1.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+  for (int k = 0; k < 9; ++k) G[k] = 0.0f;
+  if (live) {
+    rad = radius[i];
+    mu[0] = means[3 * i]; mu[1] = means[3 * i + 1]; mu[2] = means[3 * i + 2];
+    ls[0] = log_scales[3 * i]; ls[1] = log_scales[3 * i + 1]; ls[2] = log_scales[3 * i + 2];
+    q4 = *reinterpret_cast<const float4*>(quats + 4 * i);
+    ologit = opacity_logits[i];
+#pragma unroll
+    for (int k = 0; k < 9; ++k) G[k] = g2d[9 * i + k];
+  }
+  sh_stage_in<D>(sh, base, cnt, s_sh);
+  __syncthreads();
   float* kk = s_sh + threadIdx.x * Tl::kStride;  // SH in, then dL/dSH out
   float gm[3] = {0, 0, 0}, gl[3] = {0, 0, 0}, gq[4] = {0, 0, 0, 0}, gop = 0.0f;
   float gu = 0.0f, gv = 0.0f;
   Proj pr;
-  bool vis = live && radius[i] > 0.0f;
-  float mu[3] = {0, 0, 0};
+  bool vis = live && rad > 0.0f;
   if (vis) {
-    mu[0] = means[3 * i]; mu[1] = means[3 * i + 1]; mu[2] = means[3 * i + 2];
-    const float ls[3] = {log_scales[3 * i], log_scales[3 * i + 1], log_scales[3 * i + 2]};
-    const float4 q4 = *reinterpret_cast<const float4*>(quats + 4 * i);
     const float q[4] = {q4.x, q4.y, q4.z, q4.w};
     vis = project_chain(cam, prm, ntx, nty, mu, ls, q, pr);
   }
   if (vis) {
-    const float* G = g2d + 9 * i;
     gu = G[0];
     gv = G[1];
     const float ga = G[2], gb = G[3], gc = G[4], go = G[5];
@@ -425,7 +485,7 @@ __global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
     gq[2] = (gy - y * dotq) * iq;
     gq[3] = (gz - z * dotq) * iq;
     // opacity
-    const float o = 1.0f / (1.0f + __expf(-opacity_logits[i]));
+    const float o = 1.0f / (1.0f + __expf(-ologit));
     gop = go * o * (1.0f - o);
     // colour: dL/dSH overwrites the thread's SH row in LDS after use
     const float d[3] = {mu[0] - cam.campos[0], mu[1] - cam.campos[1], mu[2] - cam.campos[2]};
@@ -479,12 +539,7 @@ __global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
   }
   __syncthreads();
   // coalesced write-out of dL/dSH
-  float* dst = d_sh + base * Tl::kFloats;
-  for (int e = threadIdx.x; e < cnt * Tl::kFloats; e += kProjThreads) {
-    const int g = e / Tl::kFloats;
-    const float v = s_sh[g * Tl::kStride + (e - g * Tl::kFloats)];
-    dst[e] = accumulate ? dst[e] + v : v;
-  }
+  sh_stage_out<D>(s_sh, cnt, accumulate, d_sh + base * Tl::kFloats);
 }
 
 }  // namespace

@@ -35,7 +35,7 @@ __device__ __forceinline__ uint32_t rank_in_wave(int key, Emit emit) {
   while (true) {
     const uint64_t act = __ballot(pending);
     if (!act) break;
-    const int kb = __shfl(key, __ffsll((unsigned long long)act) - 1, 64);
+    const int kb = __builtin_amdgcn_readlane(key, __ffsll((unsigned long long)act) - 1);
     const uint64_t same = __ballot(key == kb);
     if (key == kb) {
       rank = __popcll(same & below);
@@ -50,16 +50,20 @@ __global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
                                                                    const uint32_t* __restrict__ work,
                                                                    uint32_t* __restrict__ order,
                                                                    const uint32_t* __restrict__ skip) {
+  __shared__ uint8_t s_key[ABCD_MAX_TILES];
   __shared__ uint32_t s_base[kBuckets];
   __shared__ uint32_t s_wc[kOrderWaves][kBuckets];
   if (skip && *skip) return;
   const int tid = threadIdx.x, w = tid >> 6;
   if (tid < kBuckets) s_base[tid] = 0;
+  // all loads in flight at once; buckets kept in LDS for both passes
+#pragma unroll 8
+  for (int t = tid; t < ntiles; t += kOrderThreads) s_key[t] = (uint8_t)bucket_of(work[t]);
   __syncthreads();
   // bucket totals
   for (int t0 = 0; t0 < ntiles; t0 += kOrderThreads) {
     const int t = t0 + tid;
-    const int key = t < ntiles ? bucket_of(work[t]) : kNone;
+    const int key = t < ntiles ? s_key[t] : kNone;
     rank_in_wave(key, [&](int b, uint32_t c) { atomicAdd(&s_base[b], c); });
   }
   __syncthreads();
@@ -76,7 +80,7 @@ __global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
     for (int i = tid; i < kOrderWaves * kBuckets; i += kOrderThreads) (&s_wc[0][0])[i] = 0;
     __syncthreads();
     const int t = t0 + tid;
-    const int key = t < ntiles ? bucket_of(work[t]) : kNone;
+    const int key = t < ntiles ? s_key[t] : kNone;
     const uint32_t rank = rank_in_wave(key, [&](int b, uint32_t c) { s_wc[w][b] = c; });
     __syncthreads();
     if (key != kNone) {
