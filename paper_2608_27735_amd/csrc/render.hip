@@ -133,26 +133,37 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     // gathers of the next batch overlap the blend of this one
     const uint32_t nxt = b0 + 256 + tid;
     rec = load_rec(values, nxt, nxt < end, means2d, conic_opacity, rgb);
-    if (!done) {
+    if (__ballot(!done)) {
+      // Lanes step through the entries together without divergent branches:
+      // a lane that skips an entry, or has stopped, blends with weight 0.
+      // The next entry's LDS reads are issued before this entry's arithmetic.
+      int jl = -1;  // last entry of this batch the lane blended
+      float4 nga = s_ga[0], ngb = s_gb[0];
+      float nbl = s_bl[0];
       for (int j = 0; j < cnt; ++j) {
-        const float4 ga = s_ga[j];
-        const float4 gb = s_gb[j];
+        const float4 ga = nga, gb = ngb;
+        const float bl = nbl;
+        const int jn = j + 1 < cnt ? j + 1 : j;
+        nga = s_ga[jn];
+        ngb = s_gb[jn];
+        nbl = s_bl[jn];
         const AlphaEval ae = eval_alpha(fx - ga.x, fy - ga.y, ga.z, ga.w, gb.x, gb.y, k.alpha_min,
                                         k.alpha_max);
-        if (ae.skip) continue;
         const float Tn = T * (1.0f - ae.alpha);
-        if (Tn < k.t_min) {
-          done = true;
-          break;
-        }
-        const float wgt = ae.alpha * T;
+        const bool hit = !done && !ae.skip;
+        const bool stop = hit && Tn < k.t_min;
+        const bool blend = hit && !stop;
+        done = done || stop;
+        const float wgt = blend ? ae.alpha * T : 0.0f;
         cr += gb.z * wgt;
         cg += gb.w * wgt;
-        cb += s_bl[j] * wgt;
-        T = Tn;
-        lastk = (uint32_t)s_pos[j] + 1;
-        ++nb;
+        cb += bl * wgt;
+        T = blend ? Tn : T;
+        jl = blend ? j : jl;
+        nb += blend ? 1u : 0u;
+        if (!__ballot(!done)) break;  // wave-uniform
       }
+      if (jl >= 0) lastk = (uint32_t)s_pos[jl] + 1;
     }
     // s_wcnt is rewritten only after the next barrier
   }
@@ -299,53 +310,50 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
       const bool v = (uint32_t)tid < nxt_end - start;
       rec = load_rec(values, nxt_end - 1 - tid, v, means2d, conic_opacity, rgb);
     }
+    // The next entry's LDS reads are issued before this entry's arithmetic.
+    float4 nga = s_ga[0], ngb = s_gb[0], ngc = s_gc[0];
+    uint32_t nkk = (uint32_t)s_pos[0];
     for (int j = 0; j < cnt; ++j) {
-      const uint32_t kk = (uint32_t)s_pos[j];
+      const uint32_t kk = nkk;
+      const float4 ga = nga, gb = ngb, gc = ngc;
+      const int jn = j + 1 < cnt ? j + 1 : j;
+      nga = s_ga[jn];
+      ngb = s_gb[jn];
+      ngc = s_gc[jn];
+      nkk = (uint32_t)s_pos[jn];
       if (kk >= wml) continue;  // wave-uniform: no pixel of this wave reaches entry kk
+      const float dx = fx - ga.x, dy = fy - ga.y;
+      const AlphaEval ae = eval_alpha(dx, dy, ga.z, ga.w, gb.x, gb.y, k.alpha_min, k.alpha_max);
+      const bool contrib = kk < lastp && !ae.skip;
+      if (!__ballot(contrib)) continue;  // wave-uniform
+      // Branch-free per lane: a lane that does not blend this entry takes
+      // alpha = 0, which leaves T and R unchanged, and a zero mask on the
+      // alpha-derivative terms.
+      const float a = contrib ? ae.alpha : 0.0f;
+      const float om = 1.0f - a;
+      const float iom = __builtin_amdgcn_rcpf(om);  // om >= 1 - alpha_max > 0
+      const float Tk = T * iom;
+      const float wgt = a * Tk;
       float gr[9];
-      bool contrib = false;
-      if (kk < lastp) {
-        const float4 ga = s_ga[j];
-        const float4 gb = s_gb[j];
-        const float dx = fx - ga.x, dy = fy - ga.y;
-        const AlphaEval ae = eval_alpha(dx, dy, ga.z, ga.w, gb.x, gb.y, k.alpha_min, k.alpha_max);
-        if (!ae.skip) {
-          contrib = true;
-          const float4 gc = s_gc[j];
-          const float om = 1.0f - ae.alpha;
-          const float iom = __builtin_amdgcn_rcpf(om);  // om >= 1 - alpha_max > 0
-          const float Tk = T * iom;
-          const float wgt = ae.alpha * Tk;
-          gr[6] = wgt * gcr;
-          gr[7] = wgt * gcg;
-          gr[8] = wgt * gcb;
-          const float dLda = Tk * ((gb.z - Rr) * gcr + (gb.w - Rg) * gcg + (gc.w - Rb) * gcb) -
-                             (Tfin * iom) * gT;
-          Rr = ae.alpha * gb.z + om * Rr;
-          Rg = ae.alpha * gb.w + om * Rg;
-          Rb = ae.alpha * gc.w + om * Rb;
-          T = Tk;
-          if (ae.clamped) {
-            gr[0] = gr[1] = gr[2] = gr[3] = gr[4] = gr[5] = 0.0f;
-          } else {
-            const float gp = ae.alpha * dLda;
-            gr[5] = ae.e * dLda;
-            gr[0] = gp * (gc.x * dx + gc.y * dy);
-            gr[1] = gp * (gc.y * dx + gc.z * dy);
-            gr[2] = -0.5f * gp * dx * dx;
-            gr[3] = -gp * dx * dy;
-            gr[4] = -0.5f * gp * dy * dy;
-          }
-        }
-      }
-      if (__ballot(contrib)) {
-        if (!contrib) {
-#pragma unroll
-          for (int q = 0; q < 9; ++q) gr[q] = 0.0f;
-        }
-        const float v = wave_sum9(gr, lane);
-        if (lane < 9) atomicAdd(&s_acc[9 * j + slot], v);
-      }
+      gr[6] = wgt * gcr;
+      gr[7] = wgt * gcg;
+      gr[8] = wgt * gcb;
+      const float dLda = Tk * ((gb.z - Rr) * gcr + (gb.w - Rg) * gcg + (gc.w - Rb) * gcb) -
+                         (Tfin * iom) * gT;
+      Rr = a * gb.z + om * Rr;
+      Rg = a * gb.w + om * Rg;
+      Rb = a * gc.w + om * Rb;
+      T = Tk;
+      const float dm = (contrib && !ae.clamped) ? dLda : 0.0f;
+      const float gp = a * dm;
+      gr[5] = ae.e * dm;
+      gr[0] = gp * (gc.x * dx + gc.y * dy);
+      gr[1] = gp * (gc.y * dx + gc.z * dy);
+      gr[2] = -0.5f * gp * dx * dx;
+      gr[3] = -gp * dx * dy;
+      gr[4] = -0.5f * gp * dy * dy;
+      const float v = wave_sum9(gr, lane);
+      if (lane < 9) atomicAdd(&s_acc[9 * j + slot], v);
     }
     __syncthreads();
     if (tid < cnt) {
