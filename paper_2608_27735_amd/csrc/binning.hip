@@ -11,9 +11,11 @@
 //   level 1  Gaussians -> buckets of 8x8-tile blocks (a few per Gaussian)
 //   level 2  each block's bucket -> its 64 tile lists
 //
-// Both levels use the same ordered scatter: a wave walks its entries in depth
-// order and its lanes cover the distinct cells (blocks, tiles) of one
-// rectangle, so every write position is the pair's stable rank. Level 2 is
+// Both levels place every pair at its stable rank. Level 1: a wave visits the
+// distinct blocks its 256 entries cover in increasing block order, and ballots
+// rank the entries covering each block. Level 2: lane l of a wave owns local
+// tile l and walks the wave's 64 entries in depth order. Counts come from LDS
+// atomics (level 1) and 2D difference arrays (level 2). Level 2 is
 // split into sub-chunks of a bucket, each of which writes only 64 output
 // streams, so consecutive writes of a stream meet in L2 and leave it as whole
 // lines (a one-level scatter over all tiles of the frame writes every 4-byte
@@ -72,8 +74,8 @@ inline Geo geo_of(int width, int height) {
 }
 
 struct WsLayout {
-  size_t hdr, keys_a, keys_b, vals_a, vals_b, rects, hist, totals, c1, blk_total, blk_off, sub_off,
-      pairs, c2, tile_total, tile_off, total;
+  size_t hdr, keys_a, keys_b, vals_a, vals_b, rects, hist, totals, c1, cm, blk_total, blk_off,
+      sub_off, pairs, c2, tile_total, tile_off, total;
   int64_t rs_blocks, chunks, max_sub;
 };
 
@@ -98,6 +100,7 @@ WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
   L.hist = take(sizeof(uint32_t) * 256 * L.rs_blocks);
   L.totals = take(sizeof(uint32_t) * 256);
   L.c1 = take(sizeof(uint32_t) * (size_t)L.chunks * g.nblk);
+  L.cm = take(sizeof(uint32_t) * (size_t)L.chunks);
   L.blk_total = take(sizeof(uint32_t) * g.nblk);
   L.blk_off = take(sizeof(uint32_t) * (g.nblk + 1));
   L.sub_off = take(sizeof(uint32_t) * (g.nblk + 1));
@@ -293,23 +296,32 @@ __device__ __forceinline__ int pack_local(const Rect& r) {
   return r.x0 | (r.y0 << 3) | (r.x1 << 6) | (r.y1 << 9) | (1 << 12);
 }
 
-// cell -> (cx, cy) of a rectangle of width wr, row major; exact for cell < 2^22
-__device__ __forceinline__ void cell_xy(int cell, int wr, float inv_wr, int& cx, int& cy) {
-  int q = (int)((float)cell * inv_wr);
-  if (q * wr > cell) --q;
-  if ((q + 1) * wr <= cell) ++q;
-  cy = q;
-  cx = cell - q * wr;
-}
-
 // ------------------------------------------------------------- level 1
 
+constexpr uint32_t kNoBlock = 0xffffffffu;
+
+// Wave64 minimum with DPP row operations; the result is uniform.
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
+  const int no = (int)kNoBlock;
+  x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(no, (int)x, 0xB1, 0xF, 0xF, false));
+  x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(no, (int)x, 0x4E, 0xF, 0xF, false));
+  x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(no, (int)x, 0x141, 0xF, 0xF, false));
+  x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(no, (int)x, 0x140, 0xF, 0xF, false));
+  x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(no, (int)x, 0x142, 0xA, 0xF, false));
+  x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(no, (int)x, 0x143, 0xC, 0xF, false));
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+
+// Per chunk of 1024 depth ranks: block counts (c1 row) and the chunk's
+// intersection count (cm; at most 1024 x 32768, so 32 bits suffice).
 __global__ __launch_bounds__(256) void l1_count_kernel(
     int64_t n, const uint32_t* __restrict__ order, const unsigned long long* __restrict__ rects,
-    const uint32_t* __restrict__ tiles, Geo geo, uint32_t* __restrict__ c1,
-    WsHeader* __restrict__ hdr) {
+    Geo geo, uint32_t* __restrict__ c1, uint32_t* __restrict__ cm) {
   extern __shared__ uint32_t cnt[];  // [nblk]
+  __shared__ uint32_t s_m;
   for (int b = threadIdx.x; b < geo.nblk; b += blockDim.x) cnt[b] = 0;
+  if (threadIdx.x == 0) s_m = 0;
   __syncthreads();
   const int64_t r0 = (int64_t)blockIdx.x * kChunk;
   const int64_t r1 = min<int64_t>(n, r0 + kChunk);
@@ -323,8 +335,9 @@ __global__ __launch_bounds__(256) void l1_count_kernel(
       for (int x = b.x0; x <= b.x1; ++x) atomicAdd(&cnt[y * geo.nbx + x], 1u);
   }
   const unsigned int wm = wave_sum_u32(m);
-  if ((threadIdx.x & 63) == 0 && wm) atomicAdd(&hdr->m, (unsigned long long)wm);
+  if ((threadIdx.x & 63) == 0 && wm) atomicAdd(&s_m, wm);
   __syncthreads();
+  if (threadIdx.x == 0) cm[blockIdx.x] = s_m;
   uint32_t* out = c1 + (int64_t)blockIdx.x * geo.nblk;
   for (int b = threadIdx.x; b < geo.nblk; b += blockDim.x) out[b] = cnt[b];
 }
@@ -356,13 +369,29 @@ __global__ __launch_bounds__(1024) void scan_columns_kernel(uint32_t* __restrict
   }
 }
 
-// Bucket offsets, sub-chunk offsets and the overflow decision; one workgroup.
+// Intersection count M (sum of the chunk counts), bucket offsets, sub-chunk
+// offsets and the overflow decision; one workgroup.
 __global__ __launch_bounds__(kScanThreads) void l1_finish_kernel(
-    const uint32_t* __restrict__ blk_total, int nblk, unsigned long long capacity,
-    uint32_t* __restrict__ blk_off, uint32_t* __restrict__ sub_off, WsHeader* __restrict__ hdr) {
+    const uint32_t* __restrict__ blk_total, int nblk, const uint32_t* __restrict__ cm,
+    int64_t chunks, unsigned long long capacity, uint32_t* __restrict__ blk_off,
+    uint32_t* __restrict__ sub_off, WsHeader* __restrict__ hdr) {
   __shared__ unsigned long long part[kScanThreads];
   __shared__ unsigned long long spart[kScanThreads];
-  const unsigned long long m = hdr->m;
+  __shared__ unsigned long long s_m;
+  if (threadIdx.x == 0) s_m = 0;
+  __syncthreads();
+  unsigned long long mc = 0;
+  for (int64_t c = threadIdx.x; c < chunks; c += kScanThreads) mc += cm[c];
+  mc += __shfl_xor(mc, 32, 64);
+  mc += __shfl_xor(mc, 16, 64);
+  mc += __shfl_xor(mc, 8, 64);
+  mc += __shfl_xor(mc, 4, 64);
+  mc += __shfl_xor(mc, 2, 64);
+  mc += __shfl_xor(mc, 1, 64);
+  if ((threadIdx.x & 63) == 0) atomicAdd(&s_m, mc);
+  __syncthreads();
+  const unsigned long long m = s_m;
+  if (threadIdx.x == 0) hdr->m = m;
   const bool over = m > capacity || m >= (1ull << 32);
   const int per = (nblk + kScanThreads - 1) / kScanThreads;
   const int lo = min(nblk, per * (int)threadIdx.x), hi = min(nblk, lo + per);
@@ -437,31 +466,43 @@ __global__ __launch_bounds__(256) void l1_scatter_kernel(
     }
   }
   __syncthreads();
+  // Placement, one distinct block at a time in increasing block order: each
+  // entry walks its block rectangle row-major, so the smallest pending block
+  // of the wave is the current cell of every entry that covers it; ballots
+  // give each such entry its rank (entries in rank order: j, then lane).
+  uint32_t nb[4];
+  int cx[4], cy[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-#pragma unroll 1
-    for (int l = 0; l < 64; ++l) {
-      const int x0 = __builtin_amdgcn_readlane(bj[j].x0, l);
-      const int x1 = __builtin_amdgcn_readlane(bj[j].x1, l);
-      if (x1 < x0) continue;
-      const int y0 = __builtin_amdgcn_readlane(bj[j].y0, l);
-      const int y1 = __builtin_amdgcn_readlane(bj[j].y1, l);
-      const uint32_t g = (uint32_t)__builtin_amdgcn_readlane((int)gj[j], l);
-      const Rect t{__builtin_amdgcn_readlane(tj[j].x0, l), __builtin_amdgcn_readlane(tj[j].y0, l),
-                   __builtin_amdgcn_readlane(tj[j].x1, l), __builtin_amdgcn_readlane(tj[j].y1, l)};
-      const int wr = x1 - x0 + 1;
-      const int area = wr * (y1 - y0 + 1);
-      const float inv_wr = 1.0f / (float)wr;
-      for (int cell = lane; cell < area; cell += 64) {
-        int cx, cy;
-        cell_xy(cell, wr, inv_wr, cx, cy);
-        const int bx = x0 + cx, by = y0 + cy;
-        const uint32_t pos = atomicAdd(&my[by * geo.nbx + bx], 1u);
+    cx[j] = bj[j].x0;
+    cy[j] = bj[j].y0;
+    nb[j] = bj[j].x1 >= bj[j].x0 ? (uint32_t)(cy[j] * geo.nbx + cx[j]) : kNoBlock;
+  }
+  const uint64_t lt = lanemask_lt();
+  while (true) {
+    const uint32_t B = wave_min_u32(min(min(nb[0], nb[1]), min(nb[2], nb[3])));
+    if (B == kNoBlock) break;
+    uint32_t run = my[B];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool hit = nb[j] == B;
+      const uint64_t bal = __ballot(hit);
+      if (hit) {
         // the pair carries the rectangle clipped to its block, packed
-        pairs[pos] = (unsigned long long)g |
-                     ((unsigned long long)pack_local(clip_to_block(t, bx, by)) << 32);
+        pairs[run + __popcll(bal & lt)] =
+            (unsigned long long)gj[j] |
+            ((unsigned long long)pack_local(clip_to_block(tj[j], cx[j], cy[j])) << 32);
+        if (cx[j] < bj[j].x1) {
+          ++cx[j];
+        } else {
+          cx[j] = bj[j].x0;
+          ++cy[j];
+        }
+        nb[j] = cy[j] <= bj[j].y1 ? (uint32_t)(cy[j] * geo.nbx + cx[j]) : kNoBlock;
       }
+      run += (uint32_t)__popcll(bal);
     }
+    if (lane == 0) my[B] = run;
   }
 }
 
@@ -500,6 +541,35 @@ __device__ __forceinline__ bool lane_in(int packed, int lx, int ly) {
   return packed != 0 && lx >= x0 && lx <= x1 && ly >= y0 && ly <= y1;
 }
 
+// Coverage counts of a wave's entries per local tile by a 2D difference
+// array: an entry covering [x0, x1] x [y0, y1] adds +1 at (x0, y0), -1 at
+// (x1 + 1, y0) and (x0, y1 + 1), +1 at (x1 + 1, y1 + 1) (corners outside the
+// 8 x 8 block are dropped); the 2D inclusive prefix sum at tile (lx, ly) is
+// the number of entries covering it. d is the wave's 64-word LDS array,
+// zeroed by the caller; lane l returns the count of local tile l.
+__device__ __forceinline__ void diff_add(uint32_t* d, int packed) {
+  if (packed == 0) return;
+  const int x0 = packed & 7, y0 = (packed >> 3) & 7, x1 = (packed >> 6) & 7, y1 = (packed >> 9) & 7;
+  atomicAdd(&d[y0 * 8 + x0], 1u);
+  if (x1 < 7) atomicAdd(&d[y0 * 8 + x1 + 1], 0xffffffffu);
+  if (y1 < 7) atomicAdd(&d[(y1 + 1) * 8 + x0], 0xffffffffu);
+  if (x1 < 7 && y1 < 7) atomicAdd(&d[(y1 + 1) * 8 + x1 + 1], 1u);
+}
+
+__device__ __forceinline__ uint32_t diff_prefix(uint32_t v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 8; off <<= 1) {  // along the row (x)
+    const uint32_t t = __shfl_up(v, off, 8);
+    if ((lane & 7) >= off) v += t;
+  }
+#pragma unroll
+  for (int off = 8; off < 64; off <<= 1) {  // down the columns (y)
+    const uint32_t t = __shfl_up(v, off, 64);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
 __device__ __forceinline__ void load_entry(const unsigned long long* __restrict__ pairs,
                                            uint32_t e, uint32_t e1, uint32_t& g, int& packed) {
   g = 0;
@@ -516,8 +586,9 @@ __global__ __launch_bounds__(64) void l2_count_kernel(
     const unsigned long long* __restrict__ pairs, Geo geo, const uint32_t* __restrict__ sub_off,
     const uint32_t* __restrict__ blk_off, const WsHeader* __restrict__ hdr,
     uint32_t* __restrict__ c2) {
+  __shared__ uint32_t d[kBlkTiles];
   const uint32_t total = hdr->total_sub;
-  const int lane = threadIdx.x, lx = lane & 7, ly = lane >> 3;
+  const int lane = threadIdx.x;
   for (uint32_t s = blockIdx.x; s < total; s += gridDim.x) {
     const SubChunk sc = sub_chunk(s, sub_off, blk_off, geo);
     int pk[4];
@@ -526,12 +597,13 @@ __global__ __launch_bounds__(64) void l2_count_kernel(
       uint32_t g;
       load_entry(pairs, sc.e0 + lane + 64 * j, sc.e1, g, pk[j]);
     }
-    uint32_t cnt = 0;
+    d[lane] = 0;
+    __syncthreads();
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll 8
-      for (int l = 0; l < 64; ++l) cnt += lane_in(__builtin_amdgcn_readlane(pk[j], l), lx, ly);
-    c2[(int64_t)s * kBlkTiles + lane] = cnt;
+    for (int j = 0; j < 4; ++j) diff_add(d, pk[j]);
+    __syncthreads();
+    c2[(int64_t)s * kBlkTiles + lane] = diff_prefix(d[lane], lane);
+    __syncthreads();
   }
 }
 
@@ -606,6 +678,7 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
   __shared__ uint8_t stage[kSub * kBlkTiles];   // per tile, a run of sub-chunk entry indices
   __shared__ uint32_t s_gid[kSub];               // Gaussian of each sub-chunk entry
   __shared__ uint32_t wcnt[4][kBlkTiles];       // per wave counts, then first slots
+  __shared__ uint32_t wdiff[4][kBlkTiles];      // per wave difference arrays
   __shared__ uint32_t soff[kBlkTiles + 1];      // run start of each tile in `stage`
   __shared__ uint32_t dst[kBlkTiles];           // global start of each tile's run
   const uint32_t total = hdr->total_sub;
@@ -616,10 +689,11 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
     int pk;
     load_entry(pairs, sc.e0 + threadIdx.x, sc.e1, g, pk);
     s_gid[threadIdx.x] = g;
-    uint32_t cnt = 0;
-#pragma unroll 8
-    for (int l = 0; l < 64; ++l) cnt += lane_in(__builtin_amdgcn_readlane(pk, l), lx, ly);
-    wcnt[w][lane] = cnt;
+    wdiff[w][lane] = 0;
+    __syncthreads();
+    diff_add(wdiff[w], pk);
+    __syncthreads();
+    wcnt[w][lane] = diff_prefix(wdiff[w][lane], lane);
     __syncthreads();
     if (w == 0) {
       uint32_t c[4], tot = 0;
@@ -751,12 +825,13 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   uint32_t* c2 = u32(L.c2);
   uint32_t* tile_total = u32(L.tile_total);
   uint32_t* tile_off = u32(L.tile_off);
+  uint32_t* cm = u32(L.cm);
   ABCD_LAUNCH("l1_count", l1_count_kernel, L.chunks, kBlock, sizeof(uint32_t) * geo.nblk, stream, n,
-              order, rects, tiles_touched, geo, c1, hdr);
+              order, rects, geo, c1, cm);
   ABCD_LAUNCH("l1_scan_columns", scan_columns_kernel, (geo.nblk + 63) / 64, 1024, 0, stream, c1,
               L.chunks, geo.nblk, blk_total);
-  ABCD_LAUNCH("l1_finish", l1_finish_kernel, 1, kScanThreads, 0, stream, blk_total, geo.nblk, cap,
-              blk_off, sub_off, hdr);
+  ABCD_LAUNCH("l1_finish", l1_finish_kernel, 1, kScanThreads, 0, stream, blk_total, geo.nblk, cm,
+              L.chunks, cap, blk_off, sub_off, hdr);
   ABCD_LAUNCH("l1_scatter", l1_scatter_kernel, L.chunks, kBlock, 4 * sizeof(uint32_t) * geo.nblk,
               stream, n, order, rects, geo, c1, blk_off, hdr, pairs);
   ABCD_LAUNCH("l2_count", l2_count_kernel, 4 * kStrideGrid, 64, 0, stream, pairs, geo, sub_off,
