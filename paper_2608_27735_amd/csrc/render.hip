@@ -89,6 +89,9 @@ __device__ __forceinline__ int compact(bool keep, int* s_wcnt, int& pos) {
   return tot;
 }
 
+constexpr int kGroup = 8;
+constexpr int kBwdGroup = 8;  // the backward's group
+
 __global__ __launch_bounds__(256) void render_fwd_kernel(
     BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
     const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
@@ -137,30 +140,37 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
       // Lanes step through the entries together without divergent branches:
       // a lane that skips an entry, or has stopped, blends with weight 0.
       // The next entry's LDS reads are issued before this entry's arithmetic.
+      // Entries are read from LDS kGroup at a time, all reads issued before
+      // the first is used, so the LDS latency is paid once per group.
       int jl = -1;  // last entry of this batch the lane blended
-      float4 nga = s_ga[0], ngb = s_gb[0];
-      float nbl = s_bl[0];
-      for (int j = 0; j < cnt; ++j) {
-        const float4 ga = nga, gb = ngb;
-        const float bl = nbl;
-        const int jn = j + 1 < cnt ? j + 1 : j;
-        nga = s_ga[jn];
-        ngb = s_gb[jn];
-        nbl = s_bl[jn];
-        const AlphaEval ae = eval_alpha(fx - ga.x, fy - ga.y, ga.z, ga.w, gb.x, gb.y, k.alpha_min,
-                                        k.alpha_max);
-        const float Tn = T * (1.0f - ae.alpha);
-        const bool hit = !done && !ae.skip;
-        const bool stop = hit && Tn < k.t_min;
-        const bool blend = hit && !stop;
-        done = done || stop;
-        const float wgt = blend ? ae.alpha * T : 0.0f;
-        cr += gb.z * wgt;
-        cg += gb.w * wgt;
-        cb += bl * wgt;
-        T = blend ? Tn : T;
-        jl = blend ? j : jl;
-        nb += blend ? 1u : 0u;
+      for (int j0 = 0; j0 < cnt; j0 += kGroup) {
+        float4 ga[kGroup], gb[kGroup];
+        float bl[kGroup];
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) {
+          const int j = min(j0 + i, 255);
+          ga[i] = s_ga[j];
+          gb[i] = s_gb[j];
+          bl[i] = s_bl[j];
+        }
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) {
+          if (j0 + i >= cnt) break;  // wave-uniform
+          const AlphaEval ae = eval_alpha(fx - ga[i].x, fy - ga[i].y, ga[i].z, ga[i].w, gb[i].x,
+                                          gb[i].y, k.alpha_min, k.alpha_max);
+          const float Tn = T * (1.0f - ae.alpha);
+          const bool hit = !done && !ae.skip;
+          const bool stop = hit && Tn < k.t_min;
+          const bool blend = hit && !stop;
+          done = done || stop;
+          const float wgt = blend ? ae.alpha * T : 0.0f;
+          cr += gb[i].z * wgt;
+          cg += gb[i].w * wgt;
+          cb += bl[i] * wgt;
+          T = blend ? Tn : T;
+          jl = blend ? j0 + i : jl;
+          nb += blend ? 1u : 0u;
+        }
         if (!__ballot(!done)) break;  // wave-uniform
       }
       if (jl >= 0) lastk = (uint32_t)s_pos[jl] + 1;
@@ -197,12 +207,12 @@ __device__ __forceinline__ float dpp_mov(float x) {
 // first three exchanges a lane keeps half of its values and receives the
 // partner's partial sums of that half (quad xor 1, quad xor 2, row rotate 4),
 // the fourth pairs the survivor with the ninth value (row rotate 8), and two
-// cross-row swaps finish. A rotation by 4 (by 8) within a 16-lane row pairs
-// lanes that differ in bit 2 (bit 3) and agree in the lower bits, so partners
-// hold partial sums of the same values over disjoint lane sets. About 30
-// instructions instead of 9 separate six-step reductions. On return, lane
-// l < 16 holds the wave total of value sum9_slot(l); every row holds the same
-// totals.
+// cross-row swaps (v_permlane16_swap, v_permlane32_swap) finish. A rotation
+// by 4 (by 8) within a 16-lane row pairs lanes that differ in bit 2 (bit 3)
+// and agree in the lower bits, so partners hold partial sums of the same
+// values over disjoint lane sets. About 30 instructions, all VALU, instead of
+// 9 separate six-step reductions. On return, lane l < 16 holds the wave
+// total of value sum9_slot(l); every row holds the same totals.
 __device__ __forceinline__ float wave_sum9(const float (&g)[9], int lane) {
   const bool b0 = lane & 1, b1 = lane & 2, b2 = lane & 4, b3 = lane & 8;
   float a[4];
@@ -224,8 +234,19 @@ __device__ __forceinline__ float wave_sum9(const float (&g)[9], int lane) {
   const float c = (b2 ? b[1] : b[0]) + dpp_mov<0x124>(b2 ? b[0] : b[1]);
   v8 += dpp_mov<0x124>(v8);
   float d = (b3 ? v8 : c) + dpp_mov<0x128>(b3 ? c : v8);
-  d += __shfl_xor(d, 16, 64);
-  d += __shfl_xor(d, 32, 64);
+  // across rows: v_permlane16_swap / v_permlane32_swap exchange rows 0 <-> 1,
+  // 2 <-> 3 (halves 0 <-> 1); of the two registers each lane gets back, one
+  // is its own value and the other its partner's, so their sum is the pair sum
+  {
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_int(d), __float_as_int(d), false,
+                                                    false);
+    d = __int_as_float(p[0]) + __int_as_float(p[1]);
+  }
+  {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(d), __float_as_int(d), false,
+                                                    false);
+    d = __int_as_float(p[0]) + __int_as_float(p[1]);
+  }
   return d;
 }
 
@@ -276,7 +297,10 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
     if (lastp) atomicMax(&s_max, lastp);
   }
   const float Tfin = T;
-  float Rr = 0.0f, Rg = 0.0f, Rb = 0.0f;
+  // RG = sum over channels of gc_ch R_ch, where R is the colour accumulated
+  // behind the current entry (normalised by its transmittance): the
+  // alpha-derivative needs R only through this sum.
+  float RG = 0.0f;
   __syncthreads();
   const uint32_t nent = s_max;
   const int lane = tid & 63, slot = sum9_slot(lane & 15);
@@ -310,17 +334,25 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
       const bool v = (uint32_t)tid < nxt_end - start;
       rec = load_rec(values, nxt_end - 1 - tid, v, means2d, conic_opacity, rgb);
     }
-    // The next entry's LDS reads are issued before this entry's arithmetic.
-    float4 nga = s_ga[0], ngb = s_gb[0], ngc = s_gc[0];
-    uint32_t nkk = (uint32_t)s_pos[0];
-    for (int j = 0; j < cnt; ++j) {
-      const uint32_t kk = nkk;
-      const float4 ga = nga, gb = ngb, gc = ngc;
-      const int jn = j + 1 < cnt ? j + 1 : j;
-      nga = s_ga[jn];
-      ngb = s_gb[jn];
-      ngc = s_gc[jn];
-      nkk = (uint32_t)s_pos[jn];
+    // Entries are read from LDS kGroup at a time, all reads issued before the
+    // first is used, so the LDS latency is paid once per group.
+    for (int j0 = 0; j0 < cnt; j0 += kBwdGroup) {
+    float4 gav[kBwdGroup], gbv[kBwdGroup], gcv[kBwdGroup];
+    uint32_t kkv[kBwdGroup];
+#pragma unroll
+    for (int i = 0; i < kBwdGroup; ++i) {
+      const int j = min(j0 + i, 255);
+      gav[i] = s_ga[j];
+      gbv[i] = s_gb[j];
+      gcv[i] = s_gc[j];
+      kkv[i] = (uint32_t)s_pos[j];
+    }
+#pragma unroll
+    for (int i = 0; i < kBwdGroup; ++i) {
+      const int j = j0 + i;
+      if (j >= cnt) break;  // wave-uniform
+      const uint32_t kk = kkv[i];
+      const float4 ga = gav[i], gb = gbv[i], gc = gcv[i];
       if (kk >= wml) continue;  // wave-uniform: no pixel of this wave reaches entry kk
       const float dx = fx - ga.x, dy = fy - ga.y;
       const AlphaEval ae = eval_alpha(dx, dy, ga.z, ga.w, gb.x, gb.y, k.alpha_min, k.alpha_max);
@@ -338,31 +370,44 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
       gr[6] = wgt * gcr;
       gr[7] = wgt * gcg;
       gr[8] = wgt * gcb;
-      const float dLda = Tk * ((gb.z - Rr) * gcr + (gb.w - Rg) * gcg + (gc.w - Rb) * gcb) -
-                         (Tfin * iom) * gT;
-      Rr = a * gb.z + om * Rr;
-      Rg = a * gb.w + om * Rg;
-      Rb = a * gc.w + om * Rb;
+      const float CG = gb.z * gcr + gb.w * gcg + gc.w * gcb;
+      const float dLda = Tk * (CG - RG) - (Tfin * iom) * gT;
+      RG = a * CG + om * RG;
       T = Tk;
       const float dm = (contrib && !ae.clamped) ? dLda : 0.0f;
       const float gp = a * dm;
+      // first and second moments of gp over the pixels; the conic and the
+      // constant factors are applied once per entry at the flush
+      const float q = gp * dx, r = gp * dy;
+      gr[0] = q;
+      gr[1] = r;
+      gr[2] = q * dx;
+      gr[3] = q * dy;
+      gr[4] = r * dy;
       gr[5] = ae.e * dm;
-      gr[0] = gp * (gc.x * dx + gc.y * dy);
-      gr[1] = gp * (gc.y * dx + gc.z * dy);
-      gr[2] = -0.5f * gp * dx * dx;
-      gr[3] = -gp * dx * dy;
-      gr[4] = -0.5f * gp * dy * dy;
       const float v = wave_sum9(gr, lane);
       if (lane < 9) atomicAdd(&s_acc[9 * j + slot], v);
     }
+    }
     __syncthreads();
     if (tid < cnt) {
+      // moments -> dL/d(u, v, a, b, c): with q = dL/dpower * (dx, dy),
+      // d power / d(u, v) = (a dx + b dy, b dx + c dy), d power / d(a, b, c)
+      // = (-dx^2 / 2, -dx dy, -dy^2 / 2)
+      const float4 co = s_gc[tid];
+      float g[9];
+#pragma unroll
+      for (int q = 0; q < 9; ++q) g[q] = s_acc[9 * tid + q];
+      const float mx = g[0], my = g[1];
+      g[0] = co.x * mx + co.y * my;
+      g[1] = co.y * mx + co.z * my;
+      g[2] = -0.5f * g[2];
+      g[3] = -g[3];
+      g[4] = -0.5f * g[4];
       float* dst = g2d + 9 * (int64_t)s_g[tid];
 #pragma unroll
-      for (int q = 0; q < 9; ++q) {
-        const float v = s_acc[9 * tid + q];
-        if (v != 0.0f) atomicAdd(dst + q, v);
-      }
+      for (int q = 0; q < 9; ++q)
+        if (g[q] != 0.0f) atomicAdd(dst + q, g[q]);
     }
     bend = bbeg;
   }
