@@ -352,18 +352,30 @@ __global__ __launch_bounds__(1024) void scan_columns_kernel(uint32_t* __restrict
   const int c = blockIdx.x * 64 + lane;
   const int64_t per = (rows + 15) / 16;
   const int64_t q0 = min<int64_t>(rows, per * w), q1 = min<int64_t>(rows, q0 + per);
+  // rows are read eight at a time so that eight loads are in flight
   uint32_t s = 0;
   if (c < cols)
-    for (int64_t q = q0; q < q1; ++q) s += counts[q * cols + c];
+    for (int64_t q = q0; q < q1; q += 8) {
+      uint32_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? counts[(q + u) * cols + c] : 0u;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
   part[w][lane] = s;
   __syncthreads();
   uint32_t run = 0;
   for (int k = 0; k < w; ++k) run += part[k][lane];
   if (c < cols) {
-    for (int64_t q = q0; q < q1; ++q) {
-      const uint32_t v = counts[q * cols + c];
-      counts[q * cols + c] = run;
-      run += v;
+    for (int64_t q = q0; q < q1; q += 8) {
+      uint32_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? counts[(q + u) * cols + c] : 0u;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (q + u < q1) counts[(q + u) * cols + c] = run;
+        run += v[u];
+      }
     }
     if (w == 15) col_total[c] = run;
   }
@@ -619,16 +631,28 @@ __global__ __launch_bounds__(1024) void l2_scan_kernel(uint32_t* __restrict__ c2
   const uint32_t s0 = live ? sub_off[b] : 0u, s1 = live ? sub_off[b + 1] : 0u;
   const uint32_t per = (s1 - s0 + 15) / 16;
   const uint32_t q0 = min(s1, s0 + per * w), q1 = min(s1, q0 + per);
+  // rows are read eight at a time so that eight loads are in flight
   uint32_t sum = 0;
-  for (uint32_t q = q0; q < q1; ++q) sum += c2[(int64_t)q * kBlkTiles + lt];
+  for (uint32_t q = q0; q < q1; q += 8) {
+    uint32_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? c2[(int64_t)(q + u) * kBlkTiles + lt] : 0u;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) sum += v[u];
+  }
   part[w][lt] = sum;
   __syncthreads();
   uint32_t run = 0;
   for (int k = 0; k < w; ++k) run += part[k][lt];
-  for (uint32_t q = q0; q < q1; ++q) {
-    const uint32_t v = c2[(int64_t)q * kBlkTiles + lt];
-    c2[(int64_t)q * kBlkTiles + lt] = run;
-    run += v;
+  for (uint32_t q = q0; q < q1; q += 8) {
+    uint32_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? c2[(int64_t)(q + u) * kBlkTiles + lt] : 0u;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (q + u < q1) c2[(int64_t)(q + u) * kBlkTiles + lt] = run;
+      run += v[u];
+    }
   }
   if (w == 15) {
     const int bx = b % geo.nbx, by = b / geo.nbx;

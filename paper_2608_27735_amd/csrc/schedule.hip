@@ -19,31 +19,21 @@ namespace {
 constexpr int kOrderThreads = 1024;
 constexpr int kOrderWaves = kOrderThreads / 64;
 constexpr int kBuckets = 33;  // leading-zero count of the work, 32 for no work
-constexpr int kNone = 64;     // no tile
+constexpr int kNone = 64;     // no tile (matches no bucket)
 
 __device__ __forceinline__ int bucket_of(uint32_t work) { return work ? __clz(work) : 32; }
 
-// For each distinct bucket among the wave's lanes: the lanes holding it, and
-// this lane's rank among them. Returns per-lane rank; calls emit(bucket,
-// count) once per distinct bucket from lane 0.
-template <typename Emit>
-__device__ __forceinline__ uint32_t rank_in_wave(int key, Emit emit) {
-  const int l = threadIdx.x & 63;
-  const uint64_t below = (1ull << l) - 1ull;
-  uint32_t rank = 0;
-  bool pending = key != kNone;
-  while (true) {
-    const uint64_t act = __ballot(pending);
-    if (!act) break;
-    const int kb = __builtin_amdgcn_readlane(key, __ffsll((unsigned long long)act) - 1);
-    const uint64_t same = __ballot(key == kb);
-    if (key == kb) {
-      rank = __popcll(same & below);
-      pending = false;
-    }
-    if (l == 0) emit(kb, (uint32_t)__popcll(same));
+// Lanes of the calling wave holding the same bucket as this lane (buckets
+// below 64; kNone never matches a real bucket).
+__device__ __forceinline__ uint64_t match_bucket(int key) {
+  uint64_t peers = __ballot(1);
+#pragma unroll
+  for (int b = 0; b < 7; ++b) {
+    const bool bit = (key >> b) & 1;
+    const uint64_t m = __ballot(bit);
+    peers &= bit ? m : ~m;
   }
-  return rank;
+  return peers;
 }
 
 __global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
@@ -52,19 +42,21 @@ __global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
                                                                    const uint32_t* __restrict__ skip) {
   __shared__ uint8_t s_key[ABCD_MAX_TILES];
   __shared__ uint32_t s_base[kBuckets];
-  __shared__ uint32_t s_wc[kOrderWaves][kBuckets];
+  __shared__ uint32_t s_wc[kOrderWaves][kBuckets];  // per wave counts, then exclusive offsets
   if (skip && *skip) return;
-  const int tid = threadIdx.x, w = tid >> 6;
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+  const uint64_t below = (1ull << l) - 1ull;
   if (tid < kBuckets) s_base[tid] = 0;
   // all loads in flight at once; buckets kept in LDS for both passes
 #pragma unroll 8
   for (int t = tid; t < ntiles; t += kOrderThreads) s_key[t] = (uint8_t)bucket_of(work[t]);
   __syncthreads();
-  // bucket totals
+  // bucket totals: the first lane of each group of equal buckets adds the group
   for (int t0 = 0; t0 < ntiles; t0 += kOrderThreads) {
     const int t = t0 + tid;
     const int key = t < ntiles ? s_key[t] : kNone;
-    rank_in_wave(key, [&](int b, uint32_t c) { atomicAdd(&s_base[b], c); });
+    const uint64_t peers = match_bucket(key);
+    if (key != kNone && (peers & below) == 0) atomicAdd(&s_base[key], (uint32_t)__popcll(peers));
   }
   __syncthreads();
   if (tid == 0) {
@@ -81,19 +73,20 @@ __global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
     __syncthreads();
     const int t = t0 + tid;
     const int key = t < ntiles ? s_key[t] : kNone;
-    const uint32_t rank = rank_in_wave(key, [&](int b, uint32_t c) { s_wc[w][b] = c; });
+    const uint64_t peers = match_bucket(key);
+    if (key != kNone && (peers & below) == 0) s_wc[w][key] = (uint32_t)__popcll(peers);
     __syncthreads();
-    if (key != kNone) {
-      uint32_t off = s_base[key] + rank;
-      for (int v = 0; v < w; ++v) off += s_wc[v][key];
-      order[off] = (uint32_t)t;
+    if (tid < kBuckets) {  // exclusive offsets over the waves; advance the bucket base
+      uint32_t run = s_base[tid];
+      for (int v = 0; v < kOrderWaves; ++v) {
+        const uint32_t c = s_wc[v][tid];
+        s_wc[v][tid] = run;
+        run += c;
+      }
+      s_base[tid] = run;
     }
     __syncthreads();
-    if (tid < kBuckets) {
-      uint32_t c = 0;
-      for (int v = 0; v < kOrderWaves; ++v) c += s_wc[v][tid];
-      s_base[tid] += c;
-    }
+    if (key != kNone) order[s_wc[w][key] + __popcll(peers & below)] = (uint32_t)t;
     __syncthreads();
   }
 }
