@@ -168,15 +168,15 @@ __global__ __launch_bounds__(256) void radix_hist_kernel(const uint32_t* __restr
   h[threadIdx.x] = 0;
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * kRsTile;
-#pragma unroll 4
+  uint32_t d[kRsItems];
+#pragma unroll
   for (int it = 0; it < kRsItems; ++it) {
     const int64_t idx = base + it * kBlock + threadIdx.x;
-    if (idx < n) {
-      const uint32_t d = (keys[idx] >> shift) & 255u;
-      const uint64_t peers = match_digit(d, __ballot(1));
-      if (__lane_id() == __ffsll((unsigned long long)peers) - 1) atomicAdd(&h[d], (uint32_t)__popcll(peers));
-    }
+    d[it] = idx < n ? (keys[idx] >> shift) & 255u : 256u;
   }
+#pragma unroll
+  for (int it = 0; it < kRsItems; ++it)
+    if (d[it] < 256u) atomicAdd(&h[d[it]], 1u);
   __syncthreads();
   hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
 }
@@ -207,16 +207,26 @@ __global__ __launch_bounds__(256) void radix_scan_rows_kernel(uint32_t* __restri
   if (threadIdx.x == 0) totals[blockIdx.x] = carry;
 }
 
+// Stable scatter of one block of kRsTile keys. Wave w owns the contiguous
+// quarter [w kRsTile / 4, (w + 1) kRsTile / 4) of the block and walks it in
+// order, ranking each key among the wave's earlier keys of its digit (ballot
+// match + a per-wave running count in LDS); the waves' counts are then turned
+// into offsets (wave-major, after the digit's global base) and every key is
+// written once. Two barriers per block.
 __global__ __launch_bounds__(256) void radix_scatter_kernel(
     const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, int64_t n, int shift,
     const uint32_t* __restrict__ hist, int64_t nblocks, const uint32_t* __restrict__ totals,
     uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out) {
+  constexpr int kPerWave = kRsTile / 4;
+  constexpr int kWaveItems = kPerWave / 64;
   __shared__ uint32_t sbase[256];
   __shared__ uint32_t wcnt[4][256];
-  const int tid = threadIdx.x, w = tid >> 6;
-  // digit base = exclusive scan of the digit totals
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  // digit base = exclusive scan of the digit totals + this block's row prefix
   const uint32_t tot = totals[tid];
   sbase[tid] = tot;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) wcnt[k][tid] = 0;
   __syncthreads();
   for (int off = 1; off < 256; off <<= 1) {
     const uint32_t x = tid >= off ? sbase[tid - off] : 0u;
@@ -224,41 +234,45 @@ __global__ __launch_bounds__(256) void radix_scatter_kernel(
     sbase[tid] += x;
     __syncthreads();
   }
-  sbase[tid] += hist[(int64_t)tid * nblocks + blockIdx.x] - tot;
+  const uint32_t dbase = sbase[tid] - tot + hist[(int64_t)tid * nblocks + blockIdx.x];
+  const int64_t base = (int64_t)blockIdx.x * kRsTile + (int64_t)w * kPerWave;
+  uint32_t key[kWaveItems], val[kWaveItems], rank[kWaveItems];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) wcnt[k][tid] = 0;
-  const int64_t base = (int64_t)blockIdx.x * kRsTile;
-  uint32_t key[kRsItems], val[kRsItems];
-#pragma unroll
-  for (int it = 0; it < kRsItems; ++it) {
-    const int64_t idx = base + it * kBlock + tid;
+  for (int it = 0; it < kWaveItems; ++it) {
+    const int64_t idx = base + it * 64 + lane;
     key[it] = idx < n ? keys_in[idx] : 0u;
     val[it] = idx < n ? vals_in[idx] : 0u;
   }
+  const uint64_t lt = lanemask_lt();
+#pragma unroll
+  for (int it = 0; it < kWaveItems; ++it) {
+    const bool valid = base + it * 64 + lane < n;
+    const uint32_t d = (key[it] >> shift) & 255u;
+    const uint64_t peers = match_digit(d, __ballot(valid));
+    rank[it] = 0;
+    if (valid) {
+      rank[it] = wcnt[w][d] + __popcll(peers & lt);
+      if (lane == __ffsll((unsigned long long)peers) - 1) wcnt[w][d] += __popcll(peers);
+    }
+  }
+  __syncthreads();
+  {  // wave-major offsets of each digit
+    uint32_t run = dbase;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t c = wcnt[k][tid];
+      wcnt[k][tid] = run;
+      run += c;
+    }
+  }
   __syncthreads();
 #pragma unroll
-  for (int it = 0; it < kRsItems; ++it) {
-    const int64_t idx = base + it * kBlock + tid;
-    const bool valid = idx < n;
-    const uint32_t d = (key[it] >> shift) & 255u;
-    uint32_t rank = 0;
-    if (valid) {
-      const uint64_t peers = match_digit(d, __ballot(1));
-      rank = __popcll(peers & lanemask_lt());
-      if (__lane_id() == __ffsll((unsigned long long)peers) - 1) wcnt[w][d] = __popcll(peers);
-    }
-    __syncthreads();
-    if (valid) {
-      uint32_t pos = sbase[d] + rank;
-      for (int k = 0; k < w; ++k) pos += wcnt[k][d];
+  for (int it = 0; it < kWaveItems; ++it) {
+    if (base + it * 64 + lane < n) {
+      const uint32_t pos = wcnt[w][(key[it] >> shift) & 255u] + rank[it];
       keys_out[pos] = key[it];
       vals_out[pos] = val[it];
     }
-    __syncthreads();
-    sbase[tid] += wcnt[0][tid] + wcnt[1][tid] + wcnt[2][tid] + wcnt[3][tid];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) wcnt[k][tid] = 0;
-    __syncthreads();
   }
 }
 

@@ -139,7 +139,6 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     if (__ballot(!done)) {
       // Lanes step through the entries together without divergent branches:
       // a lane that skips an entry, or has stopped, blends with weight 0.
-      // The next entry's LDS reads are issued before this entry's arithmetic.
       // Entries are read from LDS kGroup at a time, all reads issued before
       // the first is used, so the LDS latency is paid once per group.
       int jl = -1;  // last entry of this batch the lane blended
