@@ -36,7 +36,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 KERNELS = ["composite", "project", "depth_keys", "radix_hist", "radix_scan", "radix_scatter",
            "l1_count", "l1_scan_columns", "l1_finish", "l1_scatter", "l2_count", "l2_scan",
            "bin_scan_tiles", "l2_scatter", "bin_tile_order", "render_fwd", "loss_l1", "zero_fill",
-           "bwd_order", "render_bwd", "project_bwd"]
+           "bwd_order", "render_bwd", "project_bwd", "adam"]
 
 
 def parse():
@@ -197,6 +197,27 @@ def main():
         if b is not None:
             d["algorithmic_GBs"] = b / d["launches_per_step"] / (d["ms_per_launch"] / 1e3) / 1e9
 
+    # the optimizer side of the step (reported beside the metric, not in it):
+    # one Adam update of the five parameter groups
+    exp_avg = {kk: torch.zeros_like(v) for kk, v in params.items()}
+    exp_avg_sq = {kk: torch.zeros_like(v) for kk, v in params.items()}
+    lrs = dict(means=1.6e-4, log_scales=5e-3, quats=1e-3, opacity_logits=5e-2, sh=2.5e-3)
+    for t in range(1, 4):
+        api.adam_step(params, st.grads, exp_avg, exp_avg_sq, lrs, t)
+    torch.cuda.synchronize()
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record()
+    for t in range(4, 4 + args.steps):
+        api.adam_step(params, st.grads, exp_avg, exp_avg_sq, lrs, t)
+    a1.record()
+    torch.cuda.synchronize()
+    adam_ms = a0.elapsed_time(a1) / args.steps
+    n_el = sum(v.numel() for v in params.values())
+    optimizer = dict(kernel="adam", ms_per_step=adam_ms, elements=n_el,
+                     algorithmic_GBs=28.0 * n_el / (adam_ms / 1e3) / 1e9,
+                     note="28 B per element (parameter, gradient, two moments read; "
+                          "parameter and moments written); not part of ms_per_step")
+
     if args.copy_calibration_mb:
         nbytes = args.copy_calibration_mb << 20
         src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
@@ -225,6 +246,7 @@ def main():
                    "sync_in_step": False},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "optimizer": optimizer,
         "kernels": kern,
         "setup_s": setup_s,
     }

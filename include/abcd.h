@@ -221,14 +221,40 @@ ABCD_API int32_t abcd_loss_l1_grad(int32_t width, int32_t height, const float* o
                           float* dL_dout, float* loss, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* Adam update of the active parameters after the backward (the step on the
+ * optimizer side; the paper trains with gradient steps but does not name the
+ * optimizer, the 3DGS line it builds on uses Adam with one learning rate per
+ * parameter group). For every element of every group, in place, fp32:
+ *   m = beta1 m + (1 - beta1) g;  v = beta2 v + (1 - beta2) g^2;
+ *   param -= lr (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps)
+ * (Kingma and Ba 2015, Algorithm 1). groups (host array of n_groups <=
+ * ABCD_ADAM_MAX_GROUPS): device arrays of `count` floats each; param,
+ * exp_avg (m) and exp_avg_sq (v) are read and written, grad is read; a group
+ * with count 0 is skipped. step >= 1 counts the updates made so far, this one
+ * included; 0 <= beta1, beta2 < 1; eps >= 0. One launch. */
+#define ABCD_ADAM_MAX_GROUPS 8
+typedef struct abcd_adam_group {
+  float* param;
+  const float* grad;
+  float* exp_avg;
+  float* exp_avg_sq;
+  int64_t count;
+  float lr;
+} abcd_adam_group;
+ABCD_API int32_t abcd_adam_step(const abcd_adam_group* groups /* host */, int32_t n_groups,
+                                float beta1, float beta2, float eps, int64_t step,
+                                hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Helpers. abcd_last_error: message of the last failure on this thread.
  * abcd_timing_*: optional per-kernel HIP-event timing of every launch made by
  * this thread (off by default; enabling it adds two event records per launch
  * on the caller's stream). abcd_timing_read synchronises, and returns the
  * accumulated milliseconds and launch count of the kernel named `kernel`
- * (names: project, project_bwd, depth_keys, radix_hist, radix_scan,
- * radix_scatter, bin_count, bin_scan_columns, bin_scan_tiles, bin_scatter,
- * render_fwd, render_bwd, zero_fill, composite, loss_l1). */
+ * (names: composite, project, depth_keys, radix_hist, radix_scan,
+ * radix_scatter, l1_count, l1_scan_columns, l1_finish, l1_scatter, l2_count,
+ * l2_scan, bin_scan_tiles, l2_scatter, bin_tile_order, render_fwd, loss_l1,
+ * zero_fill, bwd_order, render_bwd, project_bwd, adam). */
 ABCD_API const char* abcd_last_error(void);
 ABCD_API const char* abcd_version(void);
 ABCD_API const char* abcd_status_string(int32_t status);

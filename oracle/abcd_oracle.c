@@ -780,3 +780,14 @@ void orc_composite(int32_t width, int32_t height, int32_t k, const uint16_t* ima
     }
   }
 }
+
+void orc_adam(int64_t n, double* theta, const double* g, double* m, double* v, double lr,
+              double b1, double b2, double eps, int64_t t) {
+  const double c1 = 1.0 - pow(b1, (double)t), c2 = 1.0 - pow(b2, (double)t);
+  for (int64_t i = 0; i < n; i++) {
+    m[i] = b1 * m[i] + (1.0 - b1) * g[i];
+    v[i] = b2 * v[i] + (1.0 - b2) * g[i] * g[i];
+    const double mhat = m[i] / c1, vhat = v[i] / c2;
+    theta[i] = theta[i] - lr * mhat / (sqrt(vhat) + eps);
+  }
+}

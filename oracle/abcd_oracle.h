@@ -119,6 +119,15 @@ void orc_composite(int32_t width, int32_t height, int32_t k, const uint16_t* ima
 
 /* ---- helpers exposed for the pin tests --------------------------------- */
 
+/* Adam (Kingma and Ba, "Adam: A Method for Stochastic Optimization", 2015,
+ * Algorithm 1), one step t >= 1 on n elements, in place, fp64:
+ *   m = b1 m + (1 - b1) g;  v = b2 v + (1 - b2) g^2;
+ *   theta = theta - lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps).
+ * The paper does not name its optimizer; the 3DGS line it builds on uses Adam
+ * with a learning rate per parameter group, so the step takes one lr. */
+void orc_adam(int64_t n, double* theta, const double* g, double* m, double* v, double lr,
+              double b1, double b2, double eps, int64_t t);
+
 double orc_half_to_double(uint16_t h);
 /* real orthonormal SH basis Y_i(d), i = l^2 + l + m, 16 values; grad[3*i..] = dY_i/dd */
 void orc_sh_basis(const double* dir, double* y, double* grad);

@@ -84,6 +84,9 @@ def lib():
     L.orc_composite.argtypes = [C.c_int32, C.c_int32, C.c_int32, _u16p, _i32p, C.c_int32,
                                 _f64p, _f64p, C.c_int32]
     L.orc_composite.restype = None
+    L.orc_adam.argtypes = [C.c_int64, _f64p, _f64p, _f64p, _f64p, C.c_double, C.c_double,
+                           C.c_double, C.c_double, C.c_int64]
+    L.orc_adam.restype = None
     L.orc_half_to_double.argtypes = [C.c_uint16]
     L.orc_half_to_double.restype = C.c_double
     L.orc_sh_basis.argtypes = [_f64p, _f64p, _f64p]
@@ -246,6 +249,14 @@ def composite(width, height, images_f16, order, n_front, F=None, B=None):
 
 
 # ------------------------------------------------------------------- helpers
+
+def adam(theta, g, m, v, lr, b1=0.9, b2=0.999, eps=1e-15, t=1):
+    """One Adam step in fp64; returns (theta, m, v) (new arrays)."""
+    theta, m, v = (np.array(x, np.float64).ravel().copy() for x in (theta, m, v))
+    g = _c(np.asarray(g, np.float64).ravel(), np.float64)
+    lib().orc_adam(theta.size, theta, g, m, v, float(lr), float(b1), float(b2), float(eps), int(t))
+    return theta, m, v
+
 
 def sh_basis(direction):
     d = _c(direction, np.float64)

@@ -26,6 +26,14 @@ class abcd_raster_params(C.Structure):
                 ("sh_degree", C.c_int32), ("flags", C.c_uint32)]
 
 
+ADAM_MAX_GROUPS = 8
+
+
+class abcd_adam_group(C.Structure):
+    _fields_ = [("param", C.c_void_p), ("grad", C.c_void_p), ("exp_avg", C.c_void_p),
+                ("exp_avg_sq", C.c_void_p), ("count", C.c_int64), ("lr", C.c_float)]
+
+
 _P = C.c_void_p  # device pointers travel as integers
 _I32, _I64, _SZ = C.c_int32, C.c_int64, C.c_size_t
 _CAM, _PRM = C.POINTER(abcd_camera), C.POINTER(abcd_raster_params)
@@ -43,6 +51,8 @@ SIGNATURES = {
     "abcd_composite_cache": (_I32, [_I32, _I32, _I32, _P, C.POINTER(C.c_int32), _I32, _P, _P,
                                     _I32, _P]),
     "abcd_loss_l1_grad": (_I32, [_I32, _I32, _P, _P, C.POINTER(C.c_float), _P, _P, _P]),
+    "abcd_adam_step": (_I32, [C.POINTER(abcd_adam_group), _I32, C.c_float, C.c_float, C.c_float,
+                              _I64, _P]),
     "abcd_last_error": (C.c_char_p, []),
     "abcd_version": (C.c_char_p, []),
     "abcd_status_string": (C.c_char_p, [_I32]),

@@ -200,6 +200,30 @@ def render_bwd(cam, prm, params, proj, bins, fwd, dL_dout, F=None, B=None, works
     return grads
 
 
+# --------------------------------------------------------------- optimizer
+
+PARAM_GROUPS = ("means", "log_scales", "quats", "opacity_logits", "sh")
+
+
+def adam_step(params, grads, exp_avg, exp_avg_sq, lr, step, beta1=0.9, beta2=0.999, eps=1e-15):
+    """One Adam update of the parameter groups (dicts of fp32 GPU tensors, in
+    place); lr is a dict (one rate per group) or a float."""
+    names = [k for k in params if params[k].numel() > 0]
+    if len(names) > _lib.ADAM_MAX_GROUPS:
+        raise ValueError("too many parameter groups")
+    arr = (_lib.abcd_adam_group * max(len(names), 1))()
+    for i, k in enumerate(names):
+        for t, nm in ((params[k], "param"), (grads[k], "grad"), (exp_avg[k], "exp_avg"),
+                      (exp_avg_sq[k], "exp_avg_sq")):
+            _need(t, f"{nm}[{k}]", torch.float32, tuple(params[k].shape))
+        arr[i].param, arr[i].grad = _ptr(params[k]), _ptr(grads[k])
+        arr[i].exp_avg, arr[i].exp_avg_sq = _ptr(exp_avg[k]), _ptr(exp_avg_sq[k])
+        arr[i].count = params[k].numel()
+        arr[i].lr = float(lr[k] if isinstance(lr, dict) else lr)
+    check(_lib.load().abcd_adam_step(arr, len(names), float(beta1), float(beta2), float(eps),
+                                     int(step), _stream()))
+
+
 # ---------------------------------------------------------------- collapse
 
 def composite_cache(images, order, n_front, F=None, B=None, accumulate=False):
@@ -257,4 +281,4 @@ def timing_read(kernel):
 
 __all__ = ["AbcdError", "project", "bin_sort", "bin_sort_workspace_size", "render_fwd",
            "render_bwd", "render_bwd_workspace_size", "composite_cache", "loss_l1_grad",
-           "timing_enable", "timing_reset", "timing_read", "version", "n_tiles"]
+           "timing_enable", "timing_reset", "timing_read", "version", "n_tiles", "adam_step"]

@@ -218,6 +218,10 @@ int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, con
 int32_t launch_tile_walk(int width, int height, const uint32_t* last, uint32_t* work,
                          hipStream_t stream);
 
+// adam.hip
+int32_t launch_adam(const abcd_adam_group* groups, int ngroups, float beta1, float beta2, float eps,
+                    int64_t t, hipStream_t stream);
+
 // composite.hip
 int32_t launch_composite(int width, int height, int k, const uint16_t* images,
                          const int32_t* order, int n_front, float* F, float* B, int accumulate,

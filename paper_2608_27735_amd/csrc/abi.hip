@@ -299,6 +299,25 @@ int32_t abcd_loss_l1_grad(int32_t width, int32_t height, const float* out_rgba,
   return launch_loss_l1(width, height, out_rgba, target_rgb, b0, b1, b2, dL_dout, loss, stream);
 }
 
+int32_t abcd_adam_step(const abcd_adam_group* groups, int32_t n_groups, float beta1, float beta2,
+                       float eps, int64_t step, hipStream_t stream) {
+  REQUIRE(n_groups >= 0 && n_groups <= ABCD_ADAM_MAX_GROUPS, "n_groups must be in [0, %d]",
+          ABCD_ADAM_MAX_GROUPS);
+  REQUIRE(n_groups == 0 || groups != nullptr, "groups is NULL");
+  REQUIRE(beta1 >= 0.0f && beta1 < 1.0f && beta2 >= 0.0f && beta2 < 1.0f,
+          "beta1 and beta2 must be in [0, 1)");
+  REQUIRE(eps >= 0.0f && std::isfinite(eps), "eps must be finite and >= 0");
+  REQUIRE(step >= 1, "step must be >= 1");
+  for (int32_t i = 0; i < n_groups; ++i) {
+    const abcd_adam_group& g = groups[i];
+    REQUIRE(g.count >= 0, "group %d: count < 0", i);
+    REQUIRE(std::isfinite(g.lr), "group %d: lr is not finite", i);
+    if (g.count > 0)
+      REQUIRE(g.param && g.grad && g.exp_avg && g.exp_avg_sq, "group %d: array is NULL", i);
+  }
+  return launch_adam(groups, n_groups, beta1, beta2, eps, step, stream);
+}
+
 int32_t abcd_timing_enable(int32_t enable) {
   g_timing = enable != 0;
   return ABCD_OK;

@@ -159,3 +159,20 @@ def test_render_calls_reject_bad_arguments(lib):
     bwd = [FAKE] * 16 + [FAKE, 8] + [FAKE] * 6 + [0, None]  # workspace too small
     assert lib.abcd_render_bwd(C.byref(c), C.byref(p), 10, *bwd) == 1
     assert lib.abcd_loss_l1_grad(0, 8, FAKE, FAKE, None, FAKE, None, None) == 1
+
+
+def test_adam_rejects_bad_arguments(lib):
+    from paper_2608_27735_amd import _lib
+    g = (_lib.abcd_adam_group * 9)()
+    for i in range(9):
+        g[i].param = g[i].grad = g[i].exp_avg = g[i].exp_avg_sq = FAKE
+        g[i].count, g[i].lr = 16, 1e-3
+    assert lib.abcd_adam_step(g, 9, 0.9, 0.999, 1e-15, 1, None) == 1   # too many groups
+    assert lib.abcd_adam_step(g, 1, 1.0, 0.999, 1e-15, 1, None) == 1   # beta1 = 1
+    assert lib.abcd_adam_step(g, 1, 0.9, 0.999, -1.0, 1, None) == 1    # eps < 0
+    assert lib.abcd_adam_step(g, 1, 0.9, 0.999, 1e-15, 0, None) == 1   # step 0
+    g[0].grad = None
+    assert lib.abcd_adam_step(g, 1, 0.9, 0.999, 1e-15, 1, None) == 1   # NULL array
+    g[0].grad, g[0].count = FAKE, -1
+    assert lib.abcd_adam_step(g, 1, 0.9, 0.999, 1e-15, 1, None) == 1   # count < 0
+    assert lib.abcd_adam_step(None, 0, 0.9, 0.999, 1e-15, 1, None) == 0  # nothing to do

@@ -395,3 +395,52 @@ def test_loss_l1_gradient(api):
     exp = np.concatenate([s, -(s * np.array(bg)).sum(-1, keepdims=True)], -1)
     assert np.abs(np32(g) - exp).max() < 1e-9
     assert abs(loss.item() - np.abs(img - tgt).sum() / (3 * H * W)) < 1e-5
+
+
+def test_adam_step_matches_oracle(api):
+    """Three Adam steps on the five parameter groups of 1003 Gaussians plus an
+    unaligned group (scalar path), stage by stage against the fp64 oracle on the
+    GPU's own fp32 state. Bar: fp32 evaluation of the formulas, with the
+    rounding measured on the magnitudes of the terms (m = b1 m + (1 - b1) g can
+    cancel): each moment within 3e-7 of the sum of its terms' magnitudes, theta
+    within 4e-7 |theta| + 2e-6 (|update| + the same bound carried through the
+    moment)."""
+    r = S.rng(90)
+    n = 1003
+    shapes = dict(means=(n, 3), log_scales=(n, 3), quats=(n, 4), opacity_logits=(n,),
+                  sh=(n, 16, 3), odd=(1001,))
+    lr = dict(means=1.6e-4, log_scales=5e-3, quats=1e-3, opacity_logits=5e-2, sh=2.5e-3, odd=1e-2)
+    say("adam", n)
+
+    def mk(shape, scale=1.0):
+        return torch.from_numpy((scale * r.normal(size=shape)).astype(np.float32)).to(dev())
+
+    buf = {k: mk((int(np.prod(s)) + 1,)) for k, s in shapes.items()}
+    # the odd group lives one float past a 16-byte boundary
+    th = {k: (buf[k][1:] if k == "odd" else buf[k][:-1]).view(*shapes[k]) for k in shapes}
+    m = {k: torch.zeros_like(th[k]) for k in shapes}
+    v = {k: torch.zeros_like(th[k]) for k in shapes}
+    for t in (1, 2, 3):
+        g = {k: mk(shapes[k], 10.0 ** r.uniform(-4, 1)) for k in shapes}
+        before = {k: (th[k].cpu().numpy().astype(np.float64), m[k].cpu().numpy().astype(np.float64),
+                      v[k].cpu().numpy().astype(np.float64)) for k in shapes}
+        api.adam_step(th, g, m, v, lr, t, beta1=0.9, beta2=0.999, eps=1e-15)
+        torch.cuda.synchronize()
+        for k in shapes:
+            t0, m0, v0 = before[k]
+            # the hyperparameters the kernel receives are fp32
+            f32 = lambda x: float(np.float32(x))
+            rt, rm, rv = O.adam(t0, g[k].cpu().numpy(), m0, v0, f32(lr[k]), f32(0.9), f32(0.999),
+                                f32(1e-15), t)
+            gk = g[k].cpu().numpy().astype(np.float64).ravel()
+            mterm = f32(0.9) * np.abs(m0.ravel()) + (1 - f32(0.9)) * np.abs(gk)
+            vterm = f32(0.999) * v0.ravel() + (1 - f32(0.999)) * gk * gk
+            gm = m[k].cpu().numpy().astype(np.float64).ravel()
+            gv = v[k].cpu().numpy().astype(np.float64).ravel()
+            assert np.all(np.abs(gm - rm) <= 3e-7 * mterm), (k, t)
+            assert np.all(np.abs(gv - rv) <= 3e-7 * vterm), (k, t)
+            lr_t = f32(lr[k]) / (1 - f32(0.9) ** t)
+            denom = np.sqrt(rv / (1 - f32(0.999) ** t)) + f32(1e-15)
+            scale = np.abs(rt - t0.ravel()) + lr_t * mterm / denom
+            gt = th[k].cpu().numpy().astype(np.float64).ravel()
+            assert np.all(np.abs(gt - rt) <= 4e-7 * np.abs(rt) + 2e-6 * scale), (k, t)

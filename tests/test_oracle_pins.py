@@ -661,3 +661,38 @@ def test_split_gradient_equals_joint_gradient_and_frozen_blocks_vanish():
     hidden = O.step(cam, prm, act, F=Fo, B=B, dL_dout=w)
     for key in ("means", "log_scales", "quats", "opacity_logits", "sh"):
         assert not np.any(hidden["grads"][key]), key
+
+
+# ------------------------------------------------------------------- Adam
+# The optimizer is not named by the paper; the step follows Adam as published
+# (Kingma and Ba 2015, Algorithm 1). Pins: closed forms of the bias-corrected
+# moments, which a dropped bias correction, a swapped beta or a wrong sign
+# would break.
+
+def test_adam_first_step_is_normalised_gradient():
+    r = np.random.default_rng(3)
+    g = r.normal(size=50) * np.exp(r.uniform(-5, 5, 50))
+    theta = r.normal(size=50)
+    lr, eps = 0.01, 1e-8
+    th, m, v = O.adam(theta, g, np.zeros(50), np.zeros(50), lr, 0.9, 0.999, eps, 1)
+    # t = 1: m_hat = g and v_hat = g^2 exactly, so the step is lr g / (|g| + eps)
+    assert np.allclose(th, theta - lr * g / (np.abs(g) + eps), rtol=0, atol=1e-15)
+    assert np.allclose(m, 0.1 * g, rtol=1e-15) and np.allclose(v, 0.001 * g * g, rtol=1e-15)
+
+
+def test_adam_constant_gradient_keeps_unit_step():
+    # with a constant gradient the bias-corrected moments equal g and g^2 at
+    # every step, so every step moves theta by lr g / (|g| + eps)
+    g = np.array([2.0, -0.5, 1e-3, -7.0])
+    theta = np.zeros(4)
+    m, v = np.zeros(4), np.zeros(4)
+    lr, eps = 0.1, 1e-12
+    for t in range(1, 31):
+        theta, m, v = O.adam(theta, g, m, v, lr, 0.9, 0.999, eps, t)
+        assert np.allclose(theta, -t * lr * g / (np.abs(g) + eps), rtol=1e-12, atol=0)
+
+
+def test_adam_zero_gradient_from_rest_stays():
+    theta = np.array([1.0, -2.0, 3.0])
+    th, m, v = O.adam(theta, np.zeros(3), np.zeros(3), np.zeros(3), 0.5, 0.9, 0.999, 1e-15, 1)
+    assert np.array_equal(th, theta) and not m.any() and not v.any()
