@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--height", type=int, default=840)
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the CPU oracle on a sample")
     ap.add_argument("--profile-kernels", type=int, default=1)
+    ap.add_argument("--extras", type=int, default=1,
+                    help="also time the graph replay, the 128x128 workload, Adam and the cache "
+                         "refresh (0: only the step, e.g. under a profiler)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the steps, copy this many MiB device to device (a plain copy of "
                          "known size that scales the HBM byte counters)")
@@ -151,6 +154,32 @@ def main():
     blends_step = st.n_blends.item() / args.steps
     value = blends_step / (ms_step / 1e3)
 
+    graph = small = optimizer = cache_refresh = None
+    if args.extras:
+        # the same step replayed as one HIP graph (collapse + step captured once)
+        st.capture(target, F=F, B=B,
+                   before=lambda: api.composite_cache(images, order_idx, n_front, F=F, B=B))
+        for _ in range(args.warmup):
+            st.replay()
+        torch.cuda.synchronize()
+        st.n_blends.zero_()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record()
+        for _ in range(args.steps):
+            st.replay()
+        g1.record()
+        torch.cuda.synchronize()
+        ms_graph = g0.elapsed_time(g1) / args.steps
+        blends_graph = st.n_blends.item() / args.steps
+        graph = dict(ms_per_step=ms_graph, value=blends_graph / (ms_graph / 1e3),
+                     blends_per_step=blends_graph)
+
+        # launch-bound regime (Results section: small active partitions leave the
+        # rasterizer underused and launch costs dominate): the 512-Gaussian active
+        # cell of the 4,096-Gaussian 128x128 workload, eager launches vs one graph
+        # replay
+        small = small_config(api, S, ActiveBlockStep, dev, args.steps, args.warmup)
+
     # per-kernel durations: HIP events around every launch, on the launch stream
     kern = {}
     if args.profile_kernels:
@@ -197,26 +226,53 @@ def main():
         if b is not None:
             d["algorithmic_GBs"] = b / d["launches_per_step"] / (d["ms_per_launch"] / 1e3) / 1e9
 
-    # the optimizer side of the step (reported beside the metric, not in it):
-    # one Adam update of the five parameter groups
-    exp_avg = {kk: torch.zeros_like(v) for kk, v in params.items()}
-    exp_avg_sq = {kk: torch.zeros_like(v) for kk, v in params.items()}
-    lrs = dict(means=1.6e-4, log_scales=5e-3, quats=1e-3, opacity_logits=5e-2, sh=2.5e-3)
-    for t in range(1, 4):
-        api.adam_step(params, st.grads, exp_avg, exp_avg_sq, lrs, t)
-    torch.cuda.synchronize()
-    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a0.record()
-    for t in range(4, 4 + args.steps):
-        api.adam_step(params, st.grads, exp_avg, exp_avg_sq, lrs, t)
-    a1.record()
-    torch.cuda.synchronize()
-    adam_ms = a0.elapsed_time(a1) / args.steps
-    n_el = sum(v.numel() for v in params.values())
-    optimizer = dict(kernel="adam", ms_per_step=adam_ms, elements=n_el,
-                     algorithmic_GBs=28.0 * n_el / (adam_ms / 1e3) / 1e9,
-                     note="28 B per element (parameter, gradient, two moments read; "
-                          "parameter and moments written); not part of ms_per_step")
+    if args.extras:
+        # the optimizer side of the step (reported beside the metric, not in it):
+        # one Adam update of the five parameter groups
+        exp_avg = {kk: torch.zeros_like(v) for kk, v in params.items()}
+        exp_avg_sq = {kk: torch.zeros_like(v) for kk, v in params.items()}
+        lrs = dict(means=1.6e-4, log_scales=5e-3, quats=1e-3, opacity_logits=5e-2, sh=2.5e-3)
+        for t in range(1, 4):
+            api.adam_step(params, st.grads, exp_avg, exp_avg_sq, lrs, t)
+        torch.cuda.synchronize()
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record()
+        for t in range(4, 4 + args.steps):
+            api.adam_step(params, st.grads, exp_avg, exp_avg_sq, lrs, t)
+        a1.record()
+        torch.cuda.synchronize()
+        adam_ms = a0.elapsed_time(a1) / args.steps
+        n_el = sum(v.numel() for v in params.values())
+        optimizer = dict(kernel="adam", ms_per_step=adam_ms, elements=n_el,
+                         algorithmic_GBs=28.0 * n_el / (adam_ms / 1e3) / 1e9,
+                         note="28 B per element (parameter, gradient, two moments read; "
+                              "parameter and moments written); not part of ms_per_step")
+
+        # the cache refresh after a block's T updates (reported beside the metric):
+        # the block re-rendered for 8 cameras spread around the scene, fp16 images
+        # copied into pinned host memory, copies overlapped with the next render
+        from paper_2608_27735_amd.cache import CacheRefresher
+        rcams = w.cams[::len(w.cams) // 8][:8]
+        refresher = CacheRefresher(prm, params, cam.width, cam.height)
+        hosts = [torch.empty((cam.height, cam.width, 4), dtype=torch.float16).pin_memory()
+                 for _ in rcams]
+        refresher.refresh(rcams, hosts)  # sizes the binning buffers
+        torch.cuda.synchronize()
+        r0 = time.perf_counter()
+        refresher.refresh(rcams, hosts)
+        refresh_ms = (time.perf_counter() - r0) * 1e3 / len(rcams)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        for c in rcams:
+            refresher.render(c, refresher.staging[0])
+        c1.record()
+        torch.cuda.synchronize()
+        cache_refresh = dict(cameras=len(rcams), ms_per_camera=refresh_ms,
+                             render_ms_per_camera=c0.elapsed_time(c1) / len(rcams),
+                             image_bytes=cam.width * cam.height * 8,
+                             note="project, bin (intersection count read back), fp16 cached "
+                                  "render, async D2H into pinned memory; wall clock per camera")
+        del hosts
 
     if args.copy_calibration_mb:
         nbytes = args.copy_calibration_mb << 20
@@ -247,10 +303,45 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "optimizer": optimizer,
+        "graph": graph,
+        "cache_refresh": cache_refresh,
+        "small_config": small,
         "kernels": kern,
         "setup_s": setup_s,
     }
     print(json.dumps(out))
+
+
+def small_config(api, S, ActiveBlockStep, dev, steps, warmup):
+    import numpy as np
+    import torch
+    w = S.tiny()
+    cam, prm = w.cams[0], w.params
+    sub = S.subset(w.scene, w.cell_of == w.active)
+    params = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in sub.items()}
+    F0, B0 = S.background_pair(S.rng(4103), cam.height, cam.width)
+    F, B = torch.from_numpy(F0).to(dev), torch.from_numpy(B0).to(dev)
+    target = torch.from_numpy(w.target).to(dev)
+    st = ActiveBlockStep(cam, prm, params)
+    reps = max(steps, 50)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    eager = timed(lambda: st.step(target, F=F, B=B))
+    st.capture(target, F=F, B=B)
+    graph = timed(st.replay)
+    return dict(workload=f"{len(sub['means'])} active Gaussians (SH 0) at {cam.width}x{cam.height}",
+                eager_ms_per_step=eager, graph_ms_per_step=graph, steps=reps)
 
 
 def cpu_baseline(w, cam, prm, k):

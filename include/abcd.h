@@ -2,7 +2,7 @@
  * abcd.h -- C ABI of the ABCD active-block step on MI355X (gfx950).
  *
  * ABCD (Alpha-Composited Block Coordinate Descent) trains a radiance field one
- * spatial partition at a time: only the active partition is rendered; its
+ * spatial partition at a time: a step draws the active partition alone; its
  * image is composited between a foreground F and a background B that hold the
  * pre-accumulated renders of the frozen partitions in front of and behind it,
  * and gradients flow into the active parameters only (paper, Method section).
@@ -168,6 +168,20 @@ ABCD_API int32_t abcd_render_fwd(const abcd_camera* cam /* host */, const abcd_r
                         uint32_t* last, unsigned long long* n_blends, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* Cached render of a partition (Method section: the frozen partitions' renders
+ * are cached per camera and refreshed after the block they belong to has been
+ * trained): the forward above with F = B = transparent, written as
+ * premultiplied fp16 RGBA, image_f16[H][W][4] = binary16 (round to nearest
+ * even) of (C, 1 - T). Its input is that partition's projection and binning on
+ * the camera; its output feeds abcd_composite_cache. tile_order as in
+ * abcd_render_fwd (may be NULL). image_f16 8-byte aligned. */
+ABCD_API int32_t abcd_render_cache(const abcd_camera* cam /* host */,
+                          const abcd_raster_params* prm /* host */, const uint32_t* tile_ranges,
+                          const uint32_t* tile_order, const uint32_t* values_sorted,
+                          const float* means2d, const float* conic_opacity, const float* rgb,
+                          uint16_t* image_f16, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Backward (Method section: gradients are back-propagated only through the
  * active parameters; F and B are constants).
  *
@@ -195,8 +209,8 @@ ABCD_API int32_t abcd_render_bwd(const abcd_camera* cam /* host */, const abcd_r
 
 /* ------------------------------------------------------------------------ */
 /* Collapse of cached partition renders into F and B (Abstract; Method section:
- * cached renders of frozen partitions are composited into F and B according
- * to depth ordering).
+ * the stored renders of the frozen partitions are merged, front to back in
+ * their depth order, into the two layers).
  *
  * images: k premultiplied RGBA fp16 renders [k][H][W][4]. order (host): a
  * permutation of 0..k-1, front to back. F = images[order[0]] over ... over
@@ -254,7 +268,7 @@ ABCD_API int32_t abcd_adam_step(const abcd_adam_group* groups /* host */, int32_
  * (names: composite, project, depth_keys, radix_hist, radix_scan,
  * radix_scatter, l1_count, l1_scan_columns, l1_finish, l1_scatter, l2_count,
  * l2_scan, bin_scan_tiles, l2_scatter, bin_tile_order, render_fwd, loss_l1,
- * zero_fill, bwd_order, render_bwd, project_bwd, adam). */
+ * zero_fill, bwd_order, render_bwd, project_bwd, adam, render_cache). */
 ABCD_API const char* abcd_last_error(void);
 ABCD_API const char* abcd_version(void);
 ABCD_API const char* abcd_status_string(int32_t status);

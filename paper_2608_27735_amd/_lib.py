@@ -45,6 +45,7 @@ SIGNATURES = {
     "abcd_bin_sort": (_I32, [_I32, _I32, _I64, _P, _P, _P, _P, _I64, _P, _SZ, _P, _P, _P, _P,
                              C.POINTER(_I64), _P]),
     "abcd_render_fwd": (_I32, [_CAM, _PRM] + [_P] * 12 + [_P]),
+    "abcd_render_cache": (_I32, [_CAM, _PRM] + [_P] * 7 + [_P]),
     "abcd_render_bwd_workspace_size": (_I32, [_I64, C.POINTER(_SZ)]),
     "abcd_render_bwd": (_I32, [_CAM, _PRM, _I64] + [_P] * 5 + [_P] * 4 + [_P] * 2 + [_P] * 5 +
                         [_P, _SZ] + [_P] * 6 + [_I32, _P]),

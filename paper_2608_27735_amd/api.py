@@ -163,6 +163,21 @@ def render_fwd(cam, prm, bins, proj, F=None, B=None, n_blends=None, out=None):
     return out
 
 
+def render_cache(cam, prm, bins, proj, image=None):
+    """The partition rendered alone (F = B = transparent) as premultiplied fp16
+    RGBA [H, W, 4] (torch.float16), the form abcd_composite_cache consumes."""
+    H, W = cam.height, cam.width
+    if image is None:
+        image = _empty((H, W, 4), torch.float16, proj["means2d"].device)
+    _need(image, "image", torch.float16, (H, W, 4))
+    check(_lib.load().abcd_render_cache(
+        C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)),
+        _ptr(bins["tile_ranges"]), _ptr(bins.get("tile_order")), _ptr(bins["values"]),
+        _ptr(proj["means2d"]), _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]), _ptr(image),
+        _stream()))
+    return image
+
+
 def render_bwd_workspace_size(n):
     sz = C.c_size_t(0)
     check(_lib.load().abcd_render_bwd_workspace_size(n, C.byref(sz)))
@@ -281,4 +296,5 @@ def timing_read(kernel):
 
 __all__ = ["AbcdError", "project", "bin_sort", "bin_sort_workspace_size", "render_fwd",
            "render_bwd", "render_bwd_workspace_size", "composite_cache", "loss_l1_grad",
-           "timing_enable", "timing_reset", "timing_read", "version", "n_tiles", "adam_step"]
+           "timing_enable", "timing_reset", "timing_read", "version", "n_tiles", "adam_step",
+           "render_cache"]

@@ -199,6 +199,11 @@ int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
                           const float* F, const float* B, float* out_rgba, float* final_T,
                           uint32_t* last, unsigned long long* n_blends, const uint32_t* tile_order,
                           hipStream_t stream);
+int32_t launch_render_cache(const abcd_camera& cam, const abcd_raster_params& prm,
+                            const uint32_t* tile_ranges, const uint32_t* tile_order,
+                            const uint32_t* values_sorted, const float* means2d,
+                            const float* conic_opacity, const float* rgb, uint16_t* image_f16,
+                            hipStream_t stream);
 int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
                                  const uint32_t* tile_ranges, const uint32_t* values_sorted,
                                  const float* means2d, const float* conic_opacity,

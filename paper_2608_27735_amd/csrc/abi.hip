@@ -216,6 +216,22 @@ int32_t abcd_render_fwd(const abcd_camera* cam, const abcd_raster_params* prm,
                            B, out_rgba, final_T, last, n_blends, tile_order, stream);
 }
 
+int32_t abcd_render_cache(const abcd_camera* cam, const abcd_raster_params* prm,
+                          const uint32_t* tile_ranges, const uint32_t* tile_order,
+                          const uint32_t* values_sorted, const float* means2d,
+                          const float* conic_opacity, const float* rgb, uint16_t* image_f16,
+                          hipStream_t stream) {
+  TRY(check_camera(cam));
+  TRY(check_params(prm));
+  REQUIRE(tile_ranges && image_f16, "tile_ranges or image_f16 is NULL");
+  REQUIRE((reinterpret_cast<uintptr_t>(image_f16) & 7) == 0 &&
+              (reinterpret_cast<uintptr_t>(conic_opacity) & 15) == 0 &&
+              (reinterpret_cast<uintptr_t>(means2d) & 7) == 0,
+          "image_f16 and means2d must be 8-byte aligned, conic_opacity 16-byte aligned");
+  return launch_render_cache(*cam, *prm, tile_ranges, tile_order, values_sorted, means2d,
+                             conic_opacity, rgb, image_f16, stream);
+}
+
 int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes) {
   TRY(check_n(n));
   REQUIRE(bytes != nullptr, "bytes is NULL");

@@ -92,12 +92,16 @@ __device__ __forceinline__ int compact(bool keep, int* s_wcnt, int& pos) {
 constexpr int kGroup = 8;
 constexpr int kBwdGroup = 8;  // the backward's group
 
+// kHalf: the cached-render variant: F = B = transparent, the image is written
+// as fp16 RGBA to out16 (round to nearest even), no final T or walk lengths.
+template <bool kHalf>
 __global__ __launch_bounds__(256) void render_fwd_kernel(
     BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
     const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
     float4* __restrict__ out, float* __restrict__ final_T, uint32_t* __restrict__ last,
-    unsigned long long* __restrict__ n_blends, const uint32_t* __restrict__ order) {
+    unsigned long long* __restrict__ n_blends, const uint32_t* __restrict__ order,
+    uint2* __restrict__ out16) {
   __shared__ float4 s_ga[256];  // u, v, qa, qb
   __shared__ float4 s_gb[256];  // qc, o, r, g
   __shared__ float s_bl[256];   // b
@@ -178,13 +182,18 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
   }
   if (inside) {
     const int64_t p = (int64_t)py * k.width + px;
-    const float4 f = F ? F[p] : make_float4(0, 0, 0, 0);
-    const float4 bb = B ? B[p] : make_float4(0, 0, 0, 0);
-    const float s = 1.0f - f.w;
-    out[p] = make_float4(f.x + s * (cr + T * bb.x), f.y + s * (cg + T * bb.y),
-                         f.z + s * (cb + T * bb.z), f.w + s * (1.0f - T * (1.0f - bb.w)));
-    final_T[p] = T;
-    last[p] = lastk;
+    if (kHalf) {
+      const _Float16 h[4] = {(_Float16)cr, (_Float16)cg, (_Float16)cb, (_Float16)(1.0f - T)};
+      out16[p] = __builtin_bit_cast(uint2, h);
+    } else {
+      const float4 f = F ? F[p] : make_float4(0, 0, 0, 0);
+      const float4 bb = B ? B[p] : make_float4(0, 0, 0, 0);
+      const float s = 1.0f - f.w;
+      out[p] = make_float4(f.x + s * (cr + T * bb.x), f.y + s * (cg + T * bb.y),
+                           f.z + s * (cb + T * bb.z), f.w + s * (1.0f - T * (1.0f - bb.w)));
+      final_T[p] = T;
+      last[p] = lastk;
+    }
   }
   if (n_blends) {
     const unsigned long long wsum = wave_sum_u32(nb);
@@ -481,11 +490,26 @@ int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
                           hipStream_t stream) {
   const BlendConsts k = consts(cam, prm);
   const int grid = tile_order ? k.ntiles : 8 * k.per_xcd;
-  ABCD_LAUNCH("render_fwd", render_fwd_kernel, grid, kBlock, 0, stream, k, tile_ranges,
+  ABCD_LAUNCH("render_fwd", render_fwd_kernel<false>, grid, kBlock, 0, stream, k, tile_ranges,
               values_sorted, reinterpret_cast<const float2*>(means2d),
               reinterpret_cast<const float4*>(conic_opacity), rgb,
               reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B),
-              reinterpret_cast<float4*>(out_rgba), final_T, last, n_blends, tile_order);
+              reinterpret_cast<float4*>(out_rgba), final_T, last, n_blends, tile_order, nullptr);
+  ABCD_HIP(hipGetLastError());
+  return ABCD_OK;
+}
+
+int32_t launch_render_cache(const abcd_camera& cam, const abcd_raster_params& prm,
+                            const uint32_t* tile_ranges, const uint32_t* tile_order,
+                            const uint32_t* values_sorted, const float* means2d,
+                            const float* conic_opacity, const float* rgb, uint16_t* image_f16,
+                            hipStream_t stream) {
+  const BlendConsts k = consts(cam, prm);
+  const int grid = tile_order ? k.ntiles : 8 * k.per_xcd;
+  ABCD_LAUNCH("render_cache", render_fwd_kernel<true>, grid, kBlock, 0, stream, k, tile_ranges,
+              values_sorted, reinterpret_cast<const float2*>(means2d),
+              reinterpret_cast<const float4*>(conic_opacity), rgb, nullptr, nullptr, nullptr,
+              nullptr, nullptr, nullptr, tile_order, reinterpret_cast<uint2*>(image_f16));
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }

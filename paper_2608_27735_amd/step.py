@@ -79,3 +79,30 @@ class ActiveBlockStep:
         self.forward(F, B)
         self.loss_grad(target)
         return self.backward(self.dL_dout, F, B)
+
+    def capture(self, target, F=None, B=None, before=None):
+        """Record one step (and `before()`, e.g. the F/B collapse, ahead of it)
+        as a HIP graph; replay() then launches the whole step at once. Every
+        buffer the step touches is owned here or passed in, so a replay reads
+        the current contents of params, target, F and B. The graph holds no
+        memset nodes: the library clears with its own fill kernel."""
+        def body():
+            if before is not None:
+                before()
+            self.step(target, F, B)
+
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            body()  # one eager pass on the capture stream first
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            body()
+        self.graph = graph
+        return graph
+
+    def replay(self):
+        """Launch the captured step on the current stream."""
+        self.graph.replay()
+        return self.grads

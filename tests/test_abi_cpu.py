@@ -153,6 +153,12 @@ def test_render_calls_reject_bad_arguments(lib):
     args = [FAKE] * 12
     args[6] = FAKE + 4  # F misaligned
     assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, None) == 1
+    cache = [FAKE] * 7
+    cache[6] = None  # image
+    assert lib.abcd_render_cache(C.byref(c), C.byref(p), *cache, None) == 1
+    cache = [FAKE] * 7
+    cache[6] = FAKE + 2  # image misaligned
+    assert lib.abcd_render_cache(C.byref(c), C.byref(p), *cache, None) == 1
     bwd = [FAKE] * 16 + [FAKE, 1 << 20] + [FAKE] * 6 + [0, None]
     bwd[13] = None  # final_T
     assert lib.abcd_render_bwd(C.byref(c), C.byref(p), 10, *bwd) == 1

@@ -189,6 +189,86 @@ def test_render_fwd_stage(api, case, with_fb):
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_render_cache_refresh(api, case):
+    """The cached render of a partition: the forward with F = B = transparent
+    as fp16 premultiplied RGBA. Against the fp64 oracle: off the knife-edge
+    pixels within FWD_TOL plus half an fp16 ulp (the rounding of the store);
+    against the fp32 forward of the same bins: bit-identical after numpy's
+    round-to-nearest-even conversion."""
+    name, cam, prm, scene = case
+    say("render_cache", name)
+    ob, proj = _oracle_inputs_f32(cam, prm, scene)
+    _, values, ranges = O.bin(cam.width, cam.height, ob["depth"], ob["rect"], ob["tiles_touched"])
+    ref = O.render_fwd(cam, prm, ranges, values, proj["means2d"].astype(np.float64),
+                       proj["conic_opacity"][:, :3].astype(np.float64),
+                       proj["conic_opacity"][:, 3].astype(np.float64),
+                       proj["rgb"].astype(np.float64), None, None, rel_margin=KNIFE)
+    pd = to_dev(proj)
+    bins = api.bin_sort(cam.width, cam.height, pd)
+    img = torch.full((cam.height, cam.width, 4), float("nan"), dtype=torch.float16, device=dev())
+    api.render_cache(cam, prm, bins, pd, image=img)
+    fw = api.render_fwd(cam, prm, bins, pd)
+    torch.cuda.synchronize()
+    got = img.cpu().numpy()
+    assert np.array_equal(got.view(np.uint16), np32(fw["out"]).astype(np.float16).view(np.uint16))
+    g64 = got.astype(np.float64)
+    half_ulp = np.spacing(np.abs(got)).astype(np.float64) / 2
+    ok = ~ref["knife"]
+    excess = (np.abs(g64 - ref["out"]) - half_ulp)[ok]
+    print(f"  max error beyond the fp16 rounding {excess.max(initial=0.0):.2e}")
+    assert excess.max(initial=0.0) <= FWD_TOL
+    assert np.abs(g64 - ref["out"])[ref["knife"]].max(initial=0.0) <= 0.02
+
+
+def test_render_cache_feeds_composite(api):
+    """Cached renders of two partitions composited back over: equal to the
+    forward of the middle partition between them (fp16 storage error only)."""
+    r = S.ring()
+    cam, prm = r.cams[2], r.params
+    lab = S.rng(13).integers(0, 3, len(r.scene["means"]))
+    say("render_cache -> composite", len(lab))
+
+    def prep(sc):
+        _, proj = _oracle_inputs_f32(cam, prm, sc)
+        pd = to_dev(proj)
+        return pd, api.bin_sort(cam.width, cam.height, pd)
+
+    parts = [prep(S.subset(r.scene, lab == i)) for i in range(3)]
+    imgs = torch.stack([api.render_cache(cam, prm, b, pd) for pd, b in (parts[0], parts[2])])
+    F, B = api.composite_cache(imgs.view(torch.int16), [0, 1], 1)
+    mid = api.render_fwd(cam, prm, parts[1][1], parts[1][0], F=F, B=B)
+    ref = api.render_fwd(cam, prm, parts[1][1], parts[1][0],
+                         F=api.render_fwd(cam, prm, parts[0][1], parts[0][0])["out"],
+                         B=api.render_fwd(cam, prm, parts[2][1], parts[2][0])["out"])
+    torch.cuda.synchronize()
+    assert (mid["out"] - ref["out"]).abs().max().item() <= 2e-3
+
+
+def test_cache_refresh_to_pinned_host(api):
+    """Refresh of a partition's renders for several cameras (binning buffers
+    grown on the way, double-buffered device staging, copies on a second
+    stream): every host image equals that camera's own cached render."""
+    from paper_2608_27735_amd.cache import CacheRefresher
+    r = S.ring()
+    prm = r.params
+    sc = S.subset(r.scene, r.cell_of == r.active)
+    cams = [r.cams[i] for i in (0, 3, 5, 1, 3)]
+    say("cache refresh", len(cams), "cameras", sc["means"].shape)
+    params = to_dev(sc)
+    H, W = cams[0].height, cams[0].width
+    hosts = [torch.full((H, W, 4), float("nan"), dtype=torch.float16).pin_memory()
+             for _ in cams]
+    ref = CacheRefresher(prm, params, W, H)
+    ref.refresh(cams, hosts)
+    for cam, h in zip(cams, hosts):
+        pd = api.project(cam, prm, **params)
+        bins = api.bin_sort(W, H, pd)
+        want = api.render_cache(cam, prm, bins, pd).cpu()
+        assert torch.equal(h.view(torch.int16), want.view(torch.int16))
+    assert any(h.float().abs().sum() > 0 for h in hosts)
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_step_end_to_end(api, case):
     """Parameters -> composited image and parameter gradients, both sides from
     the same seeded parameters, F, B and upstream gradient."""
@@ -444,3 +524,46 @@ def test_adam_step_matches_oracle(api):
             scale = np.abs(rt - t0.ravel()) + lr_t * mterm / denom
             gt = th[k].cpu().numpy().astype(np.float64).ravel()
             assert np.all(np.abs(gt - rt) <= 4e-7 * np.abs(rt) + 2e-6 * scale), (k, t)
+
+
+def test_step_graph_replays_match_eager(api):
+    """The step captured as a HIP graph: four replays, each after eager work
+    that rewrites the parameters, F and B in place (and a synchronisation),
+    each checked against an eager step on the same inputs."""
+    from paper_2608_27735_amd.step import ActiveBlockStep
+    r = S.ring()
+    cam, prm = r.cams[2], r.params
+    scene = S.subset(r.scene, r.cell_of == r.active)
+    say("graph replay", scene["means"].shape)
+    rr = S.rng(91)
+    params = to_dev(scene)
+    F0, B0 = S.background_pair(rr, cam.height, cam.width)
+    F, B = torch.from_numpy(F0).to(dev()), torch.from_numpy(B0).to(dev())
+    target = torch.from_numpy(rr.uniform(0, 1, (cam.height, cam.width, 3)).astype(np.float32)).to(dev())
+    g_step = ActiveBlockStep(cam, prm, params)
+    e_params = {k: v.clone() for k, v in params.items()}
+    e_step = ActiveBlockStep(cam, prm, e_params, capacity=g_step.capacity)
+    g_step.capture(target, F=F, B=B)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        # eager work between replays: new parameters and F/B, same for both steps
+        with torch.no_grad():
+            params["means"].add_(0.01 * torch.randn_like(params["means"]))
+            params["opacity_logits"].mul_(0.9)
+            F.mul_(0.95)
+            B.mul_(0.97)
+            for k in params:
+                e_params[k].copy_(params[k])
+        torch.cuda.synchronize()
+        gg = g_step.replay()
+        torch.cuda.synchronize()
+        eg = e_step.step(target, F=F, B=B)
+        torch.cuda.synchronize()
+        assert torch.equal(g_step.fwd["out"], e_step.fwd["out"]), rep
+        assert torch.equal(g_step.fwd["last"], e_step.fwd["last"]), rep
+        assert torch.equal(g_step.values[:g_step.tile_ranges[-1, 1]],
+                           e_step.values[:e_step.tile_ranges[-1, 1]]), rep
+        for k in ("means", "log_scales", "quats", "opacity_logits", "sh"):
+            rel = (torch.linalg.norm((gg[k] - eg[k]).double()) /
+                   torch.linalg.norm(eg[k].double()).clamp_min(1e-30)).item()
+            assert rel <= 1e-5, (rep, k, rel)  # same kernels; atomics order differs
