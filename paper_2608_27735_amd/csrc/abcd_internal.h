@@ -191,7 +191,7 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
                         void* workspace, uint64_t* keys_sorted, uint32_t* values_sorted,
                         uint32_t* tile_ranges, uint32_t* tile_order, hipStream_t stream);
 
-// render.hip
+// render_fwd.hip, render_bwd.hip, loss.hip
 size_t render_bwd_workspace_bytes(int64_t n);
 int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
                           const uint32_t* tile_ranges, const uint32_t* values_sorted,

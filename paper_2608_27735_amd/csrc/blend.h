@@ -1,0 +1,109 @@
+// blend.h -- pieces shared by the forward and backward tile blend kernels:
+// the launch constants, the tile schedule lookup, list-entry loads, the
+// tile's pixel-centre box and the block-wide compaction of staged entries.
+//
+// One 256-thread workgroup (4 wave64) per 16x16 tile, one thread per pixel.
+// Gaussians of the tile's depth-sorted list are staged through LDS in batches
+// of 256; an entry is kept only if its alpha >= alpha_min ellipse reaches the
+// tile's pixel-centre box.
+#pragma once
+
+#include "abcd_internal.h"
+
+namespace abcd {
+namespace {
+
+
+struct BlendConsts {
+  int width, height, ntx, ntiles, per_xcd;
+  float alpha_min, alpha_max, t_min;
+};
+
+// Tile of this workgroup: the given schedule (heaviest tiles first), or, with
+// none, raster order with each of the 8 XCDs (which take workgroups round
+// robin) given a contiguous band of tiles, so that neighbouring tiles (which
+// share Gaussians) share an L2.
+__device__ __forceinline__ int tile_of_block(const BlendConsts& k, const uint32_t* order) {
+  const int b = blockIdx.x;
+  if (order) return (int)order[b];
+  return (b & 7) * k.per_xcd + (b >> 3);
+}
+
+// One list entry as loaded from global memory by one thread.
+struct Rec {
+  float2 m;
+  float4 co;
+  float r, g, b;
+  uint32_t gid;
+  bool valid;
+};
+
+__device__ __forceinline__ Rec load_rec(const uint32_t* __restrict__ values, uint32_t idx,
+                                        bool valid, const float2* __restrict__ means2d,
+                                        const float4* __restrict__ conic_opacity,
+                                        const float* __restrict__ rgb) {
+  Rec r;
+  r.valid = valid;
+  r.gid = 0;
+  if (valid) {
+    r.gid = values[idx];
+    r.m = means2d[r.gid];
+    r.co = conic_opacity[r.gid];
+    r.r = rgb[3 * r.gid];
+    r.g = rgb[3 * r.gid + 1];
+    r.b = rgb[3 * r.gid + 2];
+  }
+  return r;
+}
+
+// Pixel-centre box of a tile, clipped to the image.
+struct TileBox {
+  float x0, x1, y0, y1;
+};
+
+__device__ __forceinline__ TileBox tile_box(const BlendConsts& k, int tile) {
+  const int tx = tile % k.ntx, ty = tile / k.ntx;
+  TileBox b;
+  b.x0 = (float)(tx * kTile) + 0.5f;
+  b.y0 = (float)(ty * kTile) + 0.5f;
+  b.x1 = (float)(min(tx * kTile + kTile, k.width) - 1) + 0.5f;
+  b.y1 = (float)(min(ty * kTile + kTile, k.height) - 1) + 0.5f;
+  return b;
+}
+
+// Block-wide stream compaction of this thread's entry into slot `*pos`;
+// returns the number kept. s_wcnt holds 4 wave counts.
+__device__ __forceinline__ int compact(bool keep, int* s_wcnt, int& pos) {
+  const int w = threadIdx.x >> 6;
+  const uint64_t bal = __ballot(keep);
+  if ((threadIdx.x & 63) == 0) s_wcnt[w] = __popcll(bal);
+  __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int c = s_wcnt[k];
+    off += k < w ? c : 0;
+    tot += c;
+  }
+  pos = off + __popcll(bal & ((1ull << (threadIdx.x & 63)) - 1ull));
+  return tot;
+}
+
+constexpr int kGroup = 8;
+constexpr int kBwdGroup = 8;  // the backward's group
+
+BlendConsts consts(const abcd_camera& cam, const abcd_raster_params& prm) {
+  BlendConsts k;
+  k.width = cam.width;
+  k.height = cam.height;
+  k.ntx = tiles_x(cam.width);
+  k.ntiles = k.ntx * tiles_y(cam.height);
+  k.per_xcd = (k.ntiles + 7) / 8;
+  k.alpha_min = prm.alpha_min;
+  k.alpha_max = prm.alpha_max;
+  k.t_min = prm.t_min;
+  return k;
+}
+
+}  // namespace
+}  // namespace abcd

@@ -1,0 +1,260 @@
+// render_bwd.hip -- backward of the tile blend (paper, Method section:
+// gradients reach the active parameters only).
+//
+// The backward walks each pixel's list back to front from its last blended
+// entry, reduces each Gaussian's 9 screen-space gradients across the wave
+// with cross-lane adds, combines the 4 waves in LDS and issues one global
+// fp32 atomic per Gaussian and field per tile.
+#include "blend.h"
+
+namespace abcd {
+namespace {
+
+// DPP lane move inside the wave (all rows and banks enabled).
+template <int kCtrl>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xF, 0xF, false));
+}
+
+// Wave64 sum of nine values at once, by recursive halving: at each of the
+// first three exchanges a lane keeps half of its values and receives the
+// partner's partial sums of that half (quad xor 1, quad xor 2, row rotate 4),
+// the fourth pairs the survivor with the ninth value (row rotate 8), and two
+// cross-row swaps (v_permlane16_swap, v_permlane32_swap) finish. A rotation
+// by 4 (by 8) within a 16-lane row pairs lanes that differ in bit 2 (bit 3)
+// and agree in the lower bits, so partners hold partial sums of the same
+// values over disjoint lane sets. About 30 instructions, all VALU, instead of
+// 9 separate six-step reductions. On return, lane l < 16 holds the wave
+// total of value sum9_slot(l); every row holds the same totals.
+__device__ __forceinline__ float wave_sum9(const float (&g)[9], int lane) {
+  const bool b0 = lane & 1, b1 = lane & 2, b2 = lane & 4, b3 = lane & 8;
+  float a[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float keep = b0 ? g[q + 4] : g[q];
+    const float send = b0 ? g[q] : g[q + 4];
+    a[q] = keep + dpp_mov<0xB1>(send);
+  }
+  float v8 = g[8] + dpp_mov<0xB1>(g[8]);
+  float b[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const float keep = b1 ? a[q + 2] : a[q];
+    const float send = b1 ? a[q] : a[q + 2];
+    b[q] = keep + dpp_mov<0x4E>(send);
+  }
+  v8 += dpp_mov<0x4E>(v8);
+  const float c = (b2 ? b[1] : b[0]) + dpp_mov<0x124>(b2 ? b[0] : b[1]);
+  v8 += dpp_mov<0x124>(v8);
+  float d = (b3 ? v8 : c) + dpp_mov<0x128>(b3 ? c : v8);
+  // across rows: v_permlane16_swap / v_permlane32_swap exchange rows 0 <-> 1,
+  // 2 <-> 3 (halves 0 <-> 1); of the two registers each lane gets back, one
+  // is its own value and the other its partner's, so their sum is the pair sum
+  {
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_int(d), __float_as_int(d), false,
+                                                    false);
+    d = __int_as_float(p[0]) + __int_as_float(p[1]);
+  }
+  {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(d), __float_as_int(d), false,
+                                                    false);
+    d = __int_as_float(p[0]) + __int_as_float(p[1]);
+  }
+  return d;
+}
+
+// Which of the nine values lane l (< 16) holds after wave_sum9.
+__device__ __forceinline__ int sum9_slot(int l) {
+  return l < 8 ? 4 * (l & 1) + 2 * ((l >> 1) & 1) + ((l >> 2) & 1) : 8;
+}
+
+__global__ __launch_bounds__(256) void render_bwd_kernel(
+    BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
+    const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
+    const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
+    const float* __restrict__ final_T, const uint32_t* __restrict__ last,
+    const float4* __restrict__ dL_dout, float* __restrict__ g2d, const uint32_t* __restrict__ order) {
+  __shared__ float4 s_ga[256];  // u, v, qa, qb
+  __shared__ float4 s_gb[256];  // qc, o, r, g
+  __shared__ float4 s_gc[256];  // a, b, c (conic), colour b
+  __shared__ int s_pos[256];
+  __shared__ uint32_t s_g[256];
+  __shared__ float s_acc[9 * 256];  // entry-major: [entry][9]
+  __shared__ int s_wcnt[4];
+  __shared__ uint32_t s_max;
+  const int tile = tile_of_block(k, order);
+  if (tile >= k.ntiles) return;
+  const int tid = threadIdx.x;
+  const int px = (tile % k.ntx) * kTile + (tid & 15);
+  const int py = (tile / k.ntx) * kTile + (tid >> 4);
+  const bool inside = px < k.width && py < k.height;
+  const TileBox box = tile_box(k, tile);
+  const uint32_t start = tile_ranges[2 * tile];
+  const float fx = (float)px + 0.5f, fy = (float)py + 0.5f;
+  float T = 1.0f, gcr = 0, gcg = 0, gcb = 0, gT = 0;
+  uint32_t lastp = 0;
+  if (tid == 0) s_max = 0;
+  __syncthreads();
+  if (inside) {
+    const int64_t p = (int64_t)py * k.width + px;
+    T = final_T[p];
+    lastp = last[p];
+    const float4 G = dL_dout[p];
+    const float4 f = F ? F[p] : make_float4(0, 0, 0, 0);
+    const float4 bb = B ? B[p] : make_float4(0, 0, 0, 0);
+    const float s = 1.0f - f.w;
+    gcr = s * G.x;
+    gcg = s * G.y;
+    gcb = s * G.z;
+    gT = s * (G.x * bb.x + G.y * bb.y + G.z * bb.z - G.w * (1.0f - bb.w));
+    if (lastp) atomicMax(&s_max, lastp);
+  }
+  const float Tfin = T;
+  // RG = sum over channels of gc_ch R_ch, where R is the colour accumulated
+  // behind the current entry (normalised by its transmittance): the
+  // alpha-derivative needs R only through this sum.
+  float RG = 0.0f;
+  __syncthreads();
+  const uint32_t nent = s_max;
+  const int lane = tid & 63, slot = sum9_slot(lane & 15);
+  uint32_t wml = lastp;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) wml = max(wml, (uint32_t)__shfl_xor((int)wml, off, 64));
+  // entry j of a batch is list position bend - 1 - j (back to front)
+  uint32_t bend = start + nent;
+  Rec rec = load_rec(values, bend - 1 - tid, tid < (int)nent, means2d, conic_opacity, rgb);
+  while (bend > start) {
+    const uint32_t bbeg = bend - min(256u, bend - start);
+    __syncthreads();
+    const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, rec.co.x, rec.co.y, rec.co.z,
+                                                     rec.co.w, k.alpha_min, box.x0, box.x1,
+                                                     box.y0, box.y1);
+    int pos;
+    const int cnt = compact(keep, s_wcnt, pos);
+    if (keep) {
+      const Splat sp = make_splat(rec.m, rec.co);
+      s_ga[pos] = make_float4(sp.u, sp.v, sp.qa, sp.qb);
+      s_gb[pos] = make_float4(sp.qc, sp.o, rec.r, rec.g);
+      s_gc[pos] = make_float4(rec.co.x, rec.co.y, rec.co.z, rec.b);
+      s_pos[pos] = (int)(bend - 1 - tid - start);
+      s_g[pos] = rec.gid;
+#pragma unroll
+      for (int q = 0; q < 9; ++q) s_acc[9 * pos + q] = 0.0f;
+    }
+    __syncthreads();
+    {
+      const uint32_t nxt_end = bbeg;
+      const bool v = (uint32_t)tid < nxt_end - start;
+      rec = load_rec(values, nxt_end - 1 - tid, v, means2d, conic_opacity, rgb);
+    }
+    // Entries are read from LDS kGroup at a time, all reads issued before the
+    // first is used, so the LDS latency is paid once per group.
+    for (int j0 = 0; j0 < cnt; j0 += kBwdGroup) {
+    float4 gav[kBwdGroup], gbv[kBwdGroup], gcv[kBwdGroup];
+    uint32_t kkv[kBwdGroup];
+#pragma unroll
+    for (int i = 0; i < kBwdGroup; ++i) {
+      const int j = min(j0 + i, 255);
+      gav[i] = s_ga[j];
+      gbv[i] = s_gb[j];
+      gcv[i] = s_gc[j];
+      kkv[i] = (uint32_t)s_pos[j];
+    }
+#pragma unroll
+    for (int i = 0; i < kBwdGroup; ++i) {
+      const int j = j0 + i;
+      if (j >= cnt) break;  // wave-uniform
+      const uint32_t kk = kkv[i];
+      const float4 ga = gav[i], gb = gbv[i], gc = gcv[i];
+      if (kk >= wml) continue;  // wave-uniform: no pixel of this wave reaches entry kk
+      const float dx = fx - ga.x, dy = fy - ga.y;
+      const AlphaEval ae = eval_alpha(dx, dy, ga.z, ga.w, gb.x, gb.y, k.alpha_min, k.alpha_max);
+      const bool contrib = kk < lastp && !ae.skip;
+      if (!__ballot(contrib)) continue;  // wave-uniform
+      // Branch-free per lane: a lane that does not blend this entry takes
+      // alpha = 0, which leaves T and R unchanged, and a zero mask on the
+      // alpha-derivative terms.
+      const float a = contrib ? ae.alpha : 0.0f;
+      const float om = 1.0f - a;
+      const float iom = __builtin_amdgcn_rcpf(om);  // om >= 1 - alpha_max > 0
+      const float Tk = T * iom;
+      const float wgt = a * Tk;
+      float gr[9];
+      gr[6] = wgt * gcr;
+      gr[7] = wgt * gcg;
+      gr[8] = wgt * gcb;
+      const float CG = gb.z * gcr + gb.w * gcg + gc.w * gcb;
+      const float dLda = Tk * (CG - RG) - (Tfin * iom) * gT;
+      RG = a * CG + om * RG;
+      T = Tk;
+      const float dm = (contrib && !ae.clamped) ? dLda : 0.0f;
+      const float gp = a * dm;
+      // first and second moments of gp over the pixels; the conic and the
+      // constant factors are applied once per entry at the flush
+      const float q = gp * dx, r = gp * dy;
+      gr[0] = q;
+      gr[1] = r;
+      gr[2] = q * dx;
+      gr[3] = q * dy;
+      gr[4] = r * dy;
+      gr[5] = ae.e * dm;
+      const float v = wave_sum9(gr, lane);
+      if (lane < 9) atomicAdd(&s_acc[9 * j + slot], v);
+    }
+    }
+    __syncthreads();
+    if (tid < cnt) {
+      // moments -> dL/d(u, v, a, b, c): with q = dL/dpower * (dx, dy),
+      // d power / d(u, v) = (a dx + b dy, b dx + c dy), d power / d(a, b, c)
+      // = (-dx^2 / 2, -dx dy, -dy^2 / 2)
+      const float4 co = s_gc[tid];
+      float g[9];
+#pragma unroll
+      for (int q = 0; q < 9; ++q) g[q] = s_acc[9 * tid + q];
+      const float mx = g[0], my = g[1];
+      g[0] = co.x * mx + co.y * my;
+      g[1] = co.y * mx + co.z * my;
+      g[2] = -0.5f * g[2];
+      g[3] = -g[3];
+      g[4] = -0.5f * g[4];
+      float* dst = g2d + 9 * (int64_t)s_g[tid];
+#pragma unroll
+      for (int q = 0; q < 9; ++q)
+        if (g[q] != 0.0f) atomicAdd(dst + q, g[q]);
+    }
+    bend = bbeg;
+  }
+}
+
+}  // namespace
+
+static size_t g2d_bytes(int64_t n) {
+  return ((size_t)9 * sizeof(float) * (size_t)n + 255) & ~size_t(255);
+}
+
+// g2d[n][9], then the backward's tile work and tile order.
+size_t render_bwd_workspace_bytes(int64_t n) {
+  return g2d_bytes(n) + 2 * sizeof(uint32_t) * ABCD_MAX_TILES;
+}
+
+int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
+                                 const uint32_t* tile_ranges, const uint32_t* values_sorted,
+                                 const float* means2d, const float* conic_opacity,
+                                 const float* rgb, const float* F, const float* B,
+                                 const float* final_T, const uint32_t* last,
+                                 const float* dL_dout, float* g2d, hipStream_t stream) {
+  const BlendConsts k = consts(cam, prm);
+  uint32_t* work = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(g2d) + g2d_bytes(n));
+  uint32_t* order = work + ABCD_MAX_TILES;
+  TRY_STATUS(launch_tile_walk(k.width, k.height, last, work, stream));
+  TRY_STATUS(launch_tile_order(k.ntiles, work, order, nullptr, "bwd_order", stream));
+  ABCD_LAUNCH("render_bwd", render_bwd_kernel, k.ntiles, kBlock, 0, stream, k, tile_ranges,
+              values_sorted, reinterpret_cast<const float2*>(means2d),
+              reinterpret_cast<const float4*>(conic_opacity), rgb,
+              reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B), final_T,
+              last, reinterpret_cast<const float4*>(dL_dout), g2d, order);
+  ABCD_HIP(hipGetLastError());
+  return ABCD_OK;
+}
+
+}  // namespace abcd

@@ -1,0 +1,160 @@
+// render_fwd.hip -- forward tile rasterisation of the active partition,
+// composited between F and B (paper, Method section), and the cached-render
+// variant (F = B = transparent, fp16 store) used to refresh a partition's
+// cached images.
+//
+// The forward blends each pixel's list front to back and stops a pixel once
+// the next blend would take its transmittance below t_min; the workgroup
+// stops when all its pixels have stopped.
+#include "blend.h"
+
+namespace abcd {
+namespace {
+
+// kHalf: the cached-render variant: F = B = transparent, the image is written
+// as fp16 RGBA to out16 (round to nearest even), no final T or walk lengths.
+template <bool kHalf>
+__global__ __launch_bounds__(256) void render_fwd_kernel(
+    BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
+    const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
+    const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
+    float4* __restrict__ out, float* __restrict__ final_T, uint32_t* __restrict__ last,
+    unsigned long long* __restrict__ n_blends, const uint32_t* __restrict__ order,
+    uint2* __restrict__ out16) {
+  __shared__ float4 s_ga[256];  // u, v, qa, qb
+  __shared__ float4 s_gb[256];  // qc, o, r, g
+  __shared__ float s_bl[256];   // b
+  __shared__ int s_pos[256];    // position in the tile's list
+  __shared__ int s_wcnt[4];
+  __shared__ unsigned long long s_nb;
+  const int tile = tile_of_block(k, order);
+  if (tile >= k.ntiles) return;
+  const int tid = threadIdx.x;
+  const int px = (tile % k.ntx) * kTile + (tid & 15);
+  const int py = (tile / k.ntx) * kTile + (tid >> 4);
+  const bool inside = px < k.width && py < k.height;
+  const TileBox box = tile_box(k, tile);
+  const uint32_t start = tile_ranges[2 * tile], end = tile_ranges[2 * tile + 1];
+  const float fx = (float)px + 0.5f, fy = (float)py + 0.5f;
+  float T = 1.0f, cr = 0.0f, cg = 0.0f, cb = 0.0f;
+  uint32_t lastk = 0, nb = 0;
+  bool done = !inside;
+  if (tid == 0) s_nb = 0;
+  Rec rec = load_rec(values, start + tid, start + tid < end, means2d, conic_opacity, rgb);
+  for (uint32_t b0 = start; b0 < end; b0 += 256) {
+    if (__syncthreads_count(done) == 256) break;
+    const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, rec.co.x, rec.co.y, rec.co.z,
+                                                     rec.co.w, k.alpha_min, box.x0, box.x1,
+                                                     box.y0, box.y1);
+    int pos;
+    const int cnt = compact(keep, s_wcnt, pos);
+    if (keep) {
+      const Splat sp = make_splat(rec.m, rec.co);
+      s_ga[pos] = make_float4(sp.u, sp.v, sp.qa, sp.qb);
+      s_gb[pos] = make_float4(sp.qc, sp.o, rec.r, rec.g);
+      s_bl[pos] = rec.b;
+      s_pos[pos] = (int)(b0 - start) + tid;
+    }
+    __syncthreads();
+    // gathers of the next batch overlap the blend of this one
+    const uint32_t nxt = b0 + 256 + tid;
+    rec = load_rec(values, nxt, nxt < end, means2d, conic_opacity, rgb);
+    if (__ballot(!done)) {
+      // Lanes step through the entries together without divergent branches:
+      // a lane that skips an entry, or has stopped, blends with weight 0.
+      // Entries are read from LDS kGroup at a time, all reads issued before
+      // the first is used, so the LDS latency is paid once per group.
+      int jl = -1;  // last entry of this batch the lane blended
+      for (int j0 = 0; j0 < cnt; j0 += kGroup) {
+        float4 ga[kGroup], gb[kGroup];
+        float bl[kGroup];
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) {
+          const int j = min(j0 + i, 255);
+          ga[i] = s_ga[j];
+          gb[i] = s_gb[j];
+          bl[i] = s_bl[j];
+        }
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) {
+          if (j0 + i >= cnt) break;  // wave-uniform
+          const AlphaEval ae = eval_alpha(fx - ga[i].x, fy - ga[i].y, ga[i].z, ga[i].w, gb[i].x,
+                                          gb[i].y, k.alpha_min, k.alpha_max);
+          const float Tn = T * (1.0f - ae.alpha);
+          const bool hit = !done && !ae.skip;
+          const bool stop = hit && Tn < k.t_min;
+          const bool blend = hit && !stop;
+          done = done || stop;
+          const float wgt = blend ? ae.alpha * T : 0.0f;
+          cr += gb[i].z * wgt;
+          cg += gb[i].w * wgt;
+          cb += bl[i] * wgt;
+          T = blend ? Tn : T;
+          jl = blend ? j0 + i : jl;
+          nb += blend ? 1u : 0u;
+        }
+        if (!__ballot(!done)) break;  // wave-uniform
+      }
+      if (jl >= 0) lastk = (uint32_t)s_pos[jl] + 1;
+    }
+    // s_wcnt is rewritten only after the next barrier
+  }
+  if (inside) {
+    const int64_t p = (int64_t)py * k.width + px;
+    if (kHalf) {
+      const _Float16 h[4] = {(_Float16)cr, (_Float16)cg, (_Float16)cb, (_Float16)(1.0f - T)};
+      out16[p] = __builtin_bit_cast(uint2, h);
+    } else {
+      const float4 f = F ? F[p] : make_float4(0, 0, 0, 0);
+      const float4 bb = B ? B[p] : make_float4(0, 0, 0, 0);
+      const float s = 1.0f - f.w;
+      out[p] = make_float4(f.x + s * (cr + T * bb.x), f.y + s * (cg + T * bb.y),
+                           f.z + s * (cb + T * bb.z), f.w + s * (1.0f - T * (1.0f - bb.w)));
+      final_T[p] = T;
+      last[p] = lastk;
+    }
+  }
+  if (n_blends) {
+    const unsigned long long wsum = wave_sum_u32(nb);
+    __syncthreads();
+    if ((tid & 63) == 0) atomicAdd(&s_nb, wsum);
+    __syncthreads();
+    if (tid == 0 && s_nb) atomicAdd(n_blends, s_nb);
+  }
+}
+
+}  // namespace
+
+int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
+                          const uint32_t* tile_ranges, const uint32_t* values_sorted,
+                          const float* means2d, const float* conic_opacity, const float* rgb,
+                          const float* F, const float* B, float* out_rgba, float* final_T,
+                          uint32_t* last, unsigned long long* n_blends, const uint32_t* tile_order,
+                          hipStream_t stream) {
+  const BlendConsts k = consts(cam, prm);
+  const int grid = tile_order ? k.ntiles : 8 * k.per_xcd;
+  ABCD_LAUNCH("render_fwd", render_fwd_kernel<false>, grid, kBlock, 0, stream, k, tile_ranges,
+              values_sorted, reinterpret_cast<const float2*>(means2d),
+              reinterpret_cast<const float4*>(conic_opacity), rgb,
+              reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B),
+              reinterpret_cast<float4*>(out_rgba), final_T, last, n_blends, tile_order, nullptr);
+  ABCD_HIP(hipGetLastError());
+  return ABCD_OK;
+}
+
+int32_t launch_render_cache(const abcd_camera& cam, const abcd_raster_params& prm,
+                            const uint32_t* tile_ranges, const uint32_t* tile_order,
+                            const uint32_t* values_sorted, const float* means2d,
+                            const float* conic_opacity, const float* rgb, uint16_t* image_f16,
+                            hipStream_t stream) {
+  const BlendConsts k = consts(cam, prm);
+  const int grid = tile_order ? k.ntiles : 8 * k.per_xcd;
+  ABCD_LAUNCH("render_cache", render_fwd_kernel<true>, grid, kBlock, 0, stream, k, tile_ranges,
+              values_sorted, reinterpret_cast<const float2*>(means2d),
+              reinterpret_cast<const float4*>(conic_opacity), rgb, nullptr, nullptr, nullptr,
+              nullptr, nullptr, nullptr, tile_order, reinterpret_cast<uint2*>(image_f16));
+  ABCD_HIP(hipGetLastError());
+  return ABCD_OK;
+}
+
+}  // namespace abcd
