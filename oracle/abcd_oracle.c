@@ -463,6 +463,11 @@ void orc_render_fwd(const orc_camera* cam, const orc_params* prm, const uint32_t
     double T = 1.0, Cr = 0, Cg = 0, Cb = 0, tst = 0;
     uint32_t lst = 0;
     int kn = 0;
+    double f[4] = {0, 0, 0, 0}, bb[4] = {0, 0, 0, 0};
+    if (F) memcpy(f, F + 4 * pix, sizeof f);
+    if (B) memcpy(bb, B + 4 * pix, sizeof bb);
+    /* weight of the active render in the composited image: 1 - F_alpha */
+    const double vis = prm->fb_stop ? 1.0 - f[3] : 1.0;
     for (uint32_t k = start; k < end; k++) {
       const uint32_t g = values[k];
       const double dx = cxp - means2d[2 * g], dy = cyp - means2d[2 * g + 1];
@@ -477,8 +482,8 @@ void orc_render_fwd(const orc_camera* cam, const orc_params* prm, const uint32_t
       if (near_rel(alpha, prm->alpha_min, rel_margin)) kn = 1;
       if (alpha < prm->alpha_min) continue;
       const double Tn = T * (1.0 - alpha);
-      if (near_rel(Tn, prm->t_min, rel_margin)) kn = 1;
-      if (Tn < prm->t_min) {
+      if (near_rel(vis * Tn, prm->t_min, rel_margin)) kn = 1;
+      if (vis * Tn < prm->t_min) {
         tst = T;
         break;
       }
@@ -490,9 +495,6 @@ void orc_render_fwd(const orc_camera* cam, const orc_params* prm, const uint32_t
       total++;
     }
     /* premultiplied composite out = F over A over B, A = (C, 1 - T) */
-    double f[4] = {0, 0, 0, 0}, bb[4] = {0, 0, 0, 0};
-    if (F) memcpy(f, F + 4 * pix, sizeof f);
-    if (B) memcpy(bb, B + 4 * pix, sizeof bb);
     const double sfr = 1.0 - f[3];
     out[4 * pix + 0] = f[0] + sfr * (Cr + T * bb[0]);
     out[4 * pix + 1] = f[1] + sfr * (Cg + T * bb[1]);
@@ -535,6 +537,10 @@ void orc_render_bwd_2d(const orc_camera* cam, const orc_params* prm, int64_t n,
       const int64_t tile = (int64_t)(py / ORC_TILE) * ntx + px / ORC_TILE;
       const uint32_t start = tile_ranges[2 * tile], end = tile_ranges[2 * tile + 1];
       const double cxp = px + 0.5, cyp = py + 0.5;
+      double f[4] = {0, 0, 0, 0}, bb[4] = {0, 0, 0, 0};
+      if (F) memcpy(f, F + 4 * pix, sizeof f);
+      if (B) memcpy(bb, B + 4 * pix, sizeof bb);
+      const double vis = prm->fb_stop ? 1.0 - f[3] : 1.0;
       /* replay the forward walk, recording every blended entry */
       size_t nb = 0;
       double T = 1.0;
@@ -550,7 +556,7 @@ void orc_render_bwd_2d(const orc_camera* cam, const orc_params* prm, int64_t n,
         const double alpha = clamped ? prm->alpha_max : araw;
         if (alpha < prm->alpha_min) continue;
         const double Tn = T * (1.0 - alpha);
-        if (Tn < prm->t_min) break;
+        if (vis * Tn < prm->t_min) break;
         if (nb == cap) {
           cap *= 2;
           bl = (blended*)realloc(bl, sizeof(blended) * cap);
@@ -566,9 +572,6 @@ void orc_render_bwd_2d(const orc_camera* cam, const orc_params* prm, int64_t n,
         T = Tn;
       }
       /* gradients of out = F over (C, 1-T) over B with respect to C and T */
-      double f[4] = {0, 0, 0, 0}, bb[4] = {0, 0, 0, 0};
-      if (F) memcpy(f, F + 4 * pix, sizeof f);
-      if (B) memcpy(bb, B + 4 * pix, sizeof bb);
       const double* G = dL_dout + 4 * pix;
       const double sfr = 1.0 - f[3];
       const double gC[3] = {sfr * G[0], sfr * G[1], sfr * G[2]};
@@ -755,29 +758,35 @@ double orc_half_to_double(uint16_t h) {
 
 void orc_composite(int32_t width, int32_t height, int32_t k, const uint16_t* images,
                    const int32_t* order, int32_t n_front, double* F, double* B,
-                   int32_t accumulate) {
+                   int32_t accumulate, double stop_t, double rel_margin, uint8_t* knife) {
   const int64_t npix = (int64_t)width * height;
 #pragma omp parallel for schedule(static)
   for (int64_t pix = 0; pix < npix; pix++) {
-    double layer[2][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}};
+    /* acc[0] = F, acc[1] = B; a left fold of premultiplied "over" */
+    double acc[2][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}};
+    if (accumulate) {
+      memcpy(acc[0], F + 4 * pix, sizeof acc[0]);
+      memcpy(acc[1], B + 4 * pix, sizeof acc[1]);
+    }
+    int kn = 0;
     for (int j = 0; j < k; j++) {
-      double* acc = layer[j < n_front ? 0 : 1];
+      const int l = j < n_front ? 0 : 1;
+      if (stop_t > 0) {
+        /* the largest weight this layer could still get in the final image */
+        const double vis = (1.0 - acc[l][3]) * (l == 1 ? 1.0 - acc[0][3] : 1.0);
+        if (near_rel(vis, stop_t, rel_margin)) kn = 1;
+        if (vis < stop_t) continue;
+      }
       const uint16_t* px = images + ((int64_t)order[j] * npix + pix) * 4;
       double x[4];
       for (int c = 0; c < 4; c++) x[c] = orc_half_to_double(px[c]);
       /* acc = acc over x (premultiplied): acc + (1 - acc_alpha) x */
-      const double s = 1.0 - acc[3];
-      for (int c = 0; c < 4; c++) acc[c] = acc[c] + s * x[c];
+      const double s = 1.0 - acc[l][3];
+      for (int c = 0; c < 4; c++) acc[l][c] = acc[l][c] + s * x[c];
     }
-    double* dst[2] = {F + 4 * pix, B + 4 * pix};
-    for (int l = 0; l < 2; l++) {
-      if (accumulate) {
-        const double s = 1.0 - dst[l][3];
-        for (int c = 0; c < 4; c++) dst[l][c] = dst[l][c] + s * layer[l][c];
-      } else {
-        for (int c = 0; c < 4; c++) dst[l][c] = layer[l][c];
-      }
-    }
+    memcpy(F + 4 * pix, acc[0], sizeof acc[0]);
+    memcpy(B + 4 * pix, acc[1], sizeof acc[1]);
+    if (knife) knife[pix] = (uint8_t)kn;
   }
 }
 

@@ -48,6 +48,9 @@ typedef struct {
   float radius_sigmas;  /* support radius in standard deviations of the major axis */
   float guard;          /* guard-band factor on the field of view, used inside the Jacobian only */
   int32_t sh_degree;    /* 0..3 */
+  int32_t fb_stop;      /* compositing-aware stop: a blend ends the pixel when the weight
+                           (1 - F_alpha) T (1 - alpha) that later blends would get in the
+                           composited image falls below t_min (0: plain t_min rule) */
 } orc_params;
 
 /* ---- projection -------------------------------------------------------- */
@@ -84,7 +87,8 @@ void orc_bin(int32_t width, int32_t height, int64_t n, const float* depth, const
 /* Front-to-back blend of the sorted tile lists, then out = F over A over B
  * (premultiplied RGBA). F, B may be NULL (transparent). knife/t_stop may be
  * NULL; knife[p] != 0 marks a pixel one of whose threshold decisions lies
- * within rel_margin of its threshold. */
+ * within rel_margin of its threshold. With prm->fb_stop the stop test is
+ * (1 - F_alpha) T_next < t_min instead of T_next < t_min. */
 void orc_render_fwd(const orc_camera* cam, const orc_params* prm, const uint32_t* tile_ranges,
                     const uint32_t* values, const double* means2d, const double* conic,
                     const double* opacity, const double* rgb, const double* F, const double* B,
@@ -112,10 +116,15 @@ void orc_project_bwd(const orc_camera* cam, const orc_params* prm, int64_t n,
 /* F = fold_over(images[order[0..n_front)]), B = fold_over(images[order[n_front..k)]),
  * images are premultiplied RGBA IEEE binary16, [pool][h][w][4], every order[j]
  * indexes that pool and k is the number of layers folded. With accumulate,
- * the incoming F and B are kept in front: F <- F over fold, B <- B over fold. */
+ * the fold continues behind the incoming F and B. stop_t > 0 drops the layers
+ * that can no longer be seen (Limitations section: occluded renders can be
+ * ignored): a front layer is skipped once 1 - F_alpha < stop_t, a back layer
+ * once (1 - F_alpha)(1 - B_alpha) < stop_t, with the alphas accumulated so
+ * far. knife (may be NULL) marks pixels with such a decision within
+ * rel_margin of stop_t. */
 void orc_composite(int32_t width, int32_t height, int32_t k, const uint16_t* images,
                    const int32_t* order, int32_t n_front, double* F, double* B,
-                   int32_t accumulate);
+                   int32_t accumulate, double stop_t, double rel_margin, uint8_t* knife);
 
 /* ---- helpers exposed for the pin tests --------------------------------- */
 

@@ -36,7 +36,7 @@ class _Cam(C.Structure):
 class _Prm(C.Structure):
     _fields_ = [("alpha_min", C.c_float), ("alpha_max", C.c_float), ("t_min", C.c_float),
                 ("eps2d", C.c_float), ("radius_sigmas", C.c_float), ("guard", C.c_float),
-                ("sh_degree", C.c_int32)]
+                ("sh_degree", C.c_int32), ("fb_stop", C.c_int32)]
 
 
 def _opt(ptr_type):
@@ -82,7 +82,7 @@ def lib():
                                   _u32p, _f64p, _f64p, _f64p, _f64p, _f64p, _f64p]
     L.orc_project_bwd.restype = None
     L.orc_composite.argtypes = [C.c_int32, C.c_int32, C.c_int32, _u16p, _i32p, C.c_int32,
-                                _f64p, _f64p, C.c_int32]
+                                _f64p, _f64p, C.c_int32, C.c_double, C.c_double, _u8p]
     L.orc_composite.restype = None
     L.orc_adam.argtypes = [C.c_int64, _f64p, _f64p, _f64p, _f64p, C.c_double, C.c_double,
                            C.c_double, C.c_double, C.c_int64]
@@ -118,6 +118,7 @@ def _prm(p):
     q.alpha_min, q.alpha_max, q.t_min = float(p.alpha_min), float(p.alpha_max), float(p.t_min)
     q.eps2d, q.radius_sigmas, q.guard = float(p.eps2d), float(p.radius_sigmas), float(p.guard)
     q.sh_degree = int(p.sh_degree)
+    q.fb_stop = 1 if getattr(p, "fb_stop", False) else 0
     return q
 
 
@@ -225,13 +226,16 @@ def project_bwd(cam, prm, means, log_scales, quats, opacity_logits, sh, tiles_to
 
 # ------------------------------------------------------------------ collapse
 
-def composite(width, height, images_f16, order, n_front, F=None, B=None):
+def composite(width, height, images_f16, order, n_front, F=None, B=None, stop_t=0.0,
+              rel_margin=0.0, with_knife=False):
     """Collapse K cached premultiplied fp16 RGBA renders into F and B (fp64).
 
     images_f16: uint16 view of binary16 data, shape [pool, H, W, 4]; the fold
     takes images[order[0]], images[order[1]], ... front to back, the first
     n_front into F and the rest into B. With F/B given, the fold continues
-    behind them (accumulate mode)."""
+    behind them (accumulate mode). stop_t > 0 skips layers that can no longer
+    be seen (see orc_composite); with_knife also returns the pixels whose skip
+    decision lies within rel_margin of stop_t."""
     imgs = _c(images_f16, np.uint16)
     order = _c(order, np.int32).reshape(-1)
     k = int(order.shape[0])
@@ -244,7 +248,11 @@ def composite(width, height, images_f16, order, n_front, F=None, B=None):
     acc = F is not None
     Fo = _c(F, np.float64).copy() if acc else np.zeros((height, width, 4))
     Bo = _c(B, np.float64).copy() if acc else np.zeros((height, width, 4))
-    lib().orc_composite(width, height, k, imgs, order, int(n_front), Fo, Bo, 1 if acc else 0)
+    knife = np.zeros((height, width), np.uint8)
+    lib().orc_composite(width, height, k, imgs, order, int(n_front), Fo, Bo, 1 if acc else 0,
+                        float(stop_t), float(rel_margin), knife)
+    if with_knife:
+        return Fo, Bo, knife.astype(bool)
     return Fo, Bo
 
 

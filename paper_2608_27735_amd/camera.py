@@ -38,6 +38,7 @@ class RasterParams:
     radius_sigmas: float = 3.0       # support radius in sigmas of the major axis
     guard: float = 1.3               # guard band on the view frustum used in the Jacobian
     sh_degree: int = 0
+    fb_stop: bool = False            # compositing-aware stop: (1 - F_alpha) T < t_min ends a pixel
 
 
 def look_at(campos, target, width, height, fov_x_deg=60.0, up=(0.0, 0.0, 1.0), near=0.2):

@@ -696,3 +696,139 @@ def test_adam_zero_gradient_from_rest_stays():
     theta = np.array([1.0, -2.0, 3.0])
     th, m, v = O.adam(theta, np.zeros(3), np.zeros(3), np.zeros(3), 0.5, 0.9, 0.999, 1e-15, 1)
     assert np.array_equal(th, theta) and not m.any() and not v.any()
+
+
+# ------------------------------------------- visibility-aware skipping (f2)
+
+def test_fb_stop_worked_example():
+    """Flat white layers of alpha 0.95 behind F with alpha 0.9 (weight 0.1 in the
+    composite). T after each blend: 0.05, 0.0025, 1.25e-4. The plain rule
+    blends three (1.25e-4 >= 1e-4); the compositing-aware rule weighs them by
+    0.1 (5e-3, 2.5e-4, 1.25e-5) and stops before the third: last = 2,
+    T = 0.0025, out = F + 0.1 (C + T B) with C = 1 - T per colour channel."""
+    cam = axis_camera(16, 16)
+    n = 6
+    ranges, values, m2d, co, op, rgb = _splat_inputs(cam, [[8, 8]] * n, [[0, 0, 0]] * n, [0.95] * n,
+                                                     [[1, 1, 1]] * n)
+    F = np.zeros((16, 16, 4))
+    F[..., 0], F[..., 3] = 0.3, 0.9
+    B = np.zeros((16, 16, 4))
+    B[..., 1], B[..., 3] = 0.5, 0.5
+    plain = O.render_fwd(cam, RasterParams(), ranges, values, m2d, co, op, rgb, F, B)
+    assert np.all(plain["last"] == 3)
+    fw = O.render_fwd(cam, RasterParams(fb_stop=True), ranges, values, m2d, co, op, rgb, F, B)
+    assert np.all(fw["last"] == 2)
+    T = 0.05 ** 2
+    assert np.allclose(fw["final_T"], T, rtol=1e-14)
+    C = 1 - T
+    exp = [0.3 + 0.1 * C, 0.1 * (C + T * 0.5), 0.1 * C, 0.9 + 0.1 * (1 - T * 0.5)]
+    assert np.allclose(fw["out"], exp, atol=1e-15)
+    assert fw["n_blends"] == 2 * 256
+    # transparent F: the weight is 1 and the rule is the plain one
+    tr = O.render_fwd(cam, RasterParams(fb_stop=True), ranges, values, m2d, co, op, rgb, None, B)
+    assert np.all(tr["last"] == 3)
+
+
+def test_fb_stop_hidden_pixels_walk_nothing():
+    """Behind an opaque F, or one that leaves less than t_min of weight, the
+    compositing-aware rule blends nothing: last = 0, T = 1, out = F."""
+    cam = axis_camera(16, 16)
+    ranges, values, m2d, co, op, rgb = _splat_inputs(cam, [[8, 8]] * 3, [[0, 0, 0]] * 3, [0.5] * 3,
+                                                     [[1, 0, 0]] * 3)
+    for fa in (1.0, 1.0 - 5e-5):
+        F = np.zeros((16, 16, 4))
+        F[..., 2], F[..., 3] = 0.25, fa
+        B = np.full((16, 16, 4), 0.5)
+        fw = O.render_fwd(cam, RasterParams(fb_stop=True), ranges, values, m2d, co, op, rgb, F, B)
+        assert np.all(fw["last"] == 0) and np.all(fw["final_T"] == 1.0)
+        assert np.allclose(fw["out"], F + (1 - fa) * B, atol=1e-15)
+        assert fw["n_blends"] == 0
+    # just above the threshold the first blend still happens (0.5 * 2e-4 >= 1e-4)
+    F[..., 3] = 1.0 - 2e-4
+    fw = O.render_fwd(cam, RasterParams(fb_stop=True), ranges, values, m2d, co, op, rgb, F, B)
+    assert np.all(fw["last"] == 1)
+
+
+def test_fb_stop_backward_matches_finite_differences():
+    """The backward replays the compositing-aware walk: gradients of the
+    composited image agree with central differences of the forward, on a case
+    where the rule ends many pixels early (F alpha 0.9 to 0.99)."""
+    r = S.rng(17)
+    cam = axis_camera(32, 32)
+    prm = RasterParams(t_min=1e-2, fb_stop=True)
+    n = 16
+    sp = S.splats_2d(r, n, 32, 32, sigma_px=(3.0, 9.0))
+    sp["conic_opacity"][:, 3] = np.clip(sp["conic_opacity"][:, 3], 0.3, 0.95)
+    m2d = sp["means2d"].astype(np.float64)
+    co = sp["conic_opacity"][:, :3].astype(np.float64)
+    op = sp["conic_opacity"][:, 3].astype(np.float64)
+    rgb = sp["rgb"].astype(np.float64)
+    ntx, nty = O.tile_grid(32, 32)
+    rect = np.tile(np.array([0, 0, ntx - 1, nty - 1], np.int32), (n, 1))
+    _, values, ranges = O.bin(32, 32, sp["depth"], rect, np.full(n, ntx * nty, np.uint32))
+    F = np.zeros((32, 32, 4))
+    F[..., 3] = r.uniform(0.9, 0.99, (32, 32))
+    F[..., :3] = F[..., 3:] * r.uniform(0, 1, (32, 32, 3))
+    B = S.background_pair(r, 32, 32)[1].astype(np.float64)
+    base = O.render_fwd(cam, prm, ranges, values, m2d, co, op, rgb, F, B, rel_margin=1e-3)
+    plain = O.render_fwd(cam, RasterParams(t_min=1e-2), ranges, values, m2d, co, op, rgb, F, B)
+    assert (base["last"] < plain["last"]).sum() > 50  # the rule bites
+    w = r.normal(size=(32, 32, 4))
+    w[base["knife"]] = 0.0
+    g2d = O.render_bwd_2d(cam, prm, ranges, values, m2d, co, op, rgb, F, B, w)
+
+    def L(arrs):
+        return _loss(O.render_fwd(cam, prm, ranges, values, *arrs, F, B)["out"], w)
+
+    h = 1e-7
+    arrs = [m2d, co, op, rgb]
+    for i in range(n):
+        for col, (ai, k) in enumerate([(0, 0), (0, 1), (1, 0), (1, 1), (1, 2), (2, None),
+                                       (3, 0), (3, 1), (3, 2)]):
+            hh = h * (1e-2 if ai == 1 else 1.0)
+            plus, minus = [a.copy() for a in arrs], [a.copy() for a in arrs]
+            if k is None:
+                plus[ai][i] += hh
+                minus[ai][i] -= hh
+            else:
+                plus[ai][i, k] += hh
+                minus[ai][i, k] -= hh
+            fd = (L(plus) - L(minus)) / (2 * hh)
+            assert abs(fd - g2d[i, col]) <= 1e-6 * max(1.0, abs(fd)) + 1e-4 * abs(fd), \
+                (i, col, fd, g2d[i, col])
+
+
+def test_collapse_stop_worked_example():
+    """Three front layers of alpha 0.9 with stop_t = 0.05: the first two fold
+    (weights 1 and 0.1), the third would get 0.01 < 0.05 and is dropped, and
+    every back layer (weight 0.01 x 1) too."""
+    lay = np.array([[0.9, 0, 0, 0.9], [0, 0.9, 0, 0.9], [0, 0, 0.9, 0.9], [0.2, 0.2, 0.2, 0.5]])
+    imgs = S.half_bits(lay.reshape(4, 1, 1, 4))
+    F, B = O.composite(1, 1, imgs, [0, 1, 2, 3], 3, stop_t=0.05)
+    h = [float(np.float16(x)) for x in (0.9, 0.2, 0.5)]
+    exp_F = [h[0], (1 - h[0]) * h[0], 0, h[0] + (1 - h[0]) * h[0]]
+    assert np.allclose(F[0, 0], exp_F, atol=1e-15)
+    assert not np.any(B)
+    F0, B0 = O.composite(1, 1, imgs, [0, 1, 2, 3], 3)
+    assert F0[0, 0, 2] > 0 and B0[0, 0, 3] == h[2]
+
+
+def test_collapse_stop_is_chunk_invariant_and_bounded():
+    """The rule looks only at what has been folded so far, so streaming the
+    layers in chunks (accumulate) gives the one-pass result; and the dropped
+    layers change F over B by at most 2 stop_t per channel."""
+    r = S.rng(23)
+    H, W, k, nf = 12, 10, 24, 14
+    imgs = S.half_bits(S.premultiplied_images(r, k, H, W, alpha_max=0.9, coverage=0.8))
+    order = list(r.permutation(k))
+    st = 0.02
+    F1, B1 = O.composite(W, H, imgs, order, nf, stop_t=st)
+    Fc, Bc = O.composite(W, H, imgs, order[:9], 9, stop_t=st)
+    Fc, Bc = O.composite(W, H, imgs, order[9:20], nf - 9, F=Fc, B=Bc, stop_t=st)
+    Fc, Bc = O.composite(W, H, imgs, order[20:], 0, F=Fc, B=Bc, stop_t=st)
+    assert np.allclose(Fc, F1, atol=1e-15) and np.allclose(Bc, B1, atol=1e-15)
+    Fe, Be = O.composite(W, H, imgs, order, nf)
+    over = lambda f, b: f + (1 - f[..., 3:]) * b
+    d = np.abs(over(F1, B1) - over(Fe, Be))
+    assert d.max() <= 2 * st
+    assert d.max() > 0  # layers were dropped
