@@ -58,12 +58,14 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(name, n, n_vis, m, npix, k, sh_coeffs):
-    """Bytes a kernel must move at minimum (inputs read once, outputs written once)."""
+def algorithmic_bytes(name, n, n_vis, m, npix, k, sh_coeffs, covered_px=None):
+    """Bytes a kernel must move at minimum (inputs read once, outputs written once).
+    covered_px: layer-pixels inside the cached images' coverage boxes (the
+    collapse reads nothing outside them); None means every layer-pixel."""
     param = 4 * (3 + 3 + 4 + 1 + 3 * sh_coeffs)       # means, log-scales, quats, logit, SH
     proj = 4 * (2 + 4 + 1 + 1 + 1 + 3)                 # means2d, conic_opacity, depth, radius, tiles, rgb
     if name == "composite":
-        return npix * (8 * k + 32)
+        return 8 * (npix * k if covered_px is None else covered_px) + 32 * npix
     if name == "project":
         return n * (param + proj)
     if name == "project_bwd":
@@ -123,19 +125,22 @@ def main():
     order = [c for c in w.order if c != w.active]          # 99 frozen cells, front to back
     n_front = w.order.index(w.active)
     k = len(order)
-    images = S.cached_images_device(k, cam.height, cam.width, seed=4101, device=dev)
+    images, rects = S.cached_images_device(k, cam.height, cam.width, seed=4101, device=dev,
+                                           with_rects=True)
     order_idx = list(range(k))                              # images are stored in front-to-back order
     target = torch.from_numpy(S.rng(4102).uniform(0, 1, (cam.height, cam.width, 3))
                               .astype(np.float32)).to(dev)
     F = torch.empty((cam.height, cam.width, 4), dtype=torch.float32, device=dev)
     B = torch.empty_like(F)
+    r4 = rects.cpu().to(torch.int64)
+    covered = int(((r4[:, 2] - r4[:, 0]).clamp(min=0) * (r4[:, 3] - r4[:, 1]).clamp(min=0)).sum())
     st = ActiveBlockStep(cam, prm, params)
     m = st.project_and_bin(sync=True)
     n_vis = int((st.proj["tiles_touched"] > 0).sum().item())
     setup_s = time.time() - t0
 
     def one_step():
-        api.composite_cache(images, order_idx, n_front, F=F, B=B)
+        api.composite_cache(images, order_idx, n_front, F=F, B=B, rects=rects)
         st.step(target, F=F, B=B)
 
     for _ in range(args.warmup):
@@ -154,11 +159,12 @@ def main():
     blends_step = st.n_blends.item() / args.steps
     value = blends_step / (ms_step / 1e3)
 
-    graph = small = optimizer = cache_refresh = None
+    graph = small = optimizer = cache_refresh = visibility = None
     if args.extras:
         # the same step replayed as one HIP graph (collapse + step captured once)
         st.capture(target, F=F, B=B,
-                   before=lambda: api.composite_cache(images, order_idx, n_front, F=F, B=B))
+                   before=lambda: api.composite_cache(images, order_idx, n_front, F=F, B=B,
+                                                      rects=rects))
         for _ in range(args.warmup):
             st.replay()
         torch.cuda.synchronize()
@@ -173,6 +179,41 @@ def main():
         blends_graph = st.n_blends.item() / args.steps
         graph = dict(ms_per_step=ms_graph, value=blends_graph / (ms_graph / 1e3),
                      blends_per_step=blends_graph)
+
+        # visibility-aware variant (reported beside the metric, not in it): the
+        # collapse drops layers hidden below t_min and the forward stops a pixel
+        # once (1 - F_alpha) T < t_min; the image differs from the exact step's
+        # by at most t_min / (1 - alpha_max) (colour + 1) per channel
+        import dataclasses
+        prm_v = dataclasses.replace(prm, fb_stop=True)
+        st_v = ActiveBlockStep(cam, prm_v, params, capacity=st.capacity)
+        Fv, Bv = torch.empty_like(F), torch.empty_like(B)
+
+        def vis_step():
+            api.composite_cache(images, order_idx, n_front, F=Fv, B=Bv, rects=rects,
+                                stop_t=prm.t_min)
+            st_v.step(target, F=Fv, B=Bv)
+
+        for _ in range(args.warmup):
+            vis_step()
+        torch.cuda.synchronize()
+        st_v.n_blends.zero_()
+        v0, v1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        v0.record()
+        for _ in range(args.steps):
+            vis_step()
+        v1.record()
+        torch.cuda.synchronize()
+        ms_v = v0.elapsed_time(v1) / args.steps
+        blends_v = st_v.n_blends.item() / args.steps
+        hidden = float(((1.0 - Fv[..., 3]) < prm.t_min).float().mean().item())
+        diff = float((st_v.fwd["out"] - st.fwd["out"]).abs().max().item())
+        visibility = dict(ms_per_step=ms_v, blends_per_step=blends_v,
+                          value=blends_v / (ms_v / 1e3), stop_t=prm.t_min,
+                          hidden_pixel_fraction=hidden, max_abs_diff_vs_exact=diff,
+                          note="compositing-aware stop (fb_stop) and thresholded collapse; "
+                               "not the metric")
+        del st_v, Fv, Bv
 
         # launch-bound regime (Results section: small active partitions leave the
         # rasterizer underused and launch costs dominate): the 512-Gaussian active
@@ -203,7 +244,7 @@ def main():
     roofline = None
     if dominant:
         d = kern[dominant]
-        bytes_ = algorithmic_bytes(dominant, args.n, n_vis, m, npix, k, sh_coeffs)
+        bytes_ = algorithmic_bytes(dominant, args.n, n_vis, m, npix, k, sh_coeffs, covered)
         if bytes_ is not None:
             launch_bytes = bytes_ / d["launches_per_step"]
             achieved = launch_bytes / (d["ms_per_launch"] / 1e3) / 1e9
@@ -222,7 +263,7 @@ def main():
         if name in kern:
             kern[name]["TFLOPs"] = pairs * FLOPS_PER_PAIR[name] / (kern[name]["ms_per_launch"] / 1e3) / 1e12
     for name, d in kern.items():
-        b = algorithmic_bytes(name, args.n, n_vis, m, npix, k, sh_coeffs)
+        b = algorithmic_bytes(name, args.n, n_vis, m, npix, k, sh_coeffs, covered)
         if b is not None:
             d["algorithmic_GBs"] = b / d["launches_per_step"] / (d["ms_per_launch"] / 1e3) / 1e9
 
@@ -294,10 +335,11 @@ def main():
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": f"ABCD active-block step: {args.n} Gaussians (SH 3) at "
                                f"{cam.width}x{cam.height}, F/B collapsed from {k} cached fp16 "
-                               "partition renders",
+                               "partition renders (with their coverage boxes)",
                    "n_gaussians": args.n, "width": cam.width, "height": cam.height,
                    "sh_degree": prm.sh_degree, "k_cached": k, "n_front": n_front,
                    "n_isect": m, "n_visible": n_vis, "blends_per_step": blends_step,
+                   "cached_layer_pixels_covered": covered,
                    "evaluated_pairs_per_pass": pairs,
                    "sync_in_step": False},
         "roofline": roofline,
@@ -305,6 +347,7 @@ def main():
         "optimizer": optimizer,
         "graph": graph,
         "cache_refresh": cache_refresh,
+        "visibility": visibility,
         "small_config": small,
         "kernels": kern,
         "setup_s": setup_s,

@@ -85,8 +85,19 @@ typedef struct {
   float radius_sigmas; /* support radius in sigmas of the major axis (3) */
   float guard;         /* guard-band factor on the field of view inside the Jacobian (1.3) */
   int32_t sh_degree;   /* 0..3 */
-  uint32_t flags;      /* reserved, must be 0 */
+  uint32_t flags;      /* ABCD_FLAG_* bits; others must be 0 */
 } abcd_raster_params;
+
+/* Compositing-aware stop (Limitations section: what a near-opaque foreground
+ * hides need not be rendered). In abcd_render_fwd a pixel stops when the
+ * weight the next blend would leave for later ones in the composited image,
+ * (1 - F_alpha) T (1 - alpha), is below t_min, instead of T (1 - alpha); a
+ * pixel whose F leaves it less than t_min blends nothing, and a tile whose
+ * pixels all do so is skipped. Without F the rule is the plain one. The image
+ * then differs from the plain rule's by at most t_min / (1 - alpha_max) per
+ * channel times the largest colour plus one. abcd_render_bwd follows the
+ * forward's final_T and last, so it needs no flag. */
+#define ABCD_FLAG_FB_STOP 1u
 
 /* ------------------------------------------------------------------------ */
 /* Projection (3DGS EWA splatting: Introduction; Method section -- "only the
@@ -174,12 +185,16 @@ ABCD_API int32_t abcd_render_fwd(const abcd_camera* cam /* host */, const abcd_r
  * premultiplied fp16 RGBA, image_f16[H][W][4] = binary16 (round to nearest
  * even) of (C, 1 - T). Its input is that partition's projection and binning on
  * the camera; its output feeds abcd_composite_cache. tile_order as in
- * abcd_render_fwd (may be NULL). image_f16 8-byte aligned. */
+ * abcd_render_fwd (may be NULL). image_f16 8-byte aligned.
+ * rect (device, may be NULL): int32[4] = (x0, y0, x1, y1), the bounding box
+ * of the 16x16 tiles holding a pixel that blended anything, clipped to the
+ * image; the image is zero outside it (x1 <= x0 when nothing blended). It is
+ * the coverage box abcd_composite_cache takes. */
 ABCD_API int32_t abcd_render_cache(const abcd_camera* cam /* host */,
                           const abcd_raster_params* prm /* host */, const uint32_t* tile_ranges,
                           const uint32_t* tile_order, const uint32_t* values_sorted,
                           const float* means2d, const float* conic_opacity, const float* rgb,
-                          uint16_t* image_f16, hipStream_t stream);
+                          uint16_t* image_f16, int32_t* rect, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Backward (Method section: gradients are back-propagated only through the
@@ -215,13 +230,24 @@ ABCD_API int32_t abcd_render_bwd(const abcd_camera* cam /* host */, const abcd_r
  * images: k premultiplied RGBA fp16 renders [k][H][W][4]. order (host): a
  * permutation of 0..k-1, front to back. F = images[order[0]] over ... over
  * images[order[n_front-1]], B = images[order[n_front]] over ... over
- * images[order[k-1]], both fp32 [H][W][4]. With accumulate != 0 the incoming
- * F and B stay in front (F <- F over fold, B <- B over fold), so chunks of
- * cached images can stream in front to back; otherwise they are overwritten.
- * k = 0 writes transparent F and B (or leaves them unchanged when
- * accumulating). */
+ * images[order[k-1]], both fp32 [H][W][4]. With accumulate != 0 the fold
+ * continues behind the incoming F and B (F <- F over fold, B <- B over fold),
+ * so chunks of cached images can stream in front to back; otherwise they are
+ * overwritten. k = 0 writes transparent F and B (or leaves them unchanged
+ * when accumulating).
+ * rects (device, may be NULL, 16-byte aligned): int32 [k][4] = (x0, y0, x1,
+ * y1) per image, the pixel box [x0, x1) x [y0, y1) outside which that image
+ * is fully transparent (all four channels zero), as abcd_render_cache
+ * reports it; the image is not read outside its box. A box that cuts off
+ * non-zero pixels gives wrong results. NULL: every image covers the frame.
+ * stop_t (0 <= stop_t < 1; Limitations section: occluded renders can be
+ * ignored): 0 folds every layer; above 0 a front layer is skipped once
+ * 1 - F_alpha < stop_t and a back layer once (1 - F_alpha)(1 - B_alpha) <
+ * stop_t (alphas accumulated so far), which changes F over B by at most
+ * 2 stop_t per channel. */
 ABCD_API int32_t abcd_composite_cache(int32_t width, int32_t height, int32_t k, const uint16_t* images,
-                             const int32_t* order /* host */, int32_t n_front, float* F, float* B,
+                             const int32_t* order /* host */, int32_t n_front,
+                             const int32_t* rects, float stop_t, float* F, float* B,
                              int32_t accumulate, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
@@ -268,7 +294,8 @@ ABCD_API int32_t abcd_adam_step(const abcd_adam_group* groups /* host */, int32_
  * (names: composite, project, depth_keys, radix_hist, radix_scan,
  * radix_scatter, l1_count, l1_scan_columns, l1_finish, l1_scatter, l2_count,
  * l2_scan, bin_scan_tiles, l2_scatter, bin_tile_order, render_fwd, loss_l1,
- * zero_fill, bwd_order, render_bwd, project_bwd, adam, render_cache). */
+ * zero_fill, bwd_order, render_bwd, project_bwd, adam, render_cache,
+ * cache_rect_init). */
 ABCD_API const char* abcd_last_error(void);
 ABCD_API const char* abcd_version(void);
 ABCD_API const char* abcd_status_string(int32_t status);

@@ -45,12 +45,12 @@ SIGNATURES = {
     "abcd_bin_sort": (_I32, [_I32, _I32, _I64, _P, _P, _P, _P, _I64, _P, _SZ, _P, _P, _P, _P,
                              C.POINTER(_I64), _P]),
     "abcd_render_fwd": (_I32, [_CAM, _PRM] + [_P] * 12 + [_P]),
-    "abcd_render_cache": (_I32, [_CAM, _PRM] + [_P] * 7 + [_P]),
+    "abcd_render_cache": (_I32, [_CAM, _PRM] + [_P] * 8 + [_P]),
     "abcd_render_bwd_workspace_size": (_I32, [_I64, C.POINTER(_SZ)]),
     "abcd_render_bwd": (_I32, [_CAM, _PRM, _I64] + [_P] * 5 + [_P] * 4 + [_P] * 2 + [_P] * 5 +
                         [_P, _SZ] + [_P] * 6 + [_I32, _P]),
-    "abcd_composite_cache": (_I32, [_I32, _I32, _I32, _P, C.POINTER(C.c_int32), _I32, _P, _P,
-                                    _I32, _P]),
+    "abcd_composite_cache": (_I32, [_I32, _I32, _I32, _P, C.POINTER(C.c_int32), _I32, _P,
+                                    C.c_float, _P, _P, _I32, _P]),
     "abcd_loss_l1_grad": (_I32, [_I32, _I32, _P, _P, C.POINTER(C.c_float), _P, _P, _P]),
     "abcd_adam_step": (_I32, [C.POINTER(abcd_adam_group), _I32, C.c_float, C.c_float, C.c_float,
                               _I64, _P]),
@@ -110,9 +110,13 @@ def camera_struct(cam):
     return c
 
 
+FLAG_FB_STOP = 1  # ABCD_FLAG_FB_STOP
+
+
 def params_struct(p):
     q = abcd_raster_params()
     q.alpha_min, q.alpha_max, q.t_min = float(p.alpha_min), float(p.alpha_max), float(p.t_min)
     q.eps2d, q.radius_sigmas, q.guard = float(p.eps2d), float(p.radius_sigmas), float(p.guard)
-    q.sh_degree, q.flags = int(p.sh_degree), 0
+    q.sh_degree = int(p.sh_degree)
+    q.flags = FLAG_FB_STOP if getattr(p, "fb_stop", False) else 0
     return q

@@ -163,18 +163,20 @@ def render_fwd(cam, prm, bins, proj, F=None, B=None, n_blends=None, out=None):
     return out
 
 
-def render_cache(cam, prm, bins, proj, image=None):
+def render_cache(cam, prm, bins, proj, image=None, rect=None):
     """The partition rendered alone (F = B = transparent) as premultiplied fp16
-    RGBA [H, W, 4] (torch.float16), the form abcd_composite_cache consumes."""
+    RGBA [H, W, 4] (torch.float16), the form abcd_composite_cache consumes.
+    rect: optional int32 [4] GPU tensor that receives the coverage box."""
     H, W = cam.height, cam.width
     if image is None:
         image = _empty((H, W, 4), torch.float16, proj["means2d"].device)
     _need(image, "image", torch.float16, (H, W, 4))
+    _opt(rect, "rect", torch.int32, (4,))
     check(_lib.load().abcd_render_cache(
         C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)),
         _ptr(bins["tile_ranges"]), _ptr(bins.get("tile_order")), _ptr(bins["values"]),
         _ptr(proj["means2d"]), _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]), _ptr(image),
-        _stream()))
+        _ptr(rect), _stream()))
     return image
 
 
@@ -241,9 +243,12 @@ def adam_step(params, grads, exp_avg, exp_avg_sq, lr, step, beta1=0.9, beta2=0.9
 
 # ---------------------------------------------------------------- collapse
 
-def composite_cache(images, order, n_front, F=None, B=None, accumulate=False):
+def composite_cache(images, order, n_front, F=None, B=None, accumulate=False, rects=None,
+                    stop_t=0.0):
     """Collapse cached fp16 renders [K, H, W, 4] (torch.float16, or int16
-    holding binary16 bits) into F and B (fp32 [H, W, 4])."""
+    holding binary16 bits) into F and B (fp32 [H, W, 4]). rects: optional
+    int32 [K, 4] GPU tensor of per-image coverage boxes (x0, y0, x1, y1);
+    stop_t > 0 skips layers that can no longer be seen."""
     if images.dtype not in (torch.float16, torch.int16):
         raise ValueError("images must be float16 (or int16 bit patterns)")
     if not images.is_cuda or not images.is_contiguous() or images.dim() != 4:
@@ -258,9 +263,11 @@ def composite_cache(images, order, n_front, F=None, B=None, accumulate=False):
         B = _empty((H, W, 4), torch.float32, dev)
     _need(F, "F", torch.float32, (H, W, 4))
     _need(B, "B", torch.float32, (H, W, 4))
+    _opt(rects, "rects", torch.int32, (k, 4))
     order_arr = (C.c_int32 * max(k, 1))(*[int(x) for x in order])
-    check(_lib.load().abcd_composite_cache(W, H, k, _ptr(images), order_arr, int(n_front), _ptr(F),
-                                           _ptr(B), 1 if accumulate else 0, _stream()))
+    check(_lib.load().abcd_composite_cache(W, H, k, _ptr(images), order_arr, int(n_front),
+                                           _ptr(rects), float(stop_t), _ptr(F), _ptr(B),
+                                           1 if accumulate else 0, _stream()))
     return F, B
 
 

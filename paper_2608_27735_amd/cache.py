@@ -38,9 +38,10 @@ class CacheRefresher:
         self.copy_stream = torch.cuda.Stream(device=dev)
         self.copied = [None, None]  # event: staging slot free again
 
-    def render(self, cam, image):
+    def render(self, cam, image, rect=None):
         """Cached render of the partition on `cam` into `image` (fp16 [H, W, 4],
-        on the GPU), on the current stream. Returns the intersection count."""
+        on the GPU), and its coverage box into `rect` (int32 [4], optional), on
+        the current stream. Returns the intersection count."""
         if (cam.width, cam.height) != (self.W, self.H):
             raise ValueError("camera size differs from the refresher's")
         api.project(cam, self.prm, **self.params, out=self.proj)
@@ -48,13 +49,14 @@ class CacheRefresher:
                          workspace=self.workspace, values=self.values,
                          tile_ranges=self.tile_ranges, tile_order=self.tile_order, sync=True)
         self.values, self.workspace, self.capacity = b["values"], b["workspace"], b["capacity"]
-        api.render_cache(cam, self.prm, b, self.proj, image=image)
+        api.render_cache(cam, self.prm, b, self.proj, image=image, rect=rect)
         return b["n_isect"]
 
-    def refresh(self, cams, host_images):
+    def refresh(self, cams, host_images, rects=None):
         """Re-render the partition for every camera in `cams` into the pinned
-        host fp16 images host_images[i] ([H, W, 4] each). Returns when every
-        copy has landed."""
+        host fp16 images host_images[i] ([H, W, 4] each), and each image's
+        coverage box into rects[i] (int32 [len(cams), 4] on the GPU, optional).
+        Returns when every copy has landed."""
         if len(host_images) < len(cams):
             raise ValueError("one host image per camera is needed")
         for h in host_images[:len(cams)]:
@@ -67,7 +69,7 @@ class CacheRefresher:
             if self.copied[slot] is not None:
                 compute.wait_event(self.copied[slot])
             img = self.staging[slot]
-            self.render(cam, img)
+            self.render(cam, img, None if rects is None else rects[i])
             done = torch.cuda.Event()
             done.record(compute)
             with torch.cuda.stream(self.copy_stream):

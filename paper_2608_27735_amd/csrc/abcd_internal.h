@@ -203,7 +203,7 @@ int32_t launch_render_cache(const abcd_camera& cam, const abcd_raster_params& pr
                             const uint32_t* tile_ranges, const uint32_t* tile_order,
                             const uint32_t* values_sorted, const float* means2d,
                             const float* conic_opacity, const float* rgb, uint16_t* image_f16,
-                            hipStream_t stream);
+                            int32_t* rect, hipStream_t stream);
 int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
                                  const uint32_t* tile_ranges, const uint32_t* values_sorted,
                                  const float* means2d, const float* conic_opacity,
@@ -229,7 +229,7 @@ int32_t launch_adam(const abcd_adam_group* groups, int ngroups, float beta1, flo
 
 // composite.hip
 int32_t launch_composite(int width, int height, int k, const uint16_t* images,
-                         const int32_t* order, int n_front, float* F, float* B, int accumulate,
-                         hipStream_t stream);
+                         const int32_t* order, int n_front, const int32_t* rects, float stop_t,
+                         float* F, float* B, int accumulate, hipStream_t stream);
 
 }  // namespace abcd

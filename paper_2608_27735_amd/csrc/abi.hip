@@ -86,7 +86,7 @@ int32_t check_camera(const abcd_camera* c) {
 int32_t check_params(const abcd_raster_params* p) {
   REQUIRE(p != nullptr, "raster params are NULL");
   REQUIRE(p->sh_degree >= 0 && p->sh_degree <= 3, "sh_degree %d not in [0, 3]", p->sh_degree);
-  REQUIRE(p->flags == 0, "flags must be 0");
+  REQUIRE((p->flags & ~ABCD_FLAG_FB_STOP) == 0, "unknown flags 0x%x", p->flags);
   REQUIRE(p->alpha_min >= 0 && p->alpha_max > 0 && p->alpha_max < 1 && p->alpha_min <= p->alpha_max,
           "need 0 <= alpha_min <= alpha_max < 1");
   REQUIRE(p->t_min >= 0 && p->t_min < 1, "t_min must be in [0, 1)");
@@ -220,7 +220,7 @@ int32_t abcd_render_cache(const abcd_camera* cam, const abcd_raster_params* prm,
                           const uint32_t* tile_ranges, const uint32_t* tile_order,
                           const uint32_t* values_sorted, const float* means2d,
                           const float* conic_opacity, const float* rgb, uint16_t* image_f16,
-                          hipStream_t stream) {
+                          int32_t* rect, hipStream_t stream) {
   TRY(check_camera(cam));
   TRY(check_params(prm));
   REQUIRE(tile_ranges && image_f16, "tile_ranges or image_f16 is NULL");
@@ -228,8 +228,9 @@ int32_t abcd_render_cache(const abcd_camera* cam, const abcd_raster_params* prm,
               (reinterpret_cast<uintptr_t>(conic_opacity) & 15) == 0 &&
               (reinterpret_cast<uintptr_t>(means2d) & 7) == 0,
           "image_f16 and means2d must be 8-byte aligned, conic_opacity 16-byte aligned");
+  REQUIRE((reinterpret_cast<uintptr_t>(rect) & 3) == 0, "rect must be 4-byte aligned");
   return launch_render_cache(*cam, *prm, tile_ranges, tile_order, values_sorted, means2d,
-                             conic_opacity, rgb, image_f16, stream);
+                             conic_opacity, rgb, image_f16, rect, stream);
 }
 
 int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes) {
@@ -283,9 +284,12 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
 }
 
 int32_t abcd_composite_cache(int32_t width, int32_t height, int32_t k, const uint16_t* images,
-                             const int32_t* order, int32_t n_front, float* F, float* B,
-                             int32_t accumulate, hipStream_t stream) {
+                             const int32_t* order, int32_t n_front, const int32_t* rects,
+                             float stop_t, float* F, float* B, int32_t accumulate,
+                             hipStream_t stream) {
   REQUIRE(width > 0 && height > 0, "image size must be positive");
+  REQUIRE(stop_t >= 0.0f && stop_t < 1.0f, "stop_t must be in [0, 1)");
+  REQUIRE((reinterpret_cast<uintptr_t>(rects) & 15) == 0, "rects must be 16-byte aligned");
   REQUIRE(k >= 0, "k must be >= 0");
   REQUIRE(n_front >= 0 && n_front <= k, "n_front %d not in [0, %d]", n_front, k);
   REQUIRE(F && B, "F or B is NULL");
@@ -300,7 +304,8 @@ int32_t abcd_composite_cache(int32_t width, int32_t height, int32_t k, const uin
       seen[order[j]] = 1;
     }
   }
-  return launch_composite(width, height, k, images, order, n_front, F, B, accumulate, stream);
+  return launch_composite(width, height, k, images, order, n_front, rects, stop_t, F, B, accumulate,
+                          stream);
 }
 
 int32_t abcd_loss_l1_grad(int32_t width, int32_t height, const float* out_rgba,

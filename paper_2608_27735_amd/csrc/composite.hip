@@ -44,59 +44,107 @@ __device__ __forceinline__ void over(float4& acc, const float4 x) {
   acc.w += s * x.w;
 }
 
+// Coordinates of the (one or two) pixels a thread folds.
+struct PixPos {
+  int x0, y0, x1, y1;
+};
+
+__device__ __forceinline__ bool in_rect(const int4 r, int x, int y) {
+  return x >= r.x && x < r.z && y >= r.y && y < r.w;
+}
+
 // Fold layers tab[first .. first+count) at pixel pair `pp` (or single pixel).
-template <bool kPair>
+// rects (may be NULL): per image, the pixel box outside which it is fully
+// transparent; a layer is not read where it cannot contribute (folding a
+// transparent layer leaves the accumulator bit-identical, so this changes no
+// result). kStop: a pixel takes no further layer once the weight it could
+// still give one, (1 - acc_alpha) vis, is below stop_t; a wave whose pixels
+// have all stopped leaves the loop.
+template <bool kPair, bool kStop>
 __device__ __forceinline__ void fold(const uint2* __restrict__ img, int64_t npix, int64_t pp,
-                                     const LayerTable& tab, int first, int count, float4& a0,
+                                     const LayerTable& tab, int first, int count,
+                                     const int4* __restrict__ rects, const PixPos& pos,
+                                     float stop_t, float vis0, float vis1, float4& a0,
                                      float4& a1) {
   for (int j0 = 0; j0 < count; j0 += kBatch) {
     const int m = min(kBatch, count - j0);
+    bool live = true;
+    if (kStop) {
+      live = (1.0f - a0.w) * vis0 >= stop_t || (kPair && (1.0f - a1.w) * vis1 >= stop_t);
+      if (!__ballot(live)) break;  // wave-uniform
+    }
     uint4 v[kBatch];
 #pragma unroll
     for (int b = 0; b < kBatch; ++b) {
       if (b < m) {
-        const uint2* src = img + (int64_t)tab.idx[first + j0 + b] * npix + pp;
-        if (kPair) {
-          const u4v t = __builtin_nontemporal_load(reinterpret_cast<const u4v*>(src));
-          v[b] = make_uint4(t[0], t[1], t[2], t[3]);
-        } else {
-          const uint2 s = *src;
-          v[b] = make_uint4(s.x, s.y, 0u, 0u);
+        const int idx = tab.idx[first + j0 + b];
+        bool need = live;
+        if (rects) {
+          const int4 r = rects[idx];
+          need = need && (in_rect(r, pos.x0, pos.y0) || (kPair && in_rect(r, pos.x1, pos.y1)));
+        }
+        v[b] = make_uint4(0u, 0u, 0u, 0u);
+        if (need) {
+          const uint2* src = img + (int64_t)idx * npix + pp;
+          if (kPair) {
+            const u4v t = __builtin_nontemporal_load(reinterpret_cast<const u4v*>(src));
+            v[b] = make_uint4(t[0], t[1], t[2], t[3]);
+          } else {
+            const uint2 s = *src;
+            v[b] = make_uint4(s.x, s.y, 0u, 0u);
+          }
         }
       }
     }
 #pragma unroll
     for (int b = 0; b < kBatch; ++b) {
       if (b < m) {
-        over(a0, to_f4(make_uint2(v[b].x, v[b].y)));
-        if (kPair) over(a1, to_f4(make_uint2(v[b].z, v[b].w)));
+        if (!kStop || (1.0f - a0.w) * vis0 >= stop_t) over(a0, to_f4(make_uint2(v[b].x, v[b].y)));
+        if (kPair && (!kStop || (1.0f - a1.w) * vis1 >= stop_t))
+          over(a1, to_f4(make_uint2(v[b].z, v[b].w)));
       }
     }
   }
 }
 
-template <bool kPair>
-__global__ __launch_bounds__(256) void composite_kernel(int64_t npix, const uint2* __restrict__ img,
+template <bool kPair, bool kStop>
+__global__ __launch_bounds__(256) void composite_kernel(int64_t npix, int width,
+                                                        const uint2* __restrict__ img,
                                                         LayerTable tab, FoldPlan plan,
-                                                        float4* __restrict__ F,
+                                                        const int4* __restrict__ rects,
+                                                        float stop_t, float4* __restrict__ F,
                                                         float4* __restrict__ B) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t pp = kPair ? 2 * t : t;
   if (pp >= npix) return;
+  PixPos pos;
+  pos.x0 = (int)((uint32_t)pp % (uint32_t)width);
+  pos.y0 = (int)((uint32_t)pp / (uint32_t)width);
+  pos.x1 = pos.x0 + 1;
+  pos.y1 = pos.y0;
+  if (pos.x1 == width) {
+    pos.x1 = 0;
+    pos.y1 += 1;
+  }
   const float4 zero = make_float4(0, 0, 0, 0);
   // F
+  float4 f0 = zero, f1 = zero;
   if (plan.mode_f != 2) {
-    float4 a0 = plan.mode_f == 1 ? F[pp] : zero;
-    float4 a1 = (kPair && plan.mode_f == 1) ? F[pp + 1] : zero;
-    fold<kPair>(img, npix, pp, tab, 0, plan.nf, a0, a1);
-    F[pp] = a0;
-    if (kPair) F[pp + 1] = a1;
+    f0 = plan.mode_f == 1 ? F[pp] : zero;
+    f1 = (kPair && plan.mode_f == 1) ? F[pp + 1] : zero;
+    fold<kPair, kStop>(img, npix, pp, tab, 0, plan.nf, rects, pos, stop_t, 1.0f, 1.0f, f0, f1);
+    F[pp] = f0;
+    if (kPair) F[pp + 1] = f1;
+  } else if (kStop && plan.mode_b != 2) {
+    f0 = F[pp];
+    if (kPair) f1 = F[pp + 1];
   }
-  // B
+  // B, weighted by what F leaves visible
   if (plan.mode_b != 2) {
     float4 a0 = plan.mode_b == 1 ? B[pp] : zero;
     float4 a1 = (kPair && plan.mode_b == 1) ? B[pp + 1] : zero;
-    fold<kPair>(img, npix, pp, tab, plan.nf, plan.nb, a0, a1);
+    fold<kPair, kStop>(img, npix, pp, tab, plan.nf, plan.nb, rects, pos, stop_t, 1.0f - f0.w,
+                       1.0f - f1.w, a0, a1);
     B[pp] = a0;
     if (kPair) B[pp + 1] = a1;
   }
@@ -105,8 +153,8 @@ __global__ __launch_bounds__(256) void composite_kernel(int64_t npix, const uint
 }  // namespace
 
 int32_t launch_composite(int width, int height, int k, const uint16_t* images,
-                         const int32_t* order, int n_front, float* F, float* B, int accumulate,
-                         hipStream_t stream) {
+                         const int32_t* order, int n_front, const int32_t* rects, float stop_t,
+                         float* F, float* B, int accumulate, hipStream_t stream) {
   const int64_t npix = (int64_t)width * height;
   const uint2* img = reinterpret_cast<const uint2*>(images);
   // pairs need 16-byte alignment of every layer: even pixel count, aligned base
@@ -132,12 +180,21 @@ int32_t launch_composite(int width, int height, int k, const uint16_t* images,
     plan.mode_b = (bi > 0 || accumulate) ? (plan.nb ? 1 : 2) : 0;
     if (!first && plan.nf == 0) plan.mode_f = 2;
     if (!first && plan.nb == 0) plan.mode_b = 2;
-    if (pair) {
-      ABCD_LAUNCH("composite", composite_kernel<true>, blocks, kBlock, 0, stream, npix, img, tab,
-                  plan, reinterpret_cast<float4*>(F), reinterpret_cast<float4*>(B));
+    const int4* r4 = reinterpret_cast<const int4*>(rects);
+    float4* F4 = reinterpret_cast<float4*>(F);
+    float4* B4 = reinterpret_cast<float4*>(B);
+    if (pair && stop_t > 0.0f) {
+      ABCD_LAUNCH("composite", (composite_kernel<true, true>), blocks, kBlock, 0, stream, npix,
+                  width, img, tab, plan, r4, stop_t, F4, B4);
+    } else if (pair) {
+      ABCD_LAUNCH("composite", (composite_kernel<true, false>), blocks, kBlock, 0, stream, npix,
+                  width, img, tab, plan, r4, stop_t, F4, B4);
+    } else if (stop_t > 0.0f) {
+      ABCD_LAUNCH("composite", (composite_kernel<false, true>), blocks, kBlock, 0, stream, npix,
+                  width, img, tab, plan, r4, stop_t, F4, B4);
     } else {
-      ABCD_LAUNCH("composite", composite_kernel<false>, blocks, kBlock, 0, stream, npix, img, tab,
-                  plan, reinterpret_cast<float4*>(F), reinterpret_cast<float4*>(B));
+      ABCD_LAUNCH("composite", (composite_kernel<false, false>), blocks, kBlock, 0, stream, npix,
+                  width, img, tab, plan, r4, stop_t, F4, B4);
     }
     ABCD_HIP(hipGetLastError());
     fi += plan.nf;

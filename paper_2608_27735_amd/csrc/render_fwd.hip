@@ -20,7 +20,7 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
     float4* __restrict__ out, float* __restrict__ final_T, uint32_t* __restrict__ last,
     unsigned long long* __restrict__ n_blends, const uint32_t* __restrict__ order,
-    uint2* __restrict__ out16) {
+    uint2* __restrict__ out16, int* __restrict__ rect, int fb_stop) {
   __shared__ float4 s_ga[256];  // u, v, qa, qb
   __shared__ float4 s_gb[256];  // qc, o, r, g
   __shared__ float s_bl[256];   // b
@@ -39,6 +39,15 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
   float T = 1.0f, cr = 0.0f, cg = 0.0f, cb = 0.0f;
   uint32_t lastk = 0, nb = 0;
   bool done = !inside;
+  // Stop threshold on the next transmittance. The compositing-aware rule
+  // (1 - F_a) T_next < t_min is applied as T_next < t_min / (1 - F_a); a pixel
+  // whose F leaves it less than t_min of weight blends nothing.
+  float thr = k.t_min;
+  if (!kHalf && fb_stop && F && inside) {
+    const float vis = 1.0f - F[(int64_t)py * k.width + px].w;
+    thr = vis > 0.0f ? k.t_min / vis : __builtin_huge_valf();
+    done = vis < k.t_min;
+  }
   if (tid == 0) s_nb = 0;
   Rec rec = load_rec(values, start + tid, start + tid < end, means2d, conic_opacity, rgb);
   for (uint32_t b0 = start; b0 < end; b0 += 256) {
@@ -82,7 +91,7 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
                                           gb[i].y, k.alpha_min, k.alpha_max);
           const float Tn = T * (1.0f - ae.alpha);
           const bool hit = !done && !ae.skip;
-          const bool stop = hit && Tn < k.t_min;
+          const bool stop = hit && Tn < thr;
           const bool blend = hit && !stop;
           done = done || stop;
           const float wgt = blend ? ae.alpha * T : 0.0f;
@@ -98,6 +107,16 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
       if (jl >= 0) lastk = (uint32_t)s_pos[jl] + 1;
     }
     // s_wcnt is rewritten only after the next barrier
+  }
+  if (kHalf && rect) {
+    // coverage of the cached image: tiles holding any pixel that blended
+    if (__syncthreads_or(inside && T < 1.0f) && tid == 0) {
+      const int tx = tile % k.ntx, ty = tile / k.ntx;
+      atomicMin(&rect[0], tx * kTile);
+      atomicMin(&rect[1], ty * kTile);
+      atomicMax(&rect[2], min(tx * kTile + kTile, k.width));
+      atomicMax(&rect[3], min(ty * kTile + kTile, k.height));
+    }
   }
   if (inside) {
     const int64_t p = (int64_t)py * k.width + px;
@@ -123,6 +142,15 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
   }
 }
 
+__global__ void rect_init_kernel(int* __restrict__ rect, int width, int height) {
+  if (threadIdx.x == 0) {
+    rect[0] = width;
+    rect[1] = height;
+    rect[2] = 0;
+    rect[3] = 0;
+  }
+}
+
 }  // namespace
 
 int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
@@ -137,7 +165,8 @@ int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
               values_sorted, reinterpret_cast<const float2*>(means2d),
               reinterpret_cast<const float4*>(conic_opacity), rgb,
               reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B),
-              reinterpret_cast<float4*>(out_rgba), final_T, last, n_blends, tile_order, nullptr);
+              reinterpret_cast<float4*>(out_rgba), final_T, last, n_blends, tile_order, nullptr,
+              nullptr, (int)(prm.flags & ABCD_FLAG_FB_STOP));
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }
@@ -146,13 +175,17 @@ int32_t launch_render_cache(const abcd_camera& cam, const abcd_raster_params& pr
                             const uint32_t* tile_ranges, const uint32_t* tile_order,
                             const uint32_t* values_sorted, const float* means2d,
                             const float* conic_opacity, const float* rgb, uint16_t* image_f16,
-                            hipStream_t stream) {
+                            int32_t* rect, hipStream_t stream) {
   const BlendConsts k = consts(cam, prm);
   const int grid = tile_order ? k.ntiles : 8 * k.per_xcd;
+  if (rect) {
+    ABCD_LAUNCH("cache_rect_init", rect_init_kernel, 1, 64, 0, stream, rect, k.width, k.height);
+    ABCD_HIP(hipGetLastError());
+  }
   ABCD_LAUNCH("render_cache", render_fwd_kernel<true>, grid, kBlock, 0, stream, k, tile_ranges,
               values_sorted, reinterpret_cast<const float2*>(means2d),
               reinterpret_cast<const float4*>(conic_opacity), rgb, nullptr, nullptr, nullptr,
-              nullptr, nullptr, nullptr, tile_order, reinterpret_cast<uint2*>(image_f16));
+              nullptr, nullptr, nullptr, tile_order, reinterpret_cast<uint2*>(image_f16), rect, 0);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }

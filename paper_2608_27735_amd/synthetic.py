@@ -224,6 +224,18 @@ def background_pair(r, height, width):
     return f, b
 
 
+def dense_front(r, height, width, opaque_frac=0.2):
+    """A premultiplied F that hides much of the frame: alpha uniform on
+    [0.85, 1) over the left 70% of the columns, exactly 1 on a random
+    `opaque_frac` of those pixels, 0.3 elsewhere; colour uniform on [0, 1]."""
+    a = np.full((height, width, 1), 0.3, np.float32)
+    cut = int(0.7 * width)
+    a[:, :cut, 0] = r.uniform(0.85, 1.0, (height, cut))
+    a[:, :cut, 0][r.uniform(0, 1, (height, cut)) < opaque_frac] = 1.0
+    c = r.uniform(0.0, 1.0, (height, width, 3)).astype(np.float32)
+    return np.concatenate([c * a, a], -1).astype(np.float32)
+
+
 def upstream_grad(r, height, width, scale=1.0):
     """A smooth-free random dL/dout [H, W, 4]."""
     return (scale * r.normal(0.0, 1.0, (height, width, 4))).astype(np.float32)
@@ -256,12 +268,15 @@ def splats_2d(r, n, width, height, sigma_px=(1.0, 12.0), depth_range=(0.5, 20.0)
                 depth=depth.astype(f), radius=rad.astype(f), rgb=rgb.astype(f))
 
 
-def cached_images_device(k, height, width, seed, device, coverage=0.35, alpha_max=0.9):
+def cached_images_device(k, height, width, seed, device, coverage=0.35, alpha_max=0.9,
+                         with_rects=False):
     """k premultiplied fp16 RGBA cached renders [k, H, W, 4] drawn on the GPU
     with a seeded torch generator (for workloads too large to draw on the
     host): per layer a random axis-aligned rectangle covering about
     `coverage` of the frame, alpha uniform on [0, alpha_max] inside, colour
-    uniform on [0, 1], zero outside."""
+    uniform on [0, 1], zero outside. with_rects also returns each layer's
+    rectangle rounded out to 16-pixel tiles (int32 [k, 4] = x0, y0, x1, y1 on
+    the device), the coverage box a cached render comes with."""
     import torch
 
     g = torch.Generator(device=device)
@@ -270,6 +285,7 @@ def cached_images_device(k, height, width, seed, device, coverage=0.35, alpha_ma
     side = math.sqrt(coverage)
     hh, ww = max(1, int(height * side)), max(1, int(width * side))
     corners = torch.rand((k, 2), generator=g, device=device)
+    boxes = []
     for j in range(k):
         h0 = int(corners[j, 0].item() * (height - hh + 1))
         w0 = int(corners[j, 1].item() * (width - ww + 1))
@@ -277,4 +293,8 @@ def cached_images_device(k, height, width, seed, device, coverage=0.35, alpha_ma
         c = torch.rand((hh, ww, 3), generator=g, device=device)
         out[j, h0:h0 + hh, w0:w0 + ww, :3] = (c * a).half()
         out[j, h0:h0 + hh, w0:w0 + ww, 3:] = a.half()
+        boxes.append((w0 // 16 * 16, h0 // 16 * 16, min(width, -(-(w0 + ww) // 16) * 16),
+                      min(height, -(-(h0 + hh) // 16) * 16)))
+    if with_rects:
+        return out, torch.tensor(boxes, dtype=torch.int32, device=device).reshape(k, 4)
     return out

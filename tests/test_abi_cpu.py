@@ -83,7 +83,7 @@ FAKE = 0x1000  # never dereferenced: every call below fails validation first
     lambda c, p: setattr(c, "fx", float("nan")),
     lambda c, p: setattr(p, "sh_degree", 4),
     lambda c, p: setattr(p, "alpha_max", 1.0),
-    lambda c, p: setattr(p, "flags", 1),
+    lambda c, p: setattr(p, "flags", 2),  # unknown flag bit
     lambda c, p: (setattr(c, "width", 16 * 400), setattr(c, "height", 16 * 100)),  # 40000 tiles
 ])
 def test_project_rejects_bad_camera_or_params(lib, mutate):
@@ -135,14 +135,21 @@ def test_bin_sort_rejects_small_or_misaligned_workspace(lib):
 
 
 def test_composite_rejects_bad_order(lib):
+    def call(k, order, n_front, F=FAKE, rects=None, stop_t=0.0):
+        return lib.abcd_composite_cache(8, 8, k, FAKE, order, n_front, rects, stop_t, F, FAKE, 0,
+                                        None)
     order = (C.c_int32 * 3)(0, 0, 2)
-    assert lib.abcd_composite_cache(8, 8, 3, FAKE, order, 1, FAKE, FAKE, 0, None) == 1
+    assert call(3, order, 1) == 1
     order = (C.c_int32 * 3)(0, 1, 3)
-    assert lib.abcd_composite_cache(8, 8, 3, FAKE, order, 1, FAKE, FAKE, 0, None) == 1
+    assert call(3, order, 1) == 1
     order = (C.c_int32 * 3)(2, 1, 0)
-    assert lib.abcd_composite_cache(8, 8, 3, FAKE, order, 4, FAKE, FAKE, 0, None) == 1
-    assert lib.abcd_composite_cache(8, 8, -1, FAKE, order, 0, FAKE, FAKE, 0, None) == 1
-    assert lib.abcd_composite_cache(8, 8, 3, FAKE, order, 1, None, FAKE, 0, None) == 1
+    assert call(3, order, 4) == 1
+    assert call(-1, order, 0) == 1
+    assert call(3, order, 1, F=None) == 1
+    assert call(3, order, 1, rects=FAKE + 4) == 1   # rects misaligned
+    assert call(3, order, 1, stop_t=-0.1) == 1
+    assert call(3, order, 1, stop_t=1.0) == 1
+    assert call(3, order, 1, stop_t=float("nan")) == 1
 
 
 def test_render_calls_reject_bad_arguments(lib):
@@ -153,11 +160,14 @@ def test_render_calls_reject_bad_arguments(lib):
     args = [FAKE] * 12
     args[6] = FAKE + 4  # F misaligned
     assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, None) == 1
-    cache = [FAKE] * 7
+    cache = [FAKE] * 7 + [None]
     cache[6] = None  # image
     assert lib.abcd_render_cache(C.byref(c), C.byref(p), *cache, None) == 1
-    cache = [FAKE] * 7
+    cache = [FAKE] * 7 + [None]
     cache[6] = FAKE + 2  # image misaligned
+    assert lib.abcd_render_cache(C.byref(c), C.byref(p), *cache, None) == 1
+    cache = [FAKE] * 8
+    cache[7] = FAKE + 2  # rect misaligned
     assert lib.abcd_render_cache(C.byref(c), C.byref(p), *cache, None) == 1
     bwd = [FAKE] * 16 + [FAKE, 1 << 20] + [FAKE] * 6 + [0, None]
     bwd[13] = None  # final_T

@@ -259,12 +259,15 @@ def test_cache_refresh_to_pinned_host(api):
     hosts = [torch.full((H, W, 4), float("nan"), dtype=torch.float16).pin_memory()
              for _ in cams]
     ref = CacheRefresher(prm, params, W, H)
-    ref.refresh(cams, hosts)
-    for cam, h in zip(cams, hosts):
+    rects = torch.zeros((len(cams), 4), dtype=torch.int32, device=dev())
+    ref.refresh(cams, hosts, rects)
+    for i, (cam, h) in enumerate(zip(cams, hosts)):
         pd = api.project(cam, prm, **params)
         bins = api.bin_sort(W, H, pd)
-        want = api.render_cache(cam, prm, bins, pd).cpu()
+        rect = torch.zeros(4, dtype=torch.int32, device=dev())
+        want = api.render_cache(cam, prm, bins, pd, rect=rect).cpu()
         assert torch.equal(h.view(torch.int16), want.view(torch.int16))
+        assert torch.equal(rects[i], rect)
     assert any(h.float().abs().sum() > 0 for h in hosts)
 
 

@@ -1,0 +1,248 @@
+"""GPU parity of the visibility-aware variants (Limitations section: renders
+hidden behind near-opaque layers, and the parts of the frame a partition does
+not cover, need no work):
+  - the compositing-aware stop (ABCD_FLAG_FB_STOP) in the forward and, through
+    the forward's final_T and last, the backward: same bars as the plain path
+    (forward max abs <= 1e-5 off knife-edge pixels, walk lengths bit-exact
+    there, gradients <= 1e-4 relative L2);
+  - the collapse with coverage boxes: bit-identical to the collapse without
+    them (skipping transparent layers is exact);
+  - the collapse with a stop threshold: <= 1e-5 against the oracle's rule off
+    the knife-edge pixels, chunk-invariant;
+  - the coverage box of a cached render: contains every non-zero pixel and
+    equals the tile box of the oracle's covered pixels.
+Every case prints its name before touching the GPU.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2608_27735_amd import synthetic as S
+
+pytestmark = pytest.mark.gpu
+
+FWD_TOL = 1e-5
+GRAD_TOL = 1e-4
+KNIFE = 1e-4
+
+
+@pytest.fixture(scope="module")
+def api():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2608_27735_amd import api as A
+    return A
+
+
+def dev():
+    return torch.device("cuda:0")
+
+
+def to_dev(d):
+    return {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev()) for k, v in d.items()}
+
+
+def np32(t):
+    return t.detach().cpu().numpy()
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+
+
+def cases():
+    out = []
+    w = S.tiny()
+    out.append(("tiny-active", w.cams[0], w.params, S.subset(w.scene, w.cell_of == w.active)))
+    r = S.ring()
+    out.append(("ring-active-cam3", r.cams[3], r.params, S.subset(r.scene, r.cell_of == r.active)))
+    out.append(("ring-all-cam5", r.cams[5], r.params, r.scene))
+    return out
+
+
+CASES = cases()
+
+
+def _flagged(prm):
+    import dataclasses
+    return dataclasses.replace(prm, fb_stop=True)
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_fb_stop_step_matches_oracle(api, case):
+    name, cam, prm0, scene = case
+    prm = _flagged(prm0)
+    say("fb_stop step", name, scene["means"].shape)
+    r = S.rng(51)
+    F = S.dense_front(r, cam.height, cam.width)
+    B = S.background_pair(r, cam.height, cam.width)[1]
+    G = S.upstream_grad(r, cam.height, cam.width)
+    ref0 = O.step(cam, prm, scene, F=F, B=B, rel_margin=KNIFE)
+    plain = O.step(cam, prm0, scene, F=F, B=B)
+    G = G * (~ref0["fwd"]["knife"])[..., None]
+    ref = O.step(cam, prm, scene, F=F, B=B, dL_dout=G.astype(np.float64))
+    params = to_dev(scene)
+    Fd, Bd = torch.from_numpy(F).to(dev()), torch.from_numpy(B).to(dev())
+    p = api.project(cam, prm, **params)
+    bins = api.bin_sort(cam.width, cam.height, p)
+    nb = torch.zeros(1, dtype=torch.int64, device=dev())
+    fw = api.render_fwd(cam, prm, bins, p, F=Fd, B=Bd, n_blends=nb)
+    grads = api.render_bwd(cam, prm, params, p, bins, fw, torch.from_numpy(G).to(dev()), F=Fd, B=Bd)
+    torch.cuda.synchronize()
+    knife = ref0["fwd"]["knife"]
+    err = np.abs(np32(fw["out"]) - ref0["fwd"]["out"]).max(axis=-1)
+    assert err[knife].max(initial=0.0) <= 0.02
+    assert knife.sum() <= max(8, 0.01 * knife.size)
+    print(f"  fwd max err {err[~knife].max():.2e}, knife {int(knife.sum())}, blends "
+          f"{int(nb.item())} (plain rule {plain['fwd']['n_blends']})")
+    assert err[~knife].max() <= FWD_TOL
+    assert np.array_equal(np32(fw["last"]).view(np.uint32)[~knife], ref0["fwd"]["last"][~knife])
+    assert abs(int(nb.item()) - ref0["fwd"]["n_blends"]) <= 4 * int(knife.sum())
+    assert ref0["fwd"]["n_blends"] < plain["fwd"]["n_blends"]  # the rule skipped work
+    for k in ("means", "log_scales", "quats", "opacity_logits", "sh"):
+        g = np32(grads[k]).astype(np.float64)
+        gr = ref["grads"][k]
+        rel = np.linalg.norm(g - gr) / max(np.linalg.norm(gr), 1e-30)
+        print(f"  grad {k}: rel L2 {rel:.2e}")
+        assert rel <= GRAD_TOL, (k, rel)
+
+
+def test_fb_stop_opaque_front_skips_everything(api):
+    w = S.tiny()
+    cam, prm = w.cams[0], _flagged(w.params)
+    say("fb_stop opaque front", cam.width, cam.height)
+    params = to_dev(w.scene)
+    r = S.rng(52)
+    F = S.premultiplied_images(r, 1, cam.height, cam.width, alpha_max=0.9, coverage=1.0)[0]
+    F[..., 3] = 1.0
+    B = S.background_pair(r, cam.height, cam.width)[1]
+    Fd, Bd = torch.from_numpy(F).to(dev()), torch.from_numpy(B).to(dev())
+    p = api.project(cam, prm, **params)
+    bins = api.bin_sort(cam.width, cam.height, p)
+    nb = torch.zeros(1, dtype=torch.int64, device=dev())
+    fw = api.render_fwd(cam, prm, bins, p, F=Fd, B=Bd, n_blends=nb)
+    torch.cuda.synchronize()
+    assert bins["n_isect"] > 0 and nb.item() == 0
+    assert torch.equal(fw["out"], Fd)
+    assert int(fw["last"].abs().sum().item()) == 0
+    assert torch.all(fw["final_T"] == 1.0)
+
+
+def _bbox_rects(imgs_f16):
+    """Exact per-image boxes of the non-zero pixels, (x0, y0, x1, y1)."""
+    k, H, W, _ = imgs_f16.shape
+    rects = np.zeros((k, 4), np.int32)
+    for j in range(k):
+        nz = np.any(imgs_f16[j] != 0, axis=-1)
+        ys, xs = np.nonzero(nz)
+        if len(xs):
+            rects[j] = (xs.min(), ys.min(), xs.max() + 1, ys.max() + 1)
+    return rects
+
+
+@pytest.mark.parametrize("k,n_front,hw", [(7, 3, (128, 128)), (63, 20, (64, 96)), (40, 40, (33, 17)),
+                                          (500, 211, (16, 24)), (9, 4, (37, 29))])
+def test_composite_with_rects_is_bit_identical(api, k, n_front, hw):
+    H, W = hw
+    say("composite rects", k, n_front, hw)
+    r = S.rng(70 + k)
+    imgs = S.half_bits(S.premultiplied_images(r, k, H, W, coverage=0.3))
+    order = list(r.permutation(k))
+    tight = _bbox_rects(imgs)
+    loose = tight.copy()  # rounded out to 16 pixels, as cached renders report them
+    loose[:, :2] = (loose[:, :2] // 16) * 16
+    loose[:, 2] = np.minimum(-(-loose[:, 2] // 16) * 16, W)
+    loose[:, 3] = np.minimum(-(-loose[:, 3] // 16) * 16, H)
+    loose[tight[:, 2] <= tight[:, 0]] = (W, H, 0, 0)
+    img_d = torch.from_numpy(imgs.view(np.int16)).to(dev())
+    F0, B0 = api.composite_cache(img_d, order, n_front)
+    for rects in (tight, loose):
+        Fr, Br = api.composite_cache(img_d, order, n_front, rects=torch.from_numpy(rects).to(dev()))
+        torch.cuda.synchronize()
+        assert torch.equal(Fr, F0) and torch.equal(Br, B0)
+    Fo, Bo = O.composite(W, H, imgs, order, n_front)
+    assert np.abs(np32(F0) - Fo).max() <= FWD_TOL and np.abs(np32(B0) - Bo).max() <= FWD_TOL
+
+
+@pytest.mark.parametrize("k,n_front,hw,st", [(24, 14, (64, 96), 0.02), (63, 30, (33, 17), 1e-3),
+                                             (200, 120, (16, 24), 0.05), (12, 0, (40, 40), 0.01)])
+def test_composite_stop_matches_oracle(api, k, n_front, hw, st):
+    H, W = hw
+    say("composite stop", k, n_front, hw, st)
+    r = S.rng(90 + k)
+    imgs = S.half_bits(S.premultiplied_images(r, k, H, W, alpha_max=0.9, coverage=0.8))
+    order = list(r.permutation(k))
+    Fo, Bo, knife = O.composite(W, H, imgs, order, n_front, stop_t=st, rel_margin=KNIFE,
+                                with_knife=True)
+    img_d = torch.from_numpy(imgs.view(np.int16)).to(dev())
+    rects = torch.from_numpy(_bbox_rects(imgs)).to(dev())
+    Fg, Bg = api.composite_cache(img_d, order, n_front, rects=rects, stop_t=st)
+    # streamed in three chunks (accumulate): the rule only looks back
+    cut = [0, k // 3, (2 * k) // 3, k]
+    Fc = torch.zeros((H, W, 4), device=dev())
+    Bc = torch.zeros((H, W, 4), device=dev())
+    for a, b in zip(cut[:-1], cut[1:]):
+        if b == a:
+            continue
+        nf = max(0, min(n_front, b) - a)
+        idx = torch.tensor(order[a:b], device=dev())
+        api.composite_cache(img_d[idx].contiguous(), list(range(b - a)), nf, F=Fc, B=Bc,
+                            accumulate=True, rects=rects[idx].contiguous(), stop_t=st)
+    torch.cuda.synchronize()
+    ok = ~knife
+    print(f"  knife-edge pixels {int(knife.sum())} of {H * W}")
+    assert knife.sum() <= max(8, 0.02 * H * W)
+    assert np.abs(np32(Fg) - Fo)[ok].max(initial=0.0) <= FWD_TOL
+    assert np.abs(np32(Bg) - Bo)[ok].max(initial=0.0) <= FWD_TOL
+    assert np.abs(np32(Fc) - np32(Fg))[ok].max(initial=0.0) <= FWD_TOL
+    assert np.abs(np32(Bc) - np32(Bg))[ok].max(initial=0.0) <= FWD_TOL
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_render_cache_rect(api, case):
+    name, cam, prm, scene = case
+    say("render_cache rect", name)
+    params = to_dev(scene)
+    p = api.project(cam, prm, **params)
+    bins = api.bin_sort(cam.width, cam.height, p)
+    rect = torch.full((4,), -7, dtype=torch.int32, device=dev())
+    img = api.render_cache(cam, prm, bins, p, rect=rect)
+    torch.cuda.synchronize()
+    x0, y0, x1, y1 = (int(v) for v in np32(rect))
+    im = np32(img)
+    nz = np.any(im != 0, axis=-1)
+    inside = np.zeros_like(nz)
+    inside[max(y0, 0):max(y1, 0), max(x0, 0):max(x1, 0)] = True
+    assert not np.any(nz & ~inside)
+    # against the oracle: the tile box of pixels that blend, knife-edge pixels either way
+    ref = O.step(cam, prm, scene, rel_margin=KNIFE)["fwd"]
+    cov, kn = ref["final_T"] < 1.0, ref["knife"]
+
+    def tile_box(mask):
+        ys, xs = np.nonzero(mask)
+        if not len(xs):
+            return None
+        return (xs.min() // 16 * 16, ys.min() // 16 * 16, min(cam.width, (xs.max() // 16 + 1) * 16),
+                min(cam.height, (ys.max() // 16 + 1) * 16))
+    lo, hi = tile_box(cov & ~kn), tile_box(cov | kn)
+    print(f"  rect {(x0, y0, x1, y1)}, oracle box {lo} .. {hi}")
+    if hi is None:
+        assert x1 <= x0
+        return
+    assert x0 <= lo[0] and y0 <= lo[1] and x1 >= lo[2] and y1 >= lo[3]
+    assert x0 >= hi[0] and y0 >= hi[1] and x1 <= hi[2] and y1 <= hi[3]
+
+
+def test_render_cache_empty_rect(api):
+    w = S.tiny()
+    cam, prm = w.cams[0], w.params
+    say("render_cache empty rect")
+    params = to_dev(S.subset(w.scene, np.zeros(len(w.scene["means"]), bool)))
+    p = api.project(cam, prm, **params)
+    bins = api.bin_sort(cam.width, cam.height, p)
+    rect = torch.full((4,), -7, dtype=torch.int32, device=dev())
+    img = api.render_cache(cam, prm, bins, p, rect=rect)
+    torch.cuda.synchronize()
+    x0, y0, x1, y1 = (int(v) for v in np32(rect))
+    assert x1 <= x0 and y1 <= y0
+    assert int(img.view(torch.int16).abs().sum().item()) == 0
