@@ -12,6 +12,7 @@
  * are runtime parameters here (abcd_raster_params).
  *
  * One step on one camera is
+ *   abcd_stage_cached     pinned host cache -> device chunk (per camera, in chunks)
  *   abcd_composite_cache  cached partition renders -> F, B (once per camera)
  *   abcd_project          parameters -> screen-space Gaussians
  *   abcd_bin_sort         -> per 16x16 tile, Gaussians sorted by (depth, index)
@@ -249,6 +250,22 @@ ABCD_API int32_t abcd_composite_cache(int32_t width, int32_t height, int32_t k, 
                              const int32_t* order /* host */, int32_t n_front,
                              const int32_t* rects, float stop_t, float* F, float* B,
                              int32_t accumulate, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Upload of cached renders from pinned host memory (Method section: the cache
+ * of camera-partition renders is kept in system memory or on disk, and the
+ * renders a camera needs go to the GPU when a block becomes active). For each
+ * j < k, copies the coverage box rects[j] (as in abcd_composite_cache; NULL:
+ * the whole image) of host_images[j] (fp16 RGBA [H][W][4] in pinned host
+ * memory) to the same pixels of dst[j] (device, [k][H][W][4]), as one 2D
+ * copy per image, asynchronously on `stream`. Pixels of dst outside the box
+ * keep their old contents, which abcd_composite_cache with the same rects
+ * never reads; an empty box copies nothing. host_images (k pointers) and rects
+ * ([k][4] int32) are host arrays; the host images must stay unchanged until
+ * the copies complete. A box outside the image is an error. */
+ABCD_API int32_t abcd_stage_cached(int32_t width, int32_t height, int32_t k,
+                          const uint16_t* const* host_images /* host */,
+                          const int32_t* rects /* host */, uint16_t* dst, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* L1 reconstruction loss gradient (the paper evaluates a reconstruction loss

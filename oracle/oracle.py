@@ -309,3 +309,40 @@ def step(cam, prm, scene, F=None, B=None, dL_dout=None, pos32=True, rel_margin=0
         res["grads"] = project_bwd(cam, prm, scene["means"], scene["log_scales"], scene["quats"],
                                    scene["opacity_logits"], scene["sh"], pb["tiles_touched"], g2d)
     return res
+
+
+# ------------------------------------------------------ frustum visibility
+
+def box_meets_frustum(cam, lo, hi):
+    """Whether the world-space box [lo, hi] meets the camera's view frustum
+    (points with view depth >= near whose projection lies in [0, W] x [0, H]),
+    by its definition: the intersection is non-empty iff some box point
+    satisfies every frustum half-space. Solved as a linear program that
+    maximises the smallest signed distance s of a box point to the frustum's
+    planes (unit normals); returns (s >= 0, s). |s| measures how far the case
+    is from touching."""
+    from scipy.optimize import linprog
+    R = np.asarray(cam.R, np.float64).reshape(3, 3)
+    t = np.asarray(cam.t, np.float64).reshape(3)
+    fx, fy, cx, cy = (float(v) for v in (cam.fx, cam.fy, cam.cx, cam.cy))
+    W, H = float(cam.width), float(cam.height)
+    # half-spaces n . p_cam + d >= 0 in camera space
+    planes = [((0.0, 0.0, 1.0), -float(cam.near)),      # in front of the near plane
+              ((fx, 0.0, cx), 0.0),                       # u >= 0
+              ((-fx, 0.0, W - cx), 0.0),                  # u <= W
+              ((0.0, fy, cy), 0.0),                       # v >= 0
+              ((0.0, -fy, H - cy), 0.0)]                  # v <= H
+    A, b = [], []
+    for n, d in planes:
+        n = np.asarray(n) / np.linalg.norm(n)
+        # n . (R x + t) + d >= s   <=>   -(n R) . x + s <= n . t + d
+        A.append(np.concatenate([-(n @ R), [1.0]]))
+        b.append(float(n @ t + d))
+    lo = np.asarray(lo, np.float64)
+    hi = np.asarray(hi, np.float64)
+    bounds = [(lo[i], hi[i]) for i in range(3)] + [(None, 1e6)]
+    res = linprog(np.array([0.0, 0.0, 0.0, -1.0]), A_ub=np.array(A), b_ub=np.array(b),
+                  bounds=bounds, method="highs")
+    assert res.status == 0, res.message
+    s = -res.fun
+    return s >= 0.0, s

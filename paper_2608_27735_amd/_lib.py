@@ -51,6 +51,8 @@ SIGNATURES = {
                         [_P, _SZ] + [_P] * 6 + [_I32, _P]),
     "abcd_composite_cache": (_I32, [_I32, _I32, _I32, _P, C.POINTER(C.c_int32), _I32, _P,
                                     C.c_float, _P, _P, _I32, _P]),
+    "abcd_stage_cached": (_I32, [_I32, _I32, _I32, C.POINTER(_P), C.POINTER(C.c_int32), _P,
+                                 _P]),
     "abcd_loss_l1_grad": (_I32, [_I32, _I32, _P, _P, C.POINTER(C.c_float), _P, _P, _P]),
     "abcd_adam_step": (_I32, [C.POINTER(abcd_adam_group), _I32, C.c_float, C.c_float, C.c_float,
                               _I64, _P]),

@@ -271,6 +271,32 @@ def composite_cache(images, order, n_front, F=None, B=None, accumulate=False, re
     return F, B
 
 
+def stage_cached(host_images, dst, rects=None):
+    """Copy pinned host fp16 images (a list of [H, W, 4] tensors) into the
+    device chunk dst [>= k, H, W, 4], only inside each image's coverage box
+    (rects: host int32 array [k, 4], or None for whole images), on the
+    current stream."""
+    k = len(host_images)
+    if k == 0:
+        return dst
+    H, W = dst.shape[1], dst.shape[2]
+    if dst.dtype not in (torch.float16, torch.int16) or not dst.is_cuda or \
+            not dst.is_contiguous() or dst.shape[0] < k or dst.shape[3] != 4:
+        raise ValueError("dst must be a contiguous fp16 GPU tensor [>= k, H, W, 4]")
+    for h in host_images:
+        if h.is_cuda or not h.is_pinned() or h.dtype not in (torch.float16, torch.int16) or \
+                tuple(h.shape) != (H, W, 4) or not h.is_contiguous():
+            raise ValueError("host images must be pinned contiguous fp16 [H, W, 4] tensors")
+    ptrs = (C.c_void_p * k)(*[h.data_ptr() for h in host_images])
+    r = None
+    if rects is not None:
+        import numpy as np
+        ra = np.ascontiguousarray(np.asarray(rects, dtype=np.int32).reshape(-1, 4)[:k])
+        r = ra.ctypes.data_as(C.POINTER(C.c_int32))
+    check(_lib.load().abcd_stage_cached(W, H, k, ptrs, r, _ptr(dst), _stream()))
+    return dst
+
+
 def loss_l1_grad(out, target, bg=None, dL_dout=None, loss=None):
     H, W = out.shape[:2]
     _need(out, "out", torch.float32, (H, W, 4))
@@ -304,4 +330,4 @@ def timing_read(kernel):
 __all__ = ["AbcdError", "project", "bin_sort", "bin_sort_workspace_size", "render_fwd",
            "render_bwd", "render_bwd_workspace_size", "composite_cache", "loss_l1_grad",
            "timing_enable", "timing_reset", "timing_read", "version", "n_tiles", "adam_step",
-           "render_cache"]
+           "render_cache", "stage_cached"]

@@ -227,6 +227,10 @@ int32_t launch_tile_walk(int width, int height, const uint32_t* last, uint32_t* 
 int32_t launch_adam(const abcd_adam_group* groups, int ngroups, float beta1, float beta2, float eps,
                     int64_t t, hipStream_t stream);
 
+// staging.hip
+int32_t stage_cached(int width, int height, int k, const uint16_t* const* host_images,
+                     const int32_t* rects, uint16_t* dst, hipStream_t stream);
+
 // composite.hip
 int32_t launch_composite(int width, int height, int k, const uint16_t* images,
                          const int32_t* order, int n_front, const int32_t* rects, float stop_t,

@@ -283,6 +283,24 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
                             accumulate, stream);
 }
 
+int32_t abcd_stage_cached(int32_t width, int32_t height, int32_t k,
+                          const uint16_t* const* host_images, const int32_t* rects,
+                          uint16_t* dst, hipStream_t stream) {
+  REQUIRE(width > 0 && height > 0, "image size must be positive");
+  REQUIRE(k >= 0, "k must be >= 0");
+  if (k == 0) return ABCD_OK;
+  REQUIRE(host_images && dst, "host_images or dst is NULL");
+  for (int j = 0; j < k; ++j) {
+    REQUIRE(host_images[j] != nullptr, "host_images[%d] is NULL", j);
+    if (!rects) continue;
+    const int32_t* r = rects + 4 * j;
+    REQUIRE(r[0] >= 0 && r[1] >= 0 && r[2] <= width && r[3] <= height,
+            "rect %d (%d, %d, %d, %d) leaves the %dx%d image", j, r[0], r[1], r[2], r[3], width,
+            height);
+  }
+  return stage_cached(width, height, k, host_images, rects, dst, stream);
+}
+
 int32_t abcd_composite_cache(int32_t width, int32_t height, int32_t k, const uint16_t* images,
                              const int32_t* order, int32_t n_front, const int32_t* rects,
                              float stop_t, float* F, float* B, int32_t accumulate,

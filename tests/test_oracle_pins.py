@@ -832,3 +832,56 @@ def test_collapse_stop_is_chunk_invariant_and_bounded():
     d = np.abs(over(F1, B1) - over(Fe, Be))
     assert d.max() <= 2 * st
     assert d.max() > 0  # layers were dropped
+
+
+# ------------------------------------------------- frustum visibility (f3)
+
+def test_frustum_oracle_closed_cases():
+    """A box around the viewed point is inside; one behind the camera, one past
+    each image edge at a known depth are outside; their margins match the
+    geometry."""
+    cam = axis_camera(64, 48, f=50.0)  # camera at the origin looking down +z
+    ok, s = O.box_meets_frustum(cam, [-0.1, -0.1, 4.9], [0.1, 0.1, 5.1])
+    assert ok and s > 0
+    ok, s = O.box_meets_frustum(cam, [-1, -1, -3], [1, 1, -1])
+    assert not ok
+    # at depth z the image spans x in [-cx z / fx, (W - cx) z / fx]
+    z = 5.0
+    xl = -cam.cx * z / cam.fx
+    ok, _ = O.box_meets_frustum(cam, [xl - 0.5, -0.1, z], [xl - 0.05, 0.1, z])
+    assert not ok
+    ok, _ = O.box_meets_frustum(cam, [xl - 0.5, -0.1, z], [xl + 0.05, 0.1, z])
+    assert ok
+    yb = (cam.height - cam.cy) * z / cam.fy
+    ok, _ = O.box_meets_frustum(cam, [-0.1, yb + 0.05, z], [0.1, yb + 0.5, z])
+    assert not ok
+    # between the camera and the near plane only
+    ok, s = O.box_meets_frustum(cam, [-0.01, -0.01, 0.0], [0.01, 0.01, cam.near * 0.5])
+    assert not ok and s < 0
+
+
+def test_frustum_oracle_agrees_with_point_sampling():
+    """Any sampled box point that projects into the image in front of the near
+    plane proves visibility; boxes the oracle calls visible with a clear
+    margin contain such points at a fine enough sampling."""
+    r = S.rng(29)
+    cam = look_at((3.0, -4.0, 2.0), (0.0, 0.0, 0.5), 80, 60)
+    R = np.asarray(cam.R, np.float64)
+    t = np.asarray(cam.t, np.float64)
+    g = np.linspace(0, 1, 9)
+    unit = np.stack(np.meshgrid(g, g, g, indexing="ij"), -1).reshape(-1, 3)
+    for _ in range(60):
+        c = r.uniform(-6, 6, 3)
+        ext = r.uniform(0.05, 1.5, 3)
+        lo, hi = c - ext, c + ext
+        ok, s = O.box_meets_frustum(cam, lo, hi)
+        p = (lo + unit * (hi - lo)) @ R.T + t
+        z = p[:, 2]
+        with np.errstate(divide="ignore", invalid="ignore"):
+            u = cam.fx * p[:, 0] / z + cam.cx
+            v = cam.fy * p[:, 1] / z + cam.cy
+        hit = np.any((z >= cam.near) & (u >= 0) & (u <= cam.width) & (v >= 0) & (v <= cam.height))
+        if hit:
+            assert ok
+        if ok and s > 0.2:
+            assert hit
