@@ -159,7 +159,7 @@ def main():
     blends_step = st.n_blends.item() / args.steps
     value = blends_step / (ms_step / 1e3)
 
-    graph = small = optimizer = cache_refresh = visibility = hierarchy = None
+    graph = small = optimizer = cache_refresh = visibility = hierarchy = comparison = None
     if args.extras:
         # the same step replayed as one HIP graph (collapse + step captured once)
         st.capture(target, F=F, B=B,
@@ -253,6 +253,19 @@ def main():
                          note="F/B built from pinned host memory; coverage boxes only cross "
                               "PCIe; device memory = two staging chunks + F/B")
         del hcache, streamer, Fh, Bh
+
+        # the paper's three training setups on the 64K-Gaussian ring scene (4x4x4
+        # grid, 8 cameras at 512x512) with a known ground truth: targets are
+        # joint renders of the scene, training starts from a perturbed copy;
+        # every setup gives each Gaussian the same number of Adam steps
+        from paper_2608_27735_amd import train as TR
+        rw = S.ring()
+        comparison = TR.compare(rw.scene, S.perturbed(S.rng(5), rw.scene), rw.grid, rw.cell_of,
+                                rw.cams, rw.params, epochs=2, T=20)
+        comparison = dict(workload="64K Gaussians (SH 3), 4x4x4 grid, 8 cameras at 512x512; "
+                                   "targets = joint renders of the ground truth; init = means "
+                                   "jittered, opacity lowered, colours grey",
+                          epochs=2, steps_per_gaussian=40, **comparison)
 
         # launch-bound regime (Results section: small active partitions leave the
         # rasterizer underused and launch costs dominate): the 512-Gaussian active
@@ -388,6 +401,7 @@ def main():
         "cache_refresh": cache_refresh,
         "visibility": visibility,
         "hierarchy": hierarchy,
+        "comparison": comparison,
         "small_config": small,
         "kernels": kern,
         "setup_s": setup_s,

@@ -54,11 +54,16 @@ class ActiveBlockStep:
                          tile_order=self.tile_order)
 
     def project_and_bin(self, sync=False):
+        """With sync=True the intersection count is read back and the buffers
+        grow when a camera needs more; without, the capacity must suffice."""
         api.project(self.cam, self.prm, **self.params, out=self.proj)
         b = api.bin_sort(self.cam.width, self.cam.height, self.proj, capacity=self.capacity,
                          workspace=self.bin_ws, values=self.values, tile_ranges=self.tile_ranges,
                          tile_order=self.tile_order,
                          sync=sync)
+        if sync and b["values"] is not self.values:
+            self.values, self.bin_ws, self.capacity = b["values"], b["workspace"], b["capacity"]
+            self.bins["values"] = self.values
         return b["n_isect"]
 
     def forward(self, F=None, B=None):

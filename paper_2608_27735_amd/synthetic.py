@@ -193,6 +193,17 @@ def active_block_1m(seed=41, n=1_000_000, width=1297, height=840, heavy_tail=Fal
                     params=RasterParams(sh_degree=3))
 
 
+def perturbed(r, scene, pos_sd=0.01, logit_shift=-1.0):
+    """A starting point for training towards `scene`: means moved by N(0,
+    pos_sd), opacity logits shifted by logit_shift, colours reset to the
+    middle grey (SH DC 0, higher bands 0); scales and rotations kept."""
+    out = {k: np.array(v, copy=True) for k, v in scene.items()}
+    out["means"] = (out["means"] + r.normal(0.0, pos_sd, out["means"].shape)).astype(np.float32)
+    out["opacity_logits"] = (out["opacity_logits"] + logit_shift).astype(np.float32)
+    out["sh"] = np.zeros_like(out["sh"])
+    return out
+
+
 # ----------------------------------------------------------- image inputs
 
 def premultiplied_images(r, k, height, width, alpha_max=0.95, coverage=0.5):
