@@ -154,6 +154,32 @@ ABCD_API int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const f
                       int64_t* n_isect /* host */, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* Split of long tiles between the forward and the backward (a scheduling
+ * choice of this library; the paper's renderer is unchanged). The backward of
+ * a tile walks its list back to front; a tile with a list of many thousand
+ * entries would keep one workgroup busy after the rest of the GPU is idle.
+ * With a split, whenever a tile's walk in the forward crosses a chunk
+ * boundary (every `chunk` list positions, more for lists longer than 64
+ * chunks) it takes a 4 KB slot and stores each pixel's transmittance and
+ * colour there, plus one slot for the end of the walk; the backward then
+ * processes each (tile, chunk) as its own work item, starting from those
+ * states. Slots are taken in the forward's tile order (heaviest first); a
+ * tile that finds none left is not split. The same split must be given to a
+ * forward and its backward; results agree with the unsplit backward up to
+ * rounding.
+ * workspace: device memory of abcd_split_workspace_size(n_slots) bytes (or
+ * more: the slots that fit are used), 256-byte aligned; chunk: a positive
+ * multiple of 256. Slots a frame needs: about (sum over tiles of the longest
+ * walk in the tile) / chunk + (number of tiles split). */
+typedef struct {
+  void* workspace;
+  size_t bytes;
+  int32_t chunk;
+  int32_t reserved;
+} abcd_split;
+ABCD_API int32_t abcd_split_workspace_size(int64_t n_slots, size_t* bytes);
+
+/* ------------------------------------------------------------------------ */
 /* Forward render and composite (Method section: F over active over B).
  *
  * Per pixel, front to back over its tile's list, starting from T = 1, C = 0:
@@ -171,13 +197,14 @@ ABCD_API int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const f
  * tile_order (may be NULL): the order in which workgroups take tiles, a
  * permutation of the tiles such as abcd_bin_sort's tile_order (heaviest
  * first balances the GPU); it changes no output. NULL takes tiles in raster
- * order. */
+ * order. split (host, may be NULL): see abcd_split. */
 ABCD_API int32_t abcd_render_fwd(const abcd_camera* cam /* host */, const abcd_raster_params* prm /* host */,
                         const uint32_t* tile_ranges, const uint32_t* tile_order,
                         const uint32_t* values_sorted,
                         const float* means2d, const float* conic_opacity, const float* rgb,
                         const float* F, const float* B, float* out_rgba, float* final_T,
-                        uint32_t* last, unsigned long long* n_blends, hipStream_t stream);
+                        uint32_t* last, unsigned long long* n_blends, const abcd_split* split,
+                        hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Cached render of a partition (Method section: the frozen partitions' renders
@@ -209,9 +236,9 @@ ABCD_API int32_t abcd_render_cache(const abcd_camera* cam /* host */,
  * forward above, including zero derivative of a clamped alpha and of a
  * clamped colour. Inputs are those of the forward call on the same camera.
  * workspace: at least abcd_render_bwd_workspace_size(n) bytes, 256-byte
- * aligned (screen-space gradients, 36 bytes per Gaussian, and the tile
- * schedule of the backward, heaviest walk first, 8 bytes per tile at the
- * maximum tile count). */
+ * aligned (screen-space gradients, 36 bytes per Gaussian, and the work
+ * schedule of the backward, heaviest walk first, 16 bytes per tile at the
+ * maximum tile count). split (host, may be NULL): the one the forward used. */
 ABCD_API int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes);
 ABCD_API int32_t abcd_render_bwd(const abcd_camera* cam /* host */, const abcd_raster_params* prm /* host */,
                         int64_t n, const float* means, const float* log_scales, const float* quats,
@@ -221,7 +248,8 @@ ABCD_API int32_t abcd_render_bwd(const abcd_camera* cam /* host */, const abcd_r
                         const float* F, const float* B, const float* final_T, const uint32_t* last,
                         const float* dL_dout, void* workspace, size_t ws_bytes, float* d_means,
                         float* d_log_scales, float* d_quats, float* d_opacity_logits, float* d_sh,
-                        float* d_means2d, int32_t accumulate, hipStream_t stream);
+                        float* d_means2d, int32_t accumulate, const abcd_split* split,
+                        hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Collapse of cached partition renders into F and B (Abstract; Method section:

@@ -34,6 +34,11 @@ class abcd_adam_group(C.Structure):
                 ("exp_avg_sq", C.c_void_p), ("count", C.c_int64), ("lr", C.c_float)]
 
 
+class abcd_split(C.Structure):
+    _fields_ = [("workspace", C.c_void_p), ("bytes", C.c_size_t), ("chunk", C.c_int32),
+                ("reserved", C.c_int32)]
+
+
 _P = C.c_void_p  # device pointers travel as integers
 _I32, _I64, _SZ = C.c_int32, C.c_int64, C.c_size_t
 _CAM, _PRM = C.POINTER(abcd_camera), C.POINTER(abcd_raster_params)
@@ -44,11 +49,12 @@ SIGNATURES = {
     "abcd_bin_sort_workspace_size": (_I32, [_I64, _I64, _I32, _I32, C.POINTER(_SZ)]),
     "abcd_bin_sort": (_I32, [_I32, _I32, _I64, _P, _P, _P, _P, _I64, _P, _SZ, _P, _P, _P, _P,
                              C.POINTER(_I64), _P]),
-    "abcd_render_fwd": (_I32, [_CAM, _PRM] + [_P] * 12 + [_P]),
+    "abcd_render_fwd": (_I32, [_CAM, _PRM] + [_P] * 12 + [C.POINTER(abcd_split), _P]),
+    "abcd_split_workspace_size": (_I32, [_I64, C.POINTER(_SZ)]),
     "abcd_render_cache": (_I32, [_CAM, _PRM] + [_P] * 8 + [_P]),
     "abcd_render_bwd_workspace_size": (_I32, [_I64, C.POINTER(_SZ)]),
     "abcd_render_bwd": (_I32, [_CAM, _PRM, _I64] + [_P] * 5 + [_P] * 4 + [_P] * 2 + [_P] * 5 +
-                        [_P, _SZ] + [_P] * 6 + [_I32, _P]),
+                        [_P, _SZ] + [_P] * 6 + [_I32, C.POINTER(abcd_split), _P]),
     "abcd_composite_cache": (_I32, [_I32, _I32, _I32, _P, C.POINTER(C.c_int32), _I32, _P,
                                     C.c_float, _P, _P, _I32, _P]),
     "abcd_stage_cached": (_I32, [_I32, _I32, _I32, C.POINTER(_P), C.POINTER(C.c_int32), _P,

@@ -143,8 +143,32 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
 
 # -------------------------------------------------------------- rasterise
 
-def render_fwd(cam, prm, bins, proj, F=None, B=None, n_blends=None, out=None):
-    """out = F over A over B; returns dict(out, final_T, last)."""
+def split_workspace_size(n_slots):
+    sz = C.c_size_t(0)
+    check(_lib.load().abcd_split_workspace_size(int(n_slots), C.byref(sz)))
+    return sz.value
+
+
+def make_split(n_slots, chunk=2048, device=None):
+    """A split workspace (see abcd_split) with n_slots checkpoint slots; give
+    the same one to a forward and its backward."""
+    dev = device or torch.device("cuda", torch.cuda.current_device())
+    ws = torch.empty(split_workspace_size(n_slots), dtype=torch.uint8, device=dev)
+    return dict(workspace=ws, chunk=int(chunk))
+
+
+def _split_struct(split):
+    if split is None:
+        return None
+    ws = split["workspace"]
+    if not ws.is_cuda or ws.dtype != torch.uint8:
+        raise ValueError("split workspace must be a uint8 GPU tensor")
+    return C.byref(_lib.abcd_split(ws.data_ptr(), ws.numel(), int(split["chunk"]), 0))
+
+
+def render_fwd(cam, prm, bins, proj, F=None, B=None, n_blends=None, out=None, split=None):
+    """out = F over A over B; returns dict(out, final_T, last). split: see
+    make_split (the backward must get the same one)."""
     H, W = cam.height, cam.width
     dev = proj["means2d"].device
     _opt(F, "F", torch.float32, (H, W, 4))
@@ -159,7 +183,7 @@ def render_fwd(cam, prm, bins, proj, F=None, B=None, n_blends=None, out=None):
                               _ptr(bins["tile_ranges"]), _ptr(bins.get("tile_order")),
                               _ptr(bins["values"]), _ptr(proj["means2d"]), _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]),
                               _ptr(F), _ptr(B), _ptr(out["out"]), _ptr(out["final_T"]),
-                              _ptr(out["last"]), _ptr(n_blends), _stream()))
+                              _ptr(out["last"]), _ptr(n_blends), _split_struct(split), _stream()))
     return out
 
 
@@ -187,7 +211,7 @@ def render_bwd_workspace_size(n):
 
 
 def render_bwd(cam, prm, params, proj, bins, fwd, dL_dout, F=None, B=None, workspace=None,
-               grads=None, accumulate=False, want_means2d=False):
+               grads=None, accumulate=False, want_means2d=False, split=None):
     """Gradients of the active parameters; returns dict(means, log_scales, quats,
     opacity_logits, sh[, means2d])."""
     n = params["means"].shape[0]
@@ -213,7 +237,8 @@ def render_bwd(cam, prm, params, proj, bins, fwd, dL_dout, F=None, B=None, works
         _ptr(bins["tile_ranges"]), _ptr(bins["values"]), _ptr(F), _ptr(B), _ptr(fwd["final_T"]),
         _ptr(fwd["last"]), _ptr(dL_dout), _ptr(workspace), workspace.numel(), _ptr(grads["means"]),
         _ptr(grads["log_scales"]), _ptr(grads["quats"]), _ptr(grads["opacity_logits"]),
-        _ptr(grads["sh"]), _ptr(grads.get("means2d")), 1 if accumulate else 0, _stream()))
+        _ptr(grads["sh"]), _ptr(grads.get("means2d")), 1 if accumulate else 0,
+        _split_struct(split), _stream()))
     return grads
 
 
@@ -330,4 +355,4 @@ def timing_read(kernel):
 __all__ = ["AbcdError", "project", "bin_sort", "bin_sort_workspace_size", "render_fwd",
            "render_bwd", "render_bwd_workspace_size", "composite_cache", "loss_l1_grad",
            "timing_enable", "timing_reset", "timing_read", "version", "n_tiles", "adam_step",
-           "render_cache", "stage_cached"]
+           "render_cache", "stage_cached", "make_split", "split_workspace_size"]

@@ -169,6 +169,69 @@ __device__ __forceinline__ unsigned int wave_sum_u32(unsigned int x) {
   return x;
 }
 
+// ------------------------------------------------------ split workspace
+
+// Long tiles are split for the backward: while a tile's walk crosses every
+// ch_t-th position of its list, the forward stores each pixel's transmittance
+// and colour there (and, for a tile that crossed one, at the end of its walk),
+// and the backward processes each (tile, chunk) as a work item of its own.
+// Slots are taken as the walks cross boundaries, so memory follows the walks,
+// not the list lengths; a tile that finds no free slot is not split. Layout
+// of the caller's workspace:
+//   hdr[16]                  [0] checkpoint slots taken
+//   slot_of[MAX][kMaxChunks] per tile: [0] end-of-walk slot, [b] boundary b
+//   items[MAX + slots]       backward work items (tile, chunk), 8 bytes each
+//   ckpt[slots][256]         (T, C_r, C_g, C_b) per pixel, 256-byte aligned
+constexpr uint32_t kNoSlot = 0xFFFFFFFFu;
+constexpr uint32_t kMaxChunks = 64;
+
+struct SplitLayout {
+  uint32_t* hdr;
+  uint32_t* slot_of;
+  uint2* items;
+  float4* ckpt;
+  uint32_t nslots;
+  int ch;  // minimum list positions per chunk; 0: no split
+};
+
+// Chunk length of a tile with a list of `len` entries: at least ch, and long
+// enough that the list has at most kMaxChunks chunks (a multiple of 256).
+__host__ __device__ inline uint32_t chunk_of(uint32_t len, uint32_t ch) {
+  const uint32_t need = (len + kMaxChunks - 1) / kMaxChunks;
+  const uint32_t c = ((need + 255u) / 256u) * 256u;
+  return c > ch ? c : ch;
+}
+
+inline size_t split_fixed_bytes(uint32_t nslots) {
+  const size_t head = 64 + 4 * (size_t)ABCD_MAX_TILES * kMaxChunks +
+                      8 * ((size_t)ABCD_MAX_TILES + nslots);
+  return (head + 255) & ~size_t(255);
+}
+inline size_t split_bytes(uint32_t nslots) {
+  return split_fixed_bytes(nslots) + (size_t)nslots * 256 * sizeof(float4);
+}
+// Slots that fit `bytes` (0 if not even one does).
+inline uint32_t split_slots(size_t bytes) {
+  if (bytes < split_bytes(1)) return 0;
+  uint64_t ns = (bytes - split_fixed_bytes(0)) / (256 * sizeof(float4) + 8);
+  if (ns > 0x7FFF0000ull) ns = 0x7FFF0000ull;
+  while (ns > 0 && split_bytes((uint32_t)ns) > bytes) --ns;
+  return (uint32_t)ns;
+}
+inline SplitLayout split_layout(void* ws, size_t bytes, int ch) {
+  SplitLayout s{};
+  if (!ws || ch <= 0) return s;
+  s.nslots = split_slots(bytes);
+  if (s.nslots == 0) return s;
+  char* b = reinterpret_cast<char*>(ws);
+  s.hdr = reinterpret_cast<uint32_t*>(b);
+  s.slot_of = reinterpret_cast<uint32_t*>(b + 64);
+  s.items = reinterpret_cast<uint2*>(b + 64 + 4 * (size_t)ABCD_MAX_TILES * kMaxChunks);
+  s.ckpt = reinterpret_cast<float4*>(b + split_fixed_bytes(s.nslots));
+  s.ch = ch;
+  return s;
+}
+
 // ------------------------------------------------------ kernel launchers
 
 // project.hip
@@ -198,7 +261,7 @@ int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
                           const float* means2d, const float* conic_opacity, const float* rgb,
                           const float* F, const float* B, float* out_rgba, float* final_T,
                           uint32_t* last, unsigned long long* n_blends, const uint32_t* tile_order,
-                          hipStream_t stream);
+                          const SplitLayout& split, hipStream_t stream);
 int32_t launch_render_cache(const abcd_camera& cam, const abcd_raster_params& prm,
                             const uint32_t* tile_ranges, const uint32_t* tile_order,
                             const uint32_t* values_sorted, const float* means2d,
@@ -209,7 +272,8 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
                                  const float* means2d, const float* conic_opacity,
                                  const float* rgb, const float* F, const float* B,
                                  const float* final_T, const uint32_t* last,
-                                 const float* dL_dout, float* g2d, hipStream_t stream);
+                                 const float* dL_dout, float* g2d, const SplitLayout& split,
+                                 hipStream_t stream);
 int32_t launch_zero(float* p, int64_t count, hipStream_t stream);
 int32_t launch_loss_l1(int width, int height, const float* out_rgba, const float* target_rgb,
                        float bg0, float bg1, float bg2, float* dL_dout, float* loss,
@@ -220,6 +284,9 @@ int32_t launch_loss_l1(int width, int height, const float* out_rgba, const float
 // and the per-tile maximum of the forward's walk lengths as a work estimate.
 int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, const uint32_t* skip,
                           const char* name, hipStream_t stream);
+int32_t launch_bwd_items(int ntiles, const uint32_t* order, const uint32_t* work,
+                         const uint32_t* tile_ranges, const SplitLayout& split, void* items,
+                         uint32_t cap, uint32_t* queue, hipStream_t stream);
 int32_t launch_tile_walk(int width, int height, const uint32_t* last, uint32_t* work,
                          hipStream_t stream);
 

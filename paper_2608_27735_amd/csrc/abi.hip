@@ -96,6 +96,20 @@ int32_t check_params(const abcd_raster_params* p) {
   return ABCD_OK;
 }
 
+// The split workspace shared by a forward and its backward (NULL: no split).
+int32_t check_split(const abcd_split* sp, SplitLayout* out) {
+  *out = SplitLayout{};
+  if (!sp) return ABCD_OK;
+  REQUIRE(sp->workspace != nullptr && (reinterpret_cast<uintptr_t>(sp->workspace) & 255) == 0,
+          "split workspace must be non-NULL and 256-byte aligned");
+  REQUIRE(sp->chunk > 0 && sp->chunk % 256 == 0, "split chunk %d must be a positive multiple of 256",
+          sp->chunk);
+  REQUIRE(split_slots(sp->bytes) > 0, "split workspace of %zu bytes holds no checkpoint slot",
+          sp->bytes);
+  *out = split_layout(sp->workspace, sp->bytes, sp->chunk);
+  return ABCD_OK;
+}
+
 int32_t check_n(int64_t n) {
   REQUIRE(n >= 0 && n <= ABCD_MAX_GAUSSIANS, "n = %lld out of range", (long long)n);
   return ABCD_OK;
@@ -202,9 +216,12 @@ int32_t abcd_render_fwd(const abcd_camera* cam, const abcd_raster_params* prm,
                         const uint32_t* values_sorted,
                         const float* means2d, const float* conic_opacity, const float* rgb,
                         const float* F, const float* B, float* out_rgba, float* final_T,
-                        uint32_t* last, unsigned long long* n_blends, hipStream_t stream) {
+                        uint32_t* last, unsigned long long* n_blends, const abcd_split* split,
+                        hipStream_t stream) {
   TRY(check_camera(cam));
   TRY(check_params(prm));
+  SplitLayout sl;
+  TRY(check_split(split, &sl));
   REQUIRE(tile_ranges && out_rgba && final_T && last, "tile_ranges or an output is NULL");
   REQUIRE((reinterpret_cast<uintptr_t>(out_rgba) & 15) == 0 &&
               (reinterpret_cast<uintptr_t>(F) & 15) == 0 &&
@@ -213,7 +230,7 @@ int32_t abcd_render_fwd(const abcd_camera* cam, const abcd_raster_params* prm,
               (reinterpret_cast<uintptr_t>(means2d) & 7) == 0,
           "RGBA images and conic_opacity must be 16-byte aligned, means2d 8-byte aligned");
   return launch_render_fwd(*cam, *prm, tile_ranges, values_sorted, means2d, conic_opacity, rgb, F,
-                           B, out_rgba, final_T, last, n_blends, tile_order, stream);
+                           B, out_rgba, final_T, last, n_blends, tile_order, sl, stream);
 }
 
 int32_t abcd_render_cache(const abcd_camera* cam, const abcd_raster_params* prm,
@@ -233,6 +250,14 @@ int32_t abcd_render_cache(const abcd_camera* cam, const abcd_raster_params* prm,
                              conic_opacity, rgb, image_f16, rect, stream);
 }
 
+int32_t abcd_split_workspace_size(int64_t n_slots, size_t* bytes) {
+  REQUIRE(bytes != nullptr, "bytes is NULL");
+  REQUIRE(n_slots >= 1 && n_slots <= 0x7FFF0000ll, "n_slots %lld not in [1, 2^31)",
+          (long long)n_slots);
+  *bytes = split_bytes((uint32_t)n_slots);
+  return ABCD_OK;
+}
+
 int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes) {
   TRY(check_n(n));
   REQUIRE(bytes != nullptr, "bytes is NULL");
@@ -248,9 +273,12 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
                         const float* F, const float* B, const float* final_T, const uint32_t* last,
                         const float* dL_dout, void* workspace, size_t ws_bytes, float* d_means,
                         float* d_log_scales, float* d_quats, float* d_opacity_logits, float* d_sh,
-                        float* d_means2d, int32_t accumulate, hipStream_t stream) {
+                        float* d_means2d, int32_t accumulate, const abcd_split* split,
+                        hipStream_t stream) {
   TRY(check_camera(cam));
   TRY(check_params(prm));
+  SplitLayout sl;
+  TRY(check_split(split, &sl));
   TRY(check_n(n));
   REQUIRE(tile_ranges && final_T && last && dL_dout, "tile_ranges, final_T, last or dL_dout is NULL");
   REQUIRE((reinterpret_cast<uintptr_t>(dL_dout) & 15) == 0 &&
@@ -277,7 +305,7 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
   float* g2d = static_cast<float*>(workspace);
   TRY(launch_zero(g2d, 9 * n, stream));
   TRY(launch_render_bwd_pixels(*cam, *prm, n, tile_ranges, values_sorted, means2d, conic_opacity,
-                               rgb, F, B, final_T, last, dL_dout, g2d, stream));
+                               rgb, F, B, final_T, last, dL_dout, g2d, sl, stream));
   return launch_project_bwd(*cam, *prm, n, means, log_scales, quats, opacity_logits, sh, radius,
                             g2d, d_means, d_log_scales, d_quats, d_opacity_logits, d_sh, d_means2d,
                             accumulate, stream);

@@ -86,11 +86,11 @@ __device__ __forceinline__ int compact(bool keep, int* s_wcnt, int& pos) {
     tot += c;
   }
   pos = off + __popcll(bal & ((1ull << (threadIdx.x & 63)) - 1ull));
-  return tot;
+  return __builtin_amdgcn_readfirstlane(tot);  // uniform: loops over it branch on scalars
 }
 
 constexpr int kGroup = 8;
-constexpr int kBwdGroup = 8;  // the backward's group
+constexpr int kBwdGroup = 4;  // the backward's group (register budget: 5 waves per SIMD)
 
 BlendConsts consts(const abcd_camera& cam, const abcd_raster_params& prm) {
   BlendConsts k;

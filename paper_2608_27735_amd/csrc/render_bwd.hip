@@ -68,12 +68,18 @@ __device__ __forceinline__ int sum9_slot(int l) {
   return l < 8 ? 4 * (l & 1) + 2 * ((l >> 1) & 1) + ((l >> 2) & 1) : 8;
 }
 
-__global__ __launch_bounds__(256) void render_bwd_kernel(
-    BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
-    const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
-    const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
-    const float* __restrict__ final_T, const uint32_t* __restrict__ last,
-    const float4* __restrict__ dL_dout, float* __restrict__ g2d, const uint32_t* __restrict__ order) {
+// One work item of the backward: list positions [lo, hi) of `tile`, chunk j
+// of a split tile (lo = j ch) or the whole walk (j = 0, hi = 2^32 - 1). Each
+// pixel walks the positions below its walk length back to front, starting
+// from its final state in its last chunk and from the forward's checkpoint at
+// hi otherwise.
+__device__ __forceinline__ void bwd_item(
+    const BlendConsts& k, int tile, uint32_t j, const uint32_t* __restrict__ tile_ranges,
+    const uint32_t* __restrict__ values, const float2* __restrict__ means2d,
+    const float4* __restrict__ conic_opacity, const float* __restrict__ rgb,
+    const float4* __restrict__ F, const float4* __restrict__ B, const float* __restrict__ final_T,
+    const uint32_t* __restrict__ last, const float4* __restrict__ dL_dout, float* __restrict__ g2d,
+    const SplitLayout& sp) {
   __shared__ float4 s_ga[256];  // u, v, qa, qb
   __shared__ float4 s_gb[256];  // qc, o, r, g
   __shared__ float4 s_gc[256];  // a, b, c (conic), colour b
@@ -82,22 +88,44 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
   __shared__ float s_acc[9 * 256];  // entry-major: [entry][9]
   __shared__ int s_wcnt[4];
   __shared__ uint32_t s_max;
-  const int tile = tile_of_block(k, order);
-  if (tile >= k.ntiles) return;
   const int tid = threadIdx.x;
   const int px = (tile % k.ntx) * kTile + (tid & 15);
   const int py = (tile / k.ntx) * kTile + (tid >> 4);
   const bool inside = px < k.width && py < k.height;
   const TileBox box = tile_box(k, tile);
   const uint32_t start = tile_ranges[2 * tile];
+  const uint32_t len = tile_ranges[2 * tile + 1] - start;
+  // chunk bounds and checkpoint slots (a tile the forward did not split is
+  // one item; all of this is uniform)
+  uint32_t lo = 0, hi = 0xFFFFFFFFu, slot_hi = kNoSlot, slot_fin = kNoSlot;
+  if (sp.ckpt) {
+    const uint32_t* so = sp.slot_of + (size_t)tile * kMaxChunks;
+    const uint32_t fin = so[0];
+    if (fin < sp.nslots && j < kMaxChunks) {
+      const uint32_t cht = chunk_of(len, (uint32_t)sp.ch);
+      lo = j * cht;
+      hi = lo + cht;
+      slot_fin = fin;
+      if (j + 1 < kMaxChunks && so[j + 1] < sp.nslots) slot_hi = so[j + 1];
+    } else if (j != 0) {
+      return;  // not an item of this split
+    }
+  }
   const float fx = (float)px + 0.5f, fy = (float)py + 0.5f;
   float T = 1.0f, gcr = 0, gcg = 0, gcb = 0, gT = 0;
   uint32_t lastp = 0;
+  float Tfin = 1.0f;
+  // RG = sum over channels of gc_ch R_ch, where R is the colour accumulated
+  // behind the current entry (normalised by its transmittance): the
+  // alpha-derivative needs R only through this sum.
+  float RG = 0.0f;
+  __syncthreads();  // the previous item is done with the shared arrays
   if (tid == 0) s_max = 0;
   __syncthreads();
   if (inside) {
     const int64_t p = (int64_t)py * k.width + px;
     T = final_T[p];
+    Tfin = T;
     lastp = last[p];
     const float4 G = dL_dout[p];
     const float4 f = F ? F[p] : make_float4(0, 0, 0, 0);
@@ -107,24 +135,31 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
     gcg = s * G.y;
     gcb = s * G.z;
     gT = s * (G.x * bb.x + G.y * bb.y + G.z * bb.z - G.w * (1.0f - bb.w));
-    if (lastp) atomicMax(&s_max, lastp);
+    if (lastp > hi && slot_hi != kNoSlot) {  // crossed hi: its slot was taken
+      // the walk goes on past this chunk: start from the forward's state at
+      // hi; the colour behind is what the rest of the walk added
+      const float4 c = sp.ckpt[(size_t)slot_hi * 256 + tid];
+      const float4 e = sp.ckpt[(size_t)slot_fin * 256 + tid];
+      T = c.x;
+      RG = (gcr * (e.y - c.y) + gcg * (e.z - c.z) + gcb * (e.w - c.w)) / c.x;
+    }
+    const uint32_t mine = min(lastp, hi);
+    if (mine > lo) atomicMax(&s_max, mine);
   }
-  const float Tfin = T;
-  // RG = sum over channels of gc_ch R_ch, where R is the colour accumulated
-  // behind the current entry (normalised by its transmittance): the
-  // alpha-derivative needs R only through this sum.
-  float RG = 0.0f;
   __syncthreads();
-  const uint32_t nent = s_max;
+  const uint32_t nent = __builtin_amdgcn_readfirstlane(s_max);  // end of this item's walk
   const int lane = tid & 63, slot = sum9_slot(lane & 15);
   uint32_t wml = lastp;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) wml = max(wml, (uint32_t)__shfl_xor((int)wml, off, 64));
+  wml = __builtin_amdgcn_readfirstlane(wml);  // uniform, so its tests compile to scalar branches
   // entry j of a batch is list position bend - 1 - j (back to front)
-  uint32_t bend = start + nent;
-  Rec rec = load_rec(values, bend - 1 - tid, tid < (int)nent, means2d, conic_opacity, rgb);
-  while (bend > start) {
-    const uint32_t bbeg = bend - min(256u, bend - start);
+  const uint32_t bstop = start + lo;
+  uint32_t bend = nent > lo ? start + nent : bstop;
+  Rec rec = load_rec(values, bend - 1 - tid, (uint32_t)tid < bend - bstop, means2d, conic_opacity,
+                     rgb);
+  while (bend > bstop) {
+    const uint32_t bbeg = bend - min(256u, bend - bstop);
     __syncthreads();
     const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, rec.co.x, rec.co.y, rec.co.z,
                                                      rec.co.w, k.alpha_min, box.x0, box.x1,
@@ -144,28 +179,35 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
     __syncthreads();
     {
       const uint32_t nxt_end = bbeg;
-      const bool v = (uint32_t)tid < nxt_end - start;
+      const bool v = (uint32_t)tid < nxt_end - bstop;
       rec = load_rec(values, nxt_end - 1 - tid, v, means2d, conic_opacity, rgb);
     }
     // Entries are read from LDS kGroup at a time, all reads issued before the
     // first is used, so the LDS latency is paid once per group.
     for (int j0 = 0; j0 < cnt; j0 += kBwdGroup) {
-    float4 gav[kBwdGroup], gbv[kBwdGroup], gcv[kBwdGroup];
+    float4 gav[kBwdGroup], gbv[kBwdGroup];
+    float cbv[kBwdGroup];  // colour b (the conic in s_gc is needed only at the flush)
     uint32_t kkv[kBwdGroup];
 #pragma unroll
     for (int i = 0; i < kBwdGroup; ++i) {
       const int j = min(j0 + i, 255);
       gav[i] = s_ga[j];
       gbv[i] = s_gb[j];
-      gcv[i] = s_gc[j];
+      cbv[i] = s_gc[j].w;
       kkv[i] = (uint32_t)s_pos[j];
     }
+    // keep the group's reads ahead of the arithmetic (the compiler would
+    // otherwise sink each read into the branch that uses it)
+#pragma unroll
+    for (int i = 0; i < kBwdGroup; ++i)
+      asm volatile("" ::"v"(gav[i].x), "v"(gav[i].y), "v"(gav[i].z), "v"(gav[i].w), "v"(gbv[i].x),
+                   "v"(gbv[i].y), "v"(gbv[i].z), "v"(gbv[i].w), "v"(cbv[i]));
 #pragma unroll
     for (int i = 0; i < kBwdGroup; ++i) {
       const int j = j0 + i;
       if (j >= cnt) break;  // wave-uniform
-      const uint32_t kk = kkv[i];
-      const float4 ga = gav[i], gb = gbv[i], gc = gcv[i];
+      const uint32_t kk = __builtin_amdgcn_readfirstlane(kkv[i]);
+      const float4 ga = gav[i], gb = gbv[i];
       if (kk >= wml) continue;  // wave-uniform: no pixel of this wave reaches entry kk
       const float dx = fx - ga.x, dy = fy - ga.y;
       const AlphaEval ae = eval_alpha(dx, dy, ga.z, ga.w, gb.x, gb.y, k.alpha_min, k.alpha_max);
@@ -183,7 +225,7 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
       gr[6] = wgt * gcr;
       gr[7] = wgt * gcg;
       gr[8] = wgt * gcb;
-      const float CG = gb.z * gcr + gb.w * gcg + gc.w * gcb;
+      const float CG = gb.z * gcr + gb.w * gcg + cbv[i] * gcb;
       const float dLda = Tk * (CG - RG) - (Tfin * iom) * gT;
       RG = a * CG + om * RG;
       T = Tk;
@@ -226,33 +268,92 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
   }
 }
 
+// Persistent workgroups take work items, heaviest first, from a queue until
+// it is empty (every workgroup reaches the end of the queue and exits).
+__global__ __launch_bounds__(256) void render_bwd_kernel(
+    BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
+    const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
+    const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
+    const float* __restrict__ final_T, const uint32_t* __restrict__ last,
+    const float4* __restrict__ dL_dout, float* __restrict__ g2d, const uint2* __restrict__ items,
+    uint32_t* __restrict__ queue, uint32_t max_items, SplitLayout sp) {
+  __shared__ uint2 s_item;
+  const uint32_t n_items = min(queue[0], max_items);
+  for (;;) {
+    if (threadIdx.x == 0) {
+      const uint32_t i = atomicAdd(&queue[1], 1u);
+      s_item = i < n_items ? items[i] : make_uint2(kNoSlot, 0u);
+    }
+    __syncthreads();
+    const uint2 it = s_item;
+    __syncthreads();
+    if (it.x == kNoSlot) break;
+    if (it.x < (uint32_t)k.ntiles)
+      bwd_item(k, (int)it.x, it.y, tile_ranges, values, means2d, conic_opacity, rgb, F, B,
+               final_T, last, dL_dout, g2d, sp);
+  }
+}
+
 }  // namespace
 
 static size_t g2d_bytes(int64_t n) {
   return ((size_t)9 * sizeof(float) * (size_t)n + 255) & ~size_t(255);
 }
 
-// g2d[n][9], then the backward's tile work and tile order.
+// g2d[n][9], then the backward's tile work, tile order, work items (when
+// not split) and queue.
 size_t render_bwd_workspace_bytes(int64_t n) {
-  return g2d_bytes(n) + 2 * sizeof(uint32_t) * ABCD_MAX_TILES;
+  return g2d_bytes(n) + 2 * sizeof(uint32_t) * ABCD_MAX_TILES + sizeof(uint2) * ABCD_MAX_TILES +
+         256;
 }
+
+namespace {
+// Workgroups of the persistent backward that fit the device at once.
+int bwd_resident_blocks() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
+  if (cached[dev] == 0) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, render_bwd_kernel, kBlock, 0) !=
+            hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        per_cu <= 0 || cus <= 0) {
+      (void)hipGetLastError();
+      return 1024;
+    }
+    cached[dev] = per_cu * cus;
+  }
+  return cached[dev];
+}
+}  // namespace
 
 int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
                                  const uint32_t* tile_ranges, const uint32_t* values_sorted,
                                  const float* means2d, const float* conic_opacity,
                                  const float* rgb, const float* F, const float* B,
                                  const float* final_T, const uint32_t* last,
-                                 const float* dL_dout, float* g2d, hipStream_t stream) {
+                                 const float* dL_dout, float* g2d, const SplitLayout& split,
+                                 hipStream_t stream) {
   const BlendConsts k = consts(cam, prm);
-  uint32_t* work = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(g2d) + g2d_bytes(n));
+  char* tail = reinterpret_cast<char*>(g2d) + g2d_bytes(n);
+  uint32_t* work = reinterpret_cast<uint32_t*>(tail);
   uint32_t* order = work + ABCD_MAX_TILES;
+  uint2* own_items = reinterpret_cast<uint2*>(order + ABCD_MAX_TILES);
+  uint32_t* queue = reinterpret_cast<uint32_t*>(own_items + ABCD_MAX_TILES);
+  uint2* items = split.ckpt ? split.items : own_items;
+  const uint32_t max_items =
+      (uint32_t)k.ntiles + (split.ckpt ? split.nslots : 0u);
   TRY_STATUS(launch_tile_walk(k.width, k.height, last, work, stream));
   TRY_STATUS(launch_tile_order(k.ntiles, work, order, nullptr, "bwd_order", stream));
-  ABCD_LAUNCH("render_bwd", render_bwd_kernel, k.ntiles, kBlock, 0, stream, k, tile_ranges,
+  TRY_STATUS(
+      launch_bwd_items(k.ntiles, order, work, tile_ranges, split, items, max_items, queue, stream));
+  const int grid = (int)std::min<int64_t>(bwd_resident_blocks(), max_items);
+  ABCD_LAUNCH("render_bwd", render_bwd_kernel, grid, kBlock, 0, stream, k, tile_ranges,
               values_sorted, reinterpret_cast<const float2*>(means2d),
               reinterpret_cast<const float4*>(conic_opacity), rgb,
               reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B), final_T,
-              last, reinterpret_cast<const float4*>(dL_dout), g2d, order);
+              last, reinterpret_cast<const float4*>(dL_dout), g2d, items, queue, max_items, split);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }

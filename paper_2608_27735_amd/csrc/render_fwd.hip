@@ -20,13 +20,14 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
     float4* __restrict__ out, float* __restrict__ final_T, uint32_t* __restrict__ last,
     unsigned long long* __restrict__ n_blends, const uint32_t* __restrict__ order,
-    uint2* __restrict__ out16, int* __restrict__ rect, int fb_stop) {
+    uint2* __restrict__ out16, int* __restrict__ rect, int fb_stop, SplitLayout sp) {
   __shared__ float4 s_ga[256];  // u, v, qa, qb
   __shared__ float4 s_gb[256];  // qc, o, r, g
   __shared__ float s_bl[256];   // b
   __shared__ int s_pos[256];    // position in the tile's list
   __shared__ int s_wcnt[4];
   __shared__ unsigned long long s_nb;
+  __shared__ uint32_t s_base;
   const int tile = tile_of_block(k, order);
   if (tile >= k.ntiles) return;
   const int tid = threadIdx.x;
@@ -49,9 +50,32 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     done = vis < k.t_min;
   }
   if (tid == 0) s_nb = 0;
+  // Checkpoints for the split backward (uniform state): a slot per boundary
+  // the walk crosses, taken when it crosses
+  const uint32_t len = end - start;
+  const uint32_t cht = (!kHalf && sp.ckpt) ? chunk_of(len, (uint32_t)sp.ch) : 0u;
+  bool split_ok = cht != 0u && len > cht;
+  bool crossed = false;
   Rec rec = load_rec(values, start + tid, start + tid < end, means2d, conic_opacity, rgb);
   for (uint32_t b0 = start; b0 < end; b0 += 256) {
     if (__syncthreads_count(done) == 256) break;
+    if (split_ok && b0 > start && (b0 - start) % cht == 0) {
+      // state after the positions before b0; no pixel walks past a boundary
+      // the loop did not reach
+      if (tid == 0) {
+        const uint32_t got = atomicAdd(&sp.hdr[0], 1u);
+        s_base = got < sp.nslots ? got : kNoSlot;
+        sp.slot_of[(size_t)tile * kMaxChunks + (b0 - start) / cht] = s_base;
+      }
+      __syncthreads();
+      const uint32_t slot = s_base;
+      if (slot == kNoSlot) {
+        split_ok = false;  // out of slots: the backward takes this tile whole
+      } else {
+        sp.ckpt[(size_t)slot * 256 + tid] = make_float4(T, cr, cg, cb);
+        crossed = true;
+      }
+    }
     const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, rec.co.x, rec.co.y, rec.co.z,
                                                      rec.co.w, k.alpha_min, box.x0, box.x1,
                                                      box.y0, box.y1);
@@ -84,20 +108,28 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
           gb[i] = s_gb[j];
           bl[i] = s_bl[j];
         }
+        // keep the group's reads ahead of the arithmetic (the compiler would
+        // otherwise sink each read to its use)
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i)
+          asm volatile("" ::"v"(ga[i].x), "v"(ga[i].y), "v"(ga[i].z), "v"(ga[i].w), "v"(gb[i].x),
+                       "v"(gb[i].y), "v"(gb[i].z), "v"(gb[i].w), "v"(bl[i]));
 #pragma unroll
         for (int i = 0; i < kGroup; ++i) {
-          if (j0 + i >= cnt) break;  // wave-uniform
+          const bool valid = j0 + i < cnt;  // past the batch: a no-op step
           const AlphaEval ae = eval_alpha(fx - ga[i].x, fy - ga[i].y, ga[i].z, ga[i].w, gb[i].x,
                                           gb[i].y, k.alpha_min, k.alpha_max);
           const float Tn = T * (1.0f - ae.alpha);
-          const bool hit = !done && !ae.skip;
+          const bool hit = valid && !done && !ae.skip;
           const bool stop = hit && Tn < thr;
           const bool blend = hit && !stop;
           done = done || stop;
-          const float wgt = blend ? ae.alpha * T : 0.0f;
-          cr += gb[i].z * wgt;
-          cg += gb[i].w * wgt;
-          cb += bl[i] * wgt;
+          // selects, not a zero weight: entries past the batch hold stale
+          // shared memory, which may not be finite
+          const float wgt = ae.alpha * T;
+          cr = blend ? cr + gb[i].z * wgt : cr;
+          cg = blend ? cg + gb[i].w * wgt : cg;
+          cb = blend ? cb + bl[i] * wgt : cb;
           T = blend ? Tn : T;
           jl = blend ? j0 + i : jl;
           nb += blend ? 1u : 0u;
@@ -107,6 +139,21 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
       if (jl >= 0) lastk = (uint32_t)s_pos[jl] + 1;
     }
     // s_wcnt is rewritten only after the next barrier
+  }
+  if (cht != 0u) {
+    __syncthreads();  // every thread has read s_base
+    if (tid == 0) {
+      uint32_t fin = kNoSlot;
+      if (split_ok && crossed) {
+        const uint32_t got = atomicAdd(&sp.hdr[0], 1u);
+        if (got < sp.nslots) fin = got;
+      }
+      s_base = fin;
+      sp.slot_of[(size_t)tile * kMaxChunks] = fin;
+    }
+    __syncthreads();
+    const uint32_t slot = s_base;
+    if (slot != kNoSlot) sp.ckpt[(size_t)slot * 256 + tid] = make_float4(T, cr, cg, cb);
   }
   if (kHalf && rect) {
     // coverage of the cached image: tiles holding any pixel that blended
@@ -158,15 +205,16 @@ int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
                           const float* means2d, const float* conic_opacity, const float* rgb,
                           const float* F, const float* B, float* out_rgba, float* final_T,
                           uint32_t* last, unsigned long long* n_blends, const uint32_t* tile_order,
-                          hipStream_t stream) {
+                          const SplitLayout& split, hipStream_t stream) {
   const BlendConsts k = consts(cam, prm);
   const int grid = tile_order ? k.ntiles : 8 * k.per_xcd;
+  if (split.ckpt) TRY_STATUS(launch_zero(reinterpret_cast<float*>(split.hdr), 16, stream));
   ABCD_LAUNCH("render_fwd", render_fwd_kernel<false>, grid, kBlock, 0, stream, k, tile_ranges,
               values_sorted, reinterpret_cast<const float2*>(means2d),
               reinterpret_cast<const float4*>(conic_opacity), rgb,
               reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B),
               reinterpret_cast<float4*>(out_rgba), final_T, last, n_blends, tile_order, nullptr,
-              nullptr, (int)(prm.flags & ABCD_FLAG_FB_STOP));
+              nullptr, (int)(prm.flags & ABCD_FLAG_FB_STOP), split);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }
@@ -185,7 +233,8 @@ int32_t launch_render_cache(const abcd_camera& cam, const abcd_raster_params& pr
   ABCD_LAUNCH("render_cache", render_fwd_kernel<true>, grid, kBlock, 0, stream, k, tile_ranges,
               values_sorted, reinterpret_cast<const float2*>(means2d),
               reinterpret_cast<const float4*>(conic_opacity), rgb, nullptr, nullptr, nullptr,
-              nullptr, nullptr, nullptr, tile_order, reinterpret_cast<uint2*>(image_f16), rect, 0);
+              nullptr, nullptr, nullptr, tile_order, reinterpret_cast<uint2*>(image_f16), rect, 0,
+              SplitLayout{});
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }

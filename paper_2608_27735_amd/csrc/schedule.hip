@@ -109,7 +109,73 @@ __global__ __launch_bounds__(kBlock) void tile_walk_kernel(int width, int height
   if (threadIdx.x == 0) work[tile] = s_m;
 }
 
+// Work items of the backward, in the order of `order` (tiles by decreasing
+// walk): a tile with no walk has none, a tile the forward split (it has an
+// end-of-walk slot) one per chunk its walk reaches, any other tile one. Writes items (tile, chunk),
+// queue[0] = their number and queue[1] = 0 (the head the backward's
+// workgroups advance).
+__global__ __launch_bounds__(kOrderThreads) void bwd_items_kernel(
+    int ntiles, const uint32_t* __restrict__ order, const uint32_t* __restrict__ work,
+    const uint32_t* __restrict__ tile_ranges, SplitLayout sp, uint2* __restrict__ items,
+    uint32_t cap, uint32_t* __restrict__ queue) {
+  __shared__ uint32_t s_wsum[kOrderWaves];
+  __shared__ uint32_t s_off;
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+  if (tid == 0) s_off = 0;
+  __syncthreads();
+  for (int i0 = 0; i0 < ntiles; i0 += kOrderThreads) {
+    const int i = i0 + tid;
+    uint32_t t = 0, n = 0;
+    if (i < ntiles) {
+      t = order[i];
+      const uint32_t walk = work[t];
+      if (walk > 0) {
+        n = 1;
+        if (sp.ckpt && sp.slot_of[(size_t)t * kMaxChunks] < sp.nslots) {
+          const uint32_t len = tile_ranges[2 * t + 1] - tile_ranges[2 * t];
+          const uint32_t cht = chunk_of(len, (uint32_t)sp.ch);
+          n = min((walk + cht - 1) / cht, kMaxChunks);
+        }
+      }
+    }
+    // exclusive prefix of n over the workgroup
+    uint32_t inc = n;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t y = (uint32_t)__shfl_up((int)inc, d, 64);
+      if (l >= d) inc += y;
+    }
+    if (l == 63) s_wsum[w] = inc;
+    __syncthreads();
+    uint32_t before = 0, total = 0;
+#pragma unroll
+    for (int v = 0; v < kOrderWaves; ++v) {
+      const uint32_t c = s_wsum[v];
+      before += v < w ? c : 0u;
+      total += c;
+    }
+    const uint32_t off = s_off + before + inc - n;
+    for (uint32_t jj = 0; jj < n && off + jj < cap; ++jj) items[off + jj] = make_uint2(t, jj);
+    __syncthreads();
+    if (tid == 0) s_off += total;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    queue[0] = min(s_off, cap);
+    queue[1] = 0;
+  }
+}
+
 }  // namespace
+
+int32_t launch_bwd_items(int ntiles, const uint32_t* order, const uint32_t* work,
+                         const uint32_t* tile_ranges, const SplitLayout& split, void* items,
+                         uint32_t cap, uint32_t* queue, hipStream_t stream) {
+  ABCD_LAUNCH("bwd_order", bwd_items_kernel, 1, kOrderThreads, 0, stream, ntiles, order, work,
+              tile_ranges, split, reinterpret_cast<uint2*>(items), cap, queue);
+  ABCD_HIP(hipGetLastError());
+  return ABCD_OK;
+}
 
 int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, const uint32_t* skip,
                           const char* name, hipStream_t stream) {

@@ -15,7 +15,7 @@ from . import api
 
 
 class ActiveBlockStep:
-    def __init__(self, cam, prm, params, capacity=None, headroom=1.25, bg=None):
+    def __init__(self, cam, prm, params, capacity=None, headroom=1.25, bg=None, chunk=1024):
         self.cam, self.prm, self.params = cam, prm, params
         self.bg = bg
         n = params["means"].shape[0]
@@ -52,6 +52,15 @@ class ActiveBlockStep:
         self.values = torch.empty((capacity,), dtype=torch.int32, device=dev)
         self.bins = dict(values=self.values, tile_ranges=self.tile_ranges,
                          tile_order=self.tile_order)
+        # checkpoints for splitting long tiles in the backward (chunk=None: no
+        # split); slots are taken as walks cross chunk boundaries, heaviest
+        # tiles first, so a short pool only leaves light tiles whole
+        self.split = None
+        if chunk:
+            self.split = api.make_split(self._split_slots(capacity, chunk), chunk, dev)
+
+    def _split_slots(self, capacity, chunk):
+        return capacity // (8 * chunk) + api.n_tiles(self.cam.width, self.cam.height) + 1
 
     def project_and_bin(self, sync=False):
         """With sync=True the intersection count is read back and the buffers
@@ -64,11 +73,15 @@ class ActiveBlockStep:
         if sync and b["values"] is not self.values:
             self.values, self.bin_ws, self.capacity = b["values"], b["workspace"], b["capacity"]
             self.bins["values"] = self.values
+            if self.split is not None:
+                chunk = self.split["chunk"]
+                self.split = api.make_split(self._split_slots(self.capacity, chunk), chunk,
+                                            self.values.device)
         return b["n_isect"]
 
     def forward(self, F=None, B=None):
         return api.render_fwd(self.cam, self.prm, self.bins, self.proj, F=F, B=B,
-                              n_blends=self.n_blends, out=self.fwd)
+                              n_blends=self.n_blends, out=self.fwd, split=self.split)
 
     def loss_grad(self, target):
         return api.loss_l1_grad(self.fwd["out"], target, bg=self.bg, dL_dout=self.dL_dout,
@@ -76,7 +89,8 @@ class ActiveBlockStep:
 
     def backward(self, dL_dout, F=None, B=None):
         return api.render_bwd(self.cam, self.prm, self.params, self.proj, self.bins, self.fwd,
-                              dL_dout, F=F, B=B, workspace=self.bwd_ws, grads=self.grads)
+                              dL_dout, F=F, B=B, workspace=self.bwd_ws, grads=self.grads,
+                              split=self.split)
 
     def step(self, target, F=None, B=None):
         """project -> bin -> forward -> L1 gradient -> backward (no synchronisation)."""

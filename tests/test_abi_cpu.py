@@ -119,7 +119,7 @@ def test_workspace_size_helpers_are_host_only(lib):
     assert lib.abcd_bin_sort_workspace_size(10, 0, 0, 16, C.byref(sz)) == 1
     assert lib.abcd_bin_sort_workspace_size(10, 1 << 33, 16, 16, C.byref(sz)) == 1
     assert lib.abcd_render_bwd_workspace_size(1000, C.byref(sz)) == 0
-    assert sz.value >= 9 * 4 * 1000 + 8 * 32768 and sz.value % 256 == 0
+    assert sz.value >= 9 * 4 * 1000 + 16 * 32768 and sz.value % 256 == 0
 
 
 def test_bin_sort_rejects_small_or_misaligned_workspace(lib):
@@ -156,10 +156,10 @@ def test_render_calls_reject_bad_arguments(lib):
     c, p = _cam(), _prm()
     args = [FAKE] * 12
     args[0] = None  # tile_ranges
-    assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, None) == 1
+    assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, None, None) == 1
     args = [FAKE] * 12
     args[6] = FAKE + 4  # F misaligned
-    assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, None) == 1
+    assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, None, None) == 1
     cache = [FAKE] * 7 + [None]
     cache[6] = None  # image
     assert lib.abcd_render_cache(C.byref(c), C.byref(p), *cache, None) == 1
@@ -169,12 +169,33 @@ def test_render_calls_reject_bad_arguments(lib):
     cache = [FAKE] * 8
     cache[7] = FAKE + 2  # rect misaligned
     assert lib.abcd_render_cache(C.byref(c), C.byref(p), *cache, None) == 1
-    bwd = [FAKE] * 16 + [FAKE, 1 << 20] + [FAKE] * 6 + [0, None]
+    bwd = [FAKE] * 16 + [FAKE, 1 << 20] + [FAKE] * 6 + [0, None, None]
     bwd[13] = None  # final_T
     assert lib.abcd_render_bwd(C.byref(c), C.byref(p), 10, *bwd) == 1
-    bwd = [FAKE] * 16 + [FAKE, 8] + [FAKE] * 6 + [0, None]  # workspace too small
+    bwd = [FAKE] * 16 + [FAKE, 8] + [FAKE] * 6 + [0, None, None]  # workspace too small
     assert lib.abcd_render_bwd(C.byref(c), C.byref(p), 10, *bwd) == 1
     assert lib.abcd_loss_l1_grad(0, 8, FAKE, FAKE, None, FAKE, None, None) == 1
+
+
+def test_split_workspace_and_rejections(lib):
+    from paper_2608_27735_amd import _lib
+    sz = C.c_size_t(0)
+    assert lib.abcd_split_workspace_size(1, C.byref(sz)) == 0
+    one = sz.value
+    assert lib.abcd_split_workspace_size(11, C.byref(sz)) == 0
+    assert sz.value - one == 10 * (4096 + 8) or sz.value - one >= 10 * 4096
+    assert lib.abcd_split_workspace_size(0, C.byref(sz)) == 1
+    c, p = _cam(), _prm()
+    args = [FAKE] * 12
+    for ws, nbytes, chunk in ((FAKE + 8, 1 << 30, 256),   # misaligned
+                              (FAKE, 1 << 30, 300),       # chunk not a multiple of 256
+                              (FAKE, 1 << 30, 0),
+                              (FAKE, 64, 256)):           # no room for a slot
+        sp = _lib.abcd_split(ws, nbytes, chunk, 0)
+        assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, C.byref(sp), None) == 1
+    bwd = [FAKE] * 16 + [FAKE, 1 << 30] + [FAKE] * 6 + [0]
+    sp = _lib.abcd_split(FAKE, 1 << 30, 100, 0)
+    assert lib.abcd_render_bwd(C.byref(c), C.byref(p), 10, *bwd, C.byref(sp), None) == 1
 
 
 def test_adam_rejects_bad_arguments(lib):

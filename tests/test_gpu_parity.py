@@ -307,6 +307,49 @@ def test_step_end_to_end(api, case):
     assert rel <= GRAD_TOL
 
 
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+@pytest.mark.parametrize("chunk,n_slots", [(256, None), (512, None), (256, 3)])
+def test_split_backward(api, case, chunk, n_slots):
+    """Long tiles split into chunks for the backward: the forward's outputs are
+    unchanged, the gradients match the oracle to the same bar and the unsplit
+    backward up to rounding. n_slots = 3 leaves most tiles without slots
+    (those run unsplit)."""
+    name, cam, prm, scene = case
+    say("split backward", name, chunk, n_slots)
+    r = S.rng(43)
+    F, B = S.background_pair(r, cam.height, cam.width)
+    G = S.upstream_grad(r, cam.height, cam.width)
+    ref0 = O.step(cam, prm, scene, F=F, B=B, rel_margin=KNIFE)
+    G = G * (~ref0["fwd"]["knife"])[..., None]
+    ref = O.step(cam, prm, scene, F=F, B=B, dL_dout=G.astype(np.float64))
+    params = to_dev(scene)
+    Fd, Bd = torch.from_numpy(F).to(dev()), torch.from_numpy(B).to(dev())
+    Gd = torch.from_numpy(G).to(dev())
+    p = api.project(cam, prm, **params)
+    bins = api.bin_sort(cam.width, cam.height, p)
+    if n_slots is None:
+        n_slots = bins["n_isect"] // chunk + api.n_tiles(cam.width, cam.height) + 1
+    split = api.make_split(n_slots, chunk)
+    fw = api.render_fwd(cam, prm, bins, p, F=Fd, B=Bd, split=split)
+    fw0 = api.render_fwd(cam, prm, bins, p, F=Fd, B=Bd)
+    g0 = api.render_bwd(cam, prm, params, p, bins, fw0, Gd, F=Fd, B=Bd)
+    gs = api.render_bwd(cam, prm, params, p, bins, fw, Gd, F=Fd, B=Bd, split=split)
+    torch.cuda.synchronize()
+    for key in ("out", "final_T", "last"):
+        assert torch.equal(fw[key], fw0[key])
+    lens = np32(bins["tile_ranges"]).view(np.uint32).astype(np.int64)
+    print(f"  tiles longer than a chunk: {int(((lens[:, 1] - lens[:, 0]) > chunk).sum())}")
+    for k in ("means", "log_scales", "quats", "opacity_logits", "sh"):
+        a = np32(gs[k]).astype(np.float64)
+        b = np32(g0[k]).astype(np.float64)
+        gr = ref["grads"][k]
+        rel = np.linalg.norm(a - gr) / max(np.linalg.norm(gr), 1e-30)
+        rel0 = np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30)
+        print(f"  grad {k}: rel L2 {rel:.2e} vs oracle, {rel0:.2e} vs unsplit")
+        assert rel <= GRAD_TOL, (k, rel)
+        assert rel0 <= 2e-5, (k, rel0)
+
+
 def test_render_bwd_stage_and_accumulate(api):
     """Backward on identical fp32 screen-space inputs; accumulate adds."""
     w = S.ring()
