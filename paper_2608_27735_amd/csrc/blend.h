@@ -38,21 +38,23 @@ struct Rec {
   bool valid;
 };
 
-__device__ __forceinline__ Rec load_rec(const uint32_t* __restrict__ values, uint32_t idx,
-                                        bool valid, const float2* __restrict__ means2d,
-                                        const float4* __restrict__ conic_opacity,
-                                        const float* __restrict__ rgb) {
+// The gathers of one entry, for a Gaussian index read earlier. The loads are
+// unconditional (an invalid entry reads a valid index, see the callers):
+// loads under a divergent branch would make the compiler wait for them at the
+// branch's end instead of where the values are first used, which serialised
+// the staging of every batch.
+__device__ __forceinline__ Rec gather_rec(uint32_t gid, bool valid,
+                                          const float2* __restrict__ means2d,
+                                          const float4* __restrict__ conic_opacity,
+                                          const float* __restrict__ rgb) {
   Rec r;
   r.valid = valid;
-  r.gid = 0;
-  if (valid) {
-    r.gid = values[idx];
-    r.m = means2d[r.gid];
-    r.co = conic_opacity[r.gid];
-    r.r = rgb[3 * r.gid];
-    r.g = rgb[3 * r.gid + 1];
-    r.b = rgb[3 * r.gid + 2];
-  }
+  r.gid = gid;
+  r.m = means2d[gid];
+  r.co = conic_opacity[gid];
+  r.r = rgb[3 * gid];
+  r.g = rgb[3 * gid + 1];
+  r.b = rgb[3 * gid + 2];
   return r;
 }
 

@@ -156,8 +156,18 @@ __device__ __forceinline__ void bwd_item(
   // entry j of a batch is list position bend - 1 - j (back to front)
   const uint32_t bstop = start + lo;
   uint32_t bend = nent > lo ? start + nent : bstop;
-  Rec rec = load_rec(values, bend - 1 - tid, (uint32_t)tid < bend - bstop, means2d, conic_opacity,
-                     rgb);
+  // Loads run two batches ahead of use, as in the forward: positions below
+  // bstop read the entry at bstop (valid == false), so every load is
+  // unconditional and in bounds.
+  Rec rec{};
+  uint32_t gid_next = 0;
+  if (bend > bstop) {  // uniform
+    const uint32_t b1 = bend - min(256u, bend - bstop);  // end of the next batch
+    const uint32_t p0 = bend - 1 - tid, p1 = b1 - 1 - tid;
+    const uint32_t gid0 = values[(uint32_t)tid < bend - bstop ? p0 : bstop];
+    gid_next = values[(uint32_t)tid < b1 - bstop ? p1 : bstop];
+    rec = gather_rec(gid0, (uint32_t)tid < bend - bstop, means2d, conic_opacity, rgb);
+  }
   while (bend > bstop) {
     const uint32_t bbeg = bend - min(256u, bend - bstop);
     __syncthreads();
@@ -178,9 +188,12 @@ __device__ __forceinline__ void bwd_item(
     }
     __syncthreads();
     {
-      const uint32_t nxt_end = bbeg;
-      const bool v = (uint32_t)tid < nxt_end - bstop;
-      rec = load_rec(values, nxt_end - 1 - tid, v, means2d, conic_opacity, rgb);
+      // gathers of the next batch (ending at bbeg) and list values of the one
+      // after (ending at b2) overlap the walk of this one
+      const uint32_t b2 = bbeg - min(256u, bbeg - bstop);
+      const uint32_t gid_after = values[(uint32_t)tid < b2 - bstop ? b2 - 1 - tid : bstop];
+      rec = gather_rec(gid_next, (uint32_t)tid < bbeg - bstop, means2d, conic_opacity, rgb);
+      gid_next = gid_after;
     }
     // Entries are read from LDS kGroup at a time, all reads issued before the
     // first is used, so the LDS latency is paid once per group.

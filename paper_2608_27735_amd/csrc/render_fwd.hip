@@ -56,7 +56,18 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
   const uint32_t cht = (!kHalf && sp.ckpt) ? chunk_of(len, (uint32_t)sp.ch) : 0u;
   bool split_ok = cht != 0u && len > cht;
   bool crossed = false;
-  Rec rec = load_rec(values, start + tid, start + tid < end, means2d, conic_opacity, rgb);
+  // Loads run two batches ahead of use: the list values of batch b + 2 and
+  // the gathers of batch b + 1 are in flight while batch b blends. Positions
+  // past the list read its last entry (valid == false), so every load is
+  // unconditional and in bounds.
+  const uint32_t lastpos = end > start ? end - 1 : start;
+  Rec rec{};
+  uint32_t gid_next = 0;
+  if (end > start) {  // uniform
+    const uint32_t gid0 = values[min(start + tid, lastpos)];
+    gid_next = values[min(start + 256 + tid, lastpos)];
+    rec = gather_rec(gid0, start + tid < end, means2d, conic_opacity, rgb);
+  }
   for (uint32_t b0 = start; b0 < end; b0 += 256) {
     if (__syncthreads_count(done) == 256) break;
     if (split_ok && b0 > start && (b0 - start) % cht == 0) {
@@ -89,9 +100,12 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
       s_pos[pos] = (int)(b0 - start) + tid;
     }
     __syncthreads();
-    // gathers of the next batch overlap the blend of this one
+    // gathers of the next batch and list values of the one after overlap the
+    // blend of this one
     const uint32_t nxt = b0 + 256 + tid;
-    rec = load_rec(values, nxt, nxt < end, means2d, conic_opacity, rgb);
+    const uint32_t gid_after = values[min(b0 + 512 + tid, lastpos)];
+    rec = gather_rec(gid_next, nxt < end, means2d, conic_opacity, rgb);
+    gid_next = gid_after;
     if (__ballot(!done)) {
       // Lanes step through the entries together without divergent branches:
       // a lane that skips an entry, or has stopped, blends with weight 0.
