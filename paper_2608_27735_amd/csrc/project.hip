@@ -212,6 +212,91 @@ __device__ bool project_chain(const abcd_camera& c, const abcd_raster_params& p,
   return tile_rect(o.u, o.v, o.rad, ntx, nty, o.x0, o.y0, o.x1, o.y1);
 }
 
+// The geometry of one Gaussian in fp64: the 2D covariance, its inverse (the
+// conic) and the intermediates its derivative needs. The binning decisions
+// come from the fp32 chain above; the conic and the gradients come from here.
+// For large, thin Gaussians the 2D covariance is badly conditioned (its
+// determinant is far below A C, the eps2d dilation bounds only the minor
+// axis), and fp32 rounding of A, B, C would be amplified by that condition
+// number in the conic; fp64 arithmetic costs the HBM-bound projection
+// kernels nothing measurable.
+struct Geo64 {
+  double tx, ty, tz, xc, yc;
+  bool clx, cly;
+  double j00, j02, j11, j12;
+  double s[3];
+  double qn, qw, qx, qy, qz;
+  double r[9], m[9], S[6], T[6];
+  double A, B, C, det;
+};
+
+__device__ void geom_f64(const abcd_camera& c, const abcd_raster_params& p, const float* mu,
+                         const float* ls, const float* q, Geo64& o) {
+  const float* R = c.R;
+  const double m0 = mu[0], m1 = mu[1], m2 = mu[2];
+  o.tx = (double)R[0] * m0 + (double)R[1] * m1 + (double)R[2] * m2 + (double)c.t[0];
+  o.ty = (double)R[3] * m0 + (double)R[4] * m1 + (double)R[5] * m2 + (double)c.t[1];
+  o.tz = (double)R[6] * m0 + (double)R[7] * m1 + (double)R[8] * m2 + (double)c.t[2];
+  const double fx = c.fx, fy = c.fy;
+  const double xr = o.tx / o.tz, yr = o.ty / o.tz;
+  const double limx = (double)p.guard * (0.5 * (double)c.width) / fx;
+  const double limy = (double)p.guard * (0.5 * (double)c.height) / fy;
+  o.clx = xr < -limx || xr > limx;
+  o.cly = yr < -limy || yr > limy;
+  o.xc = xr < -limx ? -limx : (xr > limx ? limx : xr);
+  o.yc = yr < -limy ? -limy : (yr > limy ? limy : yr);
+  o.j00 = fx / o.tz;
+  o.j02 = -fx * o.xc / o.tz;
+  o.j11 = fy / o.tz;
+  o.j12 = -fy * o.yc / o.tz;
+  o.s[0] = exp((double)ls[0]);
+  o.s[1] = exp((double)ls[1]);
+  o.s[2] = exp((double)ls[2]);
+  const double q0 = q[0], q1 = q[1], q2 = q[2], q3 = q[3];
+  o.qn = sqrt(q0 * q0 + q1 * q1 + q2 * q2 + q3 * q3);
+  const double w = q0 / o.qn, x = q1 / o.qn, y = q2 / o.qn, z = q3 / o.qn;
+  o.qw = w; o.qx = x; o.qy = y; o.qz = z;
+  double* r = o.r;
+  r[0] = 1.0 - 2.0 * (y * y + z * z);
+  r[1] = 2.0 * (x * y - w * z);
+  r[2] = 2.0 * (x * z + w * y);
+  r[3] = 2.0 * (x * y + w * z);
+  r[4] = 1.0 - 2.0 * (x * x + z * z);
+  r[5] = 2.0 * (y * z - w * x);
+  r[6] = 2.0 * (x * z - w * y);
+  r[7] = 2.0 * (y * z + w * x);
+  r[8] = 1.0 - 2.0 * (x * x + y * y);
+#pragma unroll
+  for (int a = 0; a < 3; ++a)
+#pragma unroll
+    for (int b = 0; b < 3; ++b) o.m[3 * a + b] = r[3 * a + b] * o.s[b];
+  const double* m = o.m;
+  double* S = o.S;
+  S[0] = m[0] * m[0] + m[1] * m[1] + m[2] * m[2];
+  S[1] = m[0] * m[3] + m[1] * m[4] + m[2] * m[5];
+  S[2] = m[0] * m[6] + m[1] * m[7] + m[2] * m[8];
+  S[3] = m[3] * m[3] + m[4] * m[4] + m[5] * m[5];
+  S[4] = m[3] * m[6] + m[4] * m[7] + m[5] * m[8];
+  S[5] = m[6] * m[6] + m[7] * m[7] + m[8] * m[8];
+  double* T = o.T;
+  T[0] = o.j00 * R[0] + o.j02 * R[6];
+  T[1] = o.j00 * R[1] + o.j02 * R[7];
+  T[2] = o.j00 * R[2] + o.j02 * R[8];
+  T[3] = o.j11 * R[3] + o.j12 * R[6];
+  T[4] = o.j11 * R[4] + o.j12 * R[7];
+  T[5] = o.j11 * R[5] + o.j12 * R[8];
+  const double U00 = T[0] * S[0] + T[1] * S[1] + T[2] * S[2];
+  const double U01 = T[0] * S[1] + T[1] * S[3] + T[2] * S[4];
+  const double U02 = T[0] * S[2] + T[1] * S[4] + T[2] * S[5];
+  const double U10 = T[3] * S[0] + T[4] * S[1] + T[5] * S[2];
+  const double U11 = T[3] * S[1] + T[4] * S[3] + T[5] * S[4];
+  const double U12 = T[3] * S[2] + T[4] * S[4] + T[5] * S[5];
+  o.A = U00 * T[0] + U01 * T[1] + U02 * T[2] + (double)p.eps2d;
+  o.B = U00 * T[3] + U01 * T[4] + U02 * T[5];
+  o.C = U10 * T[3] + U11 * T[4] + U12 * T[5] + (double)p.eps2d;
+  o.det = o.A * o.C - o.B * o.B;
+}
+
 // SH coefficients of a 64-Gaussian group are staged through LDS so that the
 // global loads and stores are coalesced (each Gaussian owns 3 (D+1)^2
 // consecutive floats; one thread per Gaussian would stride by 48 floats).
@@ -316,8 +401,10 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(
     rgb[3 * i] = rgb[3 * i + 1] = rgb[3 * i + 2] = 0.0f;
     return;
   }
-  const float inv = 1.0f / pr.det;
-  const float ca = pr.C * inv, cb = -pr.B * inv, cc = pr.A * inv;
+  Geo64 g64;
+  geom_f64(cam, prm, mu, ls, q, g64);
+  const double inv = 1.0 / g64.det;
+  const float ca = (float)(g64.C * inv), cb = (float)(-g64.B * inv), cc = (float)(g64.A * inv);
   const float o = 1.0f / (1.0f + __expf(-ologit));
   float dx = mu[0] - cam.campos[0], dy = mu[1] - cam.campos[1], dz = mu[2] - cam.campos[2];
   const float dn = rsqrtf(dx * dx + dy * dy + dz * dz);
@@ -390,100 +477,105 @@ __global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
     gv = G[1];
     const float ga = G[2], gb = G[3], gc = G[4], go = G[5];
     const float gcol[3] = {G[6], G[7], G[8]};
+    // the covariance part of the chain rule runs in fp64 (see geom_f64)
+    Geo64 g;
+    {
+      const float q[4] = {q4.x, q4.y, q4.z, q4.w};
+      geom_f64(cam, prm, mu, ls, q, g);
+    }
     // conic Q = Sigma'^-1:  dL/dSigma' = -Q GQ Q, GQ = [[ga, gb/2], [gb/2, gc]]
-    const float inv = 1.0f / pr.det;
-    const float qa = pr.C * inv, qb = -pr.B * inv, qc = pr.A * inv;
-    const float hb = 0.5f * gb;
-    const float P00 = qa * ga + qb * hb, P01 = qa * hb + qb * gc;
-    const float P10 = qb * ga + qc * hb, P11 = qb * hb + qc * gc;
-    const float G00 = -(P00 * qa + P01 * qb);
-    const float G01 = -0.5f * ((P00 * qb + P01 * qc) + (P10 * qa + P11 * qb));
-    const float G11 = -(P10 * qb + P11 * qc);
+    const double inv = 1.0 / g.det;
+    const double qa = g.C * inv, qb = -g.B * inv, qc = g.A * inv;
+    const double hb = 0.5 * gb;
+    const double P00 = qa * ga + qb * hb, P01 = qa * hb + qb * gc;
+    const double P10 = qb * ga + qc * hb, P11 = qb * hb + qc * gc;
+    const double G00 = -(P00 * qa + P01 * qb);
+    const double G01 = -0.5 * ((P00 * qb + P01 * qc) + (P10 * qa + P11 * qb));
+    const double G11 = -(P10 * qb + P11 * qc);
     // Sigma' = T Sigma T^T + eps I
-    const float* T = pr.T;
-    const float* S = pr.S;
-    const float Sm[9] = {S[0], S[1], S[2], S[1], S[3], S[4], S[2], S[4], S[5]};
-    float GS[9];  // T^T G T
+    const double* T = g.T;
+    const double* S = g.S;
+    const double Sm[9] = {S[0], S[1], S[2], S[1], S[3], S[4], S[2], S[4], S[5]};
+    double GS[9];  // T^T G T
 #pragma unroll
     for (int a = 0; a < 3; ++a)
 #pragma unroll
       for (int b = 0; b < 3; ++b)
         GS[3 * a + b] = T[a] * (G00 * T[b] + G01 * T[3 + b]) + T[3 + a] * (G01 * T[b] + G11 * T[3 + b]);
-    float GT[6];  // 2 G T Sigma
+    double GT[6];  // 2 G T Sigma
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-      const float g0 = r == 0 ? G00 : G01, g1 = r == 0 ? G01 : G11;
+      const double g0 = r == 0 ? G00 : G01, g1 = r == 0 ? G01 : G11;
 #pragma unroll
       for (int b = 0; b < 3; ++b) {
-        float acc = 0.0f;
+        double acc = 0.0;
 #pragma unroll
         for (int k = 0; k < 3; ++k) acc += (g0 * T[k] + g1 * T[3 + k]) * Sm[3 * k + b];
-        GT[3 * r + b] = 2.0f * acc;
+        GT[3 * r + b] = 2.0 * acc;
       }
     }
     // T = J Rcam
     const float* Rc = cam.R;
-    const float gj00 = GT[0] * Rc[0] + GT[1] * Rc[1] + GT[2] * Rc[2];
-    const float gj02 = GT[0] * Rc[6] + GT[1] * Rc[7] + GT[2] * Rc[8];
-    const float gj11 = GT[3] * Rc[3] + GT[4] * Rc[4] + GT[5] * Rc[5];
-    const float gj12 = GT[3] * Rc[6] + GT[4] * Rc[7] + GT[5] * Rc[8];
+    const double gj00 = GT[0] * Rc[0] + GT[1] * Rc[1] + GT[2] * Rc[2];
+    const double gj02 = GT[0] * Rc[6] + GT[1] * Rc[7] + GT[2] * Rc[8];
+    const double gj11 = GT[3] * Rc[3] + GT[4] * Rc[4] + GT[5] * Rc[5];
+    const double gj12 = GT[3] * Rc[6] + GT[4] * Rc[7] + GT[5] * Rc[8];
     // J(t), (u, v)(t)
-    const float fx = cam.fx, fy = cam.fy, iz = 1.0f / pr.tz, iz2 = iz * iz;
-    float gtx = 0.0f, gty = 0.0f, gtz = 0.0f;
-    gtz += -fx * iz2 * gj00 - fy * iz2 * gj11 + fx * pr.xc * iz2 * gj02 + fy * pr.yc * iz2 * gj12;
-    const float gxc = -fx * iz * gj02, gyc = -fy * iz * gj12;
-    if (!pr.clx) {
+    const double fx = cam.fx, fy = cam.fy, iz = 1.0 / g.tz, iz2 = iz * iz;
+    double gtx = 0.0, gty = 0.0, gtz = 0.0;
+    gtz += -fx * iz2 * gj00 - fy * iz2 * gj11 + fx * g.xc * iz2 * gj02 + fy * g.yc * iz2 * gj12;
+    const double gxc = -fx * iz * gj02, gyc = -fy * iz * gj12;
+    if (!g.clx) {
       gtx += gxc * iz;
-      gtz -= gxc * pr.tx * iz2;
+      gtz -= gxc * g.tx * iz2;
     }
-    if (!pr.cly) {
+    if (!g.cly) {
       gty += gyc * iz;
-      gtz -= gyc * pr.ty * iz2;
+      gtz -= gyc * g.ty * iz2;
     }
     gtx += fx * iz * gu;
-    gtz -= fx * pr.tx * iz2 * gu;
+    gtz -= fx * g.tx * iz2 * gu;
     gty += fy * iz * gv;
-    gtz -= fy * pr.ty * iz2 * gv;
+    gtz -= fy * g.ty * iz2 * gv;
 #pragma unroll
-    for (int k = 0; k < 3; ++k) gm[k] = Rc[k] * gtx + Rc[3 + k] * gty + Rc[6 + k] * gtz;
+    for (int k = 0; k < 3; ++k) gm[k] = (float)(Rc[k] * gtx + Rc[3 + k] * gty + Rc[6 + k] * gtz);
     // Sigma = M M^T, M = Rq diag(s)
-    float GM[9];
+    double GM[9];
 #pragma unroll
     for (int a = 0; a < 3; ++a)
 #pragma unroll
       for (int b = 0; b < 3; ++b)
-        GM[3 * a + b] = 2.0f * (GS[3 * a] * pr.m[b] + GS[3 * a + 1] * pr.m[3 + b] +
-                                GS[3 * a + 2] * pr.m[6 + b]);
-    const float s[3] = {pr.s0, pr.s1, pr.s2};
-    float gR[9];
+        GM[3 * a + b] = 2.0 * (GS[3 * a] * g.m[b] + GS[3 * a + 1] * g.m[3 + b] +
+                               GS[3 * a + 2] * g.m[6 + b]);
+    double gR[9];
 #pragma unroll
     for (int b = 0; b < 3; ++b) {
-      float gs = 0.0f;
+      double gs = 0.0;
 #pragma unroll
       for (int a = 0; a < 3; ++a) {
-        gs += GM[3 * a + b] * pr.r[3 * a + b];
-        gR[3 * a + b] = GM[3 * a + b] * s[b];
+        gs += GM[3 * a + b] * g.r[3 * a + b];
+        gR[3 * a + b] = GM[3 * a + b] * g.s[b];
       }
-      gl[b] = gs * s[b];
+      gl[b] = (float)(gs * g.s[b]);
     }
     // rotation entries as functions of the unit quaternion
-    const float w = pr.qw, x = pr.qx, y = pr.qy, z = pr.qz;
-    float gw = 0.0f, gx = 0.0f, gy = 0.0f, gz = 0.0f;
-    gy += -4.0f * y * gR[0]; gz += -4.0f * z * gR[0];
-    gw += -2.0f * z * gR[1]; gx += 2.0f * y * gR[1]; gy += 2.0f * x * gR[1]; gz += -2.0f * w * gR[1];
-    gw += 2.0f * y * gR[2]; gx += 2.0f * z * gR[2]; gy += 2.0f * w * gR[2]; gz += 2.0f * x * gR[2];
-    gw += 2.0f * z * gR[3]; gx += 2.0f * y * gR[3]; gy += 2.0f * x * gR[3]; gz += 2.0f * w * gR[3];
-    gx += -4.0f * x * gR[4]; gz += -4.0f * z * gR[4];
-    gw += -2.0f * x * gR[5]; gx += -2.0f * w * gR[5]; gy += 2.0f * z * gR[5]; gz += 2.0f * y * gR[5];
-    gw += -2.0f * y * gR[6]; gx += 2.0f * z * gR[6]; gy += -2.0f * w * gR[6]; gz += 2.0f * x * gR[6];
-    gw += 2.0f * x * gR[7]; gx += 2.0f * w * gR[7]; gy += 2.0f * z * gR[7]; gz += 2.0f * y * gR[7];
-    gx += -4.0f * x * gR[8]; gy += -4.0f * y * gR[8];
-    const float dotq = gw * w + gx * x + gy * y + gz * z;
-    const float iq = 1.0f / pr.qn;
-    gq[0] = (gw - w * dotq) * iq;
-    gq[1] = (gx - x * dotq) * iq;
-    gq[2] = (gy - y * dotq) * iq;
-    gq[3] = (gz - z * dotq) * iq;
+    const double w = g.qw, x = g.qx, y = g.qy, z = g.qz;
+    double gw = 0.0, gx = 0.0, gy = 0.0, gz = 0.0;
+    gy += -4.0 * y * gR[0]; gz += -4.0 * z * gR[0];
+    gw += -2.0 * z * gR[1]; gx += 2.0 * y * gR[1]; gy += 2.0 * x * gR[1]; gz += -2.0 * w * gR[1];
+    gw += 2.0 * y * gR[2]; gx += 2.0 * z * gR[2]; gy += 2.0 * w * gR[2]; gz += 2.0 * x * gR[2];
+    gw += 2.0 * z * gR[3]; gx += 2.0 * y * gR[3]; gy += 2.0 * x * gR[3]; gz += 2.0 * w * gR[3];
+    gx += -4.0 * x * gR[4]; gz += -4.0 * z * gR[4];
+    gw += -2.0 * x * gR[5]; gx += -2.0 * w * gR[5]; gy += 2.0 * z * gR[5]; gz += 2.0 * y * gR[5];
+    gw += -2.0 * y * gR[6]; gx += 2.0 * z * gR[6]; gy += -2.0 * w * gR[6]; gz += 2.0 * x * gR[6];
+    gw += 2.0 * x * gR[7]; gx += 2.0 * w * gR[7]; gy += 2.0 * z * gR[7]; gz += 2.0 * y * gR[7];
+    gx += -4.0 * x * gR[8]; gy += -4.0 * y * gR[8];
+    const double dotq = gw * w + gx * x + gy * y + gz * z;
+    const double iq = 1.0 / g.qn;
+    gq[0] = (float)((gw - w * dotq) * iq);
+    gq[1] = (float)((gx - x * dotq) * iq);
+    gq[2] = (float)((gy - y * dotq) * iq);
+    gq[3] = (float)((gz - z * dotq) * iq);
     // opacity
     const float o = 1.0f / (1.0f + __expf(-ologit));
     gop = go * o * (1.0f - o);

@@ -204,6 +204,48 @@ def perturbed(r, scene, pos_sd=0.01, logit_shift=-1.0):
     return out
 
 
+def midscale_block(seed=3, n=300_000, width=1297, height=840, n_cams=200, cam_index=0):
+    """The mid-scale scene's active block: a 4x4x2 grid over [-10, 10]^2 x
+    [0, 6]; the active cell (1, 1, 0) holds n Gaussians, 40% on a ground
+    plane (z uniform on [0, 0.1]) and 60% in 8 Gaussian blobs (sd 0.5, centres
+    uniform in the cell, clipped to it), log-scales N(log 0.2, 0.5), SH degree
+    3; 200 cameras on the ellipse (16 cos p, 12 sin p, 5) looking at (0, 0, 1.5)."""
+    r = rng(seed)
+    grid = Grid((-10.0, -10.0, 0.0), (10.0, 10.0, 6.0), (4, 4, 2))
+    active = grid.linear((1, 1, 0))
+    lo, hi = grid.bounds(active)
+    n_ground = int(0.4 * n)
+    ground = np.stack([r.uniform(lo[0], hi[0], n_ground), r.uniform(lo[1], hi[1], n_ground),
+                       r.uniform(0.0, 0.1, n_ground)], axis=1)
+    centres = r.uniform(lo, hi, (8, 3))
+    comp = r.integers(0, 8, n - n_ground)
+    blobs = np.clip(centres[comp] + r.normal(0.0, 0.5, (n - n_ground, 3)), lo, hi - 1e-6)
+    scene = gaussians(r, np.concatenate([ground, blobs]), 3, math.log(0.2), 0.5)
+    cams = [look_at((16.0 * math.cos(2 * math.pi * k / n_cams), 12.0 * math.sin(2 * math.pi * k / n_cams),
+                     5.0), (0, 0, 1.5), width, height) for k in range(n_cams)]
+    cam = cams[cam_index]
+    return Workload(scene=scene, cams=cams, cam=cam, grid=grid, active=active,
+                    order=grid.order_from(cam.campos), params=RasterParams(sh_degree=3))
+
+
+def stress_block(seed=5, n=4_000_000, width=2560, height=1440, n_cams=200, cam_index=0):
+    """The stress configuration's active block: an 8x8x2 grid over [-20, 20]^2 x
+    [0, 10]; the active cell (3, 3, 0) holds n Gaussians with means uniform in
+    it and tiny scales, log-scales N(log 0.08, 0.5) (0.002 of the 40-unit
+    extent), SH degree 3; 200 cameras at 2560x1440 on the ellipse
+    (30 cos p, 24 sin p, 12) looking at (0, 0, 2)."""
+    r = rng(seed)
+    grid = Grid((-20.0, -20.0, 0.0), (20.0, 20.0, 10.0), (8, 8, 2))
+    active = grid.linear((3, 3, 0))
+    lo, hi = grid.bounds(active)
+    scene = gaussians(r, r.uniform(lo, hi, (n, 3)), 3, math.log(0.08), 0.5)
+    cams = [look_at((30.0 * math.cos(2 * math.pi * k / n_cams), 24.0 * math.sin(2 * math.pi * k / n_cams),
+                     12.0), (0, 0, 2.0), width, height) for k in range(n_cams)]
+    cam = cams[cam_index]
+    return Workload(scene=scene, cams=cams, cam=cam, grid=grid, active=active,
+                    order=grid.order_from(cam.campos), params=RasterParams(sh_degree=3))
+
+
 # ----------------------------------------------------------- image inputs
 
 def premultiplied_images(r, k, height, width, alpha_max=0.95, coverage=0.5):

@@ -1,10 +1,16 @@
-"""GPU parity at the full workload the bench times: 1M active Gaussians (SH
-degree 3) rendered at 1297x840, through the same ActiveBlockStep launch path
-(capacity mode, tile schedules, persistent buffers).
+"""GPU parity at the large workloads, through the launch path the bench times
+(ActiveBlockStep: capacity mode, tile schedules, split backward, persistent
+buffers):
+  - the 1M-Gaussian active block (SH degree 3) at 1297x840 the bench measures,
+    with uniform scales and with heavy-tailed scales;
+  - the mid-scale scene's 300K-Gaussian active block at 1297x840 (ground plane
+    and blobs);
+  - the stress configuration's 4M-Gaussian active block of tiny Gaussians at
+    2560x1440.
 
-The oracle cannot rasterise the whole frame in seconds, so it is run on
+The oracle cannot rasterise these frames in seconds, so it is run on
 sampled outputs it can compute on its own:
-  - projection: the binning fields of all 1M Gaussians, bit-exact;
+  - projection: the binning fields of all Gaussians, bit-exact;
   - binning: M and every tile's list length, bit-exact; the full depth-ordered
     lists of the sampled tiles, bit-exact (the oracle bins the subset of
     Gaussians whose rectangle meets a sampled tile, which leaves those tiles'
@@ -14,8 +20,8 @@ sampled outputs it can compute on its own:
   - backward: with dL/dout zero outside the sampled tiles, every parameter
     gradient depends only on those tiles, so the oracle's gradients from the
     subset lists are the full answer: relative L2 <= 1e-4 per tensor.
-The sampled tiles are the eight with the longest walks (where the schedules
-and long lists matter) and sixteen seeded random tiles.
+The sampled tiles are the eight with the longest walks (where the schedules,
+the split and long lists matter) and sixteen seeded random tiles.
 """
 import numpy as np
 import pytest
@@ -28,27 +34,38 @@ pytestmark = pytest.mark.gpu
 
 FWD_TOL = 1e-5
 GRAD_TOL = 1e-4
-# Knife-edge margin on threshold decisions. A pixel of the heaviest tiles
-# makes ~10^4 skip decisions, so the 1e-4 margin of the small cases flags a
-# few percent of them; fp32 alpha is within ~1e-6 (relative) of fp64 and the
-# transmittance after 10^4 products within ~1e-5 (random walk of 0.5-ulp
-# roundings), so 3e-5 still covers every decision the two precisions could
-# take differently.
-KNIFE = 3e-5
+# Knife-edge margin on threshold decisions, per workload. A pixel of the
+# heaviest tiles makes ~10^4 skip decisions, so the 1e-4 margin of the small
+# cases flags a few percent of them; fp32 alpha is within ~1e-6 (relative) of
+# fp64 (the conic comes from fp64 arithmetic) and the transmittance after
+# 10^4 products within ~1e-5 (random walk of 0.5-ulp roundings), so 3e-5
+# still covers every decision the two precisions could take differently.
+# With heavy-tailed scales a pixel blends up to ~4,000 entries of alpha near
+# alpha_min, whose factors 1 - alpha round alike, so the fp32 transmittance
+# drifts by up to ~1e-4 from fp64 (measured: 3e-5 leaves decisions that
+# differ): that workload takes the 1e-4 margin of the small cases, which
+# flags about 9% of its sampled pixels.
+WORKLOADS = {  # name: (generator, knife margin, largest knife-edge fraction)
+    "1m-uniform-1297x840": (lambda: S.active_block_1m(), 3e-5, 0.02),
+    "1m-heavy-tail-1297x840": (lambda: S.active_block_1m(heavy_tail=True), 1e-4, 0.12),
+    "300k-midscale-1297x840": (lambda: S.midscale_block(), 3e-5, 0.02),
+    "4m-stress-2560x1440": (lambda: S.stress_block(), 3e-5, 0.02),
+}
 
 
 def say(*a):
     print("[case]", *a, flush=True)
 
 
-@pytest.fixture(scope="module")
-def full():
+@pytest.fixture(scope="module", params=list(WORKLOADS), ids=list(WORKLOADS))
+def full(request):
     assert torch.cuda.is_available(), "GPU tests need a GPU"
     from paper_2608_27735_amd import api
     from paper_2608_27735_amd.step import ActiveBlockStep
     dev = torch.device("cuda:0")
-    say("full-size workload: 1M Gaussians, 1297x840")
-    w = S.active_block_1m()
+    say("large workload", request.param)
+    gen, knife, knife_frac = WORKLOADS[request.param]
+    w = gen()
     cam, prm, scene = w.cam, w.params, w.scene
     r = S.rng(5)
     F, B = S.background_pair(r, cam.height, cam.width)
@@ -58,7 +75,11 @@ def full():
     Fd, Bd = torch.from_numpy(F).to(dev), torch.from_numpy(B).to(dev)
     st.forward(Fd, Bd)
     torch.cuda.synchronize()
-    return dict(api=api, st=st, cam=cam, prm=prm, scene=scene, F=F, B=B, Fd=Fd, Bd=Bd, r=r)
+    pb = O.project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"])
+    yield dict(api=api, st=st, cam=cam, prm=prm, scene=scene, F=F, B=B, Fd=Fd, Bd=Bd, r=r,
+               pb=pb, name=request.param, knife=knife, knife_frac=knife_frac)
+    del st, params
+    torch.cuda.empty_cache()
 
 
 def _tiles(cam):
@@ -81,9 +102,8 @@ def _sampled_tiles(full):
 def _oracle_subset(full, tiles):
     """Oracle projection of all Gaussians; oracle lists of the sampled tiles
     from the subset of Gaussians whose rectangle meets one of them."""
-    cam, prm, scene = full["cam"], full["prm"], full["scene"]
+    cam, pb = full["cam"], full["pb"]
     ntx, _ = _tiles(cam)
-    pb = O.project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"])
     rect = pb["rect"].astype(np.int64)  # tx0, ty0, tx1, ty1 (empty if tx1 < tx0)
     tx, ty = tiles % ntx, tiles // ntx
     meets = np.zeros(len(rect), bool)
@@ -96,9 +116,8 @@ def _oracle_subset(full, tiles):
 
 
 def test_fullsize_projection_and_binning(full):
-    api, st, cam, prm, scene = full["api"], full["st"], full["cam"], full["prm"], full["scene"]
-    say("full-size projection + binning")
-    pb = O.project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"])
+    st, cam, pb = full["st"], full["cam"], full["pb"]
+    say("projection + binning", full["name"])
     P = {k: v.cpu().numpy() for k, v in st.proj.items()}
     assert np.array_equal(P["means2d"].view(np.uint32), pb["means2d"].view(np.uint32))
     assert np.array_equal(P["depth"].view(np.uint32), pb["depth"].view(np.uint32))
@@ -146,12 +165,12 @@ def _only(ranges, tiles):
 
 def test_fullsize_forward_on_sampled_tiles(full):
     st, cam, prm = full["st"], full["cam"], full["prm"]
-    say("full-size forward, sampled tiles")
+    say("forward, sampled tiles", full["name"])
     tiles = _sampled_tiles(full)
     pb, idx, vals, ranges = _oracle_subset(full, tiles)
     m2d, pv = _subset_values(full, pb, idx)
     ref = O.render_fwd(cam, prm, _only(ranges, tiles), vals, m2d, pv["conic"], pv["opacity"],
-                       pv["rgb"], full["F"], full["B"], rel_margin=KNIFE)
+                       pv["rgb"], full["F"], full["B"], rel_margin=full["knife"])
     out = st.fwd["out"].cpu().numpy()
     last = st.fwd["last"].cpu().numpy().view(np.uint32)
     ntx, _ = _tiles(cam)
@@ -168,18 +187,18 @@ def test_fullsize_forward_on_sampled_tiles(full):
         npx += kn.size
     print(f"  {len(tiles)} tiles, max err {worst:.2e}, knife-edge pixels {knives} of {npx}")
     assert worst <= FWD_TOL
-    assert knives <= max(8, 0.02 * npx)
+    assert knives <= max(8, full["knife_frac"] * npx)
 
 
 def test_fullsize_backward_from_sampled_tiles(full):
     api, st, cam, prm, scene = full["api"], full["st"], full["cam"], full["prm"], full["scene"]
-    say("full-size backward, upstream gradient on sampled tiles")
+    say("backward, upstream gradient on sampled tiles", full["name"])
     tiles = _sampled_tiles(full)
     pb, idx, vals, ranges = _oracle_subset(full, tiles)
     m2d, pv = _subset_values(full, pb, idx)
     rsub = _only(ranges, tiles)
     ref = O.render_fwd(cam, prm, rsub, vals, m2d, pv["conic"], pv["opacity"], pv["rgb"], full["F"],
-                       full["B"], rel_margin=KNIFE)
+                       full["B"], rel_margin=full["knife"])
     ntx, _ = _tiles(cam)
     mask = np.zeros((cam.height, cam.width), bool)
     for t in tiles:
