@@ -562,11 +562,6 @@ __device__ __forceinline__ SubChunk sub_chunk(uint32_t s, const uint32_t* __rest
   return c;
 }
 
-__device__ __forceinline__ bool lane_in(int packed, int lx, int ly) {
-  const int x0 = packed & 7, y0 = (packed >> 3) & 7, x1 = (packed >> 6) & 7, y1 = (packed >> 9) & 7;
-  return packed != 0 && lx >= x0 && lx <= x1 && ly >= y0 && ly <= y1;
-}
-
 // Coverage counts of a wave's entries per local tile by a 2D difference
 // array: an entry covering [x0, x1] x [y0, y1] adds +1 at (x0, y0), -1 at
 // (x1 + 1, y0) and (x0, y1 + 1), +1 at (x1 + 1, y1 + 1) (corners outside the
@@ -762,12 +757,29 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
                       : 0u;
     }
     __syncthreads();
-    // place, in depth order, into the LDS runs
+    // place, in depth order, into the LDS runs. Entry l of the wave covers
+    // this lane's local tile (lx, ly) iff its column range holds lx and its
+    // row range holds ly, so 16 ballots (one per column, one per row) give
+    // every lane the mask of its entries; lanes then walk their set bits in
+    // entry order.
+    uint64_t mine;
+    {
+      const int x0 = pk & 7, y0 = (pk >> 3) & 7, x1 = (pk >> 6) & 7, y1 = (pk >> 9) & 7;
+      const bool v = pk != 0;
+      uint64_t cm = 0, rm = 0;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const uint64_t bc = __ballot(v && x0 <= c && c <= x1);
+        const uint64_t br = __ballot(v && y0 <= c && c <= y1);
+        cm = lx == c ? bc : cm;
+        rm = ly == c ? br : rm;
+      }
+      mine = cm & rm;
+    }
     uint32_t pos = wcnt[w][lane];
-#pragma unroll 8
-    for (int l = 0; l < 64; ++l) {
-      const int p = __builtin_amdgcn_readlane(pk, l);
-      if (lane_in(p, lx, ly)) stage[pos++] = (uint8_t)(64 * w + l);
+    while (mine) {
+      stage[pos++] = (uint8_t)(64 * w + __builtin_ctzll(mine));
+      mine &= mine - 1;
     }
     __syncthreads();
     // write out: wave w copies the runs of tiles w, w + 4, ...
