@@ -546,14 +546,21 @@ struct SubChunk {
   uint32_t e0, e1;   // entries [e0, e1) of the pair array
 };
 
-// block of sub-chunk s: the last b with sub_off[b] <= s (uniform scalar search)
-__device__ __forceinline__ SubChunk sub_chunk(uint32_t s, const uint32_t* __restrict__ sub_off,
-                                              const uint32_t* __restrict__ blk_off, const Geo& geo) {
-  int lo = 0, hi = geo.nblk;  // sub_off[lo] <= s < sub_off[hi]
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (sub_off[mid] <= s) lo = mid; else hi = mid;
+// Block of sub-chunk s: the last b with sub_off[b] <= s (sub_off is
+// nondecreasing). A wave finds it at once: lane b tests block b, 64 blocks per
+// round (coalesced loads instead of a binary search's chain of dependent
+// ones), and the highest block that passes wins.
+__device__ __forceinline__ SubChunk sub_chunk_wave(uint32_t s, const uint32_t* __restrict__ sub_off,
+                                                   const uint32_t* __restrict__ blk_off,
+                                                   const Geo& geo) {
+  const int lane = threadIdx.x & 63;
+  int lo = 0;
+  for (int b0 = 0; b0 < geo.nblk; b0 += 64) {
+    const int b = b0 + lane;
+    const uint64_t ok = __ballot(b < geo.nblk && sub_off[b] <= s);
+    if (ok) lo = b0 + 63 - __clzll(ok);
   }
+  lo = __builtin_amdgcn_readfirstlane(lo);
   SubChunk c;
   c.bx = lo % geo.nbx;
   c.by = lo / geo.nbx;
@@ -611,7 +618,7 @@ __global__ __launch_bounds__(64) void l2_count_kernel(
   const uint32_t total = hdr->total_sub;
   const int lane = threadIdx.x;
   for (uint32_t s = blockIdx.x; s < total; s += gridDim.x) {
-    const SubChunk sc = sub_chunk(s, sub_off, blk_off, geo);
+    const SubChunk sc = sub_chunk_wave(s, sub_off, blk_off, geo);
     int pk[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -717,10 +724,18 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
   const uint32_t total = hdr->total_sub;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, lx = lane & 7, ly = lane >> 3;
   for (uint32_t s = blockIdx.x; s < total; s += gridDim.x) {
-    const SubChunk sc = sub_chunk(s, sub_off, blk_off, geo);
+    const SubChunk sc = sub_chunk_wave(s, sub_off, blk_off, geo);
     uint32_t g;
     int pk;
     load_entry(pairs, sc.e0 + threadIdx.x, sc.e1, g, pk);
+    // the global start of each tile's run, loaded now so that its latency
+    // overlaps the counting below
+    uint32_t dst_l = 0u;
+    if (w == 0) {
+      const int tx = sc.bx * kBlk + lx, ty = sc.by * kBlk + ly;
+      if (tx < geo.ntx && ty < geo.nty)
+        dst_l = tile_off[ty * geo.ntx + tx] + c2[(int64_t)s * kBlkTiles + lane];
+    }
     s_gid[threadIdx.x] = g;
     wdiff[w][lane] = 0;
     __syncthreads();
@@ -751,10 +766,7 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
         wcnt[k][lane] = run;
         run += c[k];
       }
-      const int tx = sc.bx * kBlk + lx, ty = sc.by * kBlk + ly;
-      dst[lane] = (tx < geo.ntx && ty < geo.nty)
-                      ? tile_off[ty * geo.ntx + tx] + c2[(int64_t)s * kBlkTiles + lane]
-                      : 0u;
+      dst[lane] = dst_l;
     }
     __syncthreads();
     // place, in depth order, into the LDS runs. Entry l of the wave covers

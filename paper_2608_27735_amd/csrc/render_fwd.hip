@@ -54,6 +54,7 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
   // the walk crosses, taken when it crosses
   const uint32_t len = end - start;
   const uint32_t cht = (!kHalf && sp.ckpt) ? chunk_of(len, (uint32_t)sp.ch) : 0u;
+  const uint32_t chd = cht != 0u ? cht : 1u;  // divisor (only used when splitting)
   bool split_ok = cht != 0u && len > cht;
   bool crossed = false;
   // Loads run two batches ahead of use: the list values of batch b + 2 and
@@ -70,13 +71,13 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
   }
   for (uint32_t b0 = start; b0 < end; b0 += 256) {
     if (__syncthreads_count(done) == 256) break;
-    if (split_ok && b0 > start && (b0 - start) % cht == 0) {
+    if (split_ok && b0 > start && (b0 - start) % chd == 0) {
       // state after the positions before b0; no pixel walks past a boundary
       // the loop did not reach
       if (tid == 0) {
         const uint32_t got = atomicAdd(&sp.hdr[0], 1u);
         s_base = got < sp.nslots ? got : kNoSlot;
-        sp.slot_of[(size_t)tile * kMaxChunks + (b0 - start) / cht] = s_base;
+        sp.slot_of[(size_t)tile * kMaxChunks + (b0 - start) / chd] = s_base;
       }
       __syncthreads();
       const uint32_t slot = s_base;
