@@ -159,18 +159,19 @@ ABCD_API int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const f
  * a tile walks its list back to front; a tile with a list of many thousand
  * entries would keep one workgroup busy after the rest of the GPU is idle.
  * With a split, whenever a tile's walk in the forward crosses a chunk
- * boundary (every `chunk` list positions, more for lists longer than 64
- * chunks) it takes a 4 KB slot and stores each pixel's transmittance and
- * colour there, plus one slot for the end of the walk; the backward then
- * processes each (tile, chunk) as its own work item, starting from those
- * states. Slots are taken in the forward's tile order (heaviest first); a
- * tile that finds none left is not split. The same split must be given to a
- * forward and its backward; results agree with the unsplit backward up to
- * rounding.
+ * boundary (every `chunk` list positions, up to 63 boundaries: the 64th
+ * chunk runs to the end of the list) it takes a 4 KB slot and stores each
+ * pixel's transmittance and colour there, plus one slot for the end of the
+ * walk; the backward then processes each (tile, chunk) as its own work item,
+ * starting from those states, heaviest items first by the number of entries
+ * the forward staged per chunk. Slots are taken in the forward's tile order
+ * (heaviest first); a tile that finds none left is not split. The same
+ * split must be given to a forward and its backward; results agree with the
+ * unsplit backward up to rounding.
  * workspace: device memory of abcd_split_workspace_size(n_slots) bytes (or
  * more: the slots that fit are used), 256-byte aligned; chunk: a positive
- * multiple of 256. Slots a frame needs: about (sum over tiles of the longest
- * walk in the tile) / chunk + (number of tiles split). */
+ * multiple of 256, at most 2^24. Slots a frame needs: about (sum over tiles
+ * of the longest walk in the tile) / chunk + (number of tiles split). */
 typedef struct {
   void* workspace;
   size_t bytes;

@@ -172,7 +172,7 @@ __device__ __forceinline__ unsigned int wave_sum_u32(unsigned int x) {
 // ------------------------------------------------------ split workspace
 
 // Long tiles are split for the backward: while a tile's walk crosses every
-// ch_t-th position of its list, the forward stores each pixel's transmittance
+// ch-th position of its list (up to kMaxChunks - 1 boundaries), the forward stores each pixel's transmittance
 // and colour there (and, for a tile that crossed one, at the end of its walk),
 // and the backward processes each (tile, chunk) as a work item of its own.
 // Slots are taken as the walks cross boundaries, so memory follows the walks,
@@ -180,6 +180,9 @@ __device__ __forceinline__ unsigned int wave_sum_u32(unsigned int x) {
 // of the caller's workspace:
 //   hdr[16]                  [0] checkpoint slots taken
 //   slot_of[MAX][kMaxChunks] per tile: [0] end-of-walk slot, [b] boundary b
+//   work[MAX]                per tile: the most entries the forward staged
+//                            (kept by the tile test) within one chunk of its
+//                            walk, the whole walk if it is not split
 //   items[MAX + slots]       backward work items (tile, chunk), 8 bytes each
 //   ckpt[slots][256]         (T, C_r, C_g, C_b) per pixel, 256-byte aligned
 constexpr uint32_t kNoSlot = 0xFFFFFFFFu;
@@ -188,22 +191,23 @@ constexpr uint32_t kMaxChunks = 64;
 struct SplitLayout {
   uint32_t* hdr;
   uint32_t* slot_of;
+  uint32_t* work;
   uint2* items;
   float4* ckpt;
   uint32_t nslots;
-  int ch;  // minimum list positions per chunk; 0: no split
+  int ch;  // list positions per chunk (the last chunk takes the rest); 0: no split
 };
 
-// Chunk length of a tile with a list of `len` entries: at least ch, and long
-// enough that the list has at most kMaxChunks chunks (a multiple of 256).
-__host__ __device__ inline uint32_t chunk_of(uint32_t len, uint32_t ch) {
-  const uint32_t need = (len + kMaxChunks - 1) / kMaxChunks;
-  const uint32_t c = ((need + 255u) / 256u) * 256u;
-  return c > ch ? c : ch;
+// Chunk j of a split tile holds list positions [j ch, (j + 1) ch) of its
+// list; the last one (j = kMaxChunks - 1) runs to the end. The boundaries are
+// fixed multiples of ch whatever the list length: a long list whose walks stop
+// early (a dense front) still splits into chunks of ch.
+__host__ __device__ inline uint32_t chunk_hi(uint32_t j, uint32_t ch) {
+  return j + 1 < kMaxChunks ? (j + 1) * ch : 0xFFFFFFFFu;
 }
 
 inline size_t split_fixed_bytes(uint32_t nslots) {
-  const size_t head = 64 + 4 * (size_t)ABCD_MAX_TILES * kMaxChunks +
+  const size_t head = 64 + 4 * (size_t)ABCD_MAX_TILES * (kMaxChunks + 1) +
                       8 * ((size_t)ABCD_MAX_TILES + nslots);
   return (head + 255) & ~size_t(255);
 }
@@ -226,7 +230,8 @@ inline SplitLayout split_layout(void* ws, size_t bytes, int ch) {
   char* b = reinterpret_cast<char*>(ws);
   s.hdr = reinterpret_cast<uint32_t*>(b);
   s.slot_of = reinterpret_cast<uint32_t*>(b + 64);
-  s.items = reinterpret_cast<uint2*>(b + 64 + 4 * (size_t)ABCD_MAX_TILES * kMaxChunks);
+  s.work = reinterpret_cast<uint32_t*>(b + 64 + 4 * (size_t)ABCD_MAX_TILES * kMaxChunks);
+  s.items = reinterpret_cast<uint2*>(b + 64 + 4 * (size_t)ABCD_MAX_TILES * (kMaxChunks + 1));
   s.ckpt = reinterpret_cast<float4*>(b + split_fixed_bytes(s.nslots));
   s.ch = ch;
   return s;
@@ -285,7 +290,7 @@ int32_t launch_loss_l1(int width, int height, const float* out_rgba, const float
 int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, const uint32_t* skip,
                           const char* name, hipStream_t stream);
 int32_t launch_bwd_items(int ntiles, const uint32_t* order, const uint32_t* work,
-                         const uint32_t* tile_ranges, const SplitLayout& split, void* items,
+                         const SplitLayout& split, void* items,
                          uint32_t cap, uint32_t* queue, hipStream_t stream);
 int32_t launch_tile_walk(int width, int height, const uint32_t* last, uint32_t* work,
                          hipStream_t stream);

@@ -102,8 +102,8 @@ int32_t check_split(const abcd_split* sp, SplitLayout* out) {
   if (!sp) return ABCD_OK;
   REQUIRE(sp->workspace != nullptr && (reinterpret_cast<uintptr_t>(sp->workspace) & 255) == 0,
           "split workspace must be non-NULL and 256-byte aligned");
-  REQUIRE(sp->chunk > 0 && sp->chunk % 256 == 0, "split chunk %d must be a positive multiple of 256",
-          sp->chunk);
+  REQUIRE(sp->chunk > 0 && sp->chunk % 256 == 0 && sp->chunk <= (1 << 24),
+          "split chunk %d must be a positive multiple of 256, at most 2^24", sp->chunk);
   REQUIRE(split_slots(sp->bytes) > 0, "split workspace of %zu bytes holds no checkpoint slot",
           sp->bytes);
   *out = split_layout(sp->workspace, sp->bytes, sp->chunk);

@@ -10,62 +10,70 @@
 namespace abcd {
 namespace {
 
-// DPP lane move inside the wave (all rows and banks enabled).
+// DPP lane move inside the wave (all rows and banks enabled; every control
+// used here reads a lane of the same row, so bound_ctrl never applies, and
+// setting it lets the move fold into the add that consumes it).
 template <int kCtrl>
 __device__ __forceinline__ float dpp_mov(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xF, 0xF, false));
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xF, 0xF, true));
 }
 
-// Wave64 sum of nine values at once, by recursive halving: at each of the
-// first three exchanges a lane keeps half of its values and receives the
-// partner's partial sums of that half (quad xor 1, quad xor 2, row rotate 4),
-// the fourth pairs the survivor with the ninth value (row rotate 8), and two
-// cross-row swaps (v_permlane16_swap, v_permlane32_swap) finish. A rotation
-// by 4 (by 8) within a 16-lane row pairs lanes that differ in bit 2 (bit 3)
-// and agree in the lower bits, so partners hold partial sums of the same
-// values over disjoint lane sets. About 30 instructions, all VALU, instead of
-// 9 separate six-step reductions. On return, lane l < 16 holds the wave
-// total of value sum9_slot(l); every row holds the same totals.
-__device__ __forceinline__ float wave_sum9(const float (&g)[9], int lane) {
-  const bool b0 = lane & 1, b1 = lane & 2, b2 = lane & 4, b3 = lane & 8;
+// Wave64 sum of nine values at once. Values 0-7 go through a butterfly that
+// halves the set at each cross-row step without selects: v_permlane32_swap
+// (v_permlane16_swap) of two registers leaves one value's upper-half (odd-row)
+// partner in the other register, so the sum of the two results holds value
+// 2q in the lower half (even rows) and 2q + 1 in the upper half (odd rows).
+// Two such steps leave two registers, folded across lane bit 3 with one
+// keep/send select pair, and the 8-lane groups finish with three DPP adds
+// (quad xor 1, quad xor 2, row rotate 4). Value 8 takes the same steps on its
+// own. About 28 VALU instructions. On return each lane l with (l & 7) >= 4
+// holds the wave total of value sum9_slot(l) in `lo` and of value 8 in `v8`.
+struct Sum9 {
+  float lo, v8;
+};
+__device__ __forceinline__ Sum9 wave_sum9(const float (&g)[9], int lane) {
   float a[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const float keep = b0 ? g[q + 4] : g[q];
-    const float send = b0 ? g[q] : g[q + 4];
-    a[q] = keep + dpp_mov<0xB1>(send);
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(g[2 * q]),
+                                                    __float_as_int(g[2 * q + 1]), false, false);
+    a[q] = __int_as_float(p[0]) + __int_as_float(p[1]);
   }
-  float v8 = g[8] + dpp_mov<0xB1>(g[8]);
   float b[2];
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
-    const float keep = b1 ? a[q + 2] : a[q];
-    const float send = b1 ? a[q] : a[q + 2];
-    b[q] = keep + dpp_mov<0x4E>(send);
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_int(a[2 * q]),
+                                                    __float_as_int(a[2 * q + 1]), false, false);
+    b[q] = __int_as_float(p[0]) + __int_as_float(p[1]);
   }
+  const bool b3 = lane & 8;
+  float c = (b3 ? b[1] : b[0]) + dpp_mov<0x128>(b3 ? b[0] : b[1]);  // row rotate 8
+  c += dpp_mov<0xB1>(c);   // quad [1,0,3,2]
+  c += dpp_mov<0x4E>(c);   // quad [2,3,0,1]
+  c += dpp_mov<0x124>(c);  // row rotate 4 (lane l reads l - 4): lanes with (l & 7) >= 4
+                           // hold the 8-lane sum
+  float v8;
+  {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(g[8]), __float_as_int(g[8]),
+                                                    false, false);
+    v8 = __int_as_float(p[0]) + __int_as_float(p[1]);
+  }
+  {
+    const auto p =
+        __builtin_amdgcn_permlane16_swap(__float_as_int(v8), __float_as_int(v8), false, false);
+    v8 = __int_as_float(p[0]) + __int_as_float(p[1]);
+  }
+  v8 += dpp_mov<0x128>(v8);
+  v8 += dpp_mov<0xB1>(v8);
   v8 += dpp_mov<0x4E>(v8);
-  const float c = (b2 ? b[1] : b[0]) + dpp_mov<0x124>(b2 ? b[0] : b[1]);
   v8 += dpp_mov<0x124>(v8);
-  float d = (b3 ? v8 : c) + dpp_mov<0x128>(b3 ? c : v8);
-  // across rows: v_permlane16_swap / v_permlane32_swap exchange rows 0 <-> 1,
-  // 2 <-> 3 (halves 0 <-> 1); of the two registers each lane gets back, one
-  // is its own value and the other its partner's, so their sum is the pair sum
-  {
-    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_int(d), __float_as_int(d), false,
-                                                    false);
-    d = __int_as_float(p[0]) + __int_as_float(p[1]);
-  }
-  {
-    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(d), __float_as_int(d), false,
-                                                    false);
-    d = __int_as_float(p[0]) + __int_as_float(p[1]);
-  }
-  return d;
+  return Sum9{c, v8};
 }
 
-// Which of the nine values lane l (< 16) holds after wave_sum9.
+// Which of the values 0-7 lane l holds in Sum9::lo: bit 3 of l picks the
+// group of four, bit 4 the pair, bit 5 the member.
 __device__ __forceinline__ int sum9_slot(int l) {
-  return l < 8 ? 4 * (l & 1) + 2 * ((l >> 1) & 1) + ((l >> 2) & 1) : 8;
+  return 4 * ((l >> 3) & 1) + 2 * ((l >> 4) & 1) + ((l >> 5) & 1);
 }
 
 // One work item of the backward: list positions [lo, hi) of `tile`, chunk j
@@ -94,7 +102,6 @@ __device__ __forceinline__ void bwd_item(
   const bool inside = px < k.width && py < k.height;
   const TileBox box = tile_box(k, tile);
   const uint32_t start = tile_ranges[2 * tile];
-  const uint32_t len = tile_ranges[2 * tile + 1] - start;
   // chunk bounds and checkpoint slots (a tile the forward did not split is
   // one item; all of this is uniform)
   uint32_t lo = 0, hi = 0xFFFFFFFFu, slot_hi = kNoSlot, slot_fin = kNoSlot;
@@ -102,9 +109,8 @@ __device__ __forceinline__ void bwd_item(
     const uint32_t* so = sp.slot_of + (size_t)tile * kMaxChunks;
     const uint32_t fin = so[0];
     if (fin < sp.nslots && j < kMaxChunks) {
-      const uint32_t cht = chunk_of(len, (uint32_t)sp.ch);
-      lo = j * cht;
-      hi = lo + cht;
+      lo = j * (uint32_t)sp.ch;
+      hi = chunk_hi(j, (uint32_t)sp.ch);
       slot_fin = fin;
       if (j + 1 < kMaxChunks && so[j + 1] < sp.nslots) slot_hi = so[j + 1];
     } else if (j != 0) {
@@ -148,7 +154,10 @@ __device__ __forceinline__ void bwd_item(
   }
   __syncthreads();
   const uint32_t nent = __builtin_amdgcn_readfirstlane(s_max);  // end of this item's walk
-  const int lane = tid & 63, slot = sum9_slot(lane & 15);
+  // lanes 4, 12, ..., 60 add values 0-7 of an entry, lane 5 value 8
+  const int lane = tid & 63;
+  const bool adder = (lane & 7) == 4 || lane == 5;
+  const int slot = lane == 5 ? 8 : sum9_slot(lane);
   uint32_t wml = lastp;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) wml = max(wml, (uint32_t)__shfl_xor((int)wml, off, 64));
@@ -253,8 +262,10 @@ __device__ __forceinline__ void bwd_item(
       gr[3] = q * dy;
       gr[4] = r * dy;
       gr[5] = ae.e * dm;
-      const float v = wave_sum9(gr, lane);
-      if (lane < 9) atomicAdd(&s_acc[9 * j + slot], v);
+      const Sum9 v = wave_sum9(gr, lane);
+      float out = lane == 5 ? v.v8 : v.lo;
+      asm volatile("" : "+v"(out));  // the last folds stay outside the branch (DPP add)
+      if (adder) atomicAdd(&s_acc[9 * j + slot], out);
     }
     }
     __syncthreads();
@@ -358,9 +369,12 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
   const uint32_t max_items =
       (uint32_t)k.ntiles + (split.ckpt ? split.nslots : 0u);
   TRY_STATUS(launch_tile_walk(k.width, k.height, last, work, stream));
-  TRY_STATUS(launch_tile_order(k.ntiles, work, order, nullptr, "bwd_order", stream));
+  // heaviest items first: by the forward's per-chunk estimate when split,
+  // else by the walk
+  TRY_STATUS(launch_tile_order(k.ntiles, split.ckpt ? split.work : work, order, nullptr,
+                               "bwd_order", stream));
   TRY_STATUS(
-      launch_bwd_items(k.ntiles, order, work, tile_ranges, split, items, max_items, queue, stream));
+      launch_bwd_items(k.ntiles, order, work, split, items, max_items, queue, stream));
   const int grid = (int)std::min<int64_t>(bwd_resident_blocks(), max_items);
   ABCD_LAUNCH("render_bwd", render_bwd_kernel, grid, kBlock, 0, stream, k, tile_ranges,
               values_sorted, reinterpret_cast<const float2*>(means2d),

@@ -53,10 +53,13 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
   // Checkpoints for the split backward (uniform state): a slot per boundary
   // the walk crosses, taken when it crosses
   const uint32_t len = end - start;
-  const uint32_t cht = (!kHalf && sp.ckpt) ? chunk_of(len, (uint32_t)sp.ch) : 0u;
+  const uint32_t cht = (!kHalf && sp.ckpt) ? (uint32_t)sp.ch : 0u;
   const uint32_t chd = cht != 0u ? cht : 1u;  // divisor (only used when splitting)
   bool split_ok = cht != 0u && len > cht;
   bool crossed = false;
+  // entries staged in the current chunk and the most in any chunk so far: the
+  // backward's cost estimate for ordering its work items
+  uint32_t staged = 0, staged_max = 0;
   // Loads run two batches ahead of use: the list values of batch b + 2 and
   // the gathers of batch b + 1 are in flight while batch b blends. Positions
   // past the list read its last entry (valid == false), so every load is
@@ -71,7 +74,7 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
   }
   for (uint32_t b0 = start; b0 < end; b0 += 256) {
     if (__syncthreads_count(done) == 256) break;
-    if (split_ok && b0 > start && (b0 - start) % chd == 0) {
+    if (split_ok && b0 > start && (b0 - start) % chd == 0 && (b0 - start) / chd < kMaxChunks) {
       // state after the positions before b0; no pixel walks past a boundary
       // the loop did not reach
       if (tid == 0) {
@@ -86,6 +89,8 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
       } else {
         sp.ckpt[(size_t)slot * 256 + tid] = make_float4(T, cr, cg, cb);
         crossed = true;
+        staged_max = max(staged_max, staged);
+        staged = 0;
       }
     }
     const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, rec.co.x, rec.co.y, rec.co.z,
@@ -93,6 +98,7 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
                                                      box.y0, box.y1);
     int pos;
     const int cnt = compact(keep, s_wcnt, pos);
+    staged += (uint32_t)cnt;
     if (keep) {
       const Splat sp = make_splat(rec.m, rec.co);
       s_ga[pos] = make_float4(sp.u, sp.v, sp.qa, sp.qb);
@@ -165,6 +171,7 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
       }
       s_base = fin;
       sp.slot_of[(size_t)tile * kMaxChunks] = fin;
+      sp.work[tile] = max(staged_max, staged);
     }
     __syncthreads();
     const uint32_t slot = s_base;

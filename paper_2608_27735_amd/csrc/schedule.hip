@@ -116,7 +116,7 @@ __global__ __launch_bounds__(kBlock) void tile_walk_kernel(int width, int height
 // workgroups advance).
 __global__ __launch_bounds__(kOrderThreads) void bwd_items_kernel(
     int ntiles, const uint32_t* __restrict__ order, const uint32_t* __restrict__ work,
-    const uint32_t* __restrict__ tile_ranges, SplitLayout sp, uint2* __restrict__ items,
+    SplitLayout sp, uint2* __restrict__ items,
     uint32_t cap, uint32_t* __restrict__ queue) {
   __shared__ uint32_t s_wsum[kOrderWaves];
   __shared__ uint32_t s_off;
@@ -132,9 +132,8 @@ __global__ __launch_bounds__(kOrderThreads) void bwd_items_kernel(
       if (walk > 0) {
         n = 1;
         if (sp.ckpt && sp.slot_of[(size_t)t * kMaxChunks] < sp.nslots) {
-          const uint32_t len = tile_ranges[2 * t + 1] - tile_ranges[2 * t];
-          const uint32_t cht = chunk_of(len, (uint32_t)sp.ch);
-          n = min((walk + cht - 1) / cht, kMaxChunks);
+          const uint32_t ch = (uint32_t)sp.ch;
+          n = min((walk + ch - 1) / ch, kMaxChunks);
         }
       }
     }
@@ -169,10 +168,10 @@ __global__ __launch_bounds__(kOrderThreads) void bwd_items_kernel(
 }  // namespace
 
 int32_t launch_bwd_items(int ntiles, const uint32_t* order, const uint32_t* work,
-                         const uint32_t* tile_ranges, const SplitLayout& split, void* items,
+                         const SplitLayout& split, void* items,
                          uint32_t cap, uint32_t* queue, hipStream_t stream) {
   ABCD_LAUNCH("bwd_order", bwd_items_kernel, 1, kOrderThreads, 0, stream, ntiles, order, work,
-              tile_ranges, split, reinterpret_cast<uint2*>(items), cap, queue);
+              split, reinterpret_cast<uint2*>(items), cap, queue);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }

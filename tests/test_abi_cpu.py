@@ -190,6 +190,7 @@ def test_split_workspace_and_rejections(lib):
     for ws, nbytes, chunk in ((FAKE + 8, 1 << 30, 256),   # misaligned
                               (FAKE, 1 << 30, 300),       # chunk not a multiple of 256
                               (FAKE, 1 << 30, 0),
+                              (FAKE, 1 << 30, 1 << 25),   # chunk above 2^24
                               (FAKE, 64, 256)):           # no room for a slot
         sp = _lib.abcd_split(ws, nbytes, chunk, 0)
         assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, C.byref(sp), None) == 1

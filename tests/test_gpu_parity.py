@@ -64,6 +64,15 @@ def cases():
     prm = RasterParams(sh_degree=2)
     sc2 = S.gaussians(rr, rr.uniform(-1, 1, (3000, 3)), 2, math.log(0.05), 0.6)
     out.append(("ragged-203x117", cam, prm, sc2))
+    # a deep tile: 24,000 faint sub-pixel Gaussians over a few tiles, so walks
+    # run through lists of thousands of entries without saturating (more than
+    # 64 chunks of 256: the split's open-ended last chunk)
+    rd = S.rng(22)
+    cam = look_at((0.0, -3.0, 0.0), (0, 0, 0), 48, 48)
+    sc3 = S.gaussians(rd, rd.uniform((-0.5, -0.5, -0.5), (0.5, 0.5, 0.5), (24000, 3)), 0,
+                      math.log(0.02), 0.2)
+    sc3["opacity_logits"] = rd.normal(-4.0, 0.3, 24000).astype(np.float32)
+    out.append(("deep-tile-48x48", cam, RasterParams(sh_degree=0), sc3))
     return out
 
 
