@@ -131,7 +131,8 @@ ABCD_API int32_t abcd_project(const abcd_camera* cam /* host */, const abcd_rast
  * NULL, then not written); tile_ranges[tiles][2] = [start, end) per tile
  * (start = number of pairs of lower tiles); tile_order[tiles] (may be NULL,
  * then not written): a schedule for abcd_render_fwd, the tile indices
- * ordered by decreasing floor(log2(list length)), ties in tile order.
+ * ordered by decreasing list length kept to its leading three bits (the
+ * octave and its quarter), ties in tile order.
  *
  * capacity: number of elements values_sorted (and keys_sorted) can hold. If
  * the intersection count M exceeds it, nothing is written to values_sorted,

@@ -8,9 +8,10 @@
 //
 // The work estimate is the tile's list length for the forward (known after
 // binning) and the tile's largest per-pixel walk length for the backward
-// (known after the forward). The order is a stable bucket sort by the octave
-// of the estimate, so tiles of one octave keep their raster order and
-// neighbouring tiles stay close in launch order.
+// (known after the forward). The order is a stable bucket sort by the
+// estimate's quarter octave (leading one and the two bits after it), so tiles
+// of one bucket keep their raster order and neighbouring tiles stay close in
+// launch order.
 #include "abcd_internal.h"
 
 namespace abcd {
@@ -18,17 +19,23 @@ namespace {
 
 constexpr int kOrderThreads = 1024;
 constexpr int kOrderWaves = kOrderThreads / 64;
-constexpr int kBuckets = 33;  // leading-zero count of the work, 32 for no work
-constexpr int kNone = 64;     // no tile (matches no bucket)
+constexpr int kBuckets = 129;  // 4 per leading-zero count of the work, 128 for no work
+constexpr int kNone = 255;     // no tile (matches no bucket)
 
-__device__ __forceinline__ int bucket_of(uint32_t work) { return work ? __clz(work) : 32; }
+// Heavier work, smaller bucket: 4 lz + (3 - the two bits after the leading one).
+__device__ __forceinline__ int bucket_of(uint32_t work) {
+  if (!work) return 128;
+  const int lz = __clz(work);
+  const uint32_t sub = lz < 31 ? (work << (lz + 1)) >> 30 : 0u;
+  return 4 * lz + 3 - (int)sub;
+}
 
 // Lanes of the calling wave holding the same bucket as this lane (buckets
-// below 64; kNone never matches a real bucket).
+// below 256; kNone never matches a real bucket).
 __device__ __forceinline__ uint64_t match_bucket(int key) {
   uint64_t peers = __ballot(1);
 #pragma unroll
-  for (int b = 0; b < 7; ++b) {
+  for (int b = 0; b < 8; ++b) {
     const bool bit = (key >> b) & 1;
     const uint64_t m = __ballot(bit);
     peers &= bit ? m : ~m;

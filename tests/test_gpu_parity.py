@@ -133,10 +133,17 @@ def test_bin_sort_bitexact(api, case):
     assert np.array_equal(np32(b["values"][:m]).view(np.uint32), values)
     assert np.array_equal(np32(b["keys"][:m]).view(np.uint64), keys)
     assert np.array_equal(np32(b["tile_ranges"]).view(np.uint32), ranges)
-    # the forward's schedule: tiles by decreasing octave of list length, stable
+    # the forward's schedule: tiles by decreasing quarter octave of list
+    # length (the leading one and the two bits after it), stable
     length = (ranges[:, 1] - ranges[:, 0]).astype(np.int64)
-    octave = np.array([32 - int(x).bit_length() for x in length])
-    assert np.array_equal(np32(b["tile_order"]), np.argsort(octave, kind="stable"))
+    def quarter_octave(x):
+        if x == 0:
+            return 128
+        nb = int(x).bit_length()
+        sub = (int(x) >> (nb - 3)) & 3 if nb >= 3 else (int(x) << (3 - nb)) & 3
+        return 4 * (32 - nb) + 3 - sub
+    key = np.array([quarter_octave(x) for x in length])
+    assert np.array_equal(np32(b["tile_order"]), np.argsort(key, kind="stable"))
     # determinism: a second call gives identical bytes
     b2 = api.bin_sort(cam.width, cam.height, pd, want_keys=True)
     torch.cuda.synchronize()
