@@ -183,6 +183,7 @@ __device__ __forceinline__ unsigned int wave_sum_u32(unsigned int x) {
 //   work[MAX]                per tile: the most entries the forward staged
 //                            (kept by the tile test) within one chunk of its
 //                            walk, the whole walk if it is not split
+//   walk[MAX]                per tile: the largest per-pixel walk length
 //   items[MAX + slots]       backward work items (tile, chunk), 8 bytes each
 //   ckpt[slots][256]         (T, C_r, C_g, C_b) per pixel, 256-byte aligned
 constexpr uint32_t kNoSlot = 0xFFFFFFFFu;
@@ -192,6 +193,7 @@ struct SplitLayout {
   uint32_t* hdr;
   uint32_t* slot_of;
   uint32_t* work;
+  uint32_t* walk;
   uint2* items;
   float4* ckpt;
   uint32_t nslots;
@@ -207,7 +209,7 @@ __host__ __device__ inline uint32_t chunk_hi(uint32_t j, uint32_t ch) {
 }
 
 inline size_t split_fixed_bytes(uint32_t nslots) {
-  const size_t head = 64 + 4 * (size_t)ABCD_MAX_TILES * (kMaxChunks + 1) +
+  const size_t head = 64 + 4 * (size_t)ABCD_MAX_TILES * (kMaxChunks + 2) +
                       8 * ((size_t)ABCD_MAX_TILES + nslots);
   return (head + 255) & ~size_t(255);
 }
@@ -231,7 +233,8 @@ inline SplitLayout split_layout(void* ws, size_t bytes, int ch) {
   s.hdr = reinterpret_cast<uint32_t*>(b);
   s.slot_of = reinterpret_cast<uint32_t*>(b + 64);
   s.work = reinterpret_cast<uint32_t*>(b + 64 + 4 * (size_t)ABCD_MAX_TILES * kMaxChunks);
-  s.items = reinterpret_cast<uint2*>(b + 64 + 4 * (size_t)ABCD_MAX_TILES * (kMaxChunks + 1));
+  s.walk = reinterpret_cast<uint32_t*>(b + 64 + 4 * (size_t)ABCD_MAX_TILES * (kMaxChunks + 1));
+  s.items = reinterpret_cast<uint2*>(b + 64 + 4 * (size_t)ABCD_MAX_TILES * (kMaxChunks + 2));
   s.ckpt = reinterpret_cast<float4*>(b + split_fixed_bytes(s.nslots));
   s.ch = ch;
   return s;
@@ -289,9 +292,9 @@ int32_t launch_loss_l1(int width, int height, const float* out_rgba, const float
 // and the per-tile maximum of the forward's walk lengths as a work estimate.
 int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, const uint32_t* skip,
                           const char* name, hipStream_t stream);
-int32_t launch_bwd_items(int ntiles, const uint32_t* order, const uint32_t* work,
-                         const SplitLayout& split, void* items,
-                         uint32_t cap, uint32_t* queue, hipStream_t stream);
+int32_t launch_bwd_schedule(int ntiles, const uint32_t* key, const uint32_t* walk,
+                            uint32_t* order, const SplitLayout& split, void* items, uint32_t cap,
+                            uint32_t* queue, hipStream_t stream);
 int32_t launch_tile_walk(int width, int height, const uint32_t* last, uint32_t* work,
                          hipStream_t stream);
 

@@ -38,7 +38,7 @@
 namespace abcd {
 namespace {
 
-constexpr int kRsItems = 16;
+constexpr int kRsItems = 8;
 constexpr int kRsTile = kBlock * kRsItems;  // keys per radix block
 constexpr int kScanThreads = 1024;
 constexpr int kRanksPerWave = 256;

@@ -368,13 +368,16 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
   uint2* items = split.ckpt ? split.items : own_items;
   const uint32_t max_items =
       (uint32_t)k.ntiles + (split.ckpt ? split.nslots : 0u);
-  TRY_STATUS(launch_tile_walk(k.width, k.height, last, work, stream));
+  // each tile's largest walk: from the forward when split, else from `last`
+  const uint32_t* walk = work;
+  if (split.ckpt)
+    walk = split.walk;
+  else
+    TRY_STATUS(launch_tile_walk(k.width, k.height, last, work, stream));
   // heaviest items first: by the forward's per-chunk estimate when split,
   // else by the walk
-  TRY_STATUS(launch_tile_order(k.ntiles, split.ckpt ? split.work : work, order, nullptr,
-                               "bwd_order", stream));
-  TRY_STATUS(
-      launch_bwd_items(k.ntiles, order, work, split, items, max_items, queue, stream));
+  TRY_STATUS(launch_bwd_schedule(k.ntiles, split.ckpt ? split.work : walk, walk, order, split,
+                                 items, max_items, queue, stream));
   const int grid = (int)std::min<int64_t>(bwd_resident_blocks(), max_items);
   ABCD_LAUNCH("render_bwd", render_bwd_kernel, grid, kBlock, 0, stream, k, tile_ranges,
               values_sorted, reinterpret_cast<const float2*>(means2d),

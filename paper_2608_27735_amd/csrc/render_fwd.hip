@@ -28,6 +28,7 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
   __shared__ int s_wcnt[4];
   __shared__ unsigned long long s_nb;
   __shared__ uint32_t s_base;
+  __shared__ uint32_t s_walk;  // largest walk of the tile (split only)
   const int tile = tile_of_block(k, order);
   if (tile >= k.ntiles) return;
   const int tid = threadIdx.x;
@@ -49,7 +50,10 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     thr = vis > 0.0f ? k.t_min / vis : __builtin_huge_valf();
     done = vis < k.t_min;
   }
-  if (tid == 0) s_nb = 0;
+  if (tid == 0) {
+    s_nb = 0;
+    s_walk = 0;
+  }
   // Checkpoints for the split backward (uniform state): a slot per boundary
   // the walk crosses, taken when it crosses
   const uint32_t len = end - start;
@@ -162,8 +166,14 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     // s_wcnt is rewritten only after the next barrier
   }
   if (cht != 0u) {
-    __syncthreads();  // every thread has read s_base
+    // the tile's largest walk, for the backward's schedule
+    uint32_t wmax = lastk;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) wmax = max(wmax, (uint32_t)__shfl_xor((int)wmax, off, 64));
+    if ((tid & 63) == 0 && wmax) atomicMax(&s_walk, wmax);
+    __syncthreads();  // every thread has read s_base; s_walk is complete
     if (tid == 0) {
+      sp.walk[tile] = s_walk;
       uint32_t fin = kNoSlot;
       if (split_ok && crossed) {
         const uint32_t got = atomicAdd(&sp.hdr[0], 1u);

@@ -43,14 +43,31 @@ __device__ __forceinline__ uint64_t match_bucket(int key) {
   return peers;
 }
 
-__global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
-                                                                   const uint32_t* __restrict__ work,
-                                                                   uint32_t* __restrict__ order,
-                                                                   const uint32_t* __restrict__ skip) {
-  __shared__ uint8_t s_key[ABCD_MAX_TILES];
+// Exclusive scan of s_base[0, kBuckets) in place by the first wave.
+__device__ __forceinline__ void scan_buckets(uint32_t* s_base) {
+  if (threadIdx.x < 64) {
+    const int l = threadIdx.x;
+    uint32_t carry = 0;
+    for (int b0 = 0; b0 < kBuckets; b0 += 64) {
+      const uint32_t c = b0 + l < kBuckets ? s_base[b0 + l] : 0u;
+      uint32_t inc = c;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t y = (uint32_t)__shfl_up((int)inc, d, 64);
+        if (l >= d) inc += y;
+      }
+      if (b0 + l < kBuckets) s_base[b0 + l] = carry + inc - c;
+      carry += (uint32_t)__shfl((int)inc, 63, 64);
+    }
+  }
+}
+
+// The ordering itself, by one workgroup of kOrderThreads threads; s_key is
+// workgroup memory of ABCD_MAX_TILES bytes.
+__device__ __forceinline__ void order_tiles(int ntiles, const uint32_t* __restrict__ work,
+                                            uint32_t* __restrict__ order, uint8_t* s_key) {
   __shared__ uint32_t s_base[kBuckets];
   __shared__ uint32_t s_wc[kOrderWaves][kBuckets];  // per wave counts, then exclusive offsets
-  if (skip && *skip) return;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
   const uint64_t below = (1ull << l) - 1ull;
   if (tid < kBuckets) s_base[tid] = 0;
@@ -66,14 +83,7 @@ __global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
     if (key != kNone && (peers & below) == 0) atomicAdd(&s_base[key], (uint32_t)__popcll(peers));
   }
   __syncthreads();
-  if (tid == 0) {
-    uint32_t acc = 0;
-    for (int b = 0; b < kBuckets; ++b) {
-      const uint32_t c = s_base[b];
-      s_base[b] = acc;
-      acc += c;
-    }
-  }
+  scan_buckets(s_base);
   // stable placement, one chunk of tiles at a time
   for (int t0 = 0; t0 < ntiles; t0 += kOrderThreads) {
     for (int i = tid; i < kOrderWaves * kBuckets; i += kOrderThreads) (&s_wc[0][0])[i] = 0;
@@ -98,6 +108,15 @@ __global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
   }
 }
 
+__global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
+                                                                   const uint32_t* __restrict__ work,
+                                                                   uint32_t* __restrict__ order,
+                                                                   const uint32_t* __restrict__ skip) {
+  __shared__ uint8_t s_key[ABCD_MAX_TILES];
+  if (skip && *skip) return;
+  order_tiles(ntiles, work, order, s_key);
+}
+
 // Largest per-pixel walk length (the forward's `last`) of each tile.
 __global__ __launch_bounds__(kBlock) void tile_walk_kernel(int width, int height, int ntx,
                                                            const uint32_t* __restrict__ last,
@@ -117,33 +136,38 @@ __global__ __launch_bounds__(kBlock) void tile_walk_kernel(int width, int height
 }
 
 // Work items of the backward, in the order of `order` (tiles by decreasing
-// walk): a tile with no walk has none, a tile the forward split (it has an
-// end-of-walk slot) one per chunk its walk reaches, any other tile one. Writes items (tile, chunk),
-// queue[0] = their number and queue[1] = 0 (the head the backward's
-// workgroups advance).
-__global__ __launch_bounds__(kOrderThreads) void bwd_items_kernel(
-    int ntiles, const uint32_t* __restrict__ order, const uint32_t* __restrict__ work,
-    SplitLayout sp, uint2* __restrict__ items,
-    uint32_t cap, uint32_t* __restrict__ queue) {
+// estimated work): a tile with no walk has none, a tile the forward split (it
+// has an end-of-walk slot) one per chunk its walk reaches, any other tile
+// one. Writes items (tile, chunk), queue[0] = their number and queue[1] = 0
+// (the head the backward's workgroups advance). s_n is workgroup memory of
+// ABCD_MAX_TILES bytes.
+__device__ __forceinline__ void build_items(int ntiles, const uint32_t* __restrict__ order,
+                                            const uint32_t* __restrict__ walk,
+                                            const SplitLayout& sp, uint2* __restrict__ items,
+                                            uint32_t cap, uint32_t* __restrict__ queue,
+                                            uint8_t* s_n) {
   __shared__ uint32_t s_wsum[kOrderWaves];
   __shared__ uint32_t s_off;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
   if (tid == 0) s_off = 0;
+  // items per position of the order, the dependent loads of eight positions
+  // in flight at once
+#pragma unroll 8
+  for (int i = tid; i < ntiles; i += kOrderThreads) {
+    const uint32_t t = order[i];
+    const uint32_t wk = walk[t];
+    uint32_t n = wk > 0 ? 1u : 0u;
+    if (wk > 0 && sp.ckpt && sp.slot_of[(size_t)t * kMaxChunks] < sp.nslots) {
+      const uint32_t ch = (uint32_t)sp.ch;
+      n = min((wk + ch - 1) / ch, kMaxChunks);
+    }
+    s_n[i] = (uint8_t)n;
+  }
   __syncthreads();
   for (int i0 = 0; i0 < ntiles; i0 += kOrderThreads) {
     const int i = i0 + tid;
-    uint32_t t = 0, n = 0;
-    if (i < ntiles) {
-      t = order[i];
-      const uint32_t walk = work[t];
-      if (walk > 0) {
-        n = 1;
-        if (sp.ckpt && sp.slot_of[(size_t)t * kMaxChunks] < sp.nslots) {
-          const uint32_t ch = (uint32_t)sp.ch;
-          n = min((walk + ch - 1) / ch, kMaxChunks);
-        }
-      }
-    }
+    const uint32_t n = i < ntiles ? s_n[i] : 0u;
+    const uint32_t t = n ? order[i] : 0u;
     // exclusive prefix of n over the workgroup
     uint32_t inc = n;
 #pragma unroll
@@ -172,13 +196,26 @@ __global__ __launch_bounds__(kOrderThreads) void bwd_items_kernel(
   }
 }
 
+// The backward's schedule in one launch: tiles ordered by `key`, then the
+// work items in that order (walk: each tile's largest per-pixel walk).
+__global__ __launch_bounds__(kOrderThreads) void bwd_schedule_kernel(
+    int ntiles, const uint32_t* __restrict__ key, const uint32_t* __restrict__ walk,
+    uint32_t* __restrict__ order, SplitLayout sp, uint2* __restrict__ items, uint32_t cap,
+    uint32_t* __restrict__ queue) {
+  __shared__ uint8_t s_buf[ABCD_MAX_TILES];  // bucket keys, then items per position
+  order_tiles(ntiles, key, order, s_buf);
+  // the order is read back by other threads of this workgroup (the barrier
+  // at the end of order_tiles also ends its use of s_buf)
+  build_items(ntiles, order, walk, sp, items, cap, queue, s_buf);
+}
+
 }  // namespace
 
-int32_t launch_bwd_items(int ntiles, const uint32_t* order, const uint32_t* work,
-                         const SplitLayout& split, void* items,
-                         uint32_t cap, uint32_t* queue, hipStream_t stream) {
-  ABCD_LAUNCH("bwd_order", bwd_items_kernel, 1, kOrderThreads, 0, stream, ntiles, order, work,
-              split, reinterpret_cast<uint2*>(items), cap, queue);
+int32_t launch_bwd_schedule(int ntiles, const uint32_t* key, const uint32_t* walk,
+                            uint32_t* order, const SplitLayout& split, void* items, uint32_t cap,
+                            uint32_t* queue, hipStream_t stream) {
+  ABCD_LAUNCH("bwd_order", bwd_schedule_kernel, 1, kOrderThreads, 0, stream, ntiles, key, walk,
+              order, split, reinterpret_cast<uint2*>(items), cap, queue);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }
