@@ -69,10 +69,13 @@ def _flagged(prm):
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_fb_stop_step_matches_oracle(api, case):
+@pytest.mark.parametrize("chunk", [None, 256], ids=["whole", "split256"])
+def test_fb_stop_step_matches_oracle(api, case, chunk):
+    """The compositing-aware stop, with and without the backward's split of
+    long tiles (its checkpoints then follow the shortened walks)."""
     name, cam, prm0, scene = case
     prm = _flagged(prm0)
-    say("fb_stop step", name, scene["means"].shape)
+    say("fb_stop step", name, scene["means"].shape, chunk)
     r = S.rng(51)
     F = S.dense_front(r, cam.height, cam.width)
     B = S.background_pair(r, cam.height, cam.width)[1]
@@ -86,8 +89,13 @@ def test_fb_stop_step_matches_oracle(api, case):
     p = api.project(cam, prm, **params)
     bins = api.bin_sort(cam.width, cam.height, p)
     nb = torch.zeros(1, dtype=torch.int64, device=dev())
-    fw = api.render_fwd(cam, prm, bins, p, F=Fd, B=Bd, n_blends=nb)
-    grads = api.render_bwd(cam, prm, params, p, bins, fw, torch.from_numpy(G).to(dev()), F=Fd, B=Bd)
+    split = None
+    if chunk:
+        split = api.make_split(bins["n_isect"] // chunk + api.n_tiles(cam.width, cam.height) + 1,
+                               chunk)
+    fw = api.render_fwd(cam, prm, bins, p, F=Fd, B=Bd, n_blends=nb, split=split)
+    grads = api.render_bwd(cam, prm, params, p, bins, fw, torch.from_numpy(G).to(dev()), F=Fd, B=Bd,
+                           split=split)
     torch.cuda.synchronize()
     knife = ref0["fwd"]["knife"]
     err = np.abs(np32(fw["out"]) - ref0["fwd"]["out"]).max(axis=-1)
