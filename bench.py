@@ -63,13 +63,13 @@ def algorithmic_bytes(name, n, n_vis, m, npix, k, sh_coeffs, covered_px=None):
     covered_px: layer-pixels inside the cached images' coverage boxes (the
     collapse reads nothing outside them); None means every layer-pixel."""
     param = 4 * (3 + 3 + 4 + 1 + 3 * sh_coeffs)       # means, log-scales, quats, logit, SH
-    proj = 4 * (2 + 4 + 1 + 1 + 1 + 3)                 # means2d, conic_opacity, depth, radius, tiles, rgb
+    proj = 4 * (2 + 4 + 1 + 2 + 1 + 3)                 # means2d, conic_opacity, depth, extent, tiles, rgb
     if name == "composite":
         return 8 * (npix * k if covered_px is None else covered_px) + 32 * npix
     if name == "project":
         return n * (param + proj)
     if name == "project_bwd":
-        return n * (2 * param + 9 * 4 + 4)             # params in, grads out, g2d and radius in
+        return n * (2 * param + 9 * 4 + 4)             # params in, grads out, g2d and extent.x in
     if name == "l2_scatter":
         return m * 4                                   # the sorted Gaussian indices
     return None

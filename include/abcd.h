@@ -106,20 +106,35 @@ typedef struct {
  *
  * Per Gaussian i writes
  *   means2d[i][2]        pixel-space mean (u, v)
- *   conic_opacity[i][4]  (a, b, c, o): inverse 2D covariance [[a, b], [b, c]]
- *                        and opacity o = sigmoid(logit)
+ *   conic_opacity[i][4]  (l11, l21, l22, o): the inverse 2D covariance (the
+ *                        conic) [[a, b], [b, c]] as its Cholesky factor,
+ *                        a = l11^2, b = l11 l21, c = l21^2 + l22^2 (computed
+ *                        in fp64; the blend kernels evaluate the quadratic
+ *                        form as a sum of two squares, which a badly
+ *                        conditioned conic does not amplify), and opacity
+ *                        o = sigmoid(logit)
  *   depth[i]             view-space z
- *   radius[i]            support radius in pixels
- *   tiles_touched[i]     number of 16x16 tiles of its support rectangle
+ *   extent[i][2]         (ex, ey): half extents in pixels of the box that bins
+ *                        the Gaussian: the support square (radius_sigmas times
+ *                        the square root of the largest eigenvalue of the 2D
+ *                        covariance) cut per axis to the extent of the ellipse
+ *                        where alpha can reach alpha_min (|dx| <= sqrt(L A),
+ *                        |dy| <= sqrt(L C), A and C the covariance's diagonal,
+ *                        L = 1.001 tau + 0.001 and tau = 2 ((1 - e) ln 2 +
+ *                        min(logit, 0)) >= 2 ln(o / alpha_min) for alpha_min =
+ *                        m 2^e, m in [0.5, 1)); no pixel of a cut-off tile
+ *                        could blend the Gaussian, so images are unchanged
+ *   tiles_touched[i]     number of 16x16 tiles of that box
  *   rgb[i][3]            colour max(0, SH(view direction) + 0.5)
- * A culled Gaussian (behind near_plane, degenerate, non-finite, or with no tile
- * on screen) gets zeros in every output. The values deciding culling, the tile
- * rectangle and the depth key follow one fixed fp32 operation order (the
- * numerical contract of this library). n may be 0. */
+ * A culled Gaussian (behind near_plane, degenerate, non-finite, with no tile
+ * on screen, or with alpha_min out of reach) gets zeros in every output. The
+ * values deciding culling, the tile box and the depth key follow one fixed
+ * fp32 operation order (the numerical contract of this library); extent must
+ * be 8-byte aligned. n may be 0. */
 ABCD_API int32_t abcd_project(const abcd_camera* cam /* host */, const abcd_raster_params* prm /* host */,
                      int64_t n, const float* means, const float* log_scales, const float* quats,
                      const float* opacity_logits, const float* sh, float* means2d,
-                     float* conic_opacity, float* depth, float* radius, uint32_t* tiles_touched,
+                     float* conic_opacity, float* depth, float* extent, uint32_t* tiles_touched,
                      float* rgb, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
@@ -149,7 +164,7 @@ ABCD_API int32_t abcd_project(const abcd_camera* cam /* host */, const abcd_rast
 ABCD_API int32_t abcd_bin_sort_workspace_size(int64_t n, int64_t capacity, int32_t width,
                                               int32_t height, size_t* bytes);
 ABCD_API int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const float* means2d,
-                      const float* radius, const float* depth, const uint32_t* tiles_touched,
+                      const float* extent, const float* depth, const uint32_t* tiles_touched,
                       int64_t capacity, void* workspace, size_t ws_bytes, uint64_t* keys_sorted,
                       uint32_t* values_sorted, uint32_t* tile_ranges, uint32_t* tile_order,
                       int64_t* n_isect /* host */, hipStream_t stream);
@@ -245,7 +260,7 @@ ABCD_API int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes);
 ABCD_API int32_t abcd_render_bwd(const abcd_camera* cam /* host */, const abcd_raster_params* prm /* host */,
                         int64_t n, const float* means, const float* log_scales, const float* quats,
                         const float* opacity_logits, const float* sh, const float* means2d,
-                        const float* conic_opacity, const float* rgb, const float* radius,
+                        const float* conic_opacity, const float* rgb, const float* extent,
                         const uint32_t* tile_ranges, const uint32_t* values_sorted,
                         const float* F, const float* B, const float* final_T, const uint32_t* last,
                         const float* dL_dout, void* workspace, size_t ws_bytes, float* d_means,

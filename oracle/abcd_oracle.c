@@ -35,8 +35,9 @@ static uint32_t f32_bits(float f) {
  * The only double step is exp() of the log-scale, rounded once to fp32.
  */
 static int proj_bin_one(const orc_camera* c, const orc_params* p, const float* mu,
-                        const float* ls, const float* q, float* u_out, float* v_out,
-                        float* z_out, float* r_out, int32_t rect[4]) {
+                        const float* ls, const float* q, float ologit, float* u_out,
+                        float* v_out, float* z_out, float* r_out, float ext_out[2],
+                        int32_t rect[4]) {
   const float* R = c->R;
   /* view-space position */
   float tx = ((R[0] * mu[0] + R[1] * mu[1]) + R[2] * mu[2]) + c->t[0];
@@ -116,11 +117,30 @@ static int proj_bin_one(const orc_camera* c, const orc_params* p, const float* m
   float lmax = mid + sqrtf(disc);
   float r = p->radius_sigmas * sqrtf(lmax);
   if (!isfinite(u) || !isfinite(v) || !isfinite(r)) return 0;
-  /* tile rectangle of the square [u-r, u+r] x [v-r, v+r] */
-  float tx0 = floorf((u - r) * 0.0625f);
-  float tx1 = floorf((u + r) * 0.0625f);
-  float ty0 = floorf((v - r) * 0.0625f);
-  float ty1 = floorf((v + r) * 0.0625f);
+  /*
+   * Binning box: the support square cut per axis to the ellipse where alpha
+   * can reach alpha_min. At a pixel offset d, alpha = o exp(-q/2) with
+   * q = d^T Sigma^-1 d >= d_x^2 / A (and >= d_y^2 / C: a diagonal entry of
+   * the inverse of a positive definite matrix is at least the reciprocal of
+   * the matching entry of the matrix), so alpha >= alpha_min needs
+   * d_x^2 <= A tau with tau = 2 ln(o / alpha_min). tau is bounded from above
+   * with exact fp32 steps only: o = sigmoid(logit) <= min(1, e^logit), and
+   * -ln(alpha_min) <= (1 - e) ln 2 where alpha_min = m 2^e, m in [0.5, 1);
+   * the margin is the blend kernels' tile-test margin.
+   */
+  int e2 = 0;
+  (void)frexpf(p->alpha_min, &e2);
+  float lnb = (float)(1 - e2) * 0.6931472f;
+  float tau = 2.0f * (lnb + fminf(ologit, 0.0f));
+  float lim = tau * 1.001f + 1e-3f;
+  if (!(lim > 0.0f)) return 0;
+  float ex = fminf(r, sqrtf(lim * A));
+  float ey = fminf(r, sqrtf(lim * C));
+  /* tile rectangle of the box [u-ex, u+ex] x [v-ey, v+ey] */
+  float tx0 = floorf((u - ex) * 0.0625f);
+  float tx1 = floorf((u + ex) * 0.0625f);
+  float ty0 = floorf((v - ey) * 0.0625f);
+  float ty1 = floorf((v + ey) * 0.0625f);
   float ntx = (float)(tiles_x_of(c->width) - 1);
   float nty = (float)(tiles_y_of(c->height) - 1);
   if (tx0 < 0.0f) tx0 = 0.0f;
@@ -132,6 +152,8 @@ static int proj_bin_one(const orc_camera* c, const orc_params* p, const float* m
   *v_out = v;
   *z_out = tz;
   *r_out = r;
+  ext_out[0] = ex;
+  ext_out[1] = ey;
   rect[0] = (int32_t)tx0;
   rect[1] = (int32_t)ty0;
   rect[2] = (int32_t)tx1;
@@ -141,18 +163,20 @@ static int proj_bin_one(const orc_camera* c, const orc_params* p, const float* m
 
 void orc_project_bin_f32(const orc_camera* cam, const orc_params* prm, int64_t n,
                          const float* means, const float* log_scales, const float* quats,
-                         float* means2d, float* depth, float* radius, int32_t* rect,
-                         uint32_t* tiles_touched) {
+                         const float* opacity_logits, float* means2d, float* depth,
+                         float* radius, float* extent, int32_t* rect, uint32_t* tiles_touched) {
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < n; i++) {
-    float u = 0, v = 0, z = 0, r = 0;
+    float u = 0, v = 0, z = 0, r = 0, ex[2] = {0, 0};
     int32_t rc[4] = {0, 0, 0, 0};
-    int vis = proj_bin_one(cam, prm, means + 3 * i, log_scales + 3 * i, quats + 4 * i, &u, &v, &z,
-                           &r, rc);
+    int vis = proj_bin_one(cam, prm, means + 3 * i, log_scales + 3 * i, quats + 4 * i,
+                           opacity_logits[i], &u, &v, &z, &r, ex, rc);
     means2d[2 * i] = vis ? u : 0.0f;
     means2d[2 * i + 1] = vis ? v : 0.0f;
     depth[i] = vis ? z : 0.0f;
     radius[i] = vis ? r : 0.0f;
+    extent[2 * i] = vis ? ex[0] : 0.0f;
+    extent[2 * i + 1] = vis ? ex[1] : 0.0f;
     for (int k = 0; k < 4; k++) rect[4 * i + k] = vis ? rc[k] : 0;
     tiles_touched[i] = vis ? (uint32_t)((rc[2] - rc[0] + 1) * (rc[3] - rc[1] + 1)) : 0u;
   }

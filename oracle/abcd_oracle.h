@@ -56,12 +56,14 @@ typedef struct {
 /* ---- projection -------------------------------------------------------- */
 
 /* fp32 chain that decides visibility, the tile rectangle and the sort key.
- * rect[4*i..] = (tx0, ty0, tx1, ty1) inclusive; all outputs are zero for a
- * culled Gaussian. */
+ * radius[i] = support radius (radius_sigmas sqrt(lambda_max)); extent[2*i..]
+ * = half extents of the binning box (the support square cut per axis to the
+ * ellipse where alpha can reach alpha_min); rect[4*i..] = (tx0, ty0, tx1,
+ * ty1) inclusive; all outputs are zero for a culled Gaussian. */
 void orc_project_bin_f32(const orc_camera* cam, const orc_params* prm, int64_t n,
                          const float* means, const float* log_scales, const float* quats,
-                         float* means2d, float* depth, float* radius, int32_t* rect,
-                         uint32_t* tiles_touched);
+                         const float* opacity_logits, float* means2d, float* depth,
+                         float* radius, float* extent, int32_t* rect, uint32_t* tiles_touched);
 
 /* fp64 values of the same projection (means2d, conic (a,b,c), opacity, rgb);
  * Gaussians with tiles_touched == 0 get zeros. */

@@ -61,7 +61,7 @@ def lib():
     L = C.CDLL(path)
     cam_p, prm_p = C.POINTER(_Cam), C.POINTER(_Prm)
     L.orc_project_bin_f32.argtypes = [cam_p, prm_p, C.c_int64, _f32p, _f32p, _f32p, _f32p,
-                                      _f32p, _f32p, _i32p, _u32p]
+                                      _f32p, _f32p, _f32p, _f32p, _i32p, _u32p]
     L.orc_project_bin_f32.restype = None
     L.orc_project_values_f64.argtypes = [cam_p, prm_p, C.c_int64, _f32p, _f32p, _f32p, _f32p,
                                          _f32p, _u32p, _f64p, _f64p, _f64p, _f64p]
@@ -132,16 +132,19 @@ def tile_grid(width, height):
 
 # ---------------------------------------------------------------- projection
 
-def project_bin(cam, prm, means, log_scales, quats):
-    """fp32 chain: means2d, depth, radius, rect (tx0, ty0, tx1, ty1), tiles_touched."""
+def project_bin(cam, prm, means, log_scales, quats, opacity_logits=None):
+    """fp32 chain: means2d, depth, radius (support), extent (half extents of the
+    binning box), rect (tx0, ty0, tx1, ty1), tiles_touched. Without
+    opacity_logits the opacity is bounded by 1 alone (logits of 0)."""
     means, log_scales, quats = _c(means, np.float32), _c(log_scales, np.float32), _c(quats, np.float32)
     n = means.shape[0]
+    logits = np.zeros(n, np.float32) if opacity_logits is None else _c(opacity_logits, np.float32)
     out = dict(means2d=np.zeros((n, 2), np.float32), depth=np.zeros(n, np.float32),
-               radius=np.zeros(n, np.float32), rect=np.zeros((n, 4), np.int32),
-               tiles_touched=np.zeros(n, np.uint32))
+               radius=np.zeros(n, np.float32), extent=np.zeros((n, 2), np.float32),
+               rect=np.zeros((n, 4), np.int32), tiles_touched=np.zeros(n, np.uint32))
     lib().orc_project_bin_f32(C.byref(_cam(cam)), C.byref(_prm(prm)), n, means, log_scales, quats,
-                              out["means2d"], out["depth"], out["radius"], out["rect"],
-                              out["tiles_touched"])
+                              logits, out["means2d"], out["depth"], out["radius"], out["extent"],
+                              out["rect"], out["tiles_touched"])
     return out
 
 
@@ -293,7 +296,8 @@ def step(cam, prm, scene, F=None, B=None, dL_dout=None, pos32=True, rel_margin=0
     blend (the GPU kernels' precision for positions); pos32=False keeps every
     value in fp64 (smooth in the parameters, for finite differences).
     """
-    pb = project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"])
+    pb = project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"],
+                     scene["opacity_logits"])
     pv = project_values(cam, prm, scene["means"], scene["log_scales"], scene["quats"],
                         scene["opacity_logits"], scene["sh"], pb["tiles_touched"])
     m2d = pb["means2d"].astype(np.float64) if pos32 else pv["means2d"]

@@ -55,8 +55,9 @@ def version():
 # ------------------------------------------------------------------ project
 
 def project(cam, prm, means, log_scales, quats, opacity_logits, sh, out=None):
-    """EWA projection; returns dict(means2d, conic_opacity, depth, radius,
-    tiles_touched (int32 view of uint32), rgb)."""
+    """EWA projection; returns dict(means2d, conic_opacity, depth, extent
+    (n, 2: half extents of the binning box), tiles_touched (int32 view of
+    uint32), rgb)."""
     n = means.shape[0]
     nc = (prm.sh_degree + 1) ** 2
     f32 = torch.float32
@@ -68,13 +69,13 @@ def project(cam, prm, means, log_scales, quats, opacity_logits, sh, out=None):
     dev = means.device
     if out is None:
         out = dict(means2d=_empty((n, 2), f32, dev), conic_opacity=_empty((n, 4), f32, dev),
-                   depth=_empty((n,), f32, dev), radius=_empty((n,), f32, dev),
+                   depth=_empty((n,), f32, dev), extent=_empty((n, 2), f32, dev),
                    tiles_touched=_empty((n,), torch.int32, dev), rgb=_empty((n, 3), f32, dev))
     lib = _lib.load()
     check(lib.abcd_project(C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)), n,
                            _ptr(means), _ptr(log_scales), _ptr(quats), _ptr(opacity_logits),
                            _ptr(sh), _ptr(out["means2d"]), _ptr(out["conic_opacity"]),
-                           _ptr(out["depth"]), _ptr(out["radius"]), _ptr(out["tiles_touched"]),
+                           _ptr(out["depth"]), _ptr(out["extent"]), _ptr(out["tiles_touched"]),
                            _ptr(out["rgb"]), _stream()))
     return out
 
@@ -96,12 +97,12 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
     the buffers are grown to fit it; with sync=False the call never
     synchronises and `capacity`/`values` must already be large enough (an
     overflow leaves the outputs unwritten)."""
-    means2d, radius = proj["means2d"], proj["radius"]
+    means2d, extent = proj["means2d"], proj["extent"]
     depth, tiles = proj["depth"], proj["tiles_touched"]
     n = means2d.shape[0]
     dev = means2d.device
     _need(means2d, "means2d", torch.float32, (n, 2))
-    _need(radius, "radius", torch.float32, (n,))
+    _need(extent, "extent", torch.float32, (n, 2))
     _need(depth, "depth", torch.float32, (n,))
     _need(tiles, "tiles_touched", torch.int32, (n,))
     if tile_ranges is None:
@@ -119,7 +120,7 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
         keys = _empty((max(capacity, 1),), torch.int64, dev)
     lib = _lib.load()
     m = C.c_int64(0)
-    st = lib.abcd_bin_sort(width, height, n, _ptr(means2d), _ptr(radius), _ptr(depth), _ptr(tiles),
+    st = lib.abcd_bin_sort(width, height, n, _ptr(means2d), _ptr(extent), _ptr(depth), _ptr(tiles),
                            capacity, _ptr(workspace), workspace.numel(),
                            _ptr(keys) if want_keys else None, _ptr(values), _ptr(tile_ranges),
                            _ptr(tile_order), C.byref(m) if sync else None, _stream())
@@ -131,7 +132,7 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
         ws_bytes = bin_sort_workspace_size(n, width, height, capacity)
         if workspace.numel() < ws_bytes:
             workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-        st = lib.abcd_bin_sort(width, height, n, _ptr(means2d), _ptr(radius), _ptr(depth),
+        st = lib.abcd_bin_sort(width, height, n, _ptr(means2d), _ptr(extent), _ptr(depth),
                                _ptr(tiles), capacity, _ptr(workspace), workspace.numel(),
                                _ptr(keys) if want_keys else None, _ptr(values), _ptr(tile_ranges),
                                _ptr(tile_order), C.byref(m), _stream())
@@ -233,7 +234,7 @@ def render_bwd(cam, prm, params, proj, bins, fwd, dL_dout, F=None, B=None, works
         C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)), n,
         _ptr(params["means"]), _ptr(params["log_scales"]), _ptr(params["quats"]),
         _ptr(params["opacity_logits"]), _ptr(params["sh"]), _ptr(proj["means2d"]),
-        _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]), _ptr(proj["radius"]),
+        _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]), _ptr(proj["extent"]),
         _ptr(bins["tile_ranges"]), _ptr(bins["values"]), _ptr(F), _ptr(B), _ptr(fwd["final_T"]),
         _ptr(fwd["last"]), _ptr(dL_dout), _ptr(workspace), workspace.numel(), _ptr(grads["means"]),
         _ptr(grads["log_scales"]), _ptr(grads["quats"]), _ptr(grads["opacity_logits"]),

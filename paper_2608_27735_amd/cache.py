@@ -24,7 +24,7 @@ class CacheRefresher:
         self.proj = dict(means2d=torch.empty((n, 2), dtype=f32, device=dev),
                          conic_opacity=torch.empty((n, 4), dtype=f32, device=dev),
                          depth=torch.empty((n,), dtype=f32, device=dev),
-                         radius=torch.empty((n,), dtype=f32, device=dev),
+                         extent=torch.empty((n, 2), dtype=f32, device=dev),
                          tiles_touched=torch.empty((n,), dtype=torch.int32, device=dev),
                          rgb=torch.empty((n, 3), dtype=f32, device=dev))
         nt = api.n_tiles(width, height)

@@ -55,17 +55,17 @@ struct TimedLaunch {
 
 // ------------------------------------------------- shared device helpers
 
-// Tile rectangle of the support square [u - r, u + r] x [v - r, v + r]:
+// Tile rectangle of the screen box [u - rx, u + rx] x [v - ry, v + ry]:
 // floor of the corner divided by the tile side, clamped to the grid; part of
 // the fixed fp32 operation order (scaling by 1/16 is exact). Returns false if
 // the rectangle is empty.
-__device__ __forceinline__ bool tile_rect(float u, float v, float r, int ntx, int nty, int& x0,
-                                          int& y0, int& x1, int& y1) {
+__device__ __forceinline__ bool tile_rect(float u, float v, float rx, float ry, int ntx, int nty,
+                                          int& x0, int& y0, int& x1, int& y1) {
 #pragma clang fp contract(off)
-  float fx0 = floorf((u - r) * 0.0625f);
-  float fx1 = floorf((u + r) * 0.0625f);
-  float fy0 = floorf((v - r) * 0.0625f);
-  float fy1 = floorf((v + r) * 0.0625f);
+  float fx0 = floorf((u - rx) * 0.0625f);
+  float fx1 = floorf((u + rx) * 0.0625f);
+  float fy0 = floorf((v - ry) * 0.0625f);
+  float fy1 = floorf((v + ry) * 0.0625f);
   const float mx = (float)(ntx - 1), my = (float)(nty - 1);
   fx0 = fx0 < 0.0f ? 0.0f : fx0;
   fy0 = fy0 < 0.0f ? 0.0f : fy0;
@@ -84,21 +84,31 @@ __device__ __forceinline__ bool tile_rect(float u, float v, float r, int ntx, in
 // alpha = min(alpha_max, o 2^p2) is one v_exp_f32 away.
 constexpr float kLog2e = 1.4426950408889634f;
 
+// conic_opacity holds (l11, l21, l22, o): the conic [[a, b], [b, c]] as its
+// Cholesky factor L = [[l11, 0], [l21, l22]], and the opacity.
 struct Splat {
-  float u, v;       // mean
-  float qa, qb, qc; // -a log2(e) / 2, -b log2(e), -c log2(e) / 2
-  float o;          // opacity
+  float u, v;          // mean
+  float qa, qb, qc;    // s l11, s l21, s l22 with s^2 = log2(e) / 2
+  float o;             // opacity
 };
+
+constexpr float kHalfLog2eSqrt = 0.84932180028801904f;  // sqrt(log2(e) / 2)
 
 __device__ __forceinline__ Splat make_splat(float2 m, float4 co) {
   Splat s;
   s.u = m.x;
   s.v = m.y;
-  s.qa = -0.5f * kLog2e * co.x;
-  s.qb = -kLog2e * co.y;
-  s.qc = -0.5f * kLog2e * co.z;
+  s.qa = kHalfLog2eSqrt * co.x;
+  s.qb = kHalfLog2eSqrt * co.y;
+  s.qc = kHalfLog2eSqrt * co.z;
   s.o = co.w;
   return s;
+}
+
+// The conic (a, b, c) = L L^T of a factor (l11, l21, l22): for the tile test
+// and the chain rule to the mean.
+__device__ __forceinline__ float3 conic_of(float4 co) {
+  return make_float3(co.x * co.x, co.x * co.y, co.y * co.y + co.z * co.z);
 }
 
 // Alpha of a splat at pixel offset (dx, dy) = centre - mean. The forward and
@@ -114,7 +124,9 @@ struct AlphaEval {
 __device__ __forceinline__ AlphaEval eval_alpha(float dx, float dy, float qa, float qb, float qc,
                                                 float o, float alpha_min, float alpha_max) {
   AlphaEval r;
-  const float p2 = dx * (qa * dx + qb * dy) + qc * (dy * dy);
+  // -log2(e) q / 2 with q = d^T L L^T d: minus a sum of two squares
+  const float e1 = qa * dx + qb * dy, e2 = qc * dy;
+  const float p2 = -(e1 * e1 + e2 * e2);
   r.e = __builtin_amdgcn_exp2f(p2);
   const float raw = o * r.e;
   r.clamped = raw > alpha_max;
@@ -246,18 +258,18 @@ inline SplitLayout split_layout(void* ws, size_t bytes, int ch) {
 int32_t launch_project(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
                        const float* means, const float* log_scales, const float* quats,
                        const float* opacity_logits, const float* sh, float* means2d,
-                       float* conic_opacity, float* depth, float* radius, uint32_t* tiles_touched,
+                       float* conic_opacity, float* depth, float* extent, uint32_t* tiles_touched,
                        float* rgb, hipStream_t stream);
 int32_t launch_project_bwd(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
                            const float* means, const float* log_scales, const float* quats,
-                           const float* opacity_logits, const float* sh, const float* radius,
+                           const float* opacity_logits, const float* sh, const float* extent,
                            const float* g2d, float* d_means, float* d_log_scales, float* d_quats,
                            float* d_opacity_logits, float* d_sh, float* d_means2d,
                            int accumulate, hipStream_t stream);
 
 // binning.hip
 size_t bin_sort_workspace_bytes(int64_t n, int64_t capacity, int width, int height);
-int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, const float* radius,
+int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, const float* extent,
                         const float* depth, const uint32_t* tiles_touched, int64_t capacity,
                         void* workspace, uint64_t* keys_sorted, uint32_t* values_sorted,
                         uint32_t* tile_ranges, uint32_t* tile_order, hipStream_t stream);

@@ -142,22 +142,23 @@ const char* abcd_status_string(int32_t s) {
 int32_t abcd_project(const abcd_camera* cam, const abcd_raster_params* prm, int64_t n,
                      const float* means, const float* log_scales, const float* quats,
                      const float* opacity_logits, const float* sh, float* means2d,
-                     float* conic_opacity, float* depth, float* radius, uint32_t* tiles_touched,
+                     float* conic_opacity, float* depth, float* extent, uint32_t* tiles_touched,
                      float* rgb, hipStream_t stream) {
   TRY(check_camera(cam));
   TRY(check_params(prm));
   TRY(check_n(n));
   if (n > 0) {
     REQUIRE(means && log_scales && quats && opacity_logits && sh, "parameter array is NULL");
-    REQUIRE(means2d && conic_opacity && depth && radius && tiles_touched && rgb,
+    REQUIRE(means2d && conic_opacity && depth && extent && tiles_touched && rgb,
             "output array is NULL");
     REQUIRE((reinterpret_cast<uintptr_t>(conic_opacity) & 15) == 0 &&
                 (reinterpret_cast<uintptr_t>(quats) & 15) == 0 &&
-                (reinterpret_cast<uintptr_t>(means2d) & 7) == 0,
-            "quats and conic_opacity must be 16-byte and means2d 8-byte aligned");
+                (reinterpret_cast<uintptr_t>(means2d) & 7) == 0 &&
+                (reinterpret_cast<uintptr_t>(extent) & 7) == 0,
+            "quats and conic_opacity must be 16-byte, means2d and extent 8-byte aligned");
   }
   return launch_project(*cam, *prm, n, means, log_scales, quats, opacity_logits, sh, means2d,
-                        conic_opacity, depth, radius, tiles_touched, rgb, stream);
+                        conic_opacity, depth, extent, tiles_touched, rgb, stream);
 }
 
 int32_t abcd_bin_sort_workspace_size(int64_t n, int64_t capacity, int32_t width, int32_t height,
@@ -173,7 +174,7 @@ int32_t abcd_bin_sort_workspace_size(int64_t n, int64_t capacity, int32_t width,
 }
 
 int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const float* means2d,
-                      const float* radius, const float* depth, const uint32_t* tiles_touched,
+                      const float* extent, const float* depth, const uint32_t* tiles_touched,
                       int64_t capacity, void* workspace, size_t ws_bytes, uint64_t* keys_sorted,
                       uint32_t* values_sorted, uint32_t* tile_ranges, uint32_t* tile_order,
                       int64_t* n_isect, hipStream_t stream) {
@@ -188,11 +189,13 @@ int32_t abcd_bin_sort(int32_t width, int32_t height, int64_t n, const float* mea
   const size_t need = bin_sort_workspace_bytes(n, capacity, width, height);
   REQUIRE(ws_bytes >= need, "workspace of %zu bytes, %zu needed", ws_bytes, need);
   if (n > 0) {
-    REQUIRE(means2d && radius && depth && tiles_touched, "input array is NULL");
-    REQUIRE((reinterpret_cast<uintptr_t>(means2d) & 7) == 0, "means2d must be 8-byte aligned");
+    REQUIRE(means2d && extent && depth && tiles_touched, "input array is NULL");
+    REQUIRE((reinterpret_cast<uintptr_t>(means2d) & 7) == 0 &&
+                (reinterpret_cast<uintptr_t>(extent) & 7) == 0,
+            "means2d and extent must be 8-byte aligned");
   }
   REQUIRE(capacity == 0 || values_sorted != nullptr, "values_sorted is NULL with capacity > 0");
-  TRY(launch_bin_sort(width, height, n, means2d, radius, depth, tiles_touched, capacity, workspace,
+  TRY(launch_bin_sort(width, height, n, means2d, extent, depth, tiles_touched, capacity, workspace,
                       keys_sorted, values_sorted, tile_ranges, tile_order, stream));
   if (n_isect) {
     unsigned long long m = 0;
@@ -268,7 +271,7 @@ int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes) {
 int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, int64_t n,
                         const float* means, const float* log_scales, const float* quats,
                         const float* opacity_logits, const float* sh, const float* means2d,
-                        const float* conic_opacity, const float* rgb, const float* radius,
+                        const float* conic_opacity, const float* rgb, const float* extent,
                         const uint32_t* tile_ranges, const uint32_t* values_sorted,
                         const float* F, const float* B, const float* final_T, const uint32_t* last,
                         const float* dL_dout, void* workspace, size_t ws_bytes, float* d_means,
@@ -288,7 +291,7 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
   const size_t need = render_bwd_workspace_bytes(n);
   if (n > 0) {
     REQUIRE(means && log_scales && quats && opacity_logits && sh && means2d && conic_opacity &&
-                rgb && radius,
+                rgb && extent,
             "input array is NULL");
     REQUIRE(d_means && d_log_scales && d_quats && d_opacity_logits && d_sh, "gradient array is NULL");
     REQUIRE(workspace != nullptr && (reinterpret_cast<uintptr_t>(workspace) & 255) == 0,
@@ -306,7 +309,7 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
   TRY(launch_zero(g2d, 9 * n, stream));
   TRY(launch_render_bwd_pixels(*cam, *prm, n, tile_ranges, values_sorted, means2d, conic_opacity,
                                rgb, F, B, final_T, last, dL_dout, g2d, sl, stream));
-  return launch_project_bwd(*cam, *prm, n, means, log_scales, quats, opacity_logits, sh, radius,
+  return launch_project_bwd(*cam, *prm, n, means, log_scales, quats, opacity_logits, sh, extent,
                             g2d, d_means, d_log_scales, d_quats, d_opacity_logits, d_sh, d_means2d,
                             accumulate, stream);
 }

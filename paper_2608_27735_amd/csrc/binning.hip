@@ -139,7 +139,7 @@ __device__ __forceinline__ unsigned long long pack_rect(int x0, int y0, int x1, 
 
 __global__ __launch_bounds__(256) void depth_keys_kernel(
     int64_t n, const float* __restrict__ depth, const uint32_t* __restrict__ tiles,
-    const float* __restrict__ means2d, const float* __restrict__ radius, int ntx, int nty,
+    const float* __restrict__ means2d, const float* __restrict__ extent, int ntx, int nty,
     uint32_t* __restrict__ keys, uint32_t* __restrict__ vals, unsigned long long* __restrict__ rects,
     WsHeader* __restrict__ hdr) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -156,7 +156,8 @@ __global__ __launch_bounds__(256) void depth_keys_kernel(
   int x0 = 1, y0 = 0, x1 = 0, y1 = 0;
   if (vis) {
     const float2 m = reinterpret_cast<const float2*>(means2d)[i];
-    if (!tile_rect(m.x, m.y, radius[i], ntx, nty, x0, y0, x1, y1)) x0 = 1, y0 = 0, x1 = 0, y1 = 0;
+    const float2 ex = reinterpret_cast<const float2*>(extent)[i];
+    if (!tile_rect(m.x, m.y, ex.x, ex.y, ntx, nty, x0, y0, x1, y1)) x0 = 1, y0 = 0, x1 = 0, y1 = 0;
   }
   rects[i] = pack_rect(x0, y0, x1, y1);
 }
@@ -834,7 +835,7 @@ size_t bin_sort_workspace_bytes(int64_t n, int64_t capacity, int width, int heig
   return ws_layout(n, capacity, geo_of(width, height)).total;
 }
 
-int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, const float* radius,
+int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, const float* extent,
                         const float* depth, const uint32_t* tiles_touched, int64_t capacity,
                         void* workspace, uint64_t* keys_sorted, uint32_t* values_sorted,
                         uint32_t* tile_ranges, uint32_t* tile_order, hipStream_t stream) {
@@ -858,7 +859,7 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   const int64_t gb = (n + kBlock - 1) / kBlock;
   unsigned long long* rects = reinterpret_cast<unsigned long long*>(ws + L.rects);
   ABCD_LAUNCH("depth_keys", depth_keys_kernel, gb, kBlock, 0, stream, n, depth, tiles_touched,
-              means2d, radius, geo.ntx, geo.nty, keys[0], vals[0], rects, hdr);
+              means2d, extent, geo.ntx, geo.nty, keys[0], vals[0], rects, hdr);
   for (int pass = 0; pass < 4; ++pass) {
     const int src = pass & 1, dst = src ^ 1;
     ABCD_LAUNCH("radix_hist", radix_hist_kernel, L.rs_blocks, kBlock, 0, stream, keys[src], n,

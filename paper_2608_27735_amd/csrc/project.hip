@@ -122,6 +122,7 @@ struct Proj {
   float T[6];        // J Rcam: row 0 then row 1
   float A, B, C, det;
   float u, v, rad;
+  float ex, ey;      // half extents of the binning box
   int x0, y0, x1, y1;
 };
 
@@ -129,7 +130,8 @@ struct Proj {
 // left-to-right sums of separately rounded products; nothing is fused except
 // the two fmaf of Kahan's determinant.
 __device__ bool project_chain(const abcd_camera& c, const abcd_raster_params& p, int ntx, int nty,
-                              const float* mu, const float* ls, const float* q, Proj& o) {
+                              const float* mu, const float* ls, const float* q, float ologit,
+                              Proj& o) {
 #pragma clang fp contract(off)
   const float* R = c.R;
   o.tx = ((R[0] * mu[0] + R[1] * mu[1]) + R[2] * mu[2]) + c.t[0];
@@ -209,7 +211,22 @@ __device__ bool project_chain(const abcd_camera& c, const abcd_raster_params& p,
   const float lmax = mid + sqrtf(disc);
   o.rad = p.radius_sigmas * sqrtf(lmax);
   if (!isfinite(o.u) || !isfinite(o.v) || !isfinite(o.rad)) return false;
-  return tile_rect(o.u, o.v, o.rad, ntx, nty, o.x0, o.y0, o.x1, o.y1);
+  // The binning box: the support square cut, per axis, to the extent of the
+  // ellipse where alpha can reach alpha_min. A pixel offset d sees alpha =
+  // o exp(-q / 2) with q = d^T Sigma^-1 d >= d_x^2 / A (and d_y^2 / C), and
+  // alpha >= alpha_min needs q <= 2 ln(o / alpha_min). Bounded without
+  // transcendentals, so the bound is exact fp32 arithmetic: o <= min(1,
+  // e^logit), and -ln alpha_min <= (1 - e) ln 2 for alpha_min = m 2^e,
+  // m in [0.5, 1). The margin is that of the blend kernels' tile test.
+  int e2 = 0;
+  (void)frexpf(p.alpha_min, &e2);
+  const float lnb = (float)(1 - e2) * 0.6931472f;
+  const float tau = 2.0f * (lnb + fminf(ologit, 0.0f));
+  const float lim = tau * 1.001f + 1e-3f;
+  if (!(lim > 0.0f)) return false;  // alpha_min is out of reach everywhere
+  o.ex = fminf(o.rad, sqrtf(lim * o.A));
+  o.ey = fminf(o.rad, sqrtf(lim * o.C));
+  return tile_rect(o.u, o.v, o.ex, o.ey, ntx, nty, o.x0, o.y0, o.x1, o.y1);
 }
 
 // The geometry of one Gaussian in fp64: the 2D covariance, its inverse (the
@@ -370,7 +387,7 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(
     abcd_camera cam, abcd_raster_params prm, int64_t n, int ntx, int nty, const float* __restrict__ means,
     const float* __restrict__ log_scales, const float* __restrict__ quats,
     const float* __restrict__ opacity_logits, const float* __restrict__ sh, float* __restrict__ means2d,
-    float* __restrict__ conic_opacity, float* __restrict__ depth, float* __restrict__ radius,
+    float* __restrict__ conic_opacity, float* __restrict__ depth, float* __restrict__ extent,
     uint32_t* __restrict__ tiles_touched, float* __restrict__ rgb) {
   using Tl = ShTile<D>;
   __shared__ float s_sh[kProjThreads * Tl::kStride];
@@ -391,20 +408,26 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(
   if (threadIdx.x >= cnt) return;
   const float q[4] = {q4.x, q4.y, q4.z, q4.w};
   Proj pr;
-  const bool vis = project_chain(cam, prm, ntx, nty, mu, ls, q, pr);
+  const bool vis = project_chain(cam, prm, ntx, nty, mu, ls, q, ologit, pr);
   if (!vis) {
     reinterpret_cast<float2*>(means2d)[i] = make_float2(0.0f, 0.0f);
     reinterpret_cast<float4*>(conic_opacity)[i] = make_float4(0, 0, 0, 0);
     depth[i] = 0.0f;
-    radius[i] = 0.0f;
+    reinterpret_cast<float2*>(extent)[i] = make_float2(0.0f, 0.0f);
     tiles_touched[i] = 0u;
     rgb[3 * i] = rgb[3 * i + 1] = rgb[3 * i + 2] = 0.0f;
     return;
   }
   Geo64 g64;
   geom_f64(cam, prm, mu, ls, q, g64);
+  // the conic [[a, b], [b, c]] = inverse 2D covariance, stored as its
+  // Cholesky factor [[l11, 0], [l21, l22]]: q = (l11 dx + l21 dy)^2 +
+  // (l22 dy)^2 is a sum of squares, so rounding the factor to fp32 perturbs q
+  // far less than rounding (a, b, c) does for a badly conditioned conic
+  // (det of the conic = 1 / det, so l22 needs no subtraction)
   const double inv = 1.0 / g64.det;
-  const float ca = (float)(g64.C * inv), cb = (float)(-g64.B * inv), cc = (float)(g64.A * inv);
+  const double l11 = sqrt(g64.C * inv);
+  const float ca = (float)l11, cb = (float)(-g64.B * inv / l11), cc = (float)(sqrt(inv) / l11);
   const float o = 1.0f / (1.0f + __expf(-ologit));
   float dx = mu[0] - cam.campos[0], dy = mu[1] - cam.campos[1], dz = mu[2] - cam.campos[2];
   const float dn = rsqrtf(dx * dx + dy * dy + dz * dz);
@@ -422,7 +445,7 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(
   reinterpret_cast<float2*>(means2d)[i] = make_float2(pr.u, pr.v);
   reinterpret_cast<float4*>(conic_opacity)[i] = make_float4(ca, cb, cc, o);
   depth[i] = pr.tz;
-  radius[i] = pr.rad;
+  reinterpret_cast<float2*>(extent)[i] = make_float2(pr.ex, pr.ey);
   tiles_touched[i] = (uint32_t)((pr.x1 - pr.x0 + 1) * (pr.y1 - pr.y0 + 1));
   rgb[3 * i] = fmaxf(col[0], 0.0f);
   rgb[3 * i + 1] = fmaxf(col[1], 0.0f);
@@ -437,7 +460,7 @@ __global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
     abcd_camera cam, abcd_raster_params prm, int64_t n, int ntx, int nty,
     const float* __restrict__ means, const float* __restrict__ log_scales,
     const float* __restrict__ quats, const float* __restrict__ opacity_logits,
-    const float* __restrict__ sh, const float* __restrict__ radius, const float* __restrict__ g2d,
+    const float* __restrict__ sh, const float* __restrict__ extent, const float* __restrict__ g2d,
     float* __restrict__ d_means, float* __restrict__ d_log_scales, float* __restrict__ d_quats,
     float* __restrict__ d_opacity_logits, float* __restrict__ d_sh, float* __restrict__ d_means2d,
     int accumulate) {
@@ -453,7 +476,7 @@ __global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
 #pragma unroll
   for (int k = 0; k < 9; ++k) G[k] = 0.0f;
   if (live) {
-    rad = radius[i];
+    rad = extent[2 * i];
     mu[0] = means[3 * i]; mu[1] = means[3 * i + 1]; mu[2] = means[3 * i + 2];
     ls[0] = log_scales[3 * i]; ls[1] = log_scales[3 * i + 1]; ls[2] = log_scales[3 * i + 2];
     q4 = *reinterpret_cast<const float4*>(quats + 4 * i);
@@ -470,7 +493,7 @@ __global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
   bool vis = live && rad > 0.0f;
   if (vis) {
     const float q[4] = {q4.x, q4.y, q4.z, q4.w};
-    vis = project_chain(cam, prm, ntx, nty, mu, ls, q, pr);
+    vis = project_chain(cam, prm, ntx, nty, mu, ls, q, ologit, pr);
   }
   if (vis) {
     gu = G[0];
@@ -639,7 +662,7 @@ __global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
 int32_t launch_project(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
                        const float* means, const float* log_scales, const float* quats,
                        const float* opacity_logits, const float* sh, float* means2d,
-                       float* conic_opacity, float* depth, float* radius, uint32_t* tiles_touched,
+                       float* conic_opacity, float* depth, float* extent, uint32_t* tiles_touched,
                        float* rgb, hipStream_t stream) {
   if (n == 0) return ABCD_OK;
   const int64_t blocks = (n + kProjThreads - 1) / kProjThreads;
@@ -647,7 +670,7 @@ int32_t launch_project(const abcd_camera& cam, const abcd_raster_params& prm, in
 #define ABCD_PROJ(Dg)                                                                          \
   ABCD_LAUNCH("project", project_kernel<Dg>, blocks, kProjThreads, 0, stream, cam, prm, n, ntx, \
               nty, means, log_scales, quats, opacity_logits, sh, means2d, conic_opacity, depth,  \
-              radius, tiles_touched, rgb)
+              extent, tiles_touched, rgb)
   switch (prm.sh_degree) {
     case 0: ABCD_PROJ(0); break;
     case 1: ABCD_PROJ(1); break;
@@ -661,7 +684,7 @@ int32_t launch_project(const abcd_camera& cam, const abcd_raster_params& prm, in
 
 int32_t launch_project_bwd(const abcd_camera& cam, const abcd_raster_params& prm, int64_t n,
                            const float* means, const float* log_scales, const float* quats,
-                           const float* opacity_logits, const float* sh, const float* radius,
+                           const float* opacity_logits, const float* sh, const float* extent,
                            const float* g2d, float* d_means, float* d_log_scales, float* d_quats,
                            float* d_opacity_logits, float* d_sh, float* d_means2d,
                            int accumulate, hipStream_t stream) {
@@ -670,7 +693,7 @@ int32_t launch_project_bwd(const abcd_camera& cam, const abcd_raster_params& prm
   const int ntx = tiles_x(cam.width), nty = tiles_y(cam.height);
 #define ABCD_PROJ_BWD(Dg)                                                                    \
   ABCD_LAUNCH("project_bwd", project_bwd_kernel<Dg>, blocks, kProjThreads, 0, stream, cam, prm, \
-              n, ntx, nty, means, log_scales, quats, opacity_logits, sh, radius, g2d, d_means,  \
+              n, ntx, nty, means, log_scales, quats, opacity_logits, sh, extent, g2d, d_means,  \
               d_log_scales, d_quats, d_opacity_logits, d_sh, d_means2d, accumulate)
   switch (prm.sh_degree) {
     case 0: ABCD_PROJ_BWD(0); break;

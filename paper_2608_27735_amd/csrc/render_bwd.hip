@@ -180,16 +180,16 @@ __device__ __forceinline__ void bwd_item(
   while (bend > bstop) {
     const uint32_t bbeg = bend - min(256u, bend - bstop);
     __syncthreads();
-    const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, rec.co.x, rec.co.y, rec.co.z,
-                                                     rec.co.w, k.alpha_min, box.x0, box.x1,
-                                                     box.y0, box.y1);
+    const float3 cn = conic_of(rec.co);
+    const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, cn.x, cn.y, cn.z, rec.co.w,
+                                                     k.alpha_min, box.x0, box.x1, box.y0, box.y1);
     int pos;
     const int cnt = compact(keep, s_wcnt, pos);
     if (keep) {
       const Splat sp = make_splat(rec.m, rec.co);
       s_ga[pos] = make_float4(sp.u, sp.v, sp.qa, sp.qb);
       s_gb[pos] = make_float4(sp.qc, sp.o, rec.r, rec.g);
-      s_gc[pos] = make_float4(rec.co.x, rec.co.y, rec.co.z, rec.b);
+      s_gc[pos] = make_float4(cn.x, cn.y, cn.z, rec.b);
       s_pos[pos] = (int)(bend - 1 - tid - start);
       s_g[pos] = rec.gid;
 #pragma unroll

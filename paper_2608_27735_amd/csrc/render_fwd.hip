@@ -97,9 +97,9 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
         staged = 0;
       }
     }
-    const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, rec.co.x, rec.co.y, rec.co.z,
-                                                     rec.co.w, k.alpha_min, box.x0, box.x1,
-                                                     box.y0, box.y1);
+    const float3 cn = conic_of(rec.co);
+    const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, cn.x, cn.y, cn.z, rec.co.w,
+                                                     k.alpha_min, box.x0, box.x1, box.y0, box.y1);
     int pos;
     const int cnt = compact(keep, s_wcnt, pos);
     staged += (uint32_t)cnt;

@@ -15,7 +15,7 @@ from . import api
 
 
 class ActiveBlockStep:
-    def __init__(self, cam, prm, params, capacity=None, headroom=1.25, bg=None, chunk=1024):
+    def __init__(self, cam, prm, params, capacity=None, headroom=1.25, bg=None, chunk=512):
         self.cam, self.prm, self.params = cam, prm, params
         self.bg = bg
         n = params["means"].shape[0]
@@ -25,7 +25,7 @@ class ActiveBlockStep:
         self.proj = dict(means2d=torch.empty((n, 2), dtype=f32, device=dev),
                          conic_opacity=torch.empty((n, 4), dtype=f32, device=dev),
                          depth=torch.empty((n,), dtype=f32, device=dev),
-                         radius=torch.empty((n,), dtype=f32, device=dev),
+                         extent=torch.empty((n, 2), dtype=f32, device=dev),
                          tiles_touched=torch.empty((n,), dtype=torch.int32, device=dev),
                          rgb=torch.empty((n, 3), dtype=f32, device=dev))
         self.fwd = dict(out=torch.empty((H, W, 4), dtype=f32, device=dev),

@@ -75,7 +75,8 @@ def full(request):
     Fd, Bd = torch.from_numpy(F).to(dev), torch.from_numpy(B).to(dev)
     st.forward(Fd, Bd)
     torch.cuda.synchronize()
-    pb = O.project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"])
+    pb = O.project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"],
+                       scene["opacity_logits"])
     yield dict(api=api, st=st, cam=cam, prm=prm, scene=scene, F=F, B=B, Fd=Fd, Bd=Bd, r=r,
                pb=pb, name=request.param, knife=knife, knife_frac=knife_frac)
     del st, params
@@ -121,7 +122,7 @@ def test_fullsize_projection_and_binning(full):
     P = {k: v.cpu().numpy() for k, v in st.proj.items()}
     assert np.array_equal(P["means2d"].view(np.uint32), pb["means2d"].view(np.uint32))
     assert np.array_equal(P["depth"].view(np.uint32), pb["depth"].view(np.uint32))
-    assert np.array_equal(P["radius"].view(np.uint32), pb["radius"].view(np.uint32))
+    assert np.array_equal(P["extent"].view(np.uint32), pb["extent"].view(np.uint32))
     assert np.array_equal(P["tiles_touched"].view(np.uint32), pb["tiles_touched"])
     # M and every tile's list length from the oracle's rectangles
     ntx, nty = _tiles(cam)

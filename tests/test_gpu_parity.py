@@ -93,28 +93,49 @@ def test_project_bitexact_binning_fields_and_close_values(api, case):
     say("project", name, scene["means"].shape)
     p = gpu_project(api, cam, prm, scene)
     torch.cuda.synchronize()
-    ob = O.project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"])
+    ob = O.project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"],
+                       scene["opacity_logits"])
     ov = O.project_values(cam, prm, **scene, tiles_touched=ob["tiles_touched"])
     assert np.array_equal(np32(p["tiles_touched"]).view(np.uint32), ob["tiles_touched"])
     assert np.array_equal(np32(p["means2d"]).view(np.uint32), ob["means2d"].view(np.uint32))
     assert np.array_equal(np32(p["depth"]).view(np.uint32), ob["depth"].view(np.uint32))
-    assert np.array_equal(np32(p["radius"]).view(np.uint32), ob["radius"].view(np.uint32))
+    assert np.array_equal(np32(p["extent"]).view(np.uint32), ob["extent"].view(np.uint32))
     vis = ob["tiles_touched"] > 0
     assert vis.sum() > 0
     co = np32(p["conic_opacity"])
-    # conic entries: relative to the conic's scale
-    scale = np.abs(ov["conic"]).max(axis=1, keepdims=True) + 1e-30
-    assert np.max(np.abs(co[vis, :3] - ov["conic"][vis]) / scale[vis]) < 1e-4
+    # the conic as its Cholesky factor (l11, l21, l22), relative to its scale
+    ref = _factor_of(ov["conic"])
+    scale = np.abs(ref).max(axis=1, keepdims=True) + 1e-30
+    assert np.max(np.abs(co[vis, :3] - ref[vis]) / scale[vis]) < 1e-5
     assert np.max(np.abs(co[:, 3] - ov["opacity"])) < 1e-6
     assert np.max(np.abs(np32(p["rgb"]) - ov["rgb"])) < 1e-5
 
 
+def _factor_of(conic):
+    """Cholesky factor (l11, l21, l22) of conics (a, b, c): [[a, b], [b, c]] = L L^T
+    with L = [[l11, 0], [l21, l22]] (zeros for a zero conic)."""
+    a, b, c = conic[:, 0], conic[:, 1], conic[:, 2]
+    l11 = np.sqrt(np.maximum(a, 0.0))
+    safe = np.where(l11 > 0, l11, 1.0)
+    l21 = np.where(l11 > 0, b / safe, 0.0)
+    l22 = np.where(l11 > 0, np.sqrt(np.maximum(a * c - b * b, 0.0)) / safe, 0.0)
+    return np.stack([l11, l21, l22], 1)
+
+
+def _conic_of(co):
+    """fp64 conic (a, b, c) = L L^T of fp32 factors stored as conic_opacity[:, :3]."""
+    l = co[:, :3].astype(np.float64)
+    return np.stack([l[:, 0] ** 2, l[:, 0] * l[:, 1], l[:, 1] ** 2 + l[:, 2] ** 2], 1)
+
+
 def _oracle_inputs_f32(cam, prm, scene):
-    """Oracle projection rounded to fp32: the stage inputs both sides consume."""
-    ob = O.project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"])
+    """Oracle projection rounded to fp32 (the conic as its Cholesky factor, as
+    the GPU stores it): the stage inputs both sides consume."""
+    ob = O.project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"],
+                       scene["opacity_logits"])
     ov = O.project_values(cam, prm, **scene, tiles_touched=ob["tiles_touched"])
-    co = np.concatenate([ov["conic"], ov["opacity"][:, None]], 1).astype(np.float32)
-    proj = dict(means2d=ob["means2d"], conic_opacity=co, depth=ob["depth"], radius=ob["radius"],
+    co = np.concatenate([_factor_of(ov["conic"]), ov["opacity"][:, None]], 1).astype(np.float32)
+    proj = dict(means2d=ob["means2d"], conic_opacity=co, depth=ob["depth"], extent=ob["extent"],
                 tiles_touched=ob["tiles_touched"].view(np.int32), rgb=ov["rgb"].astype(np.float32))
     return ob, proj
 
@@ -177,7 +198,7 @@ def test_render_fwd_stage(api, case, with_fb):
     if with_fb:
         F, B = S.background_pair(S.rng(31), cam.height, cam.width)
     ref = O.render_fwd(cam, prm, ranges, values, proj["means2d"].astype(np.float64),
-                       proj["conic_opacity"][:, :3].astype(np.float64),
+                       _conic_of(proj["conic_opacity"]),
                        proj["conic_opacity"][:, 3].astype(np.float64),
                        proj["rgb"].astype(np.float64), F, B, rel_margin=KNIFE)
     pd = to_dev(proj)
@@ -216,7 +237,7 @@ def test_render_cache_refresh(api, case):
     ob, proj = _oracle_inputs_f32(cam, prm, scene)
     _, values, ranges = O.bin(cam.width, cam.height, ob["depth"], ob["rect"], ob["tiles_touched"])
     ref = O.render_fwd(cam, prm, ranges, values, proj["means2d"].astype(np.float64),
-                       proj["conic_opacity"][:, :3].astype(np.float64),
+                       _conic_of(proj["conic_opacity"]),
                        proj["conic_opacity"][:, 3].astype(np.float64),
                        proj["rgb"].astype(np.float64), None, None, rel_margin=KNIFE)
     pd = to_dev(proj)
@@ -377,7 +398,7 @@ def test_render_bwd_stage_and_accumulate(api):
     G = S.upstream_grad(r, cam.height, cam.width)
     ob, proj = _oracle_inputs_f32(cam, prm, scene)
     _, values, ranges = O.bin(cam.width, cam.height, ob["depth"], ob["rect"], ob["tiles_touched"])
-    args = (proj["means2d"].astype(np.float64), proj["conic_opacity"][:, :3].astype(np.float64),
+    args = (proj["means2d"].astype(np.float64), _conic_of(proj["conic_opacity"]),
             proj["conic_opacity"][:, 3].astype(np.float64), proj["rgb"].astype(np.float64))
     ref = O.render_fwd(cam, prm, ranges, values, *args, F, B, rel_margin=KNIFE)
     G = G * (~ref["knife"])[..., None]
@@ -513,7 +534,7 @@ def _raw_bin(api, cam, p, capacity, values, ranges, order):
                      dtype=torch.uint8, device=dev())
     m = C.c_int64(0)
     st = _lib.load().abcd_bin_sort(cam.width, cam.height, n, p["means2d"].data_ptr(),
-                                   p["radius"].data_ptr(), p["depth"].data_ptr(),
+                                   p["extent"].data_ptr(), p["depth"].data_ptr(),
                                    p["tiles_touched"].data_ptr(), capacity, ws.data_ptr(),
                                    ws.numel(), None, values.data_ptr(), ranges.data_ptr(),
                                    order.data_ptr(), C.byref(m),

@@ -229,20 +229,24 @@ def test_culling_cases():
         assert not np.any(pb[k][:5])
 
 
-def test_tile_rectangle_is_the_overlap_of_the_support_square():
-    """tile (tx, ty) is in the rectangle iff [u-r, u+r] meets [16 tx, 16 tx + 16)
-    and likewise in y; the rectangle area is tiles_touched."""
+def test_tile_rectangle_is_the_overlap_of_the_binning_box():
+    """tile (tx, ty) is in the rectangle iff [u-ex, u+ex] meets [16 tx, 16 tx + 16)
+    and likewise in y with ey; the rectangle area is tiles_touched; the box
+    lies inside the support square."""
     r = S.rng(7)
     cam = look_at((0.0, -4.0, 1.0), (0, 0, 0), 200, 120)
     prm = RasterParams()
     sc = S.gaussians(r, r.uniform(-1.5, 1.5, (400, 3)), 0, math.log(0.08), 0.6)
-    pb = O.project_bin(cam, prm, sc["means"], sc["log_scales"], sc["quats"])
+    sc["opacity_logits"][:100] = -4.0  # faint: alpha_min is reached well inside 3 sigma
+    pb = O.project_bin(cam, prm, sc["means"], sc["log_scales"], sc["quats"], sc["opacity_logits"])
     ntx, nty = O.tile_grid(cam.width, cam.height)
+    assert np.all(pb["extent"] <= pb["radius"][:, None])
+    assert np.any(pb["extent"][:, 0] < pb["radius"])  # the cut does bind
     for i in np.nonzero(pb["tiles_touched"])[0]:
         u, v = pb["means2d"][i].astype(np.float64)
-        rad = float(pb["radius"][i])
-        lo = np.float32(np.float32(u) - np.float32(rad)), np.float32(np.float32(v) - np.float32(rad))
-        hi = np.float32(np.float32(u) + np.float32(rad)), np.float32(np.float32(v) + np.float32(rad))
+        ex, ey = (float(e) for e in pb["extent"][i])
+        lo = np.float32(np.float32(u) - np.float32(ex)), np.float32(np.float32(v) - np.float32(ey))
+        hi = np.float32(np.float32(u) + np.float32(ex)), np.float32(np.float32(v) + np.float32(ey))
         x0, y0, x1, y1 = pb["rect"][i]
         for tx in range(ntx):
             inx = float(lo[0]) < 16 * (tx + 1) and float(hi[0]) >= 16 * tx
@@ -251,6 +255,43 @@ def test_tile_rectangle_is_the_overlap_of_the_support_square():
             iny = float(lo[1]) < 16 * (ty + 1) and float(hi[1]) >= 16 * ty
             assert iny == (y0 <= ty <= y1), (i, ty)
         assert pb["tiles_touched"][i] == (x1 - x0 + 1) * (y1 - y0 + 1)
+
+
+def test_binning_box_drops_no_pixel_that_could_blend():
+    """Every pixel centre of the support square outside the binning box gets
+    alpha < alpha_min from the fp64 conic and opacity (so the cut changes no
+    image), and for an isotropic opaque Gaussian the box is the square."""
+    r = S.rng(17)
+    cam = look_at((0.0, -4.0, 1.0), (0, 0, 0), 200, 120)
+    prm = RasterParams()
+    sc = S.gaussians(r, r.uniform(-1.0, 1.0, (300, 3)), 0, math.log(0.06), 0.8)
+    sc["opacity_logits"] = r.normal(-1.0, 2.5, 300).astype(np.float32)
+    pb = O.project_bin(cam, prm, sc["means"], sc["log_scales"], sc["quats"], sc["opacity_logits"])
+    pv = O.project_values(cam, prm, sc["means"], sc["log_scales"], sc["quats"],
+                          sc["opacity_logits"], sc["sh"], pb["tiles_touched"])
+    checked = 0
+    for i in np.nonzero(pb["tiles_touched"])[0]:
+        u, v = pv["means2d"][i]
+        a, b, c = pv["conic"][i]
+        o = pv["opacity"][i]
+        rad = float(pb["radius"][i])
+        ex, ey = (float(e) for e in pb["extent"][i])
+        xs = np.arange(math.floor(u - rad), math.ceil(u + rad) + 1) + 0.5
+        ys = np.arange(math.floor(v - rad), math.ceil(v + rad) + 1) + 0.5
+        X, Y = np.meshgrid(xs - u, ys - v)
+        out = (np.abs(X) > ex + 1e-3) | (np.abs(Y) > ey + 1e-3)
+        inside_sq = (np.abs(X) <= rad) & (np.abs(Y) <= rad)
+        q = a * X * X + 2 * b * X * Y + c * Y * Y
+        alpha = np.minimum(o * np.exp(-0.5 * q), prm.alpha_max)
+        sel = out & inside_sq
+        checked += int(sel.sum())
+        assert np.all(alpha[sel] < prm.alpha_min), i
+    assert checked > 1000
+    # isotropic and opaque: the alpha_min ellipse reaches past 3 sigma, no cut
+    iso = _single([[0, 0, 3.0]], [[math.log(0.1)] * 3], [[1, 0, 0, 0]])
+    pb1 = O.project_bin(axis_camera(), prm, iso["means"], iso["log_scales"], iso["quats"],
+                        np.array([4.0], np.float32))
+    assert pb1["extent"][0, 0] == pb1["radius"][0] and pb1["extent"][0, 1] == pb1["radius"][0]
 
 
 # ------------------------------------------------------------------ binning
