@@ -7,8 +7,10 @@
 // (longest-processing-time order) lets the light tiles fill in around them.
 //
 // The work estimate is the tile's list length for the forward (known after
-// binning) and the tile's largest per-pixel walk length for the backward
-// (known after the forward). The order is a stable bucket sort by the
+// binning) and, for the backward (known after the forward), the most entries
+// the forward staged in one chunk of the tile's walk when the tile may be
+// split, else the tile's largest per-pixel walk length; a tile's work items
+// (its chunks) follow one another. The order is a stable bucket sort by the
 // estimate's quarter octave (leading one and the two bits after it), so tiles
 // of one bucket keep their raster order and neighbouring tiles stay close in
 // launch order.
