@@ -225,6 +225,51 @@ def test_render_fwd_stage(api, case, with_fb):
     assert nb2.item() == nb.item()
 
 
+def _square_rects(ob, cam):
+    """Tile rectangles of the plain support squares [u +- r] x [v +- r] (no
+    cut to the alpha_min ellipse), in the fp32 steps of the binning chain."""
+    f = np.float32
+    u, v = ob["means2d"][:, 0], ob["means2d"][:, 1]
+    r = ob["radius"]
+    ntx, nty = O.tile_grid(cam.width, cam.height)
+    x0 = np.maximum(np.floor((u - r) * f(0.0625)), f(0))
+    x1 = np.minimum(np.floor((u + r) * f(0.0625)), f(ntx - 1))
+    y0 = np.maximum(np.floor((v - r) * f(0.0625)), f(0))
+    y1 = np.minimum(np.floor((v + r) * f(0.0625)), f(nty - 1))
+    vis = (ob["tiles_touched"] > 0) & (x0 <= x1) & (y0 <= y1)
+    rect = np.stack([x0, y0, x1, y1], 1).astype(np.int32)
+    rect[~vis] = 0
+    tiles = np.where(vis, (rect[:, 2] - rect[:, 0] + 1) * (rect[:, 3] - rect[:, 1] + 1), 0)
+    return rect, tiles.astype(np.uint32)
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_binning_box_changes_no_image(api, case):
+    """The GPU forward on its cut lists against the oracle on the uncut 3-sigma
+    squares: the (tile, Gaussian) pairs the cut drops blend nothing, on the
+    GPU's own fp32 alpha as well (the cut keeps the tile test's margin)."""
+    name, cam, prm, scene = case
+    say("binning box vs squares", name)
+    ob, proj = _oracle_inputs_f32(cam, prm, scene)
+    rect, tiles = _square_rects(ob, cam)
+    assert tiles.astype(np.int64).sum() >= ob["tiles_touched"].astype(np.int64).sum()
+    _, values, ranges = O.bin(cam.width, cam.height, ob["depth"], rect, tiles)
+    ref = O.render_fwd(cam, prm, ranges, values, proj["means2d"].astype(np.float64),
+                       _conic_of(proj["conic_opacity"]),
+                       proj["conic_opacity"][:, 3].astype(np.float64),
+                       proj["rgb"].astype(np.float64), None, None, rel_margin=KNIFE)
+    pd = to_dev(proj)
+    bins = api.bin_sort(cam.width, cam.height, pd)
+    nb = torch.zeros(1, dtype=torch.int64, device=dev())
+    fw = api.render_fwd(cam, prm, bins, pd, n_blends=nb)
+    torch.cuda.synchronize()
+    err, nk = _fwd_compare(np32(fw["out"]), ref, cam.height, cam.width)
+    print(f"  {int(tiles.astype(np.int64).sum())} square pairs, {bins['n_isect']} binned; "
+          f"max err {err:.2e}, knife-edge pixels {nk}")
+    assert err <= FWD_TOL
+    assert abs(int(nb.item()) - ref["n_blends"]) <= nk * 4
+
+
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_render_cache_refresh(api, case):
     """The cached render of a partition: the forward with F = B = transparent
