@@ -100,11 +100,32 @@ def _sampled_tiles(full):
     return np.unique(np.concatenate([heavy, rnd]))
 
 
-def _oracle_subset(full, tiles):
+def _square_rect(pb, cam):
+    """Tile rectangles and counts of the plain 3-sigma support squares (no cut
+    to the alpha_min ellipse), in the fp32 steps of the binning chain."""
+    f = np.float32
+    u, v, r = pb["means2d"][:, 0], pb["means2d"][:, 1], pb["radius"]
+    ntx, nty = _tiles(cam)
+    x0 = np.maximum(np.floor((u - r) * f(0.0625)), f(0))
+    x1 = np.minimum(np.floor((u + r) * f(0.0625)), f(ntx - 1))
+    y0 = np.maximum(np.floor((v - r) * f(0.0625)), f(0))
+    y1 = np.minimum(np.floor((v + r) * f(0.0625)), f(nty - 1))
+    vis = (pb["tiles_touched"] > 0) & (x0 <= x1) & (y0 <= y1)
+    rect = np.stack([x0, y0, x1, y1], 1).astype(np.int32)
+    rect[~vis] = np.array([1, 0, 0, 0], np.int32)
+    tiles = np.where(vis, (rect[:, 2] - rect[:, 0] + 1) * (rect[:, 3] - rect[:, 1] + 1), 0)
+    return rect, tiles.astype(np.uint32)
+
+
+def _oracle_subset(full, tiles, square=False):
     """Oracle projection of all Gaussians; oracle lists of the sampled tiles
-    from the subset of Gaussians whose rectangle meets one of them."""
+    from the subset of Gaussians whose rectangle meets one of them (square:
+    the uncut 3-sigma squares instead of the binning boxes)."""
     cam, pb = full["cam"], full["pb"]
     ntx, _ = _tiles(cam)
+    if square:
+        rect_sq, tiles_sq = _square_rect(pb, cam)
+        pb = dict(pb, rect=rect_sq, tiles_touched=tiles_sq)
     rect = pb["rect"].astype(np.int64)  # tx0, ty0, tx1, ty1 (empty if tx1 < tx0)
     tx, ty = tiles % ntx, tiles // ntx
     meets = np.zeros(len(rect), bool)
@@ -184,6 +205,32 @@ def test_fullsize_forward_on_sampled_tiles(full):
         assert err[kn].max(initial=0.0) <= 0.02
         worst = max(worst, err[~kn].max(initial=0.0))
         assert np.array_equal(last[ys, xs][~kn], ref["last"][ys, xs][~kn]), t
+        knives += int(kn.sum())
+        npx += kn.size
+    print(f"  {len(tiles)} tiles, max err {worst:.2e}, knife-edge pixels {knives} of {npx}")
+    assert worst <= FWD_TOL
+    assert knives <= max(8, full["knife_frac"] * npx)
+
+
+def test_fullsize_binning_box_changes_no_image(full):
+    """The GPU's image on its cut lists against the oracle on the uncut 3-sigma
+    squares, on the sampled tiles: the dropped pairs blend nothing."""
+    st, cam, prm = full["st"], full["cam"], full["prm"]
+    say("binning box vs squares, sampled tiles", full["name"])
+    tiles = _sampled_tiles(full)
+    pb, idx, vals, ranges = _oracle_subset(full, tiles, square=True)
+    m2d, pv = _subset_values(full, pb, idx)
+    ref = O.render_fwd(cam, prm, _only(ranges, tiles), vals, m2d, pv["conic"], pv["opacity"],
+                       pv["rgb"], full["F"], full["B"], rel_margin=full["knife"])
+    out = st.fwd["out"].cpu().numpy()
+    ntx, _ = _tiles(cam)
+    worst, knives, npx = 0.0, 0, 0
+    for t in tiles:
+        y0, x0 = (t // ntx) * 16, (t % ntx) * 16
+        ys, xs = np.mgrid[y0:min(y0 + 16, cam.height), x0:min(x0 + 16, cam.width)]
+        kn = ref["knife"][ys, xs]
+        err = np.abs(out[ys, xs] - ref["out"][ys, xs]).max(axis=-1)
+        worst = max(worst, err[~kn].max(initial=0.0))
         knives += int(kn.sum())
         npx += kn.size
     print(f"  {len(tiles)} tiles, max err {worst:.2e}, knife-edge pixels {knives} of {npx}")
