@@ -518,6 +518,22 @@ def test_composite_cache(api, k, n_front, hw, acc):
     assert np.abs(np32(Bg) - Bo).max() <= FWD_TOL
 
 
+def test_composite_cache_worked_by_hand(api, over_by_hand):
+    """The collapse kernel on the hand-worked cases (dyadic values, exact in
+    fp32): every split into F and B gives F over B == the hand result."""
+    for name, lay, res in over_by_hand:
+        k = len(lay)
+        say("composite by hand", name, k)
+        imgs = S.half_bits(np.broadcast_to(lay.reshape(k, 1, 1, 4), (k, 3, 5, 4)).copy())
+        img_d = torch.from_numpy(imgs.view(np.int16)).to(dev())
+        for n in range(k + 1):
+            Fg, Bg = api.composite_cache(img_d, list(range(k)), n)
+            torch.cuda.synchronize()
+            F, B = np32(Fg).astype(np.float64), np32(Bg).astype(np.float64)
+            got = F + (1.0 - F[..., 3:4]) * B
+            assert np.array_equal(got, np.broadcast_to(res, got.shape)), (name, n)
+
+
 def test_edge_cases_empty_block_and_culled(api):
     w = S.tiny()
     cam, prm = w.cams[0], w.params

@@ -341,6 +341,28 @@ def test_over_two_layer_worked_example():
     assert np.array_equal(B[0, 0], [0.125, 0.5, 0, 0.75])
 
 
+def over_of(F, B):
+    """F over B, premultiplied, per channel."""
+    return F + (1.0 - F[..., 3:4]) * B
+
+
+def test_over_cases_worked_by_hand(over_by_hand):
+    """Every split of each hand-worked case (tests/golden/over_by_hand.txt) into
+    F (the first n layers) and B (the rest) gives F over B == the hand result,
+    and n = all layers leaves B transparent (Abstract; Method section)."""
+    for name, lay, res in over_by_hand:
+        k = len(lay)
+        imgs = S.half_bits(lay.reshape(k, 1, 1, 4))
+        assert np.array_equal(imgs.view(np.float16).astype(np.float64).reshape(k, 4), lay), name
+        for n in range(k + 1):
+            F, B = O.composite(1, 1, imgs, list(range(k)), n)
+            assert np.array_equal(over_of(F, B)[0, 0], res), (name, n)
+            if n == k:
+                assert np.array_equal(F[0, 0], res) and not np.any(B), name
+            if n == 0:
+                assert np.array_equal(B[0, 0], res) and not np.any(F), name
+
+
 def test_over_fold_equals_product_form():
     """alpha = 1 - prod(1 - a_k), rgb = sum_k c_k prod_{j<k}(1 - a_j)."""
     r = S.rng(9)
