@@ -6,15 +6,75 @@
 // The forward blends each pixel's list front to back and stops a pixel once
 // the next blend would take its transmittance below t_min; the workgroup
 // stops when all its pixels have stopped.
+//
+// Each wave (four pixel rows of the tile) walks only the staged entries whose
+// alpha >= alpha_min ellipse reaches its rows: the others cannot blend at any
+// of its pixels, so the result is the same, and in tiles of many small
+// Gaussians a wave's walk is a fraction of the tile's list.
 #include "blend.h"
 
 namespace abcd {
 namespace {
 
+// Rows mask of a kept entry: bit w set when its ellipse (the margin of
+// splat_touches_box included) reaches pixel rows 4w .. 4w + 3 of the tile.
+__device__ __forceinline__ uint32_t rows_reached(float u, float v, float a, float b, float c,
+                                                 float o, float alpha_min, const TileBox& box) {
+  uint32_t rows = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float y0 = box.y0 + 4.0f * (float)w, y1 = fminf(box.y1, y0 + 3.0f);
+    if (y0 <= y1 && splat_touches_box(u, v, a, b, c, o, alpha_min, box.x0, box.x1, y0, y1))
+      rows |= 1u << w;
+  }
+  return rows;
+}
+
+// Block-wide compaction of the staged entries (as compact() does) and, for
+// each wave w, the list of the staged slots whose rows mask has bit w, in
+// list order, into s_idx[w]. s_cnt holds 5 x 4 wave counts. Returns the
+// number kept; wcnt is the length of the calling wave's list (both uniform).
+__device__ __forceinline__ int compact_rows(bool keep, uint32_t rows, int (*s_cnt)[4],
+                                            uint8_t (*s_idx)[256], int& pos, int& wcnt) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const uint64_t below = (1ull << l) - 1ull;
+  const uint64_t bal = __ballot(keep);
+  uint64_t rb[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) rb[r] = __ballot((rows >> r) & 1u);
+  if (l == 0) {
+    s_cnt[0][w] = __popcll(bal);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) s_cnt[1 + r][w] = __popcll(rb[r]);
+  }
+  __syncthreads();
+  int off = 0, tot = 0, mine = 0;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int c = s_cnt[0][v];
+    off += v < w ? c : 0;
+    tot += c;
+    mine += s_cnt[1 + w][v];
+  }
+  pos = off + __popcll(bal & below);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if ((rows >> r) & 1u) {
+      int o = 0;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) o += v < w ? s_cnt[1 + r][v] : 0;
+      s_idx[r][o + __popcll(rb[r] & below)] = (uint8_t)pos;
+    }
+  }
+  wcnt = __builtin_amdgcn_readfirstlane(mine);
+  return __builtin_amdgcn_readfirstlane(tot);
+}
+
 // kHalf: the cached-render variant: F = B = transparent, the image is written
 // as fp16 RGBA to out16 (round to nearest even), no final T or walk lengths.
+// Register budget: four waves per SIMD (at most 128 VGPRs).
 template <bool kHalf>
-__global__ __launch_bounds__(256) void render_fwd_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void render_fwd_kernel(
     BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
     const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
@@ -23,9 +83,10 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     uint2* __restrict__ out16, int* __restrict__ rect, int fb_stop, SplitLayout sp) {
   __shared__ float4 s_ga[256];  // u, v, qa, qb
   __shared__ float4 s_gb[256];  // qc, o, r, g
-  __shared__ float s_bl[256];   // b
+  __shared__ float4 s_bl[256];  // b (16-byte stride: one address serves all three reads)
   __shared__ int s_pos[256];    // position in the tile's list
-  __shared__ int s_wcnt[4];
+  __shared__ __align__(8) uint8_t s_idx[4][256];  // per wave: staged slots reaching its rows
+  __shared__ int s_wcnt[5][4];
   __shared__ unsigned long long s_nb;
   __shared__ uint32_t s_base;
   __shared__ uint32_t s_walk;  // largest walk of the tile (split only)
@@ -100,14 +161,16 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
     const float3 cn = conic_of(rec.co);
     const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, cn.x, cn.y, cn.z, rec.co.w,
                                                      k.alpha_min, box.x0, box.x1, box.y0, box.y1);
-    int pos;
-    const int cnt = compact(keep, s_wcnt, pos);
+    const uint32_t rows =
+        keep ? rows_reached(rec.m.x, rec.m.y, cn.x, cn.y, cn.z, rec.co.w, k.alpha_min, box) : 0u;
+    int pos, wcnt;
+    const int cnt = compact_rows(keep, rows, s_wcnt, s_idx, pos, wcnt);
     staged += (uint32_t)cnt;
     if (keep) {
       const Splat sp = make_splat(rec.m, rec.co);
       s_ga[pos] = make_float4(sp.u, sp.v, sp.qa, sp.qb);
       s_gb[pos] = make_float4(sp.qc, sp.o, rec.r, rec.g);
-      s_bl[pos] = rec.b;
+      s_bl[pos].x = rec.b;
       s_pos[pos] = (int)(b0 - start) + tid;
     }
     __syncthreads();
@@ -121,17 +184,22 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
       // Lanes step through the entries together without divergent branches:
       // a lane that skips an entry, or has stopped, blends with weight 0.
       // Entries are read from LDS kGroup at a time, all reads issued before
-      // the first is used, so the LDS latency is paid once per group.
-      int jl = -1;  // last entry of this batch the lane blended
-      for (int j0 = 0; j0 < cnt; j0 += kGroup) {
+      // the first is used, so the LDS latency is paid once per group. The
+      // wave walks its own list of staged slots; slots past its end hold
+      // stale bytes, which still index s_ga.
+      static_assert(kGroup == 8, "one 8-byte read of slot indices per group");
+      const uint8_t* my_idx = s_idx[tid >> 6];
+      int jl = -1;  // position in the wave's list of the last entry the lane blended
+      for (int j0 = 0; j0 < wcnt; j0 += kGroup) {
         float4 ga[kGroup], gb[kGroup];
         float bl[kGroup];
+        const uint2 iw = *reinterpret_cast<const uint2*>(my_idx + j0);
 #pragma unroll
         for (int i = 0; i < kGroup; ++i) {
-          const int j = min(j0 + i, 255);
+          const int j = (int)(((i < 4 ? iw.x : iw.y) >> (8 * (i & 3))) & 255u);
           ga[i] = s_ga[j];
           gb[i] = s_gb[j];
-          bl[i] = s_bl[j];
+          bl[i] = s_bl[j].x;
         }
         // keep the group's reads ahead of the arithmetic (the compiler would
         // otherwise sink each read to its use)
@@ -141,7 +209,7 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
                        "v"(gb[i].y), "v"(gb[i].z), "v"(gb[i].w), "v"(bl[i]));
 #pragma unroll
         for (int i = 0; i < kGroup; ++i) {
-          const bool valid = j0 + i < cnt;  // past the batch: a no-op step
+          const bool valid = j0 + i < wcnt;  // past the list: a no-op step
           const AlphaEval ae = eval_alpha(fx - ga[i].x, fy - ga[i].y, ga[i].z, ga[i].w, gb[i].x,
                                           gb[i].y, k.alpha_min, k.alpha_max);
           const float Tn = T * (1.0f - ae.alpha);
@@ -161,7 +229,7 @@ __global__ __launch_bounds__(256) void render_fwd_kernel(
         }
         if (!__ballot(!done)) break;  // wave-uniform
       }
-      if (jl >= 0) lastk = (uint32_t)s_pos[jl] + 1;
+      if (jl >= 0) lastk = (uint32_t)s_pos[my_idx[jl]] + 1;
     }
     // s_wcnt is rewritten only after the next barrier
   }
