@@ -603,10 +603,11 @@ def _raw_bin(api, cam, p, capacity, values, ranges, order):
     _lib.check(st)
 
 
-def test_loss_l1_gradient(api):
+@pytest.mark.parametrize("H,W", [(40, 56), (97, 131), (2100, 2048)])
+def test_loss_l1_gradient(api, H, W):
+    """Small, ragged, and past one launch's pass (4096 x 1024 pixels)."""
     r = S.rng(80)
-    H, W = 40, 56
-    say("loss l1")
+    say("loss l1", H, W)
     out = np.concatenate([r.uniform(0, 1, (H, W, 3)), r.uniform(0, 1, (H, W, 1))], -1).astype(np.float32)
     tgt = r.uniform(0, 1, (H, W, 3)).astype(np.float32)
     bg = (0.2, 0.5, 0.9)
@@ -618,7 +619,7 @@ def test_loss_l1_gradient(api):
     s = np.sign(img - tgt) / (3 * H * W)
     exp = np.concatenate([s, -(s * np.array(bg)).sum(-1, keepdims=True)], -1)
     assert np.abs(np32(g) - exp).max() < 1e-9
-    assert abs(loss.item() - np.abs(img - tgt).sum() / (3 * H * W)) < 1e-5
+    assert abs(loss.item() - np.abs(img.astype(np.float64) - tgt).sum() / (3 * H * W)) < 1e-5
 
 
 def test_adam_step_matches_oracle(api):
