@@ -303,11 +303,16 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
     uint32_t* __restrict__ queue, uint32_t max_items, SplitLayout sp) {
   __shared__ uint2 s_item;
   const uint32_t n_items = min(queue[0], max_items);
+  // The first item of workgroup b is item b; later ones come from the queue
+  // (atomic adds to one address are serialised, so a grab by every workgroup
+  // at the start would stagger the starts by the whole grid's worth of them).
+  bool first = true;
   for (;;) {
     if (threadIdx.x == 0) {
-      const uint32_t i = atomicAdd(&queue[1], 1u);
+      const uint32_t i = first ? blockIdx.x : gridDim.x + atomicAdd(&queue[1], 1u);
       s_item = i < n_items ? items[i] : make_uint2(kNoSlot, 0u);
     }
+    first = false;
     __syncthreads();
     const uint2 it = s_item;
     __syncthreads();
