@@ -304,6 +304,11 @@ int32_t launch_loss_l1(int width, int height, const float* out_rgba, const float
 // and the per-tile maximum of the forward's walk lengths as a work estimate.
 int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, const uint32_t* skip,
                           const char* name, hipStream_t stream);
+// The backward's work queue: queue[0] = number of items, then kQueues
+// counters kQueueStride words apart (one cache line each): item i is served
+// by queue i mod kQueues, whose counter is queue[kQueueStride q + 1].
+constexpr int kQueues = 8;
+constexpr int kQueueStride = 64;
 int32_t launch_bwd_schedule(int ntiles, const uint32_t* key, const uint32_t* walk,
                             uint32_t* order, const SplitLayout& split, void* items, uint32_t cap,
                             uint32_t* queue, hipStream_t stream);

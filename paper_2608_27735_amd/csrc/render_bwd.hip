@@ -303,13 +303,21 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
     uint32_t* __restrict__ queue, uint32_t max_items, SplitLayout sp) {
   __shared__ uint2 s_item;
   const uint32_t n_items = min(queue[0], max_items);
-  // The first item of workgroup b is item b; later ones come from the queue
-  // (atomic adds to one address are serialised, so a grab by every workgroup
-  // at the start would stagger the starts by the whole grid's worth of them).
+  // Atomic adds to one address are serialised, and light items at the end
+  // are taken faster than one counter can serve them. So item i belongs to
+  // queue i mod nq (nq = kQueues, fewer for a smaller grid), each queue
+  // heaviest first, and workgroup b takes from queue b mod nq (one per XCD,
+  // which take workgroups round robin). The first item of workgroup b is item
+  // b, taken without an atomic; later ones come from the queue's counter.
+  const uint32_t nq = min(gridDim.x, (uint32_t)kQueues);
+  const uint32_t q = blockIdx.x % nq;
+  const uint32_t gq = (gridDim.x - q + nq - 1) / nq;  // workgroups of queue q
   bool first = true;
   for (;;) {
     if (threadIdx.x == 0) {
-      const uint32_t i = first ? blockIdx.x : gridDim.x + atomicAdd(&queue[1], 1u);
+      const uint32_t r =
+          first ? blockIdx.x / nq : gq + atomicAdd(&queue[kQueueStride * q + 1], 1u);
+      const uint64_t i = (uint64_t)q + (uint64_t)nq * r;
       s_item = i < n_items ? items[i] : make_uint2(kNoSlot, 0u);
     }
     first = false;
@@ -333,7 +341,7 @@ static size_t g2d_bytes(int64_t n) {
 // not split) and queue.
 size_t render_bwd_workspace_bytes(int64_t n) {
   return g2d_bytes(n) + 2 * sizeof(uint32_t) * ABCD_MAX_TILES + sizeof(uint2) * ABCD_MAX_TILES +
-         256;
+         sizeof(uint32_t) * kQueueStride * kQueues;
 }
 
 namespace {

@@ -140,8 +140,9 @@ __global__ __launch_bounds__(kBlock) void tile_walk_kernel(int width, int height
 // Work items of the backward, in the order of `order` (tiles by decreasing
 // estimated work): a tile with no walk has none, a tile the forward split (it
 // has an end-of-walk slot) one per chunk its walk reaches, any other tile
-// one. Writes items (tile, chunk), queue[0] = their number and queue[1] = 0
-// (the head the backward's workgroups advance). s_n is workgroup memory of
+// one. Writes items (tile, chunk), queue[0] = their number and zeroes the
+// counters of the kQueues queues (the heads the backward's workgroups
+// advance). s_n is workgroup memory of
 // ABCD_MAX_TILES bytes.
 __device__ __forceinline__ void build_items(int ntiles, const uint32_t* __restrict__ order,
                                             const uint32_t* __restrict__ walk,
@@ -192,10 +193,8 @@ __device__ __forceinline__ void build_items(int ntiles, const uint32_t* __restri
     if (tid == 0) s_off += total;
     __syncthreads();
   }
-  if (tid == 0) {
-    queue[0] = min(s_off, cap);
-    queue[1] = 0;
-  }
+  if (tid == 0) queue[0] = min(s_off, cap);
+  if (tid < kQueues) queue[kQueueStride * tid + 1] = 0;
 }
 
 // The backward's schedule in one launch: tiles ordered by `key`, then the
