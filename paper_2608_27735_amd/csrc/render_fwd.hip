@@ -187,16 +187,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
       // the first is used, so the LDS latency is paid once per group. The
       // wave walks its own list of staged slots; slots past its end hold
       // stale bytes, which still index s_ga.
-      static_assert(kGroup == 8, "one 8-byte read of slot indices per group");
-      const uint8_t* my_idx = s_idx[tid >> 6];
+      static_assert(kGroup % 4 == 0, "slot indices are read four at a time");
+      const uint32_t* my_idx = reinterpret_cast<const uint32_t*>(s_idx[tid >> 6]);
       int jl = -1;  // position in the wave's list of the last entry the lane blended
       for (int j0 = 0; j0 < wcnt; j0 += kGroup) {
         float4 ga[kGroup], gb[kGroup];
         float bl[kGroup];
-        const uint2 iw = *reinterpret_cast<const uint2*>(my_idx + j0);
+        uint32_t iw[kGroup / 4];
+#pragma unroll
+        for (int h = 0; h < kGroup / 4; ++h) iw[h] = my_idx[j0 / 4 + h];
 #pragma unroll
         for (int i = 0; i < kGroup; ++i) {
-          const int j = (int)(((i < 4 ? iw.x : iw.y) >> (8 * (i & 3))) & 255u);
+          const int j = (int)((iw[i >> 2] >> (8 * (i & 3))) & 255u);
           ga[i] = s_ga[j];
           gb[i] = s_gb[j];
           bl[i] = s_bl[j].x;
@@ -229,7 +231,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
         }
         if (!__ballot(!done)) break;  // wave-uniform
       }
-      if (jl >= 0) lastk = (uint32_t)s_pos[my_idx[jl]] + 1;
+      if (jl >= 0) lastk = (uint32_t)s_pos[s_idx[tid >> 6][jl]] + 1;
     }
     // s_wcnt is rewritten only after the next barrier
   }
