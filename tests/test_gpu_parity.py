@@ -73,6 +73,14 @@ def cases():
                       math.log(0.02), 0.2)
     sc3["opacity_logits"] = rd.normal(-4.0, 0.3, 24000).astype(np.float32)
     out.append(("deep-tile-48x48", cam, RasterParams(sh_degree=0), sc3))
+    # small splats (1-3 pixels) in a ragged 100x75 image: most entries reach
+    # only some of a tile's four-row strips, and the last tile row holds 11
+    # rows (its third strip is clipped, its fourth empty)
+    rs = S.rng(23)
+    cam = look_at((0.0, -3.0, 0.4), (0, 0, 0), 100, 75)
+    sc4 = S.gaussians(rs, rs.uniform((-0.8, -0.8, -0.6), (0.8, 0.8, 0.6), (6000, 3)), 1,
+                      math.log(0.012), 0.4)
+    out.append(("small-splats-100x75", cam, RasterParams(sh_degree=1), sc4))
     return out
 
 
