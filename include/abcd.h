@@ -37,6 +37,12 @@
  *    means2d 8 bytes, workspaces 256 bytes (an unaligned call is rejected).
  *  - Functions are stateless and reentrant; concurrent calls on one stream
  *    must not share a workspace.
+ *  - Device arrays must be ordinary (coarse-grained) device memory, as
+ *    hipMalloc and PyTorch's CUDA allocator return it. The library is built
+ *    with hardware fp32 atomic adds (-munsafe-fp-atomics) for gradients,
+ *    screen-space gradient sums and counters; on fine-grained, host-mapped or
+ *    managed memory those atomics are not guaranteed to take effect, so the
+ *    workspaces and every gradient output must not live there.
  */
 #ifndef ABCD_H
 #define ABCD_H
@@ -67,7 +73,9 @@ typedef enum {
  * z forward); pixel (i, j) covers [i, i+1) x [j, j+1) and is sampled at its
  * centre (i + 0.5, j + 0.5). campos is the camera centre in world space (for
  * the view direction of the SH colour). Gaussians with view depth <= near_plane
- * are culled. */
+ * are culled. near_plane must be positive (depth keys are the fp32 bit
+ * patterns of positive depths, which sort as unsigned integers); a call with
+ * near_plane <= 0 returns ABCD_E_INVALID. */
 typedef struct {
   int32_t width, height;
   float fx, fy, cx, cy;
@@ -150,12 +158,14 @@ ABCD_API int32_t abcd_project(const abcd_camera* cam /* host */, const abcd_rast
  * octave and its quarter), ties in tile order.
  *
  * capacity: number of elements values_sorted (and keys_sorted) can hold. If
- * the intersection count M exceeds it, nothing is written to values_sorted,
- * keys_sorted, tile_ranges or tile_order.
+ * the intersection count M exceeds it (or does not fit 32 bits), nothing is
+ * written to values_sorted or keys_sorted, every tile range is written empty
+ * (so the blend calls that follow render nothing of the active block and read
+ * no list entry) and tile_order is the identity.
  * n_isect (host, may be NULL): if given, the call synchronises `stream` once,
  * stores M there and returns ABCD_E_CAPACITY when M > capacity. If NULL, the
- * call does not synchronise; M (uint64) is left at the start of the workspace
- * and a capacity overflow leaves the outputs unwritten.
+ * call does not synchronise; M (uint64) is left at the start of the workspace,
+ * where the caller can read it later (M > capacity: that call overflowed).
  * capacity must be below 2^32.
  * workspace: at least abcd_bin_sort_workspace_size(n, capacity, width, height)
  * bytes, 256-byte aligned; it grows with the capacity (8 bytes per element for
@@ -207,7 +217,9 @@ ABCD_API int32_t abcd_split_workspace_size(int64_t n_slots, size_t* bytes);
  * The active render A = (C, 1 - T) is composited as out = F over A over B:
  *   out_rgb = F_rgb + (1 - F_a)(C + T B_rgb),
  *   out_a   = F_a + (1 - F_a)(1 - T (1 - B_a)).
- * F or B may be NULL (transparent). Also writes final_T[H][W] and last[H][W]
+ * F or B may be NULL (transparent); tile_ranges, values_sorted, means2d,
+ * conic_opacity, rgb and the three outputs may not (ABCD_E_INVALID; a
+ * placeholder buffer serves when the lists are empty). Also writes final_T[H][W] and last[H][W]
  * (entries of the tile's list walked up to and including the last blended
  * one), both needed by abcd_render_bwd. n_blends (may be NULL): the number of
  * blended (pixel, Gaussian) pairs of this call is ADDED to *n_blends.
@@ -234,7 +246,8 @@ ABCD_API int32_t abcd_render_fwd(const abcd_camera* cam /* host */, const abcd_r
  * rect (device, may be NULL): int32[4] = (x0, y0, x1, y1), the bounding box
  * of the 16x16 tiles holding a pixel that blended anything, clipped to the
  * image; the image is zero outside it (x1 <= x0 when nothing blended). It is
- * the coverage box abcd_composite_cache takes. */
+ * the coverage box abcd_composite_cache takes. tile_ranges, values_sorted,
+ * means2d, conic_opacity, rgb and image_f16 may not be NULL. */
 ABCD_API int32_t abcd_render_cache(const abcd_camera* cam /* host */,
                           const abcd_raster_params* prm /* host */, const uint32_t* tile_ranges,
                           const uint32_t* tile_order, const uint32_t* values_sorted,

@@ -430,35 +430,53 @@ static int isect_cmp(const void* pa, const void* pb) {
 void orc_bin(int32_t width, int32_t height, int64_t n, const float* depth, const int32_t* rect,
              const uint32_t* tiles_touched, uint64_t* keys, uint32_t* values,
              uint32_t* tile_ranges) {
+  /* Every (tile, Gaussian) pair of the support rectangles, ordered by
+   * (key, index) with key = tile << 32 | depth bits. The tile is the key's
+   * high part, so that order is: tiles in increasing order, and within a tile
+   * its Gaussians by (depth bits, index). The pairs are first grouped by tile
+   * (a counting pass over the rectangles, then placement in index order) and
+   * each tile's group is sorted on its own, which gives the same sequence as
+   * one sort of all pairs and lets the tiles sort in parallel. */
   const int ntx = tiles_x_of(width), nty = tiles_y_of(height);
   const int64_t ntiles = (int64_t)ntx * nty;
   const int64_t m = orc_count_isect(n, tiles_touched);
+  int64_t* start = (int64_t*)calloc((size_t)ntiles + 1, sizeof(int64_t));
+  int64_t* fill = (int64_t*)malloc(sizeof(int64_t) * (size_t)(ntiles + 1));
+  for (int64_t i = 0; i < n; i++) {
+    if (tiles_touched[i] == 0) continue;
+    const int32_t* rc = rect + 4 * i;
+    for (int ty = rc[1]; ty <= rc[3]; ty++)
+      for (int tx = rc[0]; tx <= rc[2]; tx++) start[(int64_t)ty * ntx + tx + 1]++;
+  }
+  for (int64_t t = 0; t < ntiles; t++) start[t + 1] += start[t];
+  memcpy(fill, start, sizeof(int64_t) * (size_t)(ntiles + 1));
   isect* list = (isect*)malloc(sizeof(isect) * (size_t)(m > 0 ? m : 1));
-  int64_t k = 0;
   for (int64_t i = 0; i < n; i++) {
     if (tiles_touched[i] == 0) continue;
     const int32_t* rc = rect + 4 * i;
     for (int ty = rc[1]; ty <= rc[3]; ty++)
       for (int tx = rc[0]; tx <= rc[2]; tx++) {
-        uint64_t tile = (uint64_t)ty * ntx + tx;
+        const uint64_t tile = (uint64_t)ty * ntx + tx;
+        const int64_t k = fill[tile]++;
         list[k].key = (tile << 32) | f32_bits(depth[i]);
         list[k].idx = (uint32_t)i;
-        k++;
       }
   }
-  qsort(list, (size_t)m, sizeof(isect), isect_cmp);
-  /* start(t) = #entries with tile < t, end(t) = #entries with tile <= t */
-  int64_t pos = 0;
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int64_t t = 0; t < ntiles; t++)
+    qsort(list + start[t], (size_t)(start[t + 1] - start[t]), sizeof(isect), isect_cmp);
   for (int64_t t = 0; t < ntiles; t++) {
-    tile_ranges[2 * t] = (uint32_t)pos;
-    while (pos < m && (int64_t)(list[pos].key >> 32) == t) pos++;
-    tile_ranges[2 * t + 1] = (uint32_t)pos;
+    tile_ranges[2 * t] = (uint32_t)start[t];
+    tile_ranges[2 * t + 1] = (uint32_t)start[t + 1];
   }
+#pragma omp parallel for schedule(static)
   for (int64_t j = 0; j < m; j++) {
     keys[j] = list[j].key;
     values[j] = list[j].idx;
   }
   free(list);
+  free(fill);
+  free(start);
 }
 
 /* ======================================================================= */
@@ -473,7 +491,7 @@ void orc_render_fwd(const orc_camera* cam, const orc_params* prm, const uint32_t
                     const uint32_t* values, const double* means2d, const double* conic,
                     const double* opacity, const double* rgb, const double* F, const double* B,
                     double* out, double* final_T, uint32_t* last, uint64_t* n_blends,
-                    double rel_margin, uint8_t* knife, double* t_stop) {
+                    double rel_margin, double f32_kappa, uint8_t* knife, double* t_stop) {
   const int W = cam->width, H = cam->height;
   const int ntx = tiles_x_of(W);
   const int64_t npix = (int64_t)W * H;
@@ -492,6 +510,9 @@ void orc_render_fwd(const orc_camera* cam, const orc_params* prm, const uint32_t
     if (B) memcpy(bb, B + 4 * pix, sizeof bb);
     /* weight of the active render in the composited image: 1 - F_alpha */
     const double vis = prm->fb_stop ? 1.0 - f[3] : 1.0;
+    /* relative error bound of the transmittance a fp32 walk would hold (with
+     * f32_kappa > 0): one rounding per blend plus the alpha errors below */
+    double errT = 0.0;
     for (uint32_t k = start; k < end; k++) {
       const uint32_t g = values[k];
       const double dx = cxp - means2d[2 * g], dy = cyp - means2d[2 * g + 1];
@@ -500,17 +521,39 @@ void orc_render_fwd(const orc_camera* cam, const orc_params* prm, const uint32_t
       const double terms = 0.5 * (fabs(a) * dx * dx + fabs(c) * dy * dy) + fabs(b * dx * dy);
       if (rel_margin > 0 && terms > 0 && fabs(power) <= rel_margin * terms) kn = 1;
       if (power > 0) continue;
+      /* margin of the alpha decisions: rel_margin, plus (f32_kappa > 0) a
+       * bound on the relative error of alpha evaluated in fp32 from a
+       * fp32-rounded Cholesky factor L of the conic, q = (l11 dx + l21 dy)^2 +
+       * (l22 dy)^2: each product and the factor carry a relative rounding of
+       * 2^-24, so q moves by at most a small multiple of 2^-24 times
+       * |e1| (|l11 dx| + |l21 dy|) + |e2| |l22 dy| + q, and alpha = o e^(-q/2)
+       * by half of that, relatively. Large where the two products of e1
+       * nearly cancel (long thin splats seen along their major axis). */
+      double da = rel_margin;
+      if (f32_kappa > 0) {
+        const double l11 = sqrt(a), l21 = b / l11;
+        const double l22 = sqrt(fmax(c - l21 * l21, 0.0));
+        const double e1 = l11 * dx + l21 * dy, e2 = l22 * dy;
+        da += f32_kappa * 0x1p-24 *
+              (fabs(e1) * (fabs(l11 * dx) + fabs(l21 * dy)) + fabs(e2) * fabs(l22 * dy) +
+               e1 * e1 + e2 * e2);
+      }
       const double araw = opacity[g] * exp(power);
-      if (near_rel(araw, prm->alpha_max, rel_margin)) kn = 1;
+      if (near_rel(araw, prm->alpha_max, da)) kn = 1;
       const double alpha = araw < prm->alpha_max ? araw : prm->alpha_max;
-      if (near_rel(alpha, prm->alpha_min, rel_margin)) kn = 1;
+      if (near_rel(alpha, prm->alpha_min, da)) kn = 1;
       if (alpha < prm->alpha_min) continue;
       const double Tn = T * (1.0 - alpha);
-      if (near_rel(vis * Tn, prm->t_min, rel_margin)) kn = 1;
+      /* the stop decision: rel_margin alone, or with f32_kappa > 0 the error
+       * bound of the fp32 transmittance including this entry's alpha */
+      const double dstep = alpha / (1.0 - alpha) * da;
+      const double dT = f32_kappa > 0 ? rel_margin + errT + dstep + 4 * 0x1p-24 : rel_margin;
+      if (near_rel(vis * Tn, prm->t_min, dT)) kn = 1;
       if (vis * Tn < prm->t_min) {
         tst = T;
         break;
       }
+      errT += dstep + 2 * 0x1p-24;
       Cr += rgb[3 * g] * alpha * T;
       Cg += rgb[3 * g + 1] * alpha * T;
       Cb += rgb[3 * g + 2] * alpha * T;

@@ -79,7 +79,9 @@ void orc_project_values_f64(const orc_camera* cam, const orc_params* prm, int64_
 int64_t orc_count_isect(int64_t n, const uint32_t* tiles_touched);
 
 /* Lists every (tile, Gaussian) pair, key = tile << 32 | fp32 bits of depth,
- * sorted by (key, Gaussian index); tile_ranges[2*t..] = [start, end). */
+ * sorted by (key, Gaussian index); tile_ranges[2*t..] = [start, end). The
+ * pairs are grouped by tile and each tile's group sorted by (depth bits,
+ * index), the same sequence as one sort of all pairs by (key, index). */
 void orc_bin(int32_t width, int32_t height, int64_t n, const float* depth, const int32_t* rect,
              const uint32_t* tiles_touched, uint64_t* keys, uint32_t* values,
              uint32_t* tile_ranges);
@@ -89,13 +91,20 @@ void orc_bin(int32_t width, int32_t height, int64_t n, const float* depth, const
 /* Front-to-back blend of the sorted tile lists, then out = F over A over B
  * (premultiplied RGBA). F, B may be NULL (transparent). knife/t_stop may be
  * NULL; knife[p] != 0 marks a pixel one of whose threshold decisions lies
- * within rel_margin of its threshold. With prm->fb_stop the stop test is
- * (1 - F_alpha) T_next < t_min instead of T_next < t_min. */
+ * within its margin of its threshold: rel_margin (relative) for every
+ * decision when f32_kappa = 0; with f32_kappa > 0 the alpha decisions
+ * (alpha_min, alpha_max) take rel_margin plus f32_kappa 2^-24 times the
+ * magnitude of the terms of the quadratic form in its Cholesky form (a bound
+ * on the relative error of alpha evaluated in fp32), and the stop decision
+ * rel_margin plus the accumulated bound of the transmittance. The power > 0
+ * test always takes rel_margin times the magnitude of its terms. With
+ * prm->fb_stop the stop test is (1 - F_alpha) T_next < t_min instead of
+ * T_next < t_min. */
 void orc_render_fwd(const orc_camera* cam, const orc_params* prm, const uint32_t* tile_ranges,
                     const uint32_t* values, const double* means2d, const double* conic,
                     const double* opacity, const double* rgb, const double* F, const double* B,
                     double* out, double* final_T, uint32_t* last, uint64_t* n_blends,
-                    double rel_margin, uint8_t* knife, double* t_stop);
+                    double rel_margin, double f32_kappa, uint8_t* knife, double* t_stop);
 
 /* Per-pixel backward: accumulates, per Gaussian, the 9 screen-space gradients
  * g2d[9*i..] = dL/d(u, v, a, b, c, opacity, r, g, b). g2d is overwritten. */

@@ -73,7 +73,8 @@ def lib():
     L.orc_bin.restype = None
     L.orc_render_fwd.argtypes = [cam_p, prm_p, _u32p, _u32p, _f64p, _f64p, _f64p, _f64p,
                                  _opt(_f64p), _opt(_f64p), _f64p, _f64p, _u32p,
-                                 C.POINTER(C.c_uint64), C.c_double, _opt(_u8p), _opt(_f64p)]
+                                 C.POINTER(C.c_uint64), C.c_double, C.c_double, _opt(_u8p),
+                                 _opt(_f64p)]
     L.orc_render_fwd.restype = None
     L.orc_render_bwd_2d.argtypes = [cam_p, prm_p, C.c_int64, _u32p, _u32p, _f64p, _f64p, _f64p,
                                     _f64p, _opt(_f64p), _opt(_f64p), _f64p, _f64p]
@@ -186,7 +187,11 @@ def _img(x, cam):
 
 
 def render_fwd(cam, prm, tile_ranges, values, means2d, conic, opacity, rgb, F=None, B=None,
-               rel_margin=0.0):
+               rel_margin=0.0, f32_kappa=0.0):
+    """Forward blend and composite (fp64). knife marks pixels with a threshold
+    decision within its margin (see orc_render_fwd): rel_margin for every
+    decision, or, with f32_kappa > 0, per-decision margins from an error bound
+    of the fp32 evaluation of alpha and of the transmittance."""
     H, W = cam.height, cam.width
     out = np.zeros((H, W, 4))
     final_T = np.zeros((H, W))
@@ -198,7 +203,7 @@ def render_fwd(cam, prm, tile_ranges, values, means2d, conic, opacity, rgb, F=No
     lib().orc_render_fwd(C.byref(_cam(cam)), C.byref(_prm(prm)), _c(tile_ranges, np.uint32), vals,
                          _c(means2d, np.float64), _c(conic, np.float64), _c(opacity, np.float64),
                          _c(rgb, np.float64), _img(F, cam), _img(B, cam), out, final_T, last,
-                         C.byref(nb), float(rel_margin), knife, t_stop)
+                         C.byref(nb), float(rel_margin), float(f32_kappa), knife, t_stop)
     return dict(out=out, final_T=final_T, last=last, n_blends=int(nb.value), knife=knife.astype(bool),
                 t_stop=t_stop)
 

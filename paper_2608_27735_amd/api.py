@@ -22,6 +22,21 @@ def _stream():
     return torch.cuda.current_stream().cuda_stream
 
 
+_dummies = {}
+
+
+def _ptr_nz(t, device):
+    """Device pointer of t; for a missing or empty tensor (whose pointer may be
+    NULL) a small placeholder buffer on the device that no kernel reads (the
+    library requires these input pointers to be non-NULL)."""
+    if t is not None and t.numel() > 0:
+        return t.data_ptr()
+    d = _dummies.get(device)
+    if d is None:
+        d = _dummies[device] = torch.zeros(64, dtype=torch.float32, device=device)
+    return d.data_ptr()
+
+
 def _need(t, name, dtype, shape=None):
     if t is None:
         raise ValueError(f"{name} is required")
@@ -95,8 +110,9 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
 
     With sync=True (default) M is read back (one stream synchronisation) and
     the buffers are grown to fit it; with sync=False the call never
-    synchronises and `capacity`/`values` must already be large enough (an
-    overflow leaves the outputs unwritten)."""
+    synchronises and `capacity`/`values` must already be large enough: an
+    overflow leaves values unwritten and every tile range empty, and
+    intersections(workspace) > capacity tells it afterwards."""
     means2d, extent = proj["means2d"], proj["extent"]
     depth, tiles = proj["depth"], proj["tiles_touched"]
     n = means2d.shape[0]
@@ -142,6 +158,13 @@ def bin_sort(width, height, proj, capacity=None, workspace=None, values=None, ke
                 n_isect=int(m.value) if sync else None, workspace=workspace, capacity=capacity)
 
 
+def intersections(workspace):
+    """The intersection count M the last abcd_bin_sort on this workspace found
+    (the uint64 at the workspace's start; reading it synchronises with the
+    stream). M > capacity means that call overflowed and rendered nothing."""
+    return int(workspace[:8].cpu().view(torch.int64).item())
+
+
 # -------------------------------------------------------------- rasterise
 
 def split_workspace_size(n_slots):
@@ -182,7 +205,8 @@ def render_fwd(cam, prm, bins, proj, F=None, B=None, n_blends=None, out=None, sp
     lib = _lib.load()
     check(lib.abcd_render_fwd(C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)),
                               _ptr(bins["tile_ranges"]), _ptr(bins.get("tile_order")),
-                              _ptr(bins["values"]), _ptr(proj["means2d"]), _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]),
+                              _ptr_nz(bins["values"], dev), _ptr_nz(proj["means2d"], dev),
+                              _ptr_nz(proj["conic_opacity"], dev), _ptr_nz(proj["rgb"], dev),
                               _ptr(F), _ptr(B), _ptr(out["out"]), _ptr(out["final_T"]),
                               _ptr(out["last"]), _ptr(n_blends), _split_struct(split), _stream()))
     return out
@@ -197,10 +221,12 @@ def render_cache(cam, prm, bins, proj, image=None, rect=None):
         image = _empty((H, W, 4), torch.float16, proj["means2d"].device)
     _need(image, "image", torch.float16, (H, W, 4))
     _opt(rect, "rect", torch.int32, (4,))
+    dev = proj["means2d"].device
     check(_lib.load().abcd_render_cache(
         C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)),
-        _ptr(bins["tile_ranges"]), _ptr(bins.get("tile_order")), _ptr(bins["values"]),
-        _ptr(proj["means2d"]), _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]), _ptr(image),
+        _ptr(bins["tile_ranges"]), _ptr(bins.get("tile_order")), _ptr_nz(bins["values"], dev),
+        _ptr_nz(proj["means2d"], dev), _ptr_nz(proj["conic_opacity"], dev),
+        _ptr_nz(proj["rgb"], dev), _ptr(image),
         _ptr(rect), _stream()))
     return image
 
@@ -235,7 +261,8 @@ def render_bwd(cam, prm, params, proj, bins, fwd, dL_dout, F=None, B=None, works
         _ptr(params["means"]), _ptr(params["log_scales"]), _ptr(params["quats"]),
         _ptr(params["opacity_logits"]), _ptr(params["sh"]), _ptr(proj["means2d"]),
         _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]), _ptr(proj["extent"]),
-        _ptr(bins["tile_ranges"]), _ptr(bins["values"]), _ptr(F), _ptr(B), _ptr(fwd["final_T"]),
+        _ptr(bins["tile_ranges"]), _ptr_nz(bins["values"], dev), _ptr(F), _ptr(B),
+        _ptr(fwd["final_T"]),
         _ptr(fwd["last"]), _ptr(dL_dout), _ptr(workspace), workspace.numel(), _ptr(grads["means"]),
         _ptr(grads["log_scales"]), _ptr(grads["quats"]), _ptr(grads["opacity_logits"]),
         _ptr(grads["sh"]), _ptr(grads.get("means2d")), 1 if accumulate else 0,
@@ -356,4 +383,4 @@ def timing_read(kernel):
 __all__ = ["AbcdError", "project", "bin_sort", "bin_sort_workspace_size", "render_fwd",
            "render_bwd", "render_bwd_workspace_size", "composite_cache", "loss_l1_grad",
            "timing_enable", "timing_reset", "timing_read", "version", "n_tiles", "adam_step",
-           "render_cache", "stage_cached", "make_split", "split_workspace_size"]
+           "render_cache", "stage_cached", "make_split", "split_workspace_size", "intersections"]

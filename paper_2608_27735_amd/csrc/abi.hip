@@ -75,8 +75,11 @@ int32_t check_camera(const abcd_camera* c) {
           ABCD_MAX_TILES);
   REQUIRE(std::isfinite(c->fx) && std::isfinite(c->fy) && c->fx > 0 && c->fy > 0,
           "focal lengths must be positive and finite");
-  REQUIRE(std::isfinite(c->cx) && std::isfinite(c->cy) && std::isfinite(c->near_plane),
-          "principal point and near plane must be finite");
+  REQUIRE(std::isfinite(c->cx) && std::isfinite(c->cy), "principal point must be finite");
+  // depth keys are fp32 bit patterns, which order as unsigned integers only
+  // for positive depths
+  REQUIRE(std::isfinite(c->near_plane) && c->near_plane > 0.0f,
+          "near_plane must be positive and finite");
   for (int i = 0; i < 9; ++i) REQUIRE(std::isfinite(c->R[i]), "R must be finite");
   for (int i = 0; i < 3; ++i)
     REQUIRE(std::isfinite(c->t[i]) && std::isfinite(c->campos[i]), "t and campos must be finite");
@@ -226,6 +229,8 @@ int32_t abcd_render_fwd(const abcd_camera* cam, const abcd_raster_params* prm,
   SplitLayout sl;
   TRY(check_split(split, &sl));
   REQUIRE(tile_ranges && out_rgba && final_T && last, "tile_ranges or an output is NULL");
+  REQUIRE(values_sorted && means2d && conic_opacity && rgb,
+          "values_sorted, means2d, conic_opacity or rgb is NULL");
   REQUIRE((reinterpret_cast<uintptr_t>(out_rgba) & 15) == 0 &&
               (reinterpret_cast<uintptr_t>(F) & 15) == 0 &&
               (reinterpret_cast<uintptr_t>(B) & 15) == 0 &&
@@ -244,6 +249,8 @@ int32_t abcd_render_cache(const abcd_camera* cam, const abcd_raster_params* prm,
   TRY(check_camera(cam));
   TRY(check_params(prm));
   REQUIRE(tile_ranges && image_f16, "tile_ranges or image_f16 is NULL");
+  REQUIRE(values_sorted && means2d && conic_opacity && rgb,
+          "values_sorted, means2d, conic_opacity or rgb is NULL");
   REQUIRE((reinterpret_cast<uintptr_t>(image_f16) & 7) == 0 &&
               (reinterpret_cast<uintptr_t>(conic_opacity) & 15) == 0 &&
               (reinterpret_cast<uintptr_t>(means2d) & 7) == 0,
@@ -284,6 +291,7 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
   TRY(check_split(split, &sl));
   TRY(check_n(n));
   REQUIRE(tile_ranges && final_T && last && dL_dout, "tile_ranges, final_T, last or dL_dout is NULL");
+  REQUIRE(n == 0 || values_sorted, "values_sorted is NULL");
   REQUIRE((reinterpret_cast<uintptr_t>(dL_dout) & 15) == 0 &&
               (reinterpret_cast<uintptr_t>(F) & 15) == 0 &&
               (reinterpret_cast<uintptr_t>(B) & 15) == 0,

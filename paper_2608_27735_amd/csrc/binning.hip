@@ -25,7 +25,9 @@
 //   depth_keys, radix x4   depth order of the n Gaussians
 //   l1_count               per chunk of 1024 ranks: block counts; total M
 //   l1_scan_columns        exclusive prefix of the chunk counts per block
-//   l1_finish              bucket offsets, sub-chunk table, overflow flag
+//   l1_finish              bucket offsets, sub-chunk table, overflow flag (on
+//                          overflow nothing is counted or placed: every tile
+//                          range comes out empty)
 //   l1_scatter             (block, Gaussian) pairs, bucket-major, depth order
 //   l2_count               per sub-chunk: counts of its block's 64 tiles
 //   l2_scan                exclusive prefix of the sub-chunk counts per tile
@@ -682,8 +684,9 @@ __global__ __launch_bounds__(1024) void l2_scan_kernel(uint32_t* __restrict__ c2
 __global__ __launch_bounds__(kScanThreads) void bin_scan_tiles_kernel(
     const uint32_t* __restrict__ tile_total, int ntiles, uint32_t* __restrict__ tile_off,
     uint32_t* __restrict__ tile_ranges, const WsHeader* __restrict__ hdr) {
+  // on overflow every tile total is 0 (no sub-chunk was counted), so the
+  // ranges written are all empty and the blend kernels render nothing
   __shared__ unsigned long long part[kScanThreads];
-  if (hdr->overflow) return;
   const int per = (ntiles + kScanThreads - 1) / kScanThreads;
   const int lo = min(ntiles, per * (int)threadIdx.x), hi = min(ntiles, lo + per);
   unsigned long long s = 0;
@@ -907,10 +910,10 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
               sub_off, blk_off, c2, tile_off, hdr, values_sorted,
               reinterpret_cast<unsigned long long*>(keys_sorted));
   ABCD_HIP(hipGetLastError());
-  // forward schedule: heaviest lists first (nothing is written on overflow)
+  // forward schedule: heaviest lists first (on overflow every total is 0,
+  // which gives the identity order)
   if (tile_order)
-    TRY_STATUS(launch_tile_order(ntiles, tile_total, tile_order, &hdr->overflow, "bin_tile_order",
-                                 stream));
+    TRY_STATUS(launch_tile_order(ntiles, tile_total, tile_order, nullptr, "bin_tile_order", stream));
   return ABCD_OK;
 }
 

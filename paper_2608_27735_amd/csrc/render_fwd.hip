@@ -91,7 +91,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
   __shared__ uint32_t s_base;
   __shared__ uint32_t s_walk;  // largest walk of the tile (split only)
   const int tile = tile_of_block(k, order);
-  if (tile >= k.ntiles) return;
+  if ((unsigned)tile >= (unsigned)k.ntiles) return;
   const int tid = threadIdx.x;
   const int px = (tile % k.ntx) * kTile + (tid & 15);
   const int py = (tile / k.ntx) * kTile + (tid >> 4);
@@ -214,7 +214,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
           const bool valid = j0 + i < wcnt;  // past the list: a no-op step
           const AlphaEval ae = eval_alpha(fx - ga[i].x, fy - ga[i].y, ga[i].z, ga[i].w, gb[i].x,
                                           gb[i].y, k.alpha_min, k.alpha_max);
-          const float Tn = T * (1.0f - ae.alpha);
+          // T (1 - alpha) with one rounding
+          const float Tn = fmaf(-T, ae.alpha, T);
           const bool hit = valid && !done && !ae.skip;
           const bool stop = hit && Tn < thr;
           const bool blend = hit && !stop;

@@ -36,7 +36,7 @@ class ActiveBlockStep:
         self.n_blends = torch.zeros((1,), dtype=torch.int64, device=dev)
         self.bwd_ws = torch.empty(max(api.render_bwd_workspace_size(n), 256), dtype=torch.uint8,
                                   device=dev)
-        self.tile_ranges = torch.empty((api.n_tiles(W, H), 2), dtype=torch.int32, device=dev)
+        self.tile_ranges = torch.zeros((api.n_tiles(W, H), 2), dtype=torch.int32, device=dev)
         self.tile_order = torch.empty((api.n_tiles(W, H),), dtype=torch.int32, device=dev)
         self.grads = {k: torch.zeros_like(params[k]) for k in
                       ("means", "log_scales", "quats", "opacity_logits", "sh")}
@@ -78,6 +78,13 @@ class ActiveBlockStep:
                 self.split = api.make_split(self._split_slots(self.capacity, chunk), chunk,
                                             self.values.device)
         return b["n_isect"]
+
+    def overflowed(self):
+        """Whether the last binning found more intersections than the capacity
+        (reads the count back, so it synchronises). Such a step rendered the
+        active block as empty (every tile range is empty) and its gradients
+        are zero; call project_and_bin(sync=True) to grow the buffers."""
+        return api.intersections(self.bin_ws) > self.capacity
 
     def forward(self, F=None, B=None):
         return api.render_fwd(self.cam, self.prm, self.bins, self.proj, F=F, B=B,
@@ -122,6 +129,8 @@ class ActiveBlockStep:
         return graph
 
     def replay(self):
-        """Launch the captured step on the current stream."""
+        """Launch the captured step on the current stream (check overflowed()
+        when the parameters or the camera may have grown the intersection
+        count past the capacity)."""
         self.graph.replay()
         return self.grads

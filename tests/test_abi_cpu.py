@@ -81,6 +81,8 @@ FAKE = 0x1000  # never dereferenced: every call below fails validation first
     lambda c, p: setattr(c, "width", 0),
     lambda c, p: setattr(c, "fx", -1.0),
     lambda c, p: setattr(c, "fx", float("nan")),
+    lambda c, p: setattr(c, "near_plane", 0.0),   # depth keys need positive depths
+    lambda c, p: setattr(c, "near_plane", -0.5),
     lambda c, p: setattr(p, "sh_degree", 4),
     lambda c, p: setattr(p, "alpha_max", 1.0),
     lambda c, p: setattr(p, "flags", 2),  # unknown flag bit
@@ -175,6 +177,22 @@ def test_render_calls_reject_bad_arguments(lib):
     bwd = [FAKE] * 16 + [FAKE, 8] + [FAKE] * 6 + [0, None, None]  # workspace too small
     assert lib.abcd_render_bwd(C.byref(c), C.byref(p), 10, *bwd) == 1
     assert lib.abcd_loss_l1_grad(0, 8, FAKE, FAKE, None, FAKE, None, None) == 1
+
+
+@pytest.mark.parametrize("which", [2, 3, 4, 5])  # values_sorted, means2d, conic_opacity, rgb
+def test_blend_inputs_may_not_be_null(lib, which):
+    """A NULL list or splat array with non-empty tile ranges would fault the
+    GPU; both blend entry points reject it on the host instead."""
+    c, p = _cam(), _prm()
+    args = [FAKE] * 12
+    args[which] = None
+    assert lib.abcd_render_fwd(C.byref(c), C.byref(p), *args, None, None) == 1
+    cache = [FAKE] * 7 + [None]
+    cache[which] = None
+    assert lib.abcd_render_cache(C.byref(c), C.byref(p), *cache, None) == 1
+    bwd = [FAKE] * 16 + [FAKE, 1 << 30] + [FAKE] * 6 + [0, None, None]
+    bwd[10] = None  # values_sorted of the backward
+    assert lib.abcd_render_bwd(C.byref(c), C.byref(p), 10, *bwd) == 1
 
 
 def test_split_workspace_and_rejections(lib):

@@ -3,18 +3,19 @@
 buffers):
   - the 1M-Gaussian active block (SH degree 3) at 1297x840 the bench measures,
     with uniform scales and with heavy-tailed scales;
+  - the same block at 1920x1080, uniform and heavy-tailed (the large-block
+    configuration);
   - the mid-scale scene's 300K-Gaussian active block at 1297x840 (ground plane
     and blobs);
   - the stress configuration's 4M-Gaussian active block of tiny Gaussians at
     2560x1440.
 
-The oracle cannot rasterise these frames in seconds, so it is run on
-sampled outputs it can compute on its own:
+The oracle bins every workload whole; it cannot rasterise these frames in
+seconds, so the images and gradients are checked on sampled outputs it can
+compute on its own:
   - projection: the binning fields of all Gaussians, bit-exact;
-  - binning: M and every tile's list length, bit-exact; the full depth-ordered
-    lists of the sampled tiles, bit-exact (the oracle bins the subset of
-    Gaussians whose rectangle meets a sampled tile, which leaves those tiles'
-    lists complete and in the same (depth, index) order);
+  - binning: M, every tile range, the whole sorted value list and the whole
+    sorted key list, bit-exact against the oracle's binning of all Gaussians;
   - forward: every pixel of the sampled tiles, max abs <= 1e-5 off the
     knife-edge pixels, `last` bit-exact there;
   - backward: with dL/dout zero outside the sampled tiles, every parameter
@@ -34,22 +35,24 @@ pytestmark = pytest.mark.gpu
 
 FWD_TOL = 1e-5
 GRAD_TOL = 1e-4
-# Knife-edge margin on threshold decisions, per workload. A pixel of the
-# heaviest tiles makes ~10^4 skip decisions, so the 1e-4 margin of the small
-# cases flags a few percent of them; fp32 alpha is within ~1e-6 (relative) of
-# fp64 (the conic comes from fp64 arithmetic) and the transmittance after
-# 10^4 products within ~1e-5 (random walk of 0.5-ulp roundings), so 3e-5
-# still covers every decision the two precisions could take differently.
-# With heavy-tailed scales a pixel blends up to ~4,000 entries of alpha near
-# alpha_min, whose factors 1 - alpha round alike, so the fp32 transmittance
-# drifts by up to ~1e-4 from fp64 (measured: 3e-5 leaves decisions that
-# differ): that workload takes the 1e-4 margin of the small cases, which
-# flags about 9% of its sampled pixels.
-WORKLOADS = {  # name: (generator, knife margin, largest knife-edge fraction)
-    "1m-uniform-1297x840": (lambda: S.active_block_1m(), 3e-5, 0.02),
-    "1m-heavy-tail-1297x840": (lambda: S.active_block_1m(heavy_tail=True), 1e-4, 0.12),
-    "300k-midscale-1297x840": (lambda: S.midscale_block(), 3e-5, 0.02),
-    "4m-stress-2560x1440": (lambda: S.stress_block(), 3e-5, 0.02),
+# Knife-edge pixels: a threshold decision within the error the fp32 kernels
+# can make on it. Alpha decisions take a relative 2e-6 (exp2 and opacity
+# rounding) plus 8 x 2^-24 times the magnitude of the terms of the quadratic
+# form in Cholesky form (the two products of its first square cancel for long
+# thin splats far along their major axis; the oracle pin against an fp32
+# emulation finds the actual error within 1/8 of that bound); the stop
+# decision takes the accumulated bound of the transmittance. At most 2 % of
+# the sampled pixels of any workload may be knife-edge.
+KNIFE_REL = 2e-6
+KNIFE_KAPPA = 8.0
+KNIFE_FRAC = 0.02
+WORKLOADS = {
+    "1m-uniform-1297x840": lambda: S.active_block_1m(),
+    "1m-heavy-tail-1297x840": lambda: S.active_block_1m(heavy_tail=True),
+    "1m-uniform-1920x1080": lambda: S.active_block_1m(width=1920, height=1080),
+    "1m-heavy-tail-1920x1080": lambda: S.active_block_1m(width=1920, height=1080, heavy_tail=True),
+    "300k-midscale-1297x840": lambda: S.midscale_block(),
+    "4m-stress-2560x1440": lambda: S.stress_block(),
 }
 
 
@@ -64,8 +67,7 @@ def full(request):
     from paper_2608_27735_amd.step import ActiveBlockStep
     dev = torch.device("cuda:0")
     say("large workload", request.param)
-    gen, knife, knife_frac = WORKLOADS[request.param]
-    w = gen()
+    w = WORKLOADS[request.param]()
     cam, prm, scene = w.cam, w.params, w.scene
     r = S.rng(5)
     F, B = S.background_pair(r, cam.height, cam.width)
@@ -78,7 +80,7 @@ def full(request):
     pb = O.project_bin(cam, prm, scene["means"], scene["log_scales"], scene["quats"],
                        scene["opacity_logits"])
     yield dict(api=api, st=st, cam=cam, prm=prm, scene=scene, F=F, B=B, Fd=Fd, Bd=Bd, r=r,
-               pb=pb, name=request.param, knife=knife, knife_frac=knife_frac)
+               pb=pb, name=request.param)
     del st, params
     torch.cuda.empty_cache()
 
@@ -160,15 +162,24 @@ def test_fullsize_projection_and_binning(full):
     assert int(tr[-1, 1]) == m
     assert np.array_equal(tr[:, 1] - tr[:, 0], count)
     assert np.array_equal(tr[1:, 0], tr[:-1, 1]) and tr[0, 0] == 0
-    # full lists of the sampled tiles
-    tiles = _sampled_tiles(full)
-    _, idx, vals, ranges = _oracle_subset(full, tiles)
-    values = st.values.cpu().numpy().view(np.uint32)
-    for t in tiles:
-        got = values[tr[t, 0]:tr[t, 1]]
-        ref = idx[vals[ranges[t, 0]:ranges[t, 1]]]
-        assert np.array_equal(got, ref.astype(np.uint32)), t
-    print(f"  M = {m}, {len(tiles)} sampled tile lists bit-exact")
+    # the whole sorted lists and keys against the oracle's binning of every
+    # Gaussian
+    say("whole lists and keys", full["name"], "M =", m)
+    keys_o, vals_o, ranges_o = O.bin(cam.width, cam.height, pb["depth"], pb["rect"],
+                                     pb["tiles_touched"])
+    assert len(vals_o) == m
+    assert np.array_equal(tr.astype(np.uint32), ranges_o)
+    values = st.values[:m].cpu().numpy().view(np.uint32)
+    assert np.array_equal(values, vals_o)
+    del values
+    api = full["api"]
+    kb = api.bin_sort(cam.width, cam.height, st.proj, capacity=m, want_keys=True, sync=True)
+    assert kb["n_isect"] == m
+    keys = kb["keys"][:m].cpu().numpy().view(np.uint64)
+    del kb
+    torch.cuda.empty_cache()
+    assert np.array_equal(keys, keys_o)
+    print(f"  M = {m}: every tile range, value and key bit-exact")
 
 
 def _subset_values(full, pb, idx):
@@ -192,7 +203,7 @@ def test_fullsize_forward_on_sampled_tiles(full):
     pb, idx, vals, ranges = _oracle_subset(full, tiles)
     m2d, pv = _subset_values(full, pb, idx)
     ref = O.render_fwd(cam, prm, _only(ranges, tiles), vals, m2d, pv["conic"], pv["opacity"],
-                       pv["rgb"], full["F"], full["B"], rel_margin=full["knife"])
+                       pv["rgb"], full["F"], full["B"], rel_margin=KNIFE_REL, f32_kappa=KNIFE_KAPPA)
     out = st.fwd["out"].cpu().numpy()
     last = st.fwd["last"].cpu().numpy().view(np.uint32)
     ntx, _ = _tiles(cam)
@@ -209,7 +220,7 @@ def test_fullsize_forward_on_sampled_tiles(full):
         npx += kn.size
     print(f"  {len(tiles)} tiles, max err {worst:.2e}, knife-edge pixels {knives} of {npx}")
     assert worst <= FWD_TOL
-    assert knives <= max(8, full["knife_frac"] * npx)
+    assert knives <= max(8, KNIFE_FRAC * npx)
 
 
 def test_fullsize_binning_box_changes_no_image(full):
@@ -221,7 +232,7 @@ def test_fullsize_binning_box_changes_no_image(full):
     pb, idx, vals, ranges = _oracle_subset(full, tiles, square=True)
     m2d, pv = _subset_values(full, pb, idx)
     ref = O.render_fwd(cam, prm, _only(ranges, tiles), vals, m2d, pv["conic"], pv["opacity"],
-                       pv["rgb"], full["F"], full["B"], rel_margin=full["knife"])
+                       pv["rgb"], full["F"], full["B"], rel_margin=KNIFE_REL, f32_kappa=KNIFE_KAPPA)
     out = st.fwd["out"].cpu().numpy()
     ntx, _ = _tiles(cam)
     worst, knives, npx = 0.0, 0, 0
@@ -235,7 +246,7 @@ def test_fullsize_binning_box_changes_no_image(full):
         npx += kn.size
     print(f"  {len(tiles)} tiles, max err {worst:.2e}, knife-edge pixels {knives} of {npx}")
     assert worst <= FWD_TOL
-    assert knives <= max(8, full["knife_frac"] * npx)
+    assert knives <= max(8, KNIFE_FRAC * npx)
 
 
 def test_fullsize_backward_from_sampled_tiles(full):
@@ -246,7 +257,7 @@ def test_fullsize_backward_from_sampled_tiles(full):
     m2d, pv = _subset_values(full, pb, idx)
     rsub = _only(ranges, tiles)
     ref = O.render_fwd(cam, prm, rsub, vals, m2d, pv["conic"], pv["opacity"], pv["rgb"], full["F"],
-                       full["B"], rel_margin=full["knife"])
+                       full["B"], rel_margin=KNIFE_REL, f32_kappa=KNIFE_KAPPA)
     ntx, _ = _tiles(cam)
     mask = np.zeros((cam.height, cam.width), bool)
     for t in tiles:

@@ -576,7 +576,9 @@ def test_edge_cases_empty_block_and_culled(api):
         assert not torch.any(v != 0)
 
 
-def test_capacity_overflow_leaves_outputs_untouched(api):
+def test_capacity_overflow_writes_empty_ranges_only(api):
+    """On overflow the lists are not written, every tile range is empty and
+    the tile order is the identity, so the blend kernels read no entry."""
     from paper_2608_27735_amd._lib import AbcdError
     w = S.tiny()
     cam, prm = w.cams[0], w.params
@@ -591,7 +593,43 @@ def test_capacity_overflow_leaves_outputs_untouched(api):
         _raw_bin(api, cam, p, m - 1, values, ranges, order)
     assert e.value.status == 2
     torch.cuda.synchronize()
-    assert torch.all(values == -7) and torch.all(ranges == -7) and torch.all(order == -7)
+    assert torch.all(values == -7)
+    assert torch.all(ranges == 0)
+    assert np.array_equal(np32(order), np.arange(api.n_tiles(cam.width, cam.height)))
+
+
+def test_step_overflow_is_flagged_and_renders_no_stale_list(api):
+    """A step whose intersections outgrow the capacity it was sized for (no
+    synchronisation inside the step) renders the active block as empty, not
+    the previous call's lists, and overflowed() reports it."""
+    from paper_2608_27735_amd.step import ActiveBlockStep
+    w = S.tiny()
+    cam, prm = w.cams[0], w.params
+    act = S.subset(w.scene, w.cell_of == w.active)
+    r = S.rng(71)
+    F, B = S.background_pair(r, cam.height, cam.width)
+    Fd, Bd = torch.from_numpy(F).to(dev()), torch.from_numpy(B).to(dev())
+    params = to_dev(act)
+    say("step overflow", len(act["means"]))
+    st = ActiveBlockStep(cam, prm, params, headroom=1.0)  # capacity = M + 1024
+    st.project_and_bin(sync=False)
+    st.forward(Fd, Bd)
+    torch.cuda.synchronize()
+    assert not st.overflowed()
+    assert int(st.n_blends.item()) > 0
+    # grow every Gaussian 8x: many more intersections than the capacity
+    params["log_scales"] += math.log(8.0)
+    st.n_blends.zero_()
+    target = torch.from_numpy(w.target).to(dev())
+    grads = st.step(target, F=Fd, B=Bd)
+    torch.cuda.synchronize()
+    assert st.overflowed()
+    assert int(st.n_blends.item()) == 0
+    assert torch.all(st.tile_ranges == 0)
+    exp = F.astype(np.float64) + (1 - F[..., 3:]) * B
+    assert np.abs(np32(st.fwd["out"]) - exp).max() <= FWD_TOL
+    for v in grads.values():
+        assert not torch.any(v != 0)
 
 
 def _raw_bin(api, cam, p, capacity, values, ranges, order):

@@ -483,6 +483,90 @@ def test_alpha_clamp_and_skip_thresholds():
     assert np.all(fw["last"] == 1)
 
 
+def _fp32_alpha(px, py, mean32, conic, o):
+    """Alpha at pixel (px, py) evaluated the way a fp32 rasteriser does: the
+    conic's Cholesky factor rounded to fp32 and pre-scaled by sqrt(log2(e) / 2),
+    offsets in fp32, q as a sum of two squares with fused multiply-adds, 2^(-q)
+    rounded once, times the fp32 opacity. An emulation written here, not the
+    oracle's arithmetic."""
+    f = np.float32
+    a, b, c = conic
+    l11 = math.sqrt(a)
+    l21 = b / l11
+    l22 = math.sqrt(max(c - l21 * l21, 0.0))
+    k = f(math.sqrt(math.log2(math.e) / 2))
+    qa, qb, qc = k * f(l11), k * f(l21), k * f(l22)
+    dx, dy = f(px + 0.5) - f(mean32[0]), f(py + 0.5) - f(mean32[1])
+
+    def fma(x, y, z):
+        return f(float(x) * float(y) + float(z))
+
+    e1 = fma(qa, dx, f(qb * dy))
+    e2 = f(qc * dy)
+    p2 = -fma(e1, e1, f(e2 * e2))
+    return f(f(o) * f(2.0 ** float(p2)))
+
+
+def test_fp32_knife_margin_covers_every_fp32_alpha_decision():
+    """With f32_kappa > 0 the oracle flags a pixel when an alpha decision lies
+    within a bound of the fp32 evaluation's error. Splats placed so that one
+    pixel sees alpha within +-1.5e-5 (relative) of alpha_min or alpha_max, with
+    axis ratios up to 60:1 at every orientation and offsets of up to 200 px
+    along the major axis (the cancellation the bound grows with): wherever the
+    emulated fp32 decision differs from the fp64 one, the pixel is flagged,
+    and the bound is not vacuous (pixels with alpha 1e-3 away from both
+    thresholds are not flagged)."""
+    r = S.rng(2024)
+    cam = axis_camera(16, 16)
+    prm = RasterParams()
+    flips = flagged_flips = clear = clear_flagged = 0
+    for case in range(2000):
+        ang = r.uniform(0, math.pi)
+        s_major = r.uniform(3.0, 120.0)
+        s_minor = s_major / r.uniform(1.0, 60.0)
+        cs, sn = math.cos(ang), math.sin(ang)
+        Rm = np.array([[cs, -sn], [sn, cs]])
+        cov = Rm @ np.diag([s_major ** 2, s_minor ** 2]) @ Rm.T
+        conic = np.linalg.inv(cov)
+        conic = (conic[0, 0], conic[0, 1], conic[1, 1])
+        o = float(np.float32(r.uniform(0.05, 1.0)))
+        near_max = case % 4 == 3
+        far = case % 5 == 4
+        rel = r.uniform(1e-3, 2e-3) * r.choice([-1, 1]) if far else r.uniform(-1.5e-5, 1.5e-5)
+        target = (prm.alpha_max if near_max else prm.alpha_min) * (1 + rel)
+        if target >= o:
+            continue
+        q = 2 * math.log(o / target)
+        # direction: mostly along the major axis (long offsets), some at random
+        th = ang + (r.normal(0, 0.02) if case % 2 else r.uniform(0, math.pi))
+        u = np.array([math.cos(th), math.sin(th)])
+        Q = np.array([[conic[0], conic[1]], [conic[1], conic[2]]])
+        dist = math.sqrt(q / (u @ Q @ u))
+        if dist > 200:
+            continue
+        px, py = 7, 9
+        mean32 = np.array([px + 0.5, py + 0.5] - dist * u, np.float32)
+        ranges, values, m2d, co, op, rgb = _splat_inputs(cam, [mean32.astype(np.float64)], [conic],
+                                                         [o], [[0.5, 0.5, 0.5]])
+        fw = O.render_fwd(cam, prm, ranges, values, m2d, co, op, rgb, rel_margin=2e-6,
+                          f32_kappa=8.0)
+        dx, dy = px + 0.5 - float(mean32[0]), py + 0.5 - float(mean32[1])
+        power = -0.5 * (conic[0] * dx * dx + conic[2] * dy * dy) - conic[1] * dx * dy
+        araw64 = o * math.exp(power)
+        a32 = float(_fp32_alpha(px, py, mean32, conic, o))
+        thr = prm.alpha_max if near_max else prm.alpha_min
+        flip = (araw64 >= thr) != (a32 >= np.float32(thr))
+        if flip:
+            flips += 1
+            flagged_flips += int(fw["knife"][py, px])
+        if far:
+            clear += 1
+            clear_flagged += int(fw["knife"][py, px])
+    assert flips >= 5, flips                       # the cases do reach the knife edge
+    assert flagged_flips == flips, (flagged_flips, flips)
+    assert clear >= 50 and clear_flagged == 0, (clear, clear_flagged)
+
+
 def test_reductions_transparent_and_empty_and_opaque_front():
     r = S.rng(11)
     cam = look_at((0, -3.5, 1.0), (0, 0, 0), 48, 32)
