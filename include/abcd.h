@@ -282,6 +282,39 @@ ABCD_API int32_t abcd_render_bwd(const abcd_camera* cam /* host */, const abcd_r
                         hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* Allocation-free backward, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): abcd_render_bwd without the workspace arguments, same outputs.
+ * Its scratch (screen-space gradients and the backward's work schedule) is a
+ * static device array of ABCD_NOALLOC_SCRATCH_BYTES inside the library; each
+ * GPU the library runs on holds its own copy until the process ends. n may be
+ * at most ABCD_NOALLOC_MAX_GAUSSIANS; a larger n returns ABCD_E_INVALID with
+ * nothing enqueued. The call allocates nothing: no hipMalloc, no hipFree, no
+ * allocating library routine (its first call on a device looks up that
+ * device's copy of the array, with hipGetSymbolAddress, and keeps the
+ * address). The calling thread's current device must be the one of `stream`.
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * contents; each call clears what must start at zero itself (with a fill
+ * kernel, no memset node). Calls that overlap on one GPU (on other streams or
+ * threads) race on the array and give wrong gradients: serialise them. */
+#define ABCD_NOALLOC_MAX_GAUSSIANS (1LL << 20)
+#define ABCD_NOALLOC_SCRATCH_BYTES 38275072ULL /* workspace of 2^20 Gaussians */
+ABCD_API int32_t abcd_render_bwd_noalloc(const abcd_camera* cam /* host */,
+                                         const abcd_raster_params* prm /* host */, int64_t n,
+                                         const float* means, const float* log_scales,
+                                         const float* quats, const float* opacity_logits,
+                                         const float* sh, const float* means2d,
+                                         const float* conic_opacity, const float* rgb,
+                                         const float* extent, const uint32_t* tile_ranges,
+                                         const uint32_t* values_sorted, const float* F,
+                                         const float* B, const float* final_T,
+                                         const uint32_t* last, const float* dL_dout,
+                                         float* d_means, float* d_log_scales, float* d_quats,
+                                         float* d_opacity_logits, float* d_sh, float* d_means2d,
+                                         int32_t accumulate, const abcd_split* split,
+                                         hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Collapse of cached partition renders into F and B (Abstract; Method section:
  * the stored renders of the frozen partitions are merged, front to back in
  * their depth order, into the two layers).

@@ -12,6 +12,7 @@ LIB_PATH = os.path.join(HERE, "libabcd.so")
 ABCD_OK, ABCD_E_INVALID, ABCD_E_CAPACITY, ABCD_E_OVERFLOW, ABCD_E_HIP = 0, 1, 2, 3, 4
 TILE = 16
 MAX_TILES = 32768
+NOALLOC_MAX_GAUSSIANS = 1 << 20  # ABCD_NOALLOC_MAX_GAUSSIANS
 
 
 class abcd_camera(C.Structure):
@@ -55,6 +56,8 @@ SIGNATURES = {
     "abcd_render_bwd_workspace_size": (_I32, [_I64, C.POINTER(_SZ)]),
     "abcd_render_bwd": (_I32, [_CAM, _PRM, _I64] + [_P] * 5 + [_P] * 4 + [_P] * 2 + [_P] * 5 +
                         [_P, _SZ] + [_P] * 6 + [_I32, C.POINTER(abcd_split), _P]),
+    "abcd_render_bwd_noalloc": (_I32, [_CAM, _PRM, _I64] + [_P] * 5 + [_P] * 4 + [_P] * 2 +
+                                [_P] * 5 + [_P] * 6 + [_I32, C.POINTER(abcd_split), _P]),
     "abcd_composite_cache": (_I32, [_I32, _I32, _I32, _P, C.POINTER(C.c_int32), _I32, _P,
                                     C.c_float, _P, _P, _I32, _P]),
     "abcd_stage_cached": (_I32, [_I32, _I32, _I32, C.POINTER(_P), C.POINTER(C.c_int32), _P,

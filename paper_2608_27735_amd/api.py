@@ -270,6 +270,36 @@ def render_bwd(cam, prm, params, proj, bins, fwd, dL_dout, F=None, B=None, works
     return grads
 
 
+def render_bwd_noalloc(cam, prm, params, proj, bins, fwd, dL_dout, F=None, B=None, grads=None,
+                       accumulate=False, want_means2d=False, split=None):
+    """render_bwd through abcd_render_bwd_noalloc: no workspace, the library's
+    static per-GPU scratch instead (n <= NOALLOC_MAX_GAUSSIANS; calls that
+    overlap on one GPU race). `grads` should be preallocated by callers that
+    must not allocate."""
+    n = params["means"].shape[0]
+    H, W = cam.height, cam.width
+    dev = params["means"].device
+    _need(dL_dout, "dL_dout", torch.float32, (H, W, 4))
+    _opt(F, "F", torch.float32, (H, W, 4))
+    _opt(B, "B", torch.float32, (H, W, 4))
+    if grads is None:
+        grads = {k: torch.zeros_like(params[k]) for k in
+                 ("means", "log_scales", "quats", "opacity_logits", "sh")}
+        if want_means2d:
+            grads["means2d"] = torch.zeros((n, 2), dtype=torch.float32, device=dev)
+    check(_lib.load().abcd_render_bwd_noalloc(
+        C.byref(_lib.camera_struct(cam)), C.byref(_lib.params_struct(prm)), n,
+        _ptr(params["means"]), _ptr(params["log_scales"]), _ptr(params["quats"]),
+        _ptr(params["opacity_logits"]), _ptr(params["sh"]), _ptr(proj["means2d"]),
+        _ptr(proj["conic_opacity"]), _ptr(proj["rgb"]), _ptr(proj["extent"]),
+        _ptr(bins["tile_ranges"]), _ptr_nz(bins["values"], dev), _ptr(F), _ptr(B),
+        _ptr(fwd["final_T"]), _ptr(fwd["last"]), _ptr(dL_dout), _ptr(grads["means"]),
+        _ptr(grads["log_scales"]), _ptr(grads["quats"]), _ptr(grads["opacity_logits"]),
+        _ptr(grads["sh"]), _ptr(grads.get("means2d")), 1 if accumulate else 0,
+        _split_struct(split), _stream()))
+    return grads
+
+
 # --------------------------------------------------------------- optimizer
 
 PARAM_GROUPS = ("means", "log_scales", "quats", "opacity_logits", "sh")
@@ -383,4 +413,5 @@ def timing_read(kernel):
 __all__ = ["AbcdError", "project", "bin_sort", "bin_sort_workspace_size", "render_fwd",
            "render_bwd", "render_bwd_workspace_size", "composite_cache", "loss_l1_grad",
            "timing_enable", "timing_reset", "timing_read", "version", "n_tiles", "adam_step",
-           "render_cache", "stage_cached", "make_split", "split_workspace_size", "intersections"]
+           "render_cache", "stage_cached", "make_split", "split_workspace_size", "intersections",
+           "render_bwd_noalloc"]

@@ -275,6 +275,16 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
                         uint32_t* tile_ranges, uint32_t* tile_order, hipStream_t stream);
 
 // render_fwd.hip, render_bwd.hip, loss.hip
+// The backward's workspace: g2d[n][9] fp32 (256-byte aligned), then per tile
+// the work estimate, the order and the work items (when not split), then the
+// queue counters.
+constexpr size_t bwd_g2d_bytes(int64_t n) {
+  return ((size_t)9 * sizeof(float) * (size_t)n + 255) & ~size_t(255);
+}
+constexpr size_t bwd_workspace_bytes(int64_t n) {
+  return bwd_g2d_bytes(n) + 2 * sizeof(uint32_t) * ABCD_MAX_TILES + 8 * (size_t)ABCD_MAX_TILES +
+         sizeof(uint32_t) * 64 * 8;
+}
 size_t render_bwd_workspace_bytes(int64_t n);
 int32_t launch_render_fwd(const abcd_camera& cam, const abcd_raster_params& prm,
                           const uint32_t* tile_ranges, const uint32_t* values_sorted,

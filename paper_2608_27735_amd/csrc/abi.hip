@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -123,6 +124,40 @@ int32_t check_n(int64_t n) {
     int32_t st_ = (x);            \
     if (st_ != ABCD_OK) return st_; \
   } while (0)
+
+// Scratch of abcd_render_bwd_noalloc: the backward's workspace for up to
+// ABCD_NOALLOC_MAX_GAUSSIANS Gaussians, as a static device array. Each GPU
+// the library runs on holds its own copy at its own address until the process
+// ends. In host code `scratch` names a host-side stand-in, not device memory:
+// only the address hipGetSymbolAddress returns for the current device may be
+// passed to kernels or copies.
+constexpr size_t kNoAllocScratchBytes = bwd_workspace_bytes(ABCD_NOALLOC_MAX_GAUSSIANS);
+static_assert(kNoAllocScratchBytes == ABCD_NOALLOC_SCRATCH_BYTES,
+              "ABCD_NOALLOC_SCRATCH_BYTES states the static scratch size");
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's copy of `scratch`, looked up once per device
+// (with that device current) and kept.
+int32_t noalloc_scratch(void** out) {
+  int dev = -1;
+  ABCD_HIP(hipGetDevice(&dev));
+  REQUIRE(dev >= 0 && dev < kMaxDevices, "device %d beyond the %d the library tracks", dev,
+          kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    ABCD_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    REQUIRE(p != nullptr, "no device address for the static scratch on device %d", dev);
+    REQUIRE((reinterpret_cast<uintptr_t>(p) & 255) == 0, "static scratch is not 256-byte aligned");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ABCD_OK;
+}
 
 }  // namespace
 
@@ -275,7 +310,7 @@ int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes) {
   return ABCD_OK;
 }
 
-int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, int64_t n,
+static int32_t render_bwd_impl(const abcd_camera* cam, const abcd_raster_params* prm, int64_t n,
                         const float* means, const float* log_scales, const float* quats,
                         const float* opacity_logits, const float* sh, const float* means2d,
                         const float* conic_opacity, const float* rgb, const float* extent,
@@ -284,7 +319,7 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
                         const float* dL_dout, void* workspace, size_t ws_bytes, float* d_means,
                         float* d_log_scales, float* d_quats, float* d_opacity_logits, float* d_sh,
                         float* d_means2d, int32_t accumulate, const abcd_split* split,
-                        hipStream_t stream) {
+                        bool noalloc, hipStream_t stream) {
   TRY(check_camera(cam));
   TRY(check_params(prm));
   SplitLayout sl;
@@ -302,9 +337,16 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
                 rgb && extent,
             "input array is NULL");
     REQUIRE(d_means && d_log_scales && d_quats && d_opacity_logits && d_sh, "gradient array is NULL");
-    REQUIRE(workspace != nullptr && (reinterpret_cast<uintptr_t>(workspace) & 255) == 0,
-            "workspace must be non-NULL and 256-byte aligned");
-    REQUIRE(ws_bytes >= need, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+    if (noalloc) {
+      REQUIRE(n <= ABCD_NOALLOC_MAX_GAUSSIANS,
+              "n = %lld exceeds the %lld Gaussians the static scratch of "
+              "abcd_render_bwd_noalloc holds; use abcd_render_bwd with a workspace",
+              (long long)n, (long long)ABCD_NOALLOC_MAX_GAUSSIANS);
+    } else {
+      REQUIRE(workspace != nullptr && (reinterpret_cast<uintptr_t>(workspace) & 255) == 0,
+              "workspace must be non-NULL and 256-byte aligned");
+      REQUIRE(ws_bytes >= need, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+    }
     REQUIRE((reinterpret_cast<uintptr_t>(conic_opacity) & 15) == 0 &&
                 (reinterpret_cast<uintptr_t>(quats) & 15) == 0 &&
                 (reinterpret_cast<uintptr_t>(d_quats) & 15) == 0 &&
@@ -313,6 +355,8 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
   } else {
     return ABCD_OK;
   }
+  // every argument is valid: only now the static scratch's address (a HIP call)
+  if (noalloc) TRY(noalloc_scratch(&workspace));
   float* g2d = static_cast<float*>(workspace);
   TRY(launch_zero(g2d, 9 * n, stream));
   TRY(launch_render_bwd_pixels(*cam, *prm, n, tile_ranges, values_sorted, means2d, conic_opacity,
@@ -320,6 +364,40 @@ int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, i
   return launch_project_bwd(*cam, *prm, n, means, log_scales, quats, opacity_logits, sh, extent,
                             g2d, d_means, d_log_scales, d_quats, d_opacity_logits, d_sh, d_means2d,
                             accumulate, stream);
+}
+
+int32_t abcd_render_bwd(const abcd_camera* cam, const abcd_raster_params* prm, int64_t n,
+                        const float* means, const float* log_scales, const float* quats,
+                        const float* opacity_logits, const float* sh, const float* means2d,
+                        const float* conic_opacity, const float* rgb, const float* extent,
+                        const uint32_t* tile_ranges, const uint32_t* values_sorted,
+                        const float* F, const float* B, const float* final_T, const uint32_t* last,
+                        const float* dL_dout, void* workspace, size_t ws_bytes, float* d_means,
+                        float* d_log_scales, float* d_quats, float* d_opacity_logits, float* d_sh,
+                        float* d_means2d, int32_t accumulate, const abcd_split* split,
+                        hipStream_t stream) {
+  return render_bwd_impl(cam, prm, n, means, log_scales, quats, opacity_logits, sh, means2d,
+                         conic_opacity, rgb, extent, tile_ranges, values_sorted, F, B, final_T,
+                         last, dL_dout, workspace, ws_bytes, d_means, d_log_scales, d_quats,
+                         d_opacity_logits, d_sh, d_means2d, accumulate, split, false, stream);
+}
+
+int32_t abcd_render_bwd_noalloc(const abcd_camera* cam, const abcd_raster_params* prm, int64_t n,
+                                const float* means, const float* log_scales, const float* quats,
+                                const float* opacity_logits, const float* sh,
+                                const float* means2d, const float* conic_opacity,
+                                const float* rgb, const float* extent,
+                                const uint32_t* tile_ranges, const uint32_t* values_sorted,
+                                const float* F, const float* B, const float* final_T,
+                                const uint32_t* last, const float* dL_dout, float* d_means,
+                                float* d_log_scales, float* d_quats, float* d_opacity_logits,
+                                float* d_sh, float* d_means2d, int32_t accumulate,
+                                const abcd_split* split, hipStream_t stream) {
+  return render_bwd_impl(cam, prm, n, means, log_scales, quats, opacity_logits, sh, means2d,
+                         conic_opacity, rgb, extent, tile_ranges, values_sorted, F, B, final_T,
+                         last, dL_dout, nullptr, kNoAllocScratchBytes, d_means, d_log_scales,
+                         d_quats, d_opacity_logits, d_sh, d_means2d, accumulate, split, true,
+                         stream);
 }
 
 int32_t abcd_stage_cached(int32_t width, int32_t height, int32_t k,

@@ -333,16 +333,11 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
 
 }  // namespace
 
-static size_t g2d_bytes(int64_t n) {
-  return ((size_t)9 * sizeof(float) * (size_t)n + 255) & ~size_t(255);
-}
+static_assert(kQueueStride * kQueues == 64 * 8, "queue block of bwd_workspace_bytes");
 
 // g2d[n][9], then the backward's tile work, tile order, work items (when
 // not split) and queue.
-size_t render_bwd_workspace_bytes(int64_t n) {
-  return g2d_bytes(n) + 2 * sizeof(uint32_t) * ABCD_MAX_TILES + sizeof(uint2) * ABCD_MAX_TILES +
-         sizeof(uint32_t) * kQueueStride * kQueues;
-}
+size_t render_bwd_workspace_bytes(int64_t n) { return bwd_workspace_bytes(n); }
 
 namespace {
 // Workgroups of the persistent backward that fit the device at once.
@@ -373,7 +368,7 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
                                  const float* dL_dout, float* g2d, const SplitLayout& split,
                                  hipStream_t stream) {
   const BlendConsts k = consts(cam, prm);
-  char* tail = reinterpret_cast<char*>(g2d) + g2d_bytes(n);
+  char* tail = reinterpret_cast<char*>(g2d) + bwd_g2d_bytes(n);
   uint32_t* work = reinterpret_cast<uint32_t*>(tail);
   uint32_t* order = work + ABCD_MAX_TILES;
   uint2* own_items = reinterpret_cast<uint2*>(order + ABCD_MAX_TILES);

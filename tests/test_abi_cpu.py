@@ -232,3 +232,16 @@ def test_adam_rejects_bad_arguments(lib):
     g[0].grad, g[0].count = FAKE, -1
     assert lib.abcd_adam_step(g, 1, 0.9, 0.999, 1e-15, 1, None) == 1   # count < 0
     assert lib.abcd_adam_step(None, 0, 0.9, 0.999, 1e-15, 1, None) == 0  # nothing to do
+
+
+def test_noalloc_backward_rejects_n_beyond_its_static_scratch(lib):
+    """abcd_render_bwd_noalloc holds at most ABCD_NOALLOC_MAX_GAUSSIANS in its
+    static scratch; a larger n is rejected on the host before any HIP call."""
+    from paper_2608_27735_amd import _lib
+    c, p = _cam(), _prm()
+    args = [FAKE] * 16 + [FAKE] * 6 + [0, None, None]
+    assert lib.abcd_render_bwd_noalloc(C.byref(c), C.byref(p), _lib.NOALLOC_MAX_GAUSSIANS + 1,
+                                       *args) == 1
+    assert "static scratch" in lib.abcd_last_error().decode()
+    args[9] = None  # tile_ranges
+    assert lib.abcd_render_bwd_noalloc(C.byref(c), C.byref(p), 10, *args) == 1
