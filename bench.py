@@ -25,13 +25,18 @@ sys.path.insert(0, ROOT)
 
 METRIC = "Gaussian-pixel blends/sec (fwd+bwd) and ms per active-block step, 1 GPU"
 HBM_PEAK_GBS = 8000.0
-# MI355X fp32 vector peak: 256 CUs x 2.4 GHz x 128 lanes-per-clock with packed FMA x 2 flops
-VALU_PEAK_TFLOPS = 157.3
-# algorithmic flops per evaluated (pixel, Gaussian) pair: alpha of the pair (offset, quadratic
-# form, exp, opacity, tests ~16) and, in the backward, its derivative terms and the sums over
-# the tile's pixels (~45)
+# MI355X vector issue: 256 CUs x 2.4 GHz x one wave64 VALU instruction per CU and clock (four
+# 16-lane SIMDs, four clocks per wave64 instruction) = 39.3 T lane-operations/s; fp32 without
+# packed instructions (which this build switches off) is 78.6 TFLOP/s counting an FMA as two
+VALU_LANE_PEAK_T = 256 * 64 * 2.4e9 / 1e12
+FP32_TFLOPS = 78.6
+# algorithmic flops per evaluated (pixel, Gaussian) pair, an estimate kept as a cross-check:
+# alpha of the pair (offset, quadratic form, exp, opacity, tests ~16) and, in the backward, its
+# derivative terms and the sums over the tile's pixels (~45)
 FLOPS_PER_PAIR = {"render_fwd": 16, "render_bwd": 45}
 PROFILES = os.path.join(ROOT, "profiles")
+HBM_PROFILE = "step_1m_1297x840_hbm_bytes.md"
+SQ_PROFILE = "step_1m_1297x840_sq_counters.md"
 
 KERNELS = ["composite", "project", "depth_keys", "radix_hist", "radix_scan", "radix_scatter",
            "l1_count", "l1_scan_columns", "l1_finish", "l1_scatter", "l2_count", "l2_scan",
@@ -52,6 +57,10 @@ def parse():
     ap.add_argument("--extras", type=int, default=1,
                     help="also time the graph replay, the 128x128 workload, Adam and the cache "
                          "refresh (0: only the step, e.g. under a profiler)")
+    ap.add_argument("--configs", type=int, default=1,
+                    help="also time the other workload configurations (ring scene, mid-scale "
+                         "block over 100 sampled cameras, 1M block at 1920x1080, stress sweep "
+                         "at 2560x1440); 0: skip them")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the steps, copy this many MiB device to device (a plain copy of "
                          "known size that scales the HBM byte counters)")
@@ -75,34 +84,89 @@ def algorithmic_bytes(name, n, n_vis, m, npix, k, sh_coeffs, covered_px=None):
     return None
 
 
-def source_digest(names):
+def library_digest():
+    """Digest of the library's sources (kernels, shared headers, C ABI header):
+    a counter summary taken on other sources no longer describes the kernels."""
+    import glob
     import hashlib
     h = hashlib.sha256()
-    for n in names:
-        with open(os.path.join(ROOT, "paper_2608_27735_amd", "csrc", n), "rb") as f:
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2608_27735_amd", "csrc", "*.hip")) +
+                   glob.glob(os.path.join(ROOT, "paper_2608_27735_amd", "csrc", "*.h")) +
+                   [os.path.join(ROOT, "include", "abcd.h")])
+    for n in files:
+        h.update(os.path.basename(n).encode())
+        with open(n, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary
-    (FETCH_SIZE and WRITE_SIZE runs, scaled by the plain-copy calibration), if
-    it was taken on the kernel source built now; else None."""
-    path = os.path.join(PROFILES, f"{kernel}_hbm_bytes.md")
+def profile_values(name):
+    """The `- key = value` lines of a committed counter summary, if it was taken
+    on the library sources built now; else {}."""
+    path = os.path.join(PROFILES, name)
     if not os.path.exists(path):
-        return None
+        return {}
     vals = {}
     for line in open(path):
         if line.startswith("- ") and " = " in line:
             k, v = line[2:].strip().split(" = ", 1)
             vals[k.strip()] = v.strip().strip("`")
+    return vals if vals.get("library_digest") == library_digest() else {}
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE runs, scaled by the plain-copy calibration), or
+    None when it is missing or stale."""
+    v = profile_values(HBM_PROFILE)
     try:
-        if vals["source_digest"] != source_digest(vals["sources"].split(",")):
-            return None
-        return (float(vals["fetch_kib"]) * float(vals["fetch_factor"]) +
-                float(vals["write_kib"]) * float(vals["write_factor"])) * 1024.0
-    except (KeyError, ValueError, OSError):
+        return (float(v[f"{kernel}.fetch_kib"]) * float(v["fetch_factor"]) +
+                float(v[f"{kernel}.write_kib"]) * float(v["write_factor"])) * 1024.0
+    except (KeyError, ValueError):
         return None
+
+
+def counted_valu(kernel):
+    """Wave-level VALU instructions per launch of `kernel` (SQ_INSTS_VALU) from
+    the committed counter summary, or None when it is missing or stale."""
+    try:
+        return float(profile_values(SQ_PROFILE)[f"{kernel}.sq_insts_valu"])
+    except (KeyError, ValueError):
+        return None
+
+
+def roofline_of(name, d, pairs, bytes_):
+    """Roofline of one kernel from its live-measured launch duration. HBM-bound
+    kernels: algorithmic bytes per launch / duration against 8 TB/s. Blend
+    kernels (bound by vector issue): counted VALU lane-operations per launch
+    (SQ_INSTS_VALU x 64 lanes) / duration against the 39.3 T lane-op/s issue
+    peak, with the flop estimate and the HBM rate beside it."""
+    dur = d["ms_per_launch"] / 1e3
+    traffic = measured_traffic(name)
+    hbm = None if traffic is None else dict(achieved=traffic / dur / 1e9, peak=HBM_PEAK_GBS,
+                                            unit="GB/s", frac=traffic / dur / 1e9 / HBM_PEAK_GBS)
+    if bytes_ is not None:
+        launch_bytes = bytes_ / d["launches_per_step"]
+        achieved = launch_bytes / dur / 1e9
+        return dict(bound="hbm", kernel=name, achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=achieved / HBM_PEAK_GBS, traffic=traffic,
+                    algorithmic_bytes_per_launch=launch_bytes, basis="algorithmic bytes")
+    if name not in FLOPS_PER_PAIR:
+        return None
+    est = pairs * FLOPS_PER_PAIR[name] / dur / 1e12
+    cross = dict(flops_per_pair=FLOPS_PER_PAIR[name], evaluated_pairs=pairs, achieved=est,
+                 peak=FP32_TFLOPS, unit="TFLOP/s", frac=est / FP32_TFLOPS)
+    insts = counted_valu(name)
+    if insts is not None:
+        achieved = insts * 64 / dur / 1e12
+        return dict(bound="alu", kernel=name, achieved=achieved, peak=VALU_LANE_PEAK_T,
+                    unit="Tlane-op/s", frac=achieved / VALU_LANE_PEAK_T, traffic=traffic,
+                    basis="counted SQ_INSTS_VALU per launch x 64 lanes / live launch time",
+                    valu_insts_per_launch=insts, flop_estimate=cross, hbm=hbm)
+    return dict(bound="alu", kernel=name, achieved=est, peak=FP32_TFLOPS, unit="TFLOP/s",
+                frac=est / FP32_TFLOPS, traffic=traffic,
+                basis="estimated flops per evaluated pair (no current counter summary)",
+                evaluated_pairs=pairs, flops_per_pair=FLOPS_PER_PAIR[name], hbm=hbm)
 
 
 def main():
@@ -295,29 +359,21 @@ def main():
     dominant = max(kern, key=lambda x: kern[x]["ms_per_step"]) if kern else None
     roofline = None
     if dominant:
-        d = kern[dominant]
-        bytes_ = algorithmic_bytes(dominant, args.n, n_vis, m, npix, k, sh_coeffs, covered)
-        if bytes_ is not None:
-            launch_bytes = bytes_ / d["launches_per_step"]
-            achieved = launch_bytes / (d["ms_per_launch"] / 1e3) / 1e9
-            roofline = dict(bound="hbm", kernel=dominant, achieved=achieved, peak=HBM_PEAK_GBS,
-                            unit="GB/s", frac=achieved / HBM_PEAK_GBS,
-                            traffic=measured_traffic(dominant),
-                            algorithmic_bytes_per_launch=launch_bytes)
-        elif dominant in FLOPS_PER_PAIR:
-            flops = pairs * FLOPS_PER_PAIR[dominant]
-            achieved = flops / (d["ms_per_launch"] / 1e3) / 1e12
-            roofline = dict(bound="alu", kernel=dominant, achieved=achieved,
-                            peak=VALU_PEAK_TFLOPS, unit="TFLOP/s",
-                            frac=achieved / VALU_PEAK_TFLOPS, traffic=measured_traffic(dominant),
-                            evaluated_pairs=pairs, flops_per_pair=FLOPS_PER_PAIR[dominant])
+        roofline = roofline_of(dominant, kern[dominant], pairs,
+                               algorithmic_bytes(dominant, args.n, n_vis, m, npix, k, sh_coeffs,
+                                                 covered))
     for name in FLOPS_PER_PAIR:
         if name in kern:
-            kern[name]["TFLOPs"] = pairs * FLOPS_PER_PAIR[name] / (kern[name]["ms_per_launch"] / 1e3) / 1e12
+            r = roofline_of(name, kern[name], pairs, None)
+            kern[name]["roofline"] = {kk: r[kk] for kk in ("achieved", "peak", "unit", "frac",
+                                                            "basis")}
     for name, d in kern.items():
         b = algorithmic_bytes(name, args.n, n_vis, m, npix, k, sh_coeffs, covered)
         if b is not None:
             d["algorithmic_GBs"] = b / d["launches_per_step"] / (d["ms_per_launch"] / 1e3) / 1e9
+        t = measured_traffic(name)
+        if t is not None:
+            d["measured_GBs"] = t / (d["ms_per_launch"] / 1e3) / 1e9
 
     if args.extras:
         # the optimizer side of the step (reported beside the metric, not in it):
@@ -377,6 +433,21 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    configs = None
+    if args.configs:
+        del st, images, rects, F, B
+        torch.cuda.empty_cache()
+        configs = dict(
+            tiny_512_128x128=small,
+            ring_64k_8cams_512x512=config_ring(api, S, ActiveBlockStep, dev, args.steps,
+                                               args.warmup),
+            midscale_300k_100steps_1297x840=config_midscale(api, S, ActiveBlockStep, dev),
+            block_1m_uniform_1920x1080=config_large(api, S, ActiveBlockStep, dev, False,
+                                                    args.steps, args.warmup),
+            block_1m_heavy_tail_1920x1080=config_large(api, S, ActiveBlockStep, dev, True,
+                                                       args.steps, args.warmup),
+            stress_2560x1440=config_stress(api, S, ActiveBlockStep, dev))
+
     cpu = None
     if args.cpu_baseline:
         cpu = cpu_baseline(w, cam, prm, k)
@@ -403,6 +474,7 @@ def main():
         "hierarchy": hierarchy,
         "comparison": comparison,
         "small_config": small,
+        "configs": configs,
         "kernels": kern,
         "setup_s": setup_s,
     }
@@ -439,6 +511,308 @@ def small_config(api, S, ActiveBlockStep, dev, steps, warmup):
     graph = timed(st.replay)
     return dict(workload=f"{len(sub['means'])} active Gaussians (SH 0) at {cam.width}x{cam.height}",
                 eager_ms_per_step=eager, graph_ms_per_step=graph, steps=reps)
+
+
+def _timed(fn, reps, warmup):
+    """Mean milliseconds of fn() over reps calls after warm-up (HIP events on the
+    current stream, synchronised on both sides)."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        fn()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def _blend_kernels(api, fn, reps):
+    """Per-launch milliseconds of the two blend kernels over reps calls of fn()."""
+    import torch
+    api.timing_reset()
+    api.timing_enable(True)
+    for _ in range(reps):
+        fn()
+    torch.cuda.synchronize()
+    api.timing_enable(False)
+    out = {}
+    for name in ("render_fwd", "render_bwd", "composite"):
+        ms, cnt = api.timing_read(name)
+        if cnt:
+            out[name] = ms / cnt
+    api.timing_reset()
+    return out
+
+
+def _blend_roofline(kern, pairs_per_call):
+    """Estimated-flop rooflines of the blend kernels (their counted instructions
+    are taken on the headline workload only)."""
+    out = {}
+    for name, ms in kern.items():
+        if name in FLOPS_PER_PAIR:
+            t = pairs_per_call * FLOPS_PER_PAIR[name] / (ms / 1e3) / 1e12
+            out[name] = dict(ms_per_launch=ms, achieved=t, peak=FP32_TFLOPS, unit="TFLOP/s",
+                             frac=t / FP32_TFLOPS, basis="estimated flops per evaluated pair")
+        else:
+            out[name] = dict(ms_per_launch=ms)
+    return out
+
+
+def _step_fields(st, ms, calls):
+    import torch
+    blends = st.n_blends.item() / calls
+    pairs = int(st.fwd["last"].to(torch.int64).sum().item())
+    return dict(ms_per_step=ms, value=blends / (ms / 1e3), unit="blends/s",
+                blends_per_step=blends, evaluated_pairs_last_step=pairs,
+                capacity=int(st.capacity))
+
+
+def config_ring(api, S, ActiveBlockStep, dev, steps, warmup):
+    """The 64K-Gaussian ring scene (SH 3, 4x4x4 grid over the unit cube's
+    [-1, 1]^3, 32 blobs): its ~1K-Gaussian active cell, 8 cameras at 512x512.
+    Every camera's F and B are collapsed from the 63 other cells' cached fp16
+    renders (drawn by the cache-refresh path, with their coverage boxes), in
+    the camera's front-to-back cell order; a step per camera."""
+    import numpy as np
+    import torch
+    from paper_2608_27735_amd.cache import CacheRefresher
+    w = S.ring()
+    prm, cams = w.params, w.cams
+    H, W = cams[0].height, cams[0].width
+    cells = [c for c in range(w.grid.n_cells) if c != w.active]
+    imgs = torch.zeros((len(cams), len(cells), H, W, 4), dtype=torch.float16, device=dev)
+    rects = torch.zeros((len(cams), len(cells), 4), dtype=torch.int32, device=dev)
+    for j, c in enumerate(cells):
+        sub = S.subset(w.scene, w.cell_of == c)
+        if len(sub["means"]) == 0:
+            continue
+        pc = {kk: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for kk, v in sub.items()}
+        ref = CacheRefresher(prm, pc, W, H)
+        for i, cam in enumerate(cams):
+            ref.render(cam, imgs[i, j], rects[i, j])
+    act = S.subset(w.scene, w.cell_of == w.active)
+    params = {kk: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for kk, v in act.items()}
+    st = ActiveBlockStep(cams[0], prm, params)
+    for cam in cams[1:]:  # capacity for every camera
+        st.cam = cam
+        st.project_and_bin(sync=True)
+    plan = []
+    for cam in cams:
+        order = [int(c) for c in w.grid.order_from(cam.campos)]
+        nf = order.index(w.active)
+        plan.append(([cells.index(c) for c in order if c != w.active], nf))
+    targets = torch.from_numpy(w.target).to(dev)
+    F = torch.empty((H, W, 4), dtype=torch.float32, device=dev)
+    B = torch.empty_like(F)
+
+    def cams_pass():
+        for i, cam in enumerate(cams):
+            st.cam = cam
+            api.composite_cache(imgs[i], plan[i][0], plan[i][1], F=F, B=B, rects=rects[i])
+            st.step(targets[i], F=F, B=B)
+
+    reps = max(2, steps // 4)
+    cams_pass()
+    torch.cuda.synchronize()
+    st.n_blends.zero_()
+    ms = _timed(cams_pass, reps, 0) / len(cams)
+    out = _step_fields(st, ms, reps * len(cams))
+    kern = _blend_kernels(api, cams_pass, 1)
+    out.update(workload=f"{len(act['means'])} active Gaussians (SH 3) of the 64K ring scene, "
+                        f"{len(cams)} cameras at {W}x{H}, F/B per camera from {len(cells)} "
+                        "cached fp16 cell renders", cameras=len(cams), k_cached=len(cells),
+               kernels_per_camera=_blend_roofline(kern, out["evaluated_pairs_last_step"]),
+               note="ms_per_step = per camera: collapse of 63 layers + project, bin, forward, "
+                    "L1 gradient, backward")
+    return out
+
+
+def config_midscale(api, S, ActiveBlockStep, dev, T=100):
+    """The mid-scale scene's 300K-Gaussian active block (ground plane and
+    blobs, SH 3) on 200 cameras at 1297x840: T = 100 steps, each on a camera
+    drawn uniformly (seeded), with that camera's F and B collapsed from the 31
+    other cells' cached renders (synthetic fp16 layers with coverage boxes,
+    ordered by the camera's cell order)."""
+    import numpy as np
+    import torch
+    w = S.midscale_block()
+    prm, cams = w.params, w.cams
+    H, W = cams[0].height, cams[0].width
+    params = {kk: torch.from_numpy(v).to(dev) for kk, v in w.scene.items()}
+    cells = [c for c in range(w.grid.n_cells) if c != w.active]
+    images, rects = S.cached_images_device(len(cells), H, W, seed=3101, device=dev,
+                                           with_rects=True)
+    st = ActiveBlockStep(cams[0], prm, params)
+    for cam in cams[1:]:
+        st.cam = cam
+        st.project_and_bin(sync=True)
+    seq = S.rng(3102).integers(0, len(cams), T)
+    plan = {}
+    for i in set(int(x) for x in seq):
+        order = [int(c) for c in w.grid.order_from(cams[i].campos)]
+        plan[i] = ([cells.index(c) for c in order if c != w.active], order.index(w.active))
+    target = torch.from_numpy(S.rng(3103).uniform(0, 1, (H, W, 3)).astype(np.float32)).to(dev)
+    F = torch.empty((H, W, 4), dtype=torch.float32, device=dev)
+    B = torch.empty_like(F)
+
+    def run():
+        for i in seq:
+            i = int(i)
+            st.cam = cams[i]
+            api.composite_cache(images, plan[i][0], plan[i][1], F=F, B=B, rects=rects)
+            st.step(target, F=F, B=B)
+
+    run()
+    torch.cuda.synchronize()
+    st.n_blends.zero_()
+    ms = _timed(run, 1, 0) / T
+    out = _step_fields(st, ms, T)
+
+    def last_cam():
+        api.composite_cache(images, plan[int(seq[-1])][0], plan[int(seq[-1])][1], F=F, B=B,
+                            rects=rects)
+        st.step(target, F=F, B=B)
+
+    kern = _blend_kernels(api, last_cam, 3)
+    out.update(kernels_last_camera=_blend_roofline(kern, out["evaluated_pairs_last_step"]))
+    out.update(workload=f"{len(w.scene['means'])} active Gaussians (SH 3), mid-scale scene "
+                        f"(4x4x2 grid), {T} steps over cameras drawn from {len(cams)} at {W}x{H}",
+               steps=T, distinct_cameras=len(plan), k_cached=len(cells),
+               note="ms_per_step = mean over the T steps, each: collapse of 31 layers + step")
+    return out
+
+
+def config_large(api, S, ActiveBlockStep, dev, heavy, steps, warmup):
+    """The 1M-Gaussian active block (SH 3) at 1920x1080, uniform or heavy-tailed
+    scales (log-normal sd 1.0), F and B from 99 cached layers."""
+    import numpy as np
+    import torch
+    w = S.active_block_1m(width=1920, height=1080, heavy_tail=heavy)
+    cam, prm = w.cam, w.params
+    params = {kk: torch.from_numpy(v).to(dev) for kk, v in w.scene.items()}
+    order = [c for c in w.order if c != w.active]
+    n_front = w.order.index(w.active)
+    k = len(order)
+    images, rects = S.cached_images_device(k, cam.height, cam.width, seed=4101, device=dev,
+                                           with_rects=True)
+    target = torch.from_numpy(S.rng(4102).uniform(0, 1, (cam.height, cam.width, 3))
+                              .astype(np.float32)).to(dev)
+    F = torch.empty((cam.height, cam.width, 4), dtype=torch.float32, device=dev)
+    B = torch.empty_like(F)
+    st = ActiveBlockStep(cam, prm, params)
+    m = st.project_and_bin(sync=True)
+
+    def one():
+        api.composite_cache(images, list(range(k)), n_front, F=F, B=B, rects=rects)
+        st.step(target, F=F, B=B)
+
+    one()
+    torch.cuda.synchronize()
+    st.n_blends.zero_()
+    reps = max(5, steps // 2)
+    ms = _timed(one, reps, warmup)
+    out = _step_fields(st, ms, reps + warmup)
+    kern = _blend_kernels(api, one, 3)
+    out.update(workload=f"1M active Gaussians (SH 3, {'heavy-tailed' if heavy else 'uniform'} "
+                        f"scales) at {cam.width}x{cam.height}, F/B from {k} cached layers",
+               n_isect=m, kernels=_blend_roofline(kern, out["evaluated_pairs_last_step"]))
+    del st, images, rects
+    torch.cuda.empty_cache()
+    return out
+
+
+def config_stress(api, S, ActiveBlockStep, dev, sizes=(262_144, 1_000_000, 4_000_000)):
+    """The stress configuration at 2560x1440 (8x8x2 grid, tiny scales): steps of
+    active blocks of 256K, 1M and 4M Gaussians, each with F and B collapsed
+    from 127 cached layers (synthetic fp16 with coverage boxes), and the peak
+    device memory of each point. Then, for the 1M block, F and B built from
+    pinned host memory (coverage boxes streamed 16 layers at a time) for
+    scenes of 10x, 50x, 100x and 128x the active block (9, 49, 99 and 127
+    frozen cells of its size): the device peak should not grow with the scene."""
+    import numpy as np
+    import torch
+    from paper_2608_27735_amd.hierarchy import FBStreamer, HostCache
+    sweep = []
+    k = 127
+    for n in sizes:
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        w = S.stress_block(n=n)
+        cam, prm = w.cam, w.params
+        params = {kk: torch.from_numpy(v).to(dev) for kk, v in w.scene.items()}
+        images, rects = S.cached_images_device(k, cam.height, cam.width, seed=5101, device=dev,
+                                               with_rects=True)
+        order = [c for c in w.order if c != w.active]
+        n_front = w.order.index(w.active)
+        target = torch.from_numpy(S.rng(5102).uniform(0, 1, (cam.height, cam.width, 3))
+                                  .astype(np.float32)).to(dev)
+        F = torch.empty((cam.height, cam.width, 4), dtype=torch.float32, device=dev)
+        B = torch.empty_like(F)
+        st = ActiveBlockStep(cam, prm, params)
+        m = st.project_and_bin(sync=True)
+
+        def one():
+            api.composite_cache(images, list(range(len(order))), n_front, F=F, B=B, rects=rects)
+            st.step(target, F=F, B=B)
+
+        one()
+        torch.cuda.synchronize()
+        st.n_blends.zero_()
+        reps = 5
+        ms = _timed(one, reps, 1)
+        row = _step_fields(st, ms, reps + 1)
+        row["kernels"] = _blend_roofline(_blend_kernels(api, one, 2), row["evaluated_pairs_last_step"])
+        cm = _timed(lambda: api.composite_cache(images, list(range(len(order))), n_front, F=F,
+                                                B=B, rects=rects), 5, 1)
+        row.update(n_gaussians=n, n_isect=m, collapse_ms=cm,
+                   device_peak_bytes=int(torch.cuda.max_memory_allocated() - base),
+                   resident_layers_bytes=int(images.numel() * 2))
+        sweep.append(row)
+        del st, images, rects, params, F, B
+    # device memory flat in the scene size: the cached layers live in pinned host memory
+    w = S.stress_block(n=sizes[1])
+    cam, prm = w.cam, w.params
+    torch.cuda.empty_cache()
+    hc = HostCache(cam.width, cam.height, k)
+    dimgs, drects = S.cached_images_device(k, cam.height, cam.width, seed=5101, device=dev,
+                                           with_rects=True)
+    hc.images.copy_(dimgs.cpu())
+    hc.rects[:] = drects.cpu().numpy()
+    del dimgs, drects
+    params = {kk: torch.from_numpy(v).to(dev) for kk, v in w.scene.items()}
+    target = torch.from_numpy(S.rng(5102).uniform(0, 1, (cam.height, cam.width, 3))
+                              .astype(np.float32)).to(dev)
+    F = torch.empty((cam.height, cam.width, 4), dtype=torch.float32, device=dev)
+    B = torch.empty_like(F)
+    st = ActiveBlockStep(cam, prm, params)
+    streamer = FBStreamer(hc, chunk=16)
+    flat = []
+    for K in (9, 49, 99, 127):
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        t0 = time.perf_counter()
+        streamer.build(list(range(K)), K // 2, F, B)
+        st.step(target, F=F, B=B)
+        torch.cuda.synchronize()
+        flat.append(dict(scene_over_active=K + 1, frozen_cells=K,
+                         fb_build_and_step_ms=(time.perf_counter() - t0) * 1e3,
+                         device_peak_growth_bytes=int(torch.cuda.max_memory_allocated() - base),
+                         host_cache_bytes=int(K * cam.width * cam.height * 8)))
+    resident = int(sum(v.numel() * v.element_size() for v in params.values()) +
+                   2 * F.numel() * 4 + sum(b.numel() * b.element_size() for b in streamer.bufs))
+    del st, streamer, hc, params, F, B
+    torch.cuda.empty_cache()
+    return dict(workload=f"stress block (tiny scales, SH 3) at {cam.width}x{cam.height}, "
+                         f"{k} cached layers per camera", sweep=sweep, scene_growth=flat,
+                resident_active_fb_staging_bytes=resident,
+                note="scene_growth: the 1M block with F/B streamed from pinned host memory; "
+                     "device_peak_growth_bytes is what building F/B and one step add on top of "
+                     "the resident active set, F/B and staging chunks")
 
 
 def cpu_baseline(w, cam, prm, k):
