@@ -181,6 +181,12 @@ __device__ __forceinline__ unsigned int wave_sum_u32(unsigned int x) {
   return x;
 }
 
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  return x;
+}
+
 // ------------------------------------------------------ split workspace
 
 // Long tiles are split for the backward: while a tile's walk crosses every

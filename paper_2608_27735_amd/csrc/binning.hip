@@ -35,7 +35,7 @@
 //   l2_scatter             values (and keys), tile-major, depth order
 #include <algorithm>
 
-#include "abcd_internal.h"
+#include "schedule.h"
 
 namespace abcd {
 namespace {
@@ -813,6 +813,238 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
   }
 }
 
+// ------------------------------------------------------- small active blocks
+//
+// A small active block (the regime where ABCD's partitions hold few Gaussians
+// and launch costs dominate) is binned in two launches instead of the general
+// path's 22: one workgroup sorts the Gaussians by depth in LDS, counts each
+// tile's list from the rectangles and scans the counts into the tile ranges;
+// then one workgroup per tile collects, in depth order, the Gaussians whose
+// rectangle covers it. The lists are the same as the general path's.
+
+constexpr int kSmallN = 2048;        // Gaussians the one-workgroup sort holds
+constexpr int kSmallTiles = 2048;    // tiles of the frame (each coordinate below 256)
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallWaves = kSmallThreads / 64;
+constexpr int kSmallKeyBytes = kSmallN * 4;
+static_assert(kSmallThreads == kOrderThreads, "the small path orders tiles with order_tiles");
+
+bool small_path(int64_t n, const Geo& g) {
+  return n <= kSmallN && (int64_t)g.ntx * g.nty <= kSmallTiles && g.ntx <= 256 && g.nty <= 256;
+}
+
+// tile rectangle in bytes: x0 | x1 << 8 | y0 << 16 | y1 << 24 (empty: x0 = 1 > x1 = 0)
+__device__ __forceinline__ uint32_t pack_rect8(int x0, int y0, int x1, int y1) {
+  return (uint32_t)x0 | ((uint32_t)x1 << 8) | ((uint32_t)y0 << 16) | ((uint32_t)y1 << 24);
+}
+
+// Exclusive scan over the threads of a workgroup of kSmallThreads: each wave
+// scans its 64 values with shuffles, one barrier publishes the wave totals
+// (s: kSmallWaves words of LDS), and each thread adds the totals of the waves
+// before its own. Returns the exclusive prefix and the total in *tot.
+__device__ __forceinline__ uint32_t scan_small(uint32_t v, uint32_t* s, uint32_t* tot) {
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  uint32_t incl = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = (uint32_t)__shfl_up((int)incl, d, 64);
+    if (lane >= d) incl += y;
+  }
+  if (lane == 63) s[w] = incl;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int k = 0; k < kSmallWaves; ++k) {
+    const uint32_t c = s[k];
+    before += k < w ? c : 0u;
+    all += c;
+  }
+  *tot = all;
+  __syncthreads();
+  return before + incl - v;
+}
+
+// One workgroup: keys (fp32 depth bits; Gaussians with no tile last) and byte
+// rectangles; a stable LSD radix sort by key in LDS (8-bit digits; wave w
+// ranks its 128 consecutive entries with ballots, the waves' digit counts give
+// the offsets), which keeps equal keys in index order; per-tile counts by LDS
+// atomics over each rectangle; their exclusive scan (tile_off, tile_ranges);
+// the sorted Gaussians and their rectangles for the per-tile collection; M
+// and the overflow decision in the header (on overflow
+// every range is empty), and the forward's tile order.
+__global__ __launch_bounds__(kSmallThreads) void bin_small_sort_kernel(
+    int n, const float* __restrict__ depth, const uint32_t* __restrict__ tiles,
+    const float* __restrict__ means2d, const float* __restrict__ extent, Geo geo,
+    unsigned long long capacity, uint32_t* __restrict__ sorted_g, uint32_t* __restrict__ sorted_rect,
+    uint32_t* __restrict__ tile_off, uint32_t* __restrict__ tile_ranges,
+    uint32_t* __restrict__ tile_order, WsHeader* __restrict__ hdr) {
+  __shared__ uint32_t s_key[2][kSmallN];
+  __shared__ uint16_t s_val[2][kSmallN];
+  __shared__ uint32_t s_rect[kSmallN];
+  __shared__ uint16_t s_cnt[kSmallWaves][256];
+  __shared__ uint32_t s_tcount[kSmallTiles];
+  __shared__ uint32_t s_scan[kSmallWaves];
+  __shared__ unsigned long long s_m;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int ntiles = geo.ntx * geo.nty;
+  for (int t = tid; t < ntiles; t += kSmallThreads) s_tcount[t] = 0;
+  if (tid == 0) s_m = 0;
+  __syncthreads();
+  unsigned long long m = 0;
+  for (int i = tid; i < n; i += kSmallThreads) {
+    const uint32_t tt = tiles[i];
+    uint32_t key = 0xffffffffu;
+    int x0 = 1, y0 = 0, x1 = 0, y1 = 0;
+    if (tt != 0) {
+      key = __float_as_uint(depth[i]);
+      const float2 mm = reinterpret_cast<const float2*>(means2d)[i];
+      const float2 ex = reinterpret_cast<const float2*>(extent)[i];
+      if (!tile_rect(mm.x, mm.y, ex.x, ex.y, geo.ntx, geo.nty, x0, y0, x1, y1))
+        x0 = 1, y0 = 0, x1 = 0, y1 = 0;
+    }
+    s_key[0][i] = key;
+    s_val[0][i] = (uint16_t)i;
+    s_rect[i] = pack_rect8(x0, y0, x1, y1);
+    if (x1 >= x0) {
+      m += tt;
+      for (int y = y0; y <= y1; ++y)
+        for (int x = x0; x <= x1; ++x) atomicAdd(&s_tcount[y * geo.ntx + x], 1u);
+    }
+  }
+  const unsigned long long wm = wave_sum_u64(m);
+  if (lane == 0 && wm) atomicAdd(&s_m, wm);
+  __syncthreads();
+  const unsigned long long mt = s_m;
+  const bool over = mt > capacity || mt >= (1ull << 32);
+  // radix sort: wave w owns positions [128 w, 128 w + 128)
+  const uint64_t lt = lanemask_lt();
+#pragma unroll 1
+  for (int pass = 0; pass < 4; ++pass) {
+    const int src = pass & 1, shift = 8 * pass;
+    for (int i = tid; i < kSmallWaves * 256; i += kSmallThreads) (&s_cnt[0][0])[i] = 0;
+    __syncthreads();
+    uint32_t key[2], rank[2];
+    uint16_t val[2];
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int idx = 128 * w + 64 * it + lane;
+      const bool valid = idx < n;
+      key[it] = valid ? s_key[src][idx] : 0u;
+      val[it] = valid ? s_val[src][idx] : (uint16_t)0;
+      const uint32_t d = (key[it] >> shift) & 255u;
+      const uint64_t peers = match_digit(d, __ballot(valid));
+      rank[it] = 0;
+      if (valid) {
+        rank[it] = s_cnt[w][d] + (uint32_t)__popcll(peers & lt);
+        if (lane == __ffsll((unsigned long long)peers) - 1)
+          s_cnt[w][d] = (uint16_t)(s_cnt[w][d] + __popcll(peers));
+      }
+    }
+    __syncthreads();
+    // digit d: total over the waves, exclusive base over the digits, then the
+    // waves' offsets in place
+    uint32_t tot_d = 0;
+    if (tid < 256)
+      for (int v = 0; v < kSmallWaves; ++v) tot_d += s_cnt[v][tid];
+    uint32_t total;
+    uint32_t base = scan_small(tid < 256 ? tot_d : 0u, s_scan, &total);
+    if (tid < 256)
+      for (int v = 0; v < kSmallWaves; ++v) {
+        const uint32_t c = s_cnt[v][tid];
+        s_cnt[v][tid] = (uint16_t)base;
+        base += c;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int idx = 128 * w + 64 * it + lane;
+      if (idx < n) {
+        const uint32_t pos = s_cnt[w][(key[it] >> shift) & 255u] + rank[it];
+        s_key[src ^ 1][pos] = key[it];
+        s_val[src ^ 1][pos] = val[it];
+      }
+    }
+    __syncthreads();
+  }
+  // four passes: sorted in buffer 0
+  for (int j = tid; j < n; j += kSmallThreads) {
+    const uint32_t g = s_val[0][j];
+    sorted_g[j] = g;
+    sorted_rect[j] = s_rect[g];
+  }
+  // tile ranges: runs of `per` tiles per thread
+  const int per = (ntiles + kSmallThreads - 1) / kSmallThreads;
+  const int lo = min(ntiles, per * tid), hi = min(ntiles, lo + per);
+  uint32_t sum = 0;
+  for (int t = lo; t < hi; ++t) sum += over ? 0u : s_tcount[t];
+  uint32_t total;
+  uint32_t run = scan_small(sum, s_scan, &total);
+  for (int t = lo; t < hi; ++t) {
+    const uint32_t c = over ? 0u : s_tcount[t];
+    tile_off[t] = run;
+    tile_ranges[2 * t] = run;
+    tile_ranges[2 * t + 1] = run + c;
+    run += c;
+    if (over) s_tcount[t] = 0u;
+  }
+  if (tile_order) {
+    // the forward's schedule: heaviest lists first (identity on overflow); the
+    // bucket keys go where the sort's second key buffer was
+    static_assert(kSmallKeyBytes >= kSmallTiles, "bucket keys fit the spare key buffer");
+    __syncthreads();
+    order_tiles(ntiles, s_tcount, tile_order, reinterpret_cast<uint8_t*>(s_key[1]));
+  }
+  if (tid == 0) {
+    hdr->m = mt;
+    hdr->m1 = 0;
+    hdr->overflow = over ? 1u : 0u;
+    hdr->total_sub = 0;
+  }
+}
+
+// One workgroup per tile: the sorted Gaussians whose rectangle covers the
+// tile, in sorted order, 256 positions per round (ballots rank them).
+__global__ __launch_bounds__(256) void bin_small_collect_kernel(
+    int n, const float* __restrict__ depth, Geo geo, const uint32_t* __restrict__ sorted_g,
+    const uint32_t* __restrict__ sorted_rect, const uint32_t* __restrict__ tile_off,
+    const WsHeader* __restrict__ hdr, uint32_t* __restrict__ values_sorted,
+    unsigned long long* __restrict__ keys_sorted) {
+  __shared__ uint32_t s_w[4];
+  if (hdr->overflow) return;
+  const int t = blockIdx.x, tx = t % geo.ntx, ty = t / geo.ntx;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const uint64_t lt = lanemask_lt();
+  uint32_t run = tile_off[t];
+  for (int j0 = 0; j0 < n; j0 += 256) {
+    const int j = j0 + threadIdx.x;
+    bool hit = false;
+    uint32_t g = 0;
+    if (j < n) {
+      const uint32_t r = sorted_rect[j];
+      const int x0 = r & 255, x1 = (r >> 8) & 255, y0 = (r >> 16) & 255, y1 = r >> 24;
+      hit = x0 <= tx && tx <= x1 && y0 <= ty && ty <= y1;
+      g = sorted_g[j];
+    }
+    const uint64_t bal = __ballot(hit);
+    if (lane == 0) s_w[w] = (uint32_t)__popcll(bal);
+    __syncthreads();
+    uint32_t before = 0, tot = 0;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const uint32_t c = s_w[v];
+      before += v < w ? c : 0u;
+      tot += c;
+    }
+    if (hit) {
+      const uint32_t pos = run + before + (uint32_t)__popcll(bal & lt);
+      values_sorted[pos] = g;
+      if (keys_sorted) keys_sorted[pos] = ((unsigned long long)t << 32) | __float_as_uint(depth[g]);
+    }
+    run += tot;
+    __syncthreads();
+  }
+}
+
 __global__ void bin_empty_kernel(int ntiles, uint32_t* __restrict__ tile_ranges,
                                  uint32_t* __restrict__ tile_order, WsHeader* __restrict__ hdr) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < 2 * ntiles; i += gridDim.x * blockDim.x) {
@@ -854,6 +1086,17 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
     return ABCD_OK;
   }
   auto u32 = [&](size_t off) { return reinterpret_cast<uint32_t*>(ws + off); };
+  if (small_path(n, geo)) {
+    const unsigned long long cap_s = (unsigned long long)std::max<int64_t>(capacity, 0);
+    ABCD_LAUNCH("bin_small_sort", bin_small_sort_kernel, 1, kSmallThreads, 0, stream, (int)n,
+                depth, tiles_touched, means2d, extent, geo, cap_s, u32(L.keys_a), u32(L.keys_b),
+                u32(L.tile_off), tile_ranges, tile_order, hdr);
+    ABCD_LAUNCH("bin_small_collect", bin_small_collect_kernel, ntiles, kBlock, 0, stream, (int)n,
+                depth, geo, u32(L.keys_a), u32(L.keys_b), u32(L.tile_off), hdr, values_sorted,
+                reinterpret_cast<unsigned long long*>(keys_sorted));
+    ABCD_HIP(hipGetLastError());
+    return ABCD_OK;
+  }
   uint32_t* keys[2] = {u32(L.keys_a), u32(L.keys_b)};
   uint32_t* vals[2] = {u32(L.vals_a), u32(L.vals_b)};
   uint32_t* hist = u32(L.hist);

@@ -94,7 +94,8 @@ __device__ __forceinline__ void bwd_item(
   __shared__ int s_pos[256];
   __shared__ uint32_t s_g[256];
   __shared__ float s_acc[9 * 256];  // entry-major: [entry][9]
-  __shared__ int s_wcnt[4];
+  __shared__ __align__(4) uint8_t s_idx[4][256];  // per wave: staged slots reaching its rows
+  __shared__ int s_wcnt[5][4];
   __shared__ uint32_t s_max;
   const int tid = threadIdx.x;
   const int px = (tile % k.ntx) * kTile + (tid & 15);
@@ -183,8 +184,12 @@ __device__ __forceinline__ void bwd_item(
     const float3 cn = conic_of(rec.co);
     const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, cn.x, cn.y, cn.z, rec.co.w,
                                                      k.alpha_min, box.x0, box.x1, box.y0, box.y1);
-    int pos;
-    const int cnt = compact(keep, s_wcnt, pos);
+    // each wave walks only the staged entries whose ellipse reaches its four
+    // pixel rows: the others contribute nothing to any of its pixels
+    const uint32_t rows =
+        keep ? rows_reached(rec.m.x, rec.m.y, cn.x, cn.y, cn.z, rec.co.w, k.alpha_min, box) : 0u;
+    int pos, wcnt;
+    const int cnt = compact_rows(keep, rows, s_wcnt, s_idx, pos, wcnt);
     if (keep) {
       const Splat sp = make_splat(rec.m, rec.co);
       s_ga[pos] = make_float4(sp.u, sp.v, sp.qa, sp.qb);
@@ -206,13 +211,18 @@ __device__ __forceinline__ void bwd_item(
     }
     // Entries are read from LDS kGroup at a time, all reads issued before the
     // first is used, so the LDS latency is paid once per group.
-    for (int j0 = 0; j0 < cnt; j0 += kBwdGroup) {
+    // The wave's list of staged slots, kBwdGroup at a time; slots past its end
+    // hold stale bytes, which still index the staged arrays.
+    static_assert(kBwdGroup == 4, "slot indices are read four at a time");
+    const uint32_t* my_idx = reinterpret_cast<const uint32_t*>(s_idx[tid >> 6]);
+    for (int j0 = 0; j0 < wcnt; j0 += kBwdGroup) {
     float4 gav[kBwdGroup], gbv[kBwdGroup];
     float cbv[kBwdGroup];  // colour b (the conic in s_gc is needed only at the flush)
     uint32_t kkv[kBwdGroup];
+    const uint32_t iw = __builtin_amdgcn_readfirstlane(my_idx[j0 / 4]);  // four slots (uniform)
 #pragma unroll
     for (int i = 0; i < kBwdGroup; ++i) {
-      const int j = min(j0 + i, 255);
+      const int j = (int)((iw >> (8 * i)) & 255u);
       gav[i] = s_ga[j];
       gbv[i] = s_gb[j];
       cbv[i] = s_gc[j].w;
@@ -226,8 +236,8 @@ __device__ __forceinline__ void bwd_item(
                    "v"(gbv[i].y), "v"(gbv[i].z), "v"(gbv[i].w), "v"(cbv[i]));
 #pragma unroll
     for (int i = 0; i < kBwdGroup; ++i) {
-      const int j = j0 + i;
-      if (j >= cnt) break;  // wave-uniform
+      if (j0 + i >= wcnt) break;  // wave-uniform
+      const int j = (int)((iw >> (8 * i)) & 255u);  // staged slot (uniform)
       const uint32_t kk = __builtin_amdgcn_readfirstlane(kkv[i]);
       const float4 ga = gav[i], gb = gbv[i];
       if (kk >= wml) continue;  // wave-uniform: no pixel of this wave reaches entry kk
@@ -294,7 +304,7 @@ __device__ __forceinline__ void bwd_item(
 
 // Persistent workgroups take work items, heaviest first, from a queue until
 // it is empty (every workgroup reaches the end of the queue and exits).
-__global__ __launch_bounds__(256) void render_bwd_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void render_bwd_kernel(
     BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
     const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
@@ -329,6 +339,21 @@ __global__ __launch_bounds__(256) void render_bwd_kernel(
       bwd_item(k, (int)it.x, it.y, tile_ranges, values, means2d, conic_opacity, rgb, F, B,
                final_T, last, dL_dout, g2d, sp);
   }
+}
+
+// Small frames (few tiles, no split): one workgroup per tile in raster order,
+// without the schedule's two launches (the launch-bound regime of small
+// active partitions).
+constexpr int kDirectTiles = 1024;
+
+__global__ __launch_bounds__(256) void render_bwd_direct_kernel(
+    BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
+    const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
+    const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
+    const float* __restrict__ final_T, const uint32_t* __restrict__ last,
+    const float4* __restrict__ dL_dout, float* __restrict__ g2d) {
+  bwd_item(k, (int)blockIdx.x, 0u, tile_ranges, values, means2d, conic_opacity, rgb, F, B, final_T,
+           last, dL_dout, g2d, SplitLayout{});
 }
 
 }  // namespace
@@ -368,6 +393,15 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
                                  const float* dL_dout, float* g2d, const SplitLayout& split,
                                  hipStream_t stream) {
   const BlendConsts k = consts(cam, prm);
+  if (!split.ckpt && k.ntiles <= kDirectTiles) {
+    ABCD_LAUNCH("render_bwd", render_bwd_direct_kernel, k.ntiles, kBlock, 0, stream, k,
+                tile_ranges, values_sorted, reinterpret_cast<const float2*>(means2d),
+                reinterpret_cast<const float4*>(conic_opacity), rgb,
+                reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B), final_T,
+                last, reinterpret_cast<const float4*>(dL_dout), g2d);
+    ABCD_HIP(hipGetLastError());
+    return ABCD_OK;
+  }
   char* tail = reinterpret_cast<char*>(g2d) + bwd_g2d_bytes(n);
   uint32_t* work = reinterpret_cast<uint32_t*>(tail);
   uint32_t* order = work + ABCD_MAX_TILES;

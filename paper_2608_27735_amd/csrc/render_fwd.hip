@@ -16,60 +16,6 @@
 namespace abcd {
 namespace {
 
-// Rows mask of a kept entry: bit w set when its ellipse (the margin of
-// splat_touches_box included) reaches pixel rows 4w .. 4w + 3 of the tile.
-__device__ __forceinline__ uint32_t rows_reached(float u, float v, float a, float b, float c,
-                                                 float o, float alpha_min, const TileBox& box) {
-  uint32_t rows = 0;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    const float y0 = box.y0 + 4.0f * (float)w, y1 = fminf(box.y1, y0 + 3.0f);
-    if (y0 <= y1 && splat_touches_box(u, v, a, b, c, o, alpha_min, box.x0, box.x1, y0, y1))
-      rows |= 1u << w;
-  }
-  return rows;
-}
-
-// Block-wide compaction of the staged entries (as compact() does) and, for
-// each wave w, the list of the staged slots whose rows mask has bit w, in
-// list order, into s_idx[w]. s_cnt holds 5 x 4 wave counts. Returns the
-// number kept; wcnt is the length of the calling wave's list (both uniform).
-__device__ __forceinline__ int compact_rows(bool keep, uint32_t rows, int (*s_cnt)[4],
-                                            uint8_t (*s_idx)[256], int& pos, int& wcnt) {
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  const uint64_t below = (1ull << l) - 1ull;
-  const uint64_t bal = __ballot(keep);
-  uint64_t rb[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) rb[r] = __ballot((rows >> r) & 1u);
-  if (l == 0) {
-    s_cnt[0][w] = __popcll(bal);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) s_cnt[1 + r][w] = __popcll(rb[r]);
-  }
-  __syncthreads();
-  int off = 0, tot = 0, mine = 0;
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int c = s_cnt[0][v];
-    off += v < w ? c : 0;
-    tot += c;
-    mine += s_cnt[1 + w][v];
-  }
-  pos = off + __popcll(bal & below);
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    if ((rows >> r) & 1u) {
-      int o = 0;
-#pragma unroll
-      for (int v = 0; v < 4; ++v) o += v < w ? s_cnt[1 + r][v] : 0;
-      s_idx[r][o + __popcll(rb[r] & below)] = (uint8_t)pos;
-    }
-  }
-  wcnt = __builtin_amdgcn_readfirstlane(mine);
-  return __builtin_amdgcn_readfirstlane(tot);
-}
-
 // kHalf: the cached-render variant: F = B = transparent, the image is written
 // as fp16 RGBA to out16 (round to nearest even), no final T or walk lengths.
 // Register budget: four waves per SIMD (at most 128 VGPRs).

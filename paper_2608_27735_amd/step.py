@@ -15,7 +15,11 @@ from . import api
 
 
 class ActiveBlockStep:
-    def __init__(self, cam, prm, params, capacity=None, headroom=1.25, bg=None, chunk=512):
+    # below this many active Gaussians the backward's split does not pay for
+    # its extra launches (the lists are short)
+    SPLIT_MIN_GAUSSIANS = 16384
+
+    def __init__(self, cam, prm, params, capacity=None, headroom=1.25, bg=None, chunk="auto"):
         self.cam, self.prm, self.params = cam, prm, params
         self.bg = bg
         n = params["means"].shape[0]
@@ -56,6 +60,8 @@ class ActiveBlockStep:
         # split); slots are taken as walks cross chunk boundaries, heaviest
         # tiles first, so a short pool only leaves light tiles whole
         self.split = None
+        if chunk == "auto":
+            chunk = 512 if n >= self.SPLIT_MIN_GAUSSIANS else None
         if chunk:
             self.split = api.make_split(self._split_slots(capacity, chunk), chunk, dev)
 

@@ -81,6 +81,17 @@ def cases():
     sc4 = S.gaussians(rs, rs.uniform((-0.8, -0.8, -0.6), (0.8, 0.8, 0.6), (6000, 3)), 1,
                       math.log(0.012), 0.4)
     out.append(("small-splats-100x75", cam, RasterParams(sh_degree=1), sc4))
+    # small active blocks take the two-launch binning (at most 2,048 Gaussians,
+    # 2,048 tiles): a ragged frame, and the largest block it takes next to one
+    # Gaussian more (the general path)
+    rk = S.rng(24)
+    cam = look_at((0.2, -3.0, 0.9), (0, 0, 0), 203, 117)
+    sc5 = S.gaussians(rk, rk.uniform(-1, 1, (1500, 3)), 2, math.log(0.05), 0.6)
+    out.append(("small-path-ragged-203x117", cam, RasterParams(sh_degree=2), sc5))
+    ring_n = {k: v[:2048] for k, v in r.scene.items()}
+    out.append(("small-path-2048-cam1", r.cams[1], r.params, ring_n))
+    out.append(("general-path-2049-cam1", r.cams[1], r.params,
+                {k: v[:2049] for k, v in r.scene.items()}))
     return out
 
 
