@@ -446,7 +446,8 @@ def main():
                                                     args.steps, args.warmup),
             block_1m_heavy_tail_1920x1080=config_large(api, S, ActiveBlockStep, dev, True,
                                                        args.steps, args.warmup),
-            stress_2560x1440=config_stress(api, S, ActiveBlockStep, dev))
+            stress_2560x1440=config_stress(api, S, ActiveBlockStep, dev),
+            comparison_midscale_5m_1297x840=comparison_midscale(S))
 
     cpu = None
     if args.cpu_baseline:
@@ -813,6 +814,26 @@ def config_stress(api, S, ActiveBlockStep, dev, sizes=(262_144, 1_000_000, 4_000
                 note="scene_growth: the 1M block with F/B streamed from pinned host memory; "
                      "device_peak_growth_bytes is what building F/B and one step add on top of "
                      "the resident active set, F/B and staging chunks")
+
+
+def comparison_midscale(S, n=5_000_000, n_cams=12, T=4):
+    """The paper's three setups (Results section: 3DGS-style joint training,
+    ABCD, ABCD without F/B) on the whole 5M-Gaussian mid-scale scene (32
+    cells, 12 of its 200 cameras at 1297x840), targets = joint renders of the
+    scene, training from a perturbed copy, T Adam steps per Gaussian (one
+    epoch): PSNR, wall time and peak device memory of each. The ABCD setup
+    keeps every camera's cached cell renders in pinned host memory and streams
+    each camera's F/B to the GPU per visit."""
+    from paper_2608_27735_amd import train as TR
+    w = S.midscale_scene(n=n, n_cams=200)
+    cams = w.cams[::200 // n_cams][:n_cams]
+    t0 = time.perf_counter()
+    res = TR.compare(w.scene, S.perturbed(S.rng(6), w.scene), w.grid, w.cell_of, cams, w.params,
+                     epochs=1, T=T)
+    return dict(workload=f"{n} Gaussians (SH 3), mid-scale scene (4x4x2 grid), {n_cams} cameras "
+                         "at 1297x840; targets = joint renders of the ground truth; init = means "
+                         "jittered, opacity lowered, colours grey", steps_per_gaussian=T,
+                total_s=time.perf_counter() - t0, **res)
 
 
 def cpu_baseline(w, cam, prm, k):

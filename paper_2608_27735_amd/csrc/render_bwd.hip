@@ -26,8 +26,9 @@ __device__ __forceinline__ float dpp_mov(float x) {
 // Two such steps leave two registers, folded across lane bit 3 with one
 // keep/send select pair, and the 8-lane groups finish with three DPP adds
 // (quad xor 1, quad xor 2, row rotate 4). Value 8 takes the same steps on its
-// own. About 28 VALU instructions. On return each lane l with (l & 7) >= 4
-// holds the wave total of value sum9_slot(l) in `lo` and of value 8 in `v8`.
+// with DPP adds within rows and two row broadcasts. About 24 VALU
+// instructions. On return each lane l with (l & 7) >= 4 holds the wave total
+// of value sum9_slot(l) in `lo`, and lanes 48-63 the total of value 8 in `v8`.
 struct Sum9 {
   float lo, v8;
 };
@@ -52,21 +53,17 @@ __device__ __forceinline__ Sum9 wave_sum9(const float (&g)[9], int lane) {
   c += dpp_mov<0x4E>(c);   // quad [2,3,0,1]
   c += dpp_mov<0x124>(c);  // row rotate 4 (lane l reads l - 4): lanes with (l & 7) >= 4
                            // hold the 8-lane sum
-  float v8;
-  {
-    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(g[8]), __float_as_int(g[8]),
-                                                    false, false);
-    v8 = __int_as_float(p[0]) + __int_as_float(p[1]);
-  }
-  {
-    const auto p =
-        __builtin_amdgcn_permlane16_swap(__float_as_int(v8), __float_as_int(v8), false, false);
-    v8 = __int_as_float(p[0]) + __int_as_float(p[1]);
-  }
-  v8 += dpp_mov<0x128>(v8);
-  v8 += dpp_mov<0xB1>(v8);
-  v8 += dpp_mov<0x4E>(v8);
-  v8 += dpp_mov<0x124>(v8);
+  // value 8: row sums by DPP adds (every lane of a row ends with its row's
+  // sum), then row broadcasts: lane 15 into row 1, lane 47 into row 3 (rows 1
+  // and 3 now hold r0 + r1 and r2 + r3), then lane 31 into rows 2 and 3, so
+  // lanes 48-63 hold the wave total
+  float v8 = g[8];
+  v8 += dpp_mov<0xB1>(v8);   // quad [1,0,3,2]
+  v8 += dpp_mov<0x4E>(v8);   // quad [2,3,0,1]
+  v8 += dpp_mov<0x124>(v8);  // row rotate 4
+  v8 += dpp_mov<0x128>(v8);  // row rotate 8
+  v8 += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v8), 0x142, 0xA, 0xF, false));
+  v8 += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v8), 0x143, 0xC, 0xF, false));
   return Sum9{c, v8};
 }
 
@@ -155,10 +152,12 @@ __device__ __forceinline__ void bwd_item(
   }
   __syncthreads();
   const uint32_t nent = __builtin_amdgcn_readfirstlane(s_max);  // end of this item's walk
-  // lanes 4, 12, ..., 60 add values 0-7 of an entry, lane 5 value 8
+  // d out / d T_final enters every entry's alpha-derivative as T_final g_T / (1 - alpha)
+  const float TgT = Tfin * gT;
+  // lanes 4, 12, ..., 60 add values 0-7 of an entry, lane 48 value 8
   const int lane = tid & 63;
-  const bool adder = (lane & 7) == 4 || lane == 5;
-  const int slot = lane == 5 ? 8 : sum9_slot(lane);
+  const bool adder = (lane & 7) == 4 || lane == 48;
+  const int slot = lane == 48 ? 8 : sum9_slot(lane);
   uint32_t wml = lastp;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) wml = max(wml, (uint32_t)__shfl_xor((int)wml, off, 64));
@@ -258,7 +257,7 @@ __device__ __forceinline__ void bwd_item(
       gr[7] = wgt * gcg;
       gr[8] = wgt * gcb;
       const float CG = gb.z * gcr + gb.w * gcg + cbv[i] * gcb;
-      const float dLda = Tk * (CG - RG) - (Tfin * iom) * gT;
+      const float dLda = Tk * (CG - RG) - iom * TgT;
       RG = a * CG + om * RG;
       T = Tk;
       const float dm = (contrib && !ae.clamped) ? dLda : 0.0f;
@@ -273,7 +272,7 @@ __device__ __forceinline__ void bwd_item(
       gr[4] = r * dy;
       gr[5] = ae.e * dm;
       const Sum9 v = wave_sum9(gr, lane);
-      float out = lane == 5 ? v.v8 : v.lo;
+      float out = lane == 48 ? v.v8 : v.lo;
       asm volatile("" : "+v"(out));  // the last folds stay outside the branch (DPP add)
       if (adder) atomicAdd(&s_acc[9 * j + slot], out);
     }

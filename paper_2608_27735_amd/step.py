@@ -9,9 +9,11 @@ frozen-partition renders (composite_cache), done once per (block, camera).
 This class only owns buffers and issues the C-ABI calls in order on the
 current stream; it never synchronises unless asked for the intersection count.
 """
+import ctypes as C
+
 import torch
 
-from . import api
+from . import _lib, api
 
 
 class ActiveBlockStep:
@@ -20,6 +22,7 @@ class ActiveBlockStep:
     SPLIT_MIN_GAUSSIANS = 16384
 
     def __init__(self, cam, prm, params, capacity=None, headroom=1.25, bg=None, chunk="auto"):
+        self._fast = None
         self.cam, self.prm, self.params = cam, prm, params
         self.bg = bg
         n = params["means"].shape[0]
@@ -65,6 +68,73 @@ class ActiveBlockStep:
         if chunk:
             self.split = api.make_split(self._split_slots(capacity, chunk), chunk, dev)
 
+    @property
+    def cam(self):
+        return self._cam
+
+    @cam.setter
+    def cam(self, cam):
+        self._cam = cam
+        self._fast = None  # the prepared arguments hold the camera
+
+    def _prepared(self):
+        """ctypes arguments of the step's five calls, built once per camera and
+        set of buffers: a step then passes only F, B, the target and the
+        current stream (argument marshalling costs microseconds per call, which
+        adds up for small active blocks whose kernels take a few)."""
+        if self._fast is not None:
+            return self._fast
+        lib = _lib.load()
+        cam_s, prm_s = _lib.camera_struct(self.cam), _lib.params_struct(self.prm)
+        P, p, g = self.proj, self.params, self.grads
+        n = p["means"].shape[0]
+        W, H = self.cam.width, self.cam.height
+        dev = p["means"].device
+        nz = lambda t: api._ptr_nz(t, dev)
+        split = None
+        if self.split is not None:
+            ws = self.split["workspace"]
+            split = _lib.abcd_split(ws.data_ptr(), ws.numel(), int(self.split["chunk"]), 0)
+        sp = C.byref(split) if split is not None else None
+        bg = None if self.bg is None else (C.c_float * 3)(*[float(x) for x in self.bg])
+        params = [p[k].data_ptr() for k in ("means", "log_scales", "quats", "opacity_logits", "sh")]
+        self._fast = dict(
+            keep=(cam_s, prm_s, split, bg), lib=lib, W=W, H=H, bg=bg,
+            project=(C.byref(cam_s), C.byref(prm_s), n, *params, P["means2d"].data_ptr(),
+                     P["conic_opacity"].data_ptr(), P["depth"].data_ptr(),
+                     P["extent"].data_ptr(), P["tiles_touched"].data_ptr(), P["rgb"].data_ptr()),
+            bin=(W, H, n, P["means2d"].data_ptr(), P["extent"].data_ptr(), P["depth"].data_ptr(),
+                 P["tiles_touched"].data_ptr(), self.capacity, self.bin_ws.data_ptr(),
+                 self.bin_ws.numel(), None, nz(self.values), self.tile_ranges.data_ptr(),
+                 self.tile_order.data_ptr(), None),
+            fwd_pre=(C.byref(cam_s), C.byref(prm_s), self.tile_ranges.data_ptr(),
+                     self.tile_order.data_ptr(), nz(self.values), nz(P["means2d"]),
+                     nz(P["conic_opacity"]), nz(P["rgb"])),
+            fwd_post=(self.fwd["out"].data_ptr(), self.fwd["final_T"].data_ptr(),
+                      self.fwd["last"].data_ptr(), self.n_blends.data_ptr(), sp),
+            loss=(self.fwd["out"].data_ptr(),),
+            loss_post=(bg, self.dL_dout.data_ptr(), self.loss.data_ptr()),
+            bwd_pre=(C.byref(cam_s), C.byref(prm_s), n, *params, P["means2d"].data_ptr(),
+                     P["conic_opacity"].data_ptr(), P["rgb"].data_ptr(), P["extent"].data_ptr(),
+                     self.tile_ranges.data_ptr(), nz(self.values)),
+            bwd_post=(self.fwd["final_T"].data_ptr(), self.fwd["last"].data_ptr()),
+            bwd_tail=(self.bwd_ws.data_ptr(), self.bwd_ws.numel(),
+                      *[g[k].data_ptr() for k in ("means", "log_scales", "quats",
+                                                  "opacity_logits", "sh")],
+                      None, 0, sp),
+            checked=set())
+        return self._fast
+
+    def _image(self, t, name, channels, f):
+        """Shape/dtype/device check of an image argument, once per tensor."""
+        if t is None:
+            return None
+        if id(t) not in f["checked"]:
+            api._need(t, name, torch.float32, (self.cam.height, self.cam.width, channels))
+            f["checked"].add(id(t))
+            f.setdefault("alive", []).append(t)  # keeps the id from being reused
+        return t.data_ptr()
+
     def _split_slots(self, capacity, chunk):
         return capacity // (8 * chunk) + api.n_tiles(self.cam.width, self.cam.height) + 1
 
@@ -77,6 +147,7 @@ class ActiveBlockStep:
                          tile_order=self.tile_order,
                          sync=sync)
         if sync and b["values"] is not self.values:
+            self._fast = None
             self.values, self.bin_ws, self.capacity = b["values"], b["workspace"], b["capacity"]
             self.bins["values"] = self.values
             if self.split is not None:
@@ -106,11 +177,20 @@ class ActiveBlockStep:
                               split=self.split)
 
     def step(self, target, F=None, B=None):
-        """project -> bin -> forward -> L1 gradient -> backward (no synchronisation)."""
-        self.project_and_bin(sync=False)
-        self.forward(F, B)
-        self.loss_grad(target)
-        return self.backward(self.dL_dout, F, B)
+        """project -> bin -> forward -> L1 gradient -> backward (no synchronisation),
+        the same calls as project_and_bin(), forward(), loss_grad() and
+        backward() with their arguments prepared once (see _prepared)."""
+        f = self._prepared()
+        lib, st = f["lib"], api._stream()
+        Fp, Bp = self._image(F, "F", 4, f), self._image(B, "B", 4, f)
+        tp = self._image(target, "target", 3, f)
+        _lib.check(lib.abcd_project(*f["project"], st))
+        _lib.check(lib.abcd_bin_sort(*f["bin"], st))
+        _lib.check(lib.abcd_render_fwd(*f["fwd_pre"], Fp, Bp, *f["fwd_post"], st))
+        _lib.check(lib.abcd_loss_l1_grad(f["W"], f["H"], *f["loss"], tp, *f["loss_post"], st))
+        _lib.check(lib.abcd_render_bwd(*f["bwd_pre"], Fp, Bp, *f["bwd_post"], self.dL_dout.data_ptr(),
+                                       *f["bwd_tail"], st))
+        return self.grads
 
     def capture(self, target, F=None, B=None, before=None):
         """Record one step (and `before()`, e.g. the F/B collapse, ahead of it)

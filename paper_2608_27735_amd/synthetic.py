@@ -228,6 +228,28 @@ def midscale_block(seed=3, n=300_000, width=1297, height=840, n_cams=200, cam_in
                     order=grid.order_from(cam.campos), params=RasterParams(sh_degree=3))
 
 
+def midscale_scene(seed=31, n=5_000_000, width=1297, height=840, n_cams=200):
+    """The whole mid-scale scene: n Gaussians over a 4x4x2 grid on
+    [-10, 10]^2 x [0, 6], 40% on a ground plane (z uniform on [0, 0.1]) and 60%
+    in 64 Gaussian blobs (sd 0.5, centres uniform in the box, clipped to it),
+    log-scales N(log 0.2, 0.5) (0.01 of the 20-unit extent), SH degree 3;
+    cameras on the ellipse (16 cos p, 12 sin p, 5) looking at (0, 0, 1.5)."""
+    r = rng(seed)
+    grid = Grid((-10.0, -10.0, 0.0), (10.0, 10.0, 6.0), (4, 4, 2))
+    lo, hi = grid.lo, grid.hi
+    n_ground = int(0.4 * n)
+    ground = np.stack([r.uniform(lo[0], hi[0], n_ground), r.uniform(lo[1], hi[1], n_ground),
+                       r.uniform(0.0, 0.1, n_ground)], axis=1)
+    centres = r.uniform(lo, hi, (64, 3))
+    comp = r.integers(0, 64, n - n_ground)
+    blobs = np.clip(centres[comp] + r.normal(0.0, 0.5, (n - n_ground, 3)), lo, hi - 1e-6)
+    scene = gaussians(r, np.concatenate([ground, blobs]), 3, math.log(0.2), 0.5)
+    cams = [look_at((16.0 * math.cos(2 * math.pi * k / n_cams), 12.0 * math.sin(2 * math.pi * k / n_cams),
+                     5.0), (0, 0, 1.5), width, height) for k in range(n_cams)]
+    return Workload(scene=scene, cams=cams, grid=grid, cell_of=grid.cell_of(scene["means"]),
+                    params=RasterParams(sh_degree=3))
+
+
 def stress_block(seed=5, n=4_000_000, width=2560, height=1440, n_cams=200, cam_index=0):
     """The stress configuration's active block: an 8x8x2 grid over [-20, 20]^2 x
     [0, 10]; the active cell (3, 3, 0) holds n Gaussians with means uniform in

@@ -92,3 +92,89 @@ def test_training_setups(setup):
     assert res["abcd"]["psnr_after"] > res["abcd"]["psnr_before"] + 1.0
     assert res["joint"]["psnr_after"] > res["joint"]["psnr_before"] + 1.0
     assert res["abcd"]["psnr_after"] > res["ablated"]["psnr_after"] + 1.0
+
+
+def _slabs(cam, scene, n=3):
+    """Partition by view depth of the means (quantiles): every Gaussian of a
+    nearer slab precedes every one of a farther slab in every tile's list, so
+    the slabs are depth-separated partitions."""
+    Rc = np.asarray(cam.R, np.float64).reshape(3, 3)
+    z = scene["means"].astype(np.float64) @ Rc[2] + float(cam.t[2])
+    return np.searchsorted(np.quantile(z, np.linspace(0, 1, n + 1)[1:-1]), z)
+
+
+@pytest.mark.parametrize("mode", ["fp32-fb-no-stop", "fp32-fb-stop", "fp16-cache-no-stop"])
+def test_partition_composite_matches_oracle_joint_render(mode):
+    """The paper's equivalence on the GPU, anchored to the oracle (Method
+    section: the active partition rendered between F and B stands for the
+    render with every partition present). The 4,096-Gaussian scene is split
+    into three slabs by view depth; F and B are the GPU's renders of the near
+    and far slab (fp32 images, or fp16 cached renders collapsed by
+    composite_cache); the GPU renders the middle slab between them. The
+    result is compared per pixel with the oracle's fp64 render of all 4,096
+    Gaussians at once: within 1e-5 without early termination; with it, within
+    the joint render's transmittance at its stop (the slabs stop on their own
+    transmittance); with fp16 caches, within the first-order effect of
+    binary16 rounding of F and B on the composite. Knife-edge pixels (a
+    threshold decision within the fp32 error bound) are excluded and must be
+    few."""
+    from oracle import oracle as O
+    from paper_2608_27735_amd import api
+    from paper_2608_27735_amd.camera import RasterParams
+    say("slab composite vs oracle joint render", mode)
+    w = S.tiny()
+    cam = w.cams[0]
+    prm = RasterParams(sh_degree=0, t_min=1e-4 if mode == "fp32-fb-stop" else 0.0)
+    sc = w.scene
+    lab = _slabs(cam, sc)
+    H, W = cam.height, cam.width
+
+    def gpu_parts(sub):
+        p = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev()) for k, v in sub.items()}
+        proj = api.project(cam, prm, **p)
+        return proj, api.bin_sort(W, H, proj)
+
+    near, mid, far = (S.subset(sc, lab == k) for k in range(3))
+    pn, bn = gpu_parts(near)
+    pm, bm = gpu_parts(mid)
+    pf, bf = gpu_parts(far)
+    if mode.startswith("fp32"):
+        F = api.render_fwd(cam, prm, bn, pn)["out"]
+        B = api.render_fwd(cam, prm, bf, pf)["out"]
+    else:
+        imgs = torch.empty((2, H, W, 4), dtype=torch.float16, device=dev())
+        api.render_cache(cam, prm, bn, pn, image=imgs[0])
+        api.render_cache(cam, prm, bf, pf, image=imgs[1])
+        F, B = api.composite_cache(imgs, [0, 1], 1)
+    out = api.render_fwd(cam, prm, bm, pm, F=F, B=B)["out"].cpu().numpy().astype(np.float64)
+    torch.cuda.synchronize()
+    joint = O.step(cam, prm, sc, rel_margin=2e-6)
+    ref = joint["fwd"]["out"]
+    # knife-edge pixels of the joint render (its decisions are the slabs')
+    kn = O.render_fwd(cam, prm, joint["tile_ranges"], joint["sorted_values"],
+                      joint["means2d_used"], joint["values"]["conic"], joint["values"]["opacity"],
+                      joint["values"]["rgb"], rel_margin=2e-6, f32_kappa=8.0)["knife"]
+    err = np.abs(out - ref)
+    if mode == "fp32-fb-no-stop":
+        bound = np.full((H, W, 1), 1e-5)
+    elif mode == "fp32-fb-stop":
+        bound = (joint["fwd"]["t_stop"] * (1.0 + ref[..., :3].max(-1)))[..., None] + 1e-5
+    else:
+        # binary16 rounding of F and B (relative 2^-11), carried to first order
+        alone = O.step(cam, prm, mid)["fwd"]
+        C, T = alone["out"][..., :3], alone["final_T"][..., None]
+        Fh, Bh = F.cpu().numpy().astype(np.float64), B.cpu().numpy().astype(np.float64)
+        eF, eB = 2.0 ** -11 * np.abs(Fh) + 2.0 ** -24, 2.0 ** -11 * np.abs(Bh) + 2.0 ** -24
+        s = 1.0 - Fh[..., 3:]
+        b_rgb = eF[..., :3] + eF[..., 3:] * np.abs(C + T * Bh[..., :3]) + s * T * eB[..., :3]
+        b_a = eF[..., 3:] * (1 + np.abs(1 - T * (1 - Bh[..., 3:]))) + s * T * eB[..., 3:]
+        bound = np.concatenate([b_rgb, b_a], -1) + 1e-5
+    ok = ~kn
+    excess = (err - bound)[ok]
+    print(f"  max |gpu composite - oracle joint| {err[ok].max():.2e}, max excess over the bound "
+          f"{excess.max():.2e}, knife-edge pixels {int(kn.sum())} of {kn.size}")
+    assert np.all(excess <= 0.0)
+    assert kn.sum() <= 0.02 * kn.size
+    # the partition alone is far from the joint render: the composite is what matches
+    alone_gpu = api.render_fwd(cam, prm, bm, pm)["out"].cpu().numpy()
+    assert np.abs(alone_gpu - ref)[ok].max() > 100 * max(float(err[ok].max()), 1e-6)
