@@ -73,18 +73,30 @@ __device__ __forceinline__ void fold(const uint2* __restrict__ img, int64_t npix
       live = (1.0f - a0.w) * vis0 >= stop_t || (kPair && (1.0f - a1.w) * vis1 >= stop_t);
       if (!__ballot(live)) break;  // wave-uniform
     }
+    // which of the batch's layers any pixel of the wave needs (a wave-uniform
+    // mask): layers whose box misses the whole wave cost no load and no fold
+    bool need[kBatch];
+    uint32_t wave_needs = 0;
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      need[b] = false;
+      if (b < m) {
+        need[b] = live;
+        if (rects) {
+          const int4 r = rects[tab.idx[first + j0 + b]];
+          need[b] = need[b] && (in_rect(r, pos.x0, pos.y0) || (kPair && in_rect(r, pos.x1, pos.y1)));
+        }
+        if (__ballot(need[b])) wave_needs |= 1u << b;
+      }
+    }
+    wave_needs = __builtin_amdgcn_readfirstlane(wave_needs);
     uint4 v[kBatch];
 #pragma unroll
     for (int b = 0; b < kBatch; ++b) {
-      if (b < m) {
+      v[b] = make_uint4(0u, 0u, 0u, 0u);
+      if ((wave_needs >> b) & 1u) {
         const int idx = tab.idx[first + j0 + b];
-        bool need = live;
-        if (rects) {
-          const int4 r = rects[idx];
-          need = need && (in_rect(r, pos.x0, pos.y0) || (kPair && in_rect(r, pos.x1, pos.y1)));
-        }
-        v[b] = make_uint4(0u, 0u, 0u, 0u);
-        if (need) {
+        if (need[b]) {
           const uint2* src = img + (int64_t)idx * npix + pp;
           if (kPair) {
             const u4v t = __builtin_nontemporal_load(reinterpret_cast<const u4v*>(src));
@@ -98,7 +110,7 @@ __device__ __forceinline__ void fold(const uint2* __restrict__ img, int64_t npix
     }
 #pragma unroll
     for (int b = 0; b < kBatch; ++b) {
-      if (b < m) {
+      if ((wave_needs >> b) & 1u) {
         if (!kStop || (1.0f - a0.w) * vis0 >= stop_t) over(a0, to_f4(make_uint2(v[b].x, v[b].y)));
         if (kPair && (!kStop || (1.0f - a1.w) * vis1 >= stop_t))
           over(a1, to_f4(make_uint2(v[b].z, v[b].w)));

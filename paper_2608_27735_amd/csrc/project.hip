@@ -333,6 +333,28 @@ __device__ __forceinline__ void sh_stage_in(const float* __restrict__ sh, int64_
                                             float* s) {
   using Tl = ShTile<D>;
   const float* src = sh + base * Tl::kFloats;
+  if constexpr (Tl::kFloats % 4 == 0) {
+    // 16-byte loads when the group's block is 16-byte aligned (a quarter of
+    // the load instructions; degrees 1 and 3)
+    if (cnt == kProjThreads && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+      constexpr int kVec = Tl::kFloats / 4;
+      float4 v[kVec];
+#pragma unroll
+      for (int r = 0; r < kVec; ++r)
+        v[r] = reinterpret_cast<const float4*>(src)[threadIdx.x + kProjThreads * r];
+#pragma unroll
+      for (int r = 0; r < kVec; ++r) {
+        const int e = 4 * (threadIdx.x + kProjThreads * r);
+        const int g = e / Tl::kFloats;  // the four floats share a Gaussian (kFloats % 4 == 0)
+        float* row = s + g * Tl::kStride + (e - g * Tl::kFloats);
+        row[0] = v[r].x;
+        row[1] = v[r].y;
+        row[2] = v[r].z;
+        row[3] = v[r].w;
+      }
+      return;
+    }
+  }
   if (cnt == kProjThreads) {
     float v[Tl::kFloats];
 #pragma unroll
@@ -356,6 +378,35 @@ template <int D>
 __device__ __forceinline__ void sh_stage_out(const float* s, int cnt, int accumulate,
                                              float* __restrict__ dst) {
   using Tl = ShTile<D>;
+  if constexpr (Tl::kFloats % 4 == 0) {
+    if (cnt == kProjThreads && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+      constexpr int kVec = Tl::kFloats / 4;
+      float4* d4 = reinterpret_cast<float4*>(dst);
+      float4 v[kVec];
+#pragma unroll
+      for (int r = 0; r < kVec; ++r) {
+        const int e = 4 * (threadIdx.x + kProjThreads * r);
+        const int g = e / Tl::kFloats;
+        const float* row = s + g * Tl::kStride + (e - g * Tl::kFloats);
+        v[r] = make_float4(row[0], row[1], row[2], row[3]);
+      }
+      if (accumulate) {
+        float4 a[kVec];
+#pragma unroll
+        for (int r = 0; r < kVec; ++r) a[r] = d4[threadIdx.x + kProjThreads * r];
+#pragma unroll
+        for (int r = 0; r < kVec; ++r) {
+          v[r].x += a[r].x;
+          v[r].y += a[r].y;
+          v[r].z += a[r].z;
+          v[r].w += a[r].w;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < kVec; ++r) d4[threadIdx.x + kProjThreads * r] = v[r];
+      return;
+    }
+  }
   if (cnt == kProjThreads) {
     float v[Tl::kFloats];
 #pragma unroll
