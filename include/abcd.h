@@ -266,7 +266,8 @@ ABCD_API int32_t abcd_render_cache(const abcd_camera* cam /* host */,
  * forward above, including zero derivative of a clamped alpha and of a
  * clamped colour. Inputs are those of the forward call on the same camera.
  * workspace: at least abcd_render_bwd_workspace_size(n) bytes, 256-byte
- * aligned (screen-space gradients, 36 bytes per Gaussian, and the work
+ * aligned (screen-space gradients, 36 bytes per Gaussian with n rounded up
+ * to a multiple of 1024, and the work
  * schedule of the backward, heaviest walk first, 16 bytes per tile at the
  * maximum tile count). split (host, may be NULL): the one the forward used. */
 ABCD_API int32_t abcd_render_bwd_workspace_size(int64_t n, size_t* bytes);

@@ -281,12 +281,14 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
                         uint32_t* tile_ranges, uint32_t* tile_order, hipStream_t stream);
 
 // render_fwd.hip, render_bwd.hip, loss.hip
-// The backward's workspace: g2d[n][9] fp32 (256-byte aligned), then per tile
-// the work estimate, the order and the work items (when not split), then the
-// queue counters.
-constexpr size_t bwd_g2d_bytes(int64_t n) {
-  return ((size_t)9 * sizeof(float) * (size_t)n + 255) & ~size_t(255);
-}
+// The backward's workspace: the screen-space gradients g2d, field-major
+// (field q of Gaussian i at q * g2d_stride(n) + i, fp32), then per tile the
+// work estimate, the order and the work items (when not split), then the
+// queue counters. Field-major, the nine atomic adds of one Gaussian fall on
+// nine cache lines instead of one or two (adds to one line are serialised in
+// L2); the stride is a multiple of 1024 floats.
+constexpr int64_t g2d_stride(int64_t n) { return (n + 1023) & ~int64_t(1023); }
+constexpr size_t bwd_g2d_bytes(int64_t n) { return (size_t)9 * sizeof(float) * (size_t)g2d_stride(n); }
 constexpr size_t bwd_workspace_bytes(int64_t n) {
   return bwd_g2d_bytes(n) + 2 * sizeof(uint32_t) * ABCD_MAX_TILES + 8 * (size_t)ABCD_MAX_TILES +
          sizeof(uint32_t) * 64 * 8;

@@ -503,8 +503,8 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(
   rgb[3 * i + 2] = fmaxf(col[2], 0.0f);
 }
 
-// Chain rule from the screen-space gradients g2d[i][9] = dL/d(u, v, a, b, c,
-// o, r, g, b) to the parameters; exact derivative of the forward chain
+// Chain rule from the screen-space gradients dL/d(u, v, a, b, c, o, r, g, b)
+// (field q of Gaussian i at g2d[q * g2d_stride(n) + i]) to the parameters; exact derivative of the forward chain
 // (guard-band clamp and colour clamp have zero derivative where active).
 template <int D>
 __global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
@@ -533,7 +533,7 @@ __global__ __launch_bounds__(kProjThreads) void project_bwd_kernel(
     q4 = *reinterpret_cast<const float4*>(quats + 4 * i);
     ologit = opacity_logits[i];
 #pragma unroll
-    for (int k = 0; k < 9; ++k) G[k] = g2d[9 * i + k];
+    for (int k = 0; k < 9; ++k) G[k] = g2d[k * g2d_stride(n) + i];
   }
   sh_stage_in<D>(sh, base, cnt, s_sh);
   __syncthreads();

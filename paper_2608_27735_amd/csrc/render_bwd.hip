@@ -84,7 +84,7 @@ __device__ __forceinline__ void bwd_item(
     const float4* __restrict__ conic_opacity, const float* __restrict__ rgb,
     const float4* __restrict__ F, const float4* __restrict__ B, const float* __restrict__ final_T,
     const uint32_t* __restrict__ last, const float4* __restrict__ dL_dout, float* __restrict__ g2d,
-    const SplitLayout& sp) {
+    int64_t gs, const SplitLayout& sp) {
   __shared__ float4 s_ga[256];  // u, v, qa, qb
   __shared__ float4 s_gb[256];  // qc, o, r, g
   __shared__ float4 s_gc[256];  // a, b, c (conic), colour b
@@ -292,10 +292,10 @@ __device__ __forceinline__ void bwd_item(
       g[2] = -0.5f * g[2];
       g[3] = -g[3];
       g[4] = -0.5f * g[4];
-      float* dst = g2d + 9 * (int64_t)s_g[tid];
+      float* dst = g2d + s_g[tid];
 #pragma unroll
       for (int q = 0; q < 9; ++q)
-        if (g[q] != 0.0f) atomicAdd(dst + q, g[q]);
+        if (g[q] != 0.0f) atomicAdd(dst + q * gs, g[q]);
     }
     bend = bbeg;
   }
@@ -308,7 +308,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void r
     const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
     const float* __restrict__ final_T, const uint32_t* __restrict__ last,
-    const float4* __restrict__ dL_dout, float* __restrict__ g2d, const uint2* __restrict__ items,
+    const float4* __restrict__ dL_dout, float* __restrict__ g2d, int64_t gs,
+    const uint2* __restrict__ items,
     uint32_t* __restrict__ queue, uint32_t max_items, SplitLayout sp) {
   __shared__ uint2 s_item;
   const uint32_t n_items = min(queue[0], max_items);
@@ -336,7 +337,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void r
     if (it.x == kNoSlot) break;
     if (it.x < (uint32_t)k.ntiles)
       bwd_item(k, (int)it.x, it.y, tile_ranges, values, means2d, conic_opacity, rgb, F, B,
-               final_T, last, dL_dout, g2d, sp);
+               final_T, last, dL_dout, g2d, gs, sp);
   }
 }
 
@@ -350,16 +351,16 @@ __global__ __launch_bounds__(256) void render_bwd_direct_kernel(
     const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
     const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
     const float* __restrict__ final_T, const uint32_t* __restrict__ last,
-    const float4* __restrict__ dL_dout, float* __restrict__ g2d) {
+    const float4* __restrict__ dL_dout, float* __restrict__ g2d, int64_t gs) {
   bwd_item(k, (int)blockIdx.x, 0u, tile_ranges, values, means2d, conic_opacity, rgb, F, B, final_T,
-           last, dL_dout, g2d, SplitLayout{});
+           last, dL_dout, g2d, gs, SplitLayout{});
 }
 
 }  // namespace
 
 static_assert(kQueueStride * kQueues == 64 * 8, "queue block of bwd_workspace_bytes");
 
-// g2d[n][9], then the backward's tile work, tile order, work items (when
+// g2d (field-major), then the backward's tile work, tile order, work items (when
 // not split) and queue.
 size_t render_bwd_workspace_bytes(int64_t n) { return bwd_workspace_bytes(n); }
 
@@ -397,7 +398,7 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
                 tile_ranges, values_sorted, reinterpret_cast<const float2*>(means2d),
                 reinterpret_cast<const float4*>(conic_opacity), rgb,
                 reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B), final_T,
-                last, reinterpret_cast<const float4*>(dL_dout), g2d);
+                last, reinterpret_cast<const float4*>(dL_dout), g2d, g2d_stride(n));
     ABCD_HIP(hipGetLastError());
     return ABCD_OK;
   }
@@ -424,7 +425,8 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
               values_sorted, reinterpret_cast<const float2*>(means2d),
               reinterpret_cast<const float4*>(conic_opacity), rgb,
               reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B), final_T,
-              last, reinterpret_cast<const float4*>(dL_dout), g2d, items, queue, max_items, split);
+              last, reinterpret_cast<const float4*>(dL_dout), g2d, g2d_stride(n), items, queue,
+              max_items, split);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }
