@@ -130,7 +130,7 @@ __device__ __forceinline__ AlphaEval eval_alpha(float dx, float dy, float qa, fl
   r.e = __builtin_amdgcn_exp2f(p2);
   const float raw = o * r.e;
   r.clamped = raw > alpha_max;
-  r.alpha = r.clamped ? alpha_max : raw;
+  r.alpha = fminf(raw, alpha_max);  // raw is finite: the clamp
   r.skip = (p2 > 0.0f) || (r.alpha < alpha_min);
   return r;
 }

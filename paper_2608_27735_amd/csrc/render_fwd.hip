@@ -11,6 +11,8 @@
 // alpha >= alpha_min ellipse reaches its rows: the others cannot blend at any
 // of its pixels, so the result is the same, and in tiles of many small
 // Gaussians a wave's walk is a fraction of the tile's list.
+#include <type_traits>
+
 #include "blend.h"
 
 namespace abcd {
@@ -57,6 +59,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
     thr = vis > 0.0f ? k.t_min / vis : __builtin_huge_valf();
     done = vis < k.t_min;
   }
+  // alpha below which the lane blends nothing: alpha_min, infinite once the
+  // pixel has stopped
+  float amin_l = done ? __builtin_huge_valf() : k.alpha_min;
   if (tid == 0) {
     s_nb = 0;
     s_walk = 0;
@@ -127,24 +132,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
     rec = gather_rec(gid_next, nxt < end, means2d, conic_opacity, rgb);
     gid_next = gid_after;
     if (__ballot(!done)) {
-      // Lanes step through the entries together without divergent branches:
-      // a lane that skips an entry, or has stopped, blends with weight 0.
-      // Entries are read from LDS kGroup at a time, all reads issued before
-      // the first is used, so the LDS latency is paid once per group. The
-      // wave walks its own list of staged slots; slots past its end hold
-      // stale bytes, which still index s_ga.
+      // The wave walks its own list of staged slots, kGroup entries at a
+      // time; all LDS reads of a group are issued before the first is used,
+      // so the LDS latency is paid once per group.
       static_assert(kGroup % 4 == 0, "slot indices are read four at a time");
       const uint32_t* my_idx = reinterpret_cast<const uint32_t*>(s_idx[tid >> 6]);
       int jl = -1;  // position in the wave's list of the last entry the lane blended
-      for (int j0 = 0; j0 < wcnt; j0 += kGroup) {
-        float4 ga[kGroup], gb[kGroup];
-        float bl[kGroup];
+      // One group; kTail: the list ends inside it, and positions past the end
+      // read the group's first entry and blend nothing (every value read is
+      // finite). Returns true when no pixel of the wave is left.
+      auto group = [&](const int j0, auto tail) -> bool {
+        constexpr bool kTail = decltype(tail)::value;
         uint32_t iw[kGroup / 4];
 #pragma unroll
-        for (int h = 0; h < kGroup / 4; ++h) iw[h] = my_idx[j0 / 4 + h];
+        for (int h = 0; h < kGroup / 4; ++h) iw[h] = __builtin_amdgcn_readfirstlane(my_idx[j0 / 4 + h]);
+        float4 ga[kGroup], gb[kGroup];
+        float bl[kGroup];
 #pragma unroll
         for (int i = 0; i < kGroup; ++i) {
-          const int j = (int)((iw[i >> 2] >> (8 * (i & 3))) & 255u);
+          int j = (int)((iw[i >> 2] >> (8 * (i & 3))) & 255u);
+          if (kTail && j0 + i >= wcnt) j = (int)(iw[0] & 255u);
           ga[i] = s_ga[j];
           gb[i] = s_gb[j];
           bl[i] = s_bl[j].x;
@@ -155,29 +162,47 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
         for (int i = 0; i < kGroup; ++i)
           asm volatile("" ::"v"(ga[i].x), "v"(ga[i].y), "v"(ga[i].z), "v"(ga[i].w), "v"(gb[i].x),
                        "v"(gb[i].y), "v"(gb[i].z), "v"(gb[i].w), "v"(bl[i]));
+        // alpha of each entry at this pixel, 0 where the lane does not blend
+        // it: below alpha_min (eval_alpha's skip: its power is minus a sum of
+        // squares, never positive), or the pixel has stopped (amin_l = inf)
+        float a[kGroup];
 #pragma unroll
         for (int i = 0; i < kGroup; ++i) {
-          const bool valid = j0 + i < wcnt;  // past the list: a no-op step
           const AlphaEval ae = eval_alpha(fx - ga[i].x, fy - ga[i].y, ga[i].z, ga[i].w, gb[i].x,
                                           gb[i].y, k.alpha_min, k.alpha_max);
-          // T (1 - alpha) with one rounding
-          const float Tn = fmaf(-T, ae.alpha, T);
-          const bool hit = valid && !done && !ae.skip;
-          const bool stop = hit && Tn < thr;
-          const bool blend = hit && !stop;
-          done = done || stop;
-          // selects, not a zero weight: entries past the batch hold stale
-          // shared memory, which may not be finite
-          const float wgt = ae.alpha * T;
-          cr = blend ? cr + gb[i].z * wgt : cr;
-          cg = blend ? cg + gb[i].w * wgt : cg;
-          cb = blend ? cb + bl[i] * wgt : cb;
-          T = blend ? Tn : T;
+          a[i] = ae.alpha < amin_l ? 0.0f : ae.alpha;
+          if (kTail && j0 + i >= wcnt) a[i] = 0.0f;
+        }
+        // The chain Tc of every hit blended, T (1 - alpha) with one rounding
+        // (exactly T where alpha = 0), holds the values of the entry-by-entry
+        // walk up to its first stop. T never increases and only hits change
+        // it, so an entry blends exactly when its next value is still at or
+        // above the threshold (ok): the first hit below stops the pixel and
+        // every later value is below too. No branch depends on the stop.
+        float Tc = T;
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) {
+          const float Tn = fmaf(-Tc, a[i], Tc);
+          const bool ok = Tn >= thr;
+          // a zero weight adds exactly zero (colours are finite and >= 0)
+          const float wgt = ok ? a[i] * Tc : 0.0f;
+          cr = fmaf(gb[i].z, wgt, cr);
+          cg = fmaf(gb[i].w, wgt, cg);
+          cb = fmaf(bl[i], wgt, cb);
+          const bool blend = ok && a[i] != 0.0f;
           jl = blend ? j0 + i : jl;
           nb += blend ? 1u : 0u;
+          T = ok ? Tn : T;
+          Tc = Tn;
         }
-        if (!__ballot(!done)) break;  // wave-uniform
-      }
+        done = done || Tc < thr;
+        amin_l = done ? __builtin_huge_valf() : amin_l;
+        return !__ballot(!done);
+      };
+      int j0 = 0;
+      bool over = false;
+      for (; j0 + kGroup <= wcnt && !over; j0 += kGroup) over = group(j0, std::false_type{});
+      if (!over && j0 < wcnt) group(j0, std::true_type{});
       if (jl >= 0) lastk = (uint32_t)s_pos[s_idx[tid >> 6][jl]] + 1;
     }
     // s_wcnt is rewritten only after the next barrier
