@@ -25,9 +25,8 @@ __device__ __forceinline__ float dpp_mov(float x) {
 // 2q in the lower half (even rows) and 2q + 1 in the upper half (odd rows).
 // Two such steps leave two registers, folded across lane bit 3 with one
 // keep/send select pair, and the 8-lane groups finish with three DPP adds
-// (quad xor 1, quad xor 2, row rotate 4). Value 8 takes the same steps on its
-// with DPP adds within rows and two row broadcasts. About 24 VALU
-// instructions. On return each lane l with (l & 7) >= 4 holds the wave total
+// (quad xor 1, quad xor 2, row rotate 4). Value 8 is summed by DPP adds
+// within rows and two row-broadcast adds. About 20 VALU instructions. On return each lane l with (l & 7) >= 4 holds the wave total
 // of value sum9_slot(l) in `lo`, and lanes 48-63 the total of value 8 in `v8`.
 struct Sum9 {
   float lo, v8;
@@ -54,16 +53,17 @@ __device__ __forceinline__ Sum9 wave_sum9(const float (&g)[9], int lane) {
   c += dpp_mov<0x124>(c);  // row rotate 4 (lane l reads l - 4): lanes with (l & 7) >= 4
                            // hold the 8-lane sum
   // value 8: row sums by DPP adds (every lane of a row ends with its row's
-  // sum), then row broadcasts: lane 15 into row 1, lane 47 into row 3 (rows 1
-  // and 3 now hold r0 + r1 and r2 + r3), then lane 31 into rows 2 and 3, so
-  // lanes 48-63 hold the wave total
+  // sum), then two row-broadcast adds over all rows: lane 15 of each row into
+  // the next (row 3 now holds r2 + r3, row 1 r0 + r1), then lane 31 into rows
+  // 2 and 3, so lanes 48-63 hold the wave total (the other rows hold partial
+  // sums, which are not used)
   float v8 = g[8];
   v8 += dpp_mov<0xB1>(v8);   // quad [1,0,3,2]
   v8 += dpp_mov<0x4E>(v8);   // quad [2,3,0,1]
   v8 += dpp_mov<0x124>(v8);  // row rotate 4
   v8 += dpp_mov<0x128>(v8);  // row rotate 8
-  v8 += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v8), 0x142, 0xA, 0xF, false));
-  v8 += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v8), 0x143, 0xC, 0xF, false));
+  v8 += dpp_mov<0x142>(v8);  // row broadcast 15
+  v8 += dpp_mov<0x143>(v8);  // row broadcast 31
   return Sum9{c, v8};
 }
 
