@@ -106,6 +106,7 @@ __device__ __forceinline__ Splat make_splat(float2 m, float4 co) {
 }
 
 // The conic (a, b, c) = L L^T of a factor (l11, l21, l22): for the tile test
+// (splat_rows)
 // and the chain rule to the mean.
 __device__ __forceinline__ float3 conic_of(float4 co) {
   return make_float3(co.x * co.x, co.x * co.y, co.y * co.y + co.z * co.z);
@@ -133,34 +134,6 @@ __device__ __forceinline__ AlphaEval eval_alpha(float dx, float dy, float qa, fl
   r.alpha = fminf(raw, alpha_max);  // raw is finite: the clamp
   r.skip = (p2 > 0.0f) || (r.alpha < alpha_min);
   return r;
-}
-
-// Conservative tile test: can any pixel centre of the box [bx0, bx1] x [by0,
-// by1] see this Gaussian with alpha >= alpha_min? That needs
-// d^T Q d <= tau = 2 ln(o / alpha_min) for some centre; the minimum of the
-// convex quadratic over the box is 0 if the mean is inside, else it lies on
-// an edge, where the one-dimensional minimiser is clamped. The margin keeps
-// every entry whose per-pixel decision could go either way in fp32.
-__device__ __forceinline__ bool splat_touches_box(float u, float v, float a, float b, float c,
-                                                  float o, float alpha_min, float bx0, float bx1,
-                                                  float by0, float by1) {
-  if (!(o >= alpha_min)) return false;
-  const float dx0 = bx0 - u, dx1 = bx1 - u, dy0 = by0 - v, dy1 = by1 - v;
-  if (dx0 <= 0.0f && dx1 >= 0.0f && dy0 <= 0.0f && dy1 >= 0.0f) return true;
-  const float tau = 2.0f * (__logf(o) - __logf(alpha_min));
-  const float lim = tau * 1.001f + 1e-3f;
-  float best = 3.4e38f;
-  const float ia = a > 0.0f ? 1.0f / a : 0.0f, ic = c > 0.0f ? 1.0f / c : 0.0f;
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const float dx = k ? dx1 : dx0;
-    const float dy = fminf(fmaxf(-b * dx * ic, dy0), dy1);
-    best = fminf(best, a * dx * dx + 2.0f * b * dx * dy + c * dy * dy);
-    const float ey = k ? dy1 : dy0;
-    const float ex = fminf(fmaxf(-b * ey * ia, dx0), dx1);
-    best = fminf(best, a * ex * ex + 2.0f * b * ex * ey + c * ey * ey);
-  }
-  return best <= lim;
 }
 
 // Wave64 sum with DPP row operations; the total is returned to every lane.

@@ -91,16 +91,33 @@ __device__ __forceinline__ int compact(bool keep, int* s_wcnt, int& pos) {
   return __builtin_amdgcn_readfirstlane(tot);  // uniform: loops over it branch on scalars
 }
 
-// Rows mask of a kept entry: bit w set when its ellipse (the margin of
-// splat_touches_box included) reaches pixel rows 4w .. 4w + 3 of the tile.
-__device__ __forceinline__ uint32_t rows_reached(float u, float v, float a, float b, float c,
-                                                 float o, float alpha_min, const TileBox& box) {
+// Tile test and rows mask of an entry in one: bit w set when some pixel
+// centre of rows 4w .. 4w + 3 of the tile (clipped to the image) can see the
+// Gaussian with alpha >= alpha_min, i.e. d^T Q d <= tau = 2 ln(o / alpha_min);
+// 0: the entry is dropped. With the tile's column range fixed, the minimum of
+// the convex quadratic over dx is a convex function of dy whose minimiser y*
+// is 0 when the mean's column lies in the range, else -b dx_e / c on the
+// nearer edge dx_e; the minimum over a band is at y* clamped to the band, with
+// dx = -b dy / a clamped to the columns. The margin keeps every entry whose
+// per-pixel decision could go either way in fp32 (no pixel that blends is
+// ever dropped, so the outputs do not depend on this test).
+__device__ __forceinline__ uint32_t splat_rows(float u, float v, float a, float b, float c, float o,
+                                               float alpha_min, const TileBox& box) {
+  if (!(o >= alpha_min)) return 0u;
+  const float tau = 2.0f * (__logf(o) - __logf(alpha_min));
+  const float lim = tau * 1.001f + 1e-3f;
+  const float ia = a > 0.0f ? 1.0f / a : 0.0f, ic = c > 0.0f ? 1.0f / c : 0.0f;
+  const float dx0 = box.x0 - u, dx1 = box.x1 - u;
+  const float dxe = dx0 > 0.0f ? dx0 : (dx1 < 0.0f ? dx1 : 0.0f);
+  const float ys = -b * dxe * ic;
   uint32_t rows = 0;
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    const float y0 = box.y0 + 4.0f * (float)w, y1 = fminf(box.y1, y0 + 3.0f);
-    if (y0 <= y1 && splat_touches_box(u, v, a, b, c, o, alpha_min, box.x0, box.x1, y0, y1))
-      rows |= 1u << w;
+    const float yb0 = box.y0 + 4.0f * (float)w, yb1 = fminf(box.y1, yb0 + 3.0f);
+    const float dy = fminf(fmaxf(ys, yb0 - v), yb1 - v);
+    const float dx = fminf(fmaxf(-b * dy * ia, dx0), dx1);
+    const float q = a * dx * dx + 2.0f * b * dx * dy + c * dy * dy;
+    if (yb0 <= yb1 && q <= lim) rows |= 1u << w;
   }
   return rows;
 }

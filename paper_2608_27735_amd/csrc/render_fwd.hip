@@ -110,10 +110,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
       }
     }
     const float3 cn = conic_of(rec.co);
-    const bool keep = rec.valid && splat_touches_box(rec.m.x, rec.m.y, cn.x, cn.y, cn.z, rec.co.w,
-                                                     k.alpha_min, box.x0, box.x1, box.y0, box.y1);
+    // each wave walks only the staged entries whose ellipse reaches its four
+    // pixel rows: the others contribute nothing to any of its pixels
     const uint32_t rows =
-        keep ? rows_reached(rec.m.x, rec.m.y, cn.x, cn.y, cn.z, rec.co.w, k.alpha_min, box) : 0u;
+        rec.valid ? splat_rows(rec.m.x, rec.m.y, cn.x, cn.y, cn.z, rec.co.w, k.alpha_min, box) : 0u;
+    const bool keep = rows != 0u;
     int pos, wcnt;
     const int cnt = compact_rows(keep, rows, s_wcnt, s_idx, pos, wcnt);
     staged += (uint32_t)cnt;
