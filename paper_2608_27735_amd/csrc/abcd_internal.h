@@ -106,8 +106,7 @@ __device__ __forceinline__ Splat make_splat(float2 m, float4 co) {
 }
 
 // The conic (a, b, c) = L L^T of a factor (l11, l21, l22): for the tile test
-// (splat_rows)
-// and the chain rule to the mean.
+// (splat_rows) and the chain rule to the mean.
 __device__ __forceinline__ float3 conic_of(float4 co) {
   return make_float3(co.x * co.x, co.x * co.y, co.y * co.y + co.z * co.z);
 }
