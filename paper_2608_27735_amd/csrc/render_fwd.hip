@@ -181,6 +181,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
         // above the threshold (ok): the first hit below stops the pixel and
         // every later value is below too. No branch depends on the stop.
         float Tc = T;
+        int jg = -1;  // the lane's last blended entry of the group
 #pragma unroll
         for (int i = 0; i < kGroup; ++i) {
           const float Tn = fmaf(-Tc, a[i], Tc);
@@ -191,11 +192,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
           cg = fmaf(gb[i].w, wgt, cg);
           cb = fmaf(bl[i], wgt, cb);
           const bool blend = ok && a[i] != 0.0f;
-          jl = blend ? j0 + i : jl;
+          jg = blend ? i : jg;
           nb += blend ? 1u : 0u;
           T = ok ? Tn : T;
           Tc = Tn;
         }
+        jl = jg >= 0 ? j0 + jg : jl;
         done = done || Tc < thr;
         amin_l = done ? __builtin_huge_valf() : amin_l;
         return !__ballot(!done);
