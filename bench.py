@@ -530,9 +530,12 @@ def _timed(fn, reps, warmup):
     return a.elapsed_time(b) / reps
 
 
-def _blend_kernels(api, fn, reps):
-    """Per-launch milliseconds of the two blend kernels over reps calls of fn()."""
+def _blend_kernels(api, fn, reps, st):
+    """Per-launch milliseconds of the two blend kernels (and the collapse) over
+    reps calls of fn(), and the pairs blended per forward launch (st: the
+    ActiveBlockStep fn runs)."""
     import torch
+    st.n_blends.zero_()
     api.timing_reset()
     api.timing_enable(True)
     for _ in range(reps):
@@ -540,25 +543,30 @@ def _blend_kernels(api, fn, reps):
     torch.cuda.synchronize()
     api.timing_enable(False)
     out = {}
+    fwd_calls = 0
     for name in ("render_fwd", "render_bwd", "composite"):
         ms, cnt = api.timing_read(name)
         if cnt:
             out[name] = ms / cnt
+            if name == "render_fwd":
+                fwd_calls = cnt
     api.timing_reset()
-    return out
+    return out, st.n_blends.item() / max(fwd_calls, 1)
 
 
-def _blend_roofline(kern, pairs_per_call):
-    """Estimated-flop rooflines of the blend kernels (their counted instructions
-    are taken on the headline workload only)."""
+def _blend_roofline(kern, blends_per_call):
+    """Launch times of the blend kernels and their rate in blended pairs. Their
+    VALU-issue roofline needs the counted instructions of the launch, which are
+    taken on the headline workload only: a flop count per list position or per
+    blend depends on the workload (how many list entries the tile test drops,
+    how many lanes of a wave blend an entry) and does not transfer."""
     out = {}
     for name, ms in kern.items():
+        row = dict(ms_per_launch=ms)
         if name in FLOPS_PER_PAIR:
-            t = pairs_per_call * FLOPS_PER_PAIR[name] / (ms / 1e3) / 1e12
-            out[name] = dict(ms_per_launch=ms, achieved=t, peak=FP32_TFLOPS, unit="TFLOP/s",
-                             frac=t / FP32_TFLOPS, basis="estimated flops per evaluated pair")
-        else:
-            out[name] = dict(ms_per_launch=ms)
+            row.update(blends_per_launch=blends_per_call,
+                       blends_per_s=blends_per_call / (ms / 1e3))
+        out[name] = row
     return out
 
 
@@ -621,11 +629,11 @@ def config_ring(api, S, ActiveBlockStep, dev, steps, warmup):
     st.n_blends.zero_()
     ms = _timed(cams_pass, reps, 0) / len(cams)
     out = _step_fields(st, ms, reps * len(cams))
-    kern = _blend_kernels(api, cams_pass, 1)
+    kern, kb = _blend_kernels(api, cams_pass, 1, st)
     out.update(workload=f"{len(act['means'])} active Gaussians (SH 3) of the 64K ring scene, "
                         f"{len(cams)} cameras at {W}x{H}, F/B per camera from {len(cells)} "
                         "cached fp16 cell renders", cameras=len(cams), k_cached=len(cells),
-               kernels_per_camera=_blend_roofline(kern, out["evaluated_pairs_last_step"]),
+               kernels_per_camera=_blend_roofline(kern, kb),
                note="ms_per_step = per camera: collapse of 63 layers + project, bin, forward, "
                     "L1 gradient, backward")
     return out
@@ -677,8 +685,8 @@ def config_midscale(api, S, ActiveBlockStep, dev, T=100):
                             rects=rects)
         st.step(target, F=F, B=B)
 
-    kern = _blend_kernels(api, last_cam, 3)
-    out.update(kernels_last_camera=_blend_roofline(kern, out["evaluated_pairs_last_step"]))
+    kern, kb = _blend_kernels(api, last_cam, 3, st)
+    out.update(kernels_last_camera=_blend_roofline(kern, kb))
     out.update(workload=f"{len(w.scene['means'])} active Gaussians (SH 3), mid-scale scene "
                         f"(4x4x2 grid), {T} steps over cameras drawn from {len(cams)} at {W}x{H}",
                steps=T, distinct_cameras=len(plan), k_cached=len(cells),
@@ -716,10 +724,10 @@ def config_large(api, S, ActiveBlockStep, dev, heavy, steps, warmup):
     reps = max(5, steps // 2)
     ms = _timed(one, reps, warmup)
     out = _step_fields(st, ms, reps + warmup)
-    kern = _blend_kernels(api, one, 3)
+    kern, kb = _blend_kernels(api, one, 3, st)
     out.update(workload=f"1M active Gaussians (SH 3, {'heavy-tailed' if heavy else 'uniform'} "
                         f"scales) at {cam.width}x{cam.height}, F/B from {k} cached layers",
-               n_isect=m, kernels=_blend_roofline(kern, out["evaluated_pairs_last_step"]))
+               n_isect=m, kernels=_blend_roofline(kern, kb))
     del st, images, rects
     torch.cuda.empty_cache()
     return out
@@ -766,7 +774,7 @@ def config_stress(api, S, ActiveBlockStep, dev, sizes=(262_144, 1_000_000, 4_000
         reps = 5
         ms = _timed(one, reps, 1)
         row = _step_fields(st, ms, reps + 1)
-        row["kernels"] = _blend_roofline(_blend_kernels(api, one, 2), row["evaluated_pairs_last_step"])
+        row["kernels"] = _blend_roofline(*_blend_kernels(api, one, 2, st))
         cm = _timed(lambda: api.composite_cache(images, list(range(len(order))), n_front, F=F,
                                                 B=B, rects=rects), 5, 1)
         row.update(n_gaussians=n, n_isect=m, collapse_ms=cm,
