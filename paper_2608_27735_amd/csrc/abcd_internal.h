@@ -116,6 +116,7 @@ __device__ __forceinline__ float3 conic_of(float4 co) {
 // decisions are bit-identical.
 struct AlphaEval {
   float alpha;   // clamped alpha (valid when !skip)
+  float raw;     // o * exp(power), before the clamp
   float e;       // exp(power)
   bool skip;     // power > 0 or alpha < alpha_min
   bool clamped;  // o * exp(power) > alpha_max
@@ -128,10 +129,12 @@ __device__ __forceinline__ AlphaEval eval_alpha(float dx, float dy, float qa, fl
   const float e1 = qa * dx + qb * dy, e2 = qc * dy;
   const float p2 = -(e1 * e1 + e2 * e2);
   r.e = __builtin_amdgcn_exp2f(p2);
-  const float raw = o * r.e;
-  r.clamped = raw > alpha_max;
-  r.alpha = fminf(raw, alpha_max);  // raw is finite: the clamp
-  r.skip = (p2 > 0.0f) || (r.alpha < alpha_min);
+  r.raw = o * r.e;
+  r.clamped = r.raw > alpha_max;
+  r.alpha = fminf(r.raw, alpha_max);  // raw is finite: the clamp
+  // alpha_min <= alpha_max (checked on the host), so the clamped alpha is
+  // below alpha_min exactly when the raw value is
+  r.skip = (p2 > 0.0f) || (r.raw < alpha_min);
   return r;
 }
 

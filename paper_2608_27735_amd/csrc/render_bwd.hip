@@ -246,7 +246,7 @@ __device__ __forceinline__ void bwd_item(
       // Branch-free per lane: a lane that does not blend this entry takes
       // alpha = 0, which leaves T and R unchanged, and a zero mask on the
       // alpha-derivative terms.
-      const float a = contrib ? ae.alpha : 0.0f;
+      const float a = contrib ? (ae.clamped ? k.alpha_max : ae.raw) : 0.0f;
       const float om = 1.0f - a;
       const float iom = __builtin_amdgcn_rcpf(om);  // om >= 1 - alpha_max > 0
       const float Tk = T * iom;
