@@ -140,7 +140,9 @@ def roofline_of(name, d, pairs, bytes_):
     kernels: algorithmic bytes per launch / duration against 8 TB/s. Blend
     kernels (bound by vector issue): counted VALU lane-operations per launch
     (SQ_INSTS_VALU x 64 lanes) / duration against the 39.3 T lane-op/s issue
-    peak, with the flop estimate and the HBM rate beside it."""
+    peak, with the HBM rate beside it; only without a current counter summary
+    a flop estimate per list position walked (which counts entries the tile
+    test drops before any arithmetic, so it is a rough upper figure)."""
     dur = d["ms_per_launch"] / 1e3
     traffic = measured_traffic(name)
     hbm = None if traffic is None else dict(achieved=traffic / dur / 1e9, peak=HBM_PEAK_GBS,
@@ -154,15 +156,13 @@ def roofline_of(name, d, pairs, bytes_):
     if name not in FLOPS_PER_PAIR:
         return None
     est = pairs * FLOPS_PER_PAIR[name] / dur / 1e12
-    cross = dict(flops_per_pair=FLOPS_PER_PAIR[name], evaluated_pairs=pairs, achieved=est,
-                 peak=FP32_TFLOPS, unit="TFLOP/s", frac=est / FP32_TFLOPS)
     insts = counted_valu(name)
     if insts is not None:
         achieved = insts * 64 / dur / 1e12
         return dict(bound="alu", kernel=name, achieved=achieved, peak=VALU_LANE_PEAK_T,
                     unit="Tlane-op/s", frac=achieved / VALU_LANE_PEAK_T, traffic=traffic,
                     basis="counted SQ_INSTS_VALU per launch x 64 lanes / live launch time",
-                    valu_insts_per_launch=insts, flop_estimate=cross, hbm=hbm)
+                    valu_insts_per_launch=insts, hbm=hbm)
     return dict(bound="alu", kernel=name, achieved=est, peak=FP32_TFLOPS, unit="TFLOP/s",
                 frac=est / FP32_TFLOPS, traffic=traffic,
                 basis="estimated flops per evaluated pair (no current counter summary)",
