@@ -374,6 +374,10 @@ def main():
         t = measured_traffic(name)
         if t is not None:
             d["measured_GBs"] = t / (d["ms_per_launch"] / 1e3) / 1e9
+            d["hbm_frac"] = d["measured_GBs"] / HBM_PEAK_GBS
+        v = counted_valu(name)
+        if v is not None:  # counted VALU lane-operations against the issue peak
+            d["valu_issue_frac"] = v * 64 / (d["ms_per_launch"] / 1e3) / 1e12 / VALU_LANE_PEAK_T
 
     if args.extras:
         # the optimizer side of the step (reported beside the metric, not in it):
