@@ -22,16 +22,20 @@
 // entry into a different line and pays several times the payload in HBM
 // writes).
 //
-//   depth_keys, radix x4   depth order of the n Gaussians
+//   bin_zero               header, digit counts, first radix pass's states
+//   depth_keys             keys, tile rectangles, digit counts
+//   radix_pass x4          depth order of the n Gaussians
 //   l1_count               per chunk of 1024 ranks: block counts; total M
-//   l1_scan_columns        exclusive prefix of the chunk counts per block
-//   l1_finish              bucket offsets, sub-chunk table, overflow flag (on
-//                          overflow nothing is counted or placed: every tile
-//                          range comes out empty)
+//   l1_scan_columns        exclusive prefix of the chunk counts per block;
+//                          its last workgroup: bucket offsets, sub-chunk
+//                          table, overflow flag (on overflow nothing is
+//                          counted or placed: every tile range comes out
+//                          empty)
 //   l1_scatter             (block, Gaussian) pairs, bucket-major, depth order
 //   l2_count               per sub-chunk: counts of its block's 64 tiles
-//   l2_scan                exclusive prefix of the sub-chunk counts per tile
-//   bin_scan_tiles         tile_ranges
+//   l2_scan                exclusive prefix of the sub-chunk counts per tile;
+//                          its last workgroup: tile_ranges and the forward's
+//                          tile order
 //   l2_scatter             values (and keys), tile-major, depth order
 #include <algorithm>
 
@@ -40,8 +44,15 @@
 namespace abcd {
 namespace {
 
-constexpr int kRsItems = 8;
-constexpr int kRsTile = kBlock * kRsItems;  // keys per radix block
+constexpr int kDkItems = 4;                 // Gaussians per thread of depth_keys
+constexpr int kDkTile = kBlock * kDkItems;
+constexpr int kRsItems = 16;                // keys per thread of a radix pass
+constexpr int kRsTile = kBlock * kRsItems;  // keys per radix partition
+constexpr int kRsLook = 8;                  // partition states read at once looking back
+// depth_keys adds the digit counts of workgroup b into copy b mod kHistCopies,
+// so that no counter takes more than a few dozen atomic adds; the radix
+// passes sum the copies
+constexpr int kHistCopies = 32;
 constexpr int kScanThreads = 1024;
 constexpr int kRanksPerWave = 256;
 constexpr int kChunk = 4 * kRanksPerWave;   // level 1: depth ranks per workgroup
@@ -55,7 +66,10 @@ struct WsHeader {
   unsigned long long m1;  // (Gaussian, block) pairs
   uint32_t overflow;      // m > capacity or m >= 2^32: nothing is written
   uint32_t total_sub;     // level-2 sub-chunks
-  uint32_t pad[58];
+  uint32_t ticket[4];     // partitions taken by each radix pass
+  uint32_t done_cols;     // workgroups of l1_scan_columns that have finished
+  uint32_t done_l2;       // workgroups of l2_scan that have finished
+  uint32_t pad[52];
 };
 static_assert(sizeof(WsHeader) == 256, "header is one 256-byte slot");
 
@@ -76,15 +90,15 @@ inline Geo geo_of(int width, int height) {
 }
 
 struct WsLayout {
-  size_t hdr, keys_a, keys_b, vals_a, vals_b, rects, hist, totals, c1, cm, blk_total, blk_off,
+  size_t hdr, ghist, st0, st1, keys_a, keys_b, vals_a, vals_b, rects, c1, cm, blk_total, blk_off,
       sub_off, pairs, c2, tile_total, tile_off, total;
-  int64_t rs_blocks, chunks, max_sub;
+  int64_t rs_parts, chunks, max_sub;
 };
 
 WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
   WsLayout L;
   const int64_t ntiles = (int64_t)g.ntx * g.nty;
-  L.rs_blocks = (n + kRsTile - 1) / kRsTile;
+  L.rs_parts = (n + kRsTile - 1) / kRsTile;
   L.chunks = (n + kChunk - 1) / kChunk;
   L.max_sub = (capacity + kSub - 1) / kSub + g.nblk;
   size_t off = 0;
@@ -93,14 +107,17 @@ WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
     off += align256(bytes);
     return at;
   };
+  // header, digit counts and the first radix pass's partition states are
+  // one region, cleared by one launch
   L.hdr = take(sizeof(WsHeader));
+  L.ghist = take(sizeof(uint32_t) * kHistCopies * 4 * 256);
+  L.st0 = take(sizeof(unsigned long long) * 256 * L.rs_parts);
+  L.st1 = take(sizeof(unsigned long long) * 256 * L.rs_parts);
   L.keys_a = take(sizeof(uint32_t) * n);
   L.keys_b = take(sizeof(uint32_t) * n);
   L.vals_a = take(sizeof(uint32_t) * n);
   L.vals_b = take(sizeof(uint32_t) * n);
   L.rects = take(sizeof(unsigned long long) * n);
-  L.hist = take(sizeof(uint32_t) * 256 * L.rs_blocks);
-  L.totals = take(sizeof(uint32_t) * 256);
   L.c1 = take(sizeof(uint32_t) * (size_t)L.chunks * g.nblk);
   L.cm = take(sizeof(uint32_t) * (size_t)L.chunks);
   L.blk_total = take(sizeof(uint32_t) * g.nblk);
@@ -132,6 +149,23 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 }
 
 // ---------------------------------------------------------- depth sort
+//
+// Stable LSD radix sort of the n depth keys, 8-bit digits, one launch per
+// digit. The counts of every digit value over all keys do not depend on the
+// order, so depth_keys takes them for all four digits at once; a pass then
+// needs, per partition of kRsTile consecutive keys, the counts of each digit
+// in the partitions before it. Each partition publishes its own counts as
+// soon as it has them and reads its predecessors' (decoupled look-back):
+// a state word per (partition, digit) holds a flag (aggregate: the
+// partition's own count; inclusive: the count over it and every partition
+// before it) and the count. Partitions take their index from a ticket
+// counter in launch order, so every partition a workgroup waits for is
+// already running and publishes without waiting itself: every wait ends.
+// Keys are ranked and grouped by digit in LDS, then leave as runs of
+// consecutive addresses.
+
+constexpr unsigned long long kStAgg = 1ull << 62;   // the partition's own count
+constexpr unsigned long long kStIncl = 2ull << 62;  // count over it and all before it
 
 // Tile rectangle packed as x0 | x1 << 16 | y0 << 32 | y1 << 48 (empty: x0 = 1 > x1 = 0).
 __device__ __forceinline__ unsigned long long pack_rect(int x0, int y0, int x1, int y1) {
@@ -139,143 +173,246 @@ __device__ __forceinline__ unsigned long long pack_rect(int x0, int y0, int x1, 
          ((unsigned long long)y1 << 48);
 }
 
+// Clears the header (with the radix passes' tickets), the digit counts and
+// the first pass's partition states: one contiguous region of 16-byte words.
+__global__ __launch_bounds__(256) void bin_zero_kernel(uint4* __restrict__ p, int64_t words) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < words;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+// Adds this wave's keys to the workgroup's counts h[4][256] of each digit
+// value. A digit that every active lane shares (the high digits of nearby
+// depths, the 0xff of off-screen Gaussians) is added once by the first lane.
+__device__ __forceinline__ void count_digits(uint32_t (*h)[256], uint32_t key, bool valid) {
+  const uint64_t act = __ballot(valid);
+  if (!act) return;
+  const int first = __ffsll((unsigned long long)act) - 1;
+  const int lane = __lane_id();
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const uint32_t d = (key >> (8 * b)) & 255u;
+    const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane((int)d, first);
+    if (__ballot(valid && d == d0) == act) {
+      if (lane == first) atomicAdd(&h[b][d0], (uint32_t)__popcll(act));
+    } else if (valid) {
+      atomicAdd(&h[b][d], 1u);
+    }
+  }
+}
+
+// Depth keys (fp32 bits; a Gaussian with no tile gets 0xffffffff and sorts
+// last), packed tile rectangles, and the counts of each value of each of the
+// four key digits (ghist[copy][digit][value], cleared before the launch).
 __global__ __launch_bounds__(256) void depth_keys_kernel(
     int64_t n, const float* __restrict__ depth, const uint32_t* __restrict__ tiles,
     const float* __restrict__ means2d, const float* __restrict__ extent, int ntx, int nty,
-    uint32_t* __restrict__ keys, uint32_t* __restrict__ vals, unsigned long long* __restrict__ rects,
-    WsHeader* __restrict__ hdr) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i == 0) {
-    hdr->m = 0;
-    hdr->m1 = 0;
-    hdr->overflow = 0;
-    hdr->total_sub = 0;
-  }
-  if (i >= n) return;
-  const bool vis = tiles[i] != 0;
-  keys[i] = vis ? __float_as_uint(depth[i]) : 0xffffffffu;
-  vals[i] = (uint32_t)i;
-  int x0 = 1, y0 = 0, x1 = 0, y1 = 0;
-  if (vis) {
-    const float2 m = reinterpret_cast<const float2*>(means2d)[i];
-    const float2 ex = reinterpret_cast<const float2*>(extent)[i];
-    if (!tile_rect(m.x, m.y, ex.x, ex.y, ntx, nty, x0, y0, x1, y1)) x0 = 1, y0 = 0, x1 = 0, y1 = 0;
-  }
-  rects[i] = pack_rect(x0, y0, x1, y1);
-}
-
-__global__ __launch_bounds__(256) void radix_hist_kernel(const uint32_t* __restrict__ keys, int64_t n,
-                                                         int shift, uint32_t* __restrict__ hist,
-                                                         int64_t nblocks) {
-  __shared__ uint32_t h[256];
-  h[threadIdx.x] = 0;
-  __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kRsTile;
-  uint32_t d[kRsItems];
+    uint32_t* __restrict__ keys, unsigned long long* __restrict__ rects,
+    uint32_t* __restrict__ ghist) {
+  __shared__ uint32_t h[4][256];
+  const int tid = threadIdx.x;
 #pragma unroll
-  for (int it = 0; it < kRsItems; ++it) {
-    const int64_t idx = base + it * kBlock + threadIdx.x;
-    d[it] = idx < n ? (keys[idx] >> shift) & 255u : 256u;
-  }
+  for (int b = 0; b < 4; ++b) h[b][tid] = 0;
+  const int64_t base = (int64_t)blockIdx.x * kDkTile;
+  // every load of the thread's Gaussians in flight at once
+  uint32_t tt[kDkItems];
+  float dp[kDkItems];
+  float2 mm[kDkItems], ee[kDkItems];
 #pragma unroll
-  for (int it = 0; it < kRsItems; ++it)
-    if (d[it] < 256u) atomicAdd(&h[d[it]], 1u);
+  for (int it = 0; it < kDkItems; ++it) {
+    const int64_t i = base + it * kBlock + tid;
+    const bool ok = i < n;
+    tt[it] = ok ? tiles[i] : 0u;
+    dp[it] = ok ? depth[i] : 0.0f;
+    mm[it] = ok ? reinterpret_cast<const float2*>(means2d)[i] : make_float2(0.0f, 0.0f);
+    ee[it] = ok ? reinterpret_cast<const float2*>(extent)[i] : make_float2(0.0f, 0.0f);
+  }
   __syncthreads();
-  hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
-}
-
-// Exclusive scan of each digit's row of block counts in place (one
-// workgroup per digit) and the digit totals.
-__global__ __launch_bounds__(256) void radix_scan_rows_kernel(uint32_t* __restrict__ hist,
-                                                              int64_t nblocks,
-                                                              uint32_t* __restrict__ totals) {
-  __shared__ uint32_t part[256];
-  uint32_t* row = hist + (int64_t)blockIdx.x * nblocks;
-  uint32_t carry = 0;
-  for (int64_t b0 = 0; b0 < nblocks; b0 += 256) {
-    const int64_t b = b0 + threadIdx.x;
-    const uint32_t v = b < nblocks ? row[b] : 0u;
-    part[threadIdx.x] = v;
-    __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {
-      const uint32_t x = threadIdx.x >= off ? part[threadIdx.x - off] : 0u;
-      __syncthreads();
-      part[threadIdx.x] += x;
-      __syncthreads();
+#pragma unroll
+  for (int it = 0; it < kDkItems; ++it) {
+    const int64_t i = base + it * kBlock + tid;
+    const bool ok = i < n;
+    const bool vis = ok && tt[it] != 0;
+    const uint32_t key = vis ? __float_as_uint(dp[it]) : 0xffffffffu;
+    int x0 = 1, y0 = 0, x1 = 0, y1 = 0;
+    if (vis && !tile_rect(mm[it].x, mm[it].y, ee[it].x, ee[it].y, ntx, nty, x0, y0, x1, y1))
+      x0 = 1, y0 = 0, x1 = 0, y1 = 0;
+    if (ok) {
+      keys[i] = key;
+      rects[i] = pack_rect(x0, y0, x1, y1);
     }
-    if (b < nblocks) row[b] = carry + part[threadIdx.x] - v;
-    carry += part[255];
-    __syncthreads();
+    count_digits(h, key, ok);
   }
-  if (threadIdx.x == 0) totals[blockIdx.x] = carry;
+  __syncthreads();
+  uint32_t* copy = ghist + (blockIdx.x % kHistCopies) * (4 * 256);
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const uint32_t v = h[b][tid];
+    if (v) atomicAdd(&copy[b * 256 + tid], v);
+  }
 }
 
-// Stable scatter of one block of kRsTile keys. Wave w owns the contiguous
-// quarter [w kRsTile / 4, (w + 1) kRsTile / 4) of the block and walks it in
-// order, ranking each key among the wave's earlier keys of its digit (ballot
-// match + a per-wave running count in LDS); the waves' counts are then turned
-// into offsets (wave-major, after the digit's global base) and every key is
-// written once. Two barriers per block.
-__global__ __launch_bounds__(256) void radix_scatter_kernel(
-    const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, int64_t n, int shift,
-    const uint32_t* __restrict__ hist, int64_t nblocks, const uint32_t* __restrict__ totals,
+// Exclusive prefix of one value per thread over the 256 threads; s4 is four
+// words of LDS.
+__device__ __forceinline__ uint32_t scan_256(uint32_t v, uint32_t* s4) {
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  uint32_t incl = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = (uint32_t)__shfl_up((int)incl, d, 64);
+    if (lane >= d) incl += y;
+  }
+  if (lane == 63) s4[w] = incl;
+  __syncthreads();
+  uint32_t before = 0;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) before += k < w ? s4[k] : 0u;
+  __syncthreads();
+  return before + incl - v;
+}
+
+// Sum of the counts of `digit` in the partitions before `part` (part > 0),
+// read back through their states kRsLook at a time: aggregates are added
+// until an inclusive count ends the walk; a state not yet published is read
+// again (its partition is running and publishes without waiting).
+__device__ __forceinline__ uint32_t look_back(const unsigned long long* __restrict__ st,
+                                              int64_t part, int digit) {
+  uint32_t excl = 0;
+  int64_t q = part - 1;
+  while (true) {
+    unsigned long long s[kRsLook];
+#pragma unroll
+    for (int j = 0; j < kRsLook; ++j)
+      s[j] = q - j >= 0 ? __hip_atomic_load(&st[(q - j) * 256 + digit], __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT)
+                        : kStIncl;
+    int used = 0;
+    bool open = true, found = false;
+#pragma unroll
+    for (int j = 0; j < kRsLook; ++j) {
+      const unsigned long long f = s[j] & (3ull << 62);
+      if (open && f != 0) {
+        excl += (uint32_t)s[j];
+        ++used;
+        if (f == kStIncl) found = true;
+      }
+      open = open && f == kStAgg;
+    }
+    if (found) return excl;
+    if (used == 0) __builtin_amdgcn_s_sleep(1);
+    q -= used;
+  }
+}
+
+// One stable pass on digit `pass` (bits 8 pass .. 8 pass + 7) of partition
+// `part` (from the ticket). Wave w ranks its consecutive quarter of the
+// partition in order: the lanes holding one digit value find each other by
+// ballots, and the first of them adds their number to the wave's running
+// count of that value (an LDS atomic returning the count before it; a wave's
+// atomics execute in program order, so the items are ranked in input order
+// without waiting on each other). The partition's keys are then regrouped
+// in LDS by digit (wave-major within a digit, which keeps the input order)
+// and written out, each at the digit's global base + its place among the
+// digit's keys of earlier partitions + its place in the partition. vals_in
+// NULL: the values are the keys' input positions. st_next (NULL on the last
+// pass): the next pass's states, whose row of this partition is cleared here.
+__global__ __launch_bounds__(256) void radix_pass_kernel(
+    const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, int64_t n, int pass,
+    const uint32_t* __restrict__ ghist, unsigned long long* __restrict__ st,
+    unsigned long long* __restrict__ st_next, uint32_t* __restrict__ ticket,
     uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out) {
   constexpr int kPerWave = kRsTile / 4;
   constexpr int kWaveItems = kPerWave / 64;
-  __shared__ uint32_t sbase[256];
-  __shared__ uint32_t wcnt[4][256];
+  __shared__ uint32_t s_key[kRsTile];
+  __shared__ uint32_t s_val[kRsTile];
+  __shared__ uint32_t wcnt[4][256];  // per wave and digit: running counts, then first slots
+  __shared__ uint32_t s_dst[256];    // per digit: global position of LDS slot 0
+  __shared__ uint32_t s4[4];
+  __shared__ uint32_t s_part;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  // digit base = exclusive scan of the digit totals + this block's row prefix
-  const uint32_t tot = totals[tid];
-  sbase[tid] = tot;
+  const int shift = 8 * pass;
+  if (tid == 0) s_part = atomicAdd(ticket, 1u);
 #pragma unroll
   for (int k = 0; k < 4; ++k) wcnt[k][tid] = 0;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    const uint32_t x = tid >= off ? sbase[tid - off] : 0u;
-    __syncthreads();
-    sbase[tid] += x;
-    __syncthreads();
+  // global base of digit value tid: counts of the smaller values over all
+  // keys (while the ticket is on its way)
+  uint32_t total = 0;
+  {
+    uint32_t c[kHistCopies];
+#pragma unroll
+    for (int r = 0; r < kHistCopies; ++r) c[r] = ghist[(r * 4 + pass) * 256 + tid];
+#pragma unroll
+    for (int r = 0; r < kHistCopies; ++r) total += c[r];
   }
-  const uint32_t dbase = sbase[tid] - tot + hist[(int64_t)tid * nblocks + blockIdx.x];
-  const int64_t base = (int64_t)blockIdx.x * kRsTile + (int64_t)w * kPerWave;
+  const uint32_t gbase = scan_256(total, s4);  // its barriers publish s_part and the zeroed counts
+  const int64_t part = s_part;
+  const int64_t base = part * kRsTile;
+  const int cnt = (int)min<int64_t>(kRsTile, n - base);
   uint32_t key[kWaveItems], val[kWaveItems], rank[kWaveItems];
 #pragma unroll
   for (int it = 0; it < kWaveItems; ++it) {
-    const int64_t idx = base + it * 64 + lane;
-    key[it] = idx < n ? keys_in[idx] : 0u;
-    val[it] = idx < n ? vals_in[idx] : 0u;
+    const int li = w * kPerWave + it * 64 + lane;
+    const bool ok = li < cnt;
+    key[it] = ok ? keys_in[base + li] : 0u;
+    val[it] = ok ? (vals_in ? vals_in[base + li] : (uint32_t)(base + li)) : 0u;
   }
+  if (st_next) st_next[part * 256 + tid] = 0ull;
   const uint64_t lt = lanemask_lt();
+  // kRankGroup items at a time: their atomics are in flight together
+  constexpr int kRankGroup = 4;
 #pragma unroll
-  for (int it = 0; it < kWaveItems; ++it) {
-    const bool valid = base + it * 64 + lane < n;
-    const uint32_t d = (key[it] >> shift) & 255u;
-    const uint64_t peers = match_digit(d, __ballot(valid));
-    rank[it] = 0;
-    if (valid) {
-      rank[it] = wcnt[w][d] + __popcll(peers & lt);
-      if (lane == __ffsll((unsigned long long)peers) - 1) wcnt[w][d] += __popcll(peers);
+  for (int g = 0; g < kWaveItems; g += kRankGroup) {
+    uint32_t before[kRankGroup];
+    int first[kRankGroup];
+#pragma unroll
+    for (int u = 0; u < kRankGroup; ++u) {
+      const int it = g + u;
+      const bool ok = w * kPerWave + it * 64 + lane < cnt;
+      const uint32_t d = (key[it] >> shift) & 255u;
+      const uint64_t peers = match_digit(d, __ballot(ok));
+      first[u] = __ffsll((unsigned long long)peers) - 1;
+      rank[it] = __popcll(peers & lt);
+      before[u] = 0;
+      if (ok && lane == first[u]) before[u] = atomicAdd(&wcnt[w][d], (uint32_t)__popcll(peers));
     }
+#pragma unroll
+    for (int u = 0; u < kRankGroup; ++u)
+      rank[g + u] += (uint32_t)__shfl((int)before[u], first[u] < 0 ? 0 : first[u], 64);
   }
   __syncthreads();
-  {  // wave-major offsets of each digit
-    uint32_t run = dbase;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t c = wcnt[k][tid];
-      wcnt[k][tid] = run;
-      run += c;
-    }
-  }
+  // thread tid = digit value: publish the partition's count, then turn the
+  // per-wave counts into LDS slots
+  const uint32_t c0 = wcnt[0][tid], c1 = wcnt[1][tid], c2 = wcnt[2][tid], c3 = wcnt[3][tid];
+  const uint32_t own = c0 + c1 + c2 + c3;
+  __hip_atomic_store(&st[part * 256 + tid], (part == 0 ? kStIncl : kStAgg) | own, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+  const uint32_t loc = scan_256(own, s4);
+  wcnt[0][tid] = loc;
+  wcnt[1][tid] = loc + c0;
+  wcnt[2][tid] = loc + c0 + c1;
+  wcnt[3][tid] = loc + c0 + c1 + c2;
   __syncthreads();
 #pragma unroll
   for (int it = 0; it < kWaveItems; ++it) {
-    if (base + it * 64 + lane < n) {
-      const uint32_t pos = wcnt[w][(key[it] >> shift) & 255u] + rank[it];
-      keys_out[pos] = key[it];
-      vals_out[pos] = val[it];
+    if (w * kPerWave + it * 64 + lane < cnt) {
+      const uint32_t slot = wcnt[w][(key[it] >> shift) & 255u] + rank[it];
+      s_key[slot] = key[it];
+      s_val[slot] = val[it];
     }
+  }
+  uint32_t excl = 0;
+  if (part > 0) {
+    excl = look_back(st, part, tid);
+    __hip_atomic_store(&st[part * 256 + tid], kStIncl | (excl + own), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  }
+  s_dst[tid] = gbase + excl - loc;
+  __syncthreads();
+  for (int i = tid; i < cnt; i += kBlock) {
+    const uint32_t k = s_key[i];
+    const uint32_t pos = s_dst[(k >> shift) & 255u] + (uint32_t)i;
+    keys_out[pos] = k;
+    vals_out[pos] = s_val[i];
   }
 }
 
@@ -314,6 +451,27 @@ __device__ __forceinline__ int pack_local(const Rect& r) {
 }
 
 // ------------------------------------------------------------- level 1
+
+// True in every thread of the last workgroup of the launch to get here (the
+// counter starts at 0). Global writes of any thread before the call are
+// visible to that workgroup's reads after it: every wave waits for its
+// stores to reach the L2 before the barrier, one thread then writes the L2
+// back (agent-scope release) before counting the workgroup in, and the last
+// workgroup's waves drop their cached lines (agent-scope acquire).
+__device__ __forceinline__ bool last_workgroup(uint32_t* counter) {
+  __shared__ uint32_t s_last;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    __builtin_amdgcn_s_waitcnt(0);  // the write-back has completed
+    s_last = atomicAdd(counter, 1u) == gridDim.x - 1 ? 1u : 0u;
+  }
+  __syncthreads();
+  const bool last = s_last != 0u;
+  if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  return last;
+}
 
 constexpr uint32_t kNoBlock = 0xffffffffu;
 
@@ -359,51 +517,14 @@ __global__ __launch_bounds__(256) void l1_count_kernel(
   for (int b = threadIdx.x; b < geo.nblk; b += blockDim.x) out[b] = cnt[b];
 }
 
-// counts[row][col] -> exclusive prefix down each column; column totals.
-// Lane = column, the 16 waves split the rows.
-__global__ __launch_bounds__(1024) void scan_columns_kernel(uint32_t* __restrict__ counts,
-                                                            int64_t rows, int cols,
-                                                            uint32_t* __restrict__ col_total) {
-  __shared__ uint32_t part[16][64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + lane;
-  const int64_t per = (rows + 15) / 16;
-  const int64_t q0 = min<int64_t>(rows, per * w), q1 = min<int64_t>(rows, q0 + per);
-  // rows are read eight at a time so that eight loads are in flight
-  uint32_t s = 0;
-  if (c < cols)
-    for (int64_t q = q0; q < q1; q += 8) {
-      uint32_t v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? counts[(q + u) * cols + c] : 0u;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) s += v[u];
-    }
-  part[w][lane] = s;
-  __syncthreads();
-  uint32_t run = 0;
-  for (int k = 0; k < w; ++k) run += part[k][lane];
-  if (c < cols) {
-    for (int64_t q = q0; q < q1; q += 8) {
-      uint32_t v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? counts[(q + u) * cols + c] : 0u;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (q + u < q1) counts[(q + u) * cols + c] = run;
-        run += v[u];
-      }
-    }
-    if (w == 15) col_total[c] = run;
-  }
-}
-
 // Intersection count M (sum of the chunk counts), bucket offsets, sub-chunk
-// offsets and the overflow decision; one workgroup.
-__global__ __launch_bounds__(kScanThreads) void l1_finish_kernel(
-    const uint32_t* __restrict__ blk_total, int nblk, const uint32_t* __restrict__ cm,
-    int64_t chunks, unsigned long long capacity, uint32_t* __restrict__ blk_off,
-    uint32_t* __restrict__ sub_off, WsHeader* __restrict__ hdr) {
+// offsets and the overflow decision, by one workgroup of kScanThreads.
+__device__ __forceinline__ void finish_l1(const uint32_t* __restrict__ blk_total, int nblk,
+                                          const uint32_t* __restrict__ cm, int64_t chunks,
+                                          unsigned long long capacity,
+                                          uint32_t* __restrict__ blk_off,
+                                          uint32_t* __restrict__ sub_off,
+                                          WsHeader* __restrict__ hdr) {
   __shared__ unsigned long long part[kScanThreads];
   __shared__ unsigned long long spart[kScanThreads];
   __shared__ unsigned long long s_m;
@@ -454,6 +575,49 @@ __global__ __launch_bounds__(kScanThreads) void l1_finish_kernel(
     hdr->overflow = over ? 1u : 0u;
     hdr->total_sub = over ? 0u : (uint32_t)srun;
   }
+}
+
+// counts[row][col] -> exclusive prefix down each column; column totals.
+// Lane = column, the 16 waves split the rows. The last workgroup then turns
+// the block totals into bucket and sub-chunk offsets (finish_l1).
+__global__ __launch_bounds__(1024) void scan_columns_kernel(
+    uint32_t* __restrict__ counts, int64_t rows, int cols, uint32_t* __restrict__ col_total,
+    const uint32_t* __restrict__ cm, unsigned long long capacity, uint32_t* __restrict__ blk_off,
+    uint32_t* __restrict__ sub_off, WsHeader* __restrict__ hdr) {
+  __shared__ uint32_t part[16][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
+  const int64_t per = (rows + 15) / 16;
+  const int64_t q0 = min<int64_t>(rows, per * w), q1 = min<int64_t>(rows, q0 + per);
+  // rows are read eight at a time so that eight loads are in flight
+  uint32_t s = 0;
+  if (c < cols)
+    for (int64_t q = q0; q < q1; q += 8) {
+      uint32_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? counts[(q + u) * cols + c] : 0u;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+  part[w][lane] = s;
+  __syncthreads();
+  uint32_t run = 0;
+  for (int k = 0; k < w; ++k) run += part[k][lane];
+  if (c < cols) {
+    for (int64_t q = q0; q < q1; q += 8) {
+      uint32_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? counts[(q + u) * cols + c] : 0u;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (q + u < q1) counts[(q + u) * cols + c] = run;
+        run += v[u];
+      }
+    }
+    if (w == 15) col_total[c] = run;
+  }
+  if (last_workgroup(&hdr->done_cols))
+    finish_l1(col_total, cols, cm, rows, capacity, blk_off, sub_off, hdr);
 }
 
 // Ordered scatter of (block, Gaussian) pairs of one chunk of depth ranks into
@@ -638,12 +802,44 @@ __global__ __launch_bounds__(64) void l2_count_kernel(
   }
 }
 
+// Exclusive scan over tiles -> tile_off and tile_ranges, by one workgroup of
+// kScanThreads (on overflow every tile total is 0, so the ranges written
+// are all empty and the blend kernels render nothing).
+__device__ __forceinline__ void scan_tiles(const uint32_t* __restrict__ tile_total, int ntiles,
+                                           uint32_t* __restrict__ tile_off,
+                                           uint32_t* __restrict__ tile_ranges) {
+  __shared__ unsigned long long part[kScanThreads];
+  const int per = (ntiles + kScanThreads - 1) / kScanThreads;
+  const int lo = min(ntiles, per * (int)threadIdx.x), hi = min(ntiles, lo + per);
+  unsigned long long s = 0;
+  for (int i = lo; i < hi; ++i) s += tile_total[i];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int off = 1; off < kScanThreads; off <<= 1) {
+    const unsigned long long v = threadIdx.x >= off ? part[threadIdx.x - off] : 0ull;
+    __syncthreads();
+    part[threadIdx.x] += v;
+    __syncthreads();
+  }
+  unsigned long long run = part[threadIdx.x] - s;
+  for (int i = lo; i < hi; ++i) {
+    const uint32_t v = tile_total[i];
+    tile_off[i] = (uint32_t)run;
+    tile_ranges[2 * i] = (uint32_t)run;
+    tile_ranges[2 * i + 1] = (uint32_t)(run + v);
+    run += v;
+  }
+}
+
 // Per block: exclusive prefix of its sub-chunks' tile counts (lane = local
-// tile, the 16 waves split the sub-chunks) and the tile totals.
-__global__ __launch_bounds__(1024) void l2_scan_kernel(uint32_t* __restrict__ c2, Geo geo,
-                                                       const uint32_t* __restrict__ sub_off,
-                                                       const WsHeader* __restrict__ hdr,
-                                                       uint32_t* __restrict__ tile_total) {
+// tile, the 16 waves split the sub-chunks) and the tile totals. The last
+// workgroup then scans the tile totals into tile_off and tile_ranges and,
+// when tile_order is given, orders the tiles for the forward (heaviest lists
+// first; on overflow every total is 0, which gives the identity order).
+__global__ __launch_bounds__(1024) void l2_scan_kernel(
+    uint32_t* __restrict__ c2, Geo geo, const uint32_t* __restrict__ sub_off,
+    WsHeader* __restrict__ hdr, uint32_t* __restrict__ tile_total, uint32_t* __restrict__ tile_off,
+    uint32_t* __restrict__ tile_ranges, uint32_t* __restrict__ tile_order) {
   __shared__ uint32_t part[16][64];
   const int b = blockIdx.x, lt = threadIdx.x & 63, w = threadIdx.x >> 6;
   const bool live = !hdr->overflow;
@@ -678,34 +874,13 @@ __global__ __launch_bounds__(1024) void l2_scan_kernel(uint32_t* __restrict__ c2
     const int tx = bx * kBlk + (lt & 7), ty = by * kBlk + (lt >> 3);
     if (tx < geo.ntx && ty < geo.nty) tile_total[ty * geo.ntx + tx] = run;
   }
-}
-
-// Exclusive scan over tiles -> tile_off and tile_ranges; one workgroup.
-__global__ __launch_bounds__(kScanThreads) void bin_scan_tiles_kernel(
-    const uint32_t* __restrict__ tile_total, int ntiles, uint32_t* __restrict__ tile_off,
-    uint32_t* __restrict__ tile_ranges, const WsHeader* __restrict__ hdr) {
-  // on overflow every tile total is 0 (no sub-chunk was counted), so the
-  // ranges written are all empty and the blend kernels render nothing
-  __shared__ unsigned long long part[kScanThreads];
-  const int per = (ntiles + kScanThreads - 1) / kScanThreads;
-  const int lo = min(ntiles, per * (int)threadIdx.x), hi = min(ntiles, lo + per);
-  unsigned long long s = 0;
-  for (int i = lo; i < hi; ++i) s += tile_total[i];
-  part[threadIdx.x] = s;
-  __syncthreads();
-  for (int off = 1; off < kScanThreads; off <<= 1) {
-    const unsigned long long v = threadIdx.x >= off ? part[threadIdx.x - off] : 0ull;
+  if (!last_workgroup(&hdr->done_l2)) return;
+  const int ntiles = geo.ntx * geo.nty;
+  scan_tiles(tile_total, ntiles, tile_off, tile_ranges);
+  if (tile_order) {
+    __shared__ uint8_t s_key[ABCD_MAX_TILES];
     __syncthreads();
-    part[threadIdx.x] += v;
-    __syncthreads();
-  }
-  unsigned long long run = part[threadIdx.x] - s;
-  for (int i = lo; i < hi; ++i) {
-    const uint32_t v = tile_total[i];
-    tile_off[i] = (uint32_t)run;
-    tile_ranges[2 * i] = (uint32_t)run;
-    tile_ranges[2 * i + 1] = (uint32_t)(run + v);
-    run += v;
+    order_tiles(ntiles, tile_total, tile_order, s_key);
   }
 }
 
@@ -1099,21 +1274,23 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   }
   uint32_t* keys[2] = {u32(L.keys_a), u32(L.keys_b)};
   uint32_t* vals[2] = {u32(L.vals_a), u32(L.vals_b)};
-  uint32_t* hist = u32(L.hist);
-  uint32_t* totals = u32(L.totals);
-
-  const int64_t gb = (n + kBlock - 1) / kBlock;
+  unsigned long long* pstate[2] = {reinterpret_cast<unsigned long long*>(ws + L.st0),
+                                   reinterpret_cast<unsigned long long*>(ws + L.st1)};
+  uint32_t* ghist = u32(L.ghist);
   unsigned long long* rects = reinterpret_cast<unsigned long long*>(ws + L.rects);
-  ABCD_LAUNCH("depth_keys", depth_keys_kernel, gb, kBlock, 0, stream, n, depth, tiles_touched,
-              means2d, extent, geo.ntx, geo.nty, keys[0], vals[0], rects, hdr);
+  {
+    const int64_t words = (int64_t)(L.st1 - L.hdr) / 16;
+    ABCD_LAUNCH("bin_zero", bin_zero_kernel, std::min<int64_t>(1024, (words + kBlock - 1) / kBlock),
+                kBlock, 0, stream, reinterpret_cast<uint4*>(ws + L.hdr), words);
+  }
+  ABCD_LAUNCH("depth_keys", depth_keys_kernel, (n + kDkTile - 1) / kDkTile, kBlock, 0, stream, n,
+              depth, tiles_touched, means2d, extent, geo.ntx, geo.nty, keys[0], rects, ghist);
   for (int pass = 0; pass < 4; ++pass) {
     const int src = pass & 1, dst = src ^ 1;
-    ABCD_LAUNCH("radix_hist", radix_hist_kernel, L.rs_blocks, kBlock, 0, stream, keys[src], n,
-                8 * pass, hist, L.rs_blocks);
-    ABCD_LAUNCH("radix_scan", radix_scan_rows_kernel, 256, kBlock, 0, stream, hist, L.rs_blocks,
-                totals);
-    ABCD_LAUNCH("radix_scatter", radix_scatter_kernel, L.rs_blocks, kBlock, 0, stream, keys[src],
-                vals[src], n, 8 * pass, hist, L.rs_blocks, totals, keys[dst], vals[dst]);
+    ABCD_LAUNCH("radix_pass", radix_pass_kernel, L.rs_parts, kBlock, 0, stream, keys[src],
+                pass == 0 ? nullptr : vals[src], n, pass, ghist, pstate[pass & 1],
+                pass < 3 ? pstate[(pass + 1) & 1] : nullptr, &hdr->ticket[pass], keys[dst],
+                vals[dst]);
   }
   const uint32_t* order = vals[0];  // four passes: back in buffer 0
 
@@ -1138,25 +1315,17 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   ABCD_LAUNCH("l1_count", l1_count_kernel, L.chunks, kBlock, sizeof(uint32_t) * geo.nblk, stream, n,
               order, rects, geo, c1, cm);
   ABCD_LAUNCH("l1_scan_columns", scan_columns_kernel, (geo.nblk + 63) / 64, 1024, 0, stream, c1,
-              L.chunks, geo.nblk, blk_total);
-  ABCD_LAUNCH("l1_finish", l1_finish_kernel, 1, kScanThreads, 0, stream, blk_total, geo.nblk, cm,
-              L.chunks, cap, blk_off, sub_off, hdr);
+              L.chunks, geo.nblk, blk_total, cm, cap, blk_off, sub_off, hdr);
   ABCD_LAUNCH("l1_scatter", l1_scatter_kernel, L.chunks, kBlock, 4 * sizeof(uint32_t) * geo.nblk,
               stream, n, order, rects, geo, c1, blk_off, hdr, pairs);
   ABCD_LAUNCH("l2_count", l2_count_kernel, 4 * kStrideGrid, 64, 0, stream, pairs, geo, sub_off,
               blk_off, hdr, c2);
   ABCD_LAUNCH("l2_scan", l2_scan_kernel, geo.nblk, 1024, 0, stream, c2, geo, sub_off, hdr,
-              tile_total);
-  ABCD_LAUNCH("bin_scan_tiles", bin_scan_tiles_kernel, 1, kScanThreads, 0, stream, tile_total,
-              ntiles, tile_off, tile_ranges, hdr);
+              tile_total, tile_off, tile_ranges, tile_order);
   ABCD_LAUNCH("l2_scatter", l2_scatter_kernel, kStrideGrid, kBlock, 0, stream, pairs, depth, geo,
               sub_off, blk_off, c2, tile_off, hdr, values_sorted,
               reinterpret_cast<unsigned long long*>(keys_sorted));
   ABCD_HIP(hipGetLastError());
-  // forward schedule: heaviest lists first (on overflow every total is 0,
-  // which gives the identity order)
-  if (tile_order)
-    TRY_STATUS(launch_tile_order(ntiles, tile_total, tile_order, nullptr, "bin_tile_order", stream));
   return ABCD_OK;
 }
 
