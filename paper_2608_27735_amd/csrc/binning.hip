@@ -885,103 +885,71 @@ __global__ __launch_bounds__(1024) void l2_scan_kernel(
 }
 
 // Ordered scatter of one 256-entry sub-chunk into its block's 64 tile lists.
-// Wave w owns entries [64 w, 64 w + 64) of the sub-chunk; lane l counts and
-// places the entries of local tile l; the runs are staged in LDS (at most
-// 256 x 64 entries) and leave as one coalesced burst per tile.
+// Wave w owns entries [64 w, 64 w + 64) of the sub-chunk, lane l entry
+// 64 w + l. Eight column and eight row ballots give, for every local tile t,
+// the mask of the wave's entries whose rectangle holds it (column mask of
+// t % 8 and row mask of t / 8, wave-uniform); the wave then walks the 64
+// tiles and the entries of each tile's mask write their Gaussian at the
+// wave's first slot in that tile's run plus their rank among the mask's
+// lanes, one store of consecutive addresses per tile. A tile's run takes the
+// waves' entries in wave order (per-wave counts by 2D difference arrays).
 __global__ __launch_bounds__(256) void l2_scatter_kernel(
     const unsigned long long* __restrict__ pairs, const float* __restrict__ depth, Geo geo,
     const uint32_t* __restrict__ sub_off, const uint32_t* __restrict__ blk_off,
     const uint32_t* __restrict__ c2, const uint32_t* __restrict__ tile_off,
     const WsHeader* __restrict__ hdr, uint32_t* __restrict__ values_sorted,
     unsigned long long* __restrict__ keys_sorted) {
-  __shared__ uint8_t stage[kSub * kBlkTiles];   // per tile, a run of sub-chunk entry indices
-  __shared__ uint32_t s_gid[kSub];               // Gaussian of each sub-chunk entry
-  __shared__ uint32_t wcnt[4][kBlkTiles];       // per wave counts, then first slots
-  __shared__ uint32_t wdiff[4][kBlkTiles];      // per wave difference arrays
-  __shared__ uint32_t soff[kBlkTiles + 1];      // run start of each tile in `stage`
-  __shared__ uint32_t dst[kBlkTiles];           // global start of each tile's run
+  __shared__ uint32_t wcnt[4][kBlkTiles];   // per wave: entries covering each tile
+  __shared__ uint32_t wdiff[4][kBlkTiles];  // per wave difference arrays
   const uint32_t total = hdr->total_sub;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, lx = lane & 7, ly = lane >> 3;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (uint32_t s = blockIdx.x; s < total; s += gridDim.x) {
     const SubChunk sc = sub_chunk_wave(s, sub_off, blk_off, geo);
     uint32_t g;
     int pk;
     load_entry(pairs, sc.e0 + threadIdx.x, sc.e1, g, pk);
-    // the global start of each tile's run, loaded now so that its latency
-    // overlaps the counting below
+    // global start of each tile's run in the sub-chunk (lane = local tile),
+    // loaded now so that its latency overlaps the counting below
     uint32_t dst_l = 0u;
-    if (w == 0) {
-      const int tx = sc.bx * kBlk + lx, ty = sc.by * kBlk + ly;
+    {
+      const int tx = sc.bx * kBlk + (lane & 7), ty = sc.by * kBlk + (lane >> 3);
       if (tx < geo.ntx && ty < geo.nty)
         dst_l = tile_off[ty * geo.ntx + tx] + c2[(int64_t)s * kBlkTiles + lane];
     }
-    s_gid[threadIdx.x] = g;
+    const uint32_t key_lo = keys_sorted && pk != 0 ? __float_as_uint(depth[g]) : 0u;
     wdiff[w][lane] = 0;
     __syncthreads();
     diff_add(wdiff[w], pk);
     __syncthreads();
     wcnt[w][lane] = diff_prefix(wdiff[w][lane], lane);
     __syncthreads();
-    if (w == 0) {
-      uint32_t c[4], tot = 0;
+    // this wave's first slot in the run of tile `lane`
+    uint32_t base = dst_l;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        c[k] = wcnt[k][lane];
-        tot += c[k];
-      }
-      // exclusive scan of the tile totals across the wave
-      uint32_t incl = tot;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t v = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += v;
-      }
-      const uint32_t start = incl - tot;
-      soff[lane] = start;
-      if (lane == 63) soff[64] = incl;
-      uint32_t run = start;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        wcnt[k][lane] = run;
-        run += c[k];
-      }
-      dst[lane] = dst_l;
-    }
-    __syncthreads();
-    // place, in depth order, into the LDS runs. Entry l of the wave covers
-    // this lane's local tile (lx, ly) iff its column range holds lx and its
-    // row range holds ly, so 16 ballots (one per column, one per row) give
-    // every lane the mask of its entries; lanes then walk their set bits in
-    // entry order.
-    uint64_t mine;
+    for (int k = 0; k < 3; ++k) base += k < w ? wcnt[k][lane] : 0u;
+    uint64_t colm[kBlk], rowm[kBlk];
     {
       const int x0 = pk & 7, y0 = (pk >> 3) & 7, x1 = (pk >> 6) & 7, y1 = (pk >> 9) & 7;
       const bool v = pk != 0;
-      uint64_t cm = 0, rm = 0;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const uint64_t bc = __ballot(v && x0 <= c && c <= x1);
-        const uint64_t br = __ballot(v && y0 <= c && c <= y1);
-        cm = lx == c ? bc : cm;
-        rm = ly == c ? br : rm;
+      for (int c = 0; c < kBlk; ++c) {
+        colm[c] = __ballot(v && x0 <= c && c <= x1);
+        rowm[c] = __ballot(v && y0 <= c && c <= y1);
       }
-      mine = cm & rm;
     }
-    uint32_t pos = wcnt[w][lane];
-    while (mine) {
-      stage[pos++] = (uint8_t)(64 * w + __builtin_ctzll(mine));
-      mine &= mine - 1;
-    }
-    __syncthreads();
-    // write out: wave w copies the runs of tiles w, w + 4, ...
-    for (int lt = w; lt < kBlkTiles; lt += 4) {
-      const uint32_t r0 = soff[lt], len = soff[lt + 1] - r0, d = dst[lt];
-      const int t = (sc.by * kBlk + (lt >> 3)) * geo.ntx + (sc.bx * kBlk + (lt & 7));
-      for (uint32_t i = lane; i < len; i += 64) {
-        const uint32_t gv = s_gid[stage[r0 + i]];
-        values_sorted[d + i] = gv;
-        if (keys_sorted)
-          keys_sorted[d + i] = ((unsigned long long)t << 32) | __float_as_uint(depth[gv]);
+#pragma unroll
+    for (int t = 0; t < kBlkTiles; ++t) {
+      const uint64_t m = colm[t & 7] & rowm[t >> 3];
+      if (m == 0) continue;
+      const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)base, t);
+      if ((m >> lane) & 1ull) {
+        const uint32_t pos =
+            b + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        values_sorted[pos] = g;
+        if (keys_sorted) {
+          const uint32_t tile = (uint32_t)((sc.by * kBlk + (t >> 3)) * geo.ntx + sc.bx * kBlk + (t & 7));
+          keys_sorted[pos] = ((unsigned long long)tile << 32) | key_lo;
+        }
       }
     }
     __syncthreads();
