@@ -60,6 +60,7 @@ constexpr int kSub = 256;                   // level 2: bucket entries per sub-c
 constexpr int kBlk = 8;                     // block side in tiles
 constexpr int kBlkTiles = kBlk * kBlk;
 constexpr int kStrideGrid = 2048;           // workgroups of the grid-stride level-2 kernels
+constexpr int kScatterGrid = 8192;          // workgroups of the grid-stride level-2 scatter
 
 struct WsHeader {
   unsigned long long m;   // intersections (sum of tiles_touched)
@@ -942,7 +943,7 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
       const uint64_t m = colm[t & 7] & rowm[t >> 3];
       if (m == 0) continue;
       const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)base, t);
-      if ((m >> lane) & 1ull) {
+      if (__builtin_amdgcn_inverse_ballot_w64(m)) {  // this lane's bit of m
         const uint32_t pos =
             b + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
         values_sorted[pos] = g;
@@ -1290,7 +1291,7 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
               blk_off, hdr, c2);
   ABCD_LAUNCH("l2_scan", l2_scan_kernel, geo.nblk, 1024, 0, stream, c2, geo, sub_off, hdr,
               tile_total, tile_off, tile_ranges, tile_order);
-  ABCD_LAUNCH("l2_scatter", l2_scatter_kernel, kStrideGrid, kBlock, 0, stream, pairs, depth, geo,
+  ABCD_LAUNCH("l2_scatter", l2_scatter_kernel, kScatterGrid, kBlock, 0, stream, pairs, depth, geo,
               sub_off, blk_off, c2, tile_off, hdr, values_sorted,
               reinterpret_cast<unsigned long long*>(keys_sorted));
   ABCD_HIP(hipGetLastError());
