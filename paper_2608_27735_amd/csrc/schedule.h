@@ -53,50 +53,67 @@ __device__ __forceinline__ void scan_buckets(uint32_t* s_base) {
   }
 }
 
-// The ordering itself, by one workgroup of kOrderThreads threads; s_key is
-// workgroup memory of ABCD_MAX_TILES bytes.
-__device__ __forceinline__ void order_tiles(int ntiles, const uint32_t* __restrict__ work,
-                                            uint32_t* __restrict__ order, uint8_t* s_key) {
+// The ordering of tiles whose buckets are in s_key (workgroup memory, filled
+// before the last barrier), by one workgroup of kOrderThreads threads. Wave w
+// takes the tiles of one contiguous range: it counts each bucket in the
+// range (LDS atomics), the counts of all waves then give each wave its first
+// slot in every bucket (buckets in order, waves in order within a bucket),
+// and a second walk, 64 tiles at a time, places each tile at that slot plus
+// its rank among the range's earlier tiles of its bucket (ballot match plus
+// a running count). s_order (may be NULL): the order also into workgroup
+// memory, as 16-bit tile indices.
+__device__ __forceinline__ void order_keyed(int ntiles, const uint8_t* s_key,
+                                            uint32_t* __restrict__ order, uint16_t* s_order) {
   __shared__ uint32_t s_base[kBuckets];
-  __shared__ uint32_t s_wc[kOrderWaves][kBuckets];  // per wave counts, then exclusive offsets
+  __shared__ uint32_t s_wc[kOrderWaves][kBuckets];  // per wave counts, then first slots
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
   const uint64_t below = (1ull << l) - 1ull;
-  if (tid < kBuckets) s_base[tid] = 0;
-  // all loads in flight at once; buckets kept in LDS for both passes
-#pragma unroll 8
-  for (int t = tid; t < ntiles; t += kOrderThreads) s_key[t] = (uint8_t)bucket_of(work[t]);
+  for (int i = tid; i < kOrderWaves * kBuckets; i += kOrderThreads) (&s_wc[0][0])[i] = 0;
   __syncthreads();
-  // bucket totals: the first lane of each group of equal buckets adds the group
-  for (int t0 = 0; t0 < ntiles; t0 += kOrderThreads) {
-    const int t = t0 + tid;
-    const int key = t < ntiles ? s_key[t] : kNone;
-    const uint64_t peers = match_bucket(key);
-    if (key != kNone && (peers & below) == 0) atomicAdd(&s_base[key], (uint32_t)__popcll(peers));
+  const int per = (ntiles + kOrderWaves - 1) / kOrderWaves;
+  const int t0 = min(ntiles, w * per), t1 = min(ntiles, t0 + per);
+  for (int t = t0 + l; t < t1; t += 64) atomicAdd(&s_wc[w][s_key[t]], 1u);
+  __syncthreads();
+  if (tid < kBuckets) {
+    uint32_t tot = 0;
+    for (int v = 0; v < kOrderWaves; ++v) tot += s_wc[v][tid];
+    s_base[tid] = tot;
   }
   __syncthreads();
   scan_buckets(s_base);
-  // stable placement, one chunk of tiles at a time
-  for (int t0 = 0; t0 < ntiles; t0 += kOrderThreads) {
-    for (int i = tid; i < kOrderWaves * kBuckets; i += kOrderThreads) (&s_wc[0][0])[i] = 0;
-    __syncthreads();
-    const int t = t0 + tid;
-    const int key = t < ntiles ? s_key[t] : kNone;
-    const uint64_t peers = match_bucket(key);
-    if (key != kNone && (peers & below) == 0) s_wc[w][key] = (uint32_t)__popcll(peers);
-    __syncthreads();
-    if (tid < kBuckets) {  // exclusive offsets over the waves; advance the bucket base
-      uint32_t run = s_base[tid];
-      for (int v = 0; v < kOrderWaves; ++v) {
-        const uint32_t c = s_wc[v][tid];
-        s_wc[v][tid] = run;
-        run += c;
-      }
-      s_base[tid] = run;
+  __syncthreads();
+  if (tid < kBuckets) {  // first slot of each wave in the bucket
+    uint32_t run = s_base[tid];
+    for (int v = 0; v < kOrderWaves; ++v) {
+      const uint32_t c = s_wc[v][tid];
+      s_wc[v][tid] = run;
+      run += c;
     }
-    __syncthreads();
-    if (key != kNone) order[s_wc[w][key] + __popcll(peers & below)] = (uint32_t)t;
-    __syncthreads();
   }
+  __syncthreads();
+  for (int tb = t0; tb < t1; tb += 64) {
+    const int t = tb + l;
+    const int key = t < t1 ? s_key[t] : kNone;
+    const uint64_t peers = match_bucket(key);
+    if (key != kNone) {
+      const uint32_t pos = s_wc[w][key] + __popcll(peers & below);
+      order[pos] = (uint32_t)t;
+      if (s_order) s_order[pos] = (uint16_t)t;
+      if ((peers & below) == 0) s_wc[w][key] += (uint32_t)__popcll(peers);
+    }
+  }
+  __syncthreads();
+}
+
+// The ordering of tiles by the bucket of work[t]; s_key is workgroup memory
+// of ABCD_MAX_TILES bytes.
+__device__ __forceinline__ void order_tiles(int ntiles, const uint32_t* __restrict__ work,
+                                            uint32_t* __restrict__ order, uint8_t* s_key) {
+  // all loads in flight at once
+#pragma unroll 8
+  for (int t = threadIdx.x; t < ntiles; t += kOrderThreads) s_key[t] = (uint8_t)bucket_of(work[t]);
+  __syncthreads();
+  order_keyed(ntiles, s_key, order, nullptr);
 }
 
 }  // namespace

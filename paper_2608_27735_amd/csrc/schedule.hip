@@ -46,77 +46,95 @@ __global__ __launch_bounds__(kBlock) void tile_walk_kernel(int width, int height
   if (threadIdx.x == 0) work[tile] = s_m;
 }
 
-// Work items of the backward, in the order of `order` (tiles by decreasing
-// estimated work): a tile with no walk has none, a tile the forward split (it
-// has an end-of-walk slot) one per chunk its walk reaches, any other tile
-// one. Writes items (tile, chunk), queue[0] = their number and zeroes the
+// Work items of the backward, in the order s_order (tiles by decreasing
+// estimated work, workgroup memory): a tile with no walk has none, a tile
+// the forward split (it has an end-of-walk slot) one per chunk its walk
+// reaches, any other tile one (s_nt: items per tile, workgroup memory).
+// Writes items (tile, chunk), queue[0] = their number and zeroes the
 // counters of the kQueues queues (the heads the backward's workgroups
-// advance). s_n is workgroup memory of
-// ABCD_MAX_TILES bytes.
-__device__ __forceinline__ void build_items(int ntiles, const uint32_t* __restrict__ order,
-                                            const uint32_t* __restrict__ walk,
-                                            const SplitLayout& sp, uint2* __restrict__ items,
-                                            uint32_t cap, uint32_t* __restrict__ queue,
-                                            uint8_t* s_n) {
+// advance). Wave w takes the positions of one contiguous range: their item
+// count, then (once every wave's count is known) their items, 64 positions
+// at a time with a running offset.
+__device__ __forceinline__ void build_items(int ntiles, const uint16_t* s_order,
+                                            const uint8_t* s_nt, uint2* __restrict__ items,
+                                            uint32_t cap, uint32_t* __restrict__ queue) {
   __shared__ uint32_t s_wsum[kOrderWaves];
-  __shared__ uint32_t s_off;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-  if (tid == 0) s_off = 0;
-  // items per position of the order, the dependent loads of eight positions
-  // in flight at once
-#pragma unroll 8
-  for (int i = tid; i < ntiles; i += kOrderThreads) {
-    const uint32_t t = order[i];
-    const uint32_t wk = walk[t];
-    uint32_t n = wk > 0 ? 1u : 0u;
-    if (wk > 0 && sp.ckpt && sp.slot_of[(size_t)t * kMaxChunks] < sp.nslots) {
-      const uint32_t ch = (uint32_t)sp.ch;
-      n = min((wk + ch - 1) / ch, kMaxChunks);
-    }
-    s_n[i] = (uint8_t)n;
-  }
+  const int per = (ntiles + kOrderWaves - 1) / kOrderWaves;
+  const int i0 = min(ntiles, w * per), i1 = min(ntiles, i0 + per);
+  uint32_t mine = 0;
+  for (int i = i0 + l; i < i1; i += 64) mine += s_nt[s_order[i]];
+  mine = wave_sum_u32(mine);
+  if (l == 0) s_wsum[w] = mine;
   __syncthreads();
-  for (int i0 = 0; i0 < ntiles; i0 += kOrderThreads) {
-    const int i = i0 + tid;
-    const uint32_t n = i < ntiles ? s_n[i] : 0u;
-    const uint32_t t = n ? order[i] : 0u;
-    // exclusive prefix of n over the workgroup
-    uint32_t inc = n;
+  uint32_t off = 0, total = 0;
+#pragma unroll
+  for (int v = 0; v < kOrderWaves; ++v) {
+    const uint32_t c = s_wsum[v];
+    off += v < w ? c : 0u;
+    total += c;
+  }
+  for (int ib = i0; ib < i1; ib += 64) {
+    const int i = ib + l;
+    const uint32_t t = i < i1 ? s_order[i] : 0u;
+    const uint32_t n = i < i1 ? s_nt[t] : 0u;
+    uint32_t inc = n;  // inclusive prefix of n over the 64 positions
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
       const uint32_t y = (uint32_t)__shfl_up((int)inc, d, 64);
       if (l >= d) inc += y;
     }
-    if (l == 63) s_wsum[w] = inc;
-    __syncthreads();
-    uint32_t before = 0, total = 0;
-#pragma unroll
-    for (int v = 0; v < kOrderWaves; ++v) {
-      const uint32_t c = s_wsum[v];
-      before += v < w ? c : 0u;
-      total += c;
-    }
-    const uint32_t off = s_off + before + inc - n;
-    for (uint32_t jj = 0; jj < n && off + jj < cap; ++jj) items[off + jj] = make_uint2(t, jj);
-    __syncthreads();
-    if (tid == 0) s_off += total;
-    __syncthreads();
+    const uint32_t at = off + inc - n;
+    for (uint32_t jj = 0; jj < n && at + jj < cap; ++jj) items[at + jj] = make_uint2(t, jj);
+    off += (uint32_t)__shfl((int)inc, 63, 64);
   }
-  if (tid == 0) queue[0] = min(s_off, cap);
+  if (tid == 0) queue[0] = min(total, cap);
   if (tid < kQueues) queue[kQueueStride * tid + 1] = 0;
 }
 
 // The backward's schedule in one launch: tiles ordered by `key`, then the
-// work items in that order (walk: each tile's largest per-pixel walk).
+// work items in that order (walk: each tile's largest per-pixel walk). Every
+// global load (key, walk and the split slot of each tile) is issued in the
+// first loop; the rest works in workgroup memory.
 __global__ __launch_bounds__(kOrderThreads) void bwd_schedule_kernel(
     int ntiles, const uint32_t* __restrict__ key, const uint32_t* __restrict__ walk,
     uint32_t* __restrict__ order, SplitLayout sp, uint2* __restrict__ items, uint32_t cap,
     uint32_t* __restrict__ queue) {
-  __shared__ uint8_t s_buf[ABCD_MAX_TILES];  // bucket keys, then items per position
-  order_tiles(ntiles, key, order, s_buf);
-  // the order is read back by other threads of this workgroup (the barrier
-  // at the end of order_tiles also ends its use of s_buf)
-  build_items(ntiles, order, walk, sp, items, cap, queue, s_buf);
+  __shared__ uint8_t s_key[ABCD_MAX_TILES];      // bucket of each tile
+  __shared__ uint8_t s_nt[ABCD_MAX_TILES];       // work items of each tile
+  __shared__ uint16_t s_order[ABCD_MAX_TILES];   // the order
+  static_assert(ABCD_MAX_TILES <= 65536, "tile indices are kept in 16 bits");
+  // eight tiles per thread at a time, their loads issued together (indices
+  // clamped into the arrays, so that no load waits behind a branch)
+  constexpr int kAt = 8;
+  const uint32_t* slot_src = sp.ckpt ? sp.slot_of : walk;
+  const size_t slot_stride = sp.ckpt ? kMaxChunks : 1;
+  for (int tb = 0; tb < ntiles; tb += kAt * kOrderThreads) {
+    uint32_t wk[kAt], kk[kAt], sl[kAt];
+#pragma unroll
+    for (int u = 0; u < kAt; ++u) {
+      const int tc = min(tb + u * kOrderThreads + (int)threadIdx.x, ntiles - 1);
+      wk[u] = walk[tc];
+      kk[u] = key[tc];
+      sl[u] = slot_src[(size_t)tc * slot_stride];
+    }
+#pragma unroll
+    for (int u = 0; u < kAt; ++u) {
+      const int t = tb + u * kOrderThreads + (int)threadIdx.x;
+      uint32_t n = wk[u] > 0 ? 1u : 0u;
+      if (wk[u] > 0 && sp.ckpt && sl[u] < sp.nslots) {
+        const uint32_t ch = (uint32_t)sp.ch;
+        n = min((wk[u] + ch - 1) / ch, kMaxChunks);
+      }
+      if (t < ntiles) {
+        s_key[t] = (uint8_t)bucket_of(kk[u]);
+        s_nt[t] = (uint8_t)n;
+      }
+    }
+  }
+  __syncthreads();
+  order_keyed(ntiles, s_key, order, s_order);
+  build_items(ntiles, s_order, s_nt, items, cap, queue);
 }
 
 }  // namespace
