@@ -12,26 +12,25 @@
 //   level 2  each block's bucket -> its 64 tile lists
 //
 // Both levels place every pair at its stable rank. Level 1: a wave visits the
-// distinct blocks its 256 entries cover in increasing block order, and ballots
-// rank the entries covering each block. Level 2: lane l of a wave owns local
-// tile l and walks the wave's 64 entries in depth order. Counts come from LDS
-// atomics (level 1) and 2D difference arrays (level 2). Level 2 is
+// distinct blocks its entries cover in increasing block order, and ballots
+// rank the entries covering each block. Level 2: ballots give each of a
+// block's 64 tiles the mask of a wave's entries covering it, and the entries
+// of each mask store at their rank in it. Counts come from LDS atomics
+// (level 1) and 2D difference arrays (level 2). Level 2 is
 // split into sub-chunks of a bucket, each of which writes only 64 output
 // streams, so consecutive writes of a stream meet in L2 and leave it as whole
 // lines (a one-level scatter over all tiles of the frame writes every 4-byte
 // entry into a different line and pays several times the payload in HBM
 // writes).
 //
-//   bin_zero               header, digit counts, first radix pass's states
-//   depth_keys             keys, tile rectangles, digit counts
+//   bin_zero               header, counters and look-back states
+//   depth_keys             keys, tile rectangles, digit counts, block totals,
+//                          intersection count M
 //   radix_pass x4          depth order of the n Gaussians
-//   l1_count               per chunk of 1024 ranks: block counts; total M
-//   l1_scan_columns        exclusive prefix of the chunk counts per block;
-//                          its last workgroup: bucket offsets, sub-chunk
-//                          table, overflow flag (on overflow nothing is
-//                          counted or placed: every tile range comes out
-//                          empty)
-//   l1_scatter             (block, Gaussian) pairs, bucket-major, depth order
+//   l1_place               (block, Gaussian) pairs, bucket-major, depth order;
+//                          bucket offsets, sub-chunk table, overflow flag (on
+//                          overflow nothing is placed: every tile range comes
+//                          out empty)
 //   l2_count               per sub-chunk: counts of its block's 64 tiles
 //   l2_scan                exclusive prefix of the sub-chunk counts per tile;
 //                          its last workgroup: tile_ranges and the forward's
@@ -49,12 +48,13 @@ constexpr int kDkTile = kBlock * kDkItems;
 constexpr int kRsItems = 16;                // keys per thread of a radix pass
 constexpr int kRsTile = kBlock * kRsItems;  // keys per radix partition
 constexpr int kRsLook = 8;                  // partition states read at once looking back
-// depth_keys adds the digit counts of workgroup b into copy b mod kHistCopies,
-// so that no counter takes more than a few dozen atomic adds; the radix
-// passes sum the copies
+// depth_keys adds the digit counts, block totals and intersection count of
+// workgroup b into copy b mod kHistCopies, so that no counter takes more
+// than a few dozen atomic adds; their readers sum the copies
 constexpr int kHistCopies = 32;
 constexpr int kScanThreads = 1024;
-constexpr int kRanksPerWave = 256;
+constexpr int kL1Items = 8;                 // level 1: depth ranks per lane
+constexpr int kRanksPerWave = 64 * kL1Items;
 constexpr int kChunk = 4 * kRanksPerWave;   // level 1: depth ranks per workgroup
 constexpr int kSub = 256;                   // level 2: bucket entries per sub-chunk
 constexpr int kBlk = 8;                     // block side in tiles
@@ -68,7 +68,7 @@ struct WsHeader {
   uint32_t overflow;      // m > capacity or m >= 2^32: nothing is written
   uint32_t total_sub;     // level-2 sub-chunks
   uint32_t ticket[4];     // partitions taken by each radix pass
-  uint32_t done_cols;     // workgroups of l1_scan_columns that have finished
+  uint32_t ticket_l1;     // chunks taken by l1_place
   uint32_t done_l2;       // workgroups of l2_scan that have finished
   uint32_t pad[52];
 };
@@ -91,7 +91,7 @@ inline Geo geo_of(int width, int height) {
 }
 
 struct WsLayout {
-  size_t hdr, ghist, st0, st1, keys_a, keys_b, vals_a, vals_b, rects, c1, cm, blk_total, blk_off,
+  size_t hdr, ghist, mcopy, bcopy, lb1, st0, st1, keys_a, keys_b, vals_a, vals_b, rects, blk_off,
       sub_off, pairs, c2, tile_total, tile_off, total;
   int64_t rs_parts, chunks, max_sub;
 };
@@ -108,10 +108,13 @@ WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
     off += align256(bytes);
     return at;
   };
-  // header, digit counts and the first radix pass's partition states are
-  // one region, cleared by one launch
+  // header, counters, level 1's and the first radix pass's look-back states
+  // are one region, cleared by one launch
   L.hdr = take(sizeof(WsHeader));
   L.ghist = take(sizeof(uint32_t) * kHistCopies * 4 * 256);
+  L.mcopy = take(sizeof(unsigned long long) * kHistCopies);
+  L.bcopy = take(sizeof(uint32_t) * kHistCopies * g.nblk);
+  L.lb1 = take(sizeof(uint32_t) * (size_t)L.chunks * g.nblk);
   L.st0 = take(sizeof(unsigned long long) * 256 * L.rs_parts);
   L.st1 = take(sizeof(unsigned long long) * 256 * L.rs_parts);
   L.keys_a = take(sizeof(uint32_t) * n);
@@ -119,9 +122,6 @@ WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
   L.vals_a = take(sizeof(uint32_t) * n);
   L.vals_b = take(sizeof(uint32_t) * n);
   L.rects = take(sizeof(unsigned long long) * n);
-  L.c1 = take(sizeof(uint32_t) * (size_t)L.chunks * g.nblk);
-  L.cm = take(sizeof(uint32_t) * (size_t)L.chunks);
-  L.blk_total = take(sizeof(uint32_t) * g.nblk);
   L.blk_off = take(sizeof(uint32_t) * (g.nblk + 1));
   L.sub_off = take(sizeof(uint32_t) * (g.nblk + 1));
   L.pairs = take(sizeof(unsigned long long) * (size_t)capacity);  // m1 <= m <= capacity
@@ -203,17 +203,27 @@ __device__ __forceinline__ void count_digits(uint32_t (*h)[256], uint32_t key, b
 }
 
 // Depth keys (fp32 bits; a Gaussian with no tile gets 0xffffffff and sorts
-// last), packed tile rectangles, and the counts of each value of each of the
-// four key digits (ghist[copy][digit][value], cleared before the launch).
+// last), packed tile rectangles, and, added into copy blockIdx mod
+// kHistCopies (cleared before the launch): the counts of each value of each
+// of the four key digits (ghist[copy][digit][value]), the Gaussians covering
+// each 8x8-tile block (bcopy[copy][block]; s_blk: 4 x geo.nblk words of
+// dynamic LDS, one row per wave so that waves do not contend) and the
+// intersection count (mcopy[copy]).
 __global__ __launch_bounds__(256) void depth_keys_kernel(
     int64_t n, const float* __restrict__ depth, const uint32_t* __restrict__ tiles,
-    const float* __restrict__ means2d, const float* __restrict__ extent, int ntx, int nty,
+    const float* __restrict__ means2d, const float* __restrict__ extent, Geo geo,
     uint32_t* __restrict__ keys, unsigned long long* __restrict__ rects,
-    uint32_t* __restrict__ ghist) {
+    uint32_t* __restrict__ ghist, uint32_t* __restrict__ bcopy,
+    unsigned long long* __restrict__ mcopy) {
+  extern __shared__ uint32_t s_blk[];
   __shared__ uint32_t h[4][256];
+  __shared__ unsigned long long s_m;
   const int tid = threadIdx.x;
 #pragma unroll
   for (int b = 0; b < 4; ++b) h[b][tid] = 0;
+  for (int b = tid; b < 4 * geo.nblk; b += kBlock) s_blk[b] = 0;
+  if (tid == 0) s_m = 0;
+  uint32_t* wblk = s_blk + (tid >> 6) * geo.nblk;
   const int64_t base = (int64_t)blockIdx.x * kDkTile;
   // every load of the thread's Gaussians in flight at once
   uint32_t tt[kDkItems];
@@ -229,6 +239,7 @@ __global__ __launch_bounds__(256) void depth_keys_kernel(
     ee[it] = ok ? reinterpret_cast<const float2*>(extent)[i] : make_float2(0.0f, 0.0f);
   }
   __syncthreads();
+  uint32_t m = 0;  // at most kDkItems x 32768 tiles
 #pragma unroll
   for (int it = 0; it < kDkItems; ++it) {
     const int64_t i = base + it * kBlock + tid;
@@ -236,21 +247,37 @@ __global__ __launch_bounds__(256) void depth_keys_kernel(
     const bool vis = ok && tt[it] != 0;
     const uint32_t key = vis ? __float_as_uint(dp[it]) : 0xffffffffu;
     int x0 = 1, y0 = 0, x1 = 0, y1 = 0;
-    if (vis && !tile_rect(mm[it].x, mm[it].y, ee[it].x, ee[it].y, ntx, nty, x0, y0, x1, y1))
-      x0 = 1, y0 = 0, x1 = 0, y1 = 0;
+    const bool hit = vis && tile_rect(mm[it].x, mm[it].y, ee[it].x, ee[it].y, geo.ntx, geo.nty, x0,
+                                      y0, x1, y1);
+    if (!hit) x0 = 1, y0 = 0, x1 = 0, y1 = 0;
     if (ok) {
       keys[i] = key;
       rects[i] = pack_rect(x0, y0, x1, y1);
     }
+    if (hit) {
+      m += (uint32_t)((x1 - x0 + 1) * (y1 - y0 + 1));
+      for (int by = y0 / kBlk; by <= y1 / kBlk; ++by)
+        for (int bx = x0 / kBlk; bx <= x1 / kBlk; ++bx) atomicAdd(&wblk[by * geo.nbx + bx], 1u);
+    }
     count_digits(h, key, ok);
   }
+  const uint32_t wm = wave_sum_u32(m);
+  if ((tid & 63) == 0 && wm) atomicAdd(&s_m, (unsigned long long)wm);
   __syncthreads();
-  uint32_t* copy = ghist + (blockIdx.x % kHistCopies) * (4 * 256);
+  const int copy = (int)(blockIdx.x % kHistCopies);
+  uint32_t* gh = ghist + copy * (4 * 256);
 #pragma unroll
   for (int b = 0; b < 4; ++b) {
     const uint32_t v = h[b][tid];
-    if (v) atomicAdd(&copy[b * 256 + tid], v);
+    if (v) atomicAdd(&gh[b * 256 + tid], v);
   }
+  uint32_t* bc = bcopy + (size_t)copy * geo.nblk;
+  for (int b = tid; b < geo.nblk; b += kBlock) {
+    const uint32_t v = s_blk[b] + s_blk[geo.nblk + b] + s_blk[2 * geo.nblk + b] +
+                       s_blk[3 * geo.nblk + b];
+    if (v) atomicAdd(&bc[b], v);
+  }
+  if (tid == 0 && s_m) atomicAdd(&mcopy[copy], s_m);
 }
 
 // Exclusive prefix of one value per thread over the 256 threads; s4 is four
@@ -272,32 +299,45 @@ __device__ __forceinline__ uint32_t scan_256(uint32_t v, uint32_t* s4) {
   return before + incl - v;
 }
 
-// Sum of the counts of `digit` in the partitions before `part` (part > 0),
-// read back through their states kRsLook at a time: aggregates are added
-// until an inclusive count ends the walk; a state not yet published is read
-// again (its partition is running and publishes without waiting).
-__device__ __forceinline__ uint32_t look_back(const unsigned long long* __restrict__ st,
-                                              int64_t part, int digit) {
+// Look-back state words: the two top bits flag the count below them as the
+// part's own (aggregate) or as the sum over it and every part before it
+// (inclusive); 0 is not yet published.
+template <typename W>
+struct StateWord {
+  static constexpr int kShift = 8 * (int)sizeof(W) - 2;
+  static constexpr W kAgg = (W)1 << kShift;
+  static constexpr W kIncl = (W)2 << kShift;
+};
+
+// Sum of the counts of item `idx` in the parts before `part` (part > 0; part
+// q's word at st[q * stride + idx]), read back kRsLook parts at a time:
+// aggregates are added until an inclusive count ends the walk; a word not yet
+// published is read again (its part is running and publishes without
+// waiting).
+template <typename W>
+__device__ __forceinline__ uint32_t look_back(const W* __restrict__ st, int64_t part,
+                                              int64_t stride, int64_t idx) {
+  using SW = StateWord<W>;
   uint32_t excl = 0;
   int64_t q = part - 1;
   while (true) {
-    unsigned long long s[kRsLook];
+    W s[kRsLook];
 #pragma unroll
     for (int j = 0; j < kRsLook; ++j)
-      s[j] = q - j >= 0 ? __hip_atomic_load(&st[(q - j) * 256 + digit], __ATOMIC_RELAXED,
+      s[j] = q - j >= 0 ? __hip_atomic_load(&st[(q - j) * stride + idx], __ATOMIC_RELAXED,
                                              __HIP_MEMORY_SCOPE_AGENT)
-                        : kStIncl;
+                        : SW::kIncl;
     int used = 0;
     bool open = true, found = false;
 #pragma unroll
     for (int j = 0; j < kRsLook; ++j) {
-      const unsigned long long f = s[j] & (3ull << 62);
+      const W f = s[j] & ((W)3 << SW::kShift);
       if (open && f != 0) {
-        excl += (uint32_t)s[j];
+        excl += (uint32_t)(s[j] & (SW::kAgg - 1));
         ++used;
-        if (f == kStIncl) found = true;
+        if (f == SW::kIncl) found = true;
       }
-      open = open && f == kStAgg;
+      open = open && f == SW::kAgg;
     }
     if (found) return excl;
     if (used == 0) __builtin_amdgcn_s_sleep(1);
@@ -403,7 +443,7 @@ __global__ __launch_bounds__(256) void radix_pass_kernel(
   }
   uint32_t excl = 0;
   if (part > 0) {
-    excl = look_back(st, part, tid);
+    excl = look_back(st, part, 256, tid);
     __hip_atomic_store(&st[part * 256 + tid], kStIncl | (excl + own), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -489,158 +529,84 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
 }
 
 
-// Per chunk of 1024 depth ranks: block counts (c1 row) and the chunk's
-// intersection count (cm; at most 1024 x 32768, so 32 bits suffice).
-__global__ __launch_bounds__(256) void l1_count_kernel(
+// Level 1, one workgroup per chunk of kChunk consecutive depth ranks (chunk
+// index from a ticket, in launch order). Wave w owns ranks [w kRanksPerWave,
+// (w + 1) kRanksPerWave) of the chunk and counts, per block, the pairs its Gaussians
+// make (LDS atomics). The chunk publishes its count of each block and reads
+// the earlier chunks' through one 32-bit state word per (chunk, block)
+// (decoupled look-back, as in the radix passes), so that a pair's slot is
+// the block's bucket offset + the block's pairs in earlier chunks + its
+// place in the chunk. Bucket offsets, the sub-chunk table and the overflow
+// decision come from the block totals and intersection count depth_keys
+// added up; every workgroup derives them (chunk 0 also writes them out). On
+// overflow nothing is placed. Dynamic LDS: 5 x geo.nblk words.
+__global__ __launch_bounds__(256) void l1_place_kernel(
     int64_t n, const uint32_t* __restrict__ order, const unsigned long long* __restrict__ rects,
-    Geo geo, uint32_t* __restrict__ c1, uint32_t* __restrict__ cm) {
-  extern __shared__ uint32_t cnt[];  // [nblk]
-  __shared__ uint32_t s_m;
-  for (int b = threadIdx.x; b < geo.nblk; b += blockDim.x) cnt[b] = 0;
-  if (threadIdx.x == 0) s_m = 0;
-  __syncthreads();
-  const int64_t r0 = (int64_t)blockIdx.x * kChunk;
-  const int64_t r1 = min<int64_t>(n, r0 + kChunk);
-  unsigned int m = 0;
-  for (int64_t r = r0 + threadIdx.x; r < r1; r += blockDim.x) {
-    const uint32_t g = order[r];
-    const Rect t = rect_of(g, rects);
-    if (t.x1 >= t.x0) m += (unsigned int)((t.x1 - t.x0 + 1) * (t.y1 - t.y0 + 1));
-    const Rect b = block_rect(t);
-    for (int y = b.y0; y <= b.y1; ++y)
-      for (int x = b.x0; x <= b.x1; ++x) atomicAdd(&cnt[y * geo.nbx + x], 1u);
-  }
-  const unsigned int wm = wave_sum_u32(m);
-  if ((threadIdx.x & 63) == 0 && wm) atomicAdd(&s_m, wm);
-  __syncthreads();
-  if (threadIdx.x == 0) cm[blockIdx.x] = s_m;
-  uint32_t* out = c1 + (int64_t)blockIdx.x * geo.nblk;
-  for (int b = threadIdx.x; b < geo.nblk; b += blockDim.x) out[b] = cnt[b];
-}
-
-// Intersection count M (sum of the chunk counts), bucket offsets, sub-chunk
-// offsets and the overflow decision, by one workgroup of kScanThreads.
-__device__ __forceinline__ void finish_l1(const uint32_t* __restrict__ blk_total, int nblk,
-                                          const uint32_t* __restrict__ cm, int64_t chunks,
-                                          unsigned long long capacity,
-                                          uint32_t* __restrict__ blk_off,
-                                          uint32_t* __restrict__ sub_off,
-                                          WsHeader* __restrict__ hdr) {
-  __shared__ unsigned long long part[kScanThreads];
-  __shared__ unsigned long long spart[kScanThreads];
+    Geo geo, const uint32_t* __restrict__ bcopy, const unsigned long long* __restrict__ mcopy,
+    unsigned long long capacity, int64_t chunks, uint32_t* __restrict__ lb,
+    uint32_t* __restrict__ blk_off, uint32_t* __restrict__ sub_off, WsHeader* __restrict__ hdr,
+    unsigned long long* __restrict__ pairs) {
+  using SW = StateWord<uint32_t>;
+  extern __shared__ uint32_t lds[];
+  uint32_t* slot = lds;                    // [4][nblk]: per wave counts, then next free slots
+  uint32_t* boff = lds + 4 * geo.nblk;     // [nblk]: block totals, then bucket offsets
+  __shared__ uint32_t s4[4];
+  __shared__ uint32_t s_chunk;
   __shared__ unsigned long long s_m;
-  if (threadIdx.x == 0) s_m = 0;
-  __syncthreads();
-  unsigned long long mc = 0;
-  for (int64_t c = threadIdx.x; c < chunks; c += kScanThreads) mc += cm[c];
-  mc += __shfl_xor(mc, 32, 64);
-  mc += __shfl_xor(mc, 16, 64);
-  mc += __shfl_xor(mc, 8, 64);
-  mc += __shfl_xor(mc, 4, 64);
-  mc += __shfl_xor(mc, 2, 64);
-  mc += __shfl_xor(mc, 1, 64);
-  if ((threadIdx.x & 63) == 0) atomicAdd(&s_m, mc);
-  __syncthreads();
+  const int nblk = geo.nblk;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  if (tid == 0) s_chunk = atomicAdd(&hdr->ticket_l1, 1u);
+  if (w == 0) {
+    const unsigned long long v = wave_sum_u64(lane < kHistCopies ? mcopy[lane] : 0ull);
+    if (lane == 0) s_m = v;
+  }
+  for (int t = tid; t < 4 * nblk; t += kBlock) slot[t] = 0;
+  // block totals and their exclusive prefixes (buckets) in pairs and in
+  // sub-chunks; thread tid takes the contiguous blocks [b0, b1)
+  const int per = (nblk + kBlock - 1) / kBlock;
+  const int b0 = min(nblk, per * tid), b1 = min(nblk, b0 + per);
+  uint32_t tot = 0, stot = 0;
+  for (int b = b0; b < b1; ++b) {
+    uint32_t c[kHistCopies];
+#pragma unroll
+    for (int r = 0; r < kHistCopies; ++r) c[r] = bcopy[(size_t)r * nblk + b];
+    uint32_t v = 0;
+#pragma unroll
+    for (int r = 0; r < kHistCopies; ++r) v += c[r];
+    boff[b] = v;
+    tot += v;
+    stot += (v + kSub - 1) / kSub;
+  }
+  uint32_t run = scan_256(tot, s4);  // its barriers publish s_chunk, s_m and the cleared slots
+  uint32_t srun = scan_256(stot, s4);
+  const int64_t chunk = s_chunk;
   const unsigned long long m = s_m;
-  if (threadIdx.x == 0) hdr->m = m;
   const bool over = m > capacity || m >= (1ull << 32);
-  const int per = (nblk + kScanThreads - 1) / kScanThreads;
-  const int lo = min(nblk, per * (int)threadIdx.x), hi = min(nblk, lo + per);
-  unsigned long long s = 0, ss = 0;
-  for (int b = lo; b < hi; ++b) {
-    s += blk_total[b];
-    ss += (blk_total[b] + kSub - 1) / kSub;
+  for (int b = b0; b < b1; ++b) {
+    const uint32_t v = boff[b];
+    boff[b] = run;
+    if (chunk == 0) {
+      blk_off[b] = run;
+      sub_off[b] = srun;
+    }
+    run += v;
+    srun += (v + kSub - 1) / kSub;
   }
-  part[threadIdx.x] = s;
-  spart[threadIdx.x] = ss;
-  __syncthreads();
-  for (int off = 1; off < kScanThreads; off <<= 1) {
-    const unsigned long long v = threadIdx.x >= off ? part[threadIdx.x - off] : 0ull;
-    const unsigned long long vs = threadIdx.x >= off ? spart[threadIdx.x - off] : 0ull;
-    __syncthreads();
-    part[threadIdx.x] += v;
-    spart[threadIdx.x] += vs;
-    __syncthreads();
-  }
-  unsigned long long run = part[threadIdx.x] - s, srun = spart[threadIdx.x] - ss;
-  for (int b = lo; b < hi; ++b) {
-    blk_off[b] = (uint32_t)run;
-    sub_off[b] = (uint32_t)srun;
-    run += blk_total[b];
-    srun += (blk_total[b] + kSub - 1) / kSub;
-  }
-  if (threadIdx.x == kScanThreads - 1) {
-    blk_off[nblk] = (uint32_t)run;
-    sub_off[nblk] = (uint32_t)srun;
+  if (chunk == 0 && tid == kBlock - 1) {  // the last range ends at the totals
+    blk_off[nblk] = run;
+    sub_off[nblk] = srun;
+    hdr->m = m;
     hdr->m1 = run;
     hdr->overflow = over ? 1u : 0u;
-    hdr->total_sub = over ? 0u : (uint32_t)srun;
+    hdr->total_sub = over ? 0u : srun;
   }
-}
-
-// counts[row][col] -> exclusive prefix down each column; column totals.
-// Lane = column, the 16 waves split the rows. The last workgroup then turns
-// the block totals into bucket and sub-chunk offsets (finish_l1).
-__global__ __launch_bounds__(1024) void scan_columns_kernel(
-    uint32_t* __restrict__ counts, int64_t rows, int cols, uint32_t* __restrict__ col_total,
-    const uint32_t* __restrict__ cm, unsigned long long capacity, uint32_t* __restrict__ blk_off,
-    uint32_t* __restrict__ sub_off, WsHeader* __restrict__ hdr) {
-  __shared__ uint32_t part[16][64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + lane;
-  const int64_t per = (rows + 15) / 16;
-  const int64_t q0 = min<int64_t>(rows, per * w), q1 = min<int64_t>(rows, q0 + per);
-  // rows are read eight at a time so that eight loads are in flight
-  uint32_t s = 0;
-  if (c < cols)
-    for (int64_t q = q0; q < q1; q += 8) {
-      uint32_t v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? counts[(q + u) * cols + c] : 0u;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) s += v[u];
-    }
-  part[w][lane] = s;
-  __syncthreads();
-  uint32_t run = 0;
-  for (int k = 0; k < w; ++k) run += part[k][lane];
-  if (c < cols) {
-    for (int64_t q = q0; q < q1; q += 8) {
-      uint32_t v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? counts[(q + u) * cols + c] : 0u;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (q + u < q1) counts[(q + u) * cols + c] = run;
-        run += v[u];
-      }
-    }
-    if (w == 15) col_total[c] = run;
-  }
-  if (last_workgroup(&hdr->done_cols))
-    finish_l1(col_total, cols, cm, rows, capacity, blk_off, sub_off, hdr);
-}
-
-// Ordered scatter of (block, Gaussian) pairs of one chunk of depth ranks into
-// the bucket-major pair array. Wave w owns ranks [w * 256, w * 256 + 256) of
-// the chunk; LDS holds, per wave and block, the next free slot.
-__global__ __launch_bounds__(256) void l1_scatter_kernel(
-    int64_t n, const uint32_t* __restrict__ order, const unsigned long long* __restrict__ rects,
-    Geo geo,
-    const uint32_t* __restrict__ c1, const uint32_t* __restrict__ blk_off,
-    const WsHeader* __restrict__ hdr, unsigned long long* __restrict__ pairs) {
-  extern __shared__ uint32_t slot[];  // [4][nblk]
-  if (hdr->overflow) return;
-  const int nblk = geo.nblk;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t rbase = (int64_t)blockIdx.x * kChunk + (int64_t)w * kRanksPerWave;
+  if (over) return;  // the same decision in every workgroup: nobody waits
   uint32_t* my = slot + w * nblk;
-  for (int t = threadIdx.x; t < 4 * nblk; t += blockDim.x) slot[t] = 0;
-  __syncthreads();
-  uint32_t gj[4];
-  Rect bj[4], tj[4];
+  const int64_t rbase = chunk * kChunk + (int64_t)w * kRanksPerWave;
+  uint32_t gj[kL1Items];
+  Rect bj[kL1Items], tj[kL1Items];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < kL1Items; ++j) {
     const int64_t r = rbase + lane + 64 * j;
     gj[j] = r < n ? order[r] : 0u;
     tj[j] = r < n ? rect_of(gj[j], rects) : Rect{0, 0, -1, -1};
@@ -649,14 +615,30 @@ __global__ __launch_bounds__(256) void l1_scatter_kernel(
       for (int x = bj[j].x0; x <= bj[j].x1; ++x) atomicAdd(&my[y * geo.nbx + x], 1u);
   }
   __syncthreads();
-  const uint32_t* crow = c1 + (int64_t)blockIdx.x * nblk;
-  for (int b = threadIdx.x; b < nblk; b += blockDim.x) {
-    uint32_t run = blk_off[b] + crow[b];
+  // publish this chunk's count of each of the thread's blocks, then read the
+  // earlier chunks' and turn the per-wave counts into slots
+  for (int b = b0; b < b1; ++b) {
+    const uint32_t own = slot[b] + slot[nblk + b] + slot[2 * nblk + b] + slot[3 * nblk + b];
+    __hip_atomic_store(&lb[chunk * nblk + b], (chunk == 0 ? SW::kIncl : SW::kAgg) | own,
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  for (int b = b0; b < b1; ++b) {
+    uint32_t excl = 0;
+    if (chunk > 0) {
+      excl = look_back(lb, chunk, nblk, b);
+      // the inclusive count of a chunk before the last stays below n <= 2^30
+      if (chunk + 1 < chunks) {
+        const uint32_t own = slot[b] + slot[nblk + b] + slot[2 * nblk + b] + slot[3 * nblk + b];
+        __hip_atomic_store(&lb[chunk * nblk + b], SW::kIncl | (excl + own), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    uint32_t at = boff[b] + excl;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const uint32_t c = slot[k * nblk + b];
-      slot[k * nblk + b] = run;
-      run += c;
+      slot[k * nblk + b] = at;
+      at += c;
     }
   }
   __syncthreads();
@@ -664,28 +646,34 @@ __global__ __launch_bounds__(256) void l1_scatter_kernel(
   // entry walks its block rectangle row-major, so the smallest pending block
   // of the wave is the current cell of every entry that covers it; ballots
   // give each such entry its rank (entries in rank order: j, then lane).
-  uint32_t nb[4];
-  int cx[4], cy[4];
+  uint32_t nb[kL1Items];
+  int cx[kL1Items], cy[kL1Items];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < kL1Items; ++j) {
     cx[j] = bj[j].x0;
     cy[j] = bj[j].y0;
     nb[j] = bj[j].x1 >= bj[j].x0 ? (uint32_t)(cy[j] * geo.nbx + cx[j]) : kNoBlock;
   }
   const uint64_t lt = lanemask_lt();
   while (true) {
-    const uint32_t B = wave_min_u32(min(min(nb[0], nb[1]), min(nb[2], nb[3])));
-    if (B == kNoBlock) break;
-    uint32_t run = my[B];
+    uint32_t lo = nb[0];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 1; j < kL1Items; ++j) lo = min(lo, nb[j]);
+    const uint32_t B = wave_min_u32(lo);
+    if (B == kNoBlock) break;
+    uint32_t at = my[B];
+#pragma unroll
+    for (int j = 0; j < kL1Items; ++j) {
       const bool hit = nb[j] == B;
       const uint64_t bal = __ballot(hit);
       if (hit) {
-        // the pair carries the rectangle clipped to its block, packed
-        pairs[run + __popcll(bal & lt)] =
-            (unsigned long long)gj[j] |
-            ((unsigned long long)pack_local(clip_to_block(tj[j], cx[j], cy[j])) << 32);
+        // the pair carries the rectangle clipped to its block, packed (the
+        // slot is below m1 <= capacity; the test keeps any inconsistency in
+        // the counts from writing past the array)
+        const uint32_t pos = at + (uint32_t)__popcll(bal & lt);
+        if (pos < capacity)
+          pairs[pos] = (unsigned long long)gj[j] |
+                       ((unsigned long long)pack_local(clip_to_block(tj[j], cx[j], cy[j])) << 32);
         if (cx[j] < bj[j].x1) {
           ++cx[j];
         } else {
@@ -694,20 +682,19 @@ __global__ __launch_bounds__(256) void l1_scatter_kernel(
         }
         nb[j] = cy[j] <= bj[j].y1 ? (uint32_t)(cy[j] * geo.nbx + cx[j]) : kNoBlock;
       }
-      run += (uint32_t)__popcll(bal);
+      at += (uint32_t)__popcll(bal);
     }
-    if (lane == 0) my[B] = run;
+    if (lane == 0) my[B] = at;
   }
 }
 
 // ------------------------------------------------------------- level 2
 //
-// A block has 8 x 8 = 64 tiles: lane l of a wave owns local tile l
-// (x = l % 8, y = l / 8). For each bucket entry, in depth order, every lane
-// tests whether its tile lies in the entry's rectangle; counts and running
-// positions stay in registers. Sub-chunks of 256 entries are staged in LDS
-// as one-byte entry indices (at most 256 x 64 of them, 16 KB, so that eight
-// workgroups fit a CU) and leave as one coalesced run per tile.
+// A block has 8 x 8 = 64 tiles (local tile l at x = l % 8, y = l / 8). Each
+// bucket is cut into sub-chunks of kSub consecutive entries; per sub-chunk,
+// l2_count counts each tile's entries, l2_scan turns the counts into each
+// sub-chunk's first slot in every tile list, and l2_scatter writes the
+// entries.
 
 struct SubChunk {
   int bx, by;        // block
@@ -1252,8 +1239,23 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
     ABCD_LAUNCH("bin_zero", bin_zero_kernel, std::min<int64_t>(1024, (words + kBlock - 1) / kBlock),
                 kBlock, 0, stream, reinterpret_cast<uint4*>(ws + L.hdr), words);
   }
-  ABCD_LAUNCH("depth_keys", depth_keys_kernel, (n + kDkTile - 1) / kDkTile, kBlock, 0, stream, n,
-              depth, tiles_touched, means2d, extent, geo.ntx, geo.nty, keys[0], rects, ghist);
+  static bool attrs_set = false;
+  if (!attrs_set) {
+    // depth_keys keeps 4 words and level 1 5 words per block of any frame of
+    // at most ABCD_MAX_TILES tiles (at most ABCD_MAX_TILES / 8 blocks)
+    int32_t st = set_max_lds((const void*)depth_keys_kernel,
+                             4 * sizeof(uint32_t) * (ABCD_MAX_TILES / kBlk + 1));
+    if (st != ABCD_OK) return st;
+    st = set_max_lds((const void*)l1_place_kernel,
+                     5 * sizeof(uint32_t) * (ABCD_MAX_TILES / kBlk + 1));
+    if (st != ABCD_OK) return st;
+    attrs_set = true;
+  }
+  uint32_t* bcopy = u32(L.bcopy);
+  unsigned long long* mcopy = reinterpret_cast<unsigned long long*>(ws + L.mcopy);
+  ABCD_LAUNCH("depth_keys", depth_keys_kernel, (n + kDkTile - 1) / kDkTile, kBlock,
+              4 * sizeof(uint32_t) * geo.nblk, stream, n, depth, tiles_touched, means2d, extent, geo,
+              keys[0], rects, ghist, bcopy, mcopy);
   for (int pass = 0; pass < 4; ++pass) {
     const int src = pass & 1, dst = src ^ 1;
     ABCD_LAUNCH("radix_pass", radix_pass_kernel, L.rs_parts, kBlock, 0, stream, keys[src],
@@ -1263,30 +1265,16 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   }
   const uint32_t* order = vals[0];  // four passes: back in buffer 0
 
-  static bool attrs_set = false;
-  if (!attrs_set) {
-    int32_t st = set_max_lds((const void*)l1_count_kernel, 65536);
-    if (st != ABCD_OK) return st;
-    st = set_max_lds((const void*)l1_scatter_kernel, 65536);
-    if (st != ABCD_OK) return st;
-    attrs_set = true;
-  }
   const unsigned long long cap = (unsigned long long)std::max<int64_t>(capacity, 0);
-  uint32_t* c1 = u32(L.c1);
-  uint32_t* blk_total = u32(L.blk_total);
   uint32_t* blk_off = u32(L.blk_off);
   uint32_t* sub_off = u32(L.sub_off);
   unsigned long long* pairs = reinterpret_cast<unsigned long long*>(ws + L.pairs);
   uint32_t* c2 = u32(L.c2);
   uint32_t* tile_total = u32(L.tile_total);
   uint32_t* tile_off = u32(L.tile_off);
-  uint32_t* cm = u32(L.cm);
-  ABCD_LAUNCH("l1_count", l1_count_kernel, L.chunks, kBlock, sizeof(uint32_t) * geo.nblk, stream, n,
-              order, rects, geo, c1, cm);
-  ABCD_LAUNCH("l1_scan_columns", scan_columns_kernel, (geo.nblk + 63) / 64, 1024, 0, stream, c1,
-              L.chunks, geo.nblk, blk_total, cm, cap, blk_off, sub_off, hdr);
-  ABCD_LAUNCH("l1_scatter", l1_scatter_kernel, L.chunks, kBlock, 4 * sizeof(uint32_t) * geo.nblk,
-              stream, n, order, rects, geo, c1, blk_off, hdr, pairs);
+  ABCD_LAUNCH("l1_place", l1_place_kernel, L.chunks, kBlock, 5 * sizeof(uint32_t) * geo.nblk,
+              stream, n, order, rects, geo, bcopy, mcopy, cap, L.chunks, u32(L.lb1), blk_off,
+              sub_off, hdr, pairs);
   ABCD_LAUNCH("l2_count", l2_count_kernel, 4 * kStrideGrid, 64, 0, stream, pairs, geo, sub_off,
               blk_off, hdr, c2);
   ABCD_LAUNCH("l2_scan", l2_scan_kernel, geo.nblk, 1024, 0, stream, c2, geo, sub_off, hdr,

@@ -191,6 +191,33 @@ def test_bin_sort_bitexact(api, case):
     assert torch.equal(b2["keys"][:m], b["keys"][:m])
 
 
+
+@pytest.mark.parametrize("width", [16400, 33000])
+def test_bin_sort_wide_strip_frames(api, width):
+    """Frames of many 8x8-tile blocks (129 and 258 in one block row; 2,050
+    and 4,126 tiles): the level-2 sub-chunk lookup scans blocks in several
+    64-lane rounds, and at 258 blocks each level-1 thread publishes and looks
+    back for two blocks. 3,000 Gaussians along the horizon of a 32-pixel-high
+    strip; lists, keys and ranges bit-exact against the oracle."""
+    say("bin_sort wide strip", width)
+    rr = S.rng(31)
+    cam = look_at((0.0, -3.0, 0.0), (0, 0, 0), width, 32, fov_x_deg=120.0)
+    prm = RasterParams(sh_degree=0)
+    means = np.stack([rr.uniform(-4.5, 4.5, 3000), rr.uniform(-0.5, 0.5, 3000),
+                      rr.uniform(-0.003, 0.003, 3000)], 1)
+    scene = S.gaussians(rr, means, 0, math.log(0.003), 0.6)
+    ob, proj = _oracle_inputs_f32(cam, prm, scene)
+    keys, values, ranges = O.bin(cam.width, cam.height, ob["depth"], ob["rect"], ob["tiles_touched"])
+    assert len(values) > 3000
+    pd = to_dev(proj)
+    b = api.bin_sort(cam.width, cam.height, pd, want_keys=True)
+    torch.cuda.synchronize()
+    m = b["n_isect"]
+    assert m == len(values)
+    assert np.array_equal(np32(b["values"][:m]).view(np.uint32), values)
+    assert np.array_equal(np32(b["keys"][:m]).view(np.uint64), keys)
+    assert np.array_equal(np32(b["tile_ranges"]).view(np.uint32), ranges)
+
 def _fwd_compare(got, ref, H, W):
     """Max error off the knife-edge pixels, and the number of knife-edge pixels.
     On a knife-edge pixel one threshold decision may legitimately differ
