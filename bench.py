@@ -38,10 +38,12 @@ PROFILES = os.path.join(ROOT, "profiles")
 HBM_PROFILE = "step_1m_1297x840_hbm_bytes.md"
 SQ_PROFILE = "step_1m_1297x840_sq_counters.md"
 
-KERNELS = ["composite", "project", "depth_keys", "radix_hist", "radix_scan", "radix_scatter",
-           "l1_count", "l1_scan_columns", "l1_finish", "l1_scatter", "l2_count", "l2_scan",
-           "bin_scan_tiles", "l2_scatter", "bin_tile_order", "render_fwd", "loss_l1", "zero_fill",
-           "bwd_order", "render_bwd", "project_bwd", "adam"]
+KERNELS = ["composite", "project", "bin_zero", "depth_keys", "radix_pass", "l1_place", "l2_count",
+           "l2_scan", "l2_scatter", "bin_small_sort", "bin_small_collect", "render_fwd", "loss_l1",
+           "zero_fill", "bwd_order", "render_bwd", "project_bwd", "adam"]
+# the launches of abcd_bin_sort (general path, then the small-block path)
+BIN_KERNELS = ["bin_zero", "depth_keys", "radix_pass", "l1_place", "l2_count", "l2_scan",
+               "l2_scatter", "bin_small_sort", "bin_small_collect"]
 
 
 def parse():
@@ -481,6 +483,9 @@ def main():
         "small_config": small,
         "configs": configs,
         "kernels": kern,
+        "binning": ({"ms_per_step": sum(kern[x]["ms_per_step"] for x in BIN_KERNELS if x in kern),
+                     "launches_per_step": sum(kern[x]["launches_per_step"] for x in BIN_KERNELS
+                                              if x in kern)} if kern else None),
         "setup_s": setup_s,
     }
     print(json.dumps(out))

@@ -796,26 +796,40 @@ __global__ __launch_bounds__(64) void l2_count_kernel(
 __device__ __forceinline__ void scan_tiles(const uint32_t* __restrict__ tile_total, int ntiles,
                                            uint32_t* __restrict__ tile_off,
                                            uint32_t* __restrict__ tile_ranges) {
-  __shared__ unsigned long long part[kScanThreads];
+  // thread t takes the contiguous tiles [lo, hi), all loads in flight at
+  // once; the sums fit 32 bits (M < 2^32 unless overflowing, and then every
+  // total is 0)
+  constexpr int kMaxPer = (ABCD_MAX_TILES + kScanThreads - 1) / kScanThreads;
+  __shared__ uint32_t s_wave[kScanThreads / 64];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int per = (ntiles + kScanThreads - 1) / kScanThreads;
-  const int lo = min(ntiles, per * (int)threadIdx.x), hi = min(ntiles, lo + per);
-  unsigned long long s = 0;
-  for (int i = lo; i < hi; ++i) s += tile_total[i];
-  part[threadIdx.x] = s;
-  __syncthreads();
-  for (int off = 1; off < kScanThreads; off <<= 1) {
-    const unsigned long long v = threadIdx.x >= off ? part[threadIdx.x - off] : 0ull;
-    __syncthreads();
-    part[threadIdx.x] += v;
-    __syncthreads();
+  const int lo = min(ntiles, per * tid), hi = min(ntiles, lo + per);
+  uint32_t v[kMaxPer];
+  uint32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kMaxPer; ++k) {
+    v[k] = lo + k < hi ? tile_total[lo + k] : 0u;
+    s += v[k];
   }
-  unsigned long long run = part[threadIdx.x] - s;
-  for (int i = lo; i < hi; ++i) {
-    const uint32_t v = tile_total[i];
-    tile_off[i] = (uint32_t)run;
-    tile_ranges[2 * i] = (uint32_t)run;
-    tile_ranges[2 * i + 1] = (uint32_t)(run + v);
-    run += v;
+  uint32_t incl = s;  // inclusive prefix over the wave
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = (uint32_t)__shfl_up((int)incl, d, 64);
+    if (lane >= d) incl += y;
+  }
+  if (lane == 63) s_wave[w] = incl;
+  __syncthreads();
+  uint32_t run = incl - s;
+#pragma unroll
+  for (int k = 0; k < kScanThreads / 64; ++k) run += k < w ? s_wave[k] : 0u;
+#pragma unroll
+  for (int k = 0; k < kMaxPer; ++k) {
+    if (lo + k < hi) {
+      tile_off[lo + k] = run;
+      tile_ranges[2 * (lo + k)] = run;
+      tile_ranges[2 * (lo + k) + 1] = run + v[k];
+    }
+    run += v[k];
   }
 }
 
@@ -1211,7 +1225,7 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   char* ws = static_cast<char*>(workspace);
   WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
   if (n == 0) {
-    ABCD_LAUNCH("bin_scan_tiles", bin_empty_kernel, std::max(1, (2 * ntiles + 255) / 256), 256, 0,
+    ABCD_LAUNCH("bin_empty", bin_empty_kernel, std::max(1, (2 * ntiles + 255) / 256), 256, 0,
                 stream, ntiles, tile_ranges, tile_order, hdr);
     ABCD_HIP(hipGetLastError());
     return ABCD_OK;
