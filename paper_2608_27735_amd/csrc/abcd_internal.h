@@ -287,6 +287,7 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
                                  const float* final_T, const uint32_t* last,
                                  const float* dL_dout, float* g2d, const SplitLayout& split,
                                  hipStream_t stream);
+// (launch_render_bwd_pixels clears g2d, 9 g2d_stride(n) floats, itself)
 int32_t launch_zero(float* p, int64_t count, hipStream_t stream);
 int32_t launch_loss_l1(int width, int height, const float* out_rgba, const float* target_rgb,
                        float bg0, float bg1, float bg2, float* dL_dout, float* loss,
@@ -302,9 +303,12 @@ int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, con
 // by queue i mod kQueues, whose counter is queue[kQueueStride q + 1].
 constexpr int kQueues = 8;
 constexpr int kQueueStride = 64;
+// The same launch clears zero[0, zero_count) (16-byte aligned, a multiple of
+// 4 floats) with workgroups of its own, beside the one that schedules.
 int32_t launch_bwd_schedule(int ntiles, const uint32_t* key, const uint32_t* walk,
                             uint32_t* order, const SplitLayout& split, void* items, uint32_t cap,
-                            uint32_t* queue, hipStream_t stream);
+                            uint32_t* queue, float* zero, int64_t zero_count,
+                            hipStream_t stream);
 int32_t launch_tile_walk(int width, int height, const uint32_t* last, uint32_t* work,
                          hipStream_t stream);
 

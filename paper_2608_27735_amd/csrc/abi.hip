@@ -358,7 +358,6 @@ static int32_t render_bwd_impl(const abcd_camera* cam, const abcd_raster_params*
   // every argument is valid: only now the static scratch's address (a HIP call)
   if (noalloc) TRY(noalloc_scratch(&workspace));
   float* g2d = static_cast<float*>(workspace);
-  TRY(launch_zero(g2d, 9 * g2d_stride(n), stream));
   TRY(launch_render_bwd_pixels(*cam, *prm, n, tile_ranges, values_sorted, means2d, conic_opacity,
                                rgb, F, B, final_T, last, dL_dout, g2d, sl, stream));
   return launch_project_bwd(*cam, *prm, n, means, log_scales, quats, opacity_logits, sh, extent,

@@ -392,7 +392,9 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
                                  const float* dL_dout, float* g2d, const SplitLayout& split,
                                  hipStream_t stream) {
   const BlendConsts k = consts(cam, prm);
+  const int64_t g2d_count = 9 * g2d_stride(n);
   if (!split.ckpt && k.ntiles <= kDirectTiles) {
+    TRY_STATUS(launch_zero(g2d, g2d_count, stream));
     ABCD_LAUNCH("render_bwd", render_bwd_direct_kernel, k.ntiles, kBlock, 0, stream, k,
                 tile_ranges, values_sorted, reinterpret_cast<const float2*>(means2d),
                 reinterpret_cast<const float4*>(conic_opacity), rgb,
@@ -418,7 +420,7 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
   // heaviest items first: by the forward's per-chunk estimate when split,
   // else by the walk
   TRY_STATUS(launch_bwd_schedule(k.ntiles, split.ckpt ? split.work : walk, walk, order, split,
-                                 items, max_items, queue, stream));
+                                 items, max_items, queue, g2d, g2d_count, stream));
   const int grid = (int)std::min<int64_t>(bwd_resident_blocks(), max_items);
   ABCD_LAUNCH("render_bwd", render_bwd_kernel, grid, kBlock, 0, stream, k, tile_ranges,
               values_sorted, reinterpret_cast<const float2*>(means2d),

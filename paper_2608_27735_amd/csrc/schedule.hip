@@ -92,18 +92,25 @@ __device__ __forceinline__ void build_items(int ntiles, const uint16_t* s_order,
   if (tid < kQueues) queue[kQueueStride * tid + 1] = 0;
 }
 
-// The backward's schedule in one launch: tiles ordered by `key`, then the
-// work items in that order (walk: each tile's largest per-pixel walk). Every
-// global load (key, walk and the split slot of each tile) is issued in the
-// first loop; the rest works in workgroup memory.
+// The backward's schedule in one launch: workgroup 0 orders the tiles by
+// `key` and writes the work items in that order (walk: each tile's largest
+// per-pixel walk; every global load -- key, walk and the split slot of each
+// tile -- is issued in its first loop, the rest works in workgroup memory);
+// the other workgroups clear zero[0, zero_count) meanwhile (16-byte stores).
 __global__ __launch_bounds__(kOrderThreads) void bwd_schedule_kernel(
     int ntiles, const uint32_t* __restrict__ key, const uint32_t* __restrict__ walk,
     uint32_t* __restrict__ order, SplitLayout sp, uint2* __restrict__ items, uint32_t cap,
-    uint32_t* __restrict__ queue) {
+    uint32_t* __restrict__ queue, float4* __restrict__ zero, int64_t zero4) {
   __shared__ uint8_t s_key[ABCD_MAX_TILES];      // bucket of each tile
   __shared__ uint8_t s_nt[ABCD_MAX_TILES];       // work items of each tile
   __shared__ uint16_t s_order[ABCD_MAX_TILES];   // the order
   static_assert(ABCD_MAX_TILES <= 65536, "tile indices are kept in 16 bits");
+  if (blockIdx.x > 0) {
+    const int64_t stride = (int64_t)(gridDim.x - 1) * kOrderThreads;
+    for (int64_t j = (int64_t)(blockIdx.x - 1) * kOrderThreads + threadIdx.x; j < zero4; j += stride)
+      zero[j] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    return;
+  }
   // eight tiles per thread at a time, their loads issued together (indices
   // clamped into the arrays, so that no load waits behind a branch)
   constexpr int kAt = 8;
@@ -141,9 +148,15 @@ __global__ __launch_bounds__(kOrderThreads) void bwd_schedule_kernel(
 
 int32_t launch_bwd_schedule(int ntiles, const uint32_t* key, const uint32_t* walk,
                             uint32_t* order, const SplitLayout& split, void* items, uint32_t cap,
-                            uint32_t* queue, hipStream_t stream) {
-  ABCD_LAUNCH("bwd_order", bwd_schedule_kernel, 1, kOrderThreads, 0, stream, ntiles, key, walk,
-              order, split, reinterpret_cast<uint2*>(items), cap, queue);
+                            uint32_t* queue, float* zero, int64_t zero_count,
+                            hipStream_t stream) {
+  // workgroups hold ~137 KB of LDS each (one per CU): one schedules, up to
+  // 255 clear
+  const int64_t zero4 = zero_count / 4;
+  const int grid = 1 + (int)std::min<int64_t>(255, (zero4 + kOrderThreads - 1) / kOrderThreads);
+  ABCD_LAUNCH("bwd_order", bwd_schedule_kernel, grid, kOrderThreads, 0, stream, ntiles, key, walk,
+              order, split, reinterpret_cast<uint2*>(items), cap, queue,
+              reinterpret_cast<float4*>(zero), zero4);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }
