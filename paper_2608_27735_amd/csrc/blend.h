@@ -122,6 +122,29 @@ __device__ __forceinline__ uint32_t splat_rows(float u, float v, float a, float 
   return rows;
 }
 
+// The same test for single pixel rows: bit w set when pixel row row0 + w of
+// the tile (clipped to the image) can see the Gaussian. With the row fixed,
+// the minimum over the columns is at dx = -b dy / a clamped to the columns.
+__device__ __forceinline__ uint32_t splat_rows_single(float u, float v, float a, float b, float c,
+                                                      float o, float alpha_min, const TileBox& box,
+                                                      int row0) {
+  if (!(o >= alpha_min)) return 0u;
+  const float tau = 2.0f * (__logf(o) - __logf(alpha_min));
+  const float lim = tau * 1.001f + 1e-3f;
+  const float ia = a > 0.0f ? 1.0f / a : 0.0f;
+  const float dx0 = box.x0 - u, dx1 = box.x1 - u;
+  uint32_t rows = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float yb = box.y0 + (float)(row0 + w);
+    const float dy = yb - v;
+    const float dx = fminf(fmaxf(-b * dy * ia, dx0), dx1);
+    const float q = a * dx * dx + 2.0f * b * dx * dy + c * dy * dy;
+    if (yb <= box.y1 && q <= lim) rows |= 1u << w;
+  }
+  return rows;
+}
+
 // Block-wide compaction of the staged entries (as compact() does) and, for
 // each wave w, the list of the staged slots whose rows mask has bit w, in
 // list order, into s_idx[w]. s_cnt holds 5 x 4 wave counts. Returns the

@@ -355,6 +355,230 @@ __global__ __launch_bounds__(256) void render_bwd_direct_kernel(
            last, dL_dout, g2d, gs, SplitLayout{});
 }
 
+// Lane-bit-4 and lane-bit-5 exchanges. v_permlane16_swap of (x, x) leaves
+// rows (0, 0, 2, 2) of x in its first result and rows (1, 1, 3, 3) in its
+// second; v_permlane32_swap of (x, x) leaves halves (low, low) and (high,
+// high). Either way the two results combined give the pair's total with the
+// same operands in the same order on both partners, and a lane with the
+// exchanged bit set finds its partner's value in the first result.
+struct Swapped {
+  float first, second;
+};
+__device__ __forceinline__ Swapped swap_bit4(float x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_int(x), __float_as_int(x), false, false);
+  return Swapped{__int_as_float(p[0]), __int_as_float(p[1])};
+}
+__device__ __forceinline__ Swapped swap_bit5(float x) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(x), __float_as_int(x), false, false);
+  return Swapped{__int_as_float(p[0]), __int_as_float(p[1])};
+}
+
+// Sums of nine values over each 16-lane row, by a butterfly over lane bits 3
+// (row rotate 8), 2 (half-row mirror, which pairs lanes whose bit 2 differs),
+// 1 and 0 (quad permutes): each step halves values 0-7 with one select pair
+// and one DPP add. On return lane c of a row holds the row total of value
+// rowsum9_slot(c), and every lane the total of value 8 in v8.
+__device__ __forceinline__ float row_sum9(const float (&g)[9], int c, float& v8) {
+  const bool b3 = c & 8, b2 = c & 4, b1 = c & 2;
+  float h[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    h[i] = (b3 ? g[2 * i + 1] : g[2 * i]) + dpp_mov<0x128>(b3 ? g[2 * i] : g[2 * i + 1]);
+  const float k0 = (b2 ? h[1] : h[0]) + dpp_mov<0x141>(b2 ? h[0] : h[1]);
+  const float k1 = (b2 ? h[3] : h[2]) + dpp_mov<0x141>(b2 ? h[2] : h[3]);
+  float m = (b1 ? k1 : k0) + dpp_mov<0x4E>(b1 ? k0 : k1);
+  m += dpp_mov<0xB1>(m);
+  v8 = g[8];
+  v8 += dpp_mov<0x128>(v8);
+  v8 += dpp_mov<0x141>(v8);
+  v8 += dpp_mov<0x4E>(v8);
+  v8 += dpp_mov<0xB1>(v8);
+  return m;
+}
+__device__ __forceinline__ int rowsum9_slot(int c) {
+  return 4 * ((c >> 1) & 1) + 2 * ((c >> 2) & 1) + ((c >> 3) & 1);
+}
+
+// Small frames, where one workgroup per tile leaves most of the chip idle and
+// the longest list sets the launch's length: four workgroups per tile (rows
+// 4q .. 4q + 3 for quarter q), one pixel row per wave, and four list entries
+// per step of a wave. Lane l holds column l & 15 of the wave's row and entry
+// l >> 4 of the step (entry 0 the backmost); the four copies of a pixel's
+// state stay identical. Within a step the pixel's back-to-front recurrences
+// over the four entries run as scans over lane bits 4 and 5: the
+// transmittance before each entry is the running one times a prefix product
+// of 1 / (1 - alpha), and the colour blended behind it a prefix sum S of
+// alpha T (c . g), not normalised by the transmittance, so that the
+// alpha-derivative is T (c . g) - (S + T_final g_T) / (1 - alpha).
+constexpr int kRowsTiles = 256;
+
+__global__ __launch_bounds__(256) void render_bwd_rows_kernel(
+    BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,
+    const float2* __restrict__ means2d, const float4* __restrict__ conic_opacity,
+    const float* __restrict__ rgb, const float4* __restrict__ F, const float4* __restrict__ B,
+    const float* __restrict__ final_T, const uint32_t* __restrict__ last,
+    const float4* __restrict__ dL_dout, float* __restrict__ g2d, int64_t gs) {
+  __shared__ float4 s_ga[256];  // u, v, qa, qb
+  __shared__ float4 s_gb[256];  // qc, o, r, g
+  __shared__ float4 s_gc[256];  // a, b, c (conic), colour b
+  __shared__ int s_pos[256];
+  __shared__ uint32_t s_g[256];
+  __shared__ float s_acc[9 * 256];  // entry-major: [entry][9]
+  __shared__ __align__(4) uint8_t s_idx[4][256];  // per wave: staged slots reaching its row
+  __shared__ int s_wcnt[5][4];
+  __shared__ uint32_t s_max;
+  const int tile = (int)(blockIdx.x >> 2), quarter = (int)(blockIdx.x & 3);
+  const int tid = threadIdx.x, lane = tid & 63, col = lane & 15, e = lane >> 4;
+  const int px = (tile % k.ntx) * kTile + col;
+  const int py = (tile / k.ntx) * kTile + 4 * quarter + (tid >> 6);
+  const bool inside = px < k.width && py < k.height;
+  const TileBox box = tile_box(k, tile);
+  const uint32_t start = tile_ranges[2 * tile];
+  const float fx = (float)px + 0.5f, fy = (float)py + 0.5f;
+  float T = 1.0f, gcr = 0, gcg = 0, gcb = 0, gT = 0;
+  uint32_t lastp = 0;
+  if (tid == 0) s_max = 0;
+  __syncthreads();
+  if (inside) {
+    const int64_t p = (int64_t)py * k.width + px;
+    T = final_T[p];
+    lastp = last[p];
+    const float4 G = dL_dout[p];
+    const float4 f = F ? F[p] : make_float4(0, 0, 0, 0);
+    const float4 bb = B ? B[p] : make_float4(0, 0, 0, 0);
+    const float s = 1.0f - f.w;
+    gcr = s * G.x;
+    gcg = s * G.y;
+    gcb = s * G.z;
+    gT = s * (G.x * bb.x + G.y * bb.y + G.z * bb.z - G.w * (1.0f - bb.w));
+    if (lastp > 0u) atomicMax(&s_max, lastp);
+  }
+  __syncthreads();
+  const uint32_t nent = __builtin_amdgcn_readfirstlane(s_max);  // end of the quarter's walk
+  const float TgT = T * gT;  // T is the final transmittance here
+  float S = 0.0f;            // colour behind the step (sum of alpha T (c . g))
+  uint32_t wml = lastp;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) wml = max(wml, (uint32_t)__shfl_xor((int)wml, off, 64));
+  wml = __builtin_amdgcn_readfirstlane(wml);
+  const bool odd = lane & 16, high = lane & 32;
+  const bool adder = (col & 1) == 0 || col == 1;
+  const int slot = col == 1 ? 8 : rowsum9_slot(col);
+  const uint32_t bstop = start;
+  uint32_t bend = start + nent;
+  Rec rec{};
+  uint32_t gid_next = 0;
+  if (bend > bstop) {  // uniform
+    const uint32_t b1 = bend - min(256u, bend - bstop);
+    const uint32_t p0 = bend - 1 - tid, p1 = b1 - 1 - tid;
+    const uint32_t gid0 = values[(uint32_t)tid < bend - bstop ? p0 : bstop];
+    gid_next = values[(uint32_t)tid < b1 - bstop ? p1 : bstop];
+    rec = gather_rec(gid0, (uint32_t)tid < bend - bstop, means2d, conic_opacity, rgb);
+  }
+  while (bend > bstop) {
+    const uint32_t bbeg = bend - min(256u, bend - bstop);
+    __syncthreads();
+    const float3 cn = conic_of(rec.co);
+    const uint32_t rows = rec.valid ? splat_rows_single(rec.m.x, rec.m.y, cn.x, cn.y, cn.z,
+                                                        rec.co.w, k.alpha_min, box, 4 * quarter)
+                                    : 0u;
+    const bool keep = rows != 0u;
+    int pos, wcnt;
+    const int cnt = compact_rows(keep, rows, s_wcnt, s_idx, pos, wcnt);
+    if (keep) {
+      const Splat sp = make_splat(rec.m, rec.co);
+      s_ga[pos] = make_float4(sp.u, sp.v, sp.qa, sp.qb);
+      s_gb[pos] = make_float4(sp.qc, sp.o, rec.r, rec.g);
+      s_gc[pos] = make_float4(cn.x, cn.y, cn.z, rec.b);
+      s_pos[pos] = (int)(bend - 1 - tid - start);
+      s_g[pos] = rec.gid;
+#pragma unroll
+      for (int q = 0; q < 9; ++q) s_acc[9 * pos + q] = 0.0f;
+    }
+    __syncthreads();
+    {
+      const uint32_t b2 = bbeg - min(256u, bbeg - bstop);
+      const uint32_t gid_after = values[(uint32_t)tid < b2 - bstop ? b2 - 1 - tid : bstop];
+      rec = gather_rec(gid_next, (uint32_t)tid < bbeg - bstop, means2d, conic_opacity, rgb);
+      gid_next = gid_after;
+    }
+    // slots past the end of the wave's list hold stale bytes: they still index
+    // the staged arrays, and their lanes take part in nothing below
+    const uint8_t* my_idx = s_idx[tid >> 6];
+    for (int j0 = 0; j0 < wcnt; j0 += 4) {
+      const bool valid = j0 + e < wcnt;
+      const int j = my_idx[j0 + e];
+      const float4 ga = s_ga[j], gb = s_gb[j];
+      const float cb = s_gc[j].w;
+      const uint32_t kk = (uint32_t)s_pos[j];
+      if (!__ballot(valid && kk < wml)) continue;  // wave-uniform
+      const float dx = fx - ga.x, dy = fy - ga.y;
+      const AlphaEval ae = eval_alpha(dx, dy, ga.z, ga.w, gb.x, gb.y, k.alpha_min, k.alpha_max);
+      const bool contrib = valid && kk < lastp && !ae.skip;
+      if (!__ballot(contrib)) continue;  // wave-uniform
+      const float a = contrib ? (ae.clamped ? k.alpha_max : ae.raw) : 0.0f;
+      const float iom = __builtin_amdgcn_rcpf(1.0f - a);  // 1 - a >= 1 - alpha_max > 0
+      // transmittance before each entry: T times the inclusive prefix product
+      // of 1 / (1 - alpha) over the step's entries, back to front
+      const Swapped p1 = swap_bit4(iom);
+      const float t1 = p1.first * p1.second;
+      const float in1 = odd ? t1 : iom;
+      const Swapped p2 = swap_bit5(t1);
+      const float Tk = T * (high ? in1 * p2.first : in1);
+      const float ptot = p2.first * p2.second;
+      const float CG = gb.z * gcr + gb.w * gcg + cb * gcb;
+      const float wgt = a * Tk;
+      // colour blended behind each entry within the step: exclusive prefix sum
+      const float c0 = contrib ? wgt * CG : 0.0f;
+      const Swapped s1 = swap_bit4(c0);
+      const float u1 = s1.first + s1.second;
+      const float ex1 = odd ? s1.first : 0.0f;
+      const Swapped s2 = swap_bit5(u1);
+      const float behind = S + (high ? ex1 + s2.first : ex1);
+      const float stot = s2.first + s2.second;
+      const float dLda = Tk * CG - iom * (behind + TgT);
+      T *= ptot;
+      S += stot;
+      const float dm = (contrib && !ae.clamped) ? dLda : 0.0f;
+      const float gp = a * dm;
+      const float q = gp * dx, r = gp * dy;
+      float gr[9];
+      gr[0] = q;
+      gr[1] = r;
+      gr[2] = q * dx;
+      gr[3] = q * dy;
+      gr[4] = r * dy;
+      gr[5] = ae.e * dm;
+      gr[6] = wgt * gcr;
+      gr[7] = wgt * gcg;
+      gr[8] = wgt * gcb;
+      float v8;
+      const float m = row_sum9(gr, col, v8);
+      float out = col == 1 ? v8 : m;
+      asm volatile("" : "+v"(out));  // the last folds stay outside the branch (DPP add)
+      if (adder && valid) atomicAdd(&s_acc[9 * j + slot], out);
+    }
+    __syncthreads();
+    if (tid < cnt) {
+      const float4 co = s_gc[tid];
+      float g[9];
+#pragma unroll
+      for (int q = 0; q < 9; ++q) g[q] = s_acc[9 * tid + q];
+      const float mx = g[0], my = g[1];
+      g[0] = co.x * mx + co.y * my;
+      g[1] = co.y * mx + co.z * my;
+      g[2] = -0.5f * g[2];
+      g[3] = -g[3];
+      g[4] = -0.5f * g[4];
+      float* dst = g2d + s_g[tid];
+#pragma unroll
+      for (int q = 0; q < 9; ++q)
+        if (g[q] != 0.0f) atomicAdd(dst + q * gs, g[q]);
+    }
+    bend = bbeg;
+  }
+}
+
 }  // namespace
 
 static_assert(kQueueStride * kQueues == 64 * 8, "queue block of bwd_workspace_bytes");
@@ -395,11 +619,18 @@ int32_t launch_render_bwd_pixels(const abcd_camera& cam, const abcd_raster_param
   const int64_t g2d_count = 9 * g2d_stride(n);
   if (!split.ckpt && k.ntiles <= kDirectTiles) {
     TRY_STATUS(launch_zero(g2d, g2d_count, stream));
-    ABCD_LAUNCH("render_bwd", render_bwd_direct_kernel, k.ntiles, kBlock, 0, stream, k,
-                tile_ranges, values_sorted, reinterpret_cast<const float2*>(means2d),
-                reinterpret_cast<const float4*>(conic_opacity), rgb,
-                reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B), final_T,
-                last, reinterpret_cast<const float4*>(dL_dout), g2d, g2d_stride(n));
+    if (k.ntiles <= kRowsTiles)
+      ABCD_LAUNCH("render_bwd", render_bwd_rows_kernel, 4 * k.ntiles, kBlock, 0, stream, k,
+                  tile_ranges, values_sorted, reinterpret_cast<const float2*>(means2d),
+                  reinterpret_cast<const float4*>(conic_opacity), rgb,
+                  reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B), final_T,
+                  last, reinterpret_cast<const float4*>(dL_dout), g2d, g2d_stride(n));
+    else
+      ABCD_LAUNCH("render_bwd", render_bwd_direct_kernel, k.ntiles, kBlock, 0, stream, k,
+                  tile_ranges, values_sorted, reinterpret_cast<const float2*>(means2d),
+                  reinterpret_cast<const float4*>(conic_opacity), rgb,
+                  reinterpret_cast<const float4*>(F), reinterpret_cast<const float4*>(B), final_T,
+                  last, reinterpret_cast<const float4*>(dL_dout), g2d, g2d_stride(n));
     ABCD_HIP(hipGetLastError());
     return ABCD_OK;
   }
