@@ -185,6 +185,29 @@ __device__ __forceinline__ int compact_rows(bool keep, uint32_t rows, int (*s_cn
   return __builtin_amdgcn_readfirstlane(tot);
 }
 
+// Frames of at most this many tiles (without a split) take the forward and
+// backward kernels that give each tile four workgroups, one pixel row per
+// wave and four list entries per step of a wave.
+constexpr int kRowsTiles = 256;
+
+// Lane-bit-4 and lane-bit-5 exchanges. v_permlane16_swap of (x, x) leaves
+// rows (0, 0, 2, 2) of x in its first result and rows (1, 1, 3, 3) in its
+// second; v_permlane32_swap of (x, x) leaves halves (low, low) and (high,
+// high). Either way the two results combined give the pair's total with the
+// same operands in the same order on both partners, and a lane with the
+// exchanged bit set finds its partner's value in the first result.
+struct Swapped {
+  float first, second;
+};
+__device__ __forceinline__ Swapped swap_bit4(float x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_int(x), __float_as_int(x), false, false);
+  return Swapped{__int_as_float(p[0]), __int_as_float(p[1])};
+}
+__device__ __forceinline__ Swapped swap_bit5(float x) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(x), __float_as_int(x), false, false);
+  return Swapped{__int_as_float(p[0]), __int_as_float(p[1])};
+}
+
 constexpr int kGroup = 8;
 constexpr int kBwdGroup = 4;  // the backward's group (register budget: 5 waves per SIMD)
 

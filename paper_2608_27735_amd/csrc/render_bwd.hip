@@ -355,24 +355,6 @@ __global__ __launch_bounds__(256) void render_bwd_direct_kernel(
            last, dL_dout, g2d, gs, SplitLayout{});
 }
 
-// Lane-bit-4 and lane-bit-5 exchanges. v_permlane16_swap of (x, x) leaves
-// rows (0, 0, 2, 2) of x in its first result and rows (1, 1, 3, 3) in its
-// second; v_permlane32_swap of (x, x) leaves halves (low, low) and (high,
-// high). Either way the two results combined give the pair's total with the
-// same operands in the same order on both partners, and a lane with the
-// exchanged bit set finds its partner's value in the first result.
-struct Swapped {
-  float first, second;
-};
-__device__ __forceinline__ Swapped swap_bit4(float x) {
-  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_int(x), __float_as_int(x), false, false);
-  return Swapped{__int_as_float(p[0]), __int_as_float(p[1])};
-}
-__device__ __forceinline__ Swapped swap_bit5(float x) {
-  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(x), __float_as_int(x), false, false);
-  return Swapped{__int_as_float(p[0]), __int_as_float(p[1])};
-}
-
 // Sums of nine values over each 16-lane row, by a butterfly over lane bits 3
 // (row rotate 8), 2 (half-row mirror, which pairs lanes whose bit 2 differs),
 // 1 and 0 (quad permutes): each step halves values 0-7 with one select pair
@@ -410,7 +392,6 @@ __device__ __forceinline__ int rowsum9_slot(int c) {
 // of 1 / (1 - alpha), and the colour blended behind it a prefix sum S of
 // alpha T (c . g), not normalised by the transmittance, so that the
 // alpha-derivative is T (c . g) - (S + T_final g_T) / (1 - alpha).
-constexpr int kRowsTiles = 256;
 
 __global__ __launch_bounds__(256) void render_bwd_rows_kernel(
     BlendConsts k, const uint32_t* __restrict__ tile_ranges, const uint32_t* __restrict__ values,

@@ -25,6 +25,9 @@ pytestmark = pytest.mark.gpu
 FWD_TOL = 1e-5
 GRAD_TOL = 1e-4
 KNIFE = 1e-4
+# frames of at most this many tiles render, when not split, with four
+# workgroups per tile (one pixel row per wave, four list entries per step)
+ROWS_TILES = 256
 
 
 @pytest.fixture(scope="module")
@@ -463,8 +466,16 @@ def test_split_backward(api, case, chunk, n_slots):
     g0 = api.render_bwd(cam, prm, params, p, bins, fw0, Gd, F=Fd, B=Bd)
     gs = api.render_bwd(cam, prm, params, p, bins, fw, Gd, F=Fd, B=Bd, split=split)
     torch.cuda.synchronize()
-    for key in ("out", "final_T", "last"):
-        assert torch.equal(fw[key], fw0[key])
+    if api.n_tiles(cam.width, cam.height) > ROWS_TILES:
+        for key in ("out", "final_T", "last"):
+            assert torch.equal(fw[key], fw0[key])
+    else:
+        # the unsplit forward of a small frame takes the four-workgroups-per-
+        # tile kernel: the same walk, rounded in another order
+        ok = ~ref0["fwd"]["knife"]
+        assert np.array_equal(np32(fw["last"])[ok], np32(fw0["last"])[ok])
+        assert (fw["out"] - fw0["out"]).abs().max().item() <= FWD_TOL
+        assert (fw["final_T"] - fw0["final_T"]).abs().max().item() <= FWD_TOL
     lens = np32(bins["tile_ranges"]).view(np.uint32).astype(np.int64)
     print(f"  tiles longer than a chunk: {int(((lens[:, 1] - lens[:, 0]) > chunk).sum())}")
     for k in ("means", "log_scales", "quats", "opacity_logits", "sh"):
