@@ -57,6 +57,7 @@ constexpr int kL1Items = 8;                 // level 1: depth ranks per lane
 constexpr int kRanksPerWave = 64 * kL1Items;
 constexpr int kChunk = 4 * kRanksPerWave;   // level 1: depth ranks per workgroup
 constexpr int kSub = 256;                   // level 2: bucket entries per sub-chunk
+constexpr int kSlice = 8;                   // level 2: sub-chunks per slice (one wave's count)
 constexpr int kBlk = 8;                     // block side in tiles
 constexpr int kBlkTiles = kBlk * kBlk;
 constexpr int kStrideGrid = 2048;           // workgroups of the grid-stride level-2 kernels
@@ -70,7 +71,8 @@ struct WsHeader {
   uint32_t ticket[4];     // partitions taken by each radix pass
   uint32_t ticket_l1;     // chunks taken by l1_place
   uint32_t done_l2;       // workgroups of l2_scan that have finished
-  uint32_t pad[52];
+  uint32_t total_slices;  // level-2 slices
+  uint32_t pad[51];
 };
 static_assert(sizeof(WsHeader) == 256, "header is one 256-byte slot");
 
@@ -92,8 +94,8 @@ inline Geo geo_of(int width, int height) {
 
 struct WsLayout {
   size_t hdr, ghist, mcopy, bcopy, lb1, st0, st1, keys_a, keys_b, vals_a, vals_b, rects, blk_off,
-      sub_off, pairs, c2, tile_total, tile_off, total;
-  int64_t rs_parts, chunks, max_sub;
+      sub_off, slice_off, pairs, c2, slice_tot, tile_total, tile_off, total;
+  int64_t rs_parts, chunks, max_sub, max_slices;
 };
 
 WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
@@ -102,6 +104,7 @@ WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
   L.rs_parts = (n + kRsTile - 1) / kRsTile;
   L.chunks = (n + kChunk - 1) / kChunk;
   L.max_sub = (capacity + kSub - 1) / kSub + g.nblk;
+  L.max_slices = L.max_sub / kSlice + g.nblk + 1;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t at = off;
@@ -124,8 +127,10 @@ WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
   L.rects = take(sizeof(unsigned long long) * n);
   L.blk_off = take(sizeof(uint32_t) * (g.nblk + 1));
   L.sub_off = take(sizeof(uint32_t) * (g.nblk + 1));
+  L.slice_off = take(sizeof(uint32_t) * (g.nblk + 1));
   L.pairs = take(sizeof(unsigned long long) * (size_t)capacity);  // m1 <= m <= capacity
   L.c2 = take(sizeof(uint32_t) * (size_t)L.max_sub * kBlkTiles);
+  L.slice_tot = take(sizeof(uint32_t) * (size_t)L.max_slices * kBlkTiles);
   L.tile_total = take(sizeof(uint32_t) * ntiles);
   L.tile_off = take(sizeof(uint32_t) * ntiles);
   L.total = off;
@@ -540,12 +545,17 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
 // decision come from the block totals and intersection count depth_keys
 // added up; every workgroup derives them (chunk 0 also writes them out). On
 // overflow nothing is placed. Dynamic LDS: 5 x geo.nblk words.
+// Level-2 slices of a bucket of v entries: groups of kSlice sub-chunks.
+__device__ __forceinline__ uint32_t slices_of(uint32_t v) {
+  return ((v + kSub - 1) / kSub + kSlice - 1) / kSlice;
+}
+
 __global__ __launch_bounds__(256) void l1_place_kernel(
     int64_t n, const uint32_t* __restrict__ order, const unsigned long long* __restrict__ rects,
     Geo geo, const uint32_t* __restrict__ bcopy, const unsigned long long* __restrict__ mcopy,
     unsigned long long capacity, int64_t chunks, uint32_t* __restrict__ lb,
-    uint32_t* __restrict__ blk_off, uint32_t* __restrict__ sub_off, WsHeader* __restrict__ hdr,
-    unsigned long long* __restrict__ pairs) {
+    uint32_t* __restrict__ blk_off, uint32_t* __restrict__ sub_off, uint32_t* __restrict__ slice_off,
+    WsHeader* __restrict__ hdr, unsigned long long* __restrict__ pairs) {
   using SW = StateWord<uint32_t>;
   extern __shared__ uint32_t lds[];
   uint32_t* slot = lds;                    // [4][nblk]: per wave counts, then next free slots
@@ -565,7 +575,7 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
   // sub-chunks; thread tid takes the contiguous blocks [b0, b1)
   const int per = (nblk + kBlock - 1) / kBlock;
   const int b0 = min(nblk, per * tid), b1 = min(nblk, b0 + per);
-  uint32_t tot = 0, stot = 0;
+  uint32_t tot = 0, stot = 0, ltot = 0;
   for (int b = b0; b < b1; ++b) {
     uint32_t c[kHistCopies];
 #pragma unroll
@@ -576,10 +586,12 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
     boff[b] = v;
     tot += v;
     stot += (v + kSub - 1) / kSub;
+    ltot += slices_of(v);
   }
   uint32_t run = scan_256(tot, s4);  // its barriers publish s_chunk, s_m and the cleared slots
   uint32_t srun = scan_256(stot, s4);
   const int64_t chunk = s_chunk;
+  uint32_t lrun = chunk == 0 ? scan_256(ltot, s4) : 0u;  // uniform: only chunk 0 writes them
   const unsigned long long m = s_m;
   const bool over = m > capacity || m >= (1ull << 32);
   for (int b = b0; b < b1; ++b) {
@@ -588,6 +600,8 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
     if (chunk == 0) {
       blk_off[b] = run;
       sub_off[b] = srun;
+      slice_off[b] = lrun;
+      lrun += slices_of(v);
     }
     run += v;
     srun += (v + kSub - 1) / kSub;
@@ -595,10 +609,12 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
   if (chunk == 0 && tid == kBlock - 1) {  // the last range ends at the totals
     blk_off[nblk] = run;
     sub_off[nblk] = srun;
+    slice_off[nblk] = lrun;
     hdr->m = m;
     hdr->m1 = run;
     hdr->overflow = over ? 1u : 0u;
     hdr->total_sub = over ? 0u : srun;
+    hdr->total_slices = over ? 0u : lrun;
   }
   if (over) return;  // the same decision in every workgroup: nobody waits
   uint32_t* my = slot + w * nblk;
@@ -691,36 +707,47 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
 // ------------------------------------------------------------- level 2
 //
 // A block has 8 x 8 = 64 tiles (local tile l at x = l % 8, y = l / 8). Each
-// bucket is cut into sub-chunks of kSub consecutive entries; per sub-chunk,
-// l2_count counts each tile's entries, l2_scan turns the counts into each
-// sub-chunk's first slot in every tile list, and l2_scatter writes the
-// entries.
+// bucket is cut into sub-chunks of kSub consecutive entries, and its
+// sub-chunks into slices of kSlice. One wave per slice (l2_count) counts each
+// tile's entries per sub-chunk and keeps their running sum over the slice:
+// each sub-chunk's first slot in every tile list relative to its slice, and
+// the slice's totals. l2_scan turns each block's slice totals into the
+// slices' first slots (a block at the frame's centre can hold thousands of
+// sub-chunks, and its scan runs on one workgroup: over slices it reads
+// kSlice times fewer rows), and l2_scatter writes the entries.
 
 struct SubChunk {
-  int bx, by;        // block
+  int bx, by, blk;   // block
   uint32_t e0, e1;   // entries [e0, e1) of the pair array
 };
 
-// Block of sub-chunk s: the last b with sub_off[b] <= s (sub_off is
-// nondecreasing). A wave finds it at once: lane b tests block b, 64 blocks per
-// round (coalesced loads instead of a binary search's chain of dependent
-// ones), and the highest block that passes wins.
-__device__ __forceinline__ SubChunk sub_chunk_wave(uint32_t s, const uint32_t* __restrict__ sub_off,
-                                                   const uint32_t* __restrict__ blk_off,
-                                                   const Geo& geo) {
+// The last b with off[b] <= x (off is nondecreasing over the blocks). A wave
+// finds it at once: lane b tests block b, 64 blocks per round (coalesced
+// loads instead of a binary search's chain of dependent ones), and the
+// highest block that passes wins.
+__device__ __forceinline__ int block_of_wave(uint32_t x, const uint32_t* __restrict__ off,
+                                             int nblk) {
   const int lane = threadIdx.x & 63;
   int lo = 0;
-  for (int b0 = 0; b0 < geo.nblk; b0 += 64) {
+  for (int b0 = 0; b0 < nblk; b0 += 64) {
     const int b = b0 + lane;
-    const uint64_t ok = __ballot(b < geo.nblk && sub_off[b] <= s);
+    const uint64_t ok = __ballot(b < nblk && off[b] <= x);
     if (ok) lo = b0 + 63 - __clzll(ok);
   }
-  lo = __builtin_amdgcn_readfirstlane(lo);
+  return __builtin_amdgcn_readfirstlane(lo);
+}
+
+// Sub-chunk s of block b.
+__device__ __forceinline__ SubChunk sub_chunk_of(uint32_t s, int b,
+                                                 const uint32_t* __restrict__ sub_off,
+                                                 const uint32_t* __restrict__ blk_off,
+                                                 const Geo& geo) {
   SubChunk c;
-  c.bx = lo % geo.nbx;
-  c.by = lo / geo.nbx;
-  c.e0 = blk_off[lo] + (s - sub_off[lo]) * kSub;
-  c.e1 = min(c.e0 + (uint32_t)kSub, blk_off[lo + 1]);
+  c.blk = b;
+  c.bx = b % geo.nbx;
+  c.by = b / geo.nbx;
+  c.e0 = blk_off[b] + (s - sub_off[b]) * kSub;
+  c.e1 = min(c.e0 + (uint32_t)kSub, blk_off[b + 1]);
   return c;
 }
 
@@ -764,38 +791,58 @@ __device__ __forceinline__ void load_entry(const unsigned long long* __restrict_
   }
 }
 
-// One wave per sub-chunk (grid stride): c2[s][tile] = entries covering the tile.
+// One wave per slice (grid stride): for each sub-chunk s of the slice,
+// c2[s][tile] = entries of the slice's earlier sub-chunks covering the tile,
+// and slice_tot[slice][tile] = all of the slice's. The slice's entries are
+// loaded at once, kSlice sub-chunks of 256 (4 per lane each).
 __global__ __launch_bounds__(64) void l2_count_kernel(
     const unsigned long long* __restrict__ pairs, Geo geo, const uint32_t* __restrict__ sub_off,
-    const uint32_t* __restrict__ blk_off, const WsHeader* __restrict__ hdr,
-    uint32_t* __restrict__ c2) {
+    const uint32_t* __restrict__ slice_off, const uint32_t* __restrict__ blk_off,
+    const WsHeader* __restrict__ hdr, uint32_t* __restrict__ c2,
+    uint32_t* __restrict__ slice_tot) {
+  static_assert(kSub == 4 * 64, "a sub-chunk is four entries per lane");
   __shared__ uint32_t d[kBlkTiles];
-  const uint32_t total = hdr->total_sub;
+  const uint32_t total = hdr->total_slices;
   const int lane = threadIdx.x;
-  for (uint32_t s = blockIdx.x; s < total; s += gridDim.x) {
-    const SubChunk sc = sub_chunk_wave(s, sub_off, blk_off, geo);
-    int pk[4];
+  for (uint32_t sl = blockIdx.x; sl < total; sl += gridDim.x) {
+    const int b = block_of_wave(sl, slice_off, geo.nblk);
+    const uint32_t s0 = sub_off[b] + (sl - slice_off[b]) * kSlice;
+    const uint32_t ns = min((uint32_t)kSlice, sub_off[b + 1] - s0);  // uniform, >= 1
+    const uint32_t e0 = blk_off[b] + (s0 - sub_off[b]) * kSub, e1 = blk_off[b + 1];
+    int pk[kSlice][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      uint32_t g;
-      load_entry(pairs, sc.e0 + lane + 64 * j, sc.e1, g, pk[j]);
+    for (int k = 0; k < kSlice; ++k)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        uint32_t g;
+        load_entry(pairs, e0 + k * kSub + lane + 64 * j, e1, g, pk[k][j]);
+      }
+    uint32_t run = 0;
+#pragma unroll
+    for (int k = 0; k < kSlice; ++k) {
+      if ((uint32_t)k >= ns) break;  // uniform
+      d[lane] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < 4; ++j) diff_add(d, pk[k][j]);
+      __syncthreads();
+      const uint32_t cnt = diff_prefix(d[lane], lane);
+      c2[(int64_t)(s0 + k) * kBlkTiles + lane] = run;
+      run += cnt;
+      __syncthreads();
     }
-    d[lane] = 0;
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < 4; ++j) diff_add(d, pk[j]);
-    __syncthreads();
-    c2[(int64_t)s * kBlkTiles + lane] = diff_prefix(d[lane], lane);
-    __syncthreads();
+    slice_tot[(int64_t)sl * kBlkTiles + lane] = run;
   }
 }
 
 // Exclusive scan over tiles -> tile_off and tile_ranges, by one workgroup of
 // kScanThreads (on overflow every tile total is 0, so the ranges written
 // are all empty and the blend kernels render nothing).
+// s_key (workgroup memory, may be NULL): also each tile's schedule bucket,
+// from the same loads.
 __device__ __forceinline__ void scan_tiles(const uint32_t* __restrict__ tile_total, int ntiles,
                                            uint32_t* __restrict__ tile_off,
-                                           uint32_t* __restrict__ tile_ranges) {
+                                           uint32_t* __restrict__ tile_ranges, uint8_t* s_key) {
   // thread t takes the contiguous tiles [lo, hi), all loads in flight at
   // once; the sums fit 32 bits (M < 2^32 unless overflowing, and then every
   // total is 0)
@@ -810,6 +857,11 @@ __device__ __forceinline__ void scan_tiles(const uint32_t* __restrict__ tile_tot
   for (int k = 0; k < kMaxPer; ++k) {
     v[k] = lo + k < hi ? tile_total[lo + k] : 0u;
     s += v[k];
+  }
+  if (s_key) {
+#pragma unroll
+    for (int k = 0; k < kMaxPer; ++k)
+      if (lo + k < hi) s_key[lo + k] = (uint8_t)bucket_of(v[k]);
   }
   uint32_t incl = s;  // inclusive prefix over the wave
 #pragma unroll
@@ -833,40 +885,44 @@ __device__ __forceinline__ void scan_tiles(const uint32_t* __restrict__ tile_tot
   }
 }
 
-// Per block: exclusive prefix of its sub-chunks' tile counts (lane = local
-// tile, the 16 waves split the sub-chunks) and the tile totals. The last
+// Per block: exclusive prefix of its slices' tile totals (lane = local tile,
+// the 16 waves split the slices) and the tile totals. The last
 // workgroup then scans the tile totals into tile_off and tile_ranges and,
 // when tile_order is given, orders the tiles for the forward (heaviest lists
 // first; on overflow every total is 0, which gives the identity order).
+constexpr int kScanRows = 32;
+
 __global__ __launch_bounds__(1024) void l2_scan_kernel(
-    uint32_t* __restrict__ c2, Geo geo, const uint32_t* __restrict__ sub_off,
+    uint32_t* __restrict__ c2, Geo geo, const uint32_t* __restrict__ slice_off,
     WsHeader* __restrict__ hdr, uint32_t* __restrict__ tile_total, uint32_t* __restrict__ tile_off,
     uint32_t* __restrict__ tile_ranges, uint32_t* __restrict__ tile_order) {
   __shared__ uint32_t part[16][64];
   const int b = blockIdx.x, lt = threadIdx.x & 63, w = threadIdx.x >> 6;
   const bool live = !hdr->overflow;
-  const uint32_t s0 = live ? sub_off[b] : 0u, s1 = live ? sub_off[b + 1] : 0u;
+  const uint32_t s0 = live ? slice_off[b] : 0u, s1 = live ? slice_off[b + 1] : 0u;
   const uint32_t per = (s1 - s0 + 15) / 16;
   const uint32_t q0 = min(s1, s0 + per * w), q1 = min(s1, q0 + per);
-  // rows are read eight at a time so that eight loads are in flight
+  // rows are read kScanRows at a time so that as many loads are in flight
   uint32_t sum = 0;
-  for (uint32_t q = q0; q < q1; q += 8) {
-    uint32_t v[8];
+  for (uint32_t q = q0; q < q1; q += kScanRows) {
+    uint32_t v[kScanRows];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? c2[(int64_t)(q + u) * kBlkTiles + lt] : 0u;
+    for (int u = 0; u < kScanRows; ++u)
+      v[u] = q + u < q1 ? c2[(int64_t)(q + u) * kBlkTiles + lt] : 0u;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) sum += v[u];
+    for (int u = 0; u < kScanRows; ++u) sum += v[u];
   }
   part[w][lt] = sum;
   __syncthreads();
   uint32_t run = 0;
   for (int k = 0; k < w; ++k) run += part[k][lt];
-  for (uint32_t q = q0; q < q1; q += 8) {
-    uint32_t v[8];
+  for (uint32_t q = q0; q < q1; q += kScanRows) {
+    uint32_t v[kScanRows];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = q + u < q1 ? c2[(int64_t)(q + u) * kBlkTiles + lt] : 0u;
+    for (int u = 0; u < kScanRows; ++u)
+      v[u] = q + u < q1 ? c2[(int64_t)(q + u) * kBlkTiles + lt] : 0u;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < kScanRows; ++u) {
       if (q + u < q1) c2[(int64_t)(q + u) * kBlkTiles + lt] = run;
       run += v[u];
     }
@@ -878,11 +934,11 @@ __global__ __launch_bounds__(1024) void l2_scan_kernel(
   }
   if (!last_workgroup(&hdr->done_l2)) return;
   const int ntiles = geo.ntx * geo.nty;
-  scan_tiles(tile_total, ntiles, tile_off, tile_ranges);
+  __shared__ uint8_t s_key[ABCD_MAX_TILES];
+  scan_tiles(tile_total, ntiles, tile_off, tile_ranges, tile_order ? s_key : nullptr);
   if (tile_order) {
-    __shared__ uint8_t s_key[ABCD_MAX_TILES];
     __syncthreads();
-    order_tiles(ntiles, tile_total, tile_order, s_key);
+    order_keyed(ntiles, s_key, tile_order, nullptr);
   }
 }
 
@@ -897,8 +953,9 @@ __global__ __launch_bounds__(1024) void l2_scan_kernel(
 // waves' entries in wave order (per-wave counts by 2D difference arrays).
 __global__ __launch_bounds__(256) void l2_scatter_kernel(
     const unsigned long long* __restrict__ pairs, const float* __restrict__ depth, Geo geo,
-    const uint32_t* __restrict__ sub_off, const uint32_t* __restrict__ blk_off,
-    const uint32_t* __restrict__ c2, const uint32_t* __restrict__ tile_off,
+    const uint32_t* __restrict__ sub_off, const uint32_t* __restrict__ slice_off,
+    const uint32_t* __restrict__ blk_off, const uint32_t* __restrict__ c2,
+    const uint32_t* __restrict__ slice_tot, const uint32_t* __restrict__ tile_off,
     const WsHeader* __restrict__ hdr, uint32_t* __restrict__ values_sorted,
     unsigned long long* __restrict__ keys_sorted) {
   __shared__ uint32_t wcnt[4][kBlkTiles];   // per wave: entries covering each tile
@@ -906,7 +963,7 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
   const uint32_t total = hdr->total_sub;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (uint32_t s = blockIdx.x; s < total; s += gridDim.x) {
-    const SubChunk sc = sub_chunk_wave(s, sub_off, blk_off, geo);
+    const SubChunk sc = sub_chunk_of(s, block_of_wave(s, sub_off, geo.nblk), sub_off, blk_off, geo);
     uint32_t g;
     int pk;
     load_entry(pairs, sc.e0 + threadIdx.x, sc.e1, g, pk);
@@ -915,8 +972,10 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
     uint32_t dst_l = 0u;
     {
       const int tx = sc.bx * kBlk + (lane & 7), ty = sc.by * kBlk + (lane >> 3);
+      const uint32_t sl = slice_off[sc.blk] + (s - sub_off[sc.blk]) / kSlice;
       if (tx < geo.ntx && ty < geo.nty)
-        dst_l = tile_off[ty * geo.ntx + tx] + c2[(int64_t)s * kBlkTiles + lane];
+        dst_l = tile_off[ty * geo.ntx + tx] + slice_tot[(int64_t)sl * kBlkTiles + lane] +
+                c2[(int64_t)s * kBlkTiles + lane];
     }
     const uint32_t key_lo = keys_sorted && pk != 0 ? __float_as_uint(depth[g]) : 0u;
     wdiff[w][lane] = 0;
@@ -1144,6 +1203,7 @@ __global__ __launch_bounds__(kSmallThreads) void bin_small_sort_kernel(
     hdr->m1 = 0;
     hdr->overflow = over ? 1u : 0u;
     hdr->total_sub = 0;
+    hdr->total_slices = 0;
   }
 }
 
@@ -1201,6 +1261,7 @@ __global__ void bin_empty_kernel(int ntiles, uint32_t* __restrict__ tile_ranges,
     hdr->m1 = 0;
     hdr->overflow = 0;
     hdr->total_sub = 0;
+    hdr->total_slices = 0;
   }
 }
 
@@ -1286,15 +1347,17 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   uint32_t* c2 = u32(L.c2);
   uint32_t* tile_total = u32(L.tile_total);
   uint32_t* tile_off = u32(L.tile_off);
+  uint32_t* slice_off = u32(L.slice_off);
+  uint32_t* slice_tot = u32(L.slice_tot);
   ABCD_LAUNCH("l1_place", l1_place_kernel, L.chunks, kBlock, 5 * sizeof(uint32_t) * geo.nblk,
               stream, n, order, rects, geo, bcopy, mcopy, cap, L.chunks, u32(L.lb1), blk_off,
-              sub_off, hdr, pairs);
+              sub_off, slice_off, hdr, pairs);
   ABCD_LAUNCH("l2_count", l2_count_kernel, 4 * kStrideGrid, 64, 0, stream, pairs, geo, sub_off,
-              blk_off, hdr, c2);
-  ABCD_LAUNCH("l2_scan", l2_scan_kernel, geo.nblk, 1024, 0, stream, c2, geo, sub_off, hdr,
+              slice_off, blk_off, hdr, c2, slice_tot);
+  ABCD_LAUNCH("l2_scan", l2_scan_kernel, geo.nblk, 1024, 0, stream, slice_tot, geo, slice_off, hdr,
               tile_total, tile_off, tile_ranges, tile_order);
   ABCD_LAUNCH("l2_scatter", l2_scatter_kernel, kScatterGrid, kBlock, 0, stream, pairs, depth, geo,
-              sub_off, blk_off, c2, tile_off, hdr, values_sorted,
+              sub_off, slice_off, blk_off, c2, slice_tot, tile_off, hdr, values_sorted,
               reinterpret_cast<unsigned long long*>(keys_sorted));
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
