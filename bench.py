@@ -39,11 +39,11 @@ HBM_PROFILE = "step_1m_1297x840_hbm_bytes.md"
 SQ_PROFILE = "step_1m_1297x840_sq_counters.md"
 
 KERNELS = ["composite", "project", "bin_zero", "depth_keys", "radix_pass", "l1_place", "l2_count",
-           "l2_scan", "l2_scatter", "bin_small_sort", "bin_small_collect", "render_fwd", "loss_l1",
+           "l2_scatter", "bin_small_sort", "bin_small_collect", "render_fwd", "loss_l1",
            "zero_fill", "bwd_order", "render_bwd", "project_bwd", "adam"]
 # the launches of abcd_bin_sort (general path, then the small-block path)
-BIN_KERNELS = ["bin_zero", "depth_keys", "radix_pass", "l1_place", "l2_count", "l2_scan",
-               "l2_scatter", "bin_small_sort", "bin_small_collect"]
+BIN_KERNELS = ["bin_zero", "depth_keys", "radix_pass", "l1_place", "l2_count", "l2_scatter",
+               "bin_small_sort", "bin_small_collect"]
 
 
 def parse():

@@ -28,13 +28,13 @@
 //                          intersection count M
 //   radix_pass x4          depth order of the n Gaussians
 //   l1_place               (block, Gaussian) pairs, bucket-major, depth order;
-//                          bucket offsets, sub-chunk table, overflow flag (on
-//                          overflow nothing is placed: every tile range comes
-//                          out empty)
-//   l2_count               per sub-chunk: counts of its block's 64 tiles
-//   l2_scan                exclusive prefix of the sub-chunk counts per tile;
-//                          its last workgroup: tile_ranges and the forward's
-//                          tile order
+//                          bucket offsets, sub-chunk and slice tables,
+//                          overflow flag (on overflow nothing is placed: every
+//                          tile range comes out empty)
+//   l2_count               per slice of 16 sub-chunks: counts of its block's
+//                          64 tiles per sub-chunk; per block (its last slice
+//                          counted): the slices' prefix and the tile totals;
+//                          last: tile_ranges and the forward's tile order
 //   l2_scatter             values (and keys), tile-major, depth order
 #include <algorithm>
 
@@ -57,10 +57,10 @@ constexpr int kL1Items = 8;                 // level 1: depth ranks per lane
 constexpr int kRanksPerWave = 64 * kL1Items;
 constexpr int kChunk = 4 * kRanksPerWave;   // level 1: depth ranks per workgroup
 constexpr int kSub = 256;                   // level 2: bucket entries per sub-chunk
-constexpr int kSlice = 8;                   // level 2: sub-chunks per slice (one wave's count)
+constexpr int kSlice = 16;                  // level 2: sub-chunks per slice (a wave each)
 constexpr int kBlk = 8;                     // block side in tiles
 constexpr int kBlkTiles = kBlk * kBlk;
-constexpr int kStrideGrid = 2048;           // workgroups of the grid-stride level-2 kernels
+constexpr int kCountGrid = 512;             // workgroups of the grid-stride level-2 count
 constexpr int kScatterGrid = 8192;          // workgroups of the grid-stride level-2 scatter
 
 struct WsHeader {
@@ -70,8 +70,8 @@ struct WsHeader {
   uint32_t total_sub;     // level-2 sub-chunks
   uint32_t ticket[4];     // partitions taken by each radix pass
   uint32_t ticket_l1;     // chunks taken by l1_place
-  uint32_t done_l2;       // workgroups of l2_scan that have finished
-  uint32_t total_slices;  // level-2 slices
+  uint32_t done_l2;       // blocks whose level-2 scan is done
+  uint32_t nonempty;      // blocks holding at least one entry
   uint32_t pad[51];
 };
 static_assert(sizeof(WsHeader) == 256, "header is one 256-byte slot");
@@ -93,7 +93,7 @@ inline Geo geo_of(int width, int height) {
 }
 
 struct WsLayout {
-  size_t hdr, ghist, mcopy, bcopy, lb1, st0, st1, keys_a, keys_b, vals_a, vals_b, rects, blk_off,
+  size_t hdr, ghist, mcopy, bcopy, blk_done, lb1, st0, st1, keys_a, keys_b, vals_a, vals_b, rects, blk_off,
       sub_off, slice_off, pairs, c2, slice_tot, tile_total, tile_off, total;
   int64_t rs_parts, chunks, max_sub, max_slices;
 };
@@ -104,7 +104,9 @@ WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
   L.rs_parts = (n + kRsTile - 1) / kRsTile;
   L.chunks = (n + kChunk - 1) / kChunk;
   L.max_sub = (capacity + kSub - 1) / kSub + g.nblk;
-  L.max_slices = L.max_sub / kSlice + g.nblk + 1;
+  // (group of kSlice sub-chunks, block) pairs: each block start splits at
+  // most one group
+  L.max_slices = L.max_sub / kSlice + g.nblk + 2;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t at = off;
@@ -117,6 +119,7 @@ WsLayout ws_layout(int64_t n, int64_t capacity, const Geo& g) {
   L.ghist = take(sizeof(uint32_t) * kHistCopies * 4 * 256);
   L.mcopy = take(sizeof(unsigned long long) * kHistCopies);
   L.bcopy = take(sizeof(uint32_t) * kHistCopies * g.nblk);
+  L.blk_done = take(sizeof(uint32_t) * g.nblk);
   L.lb1 = take(sizeof(uint32_t) * (size_t)L.chunks * g.nblk);
   L.st0 = take(sizeof(unsigned long long) * 256 * L.rs_parts);
   L.st1 = take(sizeof(unsigned long long) * 256 * L.rs_parts);
@@ -498,25 +501,17 @@ __device__ __forceinline__ int pack_local(const Rect& r) {
 
 // ------------------------------------------------------------- level 1
 
-// True in every thread of the last workgroup of the launch to get here (the
-// counter starts at 0). Global writes of any thread before the call are
-// visible to that workgroup's reads after it: every wave waits for its
-// stores to reach the L2 before the barrier, one thread then writes the L2
-// back (agent-scope release) before counting the workgroup in, and the last
-// workgroup's waves drop their cached lines (agent-scope acquire).
-__device__ __forceinline__ bool last_workgroup(uint32_t* counter) {
-  __shared__ uint32_t s_last;
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    __builtin_amdgcn_s_waitcnt(0);  // the write-back has completed
-    s_last = atomicAdd(counter, 1u) == gridDim.x - 1 ? 1u : 0u;
-  }
-  __syncthreads();
-  const bool last = s_last != 0u;
-  if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  return last;
+// Agent-scope relaxed atomic loads and stores of 32-bit words: they reach the
+// memory side, past every XCD's L2, so words handed from one workgroup to
+// another through them need no cache write-back or invalidation. The writer's
+// waves wait for their stores to complete before a barrier, after which one
+// thread counts the workgroup in with an agent-scope atomic; the workgroup
+// whose count completes a total then reads the words.
+__device__ __forceinline__ void store_agent(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t load_agent(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 constexpr uint32_t kNoBlock = 0xffffffffu;
@@ -545,9 +540,11 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
 // decision come from the block totals and intersection count depth_keys
 // added up; every workgroup derives them (chunk 0 also writes them out). On
 // overflow nothing is placed. Dynamic LDS: 5 x geo.nblk words.
-// Level-2 slices of a bucket of v entries: groups of kSlice sub-chunks.
-__device__ __forceinline__ uint32_t slices_of(uint32_t v) {
-  return ((v + kSub - 1) / kSub + kSlice - 1) / kSlice;
+// Level-2 slices of a block whose sub-chunks are [s0, s1): its parts of the
+// aligned groups of kSlice consecutive sub-chunks (one l2_count workgroup
+// each).
+__device__ __forceinline__ uint32_t slices_of(uint32_t s0, uint32_t s1) {
+  return s1 > s0 ? (s1 - 1) / kSlice - s0 / kSlice + 1 : 0u;
 }
 
 __global__ __launch_bounds__(256) void l1_place_kernel(
@@ -555,7 +552,8 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
     Geo geo, const uint32_t* __restrict__ bcopy, const unsigned long long* __restrict__ mcopy,
     unsigned long long capacity, int64_t chunks, uint32_t* __restrict__ lb,
     uint32_t* __restrict__ blk_off, uint32_t* __restrict__ sub_off, uint32_t* __restrict__ slice_off,
-    WsHeader* __restrict__ hdr, unsigned long long* __restrict__ pairs) {
+    WsHeader* __restrict__ hdr, unsigned long long* __restrict__ pairs,
+    uint32_t* __restrict__ tile_total) {
   using SW = StateWord<uint32_t>;
   extern __shared__ uint32_t lds[];
   uint32_t* slot = lds;                    // [4][nblk]: per wave counts, then next free slots
@@ -575,7 +573,7 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
   // sub-chunks; thread tid takes the contiguous blocks [b0, b1)
   const int per = (nblk + kBlock - 1) / kBlock;
   const int b0 = min(nblk, per * tid), b1 = min(nblk, b0 + per);
-  uint32_t tot = 0, stot = 0, ltot = 0;
+  uint32_t tot = 0, stot = 0;
   for (int b = b0; b < b1; ++b) {
     uint32_t c[kHistCopies];
 #pragma unroll
@@ -586,14 +584,40 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
     boff[b] = v;
     tot += v;
     stot += (v + kSub - 1) / kSub;
-    ltot += slices_of(v);
   }
   uint32_t run = scan_256(tot, s4);  // its barriers publish s_chunk, s_m and the cleared slots
   uint32_t srun = scan_256(stot, s4);
   const int64_t chunk = s_chunk;
-  uint32_t lrun = chunk == 0 ? scan_256(ltot, s4) : 0u;  // uniform: only chunk 0 writes them
+  uint32_t lrun = 0;
+  if (chunk == 0) {  // uniform: only chunk 0 writes the slice table
+    uint32_t ltot = 0, sr = srun;
+    for (int b = b0; b < b1; ++b) {
+      const uint32_t ns = (boff[b] + kSub - 1) / kSub;
+      ltot += slices_of(sr, sr + ns);
+      sr += ns;
+    }
+    lrun = scan_256(ltot, s4);
+  }
   const unsigned long long m = s_m;
   const bool over = m > capacity || m >= (1ull << 32);
+  if (chunk == 0) {
+    // blocks without entries (every block on overflow): their tiles' totals
+    // are 0, and level 2 counts only the others
+    uint32_t ne = 0;
+    for (int b = b0; b < b1; ++b) {
+      if (boff[b] != 0u && !over) {
+        ++ne;
+        continue;
+      }
+      const int bx = b % geo.nbx, by = b / geo.nbx;
+      for (int t = 0; t < kBlkTiles; ++t) {
+        const int tx = bx * kBlk + (t & 7), ty = by * kBlk + (t >> 3);
+        if (tx < geo.ntx && ty < geo.nty) tile_total[ty * geo.ntx + tx] = 0u;
+      }
+    }
+    ne = wave_sum_u32(ne);
+    if (lane == 0 && ne) atomicAdd(&hdr->nonempty, ne);
+  }
   for (int b = b0; b < b1; ++b) {
     const uint32_t v = boff[b];
     boff[b] = run;
@@ -601,7 +625,7 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
       blk_off[b] = run;
       sub_off[b] = srun;
       slice_off[b] = lrun;
-      lrun += slices_of(v);
+      lrun += slices_of(srun, srun + (v + kSub - 1) / kSub);
     }
     run += v;
     srun += (v + kSub - 1) / kSub;
@@ -614,7 +638,6 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
     hdr->m1 = run;
     hdr->overflow = over ? 1u : 0u;
     hdr->total_sub = over ? 0u : srun;
-    hdr->total_slices = over ? 0u : lrun;
   }
   if (over) return;  // the same decision in every workgroup: nobody waits
   uint32_t* my = slot + w * nblk;
@@ -708,31 +731,40 @@ __global__ __launch_bounds__(256) void l1_place_kernel(
 //
 // A block has 8 x 8 = 64 tiles (local tile l at x = l % 8, y = l / 8). Each
 // bucket is cut into sub-chunks of kSub consecutive entries, and its
-// sub-chunks into slices of kSlice. One wave per slice (l2_count) counts each
-// tile's entries per sub-chunk and keeps their running sum over the slice:
-// each sub-chunk's first slot in every tile list relative to its slice, and
-// the slice's totals. l2_scan turns each block's slice totals into the
-// slices' first slots (a block at the frame's centre can hold thousands of
-// sub-chunks, and its scan runs on one workgroup: over slices it reads
-// kSlice times fewer rows), and l2_scatter writes the entries.
+// sub-chunks into slices of kSlice. l2_count counts each tile's entries per
+// sub-chunk and sums them over the slice: each sub-chunk's first slot in
+// every tile list relative to its slice, and the slice's totals; a block's
+// slice totals then become the slices' first slots (a block at the frame's
+// centre can hold thousands of sub-chunks, and its scan runs on one
+// workgroup: over slices it reads kSlice times fewer rows). l2_scatter writes
+// the entries.
 
 struct SubChunk {
   int bx, by, blk;   // block
   uint32_t e0, e1;   // entries [e0, e1) of the pair array
 };
 
-// The last b with off[b] <= x (off is nondecreasing over the blocks). A wave
-// finds it at once: lane b tests block b, 64 blocks per round (coalesced
-// loads instead of a binary search's chain of dependent ones), and the
-// highest block that passes wins.
+// The last b with off[b] <= x (off is nondecreasing over the blocks), with
+// off[b] and other[b]. A wave finds it at once: lane b tests block b, 64
+// blocks per round (coalesced loads instead of a binary search's chain of
+// dependent ones), and the highest block that passes wins; its two values
+// come from the same loads.
 __device__ __forceinline__ int block_of_wave(uint32_t x, const uint32_t* __restrict__ off,
-                                             int nblk) {
+                                              const uint32_t* __restrict__ other, int nblk,
+                                              uint32_t& off_b, uint32_t& other_b) {
   const int lane = threadIdx.x & 63;
   int lo = 0;
+  off_b = other_b = 0;
   for (int b0 = 0; b0 < nblk; b0 += 64) {
     const int b = b0 + lane;
-    const uint64_t ok = __ballot(b < nblk && off[b] <= x);
-    if (ok) lo = b0 + 63 - __clzll(ok);
+    const uint32_t o = b < nblk ? off[b] : 0u, t = b < nblk ? other[b] : 0u;
+    const uint64_t ok = __ballot(b < nblk && o <= x);
+    if (ok) {
+      const int hi = 63 - __clzll(ok);
+      lo = b0 + hi;
+      off_b = (uint32_t)__builtin_amdgcn_readlane((int)o, hi);
+      other_b = (uint32_t)__builtin_amdgcn_readlane((int)t, hi);
+    }
   }
   return __builtin_amdgcn_readfirstlane(lo);
 }
@@ -791,50 +823,6 @@ __device__ __forceinline__ void load_entry(const unsigned long long* __restrict_
   }
 }
 
-// One wave per slice (grid stride): for each sub-chunk s of the slice,
-// c2[s][tile] = entries of the slice's earlier sub-chunks covering the tile,
-// and slice_tot[slice][tile] = all of the slice's. The slice's entries are
-// loaded at once, kSlice sub-chunks of 256 (4 per lane each).
-__global__ __launch_bounds__(64) void l2_count_kernel(
-    const unsigned long long* __restrict__ pairs, Geo geo, const uint32_t* __restrict__ sub_off,
-    const uint32_t* __restrict__ slice_off, const uint32_t* __restrict__ blk_off,
-    const WsHeader* __restrict__ hdr, uint32_t* __restrict__ c2,
-    uint32_t* __restrict__ slice_tot) {
-  static_assert(kSub == 4 * 64, "a sub-chunk is four entries per lane");
-  __shared__ uint32_t d[kBlkTiles];
-  const uint32_t total = hdr->total_slices;
-  const int lane = threadIdx.x;
-  for (uint32_t sl = blockIdx.x; sl < total; sl += gridDim.x) {
-    const int b = block_of_wave(sl, slice_off, geo.nblk);
-    const uint32_t s0 = sub_off[b] + (sl - slice_off[b]) * kSlice;
-    const uint32_t ns = min((uint32_t)kSlice, sub_off[b + 1] - s0);  // uniform, >= 1
-    const uint32_t e0 = blk_off[b] + (s0 - sub_off[b]) * kSub, e1 = blk_off[b + 1];
-    int pk[kSlice][4];
-#pragma unroll
-    for (int k = 0; k < kSlice; ++k)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        uint32_t g;
-        load_entry(pairs, e0 + k * kSub + lane + 64 * j, e1, g, pk[k][j]);
-      }
-    uint32_t run = 0;
-#pragma unroll
-    for (int k = 0; k < kSlice; ++k) {
-      if ((uint32_t)k >= ns) break;  // uniform
-      d[lane] = 0;
-      __syncthreads();
-#pragma unroll
-      for (int j = 0; j < 4; ++j) diff_add(d, pk[k][j]);
-      __syncthreads();
-      const uint32_t cnt = diff_prefix(d[lane], lane);
-      c2[(int64_t)(s0 + k) * kBlkTiles + lane] = run;
-      run += cnt;
-      __syncthreads();
-    }
-    slice_tot[(int64_t)sl * kBlkTiles + lane] = run;
-  }
-}
-
 // Exclusive scan over tiles -> tile_off and tile_ranges, by one workgroup of
 // kScanThreads (on overflow every tile total is 0, so the ranges written
 // are all empty and the blend kernels render nothing).
@@ -843,98 +831,200 @@ __global__ __launch_bounds__(64) void l2_count_kernel(
 __device__ __forceinline__ void scan_tiles(const uint32_t* __restrict__ tile_total, int ntiles,
                                            uint32_t* __restrict__ tile_off,
                                            uint32_t* __restrict__ tile_ranges, uint8_t* s_key) {
-  // thread t takes the contiguous tiles [lo, hi), all loads in flight at
-  // once; the sums fit 32 bits (M < 2^32 unless overflowing, and then every
-  // total is 0)
-  constexpr int kMaxPer = (ABCD_MAX_TILES + kScanThreads - 1) / kScanThreads;
+  // rounds of kScanThreads * kPer tiles, thread t taking kPer contiguous
+  // tiles of each, all loads of a round in flight at once; the sums fit 32
+  // bits (M < 2^32 unless overflowing, and then every total is 0)
+  constexpr int kPer = 8;
   __shared__ uint32_t s_wave[kScanThreads / 64];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  const int per = (ntiles + kScanThreads - 1) / kScanThreads;
-  const int lo = min(ntiles, per * tid), hi = min(ntiles, lo + per);
-  uint32_t v[kMaxPer];
-  uint32_t s = 0;
+  uint32_t carry = 0;
+  for (int r0 = 0; r0 < ntiles; r0 += kScanThreads * kPer) {
+    const int lo = r0 + kPer * tid;
+    uint32_t v[kPer];
+    uint32_t s = 0;
 #pragma unroll
-  for (int k = 0; k < kMaxPer; ++k) {
-    v[k] = lo + k < hi ? tile_total[lo + k] : 0u;
-    s += v[k];
-  }
-  if (s_key) {
-#pragma unroll
-    for (int k = 0; k < kMaxPer; ++k)
-      if (lo + k < hi) s_key[lo + k] = (uint8_t)bucket_of(v[k]);
-  }
-  uint32_t incl = s;  // inclusive prefix over the wave
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t y = (uint32_t)__shfl_up((int)incl, d, 64);
-    if (lane >= d) incl += y;
-  }
-  if (lane == 63) s_wave[w] = incl;
-  __syncthreads();
-  uint32_t run = incl - s;
-#pragma unroll
-  for (int k = 0; k < kScanThreads / 64; ++k) run += k < w ? s_wave[k] : 0u;
-#pragma unroll
-  for (int k = 0; k < kMaxPer; ++k) {
-    if (lo + k < hi) {
-      tile_off[lo + k] = run;
-      tile_ranges[2 * (lo + k)] = run;
-      tile_ranges[2 * (lo + k) + 1] = run + v[k];
+    for (int k = 0; k < kPer; ++k) {
+      v[k] = lo + k < ntiles ? load_agent(&tile_total[lo + k]) : 0u;
+      s += v[k];
     }
-    run += v[k];
+    if (s_key) {
+#pragma unroll
+      for (int k = 0; k < kPer; ++k)
+        if (lo + k < ntiles) s_key[lo + k] = (uint8_t)bucket_of(v[k]);
+    }
+    uint32_t incl = s;  // inclusive prefix over the wave
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t y = (uint32_t)__shfl_up((int)incl, d, 64);
+      if (lane >= d) incl += y;
+    }
+    if (lane == 63) s_wave[w] = incl;
+    __syncthreads();
+    uint32_t run = carry + incl - s, all = 0;
+#pragma unroll
+    for (int k = 0; k < kScanThreads / 64; ++k) {
+      const uint32_t c = s_wave[k];
+      run += k < w ? c : 0u;
+      all += c;
+    }
+    __syncthreads();  // s_wave is rewritten by the next round
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      if (lo + k < ntiles) {
+        tile_off[lo + k] = run;
+        tile_ranges[2 * (lo + k)] = run;
+        tile_ranges[2 * (lo + k) + 1] = run + v[k];
+      }
+      run += v[k];
+    }
+    carry += all;
   }
 }
 
-// Per block: exclusive prefix of its slices' tile totals (lane = local tile,
-// the 16 waves split the slices) and the tile totals. The last
-// workgroup then scans the tile totals into tile_off and tile_ranges and,
-// when tile_order is given, orders the tiles for the forward (heaviest lists
-// first; on overflow every total is 0, which gives the identity order).
-constexpr int kScanRows = 32;
+// Level 2's counts and scans in one launch. Workgroup k (grid stride) takes
+// the sub-chunks [kSlice k, kSlice k + kSlice), wave w sub-chunk kSlice k + w,
+// and counts its entries per tile; the group holds one slice of each block
+// it meets. For each sub-chunk s, c2[s][tile] = entries of the earlier
+// sub-chunks of its slice covering the tile, and slice_tot[slice][tile] =
+// all of the slice's. The workgroup that completes a block's last slice turns
+// the block's slice totals into each slice's first slot relative to the
+// block (lane = local tile, the 16 waves split the slices, kScanRows rows in
+// flight per wave) and writes the block's tile totals; the one that completes
+// the last nonempty block scans the tile totals into tile_off and
+// tile_ranges and, when tile_order is given, orders the tiles for the
+// forward (heaviest lists first). With no sub-chunk at all (no entries, or
+// overflow: every tile total is 0, which gives empty ranges and the identity
+// order) the first workgroup does that directly. Slice totals and tile totals
+// pass between workgroups through store_agent and load_agent.
+constexpr int kScanRows = 4;
 
-__global__ __launch_bounds__(1024) void l2_scan_kernel(
-    uint32_t* __restrict__ c2, Geo geo, const uint32_t* __restrict__ slice_off,
-    WsHeader* __restrict__ hdr, uint32_t* __restrict__ tile_total, uint32_t* __restrict__ tile_off,
-    uint32_t* __restrict__ tile_ranges, uint32_t* __restrict__ tile_order) {
-  __shared__ uint32_t part[16][64];
-  const int b = blockIdx.x, lt = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const bool live = !hdr->overflow;
-  const uint32_t s0 = live ? slice_off[b] : 0u, s1 = live ? slice_off[b + 1] : 0u;
-  const uint32_t per = (s1 - s0 + 15) / 16;
-  const uint32_t q0 = min(s1, s0 + per * w), q1 = min(s1, q0 + per);
-  // rows are read kScanRows at a time so that as many loads are in flight
-  uint32_t sum = 0;
-  for (uint32_t q = q0; q < q1; q += kScanRows) {
-    uint32_t v[kScanRows];
-#pragma unroll
-    for (int u = 0; u < kScanRows; ++u)
-      v[u] = q + u < q1 ? c2[(int64_t)(q + u) * kBlkTiles + lt] : 0u;
-#pragma unroll
-    for (int u = 0; u < kScanRows; ++u) sum += v[u];
-  }
-  part[w][lt] = sum;
-  __syncthreads();
-  uint32_t run = 0;
-  for (int k = 0; k < w; ++k) run += part[k][lt];
-  for (uint32_t q = q0; q < q1; q += kScanRows) {
-    uint32_t v[kScanRows];
-#pragma unroll
-    for (int u = 0; u < kScanRows; ++u)
-      v[u] = q + u < q1 ? c2[(int64_t)(q + u) * kBlkTiles + lt] : 0u;
-#pragma unroll
-    for (int u = 0; u < kScanRows; ++u) {
-      if (q + u < q1) c2[(int64_t)(q + u) * kBlkTiles + lt] = run;
-      run += v[u];
-    }
-  }
-  if (w == 15) {
-    const int bx = b % geo.nbx, by = b / geo.nbx;
-    const int tx = bx * kBlk + (lt & 7), ty = by * kBlk + (lt >> 3);
-    if (tx < geo.ntx && ty < geo.nty) tile_total[ty * geo.ntx + tx] = run;
-  }
-  if (!last_workgroup(&hdr->done_l2)) return;
-  const int ntiles = geo.ntx * geo.nty;
+__global__ __launch_bounds__(64 * kSlice) __attribute__((amdgpu_waves_per_eu(8))) void l2_count_kernel(
+    const unsigned long long* __restrict__ pairs, Geo geo, const uint32_t* __restrict__ sub_off,
+    const uint32_t* __restrict__ slice_off, const uint32_t* __restrict__ blk_off,
+    WsHeader* __restrict__ hdr, uint32_t* __restrict__ c2, uint32_t* __restrict__ slice_tot,
+    uint32_t* __restrict__ blk_done, uint32_t* __restrict__ tile_total,
+    uint32_t* __restrict__ tile_off, uint32_t* __restrict__ tile_ranges,
+    uint32_t* __restrict__ tile_order) {
+  static_assert(kSub == 4 * 64, "a sub-chunk is four entries per lane");
+  static_assert(64 * kSlice == kScanThreads && kScanThreads == kOrderThreads,
+                "the tile scan and the tile order take the whole workgroup");
+  __shared__ uint32_t d[kSlice][kBlkTiles];
+  __shared__ int s_blk[kSlice];          // block of each wave's sub-chunk (-1: none)
+  __shared__ uint32_t s_nsl[kSlice];     // slices of that block
+  __shared__ uint32_t s_soff[kSlice];    // its first slice
+  __shared__ int s_done[kSlice + 1];     // blocks completed here, then their count
+  __shared__ uint32_t s_final;
   __shared__ uint8_t s_key[ABCD_MAX_TILES];
+  const uint32_t total = hdr->total_sub, nonempty = hdr->nonempty;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int ntiles = geo.ntx * geo.nty;
+  bool final_step = total == 0u && blockIdx.x == 0;
+  for (uint32_t g0 = blockIdx.x * (uint32_t)kSlice; g0 < total; g0 += gridDim.x * (uint32_t)kSlice) {
+    const uint32_t s = g0 + (uint32_t)w;
+    const bool live = s < total;  // uniform per wave
+    int b = -1;
+    uint32_t subb = 0, soff = 0, sub1 = 0, cnt = 0;
+    int pk[4] = {0, 0, 0, 0};
+    if (live) {
+      b = block_of_wave(s, sub_off, slice_off, geo.nblk, subb, soff);
+      sub1 = sub_off[b + 1];
+      const uint32_t e0 = blk_off[b] + (s - subb) * kSub, e1 = blk_off[b + 1];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        uint32_t g;
+        load_entry(pairs, e0 + lane + 64 * j, e1, g, pk[j]);
+      }
+    }
+    d[w][lane] = 0;
+    if (lane == 0) {
+      s_blk[w] = b;
+      s_nsl[w] = live ? slice_off[b + 1] - soff : 0u;
+      s_soff[w] = soff;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) diff_add(d[w], pk[j]);  // 0 for no entry
+    __syncthreads();
+    cnt = diff_prefix(d[w][lane], lane);
+    __syncthreads();
+    d[w][lane] = cnt;
+    __syncthreads();
+    uint32_t before = 0;
+    for (int v = 0; v < w; ++v) before += s_blk[v] == b ? d[v][lane] : 0u;
+    if (live) {
+      c2[(int64_t)s * kBlkTiles + lane] = before;
+      // the slice's last sub-chunk here: the slice total
+      if (w == kSlice - 1 || s + 1 == sub1)
+        store_agent(&slice_tot[(int64_t)(soff + s / kSlice - subb / kSlice) * kBlkTiles + lane],
+                    before + cnt);
+    }
+    // count this group's slices in, one per block met: lane v of the first
+    // wave for the slice ending at sub-chunk v (all atomics in flight at once)
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (w == 0) {
+      bool done = false;
+      if (lane < kSlice) {
+        const int bv = s_blk[lane];
+        if (bv >= 0 && (lane + 1 == kSlice || s_blk[lane + 1] != bv))
+          done = __hip_atomic_fetch_add(&blk_done[bv], 1u, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT) + 1u == s_nsl[lane];
+      }
+      const uint64_t m = __ballot(done);
+      if (done) s_done[__popcll(m & ((1ull << lane) - 1ull))] = lane;
+      if (lane == 0) s_done[kSlice] = __popcll(m);
+    }
+    __syncthreads();
+    const int nd = s_done[kSlice];
+    for (int i = 0; i < nd; ++i) {
+      // block bb's slices, all counted: prefix over them and the tile totals
+      const int v = s_done[i], bb = s_blk[v];
+      const uint32_t nsl = s_nsl[v], base = s_soff[v];
+      const uint32_t per = (nsl + kSlice - 1) / kSlice;
+      const uint32_t q0 = min(nsl, per * w) + base, q1 = min(nsl, per * w + per) + base;
+      uint32_t sum = 0;
+      for (uint32_t q = q0; q < q1; q += kScanRows) {
+        uint32_t x[kScanRows];
+#pragma unroll
+        for (int u = 0; u < kScanRows; ++u)
+          x[u] = q + u < q1 ? load_agent(&slice_tot[(int64_t)(q + u) * kBlkTiles + lane]) : 0u;
+#pragma unroll
+        for (int u = 0; u < kScanRows; ++u) sum += x[u];
+      }
+      __syncthreads();  // every wave is done reading d
+      d[w][lane] = sum;
+      __syncthreads();
+      uint32_t run = 0;
+      for (int k = 0; k < w; ++k) run += d[k][lane];
+      for (uint32_t q = q0; q < q1; q += kScanRows) {
+        uint32_t x[kScanRows];
+#pragma unroll
+        for (int u = 0; u < kScanRows; ++u)
+          x[u] = q + u < q1 ? load_agent(&slice_tot[(int64_t)(q + u) * kBlkTiles + lane]) : 0u;
+#pragma unroll
+        for (int u = 0; u < kScanRows; ++u) {
+          if (q + u < q1) slice_tot[(int64_t)(q + u) * kBlkTiles + lane] = run;
+          run += x[u];
+        }
+      }
+      if (w == kSlice - 1) {
+        const int bx = bb % geo.nbx, by = bb / geo.nbx;
+        const int tx = bx * kBlk + (lane & 7), ty = by * kBlk + (lane >> 3);
+        if (tx < geo.ntx && ty < geo.nty) store_agent(&tile_total[ty * geo.ntx + tx], run);
+      }
+    }
+    if (nd > 0) {  // uniform
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      if (tid == 0)
+        s_final = __hip_atomic_fetch_add(&hdr->done_l2, (uint32_t)nd, __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT) + (uint32_t)nd == nonempty;
+      __syncthreads();
+      if (s_final) final_step = true;
+    }
+    __syncthreads();  // the shared arrays are rewritten by the next group
+  }
+  if (!final_step) return;
   scan_tiles(tile_total, ntiles, tile_off, tile_ranges, tile_order ? s_key : nullptr);
   if (tile_order) {
     __syncthreads();
@@ -963,7 +1053,9 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
   const uint32_t total = hdr->total_sub;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (uint32_t s = blockIdx.x; s < total; s += gridDim.x) {
-    const SubChunk sc = sub_chunk_of(s, block_of_wave(s, sub_off, geo.nblk), sub_off, blk_off, geo);
+    uint32_t subb, soff;
+    const SubChunk sc =
+        sub_chunk_of(s, block_of_wave(s, sub_off, slice_off, geo.nblk, subb, soff), sub_off, blk_off, geo);
     uint32_t g;
     int pk;
     load_entry(pairs, sc.e0 + threadIdx.x, sc.e1, g, pk);
@@ -972,7 +1064,7 @@ __global__ __launch_bounds__(256) void l2_scatter_kernel(
     uint32_t dst_l = 0u;
     {
       const int tx = sc.bx * kBlk + (lane & 7), ty = sc.by * kBlk + (lane >> 3);
-      const uint32_t sl = slice_off[sc.blk] + (s - sub_off[sc.blk]) / kSlice;
+      const uint32_t sl = soff + s / kSlice - subb / kSlice;
       if (tx < geo.ntx && ty < geo.nty)
         dst_l = tile_off[ty * geo.ntx + tx] + slice_tot[(int64_t)sl * kBlkTiles + lane] +
                 c2[(int64_t)s * kBlkTiles + lane];
@@ -1203,7 +1295,6 @@ __global__ __launch_bounds__(kSmallThreads) void bin_small_sort_kernel(
     hdr->m1 = 0;
     hdr->overflow = over ? 1u : 0u;
     hdr->total_sub = 0;
-    hdr->total_slices = 0;
   }
 }
 
@@ -1261,7 +1352,6 @@ __global__ void bin_empty_kernel(int ntiles, uint32_t* __restrict__ tile_ranges,
     hdr->m1 = 0;
     hdr->overflow = 0;
     hdr->total_sub = 0;
-    hdr->total_slices = 0;
   }
 }
 
@@ -1351,11 +1441,10 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
   uint32_t* slice_tot = u32(L.slice_tot);
   ABCD_LAUNCH("l1_place", l1_place_kernel, L.chunks, kBlock, 5 * sizeof(uint32_t) * geo.nblk,
               stream, n, order, rects, geo, bcopy, mcopy, cap, L.chunks, u32(L.lb1), blk_off,
-              sub_off, slice_off, hdr, pairs);
-  ABCD_LAUNCH("l2_count", l2_count_kernel, 4 * kStrideGrid, 64, 0, stream, pairs, geo, sub_off,
-              slice_off, blk_off, hdr, c2, slice_tot);
-  ABCD_LAUNCH("l2_scan", l2_scan_kernel, geo.nblk, 1024, 0, stream, slice_tot, geo, slice_off, hdr,
-              tile_total, tile_off, tile_ranges, tile_order);
+              sub_off, slice_off, hdr, pairs, tile_total);
+  ABCD_LAUNCH("l2_count", l2_count_kernel, kCountGrid, 64 * kSlice, 0, stream, pairs, geo, sub_off,
+              slice_off, blk_off, hdr, c2, slice_tot, u32(L.blk_done), tile_total, tile_off,
+              tile_ranges, tile_order);
   ABCD_LAUNCH("l2_scatter", l2_scatter_kernel, kScatterGrid, kBlock, 0, stream, pairs, depth, geo,
               sub_off, slice_off, blk_off, c2, slice_tot, tile_off, hdr, values_sorted,
               reinterpret_cast<unsigned long long*>(keys_sorted));
