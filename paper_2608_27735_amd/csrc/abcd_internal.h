@@ -175,12 +175,15 @@ __device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long x)
 //   slot_of[MAX][kMaxChunks] per tile: [0] end-of-walk slot, [b] boundary b
 //   work[MAX]                per tile: the most entries the forward staged
 //                            (kept by the tile test) within one chunk of its
-//                            walk, the whole walk if it is not split
+//                            walk, the whole walk if it is not split; bit 31
+//                            (kSplitTile) set when the tile has an end-of-walk
+//                            slot (the schedule then needs no read of slot_of)
 //   walk[MAX]                per tile: the largest per-pixel walk length
 //   items[MAX + slots]       backward work items (tile, chunk), 8 bytes each
 //   ckpt[slots][256]         (T, C_r, C_g, C_b) per pixel, 256-byte aligned
 constexpr uint32_t kNoSlot = 0xFFFFFFFFu;
 constexpr uint32_t kMaxChunks = 64;
+constexpr uint32_t kSplitTile = 1u << 31;
 
 struct SplitLayout {
   uint32_t* hdr;

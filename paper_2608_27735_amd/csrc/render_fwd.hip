@@ -226,7 +226,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void r
       }
       s_base = fin;
       sp.slot_of[(size_t)tile * kMaxChunks] = fin;
-      sp.work[tile] = max(staged_max, staged);
+      sp.work[tile] = min(max(staged_max, staged), kSplitTile - 1u) | (fin != kNoSlot ? kSplitTile : 0u);
     }
     __syncthreads();
     const uint32_t slot = s_base;

@@ -112,29 +112,29 @@ __global__ __launch_bounds__(kOrderThreads) void bwd_schedule_kernel(
     return;
   }
   // eight tiles per thread at a time, their loads issued together (indices
-  // clamped into the arrays, so that no load waits behind a branch)
+  // clamped into the arrays, so that no load waits behind a branch). With a
+  // split, key is the forward's per-tile work whose bit 31 marks a split tile
+  // (reading slot_of instead, one 256-byte-strided word per tile, took 13 us).
   constexpr int kAt = 8;
-  const uint32_t* slot_src = sp.ckpt ? sp.slot_of : walk;
-  const size_t slot_stride = sp.ckpt ? kMaxChunks : 1;
   for (int tb = 0; tb < ntiles; tb += kAt * kOrderThreads) {
-    uint32_t wk[kAt], kk[kAt], sl[kAt];
+    uint32_t wk[kAt], kk[kAt];
 #pragma unroll
     for (int u = 0; u < kAt; ++u) {
       const int tc = min(tb + u * kOrderThreads + (int)threadIdx.x, ntiles - 1);
       wk[u] = walk[tc];
       kk[u] = key[tc];
-      sl[u] = slot_src[(size_t)tc * slot_stride];
     }
 #pragma unroll
     for (int u = 0; u < kAt; ++u) {
       const int t = tb + u * kOrderThreads + (int)threadIdx.x;
       uint32_t n = wk[u] > 0 ? 1u : 0u;
-      if (wk[u] > 0 && sp.ckpt && sl[u] < sp.nslots) {
+      const bool split = sp.ckpt && (kk[u] & kSplitTile);
+      if (wk[u] > 0 && split) {
         const uint32_t ch = (uint32_t)sp.ch;
         n = min((wk[u] + ch - 1) / ch, kMaxChunks);
       }
       if (t < ntiles) {
-        s_key[t] = (uint8_t)bucket_of(kk[u]);
+        s_key[t] = (uint8_t)bucket_of(sp.ckpt ? kk[u] & ~kSplitTile : kk[u]);
         s_nt[t] = (uint8_t)n;
       }
     }
