@@ -53,7 +53,7 @@ constexpr int kRsLook = 8;                  // partition states read at once loo
 // than a few dozen atomic adds; their readers sum the copies
 constexpr int kHistCopies = 32;
 constexpr int kScanThreads = 1024;
-constexpr int kL1Items = 8;                 // level 1: depth ranks per lane
+constexpr int kL1Items = 4;                 // level 1: depth ranks per lane
 constexpr int kRanksPerWave = 64 * kL1Items;
 constexpr int kChunk = 4 * kRanksPerWave;   // level 1: depth ranks per workgroup
 constexpr int kSub = 256;                   // level 2: bucket entries per sub-chunk
