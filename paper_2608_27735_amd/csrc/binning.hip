@@ -1181,12 +1181,18 @@ __global__ __launch_bounds__(kSmallThreads) void bin_small_sort_kernel(
   __shared__ uint32_t s_tcount[kSmallTiles];
   __shared__ uint32_t s_scan[kSmallWaves];
   __shared__ unsigned long long s_m;
+  __shared__ uint32_t s_kor, s_kand;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int ntiles = geo.ntx * geo.nty;
   for (int t = tid; t < ntiles; t += kSmallThreads) s_tcount[t] = 0;
-  if (tid == 0) s_m = 0;
+  if (tid == 0) {
+    s_m = 0;
+    s_kor = 0u;
+    s_kand = 0xffffffffu;
+  }
   __syncthreads();
   unsigned long long m = 0;
+  uint32_t kor = 0u, kand = 0xffffffffu;  // bits set in some key / in every key
   for (int i = tid; i < n; i += kSmallThreads) {
     const uint32_t tt = tiles[i];
     uint32_t key = 0xffffffffu;
@@ -1201,6 +1207,8 @@ __global__ __launch_bounds__(kSmallThreads) void bin_small_sort_kernel(
     s_key[0][i] = key;
     s_val[0][i] = (uint16_t)i;
     s_rect[i] = pack_rect8(x0, y0, x1, y1);
+    kor |= key;
+    kand &= key;
     if (x1 >= x0) {
       m += tt;
       for (int y = y0; y <= y1; ++y)
@@ -1209,15 +1217,30 @@ __global__ __launch_bounds__(kSmallThreads) void bin_small_sort_kernel(
   }
   const unsigned long long wm = wave_sum_u64(m);
   if (lane == 0 && wm) atomicAdd(&s_m, wm);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    kor |= (uint32_t)__shfl_xor((int)kor, off, 64);
+    kand &= (uint32_t)__shfl_xor((int)kand, off, 64);
+  }
+  if (lane == 0) {
+    atomicOr(&s_kor, kor);
+    atomicAnd(&s_kand, kand);
+  }
   __syncthreads();
   const unsigned long long mt = s_m;
   const bool over = mt > capacity || mt >= (1ull << 32);
-  // radix sort: wave w owns positions [128 w, 128 w + 128)
+  // radix sort: wave w owns positions [128 w, 128 w + 128); the waves past
+  // the last key (nw and on) hold nothing, and a digit that every key shares
+  // would leave the order as it is, so its pass is skipped
   const uint64_t lt = lanemask_lt();
+  const int nw = (n + 127) / 128;
+  const uint32_t varying = s_kor ^ s_kand;
+  int src = 0;  // buffer holding the order so far (uniform)
 #pragma unroll 1
   for (int pass = 0; pass < 4; ++pass) {
-    const int src = pass & 1, shift = 8 * pass;
-    for (int i = tid; i < kSmallWaves * 256; i += kSmallThreads) (&s_cnt[0][0])[i] = 0;
+    const int shift = 8 * pass;
+    if (((varying >> shift) & 255u) == 0u) continue;  // uniform
+    for (int i = tid; i < nw * 256; i += kSmallThreads) (&s_cnt[0][0])[i] = 0;
     __syncthreads();
     uint32_t key[2], rank[2];
     uint16_t val[2];
@@ -1241,11 +1264,11 @@ __global__ __launch_bounds__(kSmallThreads) void bin_small_sort_kernel(
     // waves' offsets in place
     uint32_t tot_d = 0;
     if (tid < 256)
-      for (int v = 0; v < kSmallWaves; ++v) tot_d += s_cnt[v][tid];
+      for (int v = 0; v < nw; ++v) tot_d += s_cnt[v][tid];
     uint32_t total;
     uint32_t base = scan_small(tid < 256 ? tot_d : 0u, s_scan, &total);
     if (tid < 256)
-      for (int v = 0; v < kSmallWaves; ++v) {
+      for (int v = 0; v < nw; ++v) {
         const uint32_t c = s_cnt[v][tid];
         s_cnt[v][tid] = (uint16_t)base;
         base += c;
@@ -1261,10 +1284,10 @@ __global__ __launch_bounds__(kSmallThreads) void bin_small_sort_kernel(
       }
     }
     __syncthreads();
+    src ^= 1;
   }
-  // four passes: sorted in buffer 0
   for (int j = tid; j < n; j += kSmallThreads) {
-    const uint32_t g = s_val[0][j];
+    const uint32_t g = s_val[src][j];
     sorted_g[j] = g;
     sorted_rect[j] = s_rect[g];
   }
