@@ -93,6 +93,14 @@ def cases():
     out.append(("small-path-ragged-203x117", cam, RasterParams(sh_degree=2), sc5))
     ring_n = {k: v[:2048] for k, v in r.scene.items()}
     out.append(("small-path-2048-cam1", r.cams[1], r.params, ring_n))
+    # frames on both sides of the tile count up to which the blend kernels
+    # give each tile four workgroups (256 = 16 x 16 tiles; 17 x 16 = 272)
+    rb = S.rng(25)
+    scb = S.gaussians(rb, rb.uniform(-1, 1, (2500, 3)), 1, math.log(0.04), 0.5)
+    out.append(("rows-256-tiles-256x256", look_at((0.1, -3.0, 0.8), (0, 0, 0), 256, 256),
+                RasterParams(sh_degree=1), scb))
+    out.append(("general-272-tiles-272x256", look_at((0.1, -3.0, 0.8), (0, 0, 0), 272, 256),
+                RasterParams(sh_degree=1), scb))
     out.append(("general-path-2049-cam1", r.cams[1], r.params,
                 {k: v[:2049] for k, v in r.scene.items()}))
     return out
