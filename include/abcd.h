@@ -400,11 +400,10 @@ ABCD_API int32_t abcd_adam_step(const abcd_adam_group* groups /* host */, int32_
  * this thread (off by default; enabling it adds two event records per launch
  * on the caller's stream). abcd_timing_read synchronises, and returns the
  * accumulated milliseconds and launch count of the kernel named `kernel`
- * (names: composite, project, depth_keys, radix_hist, radix_scan,
- * radix_scatter, l1_count, l1_scan_columns, l1_finish, l1_scatter, l2_count,
- * l2_scan, bin_scan_tiles, l2_scatter, bin_tile_order, render_fwd, loss_l1,
- * zero_fill, bwd_order, render_bwd, project_bwd, adam, render_cache,
- * cache_rect_init). */
+ * (names: composite, project, bin_zero, depth_keys, radix_pass, l1_place,
+ * l2_count, l2_scatter, bin_small_sort, bin_small_collect, bin_empty,
+ * render_fwd, loss_l1, zero_fill, bwd_order, render_bwd, project_bwd, adam,
+ * render_cache, cache_rect_init). */
 ABCD_API const char* abcd_last_error(void);
 ABCD_API const char* abcd_version(void);
 ABCD_API const char* abcd_status_string(int32_t status);

@@ -296,11 +296,8 @@ int32_t launch_loss_l1(int width, int height, const float* out_rgba, const float
                        float bg0, float bg1, float bg2, float* dL_dout, float* loss,
                        hipStream_t stream);
 
-// schedule.hip: tiles ordered by decreasing octave of `work` (stable; the
-// kernel does nothing if `skip` is non-NULL and *skip != 0 on the device),
-// and the per-tile maximum of the forward's walk lengths as a work estimate.
-int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, const uint32_t* skip,
-                          const char* name, hipStream_t stream);
+// schedule.hip: the backward's schedule (work items heaviest first) and the
+// per-tile maximum of the forward's walk lengths as a work estimate.
 // The backward's work queue: queue[0] = number of items, then kQueues
 // counters kQueueStride words apart (one cache line each): item i is served
 // by queue i mod kQueues, whose counter is queue[kQueueStride q + 1].

@@ -1,6 +1,7 @@
 // schedule.h -- the stable bucket sort of tiles by decreasing quarter octave
-// of a work estimate (heaviest first), shared by the tile-order kernels of
-// schedule.hip and the one-workgroup binning of small active blocks.
+// of a work estimate (heaviest first), shared by the backward's schedule
+// (schedule.hip), the forward's tile order made at the end of binning, and
+// the one-workgroup binning of small active blocks.
 #pragma once
 
 #include "abcd_internal.h"

@@ -19,15 +19,6 @@
 namespace abcd {
 namespace {
 
-__global__ __launch_bounds__(kOrderThreads) void tile_order_kernel(int ntiles,
-                                                                   const uint32_t* __restrict__ work,
-                                                                   uint32_t* __restrict__ order,
-                                                                   const uint32_t* __restrict__ skip) {
-  __shared__ uint8_t s_key[ABCD_MAX_TILES];
-  if (skip && *skip) return;
-  order_tiles(ntiles, work, order, s_key);
-}
-
 // Largest per-pixel walk length (the forward's `last`) of each tile.
 __global__ __launch_bounds__(kBlock) void tile_walk_kernel(int width, int height, int ntx,
                                                            const uint32_t* __restrict__ last,
@@ -157,14 +148,6 @@ int32_t launch_bwd_schedule(int ntiles, const uint32_t* key, const uint32_t* wal
   ABCD_LAUNCH("bwd_order", bwd_schedule_kernel, grid, kOrderThreads, 0, stream, ntiles, key, walk,
               order, split, reinterpret_cast<uint2*>(items), cap, queue,
               reinterpret_cast<float4*>(zero), zero4);
-  ABCD_HIP(hipGetLastError());
-  return ABCD_OK;
-}
-
-int32_t launch_tile_order(int ntiles, const uint32_t* work, uint32_t* order, const uint32_t* skip,
-                          const char* name, hipStream_t stream) {
-  if (ntiles <= 0) return ABCD_OK;
-  ABCD_LAUNCH(name, tile_order_kernel, 1, kOrderThreads, 0, stream, ntiles, work, order, skip);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }
