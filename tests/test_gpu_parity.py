@@ -631,6 +631,14 @@ def test_edge_cases_empty_block_and_culled(api):
     assert np.array_equal(np32(bins["tile_order"]), np.arange(api.n_tiles(cam.width, cam.height)))
     for v in grads.values():
         assert not torch.any(v != 0)
+    say("all culled, general binning (more Gaussians than the one-workgroup sort takes)")
+    many = {k: np.concatenate([v] * 30) for k, v in behind.items()}  # 3,000
+    p = api.project(cam, prm, **to_dev(many))
+    bins = api.bin_sort(cam.width, cam.height, p)
+    torch.cuda.synchronize()
+    assert bins["n_isect"] == 0
+    assert torch.all(bins["tile_ranges"] == 0)
+    assert np.array_equal(np32(bins["tile_order"]), np.arange(api.n_tiles(cam.width, cam.height)))
 
 
 def test_capacity_overflow_writes_empty_ranges_only(api):
