@@ -34,8 +34,9 @@
 //   l2_count               per slice of 16 sub-chunks: counts of its block's
 //                          64 tiles per sub-chunk; per block (its last slice
 //                          counted): the slices' prefix and the tile totals;
-//                          last: tile_ranges and the forward's tile order
-//   l2_scatter             values (and keys), tile-major, depth order
+//                          last: tile_ranges
+//   l2_scatter             values (and keys), tile-major, depth order; its
+//                          first workgroup: the forward's tile order
 #include <algorithm>
 
 #include "schedule.h"
@@ -891,11 +892,10 @@ __device__ __forceinline__ void scan_tiles(const uint32_t* __restrict__ tile_tot
 // block (lane = local tile, the 16 waves split the slices, kScanRows rows in
 // flight per wave) and writes the block's tile totals; the one that completes
 // the last nonempty block scans the tile totals into tile_off and
-// tile_ranges and, when tile_order is given, orders the tiles for the
-// forward (heaviest lists first). With no sub-chunk at all (no entries, or
-// overflow: every tile total is 0, which gives empty ranges and the identity
-// order) the first workgroup does that directly. Slice totals and tile totals
-// pass between workgroups through store_agent and load_agent.
+// tile_ranges. With no sub-chunk at all (no entries, or overflow: every tile
+// total is 0, which gives empty ranges) the first workgroup does that
+// directly. Slice totals and tile totals pass between workgroups through
+// store_agent and load_agent.
 constexpr int kScanRows = 4;
 
 __global__ __launch_bounds__(64 * kSlice) __attribute__((amdgpu_waves_per_eu(8))) void l2_count_kernel(
@@ -903,18 +903,15 @@ __global__ __launch_bounds__(64 * kSlice) __attribute__((amdgpu_waves_per_eu(8))
     const uint32_t* __restrict__ slice_off, const uint32_t* __restrict__ blk_off,
     WsHeader* __restrict__ hdr, uint32_t* __restrict__ c2, uint32_t* __restrict__ slice_tot,
     uint32_t* __restrict__ blk_done, uint32_t* __restrict__ tile_total,
-    uint32_t* __restrict__ tile_off, uint32_t* __restrict__ tile_ranges,
-    uint32_t* __restrict__ tile_order) {
+    uint32_t* __restrict__ tile_off, uint32_t* __restrict__ tile_ranges) {
   static_assert(kSub == 4 * 64, "a sub-chunk is four entries per lane");
-  static_assert(64 * kSlice == kScanThreads && kScanThreads == kOrderThreads,
-                "the tile scan and the tile order take the whole workgroup");
+  static_assert(64 * kSlice == kScanThreads, "the tile scan takes the whole workgroup");
   __shared__ uint32_t d[kSlice][kBlkTiles];
   __shared__ int s_blk[kSlice];          // block of each wave's sub-chunk (-1: none)
   __shared__ uint32_t s_nsl[kSlice];     // slices of that block
   __shared__ uint32_t s_soff[kSlice];    // its first slice
   __shared__ int s_done[kSlice + 1];     // blocks completed here, then their count
   __shared__ uint32_t s_final;
-  __shared__ uint8_t s_key[ABCD_MAX_TILES];
   const uint32_t total = hdr->total_sub, nonempty = hdr->nonempty;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int ntiles = geo.ntx * geo.nty;
@@ -1025,11 +1022,7 @@ __global__ __launch_bounds__(64 * kSlice) __attribute__((amdgpu_waves_per_eu(8))
     __syncthreads();  // the shared arrays are rewritten by the next group
   }
   if (!final_step) return;
-  scan_tiles(tile_total, ntiles, tile_off, tile_ranges, tile_order ? s_key : nullptr);
-  if (tile_order) {
-    __syncthreads();
-    order_keyed(ntiles, s_key, tile_order, nullptr);
-  }
+  scan_tiles(tile_total, ntiles, tile_off, tile_ranges, nullptr);
 }
 
 // Ordered scatter of one 256-entry sub-chunk into its block's 64 tile lists.
@@ -1041,15 +1034,27 @@ __global__ __launch_bounds__(64 * kSlice) __attribute__((amdgpu_waves_per_eu(8))
 // wave's first slot in that tile's run plus their rank among the mask's
 // lanes, one store of consecutive addresses per tile. A tile's run takes the
 // waves' entries in wave order (per-wave counts by 2D difference arrays).
-__global__ __launch_bounds__(256) void l2_scatter_kernel(
+// Workgroup 0 first orders the tiles for the forward when tile_order is given
+// (heaviest lists first; on overflow every total is 0, which gives the
+// identity), beside the others' scatter; its buckets go to the dynamic
+// workgroup memory (one byte per tile).
+__global__ __launch_bounds__(kBlock) void l2_scatter_kernel(
     const unsigned long long* __restrict__ pairs, const float* __restrict__ depth, Geo geo,
     const uint32_t* __restrict__ sub_off, const uint32_t* __restrict__ slice_off,
     const uint32_t* __restrict__ blk_off, const uint32_t* __restrict__ c2,
     const uint32_t* __restrict__ slice_tot, const uint32_t* __restrict__ tile_off,
     const WsHeader* __restrict__ hdr, uint32_t* __restrict__ values_sorted,
-    unsigned long long* __restrict__ keys_sorted) {
+    unsigned long long* __restrict__ keys_sorted, const uint32_t* __restrict__ tile_total,
+    uint32_t* __restrict__ tile_order) {
   __shared__ uint32_t wcnt[4][kBlkTiles];   // per wave: entries covering each tile
   __shared__ uint32_t wdiff[4][kBlkTiles];  // per wave difference arrays
+  extern __shared__ uint8_t s_key[];        // workgroup 0: bucket of each tile
+  if (tile_order && blockIdx.x == 0) {  // uniform
+    const int ntiles = geo.ntx * geo.nty;
+    for (int t = threadIdx.x; t < ntiles; t += kBlock) s_key[t] = (uint8_t)bucket_of(tile_total[t]);
+    __syncthreads();
+    order_keyed<kBlock>(ntiles, s_key, tile_order, nullptr);
+  }
   const uint32_t total = hdr->total_sub;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (uint32_t s = blockIdx.x; s < total; s += gridDim.x) {
@@ -1467,10 +1472,11 @@ int32_t launch_bin_sort(int width, int height, int64_t n, const float* means2d, 
               sub_off, slice_off, hdr, pairs, tile_total);
   ABCD_LAUNCH("l2_count", l2_count_kernel, kCountGrid, 64 * kSlice, 0, stream, pairs, geo, sub_off,
               slice_off, blk_off, hdr, c2, slice_tot, u32(L.blk_done), tile_total, tile_off,
-              tile_ranges, tile_order);
-  ABCD_LAUNCH("l2_scatter", l2_scatter_kernel, kScatterGrid, kBlock, 0, stream, pairs, depth, geo,
-              sub_off, slice_off, blk_off, c2, slice_tot, tile_off, hdr, values_sorted,
-              reinterpret_cast<unsigned long long*>(keys_sorted));
+              tile_ranges);
+  ABCD_LAUNCH("l2_scatter", l2_scatter_kernel, kScatterGrid, kBlock,
+              tile_order ? (size_t)((ntiles + 3) & ~3) : 0u, stream, pairs, depth, geo, sub_off,
+              slice_off, blk_off, c2, slice_tot, tile_off, hdr, values_sorted,
+              reinterpret_cast<unsigned long long*>(keys_sorted), tile_total, tile_order);
   ABCD_HIP(hipGetLastError());
   return ABCD_OK;
 }

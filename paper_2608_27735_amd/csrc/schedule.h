@@ -55,7 +55,7 @@ __device__ __forceinline__ void scan_buckets(uint32_t* s_base) {
 }
 
 // The ordering of tiles whose buckets are in s_key (workgroup memory, filled
-// before the last barrier), by one workgroup of kOrderThreads threads. Wave w
+// before the last barrier), by one workgroup of kThreads threads. Wave w
 // takes the tiles of one contiguous range: it counts each bucket in the
 // range (LDS atomics), the counts of all waves then give each wave its first
 // slot in every bucket (buckets in order, waves in order within a bucket),
@@ -63,21 +63,24 @@ __device__ __forceinline__ void scan_buckets(uint32_t* s_base) {
 // its rank among the range's earlier tiles of its bucket (ballot match plus
 // a running count). s_order (may be NULL): the order also into workgroup
 // memory, as 16-bit tile indices.
+template <int kThreads = kOrderThreads>
 __device__ __forceinline__ void order_keyed(int ntiles, const uint8_t* s_key,
                                             uint32_t* __restrict__ order, uint16_t* s_order) {
+  constexpr int kWaves = kThreads / 64;
+  static_assert(kThreads >= kBuckets, "a thread per bucket");
   __shared__ uint32_t s_base[kBuckets];
-  __shared__ uint32_t s_wc[kOrderWaves][kBuckets];  // per wave counts, then first slots
+  __shared__ uint32_t s_wc[kWaves][kBuckets];  // per wave counts, then first slots
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
   const uint64_t below = (1ull << l) - 1ull;
-  for (int i = tid; i < kOrderWaves * kBuckets; i += kOrderThreads) (&s_wc[0][0])[i] = 0;
+  for (int i = tid; i < kWaves * kBuckets; i += kThreads) (&s_wc[0][0])[i] = 0;
   __syncthreads();
-  const int per = (ntiles + kOrderWaves - 1) / kOrderWaves;
+  const int per = (ntiles + kWaves - 1) / kWaves;
   const int t0 = min(ntiles, w * per), t1 = min(ntiles, t0 + per);
   for (int t = t0 + l; t < t1; t += 64) atomicAdd(&s_wc[w][s_key[t]], 1u);
   __syncthreads();
   if (tid < kBuckets) {
     uint32_t tot = 0;
-    for (int v = 0; v < kOrderWaves; ++v) tot += s_wc[v][tid];
+    for (int v = 0; v < kWaves; ++v) tot += s_wc[v][tid];
     s_base[tid] = tot;
   }
   __syncthreads();
@@ -85,7 +88,7 @@ __device__ __forceinline__ void order_keyed(int ntiles, const uint8_t* s_key,
   __syncthreads();
   if (tid < kBuckets) {  // first slot of each wave in the bucket
     uint32_t run = s_base[tid];
-    for (int v = 0; v < kOrderWaves; ++v) {
+    for (int v = 0; v < kWaves; ++v) {
       const uint32_t c = s_wc[v][tid];
       s_wc[v][tid] = run;
       run += c;
