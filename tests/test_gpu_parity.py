@@ -446,6 +446,18 @@ def test_step_end_to_end(api, case):
     assert rel <= GRAD_TOL
 
 
+@pytest.mark.parametrize("hw", [(1, 1), (3, 5), (16, 16), (1, 17), (31, 2)])
+def test_step_degenerate_frames(api, hw):
+    """Frames of one pixel, one partial tile, one whole tile, a one-pixel
+    column and a two-row strip: every tile's rows mostly clipped by the image
+    (four workgroups per tile, most of their pixels outside)."""
+    H, W = hw
+    rr = S.rng(26)
+    cam = look_at((0.0, -2.5, 0.3), (0, 0, 0), W, H, fov_x_deg=20.0)
+    sc = S.gaussians(rr, rr.uniform(-0.3, 0.3, (300, 3)), 1, math.log(0.05), 0.6)
+    test_step_end_to_end(api, (f"{W}x{H}", cam, RasterParams(sh_degree=1), sc))
+
+
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 @pytest.mark.parametrize("chunk,n_slots", [(256, None), (512, None), (256, 3)])
 def test_split_backward(api, case, chunk, n_slots):
