@@ -206,8 +206,11 @@ def main():
     setup_s = time.time() - t0
 
     def one_step():
-        api.composite_cache(images, order_idx, n_front, F=F, B=B, rects=rects)
-        st.step(target, F=F, B=B)
+        # the collapse writes F and B on a second stream, beside projection
+        # and binning (which do not read them); the forward waits for it
+        st.step(target, F=F, B=B,
+                collapse=lambda: api.composite_cache(images, order_idx, n_front, F=F, B=B,
+                                                     rects=rects, beside=True))
 
     for _ in range(args.warmup):
         one_step()
@@ -230,7 +233,7 @@ def main():
         # the same step replayed as one HIP graph (collapse + step captured once)
         st.capture(target, F=F, B=B,
                    before=lambda: api.composite_cache(images, order_idx, n_front, F=F, B=B,
-                                                      rects=rects))
+                                                      rects=rects, beside=True))
         for _ in range(args.warmup):
             st.replay()
         torch.cuda.synchronize()

@@ -323,11 +323,15 @@ ABCD_API int32_t abcd_render_bwd_noalloc(const abcd_camera* cam /* host */,
  * images: k premultiplied RGBA fp16 renders [k][H][W][4]. order (host): a
  * permutation of 0..k-1, front to back. F = images[order[0]] over ... over
  * images[order[n_front-1]], B = images[order[n_front]] over ... over
- * images[order[k-1]], both fp32 [H][W][4]. With accumulate != 0 the fold
- * continues behind the incoming F and B (F <- F over fold, B <- B over fold),
- * so chunks of cached images can stream in front to back; otherwise they are
- * overwritten. k = 0 writes transparent F and B (or leaves them unchanged
- * when accumulating).
+ * images[order[k-1]], both fp32 [H][W][4]. flags: ABCD_COMPOSITE_ACCUMULATE
+ * (1) continues the fold behind the incoming F and B (F <- F over fold, B <- B
+ * over fold), so chunks of cached images can stream in front to back;
+ * without it they are overwritten. k = 0 writes transparent F and B (or
+ * leaves them unchanged when accumulating). ABCD_COMPOSITE_BESIDE (2) runs the
+ * collapse on at most two workgroups per CU, each taking many pixels, so that
+ * work enqueued on other streams meanwhile (the binning of the same step)
+ * finds room on the CUs; alone on the GPU it is slower. Other bits:
+ * ABCD_E_INVALID.
  * rects (device, may be NULL, 16-byte aligned): int32 [k][4] = (x0, y0, x1,
  * y1) per image, the pixel box [x0, x1) x [y0, y1) outside which that image
  * is fully transparent (all four channels zero), as abcd_render_cache
@@ -341,7 +345,9 @@ ABCD_API int32_t abcd_render_bwd_noalloc(const abcd_camera* cam /* host */,
 ABCD_API int32_t abcd_composite_cache(int32_t width, int32_t height, int32_t k, const uint16_t* images,
                              const int32_t* order /* host */, int32_t n_front,
                              const int32_t* rects, float stop_t, float* F, float* B,
-                             int32_t accumulate, hipStream_t stream);
+                             int32_t flags, hipStream_t stream);
+#define ABCD_COMPOSITE_ACCUMULATE 1
+#define ABCD_COMPOSITE_BESIDE 2
 
 /* ------------------------------------------------------------------------ */
 /* Upload of cached renders from pinned host memory (Method section: the cache

@@ -327,11 +327,13 @@ def adam_step(params, grads, exp_avg, exp_avg_sq, lr, step, beta1=0.9, beta2=0.9
 # ---------------------------------------------------------------- collapse
 
 def composite_cache(images, order, n_front, F=None, B=None, accumulate=False, rects=None,
-                    stop_t=0.0):
+                    stop_t=0.0, beside=False):
     """Collapse cached fp16 renders [K, H, W, 4] (torch.float16, or int16
     holding binary16 bits) into F and B (fp32 [H, W, 4]). rects: optional
     int32 [K, 4] GPU tensor of per-image coverage boxes (x0, y0, x1, y1);
-    stop_t > 0 skips layers that can no longer be seen."""
+    stop_t > 0 skips layers that can no longer be seen. beside: at most two
+    workgroups per CU, for a collapse that runs beside other work on another
+    stream (slower alone)."""
     if images.dtype not in (torch.float16, torch.int16):
         raise ValueError("images must be float16 (or int16 bit patterns)")
     if not images.is_cuda or not images.is_contiguous() or images.dim() != 4:
@@ -350,7 +352,8 @@ def composite_cache(images, order, n_front, F=None, B=None, accumulate=False, re
     order_arr = (C.c_int32 * max(k, 1))(*[int(x) for x in order])
     check(_lib.load().abcd_composite_cache(W, H, k, _ptr(images), order_arr, int(n_front),
                                            _ptr(rects), float(stop_t), _ptr(F), _ptr(B),
-                                           1 if accumulate else 0, _stream()))
+                                           (1 if accumulate else 0) | (2 if beside else 0),
+                                           _stream()))
     return F, B
 
 

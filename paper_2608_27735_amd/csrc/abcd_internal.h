@@ -321,8 +321,9 @@ int32_t stage_cached(int width, int height, int k, const uint16_t* const* host_i
                      const int32_t* rects, uint16_t* dst, hipStream_t stream);
 
 // composite.hip
+// beside: at most two workgroups per CU (room for other streams' work)
 int32_t launch_composite(int width, int height, int k, const uint16_t* images,
                          const int32_t* order, int n_front, const int32_t* rects, float stop_t,
-                         float* F, float* B, int accumulate, hipStream_t stream);
+                         float* F, float* B, int accumulate, bool beside, hipStream_t stream);
 
 }  // namespace abcd

@@ -419,9 +419,11 @@ int32_t abcd_stage_cached(int32_t width, int32_t height, int32_t k,
 
 int32_t abcd_composite_cache(int32_t width, int32_t height, int32_t k, const uint16_t* images,
                              const int32_t* order, int32_t n_front, const int32_t* rects,
-                             float stop_t, float* F, float* B, int32_t accumulate,
+                             float stop_t, float* F, float* B, int32_t flags,
                              hipStream_t stream) {
   REQUIRE(width > 0 && height > 0, "image size must be positive");
+  REQUIRE((flags & ~(ABCD_COMPOSITE_ACCUMULATE | ABCD_COMPOSITE_BESIDE)) == 0,
+          "unknown composite flags 0x%x", (unsigned)flags);
   REQUIRE(stop_t >= 0.0f && stop_t < 1.0f, "stop_t must be in [0, 1)");
   REQUIRE((reinterpret_cast<uintptr_t>(rects) & 15) == 0, "rects must be 16-byte aligned");
   REQUIRE(k >= 0, "k must be >= 0");
@@ -438,8 +440,9 @@ int32_t abcd_composite_cache(int32_t width, int32_t height, int32_t k, const uin
       seen[order[j]] = 1;
     }
   }
-  return launch_composite(width, height, k, images, order, n_front, rects, stop_t, F, B, accumulate,
-                          stream);
+  return launch_composite(width, height, k, images, order, n_front, rects, stop_t, F, B,
+                          (flags & ABCD_COMPOSITE_ACCUMULATE) ? 1 : 0,
+                          (flags & ABCD_COMPOSITE_BESIDE) != 0, stream);
 }
 
 int32_t abcd_loss_l1_grad(int32_t width, int32_t height, const float* out_rgba,

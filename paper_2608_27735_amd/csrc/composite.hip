@@ -17,6 +17,7 @@ namespace abcd {
 namespace {
 
 constexpr int kMaxLayers = 448;  // layers per launch (order table in kernel arguments)
+constexpr int64_t kCompositeBesideGrid = 512;  // workgroups beside other work (two per CU)
 constexpr int kBatch = 16;       // loads in flight per thread
 
 struct LayerTable {
@@ -126,9 +127,10 @@ __global__ __launch_bounds__(256) void composite_kernel(int64_t npix, int width,
                                                         const int4* __restrict__ rects,
                                                         float stop_t, float4* __restrict__ F,
                                                         float4* __restrict__ B) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; (kPair ? 2 * t : t) < npix;
+       t += stride) {
   const int64_t pp = kPair ? 2 * t : t;
-  if (pp >= npix) return;
   PixPos pos;
   pos.x0 = (int)((uint32_t)pp % (uint32_t)width);
   pos.y0 = (int)((uint32_t)pp / (uint32_t)width);
@@ -160,13 +162,14 @@ __global__ __launch_bounds__(256) void composite_kernel(int64_t npix, int width,
     B[pp] = a0;
     if (kPair) B[pp + 1] = a1;
   }
+  }
 }
 
 }  // namespace
 
 int32_t launch_composite(int width, int height, int k, const uint16_t* images,
                          const int32_t* order, int n_front, const int32_t* rects, float stop_t,
-                         float* F, float* B, int accumulate, hipStream_t stream) {
+                         float* F, float* B, int accumulate, bool beside, hipStream_t stream) {
   const int64_t npix = (int64_t)width * height;
   const uint2* img = reinterpret_cast<const uint2*>(images);
   // pairs need 16-byte alignment of every layer: even pixel count, aligned base
@@ -174,7 +177,10 @@ int32_t launch_composite(int width, int height, int k, const uint16_t* images,
                     ((reinterpret_cast<uintptr_t>(F) & 31) == 0) &&
                     ((reinterpret_cast<uintptr_t>(B) & 31) == 0);
   const int64_t threads = pair ? npix / 2 : npix;
-  const int64_t blocks = (threads + kBlock - 1) / kBlock;
+  // beside: a bounded grid (each thread takes every grid-th pixel pair)
+  // leaves room on the CUs for work on other streams (the binning of the step)
+  int64_t blocks = (threads + kBlock - 1) / kBlock;
+  if (beside) blocks = std::min<int64_t>(blocks, kCompositeBesideGrid);
   int fi = 0, bi = 0;
   const int nfront = n_front, nback = k - n_front;
   bool first = true;

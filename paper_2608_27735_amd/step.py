@@ -23,6 +23,7 @@ class ActiveBlockStep:
 
     def __init__(self, cam, prm, params, capacity=None, headroom=1.25, bg=None, chunk="auto"):
         self._fast = None
+        self._side = None  # second stream of step(collapse=...), made on first use
         self.cam, self.prm, self.params = cam, prm, params
         self.bg = bg
         n = params["means"].shape[0]
@@ -176,16 +177,36 @@ class ActiveBlockStep:
                               dL_dout, F=F, B=B, workspace=self.bwd_ws, grads=self.grads,
                               split=self.split)
 
-    def step(self, target, F=None, B=None):
+    def step(self, target, F=None, B=None, collapse=None):
         """project -> bin -> forward -> L1 gradient -> backward (no synchronisation),
         the same calls as project_and_bin(), forward(), loss_grad() and
-        backward() with their arguments prepared once (see _prepared)."""
+        backward() with their arguments prepared once (see _prepared).
+
+        collapse (optional callable): the work that writes F and B (the
+        collapse of the frozen partitions' cached renders). It is enqueued on
+        a second stream once the projection is done (so also the previous
+        step's backward, which reads F and B), and runs beside the binning,
+        which does not read F or B; the forward waits for it."""
         f = self._prepared()
         lib, st = f["lib"], api._stream()
         Fp, Bp = self._image(F, "F", 4, f), self._image(B, "B", 4, f)
         tp = self._image(target, "target", 3, f)
+        main = torch.cuda.current_stream()
         _lib.check(lib.abcd_project(*f["project"], st))
+        if collapse is not None:
+            # after the projection (both are bound by memory bandwidth), beside
+            # the binning (mostly bound by latency)
+            if self._side is None:
+                self._side = torch.cuda.Stream()  # default priority
+                self._fork, self._join = torch.cuda.Event(), torch.cuda.Event()
+            self._fork.record(main)
+            self._side.wait_event(self._fork)
+            with torch.cuda.stream(self._side):
+                collapse()
+            self._join.record(self._side)
         _lib.check(lib.abcd_bin_sort(*f["bin"], st))
+        if collapse is not None:
+            main.wait_event(self._join)
         _lib.check(lib.abcd_render_fwd(*f["fwd_pre"], Fp, Bp, *f["fwd_post"], st))
         _lib.check(lib.abcd_loss_l1_grad(f["W"], f["H"], *f["loss"], tp, *f["loss_post"], st))
         _lib.check(lib.abcd_render_bwd(*f["bwd_pre"], Fp, Bp, *f["bwd_post"], self.dL_dout.data_ptr(),
@@ -193,15 +214,14 @@ class ActiveBlockStep:
         return self.grads
 
     def capture(self, target, F=None, B=None, before=None):
-        """Record one step (and `before()`, e.g. the F/B collapse, ahead of it)
-        as a HIP graph; replay() then launches the whole step at once. Every
-        buffer the step touches is owned here or passed in, so a replay reads
-        the current contents of params, target, F and B. The graph holds no
-        memset nodes: the library clears with its own fill kernel."""
+        """Record one step (and `before()`, e.g. the F/B collapse, beside its
+        projection and binning as in step(collapse=...)) as a HIP graph;
+        replay() then launches the whole step at once. Every buffer the step
+        touches is owned here or passed in, so a replay reads the current
+        contents of params, target, F and B. The graph holds no memset nodes:
+        the library clears with its own fill kernel."""
         def body():
-            if before is not None:
-                before()
-            self.step(target, F, B)
+            self.step(target, F, B, collapse=before)
 
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())

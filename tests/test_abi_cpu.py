@@ -137,9 +137,9 @@ def test_bin_sort_rejects_small_or_misaligned_workspace(lib):
 
 
 def test_composite_rejects_bad_order(lib):
-    def call(k, order, n_front, F=FAKE, rects=None, stop_t=0.0):
-        return lib.abcd_composite_cache(8, 8, k, FAKE, order, n_front, rects, stop_t, F, FAKE, 0,
-                                        None)
+    def call(k, order, n_front, F=FAKE, rects=None, stop_t=0.0, flags=0):
+        return lib.abcd_composite_cache(8, 8, k, FAKE, order, n_front, rects, stop_t, F, FAKE,
+                                        flags, None)
     order = (C.c_int32 * 3)(0, 0, 2)
     assert call(3, order, 1) == 1
     order = (C.c_int32 * 3)(0, 1, 3)
@@ -152,6 +152,8 @@ def test_composite_rejects_bad_order(lib):
     assert call(3, order, 1, stop_t=-0.1) == 1
     assert call(3, order, 1, stop_t=1.0) == 1
     assert call(3, order, 1, stop_t=float("nan")) == 1
+    assert call(3, order, 1, flags=4) == 1  # unknown flag bit
+    assert call(3, order, 1, flags=-1) == 1
 
 
 def test_render_calls_reject_bad_arguments(lib):

@@ -835,3 +835,57 @@ def test_step_graph_replays_match_eager(api):
             rel = (torch.linalg.norm((gg[k] - eg[k]).double()) /
                    torch.linalg.norm(eg[k].double()).clamp_min(1e-30)).item()
             assert rel <= 1e-5, (rep, k, rel)  # same kernels; atomics order differs
+
+
+def test_step_collapse_beside_binning(api):
+    """The F/B collapse enqueued on a second stream beside projection and
+    binning (step(collapse=...)) gives the step of the collapse run first,
+    eagerly and as a replayed graph with the fork and join captured, across
+    parameter and cache changes between steps."""
+    from paper_2608_27735_amd.step import ActiveBlockStep
+    r = S.ring()
+    cam, prm = r.cams[2], r.params
+    scene = S.subset(r.scene, r.cell_of == r.active)
+    rr = S.rng(92)
+    k, n_front = 9, 4
+    imgs = torch.from_numpy(S.half_bits(S.premultiplied_images(rr, k, cam.height, cam.width,
+                                                               coverage=0.6)).view(np.int16)).to(dev())
+    order = list(rr.permutation(k))
+    target = torch.from_numpy(rr.uniform(0, 1, (cam.height, cam.width, 3)).astype(np.float32)).to(dev())
+    say("collapse beside binning", scene["means"].shape, k)
+    params = to_dev(scene)
+    probe = ActiveBlockStep(cam, prm, params)
+    steps, FB = [], []
+    for _ in range(3):  # sequential, overlapped eager, overlapped graph
+        p = {kk: v.clone() for kk, v in params.items()}
+        steps.append((ActiveBlockStep(cam, prm, p, capacity=2 * probe.capacity), p))
+        FB.append((torch.empty((cam.height, cam.width, 4), device=dev()),
+                   torch.empty((cam.height, cam.width, 4), device=dev())))
+
+    def collapse(i):  # the overlapped ones on a bounded grid (same arithmetic per pixel)
+        return lambda: api.composite_cache(imgs, order, n_front, F=FB[i][0], B=FB[i][1],
+                                           beside=i > 0)
+
+    steps[2][0].capture(target, F=FB[2][0], B=FB[2][1], before=collapse(2))
+    torch.cuda.synchronize()
+    for rep in range(3):
+        with torch.no_grad():
+            for _, p in steps:
+                p["means"].add_(0.003 * (rep + 1))
+            if rep == 1:
+                imgs.copy_(imgs.flip(0))
+        torch.cuda.synchronize()
+        collapse(0)()
+        g0 = steps[0][0].step(target, F=FB[0][0], B=FB[0][1])
+        g1 = steps[1][0].step(target, F=FB[1][0], B=FB[1][1], collapse=collapse(1))
+        g2 = steps[2][0].replay()
+        torch.cuda.synchronize()
+        assert not any(s.overflowed() for s, _ in steps)
+        for i in (1, 2):
+            assert torch.equal(FB[i][0], FB[0][0]) and torch.equal(FB[i][1], FB[0][1]), (rep, i)
+            assert torch.equal(steps[i][0].fwd["out"], steps[0][0].fwd["out"]), (rep, i)
+            gi = (g1, g2)[i - 1]
+            for kk in ("means", "log_scales", "quats", "opacity_logits", "sh"):
+                rel = (torch.linalg.norm((gi[kk] - g0[kk]).double()) /
+                       torch.linalg.norm(g0[kk].double()).clamp_min(1e-30)).item()
+                assert rel <= 1e-5, (rep, i, kk, rel)  # same kernels; atomics order differs
