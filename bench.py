@@ -342,13 +342,19 @@ def main():
         # replay
         small = small_config(api, S, ActiveBlockStep, dev, args.steps, args.warmup)
 
-    # per-kernel durations: HIP events around every launch, on the launch stream
+    # per-kernel durations: HIP events around every launch, on the launch
+    # stream, in steps that run the collapse first (not beside the binning),
+    # so that each kernel's time is its own
+    def one_step_alone():
+        api.composite_cache(images, order_idx, n_front, F=F, B=B, rects=rects)
+        st.step(target, F=F, B=B)
+
     kern = {}
     if args.profile_kernels:
         api.timing_reset()
         api.timing_enable(True)
         for _ in range(args.steps):
-            one_step()
+            one_step_alone()
         torch.cuda.synchronize()
         api.timing_enable(False)
         for name in KERNELS:
