@@ -90,7 +90,7 @@ __device__ __forceinline__ void bwd_item(
   __shared__ float4 s_gc[256];  // a, b, c (conic), colour b
   __shared__ int s_pos[256];
   __shared__ uint32_t s_g[256];
-  __shared__ float s_acc[9 * 256];  // entry-major: [entry][9]
+  __shared__ float s_acc[9][256];  // field-major: [field][staged entry]
   __shared__ __align__(4) uint8_t s_idx[4][256];  // per wave: staged slots reaching its rows
   __shared__ int s_wcnt[5][4];
   __shared__ uint32_t s_max;
@@ -158,6 +158,7 @@ __device__ __forceinline__ void bwd_item(
   const int lane = tid & 63;
   const bool adder = (lane & 7) == 4 || lane == 48;
   const int slot = lane == 48 ? 8 : sum9_slot(lane);
+  float* const acc_lane = s_acc[slot];  // this lane's field, indexed by staged entry
   uint32_t wml = lastp;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) wml = max(wml, (uint32_t)__shfl_xor((int)wml, off, 64));
@@ -196,7 +197,7 @@ __device__ __forceinline__ void bwd_item(
       s_pos[pos] = (int)(bend - 1 - tid - start);
       s_g[pos] = rec.gid;
 #pragma unroll
-      for (int q = 0; q < 9; ++q) s_acc[9 * pos + q] = 0.0f;
+      for (int q = 0; q < 9; ++q) s_acc[q][pos] = 0.0f;
     }
     __syncthreads();
     {
@@ -273,7 +274,7 @@ __device__ __forceinline__ void bwd_item(
       const Sum9 v = wave_sum9(gr, lane);
       float out = lane == 48 ? v.v8 : v.lo;
       asm volatile("" : "+v"(out));  // the last folds stay outside the branch (DPP add)
-      if (adder) atomicAdd(&s_acc[9 * j + slot], out);
+      if (adder) atomicAdd(acc_lane + j, out);
     }
     }
     __syncthreads();
@@ -284,7 +285,7 @@ __device__ __forceinline__ void bwd_item(
       const float4 co = s_gc[tid];
       float g[9];
 #pragma unroll
-      for (int q = 0; q < 9; ++q) g[q] = s_acc[9 * tid + q];
+      for (int q = 0; q < 9; ++q) g[q] = s_acc[q][tid];
       const float mx = g[0], my = g[1];
       g[0] = co.x * mx + co.y * my;
       g[1] = co.y * mx + co.z * my;
@@ -404,7 +405,7 @@ __global__ __launch_bounds__(256) void render_bwd_rows_kernel(
   __shared__ float4 s_gc[256];  // a, b, c (conic), colour b
   __shared__ int s_pos[256];
   __shared__ uint32_t s_g[256];
-  __shared__ float s_acc[9 * 256];  // entry-major: [entry][9]
+  __shared__ float s_acc[9][256];  // field-major: [field][staged entry]
   __shared__ __align__(4) uint8_t s_idx[4][256];  // per wave: staged slots reaching its row
   __shared__ int s_wcnt[5][4];
   __shared__ uint32_t s_max;
@@ -474,7 +475,7 @@ __global__ __launch_bounds__(256) void render_bwd_rows_kernel(
       s_pos[pos] = (int)(bend - 1 - tid - start);
       s_g[pos] = rec.gid;
 #pragma unroll
-      for (int q = 0; q < 9; ++q) s_acc[9 * pos + q] = 0.0f;
+      for (int q = 0; q < 9; ++q) s_acc[q][pos] = 0.0f;
     }
     __syncthreads();
     {
@@ -537,14 +538,14 @@ __global__ __launch_bounds__(256) void render_bwd_rows_kernel(
       const float m = row_sum9(gr, col, v8);
       float out = col == 1 ? v8 : m;
       asm volatile("" : "+v"(out));  // the last folds stay outside the branch (DPP add)
-      if (adder && valid) atomicAdd(&s_acc[9 * j + slot], out);
+      if (adder && valid) atomicAdd(&s_acc[slot][j], out);
     }
     __syncthreads();
     if (tid < cnt) {
       const float4 co = s_gc[tid];
       float g[9];
 #pragma unroll
-      for (int q = 0; q < 9; ++q) g[q] = s_acc[9 * tid + q];
+      for (int q = 0; q < 9; ++q) g[q] = s_acc[q][tid];
       const float mx = g[0], my = g[1];
       g[0] = co.x * mx + co.y * my;
       g[1] = co.y * mx + co.z * my;
