@@ -266,6 +266,28 @@ def composite(width, height, images_f16, order, n_front, F=None, B=None, stop_t=
 
 # ------------------------------------------------------------------- helpers
 
+def loss_l1(out, target, bg=None):
+    """L1 reconstruction loss of a step and its gradient (Method: the active
+    block is optimised against a reconstruction loss of the composited image).
+
+    out: H x W x 4 premultiplied RGBA render; target: H x W x 3; bg: background
+    colour (black if None). The image is img = rgb + (1 - a) bg, the loss the
+    mean over pixels and colour channels of |img - target|, and its gradient
+    takes sign(0) = 0: dL/drgb = sign(img - target) / (3 H W), dL/da =
+    -sum_c bg_c dL/drgb_c. fp64 throughout. Returns (loss, H x W x 4 gradient).
+    """
+    out = np.asarray(out, np.float64)
+    target = np.asarray(target, np.float64)
+    h, w = target.shape[:2]
+    b = np.zeros(3) if bg is None else np.asarray(bg, np.float64)
+    img = out[..., :3] + (1.0 - out[..., 3:4]) * b
+    d = img - target
+    n = 3.0 * h * w
+    g_rgb = np.sign(d) / n
+    g_a = -(g_rgb * b).sum(-1, keepdims=True)
+    return float(np.abs(d).sum() / n), np.concatenate([g_rgb, g_a], -1)
+
+
 def adam(theta, g, m, v, lr, b1=0.9, b2=0.999, eps=1e-15, t=1):
     """One Adam step in fp64; returns (theta, m, v) (new arrays)."""
     theta, m, v = (np.array(x, np.float64).ravel().copy() for x in (theta, m, v))

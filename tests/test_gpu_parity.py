@@ -738,11 +738,15 @@ def test_loss_l1_gradient(api, H, W):
     g = api.loss_l1_grad(torch.from_numpy(out).to(dev()), torch.from_numpy(tgt).to(dev()), bg=bg,
                          loss=loss)
     torch.cuda.synchronize()
+    # the sign decision is taken on the fp32 image, as the kernel takes it
     img = out[..., :3] + (1 - out[..., 3:]) * np.array(bg, np.float32)
+    ref_L, ref_g = O.loss_l1(out, tgt, bg=bg)
     s = np.sign(img - tgt) / (3 * H * W)
     exp = np.concatenate([s, -(s * np.array(bg)).sum(-1, keepdims=True)], -1)
+    flip = np.sign(img - tgt) != np.sign(out[..., :3].astype(np.float64) + (1 - out[..., 3:].astype(np.float64)) * np.array(bg) - tgt)
     assert np.abs(np32(g) - exp).max() < 1e-9
-    assert abs(loss.item() - np.abs(img.astype(np.float64) - tgt).sum() / (3 * H * W)) < 1e-5
+    assert np.abs(np32(g)[~flip.any(-1)] - ref_g[~flip.any(-1)]).max() < 1e-9
+    assert abs(loss.item() - ref_L) < 1e-5
 
 
 def test_adam_step_matches_oracle(api):

@@ -1032,3 +1032,38 @@ def test_frustum_oracle_agrees_with_point_sampling():
             assert ok
         if ok and s > 0.2:
             assert hit
+
+
+def test_loss_l1_worked_example_by_hand():
+    """One pixel: rgb (0.5, 0.2, 0.1), a = 0.5 over bg (0, 0, 1) gives the
+    image (0.5, 0.2, 0.6); against the target (0.4, 0.4, 0.5) the differences
+    are (0.1, -0.2, 0.1), so L = 0.4 / 3, dL/drgb = (1, -1, 1) / 3 and
+    dL/da = -(1 * 1) / 3 (only the blue background channel is non-zero)."""
+    out = np.array([[[0.5, 0.2, 0.1, 0.5]]])
+    tgt = np.array([[[0.4, 0.4, 0.5]]])
+    L, g = O.loss_l1(out, tgt, bg=(0.0, 0.0, 1.0))
+    assert abs(L - 0.4 / 3) < 1e-15
+    assert np.allclose(g[0, 0], [1 / 3, -1 / 3, 1 / 3, -1 / 3], atol=1e-15)
+    # a pixel that matches its target exactly has zero gradient (sign(0) = 0)
+    L0, g0 = O.loss_l1(np.array([[[0.4, 0.4, 0.0, 0.5]]]), tgt, bg=(0.0, 0.0, 1.0))
+    assert L0 == 0.0 and not g0.any()
+
+
+def test_loss_l1_gradient_matches_finite_differences():
+    """Away from the kinks (|img - target| > 1e-3 everywhere) the L1 loss is
+    linear near the point, so central differences are exact up to rounding."""
+    r = np.random.default_rng(12)
+    h, w = 5, 7
+    out = np.concatenate([r.uniform(0, 1, (h, w, 3)), r.uniform(0, 1, (h, w, 1))], -1)
+    tgt = r.uniform(0, 1, (h, w, 3))
+    bg = (0.3, 0.6, 0.1)
+    img = out[..., :3] + (1 - out[..., 3:]) * np.array(bg)
+    tgt = np.where(np.abs(img - tgt) < 1e-3, tgt + 0.01, tgt)
+    _, g = O.loss_l1(out, tgt, bg=bg)
+    eps = 1e-6
+    for idx in [(0, 0, 0), (2, 3, 1), (4, 6, 2), (1, 5, 3), (3, 2, 3)]:
+        op, om = out.copy(), out.copy()
+        op[idx] += eps
+        om[idx] -= eps
+        fd = (O.loss_l1(op, tgt, bg)[0] - O.loss_l1(om, tgt, bg)[0]) / (2 * eps)
+        assert abs(fd - g[idx]) < 1e-9, (idx, fd, g[idx])
